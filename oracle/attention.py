@@ -1,0 +1,255 @@
+"""Softmax attention over graph neighbourhoods and over all pairs, in fp64.
+
+Oracle - test infrastructure only (see the package docstring).
+
+Definitions followed:
+
+* Full attention, §2.1 Eq. (1): O = softmax(Q K^T / sqrt(d_K)) V, applied per
+  head with d_K the per-head key width.
+* Local topology-induced pattern, §3.2: node i attends only to the nodes j of
+  its neighbourhood N(i); the coefficients are the softmax over j in N(i) of the
+  scaled dot products, and the new feature is the coefficient-weighted sum of
+  the neighbours' value rows.  N(i) is row i of the CSR exactly as given (the
+  caller adds the self-loop of condition C1, §3.2).
+
+Per head h and row i with neighbourhood N(i):
+
+    s_ij  = scale * <Q[i,h], K[j,h]>              j in N(i)
+    LSE_i = log sum_j exp(s_ij)                    (-inf for an empty row)
+    P_ij  = exp(s_ij - LSE_i)
+    O[i,h] = sum_j P_ij V[j,h]                     (0 for an empty row)
+
+Backward, for an upstream gradient dO:
+
+    D_i   = <dO[i,h], O[i,h]>
+    dP_ij = <dO[i,h], V[j,h]>
+    dS_ij = P_ij (dP_ij - D_i)
+    dQ_i  = scale * sum_{j in N(i)} dS_ij K[j,h]
+    dK_j  = scale * sum_{i : j in N(i)} dS_ij Q[i,h]
+    dV_j  = sum_{i : j in N(i)} P_ij dO[i,h]
+
+All arrays are [N, H, d] (node, head, feature); LSE and D are [N, H].
+Inputs are upcast to fp64; bfloat16 workloads pass the already-rounded values.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+_EDGE_BUDGET = 1 << 22  # edge x head x feature elements per chunk
+
+
+def _f64(x):
+    return np.asarray(x, dtype=np.float64)
+
+
+def _row_chunks(rowptr: np.ndarray, rows: np.ndarray, per_edge: int):
+    """Split the row list into consecutive chunks holding about _EDGE_BUDGET elements."""
+    deg = rowptr[rows + 1] - rowptr[rows]
+    budget = max(1, _EDGE_BUDGET // max(1, per_edge))
+    cum = np.cumsum(deg)
+    start = 0
+    while start < len(rows):
+        base = cum[start - 1] if start else 0
+        stop = int(np.searchsorted(cum, base + budget, side="left")) + 1
+        stop = min(max(stop, start + 1), len(rows))
+        yield rows[start:stop]
+        start = stop
+
+
+def _edges_of(rowptr, col, rows):
+    """Edge list (local row index, neighbour id) for the given rows, in CSR order."""
+    deg = (rowptr[rows + 1] - rowptr[rows]).astype(np.int64)
+    local = np.repeat(np.arange(len(rows)), deg)
+    first = np.zeros(len(rows), dtype=np.int64)
+    if len(rows):
+        np.cumsum(deg[:-1], out=first[1:])
+    idx = np.arange(int(deg.sum()), dtype=np.int64) - np.repeat(first, deg) + np.repeat(rowptr[rows], deg)
+    return local, col[idx].astype(np.int64), deg
+
+
+def _segment_softmax_stats(s, local, n_rows):
+    """Per local row and head: max and log-sum-exp of the scores s[e, h] of its edges."""
+    H = s.shape[1]
+    m = np.full((n_rows, H), -np.inf)
+    np.maximum.at(m, local, s)
+    p = np.exp(s - m[local])
+    total = np.zeros((n_rows, H))
+    np.add.at(total, local, p)
+    with np.errstate(divide="ignore"):
+        lse = m + np.log(total)
+    return lse
+
+
+def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
+    """O[rows], LSE[rows] of neighbourhood softmax attention (all rows when ``rows`` is None)."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    N, H, d = Q.shape
+    rowptr = np.asarray(rowptr, dtype=np.int64)
+    col = np.asarray(col, dtype=np.int64)
+    rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
+    O = np.zeros((len(rows), H, d))
+    LSE = np.full((len(rows), H), -np.inf)
+    pos = 0
+    for chunk in _row_chunks(rowptr, rows, H * d):
+        local, nbr, _ = _edges_of(rowptr, col, chunk)
+        n = len(chunk)
+        if len(nbr):
+            i = chunk[local]
+            s = scale * np.einsum("ehc,ehc->eh", Q[i], K[nbr])
+            lse = _segment_softmax_stats(s, local, n)
+            p = np.exp(s - lse[local])
+            o = np.zeros((n, H, d))
+            np.add.at(o, local, p[:, :, None] * V[nbr])
+            O[pos:pos + n] = o
+            LSE[pos:pos + n] = lse
+        pos += n
+    return O, LSE
+
+
+def _csc(rowptr, col, N):
+    """In-neighbour lists: for each column j, the rows i with j in N(i), ascending."""
+    rowptr = np.asarray(rowptr, dtype=np.int64)
+    col = np.asarray(col, dtype=np.int64)
+    rows = np.repeat(np.arange(N), np.diff(rowptr))
+    order = np.argsort(col, kind="stable")
+    colptr = np.zeros(N + 1, dtype=np.int64)
+    np.cumsum(np.bincount(col, minlength=N), out=colptr[1:])
+    return colptr, rows[order]
+
+
+def sparse_attn_bwd(rowptr, col, Q, K, V, dO, scale):
+    """dQ, dK, dV of neighbourhood softmax attention for the whole graph."""
+    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    N, H, d = Q.shape
+    rowptr = np.asarray(rowptr, dtype=np.int64)
+    col = np.asarray(col, dtype=np.int64)
+    O, LSE = sparse_attn_fwd(rowptr, col, Q, K, V, scale)
+    D = np.einsum("nhc,nhc->nh", dO, O)
+    dQ = np.zeros_like(Q)
+    dK = np.zeros_like(K)
+    dV = np.zeros_like(V)
+    for chunk in _row_chunks(rowptr, np.arange(N), H * d):
+        local, j, _ = _edges_of(rowptr, col, chunk)
+        if not len(j):
+            continue
+        i = chunk[local]
+        s = scale * np.einsum("ehc,ehc->eh", Q[i], K[j])
+        p = np.exp(s - LSE[i])
+        dp = np.einsum("ehc,ehc->eh", dO[i], V[j])
+        ds = p * (dp - D[i])
+        np.add.at(dQ, i, scale * ds[:, :, None] * K[j])
+        np.add.at(dK, j, scale * ds[:, :, None] * Q[i])
+        np.add.at(dV, j, p[:, :, None] * dO[i])
+    return dQ, dK, dV
+
+
+def sparse_attn_bwd_sampled(rowptr, col, Q, K, V, dO, scale, rows, cols):
+    """dQ[rows], dK[cols], dV[cols] computed from only the rows they depend on.
+
+    dQ_i needs row i alone; dK_j and dV_j need every row i that has j as a
+    neighbour (with that row's LSE_i and D_i, each row-local).
+    """
+    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    N, H, d = Q.shape
+    rowptr = np.asarray(rowptr, dtype=np.int64)
+    col = np.asarray(col, dtype=np.int64)
+    rows = np.asarray(rows, dtype=np.int64)
+    cols = np.asarray(cols, dtype=np.int64)
+
+    O_r, L_r = sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=rows)
+    D_r = np.einsum("nhc,nhc->nh", dO[rows], O_r)
+    dQ = np.zeros((len(rows), H, d))
+    local, j, _ = _edges_of(rowptr, col, rows)
+    if len(j):
+        i = rows[local]
+        s = scale * np.einsum("ehc,ehc->eh", Q[i], K[j])
+        p = np.exp(s - L_r[local])
+        dp = np.einsum("ehc,ehc->eh", dO[i], V[j])
+        ds = p * (dp - D_r[local])
+        np.add.at(dQ, local, scale * ds[:, :, None] * K[j])
+
+    colptr, inrow = _csc(rowptr, col, N)
+    dK = np.zeros((len(cols), H, d))
+    dV = np.zeros((len(cols), H, d))
+    for k, jj in enumerate(cols):
+        srcs = inrow[colptr[jj]:colptr[jj + 1]]
+        if not len(srcs):
+            continue
+        O_s, L_s = sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=srcs)
+        D_s = np.einsum("nhc,nhc->nh", dO[srcs], O_s)
+        s = scale * np.einsum("ehc,hc->eh", Q[srcs], K[jj])
+        p = np.exp(s - L_s)
+        dp = np.einsum("ehc,hc->eh", dO[srcs], V[jj])
+        ds = p * (dp - D_s)
+        dK[k] = scale * np.einsum("eh,ehc->hc", ds, Q[srcs])
+        dV[k] = np.einsum("eh,ehc->hc", p, dO[srcs])
+    return dQ, dK, dV
+
+
+# ---------------------------------------------------------------------------
+# Full softmax attention, §2.1 Eq. (1), per head.
+# ---------------------------------------------------------------------------
+
+def dense_attn_fwd(Q, K, V, scale, rows=None):
+    """O[rows], LSE[rows] of softmax(scale Q K^T) V over all N keys, per head."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    N, H, d = Q.shape
+    rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
+    O = np.zeros((len(rows), H, d))
+    LSE = np.zeros((len(rows), H))
+    step = max(1, (1 << 22) // max(1, N))
+    for a in range(0, len(rows), step):
+        r = rows[a:a + step]
+        for h in range(H):
+            s = scale * (Q[r, h, :] @ K[:, h, :].T)  # [R, N]
+            m = s.max(axis=1, keepdims=True)
+            e = np.exp(s - m)
+            tot = e.sum(axis=1, keepdims=True)
+            O[a:a + len(r), h, :] = (e / tot) @ V[:, h, :]
+            LSE[a:a + len(r), h] = (m + np.log(tot))[:, 0]
+    return O, LSE
+
+
+def dense_attn_bwd(Q, K, V, dO, scale):
+    """dQ, dK, dV of full softmax attention (materialises N x N per head: small N only)."""
+    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    N, H, d = Q.shape
+    dQ = np.zeros_like(Q)
+    dK = np.zeros_like(K)
+    dV = np.zeros_like(V)
+    for h in range(H):
+        s = scale * (Q[:, h, :] @ K[:, h, :].T)
+        s -= s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p /= p.sum(axis=1, keepdims=True)
+        o = p @ V[:, h, :]
+        Dv = (dO[:, h, :] * o).sum(axis=1, keepdims=True)
+        dp = dO[:, h, :] @ V[:, h, :].T
+        ds = p * (dp - Dv)
+        dQ[:, h, :] = scale * ds @ K[:, h, :]
+        dK[:, h, :] = scale * ds.T @ Q[:, h, :]
+        dV[:, h, :] = p.T @ dO[:, h, :]
+    return dQ, dK, dV
+
+
+def dense_attn_dq_rows(Q, K, V, dO, scale, rows):
+    """dQ[rows] of full softmax attention; each row needs only its own scores against all keys."""
+    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    N, H, d = Q.shape
+    rows = np.asarray(rows, dtype=np.int64)
+    dQ = np.zeros((len(rows), H, d))
+    step = max(1, (1 << 22) // max(1, N))
+    for a in range(0, len(rows), step):
+        r = rows[a:a + step]
+        for h in range(H):
+            s = scale * (Q[r, h, :] @ K[:, h, :].T)
+            s -= s.max(axis=1, keepdims=True)
+            p = np.exp(s)
+            p /= p.sum(axis=1, keepdims=True)
+            o = p @ V[:, h, :]
+            Dv = (dO[r, h, :] * o).sum(axis=1, keepdims=True)
+            dp = dO[r, h, :] @ V[:, h, :].T
+            ds = p * (dp - Dv)
+            dQ[a:a + len(r), h, :] = scale * ds @ K[:, h, :]
+    return dQ

@@ -1,0 +1,16 @@
+"""Seeded synthetic inputs shared by the tests, the benchmark and the oracle's callers.
+
+This package builds graphs (stochastic block model, Chung-Lu) and dense feature
+tensors.  It holds none of the attention, reorder or tiling arithmetic: both the
+HIP path and the oracle receive what is produced here as plain arrays.
+"""
+
+from .graphs import (  # noqa: F401
+    Graph,
+    sbm_graph,
+    chung_lu_graph,
+    csr_from_pairs,
+    lognormal_block_sizes,
+)
+from .tensors import bf16_round, bf16_bits, normal_tensor  # noqa: F401
+from .workloads import WORKLOADS, make_workload, Workload  # noqa: F401
