@@ -1,0 +1,226 @@
+/*
+ * gt.h - C ABI of libgt, graph-topology sparse attention for AMD MI355X (gfx950).
+ *
+ * Operations follow TorchGT (arXiv 2407.14106):
+ *   - neighbourhood softmax attention, §3.2 (local topology-induced pattern):
+ *     node i attends only to the nodes j of its CSR row N(i);
+ *   - full softmax attention, §2.1 Eq. (1), for the interleaved dense layer
+ *     of §3.2 (interleave fully-connected pattern);
+ *   - cluster reordering of the nodes, §3.3 (utilisation of graph cluster),
+ *     here a deterministic label-propagation order instead of METIS;
+ *   - the dense/sparse tile plan of §3.4 (cluster sparsity and the transfer
+ *     threshold), read as an exact execution plan: a T x T tile of the
+ *     reordered adjacency whose share of non-zeros reaches the threshold is
+ *     computed with matrix cores over the whole tile (masked), every other
+ *     edge is computed edge by edge.  The split never changes the result.
+ *
+ * Conventions shared by every entry point:
+ *   - Every pointer is device memory unless its comment says "host".  All
+ *     memory is owned by the caller; the library allocates nothing and keeps
+ *     no state between calls except the thread-local error text.
+ *   - Scratch memory comes from a caller workspace `ws` of at least the size
+ *     returned by the matching *_workspace_size() function (256-byte aligned
+ *     base).  A smaller workspace gives GT_ERR_WORKSPACE.
+ *   - Every call is enqueued on `stream` and returns without waiting, except
+ *     the calls marked SYNC, which wait for `stream` to read back a count or a
+ *     validation result.
+ *   - Arguments are checked on the host before anything is enqueued; on an
+ *     error nothing touches the device and a negative gt_status is returned
+ *     (gt_last_error() gives the reason).
+ *   - Feature tensors Q, K, V, O, dO, dQ, dK, dV are [n, H, d] row-major
+ *     (node, head, feature) in the element type `dtype`; LSE is [n, H] fp32.
+ *     Supported: d in {32, 64}; H in {1, 2, 4, 8, 16}; dtype GT_F32 or GT_BF16
+ *     (bf16 storage, fp32 arithmetic and accumulation, bf16 results rounded to
+ *     nearest even).
+ *   - CSR: rowptr int64[n+1] with rowptr[0] = 0 and rowptr[n] = nnz; col
+ *     int32[nnz], 0 <= col < n, strictly increasing inside each row.  Row i
+ *     attends to the columns of row i (its out-neighbours).  The library adds
+ *     no self-loops: condition C1 of §3.2 (each node attends to itself) is the
+ *     caller's to add.  n < 2^31, nnz < 2^32.
+ */
+#ifndef GT_H
+#define GT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t gt_status;
+#define GT_OK 0
+#define GT_ERR_INVALID_ARG (-1)  /* null pointer, negative size, inconsistent sizes */
+#define GT_ERR_UNSUPPORTED (-2)  /* d, H, T or dtype outside the supported set */
+#define GT_ERR_UNSORTED (-3)     /* CSR row not strictly increasing (or rowptr decreasing) */
+#define GT_ERR_DUPLICATE (-4)    /* repeated column inside a CSR row */
+#define GT_ERR_OUT_OF_RANGE (-5) /* column outside [0, n), or rowptr[0] != 0 / rowptr[n] != nnz */
+#define GT_ERR_WORKSPACE (-6)    /* workspace smaller than the size query returned */
+#define GT_ERR_HIP (-7)          /* a HIP runtime call failed; gt_last_error() has its text */
+
+typedef int32_t gt_dtype;
+#define GT_F32 0
+#define GT_BF16 1
+
+/* Version of this ABI (incremented on any incompatible change). */
+int32_t gt_abi_version(void);
+/* Static text for a status code. */
+const char* gt_status_string(gt_status status);
+/* Text of the last error raised on the calling thread ("" if none). */
+const char* gt_last_error(void);
+
+/* ------------------------------------------------------------------------ */
+/* CSR validation (the input convention above).                              */
+/* ------------------------------------------------------------------------ */
+
+size_t gt_validate_csr_workspace_size(void);
+/* SYNC.  GT_OK, or the first of GT_ERR_OUT_OF_RANGE, GT_ERR_UNSORTED,
+ * GT_ERR_DUPLICATE found on the device.  Never reads outside rowptr[0..n] and,
+ * for rows whose rowptr bounds are inside [0, nnz], col[rowptr[i]..rowptr[i+1]). */
+gt_status gt_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, void* ws,
+                          size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Cluster reordering, §3.3.                                                 */
+/* ------------------------------------------------------------------------ */
+/* Label propagation on the CSR (self-loops ignored), then a stable order by
+ * (label, -degree, id).  With k_t = seed + (t+1)*0x9E3779B97F4A7C15 (mod 2^64)
+ * and mix64 the SplitMix64 output function, sweep t moves every active node
+ * (the top three bits of mix64(v ^ k_t ^ 0xD6E8FEB86659FD93) not all zero) to
+ * the most frequent label among its neighbours, keeping its own label when
+ * that is among the most frequent and otherwise taking the smallest
+ * (mix64(label ^ k_t), label).  Propagation stops early when no node would
+ * move.  The result is a pure function of (CSR, iters, seed).
+ *   perm  int32[n]  out: perm[new] = old
+ *   iperm int32[n]  out: iperm[old] = new
+ *   labels int32[n] out (may be NULL): final label of each (old) node
+ *   sweeps_done (host, may be NULL): SYNC if given; sweeps that changed a label.
+ * The CSR must satisfy the input convention (see gt_validate_csr); it is
+ * validated here first (SYNC) and an invalid CSR returns its error code. */
+size_t gt_reorder_workspace_size(int64_t n, int64_t nnz);
+gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
+                     uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels, int32_t* sweeps_done,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Relabelling, §3.3 (the layout is reorganised by cluster).                 */
+/* ------------------------------------------------------------------------ */
+/* Row r of the output holds {iperm[c] : c in row perm[r]}, ascending.
+ * rowptr_out int64[n+1], col_out int32[nnz].  perm/iperm must be inverse
+ * permutations of [0, n) (not checked).  SYNC: the CSR is validated first and
+ * an invalid CSR returns its error code. */
+size_t gt_permute_workspace_size(int64_t n, int64_t nnz);
+gt_status gt_permute_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, const int32_t* perm,
+                         const int32_t* iperm, int64_t* rowptr_out, int32_t* col_out, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
+/* dst row r = src row perm[r] (rows of row_bytes bytes, a multiple of 4). */
+gt_status gt_gather_rows(int64_t n, int64_t row_bytes, const void* src, const int32_t* perm, void* dst,
+                         hipStream_t stream);
+/* dst row perm[r] = src row r (the inverse of gt_gather_rows). */
+gt_status gt_scatter_rows(int64_t n, int64_t row_bytes, const void* src, const int32_t* perm, void* dst,
+                          hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Tile plan, §3.4 (cluster sparsity; transfer threshold).                   */
+/* ------------------------------------------------------------------------ */
+/* R = ceil(n/T) tile rows/columns.  Tile (I, J) holds the edges (i, j) with
+ * i/T = I, j/T = J; cnt is their number, area = min(T, n-I*T)*min(T, n-J*T).
+ * The tile is dense iff cnt >= 1 and cnt*10^6 >= tau_ppm*area (exact integer
+ * comparison).  T in {64, 128}; R <= 16384. */
+/* Remainder rows (columns) with more than GT_LONG_ROW edges are processed by
+ * a whole workgroup each instead of a slice of a wavefront; the plan lists them. */
+#define GT_LONG_ROW 256
+
+typedef struct gt_tiles {
+    int64_t n;             /* nodes */
+    int32_t T;             /* tile edge */
+    int32_t reserved;
+    int64_t n_row_tiles;   /* R */
+    int64_t n_dense;       /* dense tiles */
+    int64_t nnz_sparse;    /* edges outside the dense tiles */
+    int64_t n_long_rows;   /* remainder rows with more than GT_LONG_ROW edges */
+    int64_t n_long_cols;   /* remainder columns with more than GT_LONG_ROW edges */
+    int64_t* tile_rowptr;  /* int64[R+1]: dense tiles of tile row I are [tile_rowptr[I], tile_rowptr[I+1]) */
+    int32_t* tile_col;     /* int32[n_dense]: J of each dense tile, sorted by (I, J) */
+    int32_t* tile_nnz;     /* int32[n_dense]: edges in the tile */
+    uint32_t* tile_mask;   /* uint32[n_dense*T*T/32]: row-major bit mask; bit b of word w of local row r
+                              marks column J*T + 32*w + b */
+    int64_t* sp_rowptr;    /* int64[n+1]: remainder CSR (edges outside dense tiles, CSR order) */
+    int32_t* sp_col;       /* int32[nnz_sparse] */
+    int64_t* sp_colptr;    /* int64[n+1]: remainder transpose (rows ascending in each column) */
+    int32_t* sp_row;       /* int32[nnz_sparse] */
+    int64_t* tileT_ptr;    /* int64[R+1]: dense tiles of tile column J, sorted by (J, I) */
+    int32_t* tileT_idx;    /* int32[n_dense]: index into the (I, J)-sorted list */
+    int32_t* long_rows;    /* int32[n_long_rows]: ascending */
+    int32_t* long_cols;    /* int32[n_long_cols]: ascending */
+} gt_tiles;
+
+size_t gt_tiles_workspace_size(int64_t n, int64_t nnz, int32_t T);
+/* SYNC.  Validates the CSR, then sets plan->n, T, n_row_tiles, n_dense,
+ * nnz_sparse, n_long_rows and n_long_cols (host struct; array pointers are
+ * left untouched). */
+gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
+                         uint32_t tau_ppm, gt_tiles* plan, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Fills every array of *plan.  The size fields must be those set by
+ * gt_tiles_count for the same arguments and every array pointer a caller
+ * allocation of the size given above.  The CSR is the one gt_tiles_count
+ * validated. */
+gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
+                         uint32_t tau_ppm, gt_tiles* plan, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Neighbourhood softmax attention, §3.2, over a plan (reordered index space).*/
+/* ------------------------------------------------------------------------ */
+/* For each node i and head h, over j in N(i) (the dense tiles plus the remainder):
+ *   s_ij = scale*<Q[i,h],K[j,h]>, LSE[i,h] = log sum_j exp(s_ij),
+ *   O[i,h] = sum_j exp(s_ij - LSE[i,h]) V[j,h].
+ * An empty row gives O = 0 and LSE = -inf.  `plan` is a host struct built by
+ * gt_build_tiles (its arrays stay valid until the call has run). */
+size_t gt_sparse_attn_fwd_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
+gt_status gt_sparse_attn_fwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
+                             const void* K, const void* V, float scale, void* O, float* LSE, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+
+/* Backward for an upstream gradient dO, given O and LSE of the forward:
+ *   D_i = <dO_i, O_i>, P_ij = exp(s_ij - LSE_i), dS_ij = P_ij (<dO_i, V_j> - D_i),
+ *   dQ_i = scale sum_j dS_ij K_j, dK_j = scale sum_i dS_ij Q_i, dV_j = sum_i P_ij dO_i.
+ * dK and dV are gathered per column (no atomics): results are bitwise
+ * reproducible for a fixed plan. */
+size_t gt_sparse_attn_bwd_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
+gt_status gt_sparse_attn_bwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
+                             const void* K, const void* V, const void* O, const void* dO, const float* LSE,
+                             float scale, void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* The backward in its two halves, for callers that schedule them apart (the
+ * combined call above is rows then cols).
+ * _rows: dQ (row-owned) and the row statistic Dstat[i, h] = <dO_i, O_i>
+ *        (fp32 [n, H], written here, read by _cols).
+ * _cols: dK and dV (column-owned), from Dstat of the _rows call. */
+size_t gt_sparse_attn_bwd_rows_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
+gt_status gt_sparse_attn_bwd_rows(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
+                                  const void* K, const void* V, const void* O, const void* dO, const float* LSE,
+                                  float scale, void* dQ, float* Dstat, void* ws, size_t ws_bytes, hipStream_t stream);
+size_t gt_sparse_attn_bwd_cols_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
+gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
+                                  const void* K, const void* V, const void* dO, const float* LSE, const float* Dstat,
+                                  float scale, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Full softmax attention, §2.1 Eq. (1) (the interleaved dense layer of §3.2).*/
+/* ------------------------------------------------------------------------ */
+/* Same formulas with N(i) = all n nodes.  GT_BF16 only; d in {32, 64}. */
+gt_status gt_dense_attn_fwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
+                            const void* V, float scale, void* O, float* LSE, hipStream_t stream);
+size_t gt_dense_attn_bwd_workspace_size(int64_t n, int32_t H, int32_t d, gt_dtype dtype);
+gt_status gt_dense_attn_bwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
+                            const void* V, const void* O, const void* dO, const float* LSE, float scale, void* dQ,
+                            void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GT_H */

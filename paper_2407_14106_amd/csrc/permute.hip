@@ -1,0 +1,135 @@
+// Relabelling of the CSR by a node permutation (§3.3: the layout is
+// reorganised by cluster once the full sequence is on the device), and row
+// gathers/scatters of feature tensors.
+//
+// The relabelled CSR is produced by one stable radix sort of the packed keys
+// (iperm[row] << B) | iperm[col]: after sorting, the keys are grouped by new
+// row and ascending inside each row, which is exactly the new CSR order.
+#include "prim.h"
+
+namespace gt {
+namespace {
+
+__global__ void k_new_degrees(int64_t n, const int64_t* rowptr, const int32_t* perm, int64_t* deg_new) {
+    for (int64_t r = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; r < n; r += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t u = perm[r];
+        deg_new[r] = rowptr[u + 1] - rowptr[u];
+    }
+}
+
+// One wavefront per old row: every edge (u, c) becomes key (iperm[u] << B) | iperm[c].
+__global__ __launch_bounds__(256) void k_edge_keys(int64_t n, const int64_t* rowptr, const int32_t* col,
+                                                   const int32_t* iperm, int bits, uint64_t* keys) {
+    const int lane = lane_id();
+    const int64_t waves = int64_t(gridDim.x) * 4;
+    for (int64_t u = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; u < n; u += waves) {
+        const int64_t a = rowptr[u], b = rowptr[u + 1];
+        const uint64_t hi = uint64_t(uint32_t(iperm[u])) << bits;
+        for (int64_t e = a + lane; e < b; e += kWave) keys[e] = hi | uint64_t(uint32_t(iperm[col[e]]));
+    }
+}
+
+__global__ void k_key_cols(int64_t nnz, const uint64_t* keys, uint64_t mask, int32_t* col_out) {
+    for (int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; e < nnz; e += int64_t(gridDim.x) * blockDim.x)
+        col_out[e] = int32_t(keys[e] & mask);
+}
+
+// One wavefront per row; dwords per lane.
+template <bool kGather>
+__global__ __launch_bounds__(256) void k_move_rows(int64_t n, int64_t words, const uint32_t* src,
+                                                   const int32_t* perm, uint32_t* dst) {
+    const int lane = lane_id();
+    const int64_t waves = int64_t(gridDim.x) * 4;
+    for (int64_t r = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; r < n; r += waves) {
+        const int64_t p = perm[r];
+        const uint32_t* s = src + (kGather ? p : r) * words;
+        uint32_t* d = dst + (kGather ? r : p) * words;
+        for (int64_t w = lane; w < words; w += kWave) d[w] = s[w];
+    }
+}
+
+struct PermuteWs {
+    uint32_t* flags;
+    int64_t* deg_new;
+    uint64_t* keys;
+    ScanTmp scan;
+    SortTmp sort;
+};
+
+PermuteWs carve(Ws& ws, int64_t n, int64_t nnz) {
+    PermuteWs p;
+    const int64_t n1 = n > 0 ? n : 1, e1 = nnz > 0 ? nnz : 1;
+    p.flags = ws.take<uint32_t>(1);
+    p.deg_new = ws.take<int64_t>(n1);
+    p.keys = ws.take<uint64_t>(e1);
+    p.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1)));
+    p.sort = sort_tmp(ws, e1, 8, false);
+    return p;
+}
+
+}  // namespace
+}  // namespace gt
+
+using namespace gt;
+
+extern "C" size_t gt_permute_workspace_size(int64_t n, int64_t nnz) {
+    Ws ws(nullptr);
+    carve(ws, n, nnz);
+    return ws.size();
+}
+
+extern "C" gt_status gt_permute_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                                    const int32_t* perm, const int32_t* iperm, int64_t* rowptr_out,
+                                    int32_t* col_out, void* ws_ptr, size_t ws_bytes, hipStream_t stream) {
+    if (n < 0 || nnz < 0 || n >= (int64_t(1) << 31) || nnz >= (int64_t(1) << 32))
+        return fail(GT_ERR_INVALID_ARG, "gt_permute_csr: n or nnz out of range");
+    if (!rowptr || !rowptr_out || (nnz > 0 && (!col || !col_out)) || (n > 0 && (!perm || !iperm)) || !ws_ptr)
+        return fail(GT_ERR_INVALID_ARG, "gt_permute_csr: null pointer");
+    if (ws_bytes < gt_permute_workspace_size(n, nnz))
+        return fail(GT_ERR_WORKSPACE, "gt_permute_csr: workspace too small");
+    Ws ws(ws_ptr);
+    PermuteWs p = carve(ws, n, nnz);
+    gt_status st;
+    if (n == 0) return fill_i64(rowptr_out, 1, 0, stream);
+    if ((st = launch_validate_csr(n, nnz, rowptr, col, p.flags, stream)) != GT_OK) return st;
+    if ((st = read_validation(p.flags, stream)) != GT_OK) return st;
+    const unsigned g = grid_for(n, 256, 8192);
+    k_new_degrees<<<g, 256, 0, stream>>>(n, rowptr, perm, p.deg_new);
+    GT_LAUNCH_CHECK("permute_degrees");
+    if ((st = exclusive_scan_i64(p.deg_new, n, rowptr_out, p.scan, stream)) != GT_OK) return st;
+    if (nnz == 0) return GT_OK;
+    const int bits = bits_for(n);
+    k_edge_keys<<<grid_for(n, 4, 65536), 256, 0, stream>>>(n, rowptr, col, iperm, bits, p.keys);
+    GT_LAUNCH_CHECK("permute_keys");
+    if ((st = radix_sort_u64(p.keys, nullptr, nnz, 2 * bits, p.sort, stream)) != GT_OK) return st;
+    k_key_cols<<<grid_for(nnz, 256, 16384), 256, 0, stream>>>(nnz, p.keys, (uint64_t(1) << bits) - 1, col_out);
+    GT_LAUNCH_CHECK("permute_cols");
+    return GT_OK;
+}
+
+static gt_status move_rows(bool gather, int64_t n, int64_t row_bytes, const void* src, const int32_t* perm,
+                           void* dst, hipStream_t stream) {
+    if (n < 0 || row_bytes < 0 || row_bytes % 4 != 0)
+        return fail(GT_ERR_INVALID_ARG, "gt_gather_rows/gt_scatter_rows: bad n or row_bytes (must be a multiple of 4)");
+    if (n == 0 || row_bytes == 0) return GT_OK;
+    if (!src || !dst || !perm) return fail(GT_ERR_INVALID_ARG, "gt_gather_rows/gt_scatter_rows: null pointer");
+    const unsigned g = grid_for(n, 4, 65536);
+    if (gather)
+        k_move_rows<true><<<g, 256, 0, stream>>>(n, row_bytes / 4, static_cast<const uint32_t*>(src), perm,
+                                                  static_cast<uint32_t*>(dst));
+    else
+        k_move_rows<false><<<g, 256, 0, stream>>>(n, row_bytes / 4, static_cast<const uint32_t*>(src), perm,
+                                                   static_cast<uint32_t*>(dst));
+    GT_LAUNCH_CHECK("move_rows");
+    return GT_OK;
+}
+
+extern "C" gt_status gt_gather_rows(int64_t n, int64_t row_bytes, const void* src, const int32_t* perm, void* dst,
+                                    hipStream_t stream) {
+    return move_rows(true, n, row_bytes, src, perm, dst, stream);
+}
+
+extern "C" gt_status gt_scatter_rows(int64_t n, int64_t row_bytes, const void* src, const int32_t* perm, void* dst,
+                                     hipStream_t stream) {
+    return move_rows(false, n, row_bytes, src, perm, dst, stream);
+}

@@ -1,0 +1,369 @@
+// Device-wide building blocks: fills, scans, key counts, stable radix sort,
+// CSR validation.  See prim.h.
+#include "prim.h"
+
+namespace gt {
+
+// ============================================================== fills/copies
+
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        p[i] = v;
+}
+__global__ void k_fill_i64(int64_t* p, int64_t n, int64_t v) {
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        p[i] = v;
+}
+__global__ void k_iota_u32(uint32_t* p, int64_t n) {
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        p[i] = uint32_t(i);
+}
+
+gt_status fill_u32(uint32_t* p, int64_t n, uint32_t value, hipStream_t s) {
+    if (n <= 0) return GT_OK;
+    k_fill_u32<<<grid_for(n, 256, 8192), 256, 0, s>>>(p, n, value);
+    GT_LAUNCH_CHECK("fill_u32");
+    return GT_OK;
+}
+gt_status fill_i64(int64_t* p, int64_t n, int64_t value, hipStream_t s) {
+    if (n <= 0) return GT_OK;
+    k_fill_i64<<<grid_for(n, 256, 8192), 256, 0, s>>>(p, n, value);
+    GT_LAUNCH_CHECK("fill_i64");
+    return GT_OK;
+}
+gt_status iota_u32(uint32_t* p, int64_t n, hipStream_t s) {
+    if (n <= 0) return GT_OK;
+    k_iota_u32<<<grid_for(n, 256, 8192), 256, 0, s>>>(p, n);
+    GT_LAUNCH_CHECK("iota_u32");
+    return GT_OK;
+}
+gt_status copy_bytes(void* dst, const void* src, int64_t bytes, hipStream_t s) {
+    if (bytes <= 0) return GT_OK;
+    GT_HIP(hipMemcpyAsync(dst, src, size_t(bytes), hipMemcpyDeviceToDevice, s));
+    return GT_OK;
+}
+
+// ===================================================================== scan
+
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kScanThreads * kScanItems;
+
+int64_t scan_tmp_elems(int64_t n) { return cdiv(n, kScanTile) + 1; }
+
+template <typename In>
+__device__ __forceinline__ int64_t load_as_i64(const In* p, int64_t i, int64_t n) {
+    return i < n ? static_cast<int64_t>(p[i]) : 0;
+}
+
+// Block-wide exclusive scan of one value per thread; returns the block total.
+__device__ __forceinline__ int64_t block_exscan(int64_t v, int64_t* excl) {
+    __shared__ int64_t s_w[kScanThreads / kWave];
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    int64_t x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        int64_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s_w[w] = x;
+    __syncthreads();
+    int64_t before = 0, total = 0;
+#pragma unroll
+    for (int i = 0; i < kScanThreads / kWave; ++i) {
+        int64_t t = s_w[i];
+        if (i < w) before += t;
+        total += t;
+    }
+    __syncthreads();
+    *excl = before + x - v;
+    return total;
+}
+
+template <typename In>
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const In* in, int64_t n, int64_t* sums) {
+    const int64_t base = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
+    int64_t acc = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) acc += load_as_i64(in, base + k, n);
+    int64_t ex;
+    int64_t tot = block_exscan(acc, &ex);
+    if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+// Single block: exclusive scan of nb sums in place; sums[nb] = total.
+__global__ __launch_bounds__(kScanThreads) void k_scan_sums(int64_t* sums, int64_t nb) {
+    const int64_t per = cdiv(nb, kScanThreads);
+    const int64_t lo = int64_t(threadIdx.x) * per;
+    const int64_t hi = lo + per < nb ? lo + per : nb;
+    int64_t acc = 0;
+    for (int64_t i = lo; i < hi; ++i) acc += sums[i];
+    int64_t ex;
+    int64_t tot = block_exscan(acc, &ex);
+    for (int64_t i = lo; i < hi; ++i) {
+        int64_t t = sums[i];
+        sums[i] = ex;
+        ex += t;
+    }
+    if (threadIdx.x == 0) sums[nb] = tot;
+}
+
+template <typename In>
+__global__ __launch_bounds__(kScanThreads) void k_scan_apply(const In* in, int64_t n, const int64_t* sums,
+                                                              int64_t nb, int64_t* out) {
+    const int64_t base = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
+    int64_t v[kScanItems];
+    int64_t acc = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        v[k] = load_as_i64(in, base + k, n);
+        acc += v[k];
+    }
+    int64_t ex;
+    block_exscan(acc, &ex);
+    ex += sums[blockIdx.x];
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        if (base + k < n) out[base + k] = ex;
+        ex += v[k];
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) out[n] = sums[nb];
+}
+
+template <typename In>
+static gt_status exscan(const In* in, int64_t n, int64_t* out, ScanTmp tmp, hipStream_t s) {
+    if (n <= 0) return fill_i64(out, 1, 0, s);
+    const int64_t nb = cdiv(n, kScanTile);
+    k_scan_reduce<In><<<unsigned(nb), kScanThreads, 0, s>>>(in, n, tmp.block_sums);
+    GT_LAUNCH_CHECK("scan_reduce");
+    k_scan_sums<<<1, kScanThreads, 0, s>>>(tmp.block_sums, nb);
+    GT_LAUNCH_CHECK("scan_sums");
+    k_scan_apply<In><<<unsigned(nb), kScanThreads, 0, s>>>(in, n, tmp.block_sums, nb, out);
+    GT_LAUNCH_CHECK("scan_apply");
+    return GT_OK;
+}
+
+gt_status exclusive_scan_i32(const int32_t* in, int64_t n, int64_t* out, ScanTmp tmp, hipStream_t s) {
+    return exscan(in, n, out, tmp, s);
+}
+gt_status exclusive_scan_u32(const uint32_t* in, int64_t n, int64_t* out, ScanTmp tmp, hipStream_t s) {
+    return exscan(in, n, out, tmp, s);
+}
+gt_status exclusive_scan_i64(const int64_t* in, int64_t n, int64_t* out, ScanTmp tmp, hipStream_t s) {
+    return exscan(in, n, out, tmp, s);
+}
+
+// =============================================================== key counts
+
+__global__ void k_count_keys(const int32_t* keys, int64_t n, uint32_t* counts) {
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        atomicAdd(&counts[keys[i]], 1u);
+}
+
+gt_status count_keys(const int32_t* keys, int64_t n, uint32_t* counts, hipStream_t s) {
+    if (n <= 0) return GT_OK;
+    k_count_keys<<<grid_for(n, 256, 16384), 256, 0, s>>>(keys, n, counts);
+    GT_LAUNCH_CHECK("count_keys");
+    return GT_OK;
+}
+
+// =============================================================== radix sort
+// 256 threads, 16 rounds of 256 keys per tile; key idx = tile*4096 + round*256 + tid.
+// Digits are ranked in (round, wave, lane) order, which is the input order, so
+// each pass is stable and the whole LSD sort is stable.
+
+constexpr int kSortThreads = 256;
+constexpr int kSortRounds = 16;
+constexpr int kSortTile = kSortThreads * kSortRounds;
+constexpr int kSortWaves = kSortThreads / kWave;
+
+int64_t sort_tiles(int64_t n) { return cdiv(n, kSortTile); }
+
+SortTmp sort_tmp(Ws& ws, int64_t n, int key_bytes, bool with_values) {
+    SortTmp t;
+    const int64_t tiles = sort_tiles(n > 0 ? n : 1);
+    t.keys_alt = ws.take<char>(size_t(n > 0 ? n : 1) * key_bytes);
+    t.vals_alt = with_values ? ws.take<uint32_t>(size_t(n > 0 ? n : 1)) : nullptr;
+    t.hist = ws.take<uint32_t>(size_t(256 * tiles));
+    t.offsets = ws.take<int64_t>(size_t(256 * tiles + 1));
+    t.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(256 * tiles)));
+    return t;
+}
+
+template <typename K>
+__global__ __launch_bounds__(kSortThreads) void k_sort_hist(const K* keys, int64_t n, int shift, int64_t tiles,
+                                                             uint32_t* hist) {
+    __shared__ uint32_t s_h[256];
+    s_h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = int64_t(blockIdx.x) * kSortTile;
+    for (int r = 0; r < kSortRounds; ++r) {
+        const int64_t i = base + r * kSortThreads + threadIdx.x;
+        if (i < n) atomicAdd(&s_h[uint32_t(keys[i] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    hist[int64_t(threadIdx.x) * tiles + blockIdx.x] = s_h[threadIdx.x];
+}
+
+template <typename K>
+__global__ __launch_bounds__(kSortThreads) void k_sort_scatter(const K* keys, const uint32_t* vals, int64_t n,
+                                                                int shift, int64_t tiles, const int64_t* offsets,
+                                                                K* keys_out, uint32_t* vals_out) {
+    __shared__ int64_t s_base[256];
+    __shared__ int64_t s_w[kSortWaves][256];
+    const int tid = threadIdx.x;
+    const int w = tid / kWave;
+    s_base[tid] = offsets[int64_t(tid) * tiles + blockIdx.x];
+#pragma unroll
+    for (int k = 0; k < kSortWaves; ++k) s_w[k][tid] = 0;
+    __syncthreads();
+    const int64_t base = int64_t(blockIdx.x) * kSortTile;
+    const uint64_t lt = lanemask_lt();
+    for (int r = 0; r < kSortRounds; ++r) {
+        const int64_t i = base + r * kSortThreads + tid;
+        const bool valid = i < n;
+        K key = valid ? keys[i] : K(0);
+        uint32_t val = (valid && vals) ? vals[i] : 0u;
+        const uint32_t d = uint32_t(key >> shift) & 255u;
+        uint64_t peers = ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bm = ballot(bit);
+            peers &= bit ? bm : ~bm;
+        }
+        const int rank = __popcll(peers & lt);
+        if (valid && rank == 0) s_w[w][d] = __popcll(peers);
+        __syncthreads();
+        {
+            int64_t run = s_base[tid];
+#pragma unroll
+            for (int k = 0; k < kSortWaves; ++k) {
+                const int64_t c = s_w[k][tid];
+                s_w[k][tid] = run;
+                run += c;
+            }
+            s_base[tid] = run;
+        }
+        __syncthreads();
+        if (valid) {
+            const int64_t pos = s_w[w][d] + rank;
+            keys_out[pos] = key;
+            if (vals) vals_out[pos] = val;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kSortWaves; ++k) s_w[k][tid] = 0;
+        __syncthreads();
+    }
+}
+
+template <typename K>
+static gt_status radix_sort(K* keys, uint32_t* values, int64_t n, int key_bits, SortTmp tmp, hipStream_t s) {
+    if (n <= 1) return GT_OK;
+    const int64_t tiles = sort_tiles(n);
+    K* src_k = keys;
+    K* dst_k = static_cast<K*>(tmp.keys_alt);
+    uint32_t* src_v = values;
+    uint32_t* dst_v = values ? tmp.vals_alt : nullptr;
+    int passes = 0;
+    for (int shift = 0; shift < key_bits; shift += 8, ++passes) {
+        k_sort_hist<K><<<unsigned(tiles), kSortThreads, 0, s>>>(src_k, n, shift, tiles, tmp.hist);
+        GT_LAUNCH_CHECK("sort_hist");
+        gt_status st = exclusive_scan_u32(tmp.hist, 256 * tiles, tmp.offsets, tmp.scan, s);
+        if (st != GT_OK) return st;
+        k_sort_scatter<K><<<unsigned(tiles), kSortThreads, 0, s>>>(src_k, src_v, n, shift, tiles, tmp.offsets,
+                                                                   dst_k, dst_v);
+        GT_LAUNCH_CHECK("sort_scatter");
+        K* tk = src_k;
+        src_k = dst_k;
+        dst_k = tk;
+        uint32_t* tv = src_v;
+        src_v = dst_v;
+        dst_v = tv;
+    }
+    if (passes & 1) {
+        gt_status st = copy_bytes(keys, src_k, n * int64_t(sizeof(K)), s);
+        if (st != GT_OK) return st;
+        if (values) {
+            st = copy_bytes(values, src_v, n * 4, s);
+            if (st != GT_OK) return st;
+        }
+    }
+    return GT_OK;
+}
+
+gt_status radix_sort_u32(uint32_t* keys, uint32_t* values, int64_t n, int key_bits, SortTmp tmp, hipStream_t s) {
+    return radix_sort<uint32_t>(keys, values, n, key_bits, tmp, s);
+}
+gt_status radix_sort_u64(uint64_t* keys, uint32_t* values, int64_t n, int key_bits, SortTmp tmp, hipStream_t s) {
+    return radix_sort<uint64_t>(keys, values, n, key_bits, tmp, s);
+}
+
+// =========================================================== CSR validation
+
+__global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                               uint32_t* flags) {
+    uint32_t f = 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        if (rowptr[0] != 0 || rowptr[n] != nnz) f |= kOutOfRange;
+    }
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t a = rowptr[i], b = rowptr[i + 1];
+        if (a > b) {
+            f |= kUnsorted;
+            continue;
+        }
+        if (a < 0 || b > nnz) {
+            f |= kOutOfRange;
+            continue;
+        }
+        int64_t prev = -1;
+        for (int64_t e = a; e < b; ++e) {
+            const int64_t c = col[e];
+            if (c < 0 || c >= n) f |= kOutOfRange;
+            if (c == prev) f |= kDuplicate;
+            else if (c < prev) f |= kUnsorted;
+            prev = c;
+        }
+    }
+    if (f) atomicOr(flags, f);
+}
+
+gt_status launch_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, uint32_t* flags,
+                              hipStream_t s) {
+    gt_status st = fill_u32(flags, 1, 0, s);
+    if (st != GT_OK) return st;
+    k_validate_csr<<<grid_for(n > 0 ? n : 1, 256, 4096), 256, 0, s>>>(n, nnz, rowptr, col, flags);
+    GT_LAUNCH_CHECK("validate_csr");
+    return GT_OK;
+}
+
+gt_status read_validation(const uint32_t* flags, hipStream_t s) {
+    uint32_t f = 0;
+    GT_HIP(hipMemcpyAsync(&f, flags, sizeof(f), hipMemcpyDeviceToHost, s));
+    GT_HIP(hipStreamSynchronize(s));
+    if (f & kOutOfRange) return fail(GT_ERR_OUT_OF_RANGE, "CSR: rowptr or column index out of range");
+    if (f & kDuplicate) return fail(GT_ERR_DUPLICATE, "CSR: repeated column inside a row");
+    if (f & kUnsorted) return fail(GT_ERR_UNSORTED, "CSR: row not strictly increasing or rowptr decreasing");
+    return GT_OK;
+}
+
+}  // namespace gt
+
+using namespace gt;
+
+extern "C" size_t gt_validate_csr_workspace_size(void) { return 256; }
+
+extern "C" gt_status gt_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, void* ws,
+                                     size_t ws_bytes, hipStream_t stream) {
+    if (n < 0 || nnz < 0 || n >= (int64_t(1) << 31) || nnz >= (int64_t(1) << 32))
+        return fail(GT_ERR_INVALID_ARG, "gt_validate_csr: n or nnz out of range");
+    if (!rowptr || (nnz > 0 && !col) || !ws) return fail(GT_ERR_INVALID_ARG, "gt_validate_csr: null pointer");
+    if (ws_bytes < gt_validate_csr_workspace_size()) return fail(GT_ERR_WORKSPACE, "gt_validate_csr: workspace too small");
+    uint32_t* flags = static_cast<uint32_t*>(ws);
+    gt_status st = launch_validate_csr(n, nnz, rowptr, col, flags, stream);
+    if (st != GT_OK) return st;
+    return read_validation(flags, stream);
+}

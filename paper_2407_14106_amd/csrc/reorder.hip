@@ -1,0 +1,393 @@
+// Cluster reordering (§3.3): label propagation with hashed tie-breaks and
+// hashed partial activation, then a stable sort by (label, -degree, id).
+//
+// Rows are handled by size:
+//   deg <= 64          one wavefront per row, one neighbour label per lane;
+//                      multiplicities by an in-register all-pairs compare.
+//   64 < deg <= 4096   one workgroup per row, open-addressing count table in LDS.
+//   deg > 4096         one workgroup per row, count table in the workspace.
+// All three compute the same function of the neighbour-label multiset.
+#include <limits.h>
+
+#include "prim.h"
+
+namespace gt {
+
+namespace {
+
+constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kActivitySalt = 0xD6E8FEB86659FD93ull;
+constexpr int kWaveRowMax = 64;
+constexpr int kLdsTable = 8192;      // entries (int32 key + uint32 count): 64 KiB
+constexpr int kLdsRowMax = kLdsTable / 2;
+constexpr int kBlock = 256;
+constexpr int kMaxSweeps = 1000;
+
+__device__ __forceinline__ bool is_active(int64_t v, uint64_t key) {
+    return (mix64(uint64_t(v) ^ key ^ kActivitySalt) >> 61) != 0;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
+    uint32_t lo = __shfl_xor(uint32_t(v), o, kWave);
+    uint32_t hi = __shfl_xor(uint32_t(v >> 32), o, kWave);
+    return (uint64_t(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        uint64_t w = shfl_xor_u64(v, o);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+__device__ __forceinline__ int wave_min_i32(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        int w = __shfl_xor(v, o, kWave);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+
+// -------------------------------------------------------------- per-row classes
+
+__global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
+                           int32_t* is_med, int32_t* is_big, int64_t* big_cap) {
+    for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        // self-loop present?  rows are sorted: binary search for v.
+        int64_t lo = a, hi = b;
+        while (lo < hi) {
+            int64_t m = (lo + hi) >> 1;
+            if (col[m] < v) lo = m + 1;
+            else hi = m;
+        }
+        const bool self = lo < b && col[lo] == v;
+        const int64_t deg = b - a;
+        deg_off[v] = uint32_t(deg - (self ? 1 : 0));
+        is_med[v] = (deg > kWaveRowMax && deg <= kLdsRowMax) ? 1 : 0;
+        const bool big = deg > kLdsRowMax;
+        is_big[v] = big ? 1 : 0;
+        int64_t cap = 1;
+        while (cap < 2 * deg) cap <<= 1;
+        big_cap[v] = big ? cap : 0;
+    }
+}
+
+__global__ void k_compact(int64_t n, const int32_t* is_med, const int32_t* is_big, const int64_t* pos_med,
+                          const int64_t* pos_big, const int64_t* cap_off, int32_t* med_list, int32_t* big_list,
+                          int64_t* big_off) {
+    for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
+        if (is_med[v]) med_list[pos_med[v]] = int32_t(v);
+        if (is_big[v]) {
+            big_list[pos_big[v]] = int32_t(v);
+            big_off[pos_big[v]] = cap_off[v];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ wave rows
+
+__global__ __launch_bounds__(kBlock) void k_lp_wave(int64_t n, const int64_t* rowptr, const int32_t* col,
+                                                    const int32_t* lab_in, int32_t* lab_out, uint64_t key,
+                                                    const uint32_t* flag_prev, uint32_t* flag_next) {
+    const bool converged = *flag_prev == 0;
+    const int lane = lane_id();
+    const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
+    for (int64_t v = int64_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave; v < n; v += waves) {
+        const int own = lab_in[v];
+        if (converged) {
+            if (lane == 0) lab_out[v] = own;
+            continue;
+        }
+        const int64_t a = rowptr[v];
+        const int deg = int(rowptr[v + 1] - a);
+        if (deg > kWaveRowMax) continue;  // handled by the workgroup kernels
+        int c = lane < deg ? col[a + lane] : -1;
+        const bool valid = lane < deg && c != v;
+        const int L = valid ? lab_in[c] : -1;
+        int cnt = 0;
+        for (int k = 0; k < deg; ++k) {
+            const int Lk = __shfl(L, k, kWave);
+            cnt += (Lk == L) ? 1 : 0;
+        }
+        if (!valid) cnt = 0;
+        const int best = wave_max(cnt);
+        int cand = own;
+        if (best > 0) {
+            const int own_cnt = __popcll(ballot(valid && L == own));
+            if (own_cnt != best) {
+                const bool top = valid && cnt == best;
+                const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
+                const uint64_t hmin = wave_min_u64(h);
+                cand = wave_min_i32((top && h == hmin) ? L : INT_MAX);
+            }
+        }
+        if (lane == 0) {
+            lab_out[v] = is_active(v, key) ? cand : own;
+            if (cand != own) *flag_next = 1u;
+        }
+    }
+}
+
+// ------------------------------------------------------------- workgroup rows
+
+__device__ __forceinline__ int block_max_i32(int v, int* s) {
+    v = wave_max(v);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) s[w] = v;
+    __syncthreads();
+    int r = s[0];
+    for (int i = 1; i < kBlock / kWave; ++i) r = s[i] > r ? s[i] : r;
+    __syncthreads();
+    return r;
+}
+__device__ __forceinline__ uint64_t block_min_u64(uint64_t v, uint64_t* s) {
+    v = wave_min_u64(v);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) s[w] = v;
+    __syncthreads();
+    uint64_t r = s[0];
+    for (int i = 1; i < kBlock / kWave; ++i) r = s[i] < r ? s[i] : r;
+    __syncthreads();
+    return r;
+}
+
+template <bool kGlobal>
+__device__ __forceinline__ int tab_load(const int* p) {
+    if (kGlobal) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return *p;
+}
+
+// One workgroup per listed row.  Table: keys (label or -1) and counts.
+template <bool kGlobal>
+__global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const int64_t* list_len,
+                                                     const int64_t* rowptr, const int32_t* col,
+                                                     const int32_t* lab_in, int32_t* lab_out, uint64_t key,
+                                                     const uint32_t* flag_prev, uint32_t* flag_next,
+                                                     int* gkeys, int* gcnts, const int64_t* big_off) {
+    __shared__ int s_keys[kGlobal ? 1 : kLdsTable];
+    __shared__ int s_cnts[kGlobal ? 1 : kLdsTable];
+    __shared__ int s_red[kBlock / kWave];
+    __shared__ uint64_t s_red64[kBlock / kWave];
+    const bool converged = *flag_prev == 0;
+    const int64_t len = *list_len;
+    for (int64_t idx = blockIdx.x; idx < len; idx += gridDim.x) {
+        const int64_t v = list[idx];
+        const int own = lab_in[v];
+        if (converged) {
+            if (threadIdx.x == 0) lab_out[v] = own;
+            continue;
+        }
+        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        const int64_t deg = b - a;
+        int64_t cap = 1;
+        while (cap < 2 * deg) cap <<= 1;
+        int* tk = kGlobal ? gkeys + big_off[idx] : s_keys;
+        int* tc = kGlobal ? gcnts + big_off[idx] : s_cnts;
+        for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+            tk[s] = -1;
+            tc[s] = 0;
+        }
+        if (kGlobal) __threadfence();
+        __syncthreads();
+        for (int64_t e = a + threadIdx.x; e < b; e += kBlock) {
+            const int c = col[e];
+            if (c == v) continue;
+            const int L = lab_in[c];
+            int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
+            while (true) {
+                const int prev = atomicCAS(&tk[slot], -1, L);
+                if (prev == -1 || prev == L) {
+                    atomicAdd(&tc[slot], 1);
+                    break;
+                }
+                slot = (slot + 1) & (cap - 1);
+            }
+        }
+        if (kGlobal) __threadfence();
+        __syncthreads();
+        int best = 0, own_cnt = 0;
+        for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+            const int k = tab_load<kGlobal>(&tk[s]);
+            if (k < 0) continue;
+            const int c = tab_load<kGlobal>(&tc[s]);
+            best = c > best ? c : best;
+            if (k == own) own_cnt = c;
+        }
+        best = block_max_i32(best, s_red);
+        own_cnt = block_max_i32(own_cnt, s_red);
+        int cand = own;
+        if (best > 0 && own_cnt != best) {
+            uint64_t hbest = ~0ull;
+            for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+                const int k = tab_load<kGlobal>(&tk[s]);
+                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
+                const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
+                hbest = h < hbest ? h : hbest;
+            }
+            hbest = block_min_u64(hbest, s_red64);
+            uint64_t lbest = ~0ull;
+            for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+                const int k = tab_load<kGlobal>(&tk[s]);
+                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
+                if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
+                lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
+            }
+            cand = int(block_min_u64(lbest, s_red64));
+        }
+        if (threadIdx.x == 0) {
+            lab_out[v] = is_active(v, key) ? cand : own;
+            if (cand != own) *flag_next = 1u;
+        }
+        __syncthreads();
+    }
+}
+
+// --------------------------------------------------------------------- order
+
+__global__ void k_order_keys(int64_t n, const int32_t* lab, const uint32_t* deg_off, uint64_t* keys) {
+    for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x)
+        keys[v] = (uint64_t(uint32_t(lab[v])) << 32) | uint64_t(0xFFFFFFFFu - deg_off[v]);
+}
+
+__global__ void k_finish_order(int64_t n, const uint32_t* sorted_ids, const int32_t* lab, int32_t* perm,
+                               int32_t* iperm, int32_t* labels) {
+    for (int64_t r = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; r < n; r += int64_t(gridDim.x) * blockDim.x) {
+        const uint32_t old = sorted_ids[r];
+        perm[r] = int32_t(old);
+        iperm[old] = int32_t(r);
+        if (labels) labels[r] = lab[r];
+    }
+}
+
+struct ReorderWs {
+    uint32_t* flags;
+    int32_t* lab[2];
+    uint32_t* deg_off;
+    int32_t* is_med;
+    int32_t* is_big;
+    int64_t* big_cap;
+    int64_t* pos_med;
+    int64_t* pos_big;
+    int64_t* cap_off;
+    int32_t* med_list;
+    int32_t* big_list;
+    int64_t* big_off;
+    int* tab_keys;
+    int* tab_cnts;
+    uint64_t* sort_keys;
+    uint32_t* sort_vals;
+    ScanTmp scan;
+    SortTmp sort;
+};
+
+ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
+    ReorderWs r;
+    const int64_t n1 = n > 0 ? n : 1;
+    (void)iters;
+    r.flags = ws.take<uint32_t>(size_t(kMaxSweeps + 2));
+    r.lab[0] = ws.take<int32_t>(n1);
+    r.lab[1] = ws.take<int32_t>(n1);
+    r.deg_off = ws.take<uint32_t>(n1);
+    r.is_med = ws.take<int32_t>(n1);
+    r.is_big = ws.take<int32_t>(n1);
+    r.big_cap = ws.take<int64_t>(n1);
+    r.pos_med = ws.take<int64_t>(n1 + 1);
+    r.pos_big = ws.take<int64_t>(n1 + 1);
+    r.cap_off = ws.take<int64_t>(n1 + 1);
+    r.med_list = ws.take<int32_t>(n1);
+    r.big_list = ws.take<int32_t>(n1);
+    r.big_off = ws.take<int64_t>(n1);
+    const int64_t tab = 4 * (nnz > 0 ? nnz : 1);  // sum over big rows of cap <= 4 * deg
+    r.tab_keys = ws.take<int>(size_t(tab));
+    r.tab_cnts = ws.take<int>(size_t(tab));
+    r.sort_keys = ws.take<uint64_t>(n1);
+    r.sort_vals = ws.take<uint32_t>(n1);
+    r.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1)));
+    r.sort = sort_tmp(ws, n1, 8, true);
+    return r;
+}
+
+}  // namespace
+
+}  // namespace gt
+
+using namespace gt;
+
+extern "C" size_t gt_reorder_workspace_size(int64_t n, int64_t nnz) {
+    Ws ws(nullptr);
+    carve(ws, n, nnz, kMaxSweeps);
+    return ws.size();
+}
+
+extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
+                                uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels,
+                                int32_t* sweeps_done, void* ws_ptr, size_t ws_bytes, hipStream_t stream) {
+    if (n < 0 || nnz < 0 || n >= (int64_t(1) << 31) || nnz >= (int64_t(1) << 32))
+        return fail(GT_ERR_INVALID_ARG, "gt_reorder: n or nnz out of range");
+    if (iters < 0 || iters > kMaxSweeps) return fail(GT_ERR_INVALID_ARG, "gt_reorder: iters must be in [0, 1000]");
+    if (!rowptr || (nnz > 0 && !col) || (n > 0 && (!perm || !iperm)) || !ws_ptr)
+        return fail(GT_ERR_INVALID_ARG, "gt_reorder: null pointer");
+    if (ws_bytes < gt_reorder_workspace_size(n, nnz))
+        return fail(GT_ERR_WORKSPACE, "gt_reorder: workspace too small");
+    if (n == 0) {
+        if (sweeps_done) *sweeps_done = 0;
+        return GT_OK;
+    }
+    Ws ws(ws_ptr);
+    ReorderWs r = carve(ws, n, nnz, iters);
+    gt_status st = launch_validate_csr(n, nnz, rowptr, col, r.flags, stream);
+    if (st != GT_OK) return st;
+    st = read_validation(r.flags, stream);
+    if (st != GT_OK) return st;
+
+    const unsigned g = grid_for(n, 256, 8192);
+    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_med, r.is_big, r.big_cap);
+    GT_LAUNCH_CHECK("reorder_classify");
+    if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(r.is_big, n, r.pos_big, r.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
+    k_compact<<<g, 256, 0, stream>>>(n, r.is_med, r.is_big, r.pos_med, r.pos_big, r.cap_off, r.med_list,
+                                     r.big_list, r.big_off);
+    GT_LAUNCH_CHECK("reorder_compact");
+
+    if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
+    if ((st = fill_u32(r.flags, iters + 1, 0, stream)) != GT_OK) return st;
+    if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
+
+    const unsigned gw = grid_for(n, kBlock / kWave, 65536);
+    for (int t = 0; t < iters; ++t) {
+        const uint64_t key = seed + uint64_t(t + 1) * kGolden;
+        const int32_t* in = r.lab[t & 1];
+        int32_t* out = r.lab[(t + 1) & 1];
+        k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
+        GT_LAUNCH_CHECK("reorder_lp_wave");
+        k_lp_block<false><<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
+                                                       r.flags + t, r.flags + t + 1, nullptr, nullptr, nullptr);
+        GT_LAUNCH_CHECK("reorder_lp_lds");
+        k_lp_block<true><<<256, kBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in, out, key,
+                                                     r.flags + t, r.flags + t + 1, r.tab_keys, r.tab_cnts,
+                                                     r.big_off);
+        GT_LAUNCH_CHECK("reorder_lp_global");
+    }
+    const int32_t* final_lab = r.lab[iters & 1];
+    k_order_keys<<<g, 256, 0, stream>>>(n, final_lab, r.deg_off, r.sort_keys);
+    GT_LAUNCH_CHECK("reorder_keys");
+    if ((st = iota_u32(r.sort_vals, n, stream)) != GT_OK) return st;
+    if ((st = radix_sort_u64(r.sort_keys, r.sort_vals, n, 32 + bits_for(n), r.sort, stream)) != GT_OK) return st;
+    k_finish_order<<<g, 256, 0, stream>>>(n, r.sort_vals, final_lab, perm, iperm, labels);
+    GT_LAUNCH_CHECK("reorder_finish");
+    if (sweeps_done) {
+        uint32_t* host = new uint32_t[size_t(iters) + 1];
+        hipError_t e = hipMemcpyAsync(host, r.flags + 1, size_t(iters) * 4 + 4, hipMemcpyDeviceToHost, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        int done = 0;
+        for (int t = 0; t < iters; ++t)
+            if (host[t]) done = t + 1;
+        delete[] host;
+        if (e != hipSuccess) return hip_fail(e, "gt_reorder: read sweep flags");
+        *sweeps_done = done;
+    }
+    return GT_OK;
+}

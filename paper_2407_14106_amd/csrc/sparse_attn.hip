@@ -1,0 +1,715 @@
+// Neighbourhood softmax attention (§3.2, local topology-induced pattern) on the
+// remainder edges of a tile plan, forward and backward, plus the two entry
+// points that also run the dense-tile kernels (tile_attn.hip).
+//
+// Edge kernels ("rows" and "cols"): a wavefront serves 64 / (H * d/F) nodes at
+// once, each (node, head) owned by d/F lanes that hold F consecutive features
+// (64 bytes) of it.  The node's own vectors stay in registers while the lanes
+// walk its edge list two edges at a time, gathering the neighbours' 64-byte
+// slices; every gathered row is read as whole 64-byte pieces by neighbouring
+// lanes.  Scores use the paper's scaled dot product in the exp2 domain; the
+// forward keeps an online max / sum per (node, head), so nothing per edge is
+// ever written to memory.
+//
+// Nodes with more than GT_LONG_ROW remainder edges are left to the "long"
+// kernels: one workgroup per node, its edges dealt round-robin over the
+// workgroup's lane groups and the partial results merged in LDS.
+//
+// The backward never uses atomics: dQ is gathered per row over the CSR, dK and
+// dV per column over the remainder's transpose.
+#include "attn_common.h"
+#include "tile_attn.h"
+
+namespace gt {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+template <typename T, int D, int H>
+struct Lanes {
+    using C = EdgeCfg<T, D, H>;
+    int slot, h, part;
+    __device__ __forceinline__ explicit Lanes(int t) {
+        slot = t / C::G;
+        h = (t / C::L) % H;
+        part = t % C::L;
+    }
+    __device__ __forceinline__ int64_t off(int64_t node) const { return (node * H + h) * D + part * C::F; }
+};
+
+// F fp32 accumulators of one (node, head) slice.
+template <int F>
+struct Acc {
+    float v[F];
+    __device__ __forceinline__ Acc() {
+#pragma unroll
+        for (int i = 0; i < F; ++i) v[i] = 0.f;
+    }
+};
+
+// Online-softmax state of one (node, head) slice.
+template <int F>
+struct Online {
+    float m = kNegInf;  // running max, log2 domain
+    float l = 0.f;      // running sum of exp2(s - m)
+    float acc[F];       // running sum of exp2(s - m) * v
+    __device__ __forceinline__ Online() {
+#pragma unroll
+        for (int i = 0; i < F; ++i) acc[i] = 0.f;
+    }
+};
+
+template <typename T, int D, int H>
+__device__ __forceinline__ void load_fwd_partial(Online<EdgeCfg<T, D, H>::F>& st, const TilePartials& tp, int64_t node,
+                                                 int h, int64_t off) {
+    constexpr int F = EdgeCfg<T, D, H>::F;
+    st.m = tp.m[node * H + h];
+    st.l = tp.l[node * H + h];
+    const float4* a = reinterpret_cast<const float4*>(tp.acc + off);
+#pragma unroll
+    for (int i = 0; i < F / 4; ++i) {
+        float4 v = a[i];
+        st.acc[4 * i] = v.x;
+        st.acc[4 * i + 1] = v.y;
+        st.acc[4 * i + 2] = v.z;
+        st.acc[4 * i + 3] = v.w;
+    }
+}
+
+// One block of two edges for the forward state.
+template <typename T, int D, int H>
+__device__ __forceinline__ void fwd_step(Online<EdgeCfg<T, D, H>::F>& st, const Slice<T, EdgeCfg<T, D, H>::F>& q,
+                                         const T* __restrict__ K, const T* __restrict__ V, int64_t j0, int64_t j1,
+                                         bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2) {
+    using C = EdgeCfg<T, D, H>;
+    Slice<T, C::F> k0, k1, v0, v1;
+    k0.zero();
+    k1.zero();
+    v0.zero();
+    v1.zero();
+    if (ok0) {
+        k0.load(K + ln.off(j0));
+        v0.load(V + ln.off(j0));
+    }
+    if (ok1) {
+        k1.load(K + ln.off(j1));
+        v1.load(V + ln.off(j1));
+    }
+    float s0 = group_sum<C::L>(q.dot(k0)) * sl2;
+    float s1 = group_sum<C::L>(q.dot(k1)) * sl2;
+    s0 = ok0 ? s0 : kNegInf;
+    s1 = ok1 ? s1 : kNegInf;
+    const float mb = fmaxf(s0, s1);
+    const float mn = fmaxf(st.m, mb);
+    if (mn == kNegInf) return;
+    const float alpha = exp2f(st.m - mn);
+    const float p0 = exp2f(s0 - mn);
+    const float p1 = exp2f(s1 - mn);
+    st.l = st.l * alpha + p0 + p1;
+#pragma unroll
+    for (int i = 0; i < C::F; ++i) st.acc[i] = fmaf(p1, v1.f(i), fmaf(p0, v0.f(i), st.acc[i] * alpha));
+    st.m = mn;
+}
+
+// ------------------------------------------------------------------ forward
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t* __restrict__ rp,
+                                                       const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                       const T* __restrict__ K, const T* __restrict__ V, float sl2,
+                                                       T* __restrict__ O, float* __restrict__ LSE, TilePartials tp) {
+    using C = EdgeCfg<T, D, H>;
+    const Lanes<T, D, H> ln(lane_id());
+    const int64_t wave = int64_t(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
+    const int64_t i = wave * C::NPW + ln.slot;
+    const bool live = i < n;
+    int64_t a = 0;
+    int deg = 0;
+    if (live) {
+        a = rp[i];
+        const int64_t dg = rp[i + 1] - a;
+        deg = dg > GT_LONG_ROW ? -1 : int(dg);
+    }
+    const int dmax = wave_max(deg);
+    const int64_t off = live ? ln.off(i) : 0;
+    Slice<T, C::F> q;
+    q.zero();
+    if (live) q.load(Q + off);
+    Online<C::F> st;
+    if (live && deg >= 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
+    for (int t = 0; t < dmax; t += 2) {
+        const bool ok0 = t < deg, ok1 = t + 1 < deg;
+        const int64_t j0 = ok0 ? cl[a + t] : 0;
+        const int64_t j1 = ok1 ? cl[a + t + 1] : 0;
+        fwd_step<T, D, H>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2);
+    }
+    if (live && deg >= 0) {
+        const float inv = st.l > 0.f ? 1.f / st.l : 0.f;
+        store_slice<T, C::F>(O + off, st.acc, inv);
+        if (ln.part == 0) LSE[i * H + ln.h] = st.l > 0.f ? (st.m + __log2f(st.l)) * kLn2 : kNegInf;
+    }
+}
+
+// One workgroup per long row; lane groups take edges round-robin, then the
+// per-group states are merged through LDS.
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_fwd_long(const int32_t* __restrict__ list,
+                                                       const int64_t* __restrict__ rp,
+                                                       const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                       const T* __restrict__ K, const T* __restrict__ V, float sl2,
+                                                       T* __restrict__ O, float* __restrict__ LSE, TilePartials tp) {
+    using C = EdgeCfg<T, D, H>;
+    constexpr int S = kThreads / C::G;  // lane groups per workgroup
+    __shared__ float s_m[S][H];
+    __shared__ float s_l[S][H];
+    __shared__ float s_acc[S][H * D];
+    const Lanes<T, D, H> ln(threadIdx.x);
+    const int64_t i = list[blockIdx.x];
+    const int64_t a = rp[i];
+    const int deg = int(rp[i + 1] - a);
+    const int64_t off = ln.off(i);
+    Slice<T, C::F> q;
+    q.load(Q + off);
+    Online<C::F> st;
+    if (ln.slot == 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
+    for (int t = ln.slot; t < deg; t += 2 * S) {
+        const bool ok1 = t + S < deg;
+        const int64_t j0 = cl[a + t];
+        const int64_t j1 = ok1 ? cl[a + t + S] : 0;
+        fwd_step<T, D, H>(st, q, K, V, j0, j1, true, ok1, ln, sl2);
+    }
+    if (ln.part == 0) {
+        s_m[ln.slot][ln.h] = st.m;
+        s_l[ln.slot][ln.h] = st.l;
+    }
+#pragma unroll
+    for (int f = 0; f < C::F; ++f) s_acc[ln.slot][ln.h * D + ln.part * C::F + f] = st.acc[f];
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        const int h = idx / D;
+        float M = kNegInf;
+        for (int s = 0; s < S; ++s) M = fmaxf(M, s_m[s][h]);
+        float lsum = 0.f, o = 0.f;
+        if (M != kNegInf) {
+            for (int s = 0; s < S; ++s) {
+                const float w = exp2f(s_m[s][h] - M);
+                lsum += s_l[s][h] * w;
+                o += s_acc[s][idx] * w;
+            }
+        }
+        const float val = lsum > 0.f ? o / lsum : 0.f;
+        if (sizeof(T) == 2)
+            reinterpret_cast<uint16_t*>(O)[i * H * D + idx] = f32_to_bf16(val);
+        else
+            reinterpret_cast<float*>(O)[i * H * D + idx] = val;
+        if (idx % D == 0) LSE[i * H + h] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : kNegInf;
+    }
+}
+
+// ----------------------------------------------------------------- backward
+
+// Row pass: dQ_i = scale * sum_j dS_ij K_j
+template <typename T, int D, int H>
+__device__ __forceinline__ void dq_step(Acc<EdgeCfg<T, D, H>::F>& dq, const Slice<T, EdgeCfg<T, D, H>::F>& q,
+                                        const Slice<T, EdgeCfg<T, D, H>::F>& g, float lse2, float Di,
+                                        const T* __restrict__ K, const T* __restrict__ V, int64_t j0, int64_t j1,
+                                        bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2) {
+    using C = EdgeCfg<T, D, H>;
+    Slice<T, C::F> k0, k1, v0, v1;
+    k0.zero();
+    k1.zero();
+    v0.zero();
+    v1.zero();
+    if (ok0) {
+        k0.load(K + ln.off(j0));
+        v0.load(V + ln.off(j0));
+    }
+    if (ok1) {
+        k1.load(K + ln.off(j1));
+        v1.load(V + ln.off(j1));
+    }
+    const float s0 = group_sum<C::L>(q.dot(k0)) * sl2;
+    const float s1 = group_sum<C::L>(q.dot(k1)) * sl2;
+    const float dp0 = group_sum<C::L>(g.dot(v0));
+    const float dp1 = group_sum<C::L>(g.dot(v1));
+    const float p0 = ok0 ? exp2f(s0 - lse2) : 0.f;
+    const float p1 = ok1 ? exp2f(s1 - lse2) : 0.f;
+    const float ds0 = p0 * (dp0 - Di);
+    const float ds1 = p1 * (dp1 - Di);
+#pragma unroll
+    for (int f = 0; f < C::F; ++f) dq.v[f] = fmaf(ds1, k1.f(f), fmaf(ds0, k0.f(f), dq.v[f]));
+}
+
+template <int F>
+__device__ __forceinline__ void load_f32_slice(float (&dst)[F], const float* src) {
+    const float4* a = reinterpret_cast<const float4*>(src);
+#pragma unroll
+    for (int i = 0; i < F / 4; ++i) {
+        float4 v = a[i];
+        dst[4 * i] = v.x;
+        dst[4 * i + 1] = v.y;
+        dst[4 * i + 2] = v.z;
+        dst[4 * i + 3] = v.w;
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t* __restrict__ rp,
+                                                       const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                       const T* __restrict__ K, const T* __restrict__ V,
+                                                       const T* __restrict__ O, const T* __restrict__ dO,
+                                                       const float* __restrict__ LSE, float* __restrict__ Dv,
+                                                       float sl2, float scale, T* __restrict__ dQ, TilePartials tp) {
+    using C = EdgeCfg<T, D, H>;
+    const Lanes<T, D, H> ln(lane_id());
+    const int64_t wave = int64_t(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
+    const int64_t i = wave * C::NPW + ln.slot;
+    const bool live = i < n;
+    int64_t a = 0;
+    int deg = 0;
+    if (live) {
+        a = rp[i];
+        const int64_t dg = rp[i + 1] - a;
+        deg = dg > GT_LONG_ROW ? -1 : int(dg);
+    }
+    const int dmax = wave_max(deg);
+    const int64_t off = live ? ln.off(i) : 0;
+    Slice<T, C::F> q, g;
+    q.zero();
+    g.zero();
+    float lse2 = 0.f, Di = 0.f;
+    if (live) {
+        Slice<T, C::F> o;
+        o.load(O + off);
+        q.load(Q + off);
+        g.load(dO + off);
+        lse2 = LSE[i * H + ln.h] * kLog2e;
+        Di = group_sum<C::L>(o.dot(g));
+        if (deg >= 0 && ln.part == 0) Dv[i * H + ln.h] = Di;
+    }
+    Acc<C::F> dq;
+    if (live && deg >= 0 && tp.has_row(i)) load_f32_slice<C::F>(dq.v, tp.acc + off);
+    for (int t = 0; t < dmax; t += 2) {
+        const bool ok0 = t < deg, ok1 = t + 1 < deg;
+        const int64_t j0 = ok0 ? cl[a + t] : 0;
+        const int64_t j1 = ok1 ? cl[a + t + 1] : 0;
+        dq_step<T, D, H>(dq, q, g, lse2, Di, K, V, j0, j1, ok0, ok1, ln, sl2);
+    }
+    if (live && deg >= 0) store_slice<T, C::F>(dQ + off, dq.v, scale);
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_rows_long(const int32_t* __restrict__ list,
+                                                            const int64_t* __restrict__ rp,
+                                                            const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                            const T* __restrict__ K, const T* __restrict__ V,
+                                                            const T* __restrict__ O, const T* __restrict__ dO,
+                                                            const float* __restrict__ LSE, float* __restrict__ Dv,
+                                                            float sl2, float scale, T* __restrict__ dQ,
+                                                            TilePartials tp) {
+    using C = EdgeCfg<T, D, H>;
+    constexpr int S = kThreads / C::G;
+    __shared__ float s_acc[S][H * D];
+    const Lanes<T, D, H> ln(threadIdx.x);
+    const int64_t i = list[blockIdx.x];
+    const int64_t a = rp[i];
+    const int deg = int(rp[i + 1] - a);
+    const int64_t off = ln.off(i);
+    Slice<T, C::F> q, g, o;
+    q.load(Q + off);
+    g.load(dO + off);
+    o.load(O + off);
+    const float lse2 = LSE[i * H + ln.h] * kLog2e;
+    const float Di = group_sum<C::L>(o.dot(g));
+    if (ln.slot == 0 && ln.part == 0) Dv[i * H + ln.h] = Di;
+    Acc<C::F> dq;
+    if (ln.slot == 0 && tp.has_row(i)) load_f32_slice<C::F>(dq.v, tp.acc + off);
+    for (int t = ln.slot; t < deg; t += 2 * S) {
+        const bool ok1 = t + S < deg;
+        const int64_t j0 = cl[a + t];
+        const int64_t j1 = ok1 ? cl[a + t + S] : 0;
+        dq_step<T, D, H>(dq, q, g, lse2, Di, K, V, j0, j1, true, ok1, ln, sl2);
+    }
+#pragma unroll
+    for (int f = 0; f < C::F; ++f) s_acc[ln.slot][ln.h * D + ln.part * C::F + f] = dq.v[f];
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        float acc = 0.f;
+        for (int s = 0; s < S; ++s) acc += s_acc[s][idx];
+        acc *= scale;
+        if (sizeof(T) == 2)
+            reinterpret_cast<uint16_t*>(dQ)[i * H * D + idx] = f32_to_bf16(acc);
+        else
+            reinterpret_cast<float*>(dQ)[i * H * D + idx] = acc;
+    }
+}
+
+// Column pass: dK_j = scale * sum_i dS_ij Q_i, dV_j = sum_i P_ij dO_i over the in-edges of j.
+template <typename T, int D, int H>
+__device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeCfg<T, D, H>::F>& dv,
+                                         const Slice<T, EdgeCfg<T, D, H>::F>& k,
+                                         const Slice<T, EdgeCfg<T, D, H>::F>& v, const T* __restrict__ Q,
+                                         const T* __restrict__ dO, const float* __restrict__ LSE,
+                                         const float* __restrict__ Dv, int64_t i0, int64_t i1, bool ok0, bool ok1,
+                                         const Lanes<T, D, H>& ln, float sl2) {
+    using C = EdgeCfg<T, D, H>;
+    Slice<T, C::F> q0, q1, g0, g1;
+    q0.zero();
+    q1.zero();
+    g0.zero();
+    g1.zero();
+    float l0 = 0.f, l1 = 0.f, D0 = 0.f, D1 = 0.f;
+    if (ok0) {
+        q0.load(Q + ln.off(i0));
+        g0.load(dO + ln.off(i0));
+        l0 = LSE[i0 * H + ln.h] * kLog2e;
+        D0 = Dv[i0 * H + ln.h];
+    }
+    if (ok1) {
+        q1.load(Q + ln.off(i1));
+        g1.load(dO + ln.off(i1));
+        l1 = LSE[i1 * H + ln.h] * kLog2e;
+        D1 = Dv[i1 * H + ln.h];
+    }
+    const float s0 = group_sum<C::L>(q0.dot(k)) * sl2;
+    const float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
+    const float dp0 = group_sum<C::L>(g0.dot(v));
+    const float dp1 = group_sum<C::L>(g1.dot(v));
+    const float p0 = ok0 ? exp2f(s0 - l0) : 0.f;
+    const float p1 = ok1 ? exp2f(s1 - l1) : 0.f;
+    const float ds0 = p0 * (dp0 - D0);
+    const float ds1 = p1 * (dp1 - D1);
+#pragma unroll
+    for (int f = 0; f < C::F; ++f) {
+        dk.v[f] = fmaf(ds1, q1.f(f), fmaf(ds0, q0.f(f), dk.v[f]));
+        dv.v[f] = fmaf(p1, g1.f(f), fmaf(p0, g0.f(f), dv.v[f]));
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t* __restrict__ cp,
+                                                       const int32_t* __restrict__ rw, const T* __restrict__ Q,
+                                                       const T* __restrict__ K, const T* __restrict__ V,
+                                                       const T* __restrict__ dO, const float* __restrict__ LSE,
+                                                       const float* __restrict__ Dv, float sl2, float scale,
+                                                       T* __restrict__ dK, T* __restrict__ dV, TilePartials tpk,
+                                                       TilePartials tpv) {
+    using C = EdgeCfg<T, D, H>;
+    const Lanes<T, D, H> ln(lane_id());
+    const int64_t wave = int64_t(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
+    const int64_t j = wave * C::NPW + ln.slot;
+    const bool live = j < n;
+    int64_t a = 0;
+    int deg = 0;
+    if (live) {
+        a = cp[j];
+        const int64_t dg = cp[j + 1] - a;
+        deg = dg > GT_LONG_ROW ? -1 : int(dg);
+    }
+    const int dmax = wave_max(deg);
+    const int64_t off = live ? ln.off(j) : 0;
+    Slice<T, C::F> k, v;
+    k.zero();
+    v.zero();
+    if (live) {
+        k.load(K + off);
+        v.load(V + off);
+    }
+    Acc<C::F> dk, dv;
+    if (live && deg >= 0 && tpk.has_col(j)) {
+        load_f32_slice<C::F>(dk.v, tpk.acc + off);
+        load_f32_slice<C::F>(dv.v, tpv.acc + off);
+    }
+    for (int t = 0; t < dmax; t += 2) {
+        const bool ok0 = t < deg, ok1 = t + 1 < deg;
+        const int64_t i0 = ok0 ? rw[a + t] : 0;
+        const int64_t i1 = ok1 ? rw[a + t + 1] : 0;
+        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, ok0, ok1, ln, sl2);
+    }
+    if (live && deg >= 0) {
+        store_slice<T, C::F>(dK + off, dk.v, scale);
+        store_slice<T, C::F>(dV + off, dv.v, 1.f);
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __restrict__ list,
+                                                            const int64_t* __restrict__ cp,
+                                                            const int32_t* __restrict__ rw, const T* __restrict__ Q,
+                                                            const T* __restrict__ K, const T* __restrict__ V,
+                                                            const T* __restrict__ dO, const float* __restrict__ LSE,
+                                                            const float* __restrict__ Dv, float sl2, float scale,
+                                                            T* __restrict__ dK, T* __restrict__ dV, TilePartials tpk,
+                                                            TilePartials tpv) {
+    using C = EdgeCfg<T, D, H>;
+    constexpr int S = kThreads / C::G;
+    __shared__ float s_k[S][H * D];
+    __shared__ float s_v[S][H * D];
+    const Lanes<T, D, H> ln(threadIdx.x);
+    const int64_t j = list[blockIdx.x];
+    const int64_t a = cp[j];
+    const int deg = int(cp[j + 1] - a);
+    const int64_t off = ln.off(j);
+    Slice<T, C::F> k, v;
+    k.load(K + off);
+    v.load(V + off);
+    Acc<C::F> dk, dv;
+    if (ln.slot == 0 && tpk.has_col(j)) {
+        load_f32_slice<C::F>(dk.v, tpk.acc + off);
+        load_f32_slice<C::F>(dv.v, tpv.acc + off);
+    }
+    for (int t = ln.slot; t < deg; t += 2 * S) {
+        const bool ok1 = t + S < deg;
+        const int64_t i0 = rw[a + t];
+        const int64_t i1 = ok1 ? rw[a + t + S] : 0;
+        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, true, ok1, ln, sl2);
+    }
+#pragma unroll
+    for (int f = 0; f < C::F; ++f) {
+        s_k[ln.slot][ln.h * D + ln.part * C::F + f] = dk.v[f];
+        s_v[ln.slot][ln.h * D + ln.part * C::F + f] = dv.v[f];
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        float ak = 0.f, av = 0.f;
+        for (int s = 0; s < S; ++s) {
+            ak += s_k[s][idx];
+            av += s_v[s][idx];
+        }
+        ak *= scale;
+        if (sizeof(T) == 2) {
+            reinterpret_cast<uint16_t*>(dK)[j * H * D + idx] = f32_to_bf16(ak);
+            reinterpret_cast<uint16_t*>(dV)[j * H * D + idx] = f32_to_bf16(av);
+        } else {
+            reinterpret_cast<float*>(dK)[j * H * D + idx] = ak;
+            reinterpret_cast<float*>(dV)[j * H * D + idx] = av;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- launchers
+
+struct FwdWs {
+    TilePartials tp;
+};
+
+template <typename T, int D, int H>
+gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V, float scale, void* O, float* LSE,
+                  void* ws_ptr, hipStream_t s) {
+    using C = EdgeCfg<T, D, H>;
+    const int64_t n = p->n;
+    if (n == 0) return GT_OK;
+    Ws ws(ws_ptr);
+    ws.take<char>(256);
+    TilePartials tp = tile_partials_fwd(ws, p, H, D);
+    const float sl2 = scale * kLog2e;
+    gt_status st;
+    if (p->n_dense > 0) {
+        if ((st = tile_fwd<T, D, H>(p, static_cast<const T*>(Q), static_cast<const T*>(K),
+                                    static_cast<const T*>(V), sl2, tp, s)) != GT_OK)
+            return st;
+    } else {
+        tp = TilePartials{};
+    }
+    const int64_t waves = cdiv(n, C::NPW);
+    k_fwd_rows<T, D, H><<<unsigned(cdiv(waves, kThreads / kWave)), kThreads, 0, s>>>(
+        n, p->sp_rowptr, p->sp_col, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
+        sl2, static_cast<T*>(O), LSE, tp);
+    GT_LAUNCH_CHECK("sparse_fwd_rows");
+    if (p->n_long_rows > 0) {
+        k_fwd_long<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
+            p->long_rows, p->sp_rowptr, p->sp_col, static_cast<const T*>(Q), static_cast<const T*>(K),
+            static_cast<const T*>(V), sl2, static_cast<T*>(O), LSE, tp);
+        GT_LAUNCH_CHECK("sparse_fwd_long");
+    }
+    return GT_OK;
+}
+
+template <typename T, int D, int H>
+gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* O,
+                       const void* dO, const float* LSE, float scale, void* dQ, float* Dv, void* ws_ptr,
+                       hipStream_t s) {
+    using C = EdgeCfg<T, D, H>;
+    const int64_t n = p->n;
+    if (n == 0) return GT_OK;
+    Ws ws(ws_ptr);
+    ws.take<char>(256);
+    TileBwdPartials tb = tile_partials_bwd(ws, p, H, D, true, false);
+    const float sl2 = scale * kLog2e;
+    const T *q = static_cast<const T*>(Q), *k = static_cast<const T*>(K), *v = static_cast<const T*>(V);
+    const T *o = static_cast<const T*>(O), *g = static_cast<const T*>(dO);
+    gt_status st;
+    if (p->n_dense > 0) {
+        if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, o, g, LSE, Dv, sl2, tb.dq, s)) != GT_OK) return st;
+    }
+    const unsigned grid = unsigned(cdiv(cdiv(n, C::NPW), kThreads / kWave));
+    k_bwd_rows<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, q, k, v, o, g, LSE, Dv, sl2, scale,
+                                                  static_cast<T*>(dQ), tb.dq);
+    GT_LAUNCH_CHECK("sparse_bwd_rows");
+    if (p->n_long_rows > 0) {
+        k_bwd_rows_long<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
+            p->long_rows, p->sp_rowptr, p->sp_col, q, k, v, o, g, LSE, Dv, sl2, scale, static_cast<T*>(dQ), tb.dq);
+        GT_LAUNCH_CHECK("sparse_bwd_rows_long");
+    }
+    return GT_OK;
+}
+
+template <typename T, int D, int H>
+gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
+                       const float* LSE, const float* Dv, float scale, void* dK, void* dV, void* ws_ptr,
+                       hipStream_t s) {
+    using C = EdgeCfg<T, D, H>;
+    const int64_t n = p->n;
+    if (n == 0) return GT_OK;
+    Ws ws(ws_ptr);
+    ws.take<char>(256);
+    TileBwdPartials tb = tile_partials_bwd(ws, p, H, D, false, true);
+    const float sl2 = scale * kLog2e;
+    const T *q = static_cast<const T*>(Q), *k = static_cast<const T*>(K), *v = static_cast<const T*>(V);
+    const T* g = static_cast<const T*>(dO);
+    gt_status st;
+    if (p->n_dense > 0) {
+        if ((st = tile_bwd_dkdv<T, D, H>(p, q, k, v, g, LSE, Dv, sl2, tb.dk, tb.dv, s)) != GT_OK) return st;
+    }
+    const unsigned grid = unsigned(cdiv(cdiv(n, C::NPW), kThreads / kWave));
+    k_bwd_cols<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2, scale,
+                                                  static_cast<T*>(dK), static_cast<T*>(dV), tb.dk, tb.dv);
+    GT_LAUNCH_CHECK("sparse_bwd_cols");
+    if (p->n_long_cols > 0) {
+        k_bwd_cols_long<T, D, H><<<unsigned(p->n_long_cols), kThreads, 0, s>>>(
+            p->long_cols, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2, scale, static_cast<T*>(dK),
+            static_cast<T*>(dV), tb.dk, tb.dv);
+        GT_LAUNCH_CHECK("sparse_bwd_cols_long");
+    }
+    return GT_OK;
+}
+
+template <typename T, int D, int H>
+gt_status run_bwd(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                  const float* LSE, float scale, void* dQ, void* dK, void* dV, void* ws_ptr, hipStream_t s) {
+    if (p->n == 0) return GT_OK;
+    Ws ws(ws_ptr);
+    float* Dv = ws.take<float>(size_t(p->n) * H);
+    char* rest = ws.take<char>(1);
+    gt_status st = run_bwd_rows<T, D, H>(p, Q, K, V, O, dO, LSE, scale, dQ, Dv, rest, s);
+    if (st != GT_OK) return st;
+    return run_bwd_cols<T, D, H>(p, Q, K, V, dO, LSE, Dv, scale, dK, dV, rest, s);
+}
+
+bool supported(int32_t H, int32_t d, gt_dtype dt) {
+    return (d == 32 || d == 64) && (H == 1 || H == 2 || H == 4 || H == 8 || H == 16) && (dt == GT_F32 || dt == GT_BF16);
+}
+
+gt_status check_plan(const char* who, const gt_tiles* p) {
+    if (!p) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": null plan");
+    if (p->n < 0 || p->n >= (int64_t(1) << 31) || (p->T != 64 && p->T != 128))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": plan not built (n or T invalid)");
+    if (p->n > 0 && (!p->sp_rowptr || !p->sp_colptr || !p->tile_rowptr || !p->tileT_ptr))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": plan arrays missing");
+    if ((p->nnz_sparse > 0 && (!p->sp_col || !p->sp_row)) || (p->n_long_rows > 0 && !p->long_rows) ||
+        (p->n_long_cols > 0 && !p->long_cols) ||
+        (p->n_dense > 0 && (!p->tile_col || !p->tile_mask || !p->tileT_idx)))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": plan arrays missing");
+    return GT_OK;
+}
+
+size_t fwd_ws(const gt_tiles* p, int32_t H, int32_t d) {
+    Ws ws(nullptr);
+    ws.take<char>(256);
+    tile_partials_fwd(ws, p, H, d);
+    return ws.size();
+}
+size_t bwd_part_ws(const gt_tiles* p, int32_t H, int32_t d, bool rows, bool cols) {
+    Ws ws(nullptr);
+    ws.take<char>(256);
+    tile_partials_bwd(ws, p, H, d, rows, cols);
+    return ws.size();
+}
+size_t bwd_ws(const gt_tiles* p, int32_t H, int32_t d) {
+    Ws ws(nullptr);
+    ws.take<float>(size_t(p->n > 0 ? p->n : 1) * H);
+    const size_t a = bwd_part_ws(p, H, d, true, false), b = bwd_part_ws(p, H, d, false, true);
+    ws.take<char>(a > b ? a : b);
+    return ws.size();
+}
+
+}  // namespace
+}  // namespace gt
+
+using namespace gt;
+
+extern "C" size_t gt_sparse_attn_fwd_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype) {
+    if (!plan || !supported(H, d, dtype)) return 0;
+    return fwd_ws(plan, H, d);
+}
+
+extern "C" gt_status gt_sparse_attn_fwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
+                                        const void* K, const void* V, float scale, void* O, float* LSE, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+    gt_status st = check_plan("gt_sparse_attn_fwd", plan);
+    if (st != GT_OK) return st;
+    if (!supported(H, d, dtype)) return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_fwd: unsupported (H, d, dtype)");
+    if (plan->n > 0 && (!Q || !K || !V || !O || !LSE || !ws))
+        return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_fwd: null pointer");
+    if (ws_bytes < fwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_fwd: workspace too small");
+    return GT_DISPATCH_ATTN(dtype, d, H, run_fwd, plan, Q, K, V, scale, O, LSE, ws, stream);
+}
+
+extern "C" size_t gt_sparse_attn_bwd_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype) {
+    if (!plan || !supported(H, d, dtype)) return 0;
+    return bwd_ws(plan, H, d);
+}
+
+extern "C" size_t gt_sparse_attn_bwd_rows_workspace_size(const gt_tiles* plan, int32_t H, int32_t d,
+                                                         gt_dtype dtype) {
+    if (!plan || !supported(H, d, dtype)) return 0;
+    return bwd_part_ws(plan, H, d, true, false);
+}
+
+extern "C" gt_status gt_sparse_attn_bwd_rows(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype,
+                                             const void* Q, const void* K, const void* V, const void* O,
+                                             const void* dO, const float* LSE, float scale, void* dQ, float* Dstat,
+                                             void* ws, size_t ws_bytes, hipStream_t stream) {
+    gt_status st = check_plan("gt_sparse_attn_bwd_rows", plan);
+    if (st != GT_OK) return st;
+    if (!supported(H, d, dtype)) return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_bwd_rows: unsupported (H, d, dtype)");
+    if (plan->n > 0 && (!Q || !K || !V || !O || !dO || !LSE || !dQ || !Dstat || !ws))
+        return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_rows: null pointer");
+    if (ws_bytes < bwd_part_ws(plan, H, d, true, false))
+        return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_rows: workspace too small");
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_rows, plan, Q, K, V, O, dO, LSE, scale, dQ, Dstat, ws, stream);
+}
+
+extern "C" size_t gt_sparse_attn_bwd_cols_workspace_size(const gt_tiles* plan, int32_t H, int32_t d,
+                                                         gt_dtype dtype) {
+    if (!plan || !supported(H, d, dtype)) return 0;
+    return bwd_part_ws(plan, H, d, false, true);
+}
+
+extern "C" gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype,
+                                             const void* Q, const void* K, const void* V, const void* dO,
+                                             const float* LSE, const float* Dstat, float scale, void* dK, void* dV,
+                                             void* ws, size_t ws_bytes, hipStream_t stream) {
+    gt_status st = check_plan("gt_sparse_attn_bwd_cols", plan);
+    if (st != GT_OK) return st;
+    if (!supported(H, d, dtype)) return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_bwd_cols: unsupported (H, d, dtype)");
+    if (plan->n > 0 && (!Q || !K || !V || !dO || !LSE || !Dstat || !dK || !dV || !ws))
+        return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_cols: null pointer");
+    if (ws_bytes < bwd_part_ws(plan, H, d, false, true))
+        return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_cols: workspace too small");
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_cols, plan, Q, K, V, dO, LSE, Dstat, scale, dK, dV, ws, stream);
+}
+
+extern "C" gt_status gt_sparse_attn_bwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
+                                        const void* K, const void* V, const void* O, const void* dO, const float* LSE,
+                                        float scale, void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes,
+                                        hipStream_t stream) {
+    gt_status st = check_plan("gt_sparse_attn_bwd", plan);
+    if (st != GT_OK) return st;
+    if (!supported(H, d, dtype)) return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_bwd: unsupported (H, d, dtype)");
+    if (plan->n > 0 && (!Q || !K || !V || !O || !dO || !LSE || !dQ || !dK || !dV || !ws))
+        return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd: null pointer");
+    if (ws_bytes < bwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd: workspace too small");
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, O, dO, LSE, scale, dQ, dK, dV, ws, stream);
+}

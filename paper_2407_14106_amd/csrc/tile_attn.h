@@ -1,0 +1,82 @@
+// Dense-tile attention (§3.4: tiles of the reordered adjacency dense enough to
+// be computed whole on the matrix cores) and the partial results it hands to
+// the edge kernels, which finish every row and column.
+#pragma once
+
+#include "attn_common.h"
+
+namespace gt {
+
+// Per-(node, head) partial state left by the dense tiles of a tile row (or
+// tile column).  `ptr` is tile_rowptr (or tileT_ptr): a node has a partial iff
+// its tile row (column) holds at least one dense tile.
+struct TilePartials {
+    const int64_t* ptr = nullptr;
+    int tshift = 0;
+    float* m = nullptr;    // [n, H] running max (log2 domain), forward only
+    float* l = nullptr;    // [n, H] running sum, forward only
+    float* acc = nullptr;  // [n, H, d] unnormalised output / gradient sums
+    __device__ __forceinline__ bool has(int64_t node) const {
+        if (!ptr) return false;
+        const int64_t I = node >> tshift;
+        return ptr[I + 1] > ptr[I];
+    }
+    __device__ __forceinline__ bool has_row(int64_t node) const { return has(node); }
+    __device__ __forceinline__ bool has_col(int64_t node) const { return has(node); }
+};
+
+struct TileBwdPartials {
+    TilePartials dq, dk, dv;
+};
+
+inline int tile_shift(int T) { return T == 128 ? 7 : 6; }
+
+// Carve the partial buffers out of the workspace (nothing when no tile is dense).
+inline TilePartials tile_partials_fwd(Ws& ws, const gt_tiles* p, int H, int D) {
+    TilePartials t;
+    if (p->n_dense <= 0 || p->n <= 0) return t;
+    t.ptr = p->tile_rowptr;
+    t.tshift = tile_shift(p->T);
+    t.m = ws.take<float>(size_t(p->n) * H);
+    t.l = ws.take<float>(size_t(p->n) * H);
+    t.acc = ws.take<float>(size_t(p->n) * H * D);
+    return t;
+}
+
+inline TileBwdPartials tile_partials_bwd(Ws& ws, const gt_tiles* p, int H, int D, bool rows, bool cols) {
+    TileBwdPartials b;
+    if (p->n_dense <= 0 || p->n <= 0) return b;
+    if (rows) {
+        b.dq.ptr = p->tile_rowptr;
+        b.dq.tshift = tile_shift(p->T);
+        b.dq.acc = ws.take<float>(size_t(p->n) * H * D);
+    }
+    if (cols) {
+        b.dk.ptr = b.dv.ptr = p->tileT_ptr;
+        b.dk.tshift = b.dv.tshift = tile_shift(p->T);
+        b.dk.acc = ws.take<float>(size_t(p->n) * H * D);
+        b.dv.acc = ws.take<float>(size_t(p->n) * H * D);
+    }
+    return b;
+}
+
+// Forward over the dense tiles: for every node of a tile row with dense
+// tiles, writes (m, l, acc) of the online softmax over its dense-tile edges.
+template <typename T, int D, int H>
+gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float sl2, TilePartials tp,
+                   hipStream_t s);
+
+// Backward over the dense tiles, row-owned: for every node of a tile row with
+// dense tiles, writes D = <dO, O> into Dv and the dq sum over its dense-tile
+// edges (unscaled by `scale`; the edge kernels apply it when they finish).
+template <typename T, int D, int H>
+gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* O, const T* dO,
+                      const float* LSE, float* Dv, float sl2, TilePartials dq, hipStream_t s);
+
+// Backward over the dense tiles, column-owned: dk (unscaled) and dv sums over
+// the dense-tile edges of every node of a tile column with dense tiles.
+template <typename T, int D, int H>
+gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
+                        const float* Dv, float sl2, TilePartials dk, TilePartials dv, hipStream_t s);
+
+}  // namespace gt

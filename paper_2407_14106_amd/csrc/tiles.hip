@@ -1,0 +1,336 @@
+// Dense/sparse tile plan (§3.4, cluster sparsity and the transfer threshold),
+// read as an exact execution plan over T x T tiles of the reordered adjacency.
+//
+// One workgroup per tile row I keeps a direct-indexed count per tile column J
+// in LDS (R <= 16384 columns: 64 KiB), so counting touches only the edges of
+// the tile row.  The same kernel, run a second time with the output offsets
+// known, writes the (I, J)-sorted dense tile list, the tile bit masks and the
+// remainder CSR.  The remainder's transpose and the column-grouped tile list
+// come from stable radix sorts, so every output is deterministic.
+#include "prim.h"
+
+namespace gt {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxR = 16384;
+constexpr uint32_t kDense = 0x80000000u;
+
+__device__ __forceinline__ int64_t block_exscan_i64(int64_t v, int64_t* s, int64_t* total) {
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    int64_t x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        int64_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s[w] = x;
+    __syncthreads();
+    int64_t before = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kThreads / kWave; ++i) {
+        const int64_t t = s[i];
+        if (i < w) before += t;
+        tot += t;
+    }
+    __syncthreads();
+    *total = tot;
+    return before + x - v;
+}
+
+// kFill = false: dense tiles per tile row, remainder degree per row.
+// kFill = true: the plan arrays (offsets from the count pass).
+template <bool kFill>
+__global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* rowptr, const int32_t* col, int T,
+                                                    int R, uint32_t tau_ppm, int32_t* dense_per_tilerow,
+                                                    int32_t* sp_deg, const int64_t* tile_rowptr, int32_t* tile_col,
+                                                    int32_t* tile_nnz, uint32_t* tile_mask,
+                                                    const int64_t* sp_rowptr, int32_t* sp_col,
+                                                    uint32_t* sp_colkey, uint32_t* sp_rowval, uint32_t* sp_colcnt) {
+    __shared__ uint32_t s_cnt[kMaxR];
+    __shared__ int64_t s_red[kThreads / kWave];
+    const int I = blockIdx.x;
+    const int64_t r0 = int64_t(I) * T;
+    const int64_t r1 = r0 + T < n ? r0 + T : n;
+    const int64_t rows = r1 - r0;
+    for (int J = threadIdx.x; J < R; J += kThreads) s_cnt[J] = 0;
+    __syncthreads();
+    const int64_t e0 = rowptr[r0], e1 = rowptr[r1];
+    for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) atomicAdd(&s_cnt[col[e] / T], 1u);
+    __syncthreads();
+    // classify; keep the count in the low bits
+    int64_t mine = 0;
+    const int chunk = (R + kThreads - 1) / kThreads;
+    const int j0 = threadIdx.x * chunk;
+    const int j1 = j0 + chunk < R ? j0 + chunk : R;
+    for (int J = j0; J < j1; ++J) {
+        const uint32_t c = s_cnt[J];
+        const int64_t wcols = n - int64_t(J) * T < T ? n - int64_t(J) * T : T;
+        const uint64_t area = uint64_t(rows) * uint64_t(wcols);
+        if (c >= 1 && uint64_t(c) * 1000000ull >= uint64_t(tau_ppm) * area) {
+            s_cnt[J] = c | kDense;
+            ++mine;
+        }
+    }
+    int64_t total;
+    const int64_t before = block_exscan_i64(mine, s_red, &total);
+    if (!kFill) {
+        if (threadIdx.x == 0) dense_per_tilerow[I] = int32_t(total);
+    } else {
+        const int64_t base = tile_rowptr[I];
+        int64_t k = before;
+        for (int J = j0; J < j1; ++J) {
+            const uint32_t f = s_cnt[J];
+            if (f & kDense) {
+                tile_col[base + k] = J;
+                tile_nnz[base + k] = int32_t(f & ~kDense);
+                s_cnt[J] = kDense | uint32_t(k);
+                ++k;
+            }
+        }
+    }
+    __syncthreads();
+    // per row: remainder degree (count) or remainder edges and mask bits (fill)
+    const int lane = lane_id();
+    const uint64_t lt = lanemask_lt();
+    const int wpr = T / 32;  // mask words per tile row
+    for (int64_t rl = threadIdx.x / kWave; rl < rows; rl += kThreads / kWave) {
+        const int64_t i = r0 + rl;
+        const int64_t a = rowptr[i], b = rowptr[i + 1];
+        int64_t sp = 0;
+        for (int64_t eb = a; eb < b; eb += kWave) {
+            const int64_t e = eb + lane;
+            const bool valid = e < b;
+            const int c = valid ? col[e] : 0;
+            const int J = c / T;
+            const uint32_t f = valid ? s_cnt[J] : 0u;
+            const bool dense = valid && (f & kDense);
+            const bool sparse = valid && !dense;
+            const uint64_t sb = ballot(sparse);
+            if (kFill) {
+                if (dense) {
+                    const int64_t k = tile_rowptr[I] + int64_t(f & ~kDense);
+                    const int cl = c - J * T;
+                    const int64_t word = k * int64_t(T) * wpr + rl * wpr + cl / 32;
+                    atomicOr(&tile_mask[word], 1u << (cl & 31));
+                }
+                if (sparse) {
+                    const int64_t pos = sp_rowptr[i] + sp + __popcll(sb & lt);
+                    sp_col[pos] = c;
+                    sp_colkey[pos] = uint32_t(c);
+                    sp_rowval[pos] = uint32_t(i);
+                }
+            }
+            if (!kFill && sparse) atomicAdd(&sp_colcnt[c], 1u);
+            sp += __popcll(sb);
+        }
+        if (!kFill && lane == 0) sp_deg[i] = int32_t(sp);
+    }
+}
+
+// flags[i] = value[i] > threshold
+template <typename V>
+__global__ void k_over(int64_t m, const V* value, int64_t threshold, int32_t* flags) {
+    for (int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; e < m; e += int64_t(gridDim.x) * blockDim.x)
+        flags[e] = int64_t(value[e]) > threshold ? 1 : 0;
+}
+
+__global__ void k_compact_list(int64_t m, const int32_t* flags, const int64_t* pos, int32_t* list) {
+    for (int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; e < m; e += int64_t(gridDim.x) * blockDim.x)
+        if (flags[e]) list[pos[e]] = int32_t(e);
+}
+
+__global__ void k_u32_to_i32(int64_t m, const uint32_t* src, int32_t* dst) {
+    for (int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; e < m; e += int64_t(gridDim.x) * blockDim.x)
+        dst[e] = int32_t(src[e]);
+}
+
+struct TilesWs {
+    uint32_t* flags;
+    int32_t* dense_per_tilerow;
+    int32_t* sp_deg;
+    int64_t* tmp_tile_rowptr;
+    int64_t* tmp_sp_rowptr;
+    uint32_t* keys;     // remainder column (then tile column) keys
+    uint32_t* vals;     // remainder row (then tile index) values
+    uint32_t* counts;   // per column / per tile column
+    uint32_t* colcnt;   // remainder in-degree per column
+    int32_t* long_row_flag;
+    int32_t* long_col_flag;
+    int64_t* long_row_pos;
+    int64_t* long_col_pos;
+    ScanTmp scan;
+    SortTmp sort;
+};
+
+TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
+    TilesWs t;
+    const int64_t n1 = n > 0 ? n : 1, e1 = nnz > 0 ? nnz : 1;
+    const int64_t R = cdiv(n1, T > 0 ? T : 1);
+    t.flags = ws.take<uint32_t>(1);
+    t.dense_per_tilerow = ws.take<int32_t>(R);
+    t.sp_deg = ws.take<int32_t>(n1);
+    t.tmp_tile_rowptr = ws.take<int64_t>(R + 1);
+    t.tmp_sp_rowptr = ws.take<int64_t>(n1 + 1);
+    t.keys = ws.take<uint32_t>(e1);
+    t.vals = ws.take<uint32_t>(e1);
+    t.counts = ws.take<uint32_t>(n1 + 1);
+    t.colcnt = ws.take<uint32_t>(n1);
+    t.long_row_flag = ws.take<int32_t>(n1);
+    t.long_col_flag = ws.take<int32_t>(n1);
+    t.long_row_pos = ws.take<int64_t>(n1 + 1);
+    t.long_col_pos = ws.take<int64_t>(n1 + 1);
+    t.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1)));
+    t.sort = sort_tmp(ws, e1, 4, true);
+    return t;
+}
+
+gt_status check_common(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
+                       void* ws_ptr, size_t ws_bytes) {
+    if (n < 0 || nnz < 0 || n >= (int64_t(1) << 31) || nnz >= (int64_t(1) << 32))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": n or nnz out of range");
+    if (T != 64 && T != 128) return fail(GT_ERR_UNSUPPORTED, std::string(who) + ": T must be 64 or 128");
+    if (cdiv(n, T) > kMaxR)
+        return fail(GT_ERR_UNSUPPORTED, std::string(who) + ": more than 16384 tile rows (n > 16384 * T)");
+    if (!rowptr || (nnz > 0 && !col) || !ws_ptr) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": null pointer");
+    if (ws_bytes < gt_tiles_workspace_size(n, nnz, T))
+        return fail(GT_ERR_WORKSPACE, std::string(who) + ": workspace too small");
+    return GT_OK;
+}
+
+// Count pass shared by gt_tiles_count and gt_build_tiles: dense tiles per tile
+// row (scanned into tile_rowptr), remainder degrees (scanned into sp_rowptr)
+// and the long-row / long-column flags and positions.
+gt_status count_pass(int64_t n, const int64_t* rowptr, const int32_t* col, int32_t T, uint32_t tau_ppm,
+                     TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, hipStream_t stream) {
+    gt_status st;
+    const int R = int(cdiv(n, T));
+    if ((st = fill_u32(t.colcnt, n, 0u, stream)) != GT_OK) return st;
+    k_tiles<false><<<R, kThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg, nullptr,
+                                               nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                               t.colcnt);
+    GT_LAUNCH_CHECK("tiles_count");
+    if ((st = exclusive_scan_i32(t.dense_per_tilerow, R, tile_rowptr, t.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(t.sp_deg, n, sp_rowptr, t.scan, stream)) != GT_OK) return st;
+    const unsigned g = grid_for(n, 256, 8192);
+    k_over<int32_t><<<g, 256, 0, stream>>>(n, t.sp_deg, GT_LONG_ROW, t.long_row_flag);
+    GT_LAUNCH_CHECK("tiles_long_rows");
+    k_over<uint32_t><<<g, 256, 0, stream>>>(n, t.colcnt, GT_LONG_ROW, t.long_col_flag);
+    GT_LAUNCH_CHECK("tiles_long_cols");
+    if ((st = exclusive_scan_i32(t.long_row_flag, n, t.long_row_pos, t.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(t.long_col_flag, n, t.long_col_pos, t.scan, stream)) != GT_OK) return st;
+    return GT_OK;
+}
+
+}  // namespace
+}  // namespace gt
+
+using namespace gt;
+
+extern "C" size_t gt_tiles_workspace_size(int64_t n, int64_t nnz, int32_t T) {
+    Ws ws(nullptr);
+    carve(ws, n, nnz, T);
+    return ws.size();
+}
+
+extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
+                                    uint32_t tau_ppm, gt_tiles* plan, void* ws_ptr, size_t ws_bytes,
+                                    hipStream_t stream) {
+    gt_status st = check_common("gt_tiles_count", n, nnz, rowptr, col, T, ws_ptr, ws_bytes);
+    if (st != GT_OK) return st;
+    if (!plan) return fail(GT_ERR_INVALID_ARG, "gt_tiles_count: null plan");
+    plan->n = n;
+    plan->T = T;
+    plan->n_row_tiles = n > 0 ? cdiv(n, T) : 0;
+    plan->n_dense = plan->nnz_sparse = plan->n_long_rows = plan->n_long_cols = 0;
+    if (n == 0) return GT_OK;
+    Ws ws(ws_ptr);
+    TilesWs t = carve(ws, n, nnz, T);
+    if ((st = launch_validate_csr(n, nnz, rowptr, col, t.flags, stream)) != GT_OK) return st;
+    if ((st = read_validation(t.flags, stream)) != GT_OK) return st;
+    if ((st = count_pass(n, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
+        return st;
+    const int64_t R = plan->n_row_tiles;
+    int64_t h[4] = {0, 0, 0, 0};
+    GT_HIP(hipMemcpyAsync(&h[0], t.tmp_tile_rowptr + R, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipMemcpyAsync(&h[1], t.tmp_sp_rowptr + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipMemcpyAsync(&h[2], t.long_row_pos + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipMemcpyAsync(&h[3], t.long_col_pos + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipStreamSynchronize(stream));
+    plan->n_dense = h[0];
+    plan->nnz_sparse = h[1];
+    plan->n_long_rows = h[2];
+    plan->n_long_cols = h[3];
+    return GT_OK;
+}
+
+extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
+                                    uint32_t tau_ppm, gt_tiles* plan, void* ws_ptr, size_t ws_bytes,
+                                    hipStream_t stream) {
+    gt_status st = check_common("gt_build_tiles", n, nnz, rowptr, col, T, ws_ptr, ws_bytes);
+    if (st != GT_OK) return st;
+    if (!plan) return fail(GT_ERR_INVALID_ARG, "gt_build_tiles: null plan");
+    if (plan->n != n || plan->T != T) return fail(GT_ERR_INVALID_ARG, "gt_build_tiles: plan->n / plan->T mismatch");
+    if (plan->n_dense < 0 || plan->nnz_sparse < 0 || plan->n_dense > nnz || plan->nnz_sparse > nnz ||
+        plan->n_long_rows < 0 || plan->n_long_cols < 0 || plan->n_long_rows > n || plan->n_long_cols > n)
+        return fail(GT_ERR_INVALID_ARG, "gt_build_tiles: plan sizes out of range");
+    if ((plan->n_long_rows > 0 && !plan->long_rows) || (plan->n_long_cols > 0 && !plan->long_cols))
+        return fail(GT_ERR_INVALID_ARG, "gt_build_tiles: null long-row list");
+    if (!plan->tile_rowptr || !plan->sp_rowptr || !plan->sp_colptr || !plan->tileT_ptr ||
+        (plan->n_dense > 0 && (!plan->tile_col || !plan->tile_nnz || !plan->tile_mask || !plan->tileT_idx)) ||
+        (plan->nnz_sparse > 0 && (!plan->sp_col || !plan->sp_row)))
+        return fail(GT_ERR_INVALID_ARG, "gt_build_tiles: null plan array");
+    const int R = n > 0 ? int(cdiv(n, T)) : 0;
+    plan->n_row_tiles = R;
+    if (n == 0) {
+        if ((st = fill_i64(plan->tile_rowptr, 1, 0, stream)) != GT_OK) return st;
+        if ((st = fill_i64(plan->tileT_ptr, 1, 0, stream)) != GT_OK) return st;
+        if ((st = fill_i64(plan->sp_rowptr, 1, 0, stream)) != GT_OK) return st;
+        return fill_i64(plan->sp_colptr, 1, 0, stream);
+    }
+    Ws ws(ws_ptr);
+    TilesWs t = carve(ws, n, nnz, T);
+    if ((st = count_pass(n, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) != GT_OK)
+        return st;
+    {
+        const unsigned g = grid_for(n, 256, 8192);
+        if (plan->n_long_rows > 0) {
+            k_compact_list<<<g, 256, 0, stream>>>(n, t.long_row_flag, t.long_row_pos, plan->long_rows);
+            GT_LAUNCH_CHECK("tiles_long_row_list");
+        }
+        if (plan->n_long_cols > 0) {
+            k_compact_list<<<g, 256, 0, stream>>>(n, t.long_col_flag, t.long_col_pos, plan->long_cols);
+            GT_LAUNCH_CHECK("tiles_long_col_list");
+        }
+    }
+    const int64_t words = plan->n_dense * int64_t(T) * (T / 32);
+    if ((st = fill_u32(plan->tile_mask, words, 0u, stream)) != GT_OK) return st;
+    k_tiles<true><<<R, kThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
+                                              plan->tile_col, plan->tile_nnz, plan->tile_mask, plan->sp_rowptr,
+                                              plan->sp_col, t.keys, t.vals, nullptr);
+    GT_LAUNCH_CHECK("tiles_fill");
+    // remainder transpose: stable sort of (column, row) pairs by column
+    const int64_t m = plan->nnz_sparse;
+    if ((st = fill_u32(t.counts, n, 0u, stream)) != GT_OK) return st;
+    if (m > 0) {
+        if ((st = count_keys(reinterpret_cast<const int32_t*>(t.keys), m, t.counts, stream)) != GT_OK) return st;
+        if ((st = radix_sort_u32(t.keys, t.vals, m, bits_for(n), t.sort, stream)) != GT_OK) return st;
+        k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, t.vals, plan->sp_row);
+        GT_LAUNCH_CHECK("tiles_sp_row");
+    }
+    if ((st = exclusive_scan_u32(t.counts, n, plan->sp_colptr, t.scan, stream)) != GT_OK) return st;
+    // tiles grouped by column: stable sort of (J, tile index) by J
+    const int64_t d = plan->n_dense;
+    if ((st = fill_u32(t.counts, R, 0u, stream)) != GT_OK) return st;
+    if (d > 0) {
+        if ((st = count_keys(plan->tile_col, d, t.counts, stream)) != GT_OK) return st;
+        if ((st = copy_bytes(t.keys, plan->tile_col, d * 4, stream)) != GT_OK) return st;
+        if ((st = iota_u32(t.vals, d, stream)) != GT_OK) return st;
+        if ((st = radix_sort_u32(t.keys, t.vals, d, bits_for(R), t.sort, stream)) != GT_OK) return st;
+        k_u32_to_i32<<<grid_for(d, 256, 16384), 256, 0, stream>>>(d, t.vals, plan->tileT_idx);
+        GT_LAUNCH_CHECK("tiles_tileT");
+    }
+    if ((st = exclusive_scan_u32(t.counts, R, plan->tileT_ptr, t.scan, stream)) != GT_OK) return st;
+    return GT_OK;
+}

@@ -1,0 +1,379 @@
+"""ctypes binding of libgt (C ABI in include/gt.h).
+
+Argument marshalling only: every wrapper checks tensor shapes/dtypes/devices,
+allocates outputs and workspace with torch on the tensors' device, and calls
+the C entry point of the same name on torch's current HIP stream.  Nothing
+here computes any part of the method.  The library must be built
+(``python -m paper_2407_14106_amd.build``); loading fails loudly otherwise.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgt.so")
+
+GT_OK = 0
+GT_ERR_INVALID_ARG = -1
+GT_ERR_UNSUPPORTED = -2
+GT_ERR_UNSORTED = -3
+GT_ERR_DUPLICATE = -4
+GT_ERR_OUT_OF_RANGE = -5
+GT_ERR_WORKSPACE = -6
+GT_ERR_HIP = -7
+GT_F32 = 0
+GT_BF16 = 1
+GT_LONG_ROW = 256
+
+_i32, _i64, _u32, _u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
+_vp, _sz, _f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
+
+
+class GtTiles(ctypes.Structure):
+    _fields_ = [
+        ("n", _i64), ("T", _i32), ("reserved", _i32), ("n_row_tiles", _i64), ("n_dense", _i64),
+        ("nnz_sparse", _i64), ("n_long_rows", _i64), ("n_long_cols", _i64),
+        ("tile_rowptr", _vp), ("tile_col", _vp), ("tile_nnz", _vp), ("tile_mask", _vp),
+        ("sp_rowptr", _vp), ("sp_col", _vp), ("sp_colptr", _vp), ("sp_row", _vp),
+        ("tileT_ptr", _vp), ("tileT_idx", _vp), ("long_rows", _vp), ("long_cols", _vp),
+    ]
+
+
+_P = ctypes.POINTER
+SIGNATURES = {
+    "gt_abi_version": (_i32, []),
+    "gt_status_string": (ctypes.c_char_p, [_i32]),
+    "gt_last_error": (ctypes.c_char_p, []),
+    "gt_validate_csr_workspace_size": (_sz, []),
+    "gt_validate_csr": (_i32, [_i64, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "gt_reorder_workspace_size": (_sz, [_i64, _i64]),
+    "gt_reorder": (_i32, [_i64, _i64, _vp, _vp, _i32, _u64, _vp, _vp, _vp, _P(_i32), _vp, _sz, _vp]),
+    "gt_permute_workspace_size": (_sz, [_i64, _i64]),
+    "gt_permute_csr": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gt_gather_rows": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp]),
+    "gt_scatter_rows": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp]),
+    "gt_tiles_workspace_size": (_sz, [_i64, _i64, _i32]),
+    "gt_tiles_count": (_i32, [_i64, _i64, _vp, _vp, _i32, _u32, _P(GtTiles), _vp, _sz, _vp]),
+    "gt_build_tiles": (_i32, [_i64, _i64, _vp, _vp, _i32, _u32, _P(GtTiles), _vp, _sz, _vp]),
+    "gt_sparse_attn_fwd_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
+    "gt_sparse_attn_fwd": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _sz, _vp]),
+    "gt_sparse_attn_bwd_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
+    "gt_sparse_attn_bwd": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp,
+                                  _vp, _vp, _sz, _vp]),
+    "gt_sparse_attn_bwd_rows_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
+    "gt_sparse_attn_bwd_rows": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp,
+                                       _vp, _vp, _sz, _vp]),
+    "gt_sparse_attn_bwd_cols_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
+    "gt_sparse_attn_bwd_cols": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp,
+                                       _vp, _vp, _sz, _vp]),
+    "gt_dense_attn_fwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp]),
+    "gt_dense_attn_bwd_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
+    "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
+                                 _sz, _vp]),
+}
+
+_LIB = None
+
+
+class GtError(RuntimeError):
+    def __init__(self, status: int, where: str, text: str):
+        super().__init__(f"{where}: status {status} ({text})")
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libgt.so and declare its signatures; raises if it is missing."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(path):
+        raise RuntimeError(f"libgt.so not found at {path}: build it with `python -m paper_2407_14106_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != GT_OK:
+        lib = load_library()
+        raise GtError(status, where, lib.gt_last_error().decode() or lib.gt_status_string(status).decode())
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _check_csr(rowptr: torch.Tensor, col: torch.Tensor):
+    _need(rowptr.is_cuda and col.is_cuda, "CSR must be on the GPU")
+    _need(rowptr.dtype == torch.int64 and col.dtype == torch.int32, "rowptr int64 and col int32 expected")
+    _need(rowptr.is_contiguous() and col.is_contiguous(), "CSR must be contiguous")
+    _need(rowptr.dim() == 1 and rowptr.numel() >= 1, "rowptr must be 1-D with n+1 entries")
+
+
+# ------------------------------------------------------------------------ integer stages
+
+def validate_csr(rowptr: torch.Tensor, col: torch.Tensor) -> None:
+    lib = load_library()
+    _check_csr(rowptr, col)
+    ws = _workspace(lib.gt_validate_csr_workspace_size(), rowptr.device)
+    _check(lib.gt_validate_csr(rowptr.numel() - 1, col.numel(), _ptr(rowptr), _ptr(col), _ptr(ws), ws.numel(),
+                               _stream(rowptr.device)), "gt_validate_csr")
+
+
+def reorder(rowptr: torch.Tensor, col: torch.Tensor, iters: int = 20, seed: int = 0, want_sweeps: bool = False):
+    """(perm, iperm, labels[, sweeps]) of the cluster reordering."""
+    lib = load_library()
+    _check_csr(rowptr, col)
+    n, nnz = rowptr.numel() - 1, col.numel()
+    dev = rowptr.device
+    perm = torch.empty(n, dtype=torch.int32, device=dev)
+    iperm = torch.empty(n, dtype=torch.int32, device=dev)
+    labels = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.gt_reorder_workspace_size(n, nnz), dev)
+    sweeps = ctypes.c_int32(-1)
+    _check(lib.gt_reorder(n, nnz, _ptr(rowptr), _ptr(col), iters, ctypes.c_uint64(seed % (1 << 64)), _ptr(perm),
+                          _ptr(iperm), _ptr(labels), ctypes.byref(sweeps) if want_sweeps else None, _ptr(ws),
+                          ws.numel(), _stream(dev)), "gt_reorder")
+    return (perm, iperm, labels, sweeps.value) if want_sweeps else (perm, iperm, labels)
+
+
+def permute_csr(rowptr: torch.Tensor, col: torch.Tensor, perm: torch.Tensor, iperm: torch.Tensor):
+    lib = load_library()
+    _check_csr(rowptr, col)
+    n, nnz = rowptr.numel() - 1, col.numel()
+    _need(perm.dtype == torch.int32 and iperm.dtype == torch.int32 and perm.numel() == n == iperm.numel(),
+          "perm/iperm must be int32[n]")
+    dev = rowptr.device
+    rp = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    cl = torch.empty(nnz, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.gt_permute_workspace_size(n, nnz), dev)
+    _check(lib.gt_permute_csr(n, nnz, _ptr(rowptr), _ptr(col), _ptr(perm), _ptr(iperm), _ptr(rp), _ptr(cl),
+                              _ptr(ws), ws.numel(), _stream(dev)), "gt_permute_csr")
+    return rp, cl
+
+
+def _row_bytes(x: torch.Tensor) -> int:
+    return x[0].numel() * x.element_size() if x.shape[0] else 0
+
+
+def gather_rows(x: torch.Tensor, perm: torch.Tensor) -> torch.Tensor:
+    """out[r] = x[perm[r]] (row gather along dim 0)."""
+    lib = load_library()
+    _need(x.is_contiguous() and perm.dtype == torch.int32 and perm.numel() == x.shape[0], "bad gather arguments")
+    out = torch.empty_like(x)
+    _check(lib.gt_gather_rows(x.shape[0], _row_bytes(x), _ptr(x), _ptr(perm), _ptr(out), _stream(x.device)),
+           "gt_gather_rows")
+    return out
+
+
+def scatter_rows(x: torch.Tensor, perm: torch.Tensor) -> torch.Tensor:
+    """out[perm[r]] = x[r] (inverse of gather_rows)."""
+    lib = load_library()
+    _need(x.is_contiguous() and perm.dtype == torch.int32 and perm.numel() == x.shape[0], "bad scatter arguments")
+    out = torch.empty_like(x)
+    _check(lib.gt_scatter_rows(x.shape[0], _row_bytes(x), _ptr(x), _ptr(perm), _ptr(out), _stream(x.device)),
+           "gt_scatter_rows")
+    return out
+
+
+@dataclass
+class Plan:
+    """A tile plan: the device arrays and the C struct pointing at them."""
+
+    c: GtTiles
+    arrays: dict
+
+    @property
+    def n(self):
+        return self.c.n
+
+    @property
+    def T(self):
+        return self.c.T
+
+    @property
+    def n_dense(self):
+        return self.c.n_dense
+
+    @property
+    def nnz_sparse(self):
+        return self.c.nnz_sparse
+
+    def to_numpy(self) -> dict:
+        out = {k: v.cpu().numpy() for k, v in self.arrays.items()}
+        out["T"] = self.c.T
+        out["n_row_tiles"] = self.c.n_row_tiles
+        return out
+
+
+def tau_to_ppm(tau: float) -> int:
+    return int(round(float(tau) * 1e6))
+
+
+def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: int = 10000) -> Plan:
+    """Tile plan of the CSR at tile edge T and density threshold tau_ppm (parts per million)."""
+    lib = load_library()
+    _check_csr(rowptr, col)
+    n, nnz = rowptr.numel() - 1, col.numel()
+    dev = rowptr.device
+    ws = _workspace(lib.gt_tiles_workspace_size(n, nnz, T), dev)
+    c = GtTiles()
+    st = _stream(dev)
+    _check(lib.gt_tiles_count(n, nnz, _ptr(rowptr), _ptr(col), T, tau_ppm, ctypes.byref(c), _ptr(ws), ws.numel(), st),
+           "gt_tiles_count")
+    R, nd, ns = c.n_row_tiles, c.n_dense, c.nnz_sparse
+    i64 = dict(dtype=torch.int64, device=dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    arrays = {
+        "tile_rowptr": torch.empty(R + 1, **i64),
+        "tile_col": torch.empty(nd, **i32),
+        "tile_nnz": torch.empty(nd, **i32),
+        "tile_mask": torch.empty(nd * T * T // 32, **i32),
+        "sp_rowptr": torch.empty(n + 1, **i64),
+        "sp_col": torch.empty(ns, **i32),
+        "sp_colptr": torch.empty(n + 1, **i64),
+        "sp_row": torch.empty(ns, **i32),
+        "tileT_ptr": torch.empty(R + 1, **i64),
+        "tileT_idx": torch.empty(nd, **i32),
+        "long_rows": torch.empty(c.n_long_rows, **i32),
+        "long_cols": torch.empty(c.n_long_cols, **i32),
+    }
+    for k, v in arrays.items():
+        setattr(c, k, v.data_ptr())
+    _check(lib.gt_build_tiles(n, nnz, _ptr(rowptr), _ptr(col), T, tau_ppm, ctypes.byref(c), _ptr(ws), ws.numel(), st),
+           "gt_build_tiles")
+    arrays["tile_mask"] = arrays["tile_mask"].view(torch.int32)
+    return Plan(c=c, arrays=arrays)
+
+
+# ------------------------------------------------------------------------------ attention
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return GT_F32
+    if t.dtype == torch.bfloat16:
+        return GT_BF16
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _check_feats(n: int, *ts: torch.Tensor):
+    ref = ts[0]
+    _need(ref.dim() == 3 and ref.shape[0] == n, "features must be [n, H, d]")
+    for t in ts:
+        _need(t.shape == ref.shape and t.dtype == ref.dtype and t.is_cuda and t.is_contiguous(),
+              "feature tensors must share shape/dtype and be contiguous GPU tensors")
+
+
+def sparse_attn_fwd(plan: Plan, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: float | None = None):
+    """(O, LSE) of neighbourhood softmax attention over the plan's graph."""
+    lib = load_library()
+    _check_feats(plan.n, Q, K, V)
+    n, H, d = Q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    O = torch.empty_like(Q)
+    LSE = torch.empty((n, H), dtype=torch.float32, device=Q.device)
+    ws = _workspace(lib.gt_sparse_attn_fwd_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    _check(lib.gt_sparse_attn_fwd(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), scale, _ptr(O),
+                                  _ptr(LSE), _ptr(ws), ws.numel(), _stream(Q.device)), "gt_sparse_attn_fwd")
+    return O, LSE
+
+
+def sparse_attn_bwd(plan: Plan, Q, K, V, O, dO, LSE, scale: float | None = None):
+    """(dQ, dK, dV) of neighbourhood softmax attention."""
+    lib = load_library()
+    _check_feats(plan.n, Q, K, V, O, dO)
+    n, H, d = Q.shape
+    _need(LSE.dtype == torch.float32 and LSE.shape == (n, H) and LSE.is_contiguous(), "LSE must be fp32 [n, H]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    ws = _workspace(lib.gt_sparse_attn_bwd_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    _check(lib.gt_sparse_attn_bwd(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO),
+                                  _ptr(LSE), scale, _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(),
+                                  _stream(Q.device)), "gt_sparse_attn_bwd")
+    return dQ, dK, dV
+
+
+def sparse_attn_bwd_rows(plan: Plan, Q, K, V, O, dO, LSE, scale: float | None = None):
+    """(dQ, Dstat) - the row-owned half of the backward."""
+    lib = load_library()
+    _check_feats(plan.n, Q, K, V, O, dO)
+    n, H, d = Q.shape
+    _need(LSE.dtype == torch.float32 and LSE.shape == (n, H) and LSE.is_contiguous(), "LSE must be fp32 [n, H]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    dQ = torch.empty_like(Q)
+    Dstat = torch.empty((n, H), dtype=torch.float32, device=Q.device)
+    ws = _workspace(lib.gt_sparse_attn_bwd_rows_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    _check(lib.gt_sparse_attn_bwd_rows(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO),
+                                       _ptr(LSE), scale, _ptr(dQ), _ptr(Dstat), _ptr(ws), ws.numel(),
+                                       _stream(Q.device)), "gt_sparse_attn_bwd_rows")
+    return dQ, Dstat
+
+
+def sparse_attn_bwd_cols(plan: Plan, Q, K, V, dO, LSE, Dstat, scale: float | None = None):
+    """(dK, dV) - the column-owned half of the backward."""
+    lib = load_library()
+    _check_feats(plan.n, Q, K, V, dO)
+    n, H, d = Q.shape
+    _need(LSE.dtype == torch.float32 and LSE.shape == (n, H) and LSE.is_contiguous(), "LSE must be fp32 [n, H]")
+    _need(Dstat.dtype == torch.float32 and Dstat.shape == (n, H) and Dstat.is_contiguous(), "Dstat must be fp32 [n, H]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    dK, dV = torch.empty_like(K), torch.empty_like(V)
+    ws = _workspace(lib.gt_sparse_attn_bwd_cols_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    _check(lib.gt_sparse_attn_bwd_cols(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(dO), _ptr(LSE),
+                                       _ptr(Dstat), scale, _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(),
+                                       _stream(Q.device)), "gt_sparse_attn_bwd_cols")
+    return dK, dV
+
+
+def dense_attn_fwd(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: float | None = None):
+    """(O, LSE) of full softmax attention over all n nodes."""
+    lib = load_library()
+    _check_feats(Q.shape[0], Q, K, V)
+    n, H, d = Q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    O = torch.empty_like(Q)
+    LSE = torch.empty((n, H), dtype=torch.float32, device=Q.device)
+    _check(lib.gt_dense_attn_fwd(n, H, d, _dtype_code(Q), _ptr(Q), _ptr(K), _ptr(V), scale, _ptr(O), _ptr(LSE),
+                                 _stream(Q.device)), "gt_dense_attn_fwd")
+    return O, LSE
+
+
+def dense_attn_bwd(Q, K, V, O, dO, LSE, scale: float | None = None):
+    """(dQ, dK, dV) of full softmax attention."""
+    lib = load_library()
+    _check_feats(Q.shape[0], Q, K, V, O, dO)
+    n, H, d = Q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    ws = _workspace(lib.gt_dense_attn_bwd_workspace_size(n, H, d, dt), Q.device)
+    _check(lib.gt_dense_attn_bwd(n, H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE), scale,
+                                 _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(), _stream(Q.device)),
+           "gt_dense_attn_bwd")
+    return dQ, dK, dV

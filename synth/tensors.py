@@ -7,7 +7,12 @@ oracle (which upcasts exactly to fp64) and the GPU read the same numbers.
 
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
+
+_CHUNK = 1 << 20  # values per independently seeded chunk
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -27,11 +32,33 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
     return bf16_to_f32(bf16_bits(x))
 
 
-def normal_tensor(shape, rng: np.random.Generator, dtype: str) -> np.ndarray:
-    """fp32 N(0,1) draws, rounded to bfloat16 when ``dtype == 'bf16'`` (returned as fp32 values)."""
-    x = rng.standard_normal(size=shape, dtype=np.float32)
-    if dtype == "bf16":
-        x = bf16_round(x)
-    elif dtype != "f32":
+def normal_tensor(shape, key, dtype: str) -> np.ndarray:
+    """fp32 N(0,1) draws, rounded to bfloat16 when ``dtype == 'bf16'`` (returned as fp32 values).
+
+    ``key`` is a tuple of integers.  The values are generated in chunks of 2^20,
+    chunk c from PCG64 seeded with SeedSequence(key + (c,)), so the result does
+    not depend on how many threads fill it.
+    """
+    if dtype not in ("f32", "bf16"):
         raise ValueError(dtype)
-    return x
+    out = np.empty(int(np.prod(shape)), dtype=np.float32)
+    n_chunks = (out.size + _CHUNK - 1) // _CHUNK
+    key = tuple(int(k) for k in key)
+
+    def fill(c):
+        part = out[c * _CHUNK:(c + 1) * _CHUNK]
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(key + (c,))))
+        rng.standard_normal(out=part, dtype=np.float32)
+        if dtype == "bf16":
+            u = part.view(np.uint32)
+            u += np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+            u &= np.uint32(0xFFFF0000)
+
+    workers = max(1, min(16, os.cpu_count() or 1, n_chunks))
+    if workers == 1:
+        for c in range(n_chunks):
+            fill(c)
+    else:
+        with ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill, range(n_chunks)))
+    return out.reshape(shape)

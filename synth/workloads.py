@@ -42,13 +42,12 @@ class Workload:
 
     def tensors(self, with_grad: bool | None = None):
         """Q, K, V (and dO when the workload has a backward pass) as fp32 numpy arrays."""
-        rng = np.random.Generator(np.random.PCG64(self.seed + 7919))
         shape = (self.graph.n, self.heads, self.dim)
-        q = normal_tensor(shape, rng, self.dtype)
-        k = normal_tensor(shape, rng, self.dtype)
-        v = normal_tensor(shape, rng, self.dtype)
+        q = normal_tensor(shape, (self.seed, 0), self.dtype)
+        k = normal_tensor(shape, (self.seed, 1), self.dtype)
+        v = normal_tensor(shape, (self.seed, 2), self.dtype)
         want = self.backward if with_grad is None else with_grad
-        do = normal_tensor(shape, rng, self.dtype) if want else None
+        do = normal_tensor(shape, (self.seed, 3), self.dtype) if want else None
         return q, k, v, do
 
 

@@ -1,0 +1,110 @@
+"""The C-ABI library loads, exports every symbol that include/gt.h declares, and
+rejects bad arguments on the host before touching any device (no GPU needed)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2407_14106_amd import gt
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "gt.h")
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails its host-side checks first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(gt.LIB_PATH):
+        from paper_2407_14106_amd import build
+
+        build.build()
+    return gt.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gt_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert "gt_sparse_attn_fwd" in names and "gt_reorder" in names and len(names) >= 20
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(gt.SIGNATURES), "binding signatures out of sync with the header"
+
+
+def test_version_and_status_strings(lib):
+    assert lib.gt_abi_version() == 1
+    assert lib.gt_status_string(gt.GT_OK) == b"ok"
+    assert lib.gt_status_string(gt.GT_ERR_WORKSPACE) == b"workspace too small"
+    assert lib.gt_status_string(-99) == b"unknown status"
+
+
+def test_struct_layout_matches_header():
+    assert ctypes.sizeof(gt.GtTiles) == 8 * 6 + 4 * 2 + 8 * 12
+
+
+def test_workspace_queries_are_host_only(lib):
+    assert lib.gt_reorder_workspace_size(1000, 5000) > lib.gt_reorder_workspace_size(10, 50) > 0
+    assert lib.gt_permute_workspace_size(1000, 5000) > 0
+    assert lib.gt_tiles_workspace_size(1000, 5000, 128) > 0
+    c = gt.GtTiles(n=1000, T=128, n_row_tiles=8, n_dense=0)
+    assert lib.gt_sparse_attn_fwd_workspace_size(ctypes.byref(c), 8, 32, gt.GT_BF16) > 0
+    c.n_dense = 5
+    with_tiles = lib.gt_sparse_attn_fwd_workspace_size(ctypes.byref(c), 8, 32, gt.GT_BF16)
+    assert with_tiles >= 1000 * 8 * 34 * 4
+    assert lib.gt_sparse_attn_fwd_workspace_size(ctypes.byref(c), 8, 48, gt.GT_BF16) == 0  # unsupported d
+
+
+def test_argument_errors_without_device(lib):
+    stream = None
+    # null plan
+    assert lib.gt_sparse_attn_fwd(None, 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, 1 << 30,
+                                  stream) == gt.GT_ERR_INVALID_ARG
+    c = gt.GtTiles(n=100, T=128, n_row_tiles=1)
+    for name in ("tile_rowptr", "sp_rowptr", "sp_colptr", "tileT_ptr"):
+        setattr(c, name, 0x1000)
+    # unsupported head width and head count
+    assert lib.gt_sparse_attn_fwd(ctypes.byref(c), 8, 48, gt.GT_BF16, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE,
+                                  1 << 30, stream) == gt.GT_ERR_UNSUPPORTED
+    assert lib.gt_sparse_attn_bwd(ctypes.byref(c), 3, 32, gt.GT_F32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1.0, FAKE,
+                                  FAKE, FAKE, FAKE, 1 << 30, stream) == gt.GT_ERR_UNSUPPORTED
+    # workspace too small
+    assert lib.gt_sparse_attn_fwd(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, 0,
+                                  stream) == gt.GT_ERR_WORKSPACE
+    # null feature pointer
+    assert lib.gt_sparse_attn_fwd(ctypes.byref(c), 8, 32, gt.GT_BF16, None, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE,
+                                  1 << 30, stream) == gt.GT_ERR_INVALID_ARG
+    assert b"null" in lib.gt_last_error()
+    # tiles: unsupported T, too many tile rows, workspace
+    t = gt.GtTiles()
+    assert lib.gt_tiles_count(1000, 10, FAKE, FAKE, 96, 100, ctypes.byref(t), FAKE, 1 << 30,
+                              stream) == gt.GT_ERR_UNSUPPORTED
+    assert lib.gt_tiles_count(64 * 20000, 10, FAKE, FAKE, 64, 100, ctypes.byref(t), FAKE, 1 << 40,
+                              stream) == gt.GT_ERR_UNSUPPORTED
+    assert lib.gt_tiles_count(1000, 10, FAKE, FAKE, 64, 100, ctypes.byref(t), FAKE, 16, stream) == gt.GT_ERR_WORKSPACE
+    # reorder / permute / validate
+    assert lib.gt_reorder(-1, 0, FAKE, FAKE, 10, 0, FAKE, FAKE, None, None, FAKE, 1 << 30,
+                          stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_reorder(100, 10, FAKE, FAKE, 5000, 0, FAKE, FAKE, None, None, FAKE, 1 << 30,
+                          stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_reorder(100, 10, FAKE, FAKE, 10, 0, FAKE, FAKE, None, None, FAKE, 8, stream) == gt.GT_ERR_WORKSPACE
+    assert lib.gt_permute_csr(100, 10, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+                              stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_validate_csr(10, 10, FAKE, FAKE, FAKE, 0, stream) == gt.GT_ERR_WORKSPACE
+    assert lib.gt_gather_rows(10, 6, FAKE, FAKE, FAKE, stream) == gt.GT_ERR_INVALID_ARG
+    # dense layer: bad pointers / sizes
+    assert lib.gt_dense_attn_fwd(100, 8, 64, gt.GT_BF16, None, FAKE, FAKE, 1.0, FAKE, FAKE,
+                                 stream) == gt.GT_ERR_INVALID_ARG
+
+
+def test_python_binding_rejects_cpu_tensors(lib):
+    import torch
+
+    rp = torch.zeros(5, dtype=torch.int64)
+    cl = torch.zeros(0, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        gt.build_tiles(rp, cl)

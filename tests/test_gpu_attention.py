@@ -1,0 +1,143 @@
+"""GPU neighbourhood softmax attention (§3.2) vs the fp64 oracle, forward and
+backward, across tile plans (§3.4: every density threshold gives the same
+result), dtypes, head counts and widths, plus edge cases: empty rows, rows and
+columns longer than one wavefront slice can take, ragged sizes, a single node.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as OA
+from oracle import plan as OP
+from oracle import reorder as OR
+from synth import csr_from_pairs, make_workload
+from synth.tensors import normal_tensor
+from tests.helpers import assert_close, dev_csr, dev_feat, host
+
+pytestmark = pytest.mark.gpu
+
+CSR_ONLY = 1_000_001  # threshold above 100%: no dense tile, every edge on the edge kernels
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def feats(n, H, d, dtype, seed):
+    return [normal_tensor((n, H, d), (seed, t), dtype) for t in range(4)]
+
+
+def run_case(gt, rowptr, col, H, d, dtype, taus=(CSR_ONLY,), T=128, seed=0, bwd=True):
+    n = len(rowptr) - 1
+    q, k, v, do = feats(n, H, d, dtype, seed)
+    scale = 1.0 / np.sqrt(d)
+    O_ref, L_ref = OA.sparse_attn_fwd(rowptr, col, q, k, v, scale)
+    grads_ref = OA.sparse_attn_bwd(rowptr, col, q, k, v, do, scale) if bwd else None
+    rp, cl = dev_csr(rowptr, col)
+    Q, K, V, dO = (dev_feat(x, dtype) for x in (q, k, v, do))
+    for tau in taus:
+        say("case", n, len(col), H, d, dtype, T, tau)
+        plan = gt.build_tiles(rp, cl, T, tau)
+        O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
+        torch.cuda.synchronize()
+        assert_close(host(O), O_ref, dtype, f"O tau={tau}")
+        assert_close(L.cpu().numpy(), L_ref, "f32" if dtype == "f32" else "bf16", f"LSE tau={tau}")
+        if bwd:
+            dQ, dK, dV = gt.sparse_attn_bwd(plan, Q, K, V, O, dO, L, scale)
+            torch.cuda.synchronize()
+            for name, x, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), grads_ref):
+                assert_close(host(x), r, dtype, f"{name} tau={tau}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("H,d", [(1, 64), (2, 32), (4, 32), (8, 32), (8, 64), (16, 32), (16, 64), (1, 32)])
+def test_small_graph_all_shapes(gt, dtype, H, d):
+    g = make_workload("c1", 0.1).graph
+    run_case(gt, g.rowptr, g.col, H, d, dtype, seed=H * 100 + d)
+
+
+def test_c1_full_fp32_forward(gt):
+    w = make_workload("c1")
+    q, k, v, _ = w.tensors()
+    g = w.graph
+    O_ref, L_ref = OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, 1 / 8)
+    rp, cl = dev_csr(g.rowptr, g.col)
+    plan = gt.build_tiles(rp, cl, 128, CSR_ONLY)
+    O, L = gt.sparse_attn_fwd(plan, dev_feat(q, "f32"), dev_feat(k, "f32"), dev_feat(v, "f32"), 1 / 8)
+    assert_close(host(O), O_ref, "f32", "O")
+    assert_close(L.cpu().numpy(), L_ref, "f32", "LSE")
+
+
+@pytest.mark.parametrize("name,scale", [("c2", 0.02), ("c3", 0.01), ("c4", 0.005), ("c5", 0.05)])
+def test_workload_shapes_bf16(gt, name, scale):
+    w = make_workload(name, scale)
+    run_case(gt, w.graph.rowptr, w.graph.col, w.heads, w.dim, w.dtype, seed=w.seed)
+
+
+def test_empty_rows_single_node_and_ragged(gt):
+    # rows 3 and 77 are empty; n = 131 is not a multiple of any tile or wave size
+    u = np.array([0, 1, 2, 5, 5, 9, 100, 130, 130])
+    v = np.array([1, 2, 4, 6, 7, 9, 101, 0, 129])
+    rowptr, col = csr_from_pairs(131, u, v, symmetric=False, self_loops=False)
+    for dtype in ("f32", "bf16"):
+        run_case(gt, rowptr, col, 4, 32, dtype, seed=3)
+    rowptr, col = csr_from_pairs(1, [], [])
+    run_case(gt, rowptr, col, 8, 64, "bf16", seed=4)
+
+
+def test_long_rows_and_columns(gt):
+    # hub 0 attends to 3000 nodes and is attended by them; node 5 has 300 in-edges only
+    n = 4000
+    u = np.concatenate([np.zeros(3000, np.int64), np.arange(1000, 1300)])
+    v = np.concatenate([np.arange(1, 3001), np.full(300, 5)])
+    rowptr, col = csr_from_pairs(n, u[:3000], v[:3000], symmetric=True, self_loops=True)
+    r2, c2 = csr_from_pairs(n, u[3000:], v[3000:], symmetric=False, self_loops=False)
+    dense = np.zeros((n, n), bool)
+    for rp_, cl_ in ((rowptr, col), (r2, c2)):
+        rows = np.repeat(np.arange(n), np.diff(rp_))
+        dense[rows, cl_] = True
+    uu, vv = np.nonzero(dense)
+    rowptr, col = csr_from_pairs(n, uu, vv, symmetric=False, self_loops=False)
+    for dtype, H, d in (("f32", 2, 64), ("bf16", 8, 32), ("bf16", 16, 64)):
+        run_case(gt, rowptr, col, H, d, dtype, seed=H + d)
+
+
+def test_bitwise_deterministic(gt):
+    w = make_workload("c4", 0.01)
+    g = w.graph
+    q, k, v, do = w.tensors()
+    rp, cl = dev_csr(g.rowptr, g.col)
+    plan = gt.build_tiles(rp, cl, 128, CSR_ONLY)
+    Q, K, V, dO = (dev_feat(x, "bf16") for x in (q, k, v, do))
+    outs = []
+    for _ in range(2):
+        O, L = gt.sparse_attn_fwd(plan, Q, K, V)
+        outs.append((O, L, *gt.sparse_attn_bwd(plan, Q, K, V, O, dO, L)))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+def test_pipeline_reorder_then_attention_is_equivariant(gt):
+    # reorder + relabel + gather on the GPU, attention in the new order, scatter back:
+    # equals the oracle on the original order.
+    w = make_workload("c5", 0.05)
+    g = w.graph
+    q, k, v, do = w.tensors()
+    scale = 1 / 8
+    rp, cl = dev_csr(g.rowptr, g.col)
+    perm, iperm, _ = gt.reorder(rp, cl)
+    rp2, cl2 = gt.permute_csr(rp, cl, perm, iperm)
+    plan = gt.build_tiles(rp2, cl2, 128, CSR_ONLY)
+    Q, K, V, dO = (gt.gather_rows(dev_feat(x, "bf16"), perm) for x in (q, k, v, do))
+    O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
+    dQ, dK, dV = gt.sparse_attn_bwd(plan, Q, K, V, O, dO, L, scale)
+    O_ref, L_ref = OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, scale)
+    ref = OA.sparse_attn_bwd(g.rowptr, g.col, q, k, v, do, scale)
+    assert_close(host(gt.scatter_rows(O, perm)), O_ref, "bf16", "O")
+    assert_close(gt.scatter_rows(L, perm).cpu().numpy(), L_ref, "bf16", "LSE")
+    for name, x, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
+        assert_close(host(gt.scatter_rows(x, perm)), r, "bf16", name)

@@ -1,0 +1,154 @@
+"""GPU integer stages vs the oracle, bit for bit: CSR validation, cluster
+reordering (§3.3), relabelling, tile plan (§3.4)."""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import plan as OP
+from oracle import reorder as OR
+from synth import csr_from_pairs, make_workload
+from tests.helpers import dev_csr
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def small_graphs():
+    rng = np.random.default_rng(7)
+    out = []
+    out.append(("single", *csr_from_pairs(1, [], [])))
+    out.append(("empty_rows", *csr_from_pairs(130, [0, 5, 9, 129], [1, 6, 120, 3], symmetric=False, self_loops=False)))
+    m = rng.random((257, 257)) < 0.05
+    u, v = np.nonzero(m)
+    out.append(("random_directed_257", *csr_from_pairs(257, u, v, symmetric=False, self_loops=True)))
+    # a star whose center has > 4096 neighbours (workspace count table) and a 100-leaf star (LDS table)
+    n = 6000
+    u = np.concatenate([np.zeros(5000, np.int64), np.full(100, 5500)])
+    v = np.concatenate([np.arange(1, 5001), np.arange(5401, 5501)])
+    u2, v2 = np.nonzero(np.random.default_rng(3).random((n, 8)) < 0.5)
+    out.append(("hubs_6000", *csr_from_pairs(n, np.concatenate([u, u2 % n]),
+                                             np.concatenate([v, (u2 * 7 + v2 * 131) % n]))))
+    for name, sc in (("c1", 1.0), ("c2", 0.05), ("c3", 0.02), ("c4", 0.02), ("c5", 0.1)):
+        g = make_workload(name, sc).graph
+        out.append((f"{name}@{sc}", g.rowptr, g.col))
+    return out
+
+
+GRAPHS = small_graphs()
+
+
+@pytest.mark.parametrize("name,rowptr,col", GRAPHS, ids=[g[0] for g in GRAPHS])
+def test_reorder_bit_exact(gt, name, rowptr, col):
+    say("reorder", name, len(rowptr) - 1, len(col))
+    rp, cl = dev_csr(rowptr, col)
+    perm, iperm, labels, sweeps = gt.reorder(rp, cl, iters=20, seed=5, want_sweeps=True)
+    lab_ref, done = OR.lp_labels(rowptr, col, iters=20, seed=5)
+    perm_ref, iperm_ref = OR.cluster_order(rowptr, col, lab_ref)
+    np.testing.assert_array_equal(labels.cpu().numpy(), lab_ref)
+    np.testing.assert_array_equal(perm.cpu().numpy(), perm_ref)
+    np.testing.assert_array_equal(iperm.cpu().numpy(), iperm_ref)
+    assert sweeps == done
+
+
+@pytest.mark.parametrize("name,rowptr,col", GRAPHS, ids=[g[0] for g in GRAPHS])
+def test_permute_bit_exact(gt, name, rowptr, col):
+    say("permute", name)
+    n = len(rowptr) - 1
+    perm = np.random.default_rng(11).permutation(n).astype(np.int32)
+    iperm = np.empty(n, np.int32)
+    iperm[perm] = np.arange(n)
+    rp, cl = dev_csr(rowptr, col)
+    rp2, cl2 = gt.permute_csr(rp, cl, torch.from_numpy(perm).cuda(), torch.from_numpy(iperm).cuda())
+    ref_rp, ref_cl = OP.permute_csr(rowptr, col, perm, iperm)
+    np.testing.assert_array_equal(rp2.cpu().numpy(), ref_rp)
+    np.testing.assert_array_equal(cl2.cpu().numpy(), ref_cl)
+
+
+def compare_plan(got: dict, ref: dict):
+    for key in ("tile_rowptr", "tile_col", "tile_nnz", "sp_rowptr", "sp_col", "sp_colptr", "sp_row", "tileT_ptr",
+                "tileT_idx"):
+        np.testing.assert_array_equal(got[key], ref[key], err_msg=key)
+    np.testing.assert_array_equal(got["tile_mask"].view(np.uint32), ref["tile_mask"], err_msg="tile_mask")
+    deg = np.diff(ref["sp_rowptr"])
+    np.testing.assert_array_equal(got["long_rows"], np.flatnonzero(deg > 256))
+    cdeg = np.diff(ref["sp_colptr"])
+    np.testing.assert_array_equal(got["long_cols"], np.flatnonzero(cdeg > 256))
+
+
+@pytest.mark.parametrize("name,rowptr,col", GRAPHS, ids=[g[0] for g in GRAPHS])
+@pytest.mark.parametrize("T", [64, 128])
+def test_tiles_bit_exact(gt, name, rowptr, col, T):
+    rp, cl = dev_csr(rowptr, col)
+    n = len(rowptr) - 1
+    for tau in (0, 5000, 10000, 50000, 200000, 1_000_001):
+        say("tiles", name, T, tau)
+        plan = gt.build_tiles(rp, cl, T, tau)
+        ref = OP.build_tiles(rowptr, col, T, tau)
+        assert plan.n_dense == len(ref["tile_col"]) and plan.nnz_sparse == len(ref["sp_col"])
+        compare_plan(plan.to_numpy(), ref)
+    assert n >= 1
+
+
+def test_tiles_threshold_equality(gt):
+    # a 64x64 tile with exactly 64 edges (density 1/64 = 15625 ppm): dense at 15625, sparse at 15626
+    u = np.arange(64)
+    v = (np.arange(64) * 5) % 64
+    rowptr, col = csr_from_pairs(64, u, v, symmetric=False, self_loops=False)
+    rp, cl = dev_csr(rowptr, col)
+    assert gt.build_tiles(rp, cl, 64, 15625).n_dense == 1
+    assert gt.build_tiles(rp, cl, 64, 15626).n_dense == 0
+
+
+def test_full_size_tile_plan_c4(gt):
+    w = make_workload("c4")
+    g = w.graph
+    say("full-size c4 tiles", g.n, g.nnz)
+    perm = np.lexsort((np.arange(g.n), g.block))
+    iperm = np.empty(g.n, np.int64)
+    iperm[perm] = np.arange(g.n)
+    rp_h, cl_h = OP.permute_csr(g.rowptr, g.col, perm, iperm)
+    rp, cl = dev_csr(rp_h, cl_h)
+    plan = gt.build_tiles(rp, cl, 128, 10000)
+    ref = OP.build_tiles(rp_h, cl_h, 128, 10000)
+    compare_plan(plan.to_numpy(), ref)
+
+
+def test_validation_errors(gt):
+    good_rp = np.array([0, 2, 3, 3], np.int64)
+    cases = [
+        (np.array([1, 0, 2], np.int32), gt.GT_ERR_UNSORTED),
+        (np.array([1, 1, 2], np.int32), gt.GT_ERR_DUPLICATE),
+        (np.array([0, 1, 7], np.int32), gt.GT_ERR_OUT_OF_RANGE),
+    ]
+    for col, code in cases:
+        rp, cl = dev_csr(good_rp, col)
+        with pytest.raises(gt.GtError) as e:
+            gt.validate_csr(rp, cl)
+        assert e.value.status == code
+        with pytest.raises(gt.GtError) as e:
+            gt.build_tiles(rp, cl, 64, 100)
+        assert e.value.status == code
+        with pytest.raises(gt.GtError) as e:
+            gt.reorder(rp, cl)
+        assert e.value.status == code
+    rp, cl = dev_csr(np.array([0, 2, 1, 3], np.int64), np.array([0, 1, 2], np.int32))
+    with pytest.raises(gt.GtError) as e:
+        gt.validate_csr(rp, cl)
+    assert e.value.status == gt.GT_ERR_UNSORTED
+    rp, cl = dev_csr(good_rp, np.array([0, 1, 2], np.int32))
+    gt.validate_csr(rp, cl)
+
+
+def test_gather_scatter_rows(gt):
+    x = torch.randn(1000, 8, 32, device="cuda").to(torch.bfloat16)
+    perm = torch.randperm(1000, device="cuda").to(torch.int32)
+    y = gt.gather_rows(x, perm)
+    assert torch.equal(y, x[perm.long()])
+    assert torch.equal(gt.scatter_rows(y, perm), x)
