@@ -2,10 +2,12 @@
 
 Tolerances, r being the fp64 oracle computed from the same (bf16-rounded) inputs:
 * fp32, "1e-5 relative" read normwise: for every (node, head) output vector
-  ||x - r||_2 <= 1e-5 ||r||_2 + 1e-7 sqrt(d) rms(r); a scalar per (node, head)
-  (LSE) must satisfy |x - r| <= 1e-5 max(1, |r|).  (Elementwise relative error
-  is not attainable in any fp32 summation order for entries that are sums of
-  hundreds of cancelling terms.)
+  ||x - r||_2 <= 1e-5 (||r||_2 + rho), rho being the root-mean-square of the
+  vector norms over the whole tensor; a scalar per (node, head) (LSE) must
+  satisfy |x - r| <= 1e-5 max(1, |r|).  Elementwise relative error is not
+  attainable in fp32 for entries that are sums of many cancelling terms, and a
+  vector that is small only through cancellation carries the absolute error of
+  terms of typical size, hence the rho floor.
 * bf16 inputs with fp32 accumulation, elementwise: |x - r| <= 2e-2 + 1e-2 |r|.
 """
 
@@ -42,9 +44,10 @@ def assert_close(x, r, dtype: str, name: str):
     assert np.array_equal(x[~fin], r[~fin]), f"{name}: infinite values differ"
     if dtype == "f32":
         if r.ndim == 3:  # [n, H, d]: normwise per (node, head)
-            rms = np.sqrt(np.mean(r * r)) if r.size else 0.0
+            rn = np.linalg.norm(r, axis=-1)
+            rho = np.sqrt(np.mean(rn * rn)) if rn.size else 0.0
             err = np.linalg.norm(x - r, axis=-1)
-            tol = 1e-5 * np.linalg.norm(r, axis=-1) + 1e-7 * np.sqrt(r.shape[-1]) * rms
+            tol = 1e-5 * (rn + rho)
         else:
             x, r = x[fin], r[fin]
             err = np.abs(x - r)

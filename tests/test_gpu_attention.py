@@ -20,6 +20,7 @@ from tests.helpers import assert_close, dev_csr, dev_feat, host
 pytestmark = pytest.mark.gpu
 
 CSR_ONLY = 1_000_001  # threshold above 100%: no dense tile, every edge on the edge kernels
+SWEEP = (0, 10_000, 50_000, CSR_ONLY)  # every non-empty tile dense, 1%, 5%, none
 
 
 def say(*a):
@@ -57,7 +58,20 @@ def run_case(gt, rowptr, col, H, d, dtype, taus=(CSR_ONLY,), T=128, seed=0, bwd=
 @pytest.mark.parametrize("H,d", [(1, 64), (2, 32), (4, 32), (8, 32), (8, 64), (16, 32), (16, 64), (1, 32)])
 def test_small_graph_all_shapes(gt, dtype, H, d):
     g = make_workload("c1", 0.1).graph
-    run_case(gt, g.rowptr, g.col, H, d, dtype, seed=H * 100 + d)
+    run_case(gt, g.rowptr, g.col, H, d, dtype, taus=SWEEP, seed=H * 100 + d)
+
+
+@pytest.mark.parametrize("T", [64, 128])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tile_sizes_on_clustered_graph(gt, T, dtype):
+    # a block-model graph in planted order: diagonal tiles well above 5%
+    w = make_workload("c5", 0.03)
+    g = w.graph
+    order = np.lexsort((np.arange(g.n), g.block))
+    inv = np.empty(g.n, np.int64)
+    inv[order] = np.arange(g.n)
+    rp, cl = OP.permute_csr(g.rowptr, g.col, order, inv)
+    run_case(gt, rp, cl, 4, 64, dtype, taus=SWEEP, T=T, seed=T)
 
 
 def test_c1_full_fp32_forward(gt):
@@ -75,7 +89,7 @@ def test_c1_full_fp32_forward(gt):
 @pytest.mark.parametrize("name,scale", [("c2", 0.02), ("c3", 0.01), ("c4", 0.005), ("c5", 0.05)])
 def test_workload_shapes_bf16(gt, name, scale):
     w = make_workload(name, scale)
-    run_case(gt, w.graph.rowptr, w.graph.col, w.heads, w.dim, w.dtype, seed=w.seed)
+    run_case(gt, w.graph.rowptr, w.graph.col, w.heads, w.dim, w.dtype, taus=(10_000, CSR_ONLY), seed=w.seed)
 
 
 def test_empty_rows_single_node_and_ragged(gt):
@@ -84,9 +98,10 @@ def test_empty_rows_single_node_and_ragged(gt):
     v = np.array([1, 2, 4, 6, 7, 9, 101, 0, 129])
     rowptr, col = csr_from_pairs(131, u, v, symmetric=False, self_loops=False)
     for dtype in ("f32", "bf16"):
-        run_case(gt, rowptr, col, 4, 32, dtype, seed=3)
+        for T in (64, 128):
+            run_case(gt, rowptr, col, 4, 32, dtype, taus=SWEEP, T=T, seed=3)
     rowptr, col = csr_from_pairs(1, [], [])
-    run_case(gt, rowptr, col, 8, 64, "bf16", seed=4)
+    run_case(gt, rowptr, col, 8, 64, "bf16", taus=SWEEP, seed=4)
 
 
 def test_long_rows_and_columns(gt):
@@ -103,7 +118,7 @@ def test_long_rows_and_columns(gt):
     uu, vv = np.nonzero(dense)
     rowptr, col = csr_from_pairs(n, uu, vv, symmetric=False, self_loops=False)
     for dtype, H, d in (("f32", 2, 64), ("bf16", 8, 32), ("bf16", 16, 64)):
-        run_case(gt, rowptr, col, H, d, dtype, seed=H + d)
+        run_case(gt, rowptr, col, H, d, dtype, taus=(0, 5000, CSR_ONLY), seed=H + d)
 
 
 def test_bitwise_deterministic(gt):
@@ -111,7 +126,8 @@ def test_bitwise_deterministic(gt):
     g = w.graph
     q, k, v, do = w.tensors()
     rp, cl = dev_csr(g.rowptr, g.col)
-    plan = gt.build_tiles(rp, cl, 128, CSR_ONLY)
+    plan = gt.build_tiles(rp, cl, 128, 10_000)
+    assert plan.n_dense > 0
     Q, K, V, dO = (dev_feat(x, "bf16") for x in (q, k, v, do))
     outs = []
     for _ in range(2):
@@ -131,7 +147,8 @@ def test_pipeline_reorder_then_attention_is_equivariant(gt):
     rp, cl = dev_csr(g.rowptr, g.col)
     perm, iperm, _ = gt.reorder(rp, cl)
     rp2, cl2 = gt.permute_csr(rp, cl, perm, iperm)
-    plan = gt.build_tiles(rp2, cl2, 128, CSR_ONLY)
+    plan = gt.build_tiles(rp2, cl2, 128, 10_000)
+    assert plan.n_dense > 0
     Q, K, V, dO = (gt.gather_rows(dev_feat(x, "bf16"), perm) for x in (q, k, v, do))
     O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
     dQ, dK, dV = gt.sparse_attn_bwd(plan, Q, K, V, O, dO, L, scale)
