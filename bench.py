@@ -48,6 +48,7 @@ def parse():
     ap.add_argument("--tile", type=int, default=128)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense-layer", action="store_true", help="skip the full-attention layer measurement")
     return ap.parse_args()
 
 
@@ -90,6 +91,47 @@ def cpu_baseline(w, target_s):
         "kind": "oracle",
         "sample": f"{rows} random rows (their {int(deg.sum())} edges x {w.heads} heads): fp64 forward of the rows, "
                   f"dQ of the rows, dK/dV of the same node ids as columns; {dt:.1f} s",
+    }
+
+
+def dense_layer(steps: int):
+    """Time the interleaved full-attention layer (65,536 nodes x 8 heads x 64, bf16) fwd and bwd."""
+    import torch
+
+    from paper_2407_14106_amd import gt
+    from synth.tensors import normal_tensor
+
+    n, H, d = 65536, 8, 64
+    dev = torch.device("cuda:0")
+    Q, K, V, dO = (torch.from_numpy(normal_tensor((n, H, d), (1005, 10 + t), "f32")).to(dev).to(torch.bfloat16)
+                   for t in range(4))
+    scale = 1.0 / math.sqrt(d)
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    for _ in range(2):
+        O, L = gt.dense_attn_fwd(Q, K, V, scale)
+        gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
+    torch.cuda.synchronize()
+    fw, bw = [], []
+    for _ in range(steps):
+        a, b, c = ev(), ev(), ev()
+        a.record()
+        O, L = gt.dense_attn_fwd(Q, K, V, scale)
+        b.record()
+        gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
+        c.record()
+        torch.cuda.synchronize()
+        fw.append(a.elapsed_time(b))
+        bw.append(b.elapsed_time(c))
+    f_ms, b_ms = float(np.mean(fw)), float(np.mean(bw))
+    flops_f = 4.0 * n * n * d * H
+    flops_b = 10.0 * n * n * d * H
+    return {
+        "workload": "full softmax attention, 65,536 nodes x 8 heads x 64, bf16",
+        "fwd_ms": round(f_ms, 3), "bwd_ms": round(b_ms, 3),
+        "fwd_TFLOPs": round(flops_f / f_ms / 1e9, 1), "bwd_TFLOPs": round(flops_b / b_ms / 1e9, 1),
+        "fwd_mfma_frac": round(flops_f / f_ms / 1e9 / 2500.0, 4),
+        "bwd_mfma_frac": round(flops_b / b_ms / 1e9 / 2500.0, 4),
+        "flops_note": "algorithmic: 4 n^2 d H forward, 10 n^2 d H backward; peak bf16 dense MFMA 2.5 PFLOP/s",
     }
 
 
@@ -230,6 +272,9 @@ def main():
         "preprocess": pre,
         "wall_s_timed": round(t_wall, 3),
     }
+    if not args.no_dense_layer:
+        log("timing the full-attention layer ...")
+        result["dense_layer"] = dense_layer(5)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle sample ...")
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

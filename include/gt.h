@@ -211,7 +211,8 @@ gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, int32_t d, gt
 /* ------------------------------------------------------------------------ */
 /* Full softmax attention, §2.1 Eq. (1) (the interleaved dense layer of §3.2).*/
 /* ------------------------------------------------------------------------ */
-/* Same formulas with N(i) = all n nodes.  GT_BF16 only; d in {32, 64}. */
+/* Same formulas with N(i) = all n nodes; same dtype / d / H support as the
+ * sparse calls.  No n x n buffer is formed. */
 gt_status gt_dense_attn_fwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
                             const void* V, float scale, void* O, float* LSE, hipStream_t stream);
 size_t gt_dense_attn_bwd_workspace_size(int64_t n, int32_t H, int32_t d, gt_dtype dtype);

@@ -160,6 +160,31 @@ __device__ __forceinline__ f32x16_t prod_acc(f32x16_t acc, const T* trow, int co
     return acc;
 }
 
+// As prod_acc, but the bf16 B operand is split into hi + lo parts (two
+// products), so P keeps about 16 mantissa bits: used where a column sums many
+// large probabilities (a hub attended by many low-degree rows).
+template <typename T>
+__device__ __forceinline__ f32x16_t prod_acc_split(f32x16_t acc, const T* trow, int col0, const f32x16_t& p, int lane) {
+    if constexpr (Mma<T>::kBf16) {
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const bf16x8_t a = Mma<T>::perm8(trow, col0 + 16 * half, lane);
+            bf16x8_t hi, lo;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                hi[t] = (__bf16)p[8 * half + t];
+                lo[t] = (__bf16)(p[8 * half + t] - float(hi[t]));
+            }
+            acc = Mma<T>::mma(a, hi, acc);
+            acc = Mma<T>::mma(a, lo, acc);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc = Mma<T>::mma(trow[col0 + crow(i, lane)], p[i], acc);
+    }
+    return acc;
+}
+
 // ------------------------------------------------------------ LDS staging
 
 template <typename T, int D>
@@ -198,102 +223,135 @@ __device__ __forceinline__ void stage(T* rm, T* tr, const T* __restrict__ X, int
     }
 }
 
-// ------------------------------------------------------------------ forward
+// Validity bits of the 32 partners of block (J, kb) when every pair is an
+// edge (the full layer): all partners below n.
+__device__ __forceinline__ uint32_t full_word(int64_t first, int64_t n) {
+    const int64_t left = n - first;
+    return left >= 32 ? 0xFFFFFFFFu : (left <= 0 ? 0u : ((1u << left) - 1u));
+}
 
-template <typename T, int D, int H, int TT>
+// ------------------------------------------------------------------ forward
+// Grid (tile rows, heads).  kFull: every node attends to all n nodes (the
+// interleaved full layer) and the kernel writes O and LSE; otherwise it walks
+// the tile row's dense tiles and leaves (m, l, acc) partials.
+
+template <typename T, int D, int H, int TT, bool kFull>
 __global__ __launch_bounds__(2 * TT) void k_tile_fwd(int64_t n, const int64_t* __restrict__ tile_rowptr,
                                                       const int32_t* __restrict__ tile_col,
                                                       const uint32_t* __restrict__ tile_mask,
                                                       const T* __restrict__ Q, const T* __restrict__ K,
                                                       const T* __restrict__ V, float sl2, float* __restrict__ pm,
-                                                      float* __restrict__ pl, float* __restrict__ pacc) {
+                                                      float* __restrict__ pl, float* __restrict__ pacc,
+                                                      T* __restrict__ O, float* __restrict__ LSE) {
     constexpr int NT = 2 * TT;  // threads: one wavefront per 32 rows
     constexpr int KB = TT / 32;
     constexpr int W = TT / 32;  // mask words per tile row
     __shared__ __attribute__((aligned(16))) T sK[TT * Pad<T, D>::kRow];
     __shared__ __attribute__((aligned(16))) T sVt[D * PadT<T, TT>::kRow];
     const int I = blockIdx.x;
-    const int64_t t0 = tile_rowptr[I], t1 = tile_rowptr[I + 1];
-    if (t0 == t1) return;
+    const int h = blockIdx.y;
+    int64_t t0, t1;
+    if (kFull) {
+        t0 = 0;
+        t1 = gridDim.x;
+    } else {
+        t0 = tile_rowptr[I];
+        t1 = tile_rowptr[I + 1];
+        if (t0 == t1) return;
+    }
     const int lane = lane_id();
     const int wv = threadIdx.x / kWave;
     const int qlocal = 32 * wv + (lane & 31);
     const int64_t q = int64_t(I) * TT + qlocal;
     const bool qok = q < n;
-    for (int h = 0; h < H; ++h) {
-        RowFrag<T, D> qf;
-        qf.load(Q + (q * H + h) * D, qok, lane);
-        float m = kNegInf, l = 0.f;
-        f32x16_t acc[D / 32];
+    RowFrag<T, D> qf;
+    qf.load(Q + (q * H + h) * D, qok, lane);
+    float m = kNegInf, l = 0.f;
+    f32x16_t acc[D / 32];
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) acc[db] = zero16();
-        for (int64_t k = t0; k < t1; ++k) {
-            const int64_t kbase = int64_t(tile_col[k]) * TT;
-            __syncthreads();
-            stage<T, D, H, TT, NT>(sK, nullptr, K, kbase, n, h);
-            stage<T, D, H, TT, NT>(nullptr, sVt, V, kbase, n, h);
-            __syncthreads();
-            f32x16_t s[KB];
-            float mloc = kNegInf;
-            const uint32_t* mrow = tile_mask + (k * TT + qlocal) * W;
+    for (int db = 0; db < D / 32; ++db) acc[db] = zero16();
+    for (int64_t k = t0; k < t1; ++k) {
+        const int64_t kbase = (kFull ? k : int64_t(tile_col[k])) * TT;
+        __syncthreads();
+        stage<T, D, H, TT, NT>(sK, nullptr, K, kbase, n, h);
+        stage<T, D, H, TT, NT>(nullptr, sVt, V, kbase, n, h);
+        __syncthreads();
+        f32x16_t s[KB];
+        float mloc = kNegInf;
+        const uint32_t* mrow = tile_mask + (k * TT + qlocal) * W;
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb) {
-                s[kb] = prod_rows<T, D>(sK + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, qf, lane);
-                const uint32_t mw = mrow[kb];
+        for (int kb = 0; kb < KB; ++kb) {
+            s[kb] = prod_rows<T, D>(sK + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, qf, lane);
+            const uint32_t mw = kFull ? full_word(kbase + 32 * kb, n) : mrow[kb];
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float v = ((mw >> crow(i, lane)) & 1u) ? s[kb][i] * sl2 : kNegInf;
-                    s[kb][i] = v;
-                    mloc = fmaxf(mloc, v);
-                }
-            }
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
-            const float mnew = fmaxf(m, mloc);
-            const float alpha = mnew == kNegInf ? 1.f : ex2(m - mnew);
-            float lsum = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float p = s[kb][i] == kNegInf ? 0.f : ex2(s[kb][i] - mnew);
-                    s[kb][i] = p;
-                    lsum += p;
-                }
-            lsum += __shfl_xor(lsum, 32, kWave);
-            l = l * alpha + lsum;
-            m = mnew;
-#pragma unroll
-            for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-                for (int i = 0; i < 16; ++i) acc[db][i] *= alpha;
-                const T* trow = sVt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
-#pragma unroll
-                for (int kb = 0; kb < KB; ++kb) acc[db] = prod_acc<T>(acc[db], trow, 32 * kb, s[kb], lane);
+            for (int i = 0; i < 16; ++i) {
+                const float v = ((mw >> crow(i, lane)) & 1u) ? s[kb][i] * sl2 : kNegInf;
+                s[kb][i] = v;
+                mloc = fmaxf(mloc, v);
             }
         }
-        if (qok) {
-            if (lane < 32) {
-                pm[q * H + h] = m;
-                pl[q * H + h] = l;
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
+        const float mnew = fmaxf(m, mloc);
+        const float alpha = mnew == kNegInf ? 1.f : ex2(m - mnew);
+        float lsum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float p = s[kb][i] == kNegInf ? 0.f : ex2(s[kb][i] - mnew);
+                s[kb][i] = p;
+                lsum += p;
             }
+        lsum += __shfl_xor(lsum, 32, kWave);
+        l = l * alpha + lsum;
+        m = mnew;
 #pragma unroll
-            for (int db = 0; db < D / 32; ++db)
+        for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) pacc[(q * H + h) * D + 32 * db + crow(i, lane)] = acc[db][i];
+            for (int i = 0; i < 16; ++i) acc[db][i] *= alpha;
+            const T* trow = sVt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) acc[db] = prod_acc<T>(acc[db], trow, 32 * kb, s[kb], lane);
         }
+    }
+    if (!qok) return;
+    if (kFull) {
+        const float inv = l > 0.f ? 1.f / l : 0.f;
+        if (lane < 32) LSE[q * H + h] = l > 0.f ? (m + __log2f(l)) * kLn2 : kNegInf;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float v = acc[db][i] * inv;
+                const int64_t o = (q * H + h) * D + 32 * db + crow(i, lane);
+                if constexpr (Mma<T>::kBf16)
+                    O[o] = f32_to_bf16(v);
+                else
+                    O[o] = v;
+            }
+    } else {
+        if (lane < 32) {
+            pm[q * H + h] = m;
+            pl[q * H + h] = l;
+        }
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) pacc[(q * H + h) * D + 32 * db + crow(i, lane)] = acc[db][i];
     }
 }
 
 // ---------------------------------------------------------------- dQ (rows)
 
-template <typename T, int D, int H, int TT>
+template <typename T, int D, int H, int TT, bool kFull>
 __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __restrict__ tile_rowptr,
                                                      const int32_t* __restrict__ tile_col,
                                                      const uint32_t* __restrict__ tile_mask,
                                                      const T* __restrict__ Q, const T* __restrict__ K,
                                                      const T* __restrict__ V, const T* __restrict__ O,
                                                      const T* __restrict__ dO, const float* __restrict__ LSE,
-                                                     float* __restrict__ Dv, float sl2, float* __restrict__ pdq) {
+                                                     float* __restrict__ Dv, float sl2, float* __restrict__ pdq,
+                                                     T* __restrict__ dQ, float scale) {
     constexpr int NT = 2 * TT;
     constexpr int KB = TT / 32;
     constexpr int W = TT / 32;
@@ -301,70 +359,85 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
     __shared__ __attribute__((aligned(16))) T sV[TT * Pad<T, D>::kRow];
     __shared__ __attribute__((aligned(16))) T sKt[D * PadT<T, TT>::kRow];
     const int I = blockIdx.x;
-    const int64_t t0 = tile_rowptr[I], t1 = tile_rowptr[I + 1];
-    if (t0 == t1) return;
+    const int h = blockIdx.y;
+    int64_t t0, t1;
+    if (kFull) {
+        t0 = 0;
+        t1 = gridDim.x;
+    } else {
+        t0 = tile_rowptr[I];
+        t1 = tile_rowptr[I + 1];
+        if (t0 == t1) return;
+    }
     const int lane = lane_id();
     const int wv = threadIdx.x / kWave;
     const int qlocal = 32 * wv + (lane & 31);
     const int64_t q = int64_t(I) * TT + qlocal;
     const bool qok = q < n;
-    for (int h = 0; h < H; ++h) {
-        RowFrag<T, D> qf, gf, of;
-        qf.load(Q + (q * H + h) * D, qok, lane);
-        gf.load(dO + (q * H + h) * D, qok, lane);
-        of.load(O + (q * H + h) * D, qok, lane);
-        float Dq = gf.dot(of);
-        Dq += __shfl_xor(Dq, 32, kWave);
-        if (qok && lane < 32) Dv[q * H + h] = Dq;
-        const float lse2 = qok ? LSE[q * H + h] * kLog2e : 0.f;
-        f32x16_t acc[D / 32];
+    RowFrag<T, D> qf, gf, of;
+    qf.load(Q + (q * H + h) * D, qok, lane);
+    gf.load(dO + (q * H + h) * D, qok, lane);
+    of.load(O + (q * H + h) * D, qok, lane);
+    float Dq = gf.dot(of);
+    Dq += __shfl_xor(Dq, 32, kWave);
+    if (qok && lane < 32) Dv[q * H + h] = Dq;
+    const float lse2 = qok ? LSE[q * H + h] * kLog2e : 0.f;
+    f32x16_t acc[D / 32];
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) acc[db] = zero16();
-        for (int64_t k = t0; k < t1; ++k) {
-            const int64_t kbase = int64_t(tile_col[k]) * TT;
-            __syncthreads();
-            stage<T, D, H, TT, NT>(sK, sKt, K, kbase, n, h);
-            stage<T, D, H, TT, NT>(sV, nullptr, V, kbase, n, h);
-            __syncthreads();
-            const uint32_t* mrow = tile_mask + (k * TT + qlocal) * W;
+    for (int db = 0; db < D / 32; ++db) acc[db] = zero16();
+    for (int64_t k = t0; k < t1; ++k) {
+        const int64_t kbase = (kFull ? k : int64_t(tile_col[k])) * TT;
+        __syncthreads();
+        stage<T, D, H, TT, NT>(sK, sKt, K, kbase, n, h);
+        stage<T, D, H, TT, NT>(sV, nullptr, V, kbase, n, h);
+        __syncthreads();
+        const uint32_t* mrow = tile_mask + (k * TT + qlocal) * W;
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb) {
-                f32x16_t s = prod_rows<T, D>(sK + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, qf, lane);
-                const f32x16_t dp = prod_rows<T, D>(sV + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, gf, lane);
-                const uint32_t mw = mrow[kb];
+        for (int kb = 0; kb < KB; ++kb) {
+            f32x16_t s = prod_rows<T, D>(sK + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, qf, lane);
+            const f32x16_t dp = prod_rows<T, D>(sV + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, gf, lane);
+            const uint32_t mw = kFull ? (qok ? full_word(kbase + 32 * kb, n) : 0u) : mrow[kb];
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float p = ((mw >> crow(i, lane)) & 1u) ? ex2(s[i] * sl2 - lse2) : 0.f;
-                    s[i] = p * (dp[i] - Dq);
-                }
+            for (int i = 0; i < 16; ++i) {
+                const float p = ((mw >> crow(i, lane)) & 1u) ? ex2(s[i] * sl2 - lse2) : 0.f;
+                s[i] = p * (dp[i] - Dq);
+            }
 #pragma unroll
-                for (int db = 0; db < D / 32; ++db) {
-                    const T* trow = sKt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
-                    acc[db] = prod_acc<T>(acc[db], trow, 32 * kb, s, lane);
-                }
+            for (int db = 0; db < D / 32; ++db) {
+                const T* trow = sKt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
+                acc[db] = prod_acc<T>(acc[db], trow, 32 * kb, s, lane);
             }
         }
-        if (qok) {
-#pragma unroll
-            for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) pdq[(q * H + h) * D + 32 * db + crow(i, lane)] = acc[db][i];
-        }
     }
+    if (!qok) return;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int64_t o = (q * H + h) * D + 32 * db + crow(i, lane);
+            if (kFull) {
+                if constexpr (Mma<T>::kBf16)
+                    dQ[o] = f32_to_bf16(acc[db][i] * scale);
+                else
+                    dQ[o] = acc[db][i] * scale;
+            } else {
+                pdq[o] = acc[db][i];
+            }
+        }
 }
 
 // ----------------------------------------------------------- dK, dV (cols)
 
-template <typename T, int D, int H, int TT>
+template <typename T, int D, int H, int TT, bool kFull, bool kSplit>
 __global__ __launch_bounds__(2 * TT) void k_tile_dkdv(int64_t n, const int64_t* __restrict__ tileT_ptr,
                                                        const int32_t* __restrict__ tileT_idx,
                                                        const int64_t* __restrict__ tile_rowptr,
-                                                       const int32_t* __restrict__ tile_col,
                                                        const uint32_t* __restrict__ tile_mask,
                                                        const T* __restrict__ Q, const T* __restrict__ K,
                                                        const T* __restrict__ V, const T* __restrict__ dO,
                                                        const float* __restrict__ LSE, const float* __restrict__ Dv,
-                                                       float sl2, float* __restrict__ pdk, float* __restrict__ pdv) {
+                                                       float sl2, float* __restrict__ pdk, float* __restrict__ pdv,
+                                                       T* __restrict__ dK, T* __restrict__ dV, float scale) {
     constexpr int NT = 2 * TT;
     constexpr int QB = TT / 32;
     constexpr int W = TT / 32;
@@ -374,102 +447,128 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dkdv(int64_t n, const int64_t* 
     __shared__ __attribute__((aligned(16))) T sGt[D * PadT<T, TT>::kRow];
     __shared__ float sL[TT];
     __shared__ float sD[TT];
-    __shared__ uint32_t sM[TT * W];
+    __shared__ uint32_t sM[kFull ? 1 : TT * W];
     const int J = blockIdx.x;
-    const int64_t u0 = tileT_ptr[J], u1 = tileT_ptr[J + 1];
-    if (u0 == u1) return;
-    (void)tile_rowptr;
+    const int h = blockIdx.y;
+    int64_t u0, u1;
+    if (kFull) {
+        u0 = 0;
+        u1 = gridDim.x;
+    } else {
+        u0 = tileT_ptr[J];
+        u1 = tileT_ptr[J + 1];
+        if (u0 == u1) return;
+    }
     const int lane = lane_id();
     const int wv = threadIdx.x / kWave;
     const int klocal = 32 * wv + (lane & 31);
     const int64_t key = int64_t(J) * TT + klocal;
     const bool kok = key < n;
-    for (int h = 0; h < H; ++h) {
-        RowFrag<T, D> kf, vf;
-        kf.load(K + (key * H + h) * D, kok, lane);
-        vf.load(V + (key * H + h) * D, kok, lane);
-        f32x16_t dk[D / 32], dv[D / 32];
+    RowFrag<T, D> kf, vf;
+    kf.load(K + (key * H + h) * D, kok, lane);
+    vf.load(V + (key * H + h) * D, kok, lane);
+    f32x16_t dk[D / 32], dv[D / 32];
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) dk[db] = dv[db] = zero16();
-        for (int64_t u = u0; u < u1; ++u) {
-            const int64_t k = tileT_idx[u];
-            // tile row I of tile k: the tile's position in the (I, J) order gives I by search
+    for (int db = 0; db < D / 32; ++db) dk[db] = dv[db] = zero16();
+    for (int64_t u = u0; u < u1; ++u) {
+        int64_t I, k = 0;
+        if (kFull) {
+            I = u;
+        } else {
+            k = tileT_idx[u];
+            // tile row of tile k: the last I with tile_rowptr[I] <= k
             int64_t lo = 0, hi = int64_t(gridDim.x);
             while (hi - lo > 1) {
                 const int64_t mid = (lo + hi) >> 1;
                 if (tile_rowptr[mid] <= k) lo = mid;
                 else hi = mid;
             }
-            const int64_t qbase = lo * TT;
-            __syncthreads();
-            stage<T, D, H, TT, NT>(sQ, sQt, Q, qbase, n, h);
-            stage<T, D, H, TT, NT>(sG, sGt, dO, qbase, n, h);
-            for (int r = threadIdx.x; r < TT; r += NT) {
-                const int64_t qn = qbase + r;
-                sL[r] = qn < n ? LSE[qn * H + h] * kLog2e : 0.f;
-                sD[r] = qn < n ? Dv[qn * H + h] : 0.f;
-            }
+            I = lo;
+        }
+        const int64_t qbase = I * TT;
+        __syncthreads();
+        stage<T, D, H, TT, NT>(sQ, sQt, Q, qbase, n, h);
+        stage<T, D, H, TT, NT>(sG, sGt, dO, qbase, n, h);
+        for (int r = threadIdx.x; r < TT; r += NT) {
+            const int64_t qn = qbase + r;
+            sL[r] = qn < n ? LSE[qn * H + h] * kLog2e : 0.f;
+            sD[r] = qn < n ? Dv[qn * H + h] : 0.f;
+        }
+        if (!kFull)
             for (int w = threadIdx.x; w < TT * W; w += NT) sM[w] = tile_mask[k * TT * W + w];
-            __syncthreads();
+        __syncthreads();
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-                f32x16_t s = prod_rows<T, D>(sQ + 32 * qb * Pad<T, D>::kRow, Pad<T, D>::kRow, kf, lane);
-                const f32x16_t dp = prod_rows<T, D>(sG + 32 * qb * Pad<T, D>::kRow, Pad<T, D>::kRow, vf, lane);
-                f32x16_t p;
+        for (int qb = 0; qb < QB; ++qb) {
+            f32x16_t s = prod_rows<T, D>(sQ + 32 * qb * Pad<T, D>::kRow, Pad<T, D>::kRow, kf, lane);
+            const f32x16_t dp = prod_rows<T, D>(sG + 32 * qb * Pad<T, D>::kRow, Pad<T, D>::kRow, vf, lane);
+            f32x16_t p;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int r = 32 * qb + crow(i, lane);
-                    const bool on = (sM[r * W + wv] >> (lane & 31)) & 1u;
-                    const float pv = on ? ex2(s[i] * sl2 - sL[r]) : 0.f;
-                    p[i] = pv;
-                    s[i] = pv * (dp[i] - sD[r]);
-                }
+            for (int i = 0; i < 16; ++i) {
+                const int r = 32 * qb + crow(i, lane);
+                const bool on = kFull ? (qbase + r < n) : ((sM[r * W + wv] >> (lane & 31)) & 1u);
+                const float pv = on ? ex2(s[i] * sl2 - sL[r]) : 0.f;
+                p[i] = pv;
+                s[i] = pv * (dp[i] - sD[r]);
+            }
 #pragma unroll
-                for (int db = 0; db < D / 32; ++db) {
-                    const T* grow = sGt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
-                    const T* qrow = sQt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
+            for (int db = 0; db < D / 32; ++db) {
+                const T* grow = sGt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
+                const T* qrow = sQt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
+                if (kSplit) {
+                    dv[db] = prod_acc_split<T>(dv[db], grow, 32 * qb, p, lane);
+                    dk[db] = prod_acc_split<T>(dk[db], qrow, 32 * qb, s, lane);
+                } else {
                     dv[db] = prod_acc<T>(dv[db], grow, 32 * qb, p, lane);
                     dk[db] = prod_acc<T>(dk[db], qrow, 32 * qb, s, lane);
                 }
             }
         }
-        if (kok) {
-#pragma unroll
-            for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int64_t o = (key * H + h) * D + 32 * db + crow(i, lane);
-                    pdk[o] = dk[db][i];
-                    pdv[o] = dv[db][i];
-                }
-        }
     }
+    if (!kok) return;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int64_t o = (key * H + h) * D + 32 * db + crow(i, lane);
+            if (kFull) {
+                if constexpr (Mma<T>::kBf16) {
+                    dK[o] = f32_to_bf16(dk[db][i] * scale);
+                    dV[o] = f32_to_bf16(dv[db][i]);
+                } else {
+                    dK[o] = dk[db][i] * scale;
+                    dV[o] = dv[db][i];
+                }
+            } else {
+                pdk[o] = dk[db][i];
+                pdv[o] = dv[db][i];
+            }
+        }
 }
 
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
 
-#define GT_TILE_SWITCH(T_, CALL)                                          \
-    do {                                                                  \
-        if ((T_) == 128) {                                                \
-            constexpr int TT = 128;                                       \
-            CALL;                                                         \
-        } else if ((T_) == 64) {                                          \
-            constexpr int TT = 64;                                        \
-            CALL;                                                         \
-        } else {                                                          \
+#define GT_TILE_SWITCH(T_, CALL)                                                 \
+    do {                                                                         \
+        if ((T_) == 128) {                                                       \
+            constexpr int TT = 128;                                              \
+            CALL;                                                                \
+        } else if ((T_) == 64) {                                                 \
+            constexpr int TT = 64;                                               \
+            CALL;                                                                \
+        } else {                                                                 \
             return fail(GT_ERR_UNSUPPORTED, "dense tiles: T must be 64 or 128"); \
-        }                                                                 \
+        }                                                                        \
     } while (0)
 
 template <typename T, int D, int H>
 gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float sl2, TilePartials tp,
                    hipStream_t s) {
-    const unsigned R = unsigned(p->n_row_tiles);
-    GT_TILE_SWITCH(p->T, (k_tile_fwd<T, D, H, TT><<<R, 2 * TT, 0, s>>>(p->n, p->tile_rowptr, p->tile_col,
-                                                                          p->tile_mask, Q, K, V, sl2, tp.m, tp.l,
-                                                                          tp.acc)));
+    const dim3 grid(unsigned(p->n_row_tiles), H);
+    GT_TILE_SWITCH(p->T, (k_tile_fwd<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
+                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc,
+                             nullptr, nullptr)));
     GT_LAUNCH_CHECK("tile_fwd");
     return GT_OK;
 }
@@ -477,10 +576,10 @@ gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float 
 template <typename T, int D, int H>
 gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* O, const T* dO,
                       const float* LSE, float* Dv, float sl2, TilePartials dq, hipStream_t s) {
-    const unsigned R = unsigned(p->n_row_tiles);
-    GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT><<<R, 2 * TT, 0, s>>>(p->n, p->tile_rowptr, p->tile_col,
-                                                                         p->tile_mask, Q, K, V, O, dO, LSE, Dv, sl2,
-                                                                         dq.acc)));
+    const dim3 grid(unsigned(p->n_row_tiles), H);
+    GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
+                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, O, dO, LSE, Dv, sl2, dq.acc,
+                             nullptr, 1.f)));
     GT_LAUNCH_CHECK("tile_bwd_dq");
     return GT_OK;
 }
@@ -488,11 +587,36 @@ gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, con
 template <typename T, int D, int H>
 gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
                         const float* Dv, float sl2, TilePartials dk, TilePartials dv, hipStream_t s) {
-    const unsigned R = unsigned(p->n_row_tiles);
-    GT_TILE_SWITCH(p->T, (k_tile_dkdv<T, D, H, TT><<<R, 2 * TT, 0, s>>>(
-                             p->n, p->tileT_ptr, p->tileT_idx, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
-                             dO, LSE, Dv, sl2, dk.acc, dv.acc)));
+    const dim3 grid(unsigned(p->n_row_tiles), H);
+    GT_TILE_SWITCH(p->T, (k_tile_dkdv<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
+                             p->n, p->tileT_ptr, p->tileT_idx, p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv,
+                             sl2, dk.acc, dv.acc, nullptr, nullptr, 1.f)));
     GT_LAUNCH_CHECK("tile_bwd_dkdv");
+    return GT_OK;
+}
+
+// The full layer: 128-node blocks, every pair attended.
+template <typename T, int D, int H>
+gt_status full_fwd(int64_t n, const T* Q, const T* K, const T* V, float sl2, T* O, float* LSE, hipStream_t s) {
+    constexpr int TT = 128;
+    const dim3 grid(unsigned(cdiv(n, TT)), H);
+    k_tile_fwd<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, sl2, nullptr,
+                                                          nullptr, nullptr, O, LSE);
+    GT_LAUNCH_CHECK("full_fwd");
+    return GT_OK;
+}
+
+template <typename T, int D, int H>
+gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, const T* dO, const float* LSE,
+                   float sl2, float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s) {
+    constexpr int TT = 128;
+    const dim3 grid(unsigned(cdiv(n, TT)), H);
+    k_tile_dq<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, O, dO, LSE, Dv,
+                                                         sl2, nullptr, dQ, scale);
+    GT_LAUNCH_CHECK("full_bwd_dq");
+    k_tile_dkdv<T, D, H, TT, true, false><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, nullptr, Q, K, V,
+                                                                  dO, LSE, Dv, sl2, nullptr, nullptr, dK, dV, scale);
+    GT_LAUNCH_CHECK("full_bwd_dkdv");
     return GT_OK;
 }
 
@@ -503,7 +627,10 @@ gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, c
                                             const float*, float*, float, TilePartials, hipStream_t);              \
     template gt_status tile_bwd_dkdv<T, D, H>(const gt_tiles*, const T*, const T*, const T*, const T*,            \
                                               const float*, const float*, float, TilePartials, TilePartials,      \
-                                              hipStream_t);
+                                              hipStream_t);                                                       \
+    template gt_status full_fwd<T, D, H>(int64_t, const T*, const T*, const T*, float, T*, float*, hipStream_t); \
+    template gt_status full_bwd<T, D, H>(int64_t, const T*, const T*, const T*, const T*, const T*, const float*, \
+                                         float, float, T*, T*, T*, float*, hipStream_t);
 #define GT_INST_H(T, D) GT_INST(T, D, 1) GT_INST(T, D, 2) GT_INST(T, D, 4) GT_INST(T, D, 8) GT_INST(T, D, 16)
 GT_INST_H(uint16_t, 32)
 GT_INST_H(uint16_t, 64)
