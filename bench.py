@@ -59,7 +59,7 @@ def algorithmic_bytes(n, nnz, H, d, b):
     stat = 4 * n * H
     return {
         "fwd": csr + 3 * row + row + stat,                      # Q,K,V in; O, LSE out
-        "bwd_rows": csr + 5 * row + stat + row + stat,          # Q,K,V,O,dO,LSE in; dQ, Dstat out
+        "bwd_rows": csr + 4 * row + stat + row + stat,          # Q,K,V,dO,LSE in; dQ, Dstat out
         "bwd_cols": csr + 4 * row + 2 * stat + 2 * row,         # Q,K,V,dO,LSE,Dstat in; dK, dV out
     }
 
@@ -109,7 +109,7 @@ def dense_layer(steps: int):
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     for _ in range(2):
         O, L = gt.dense_attn_fwd(Q, K, V, scale)
-        gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
+        gt.dense_attn_bwd(Q, K, V, dO, L, scale)
     torch.cuda.synchronize()
     fw, bw = [], []
     for _ in range(steps):
@@ -117,7 +117,7 @@ def dense_layer(steps: int):
         a.record()
         O, L = gt.dense_attn_fwd(Q, K, V, scale)
         b.record()
-        gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
+        gt.dense_attn_bwd(Q, K, V, dO, L, scale)
         c.record()
         torch.cuda.synchronize()
         fw.append(a.elapsed_time(b))
@@ -195,7 +195,7 @@ def main():
         O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
         if events:
             events[1].record()
-        dQ, Dst = gt.sparse_attn_bwd_rows(plan, Q, K, V, O, dO, L, scale)
+        dQ, Dst = gt.sparse_attn_bwd_rows(plan, Q, K, V, dO, L, scale)
         if events:
             events[2].record()
         dK, dV = gt.sparse_attn_bwd_cols(plan, Q, K, V, dO, L, Dst, scale)

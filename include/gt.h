@@ -183,26 +183,28 @@ gt_status gt_sparse_attn_fwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtyp
                              const void* K, const void* V, float scale, void* O, float* LSE, void* ws,
                              size_t ws_bytes, hipStream_t stream);
 
-/* Backward for an upstream gradient dO, given O and LSE of the forward:
- *   D_i = <dO_i, O_i>, P_ij = exp(s_ij - LSE_i), dS_ij = P_ij (<dO_i, V_j> - D_i),
+/* Backward for an upstream gradient dO, given LSE of the forward:
+ *   P_ij = exp(s_ij - LSE_i), dP_ij = <dO_i, V_j>, D_i = sum_j P_ij dP_ij,
+ *   dS_ij = P_ij (dP_ij - D_i),
  *   dQ_i = scale sum_j dS_ij K_j, dK_j = scale sum_i dS_ij Q_i, dV_j = sum_i P_ij dO_i.
+ * D_i equals <dO_i, O_i> for the exact output O; it is formed from the edges
+ * because the stored O is rounded to the feature dtype, so O is not an input.
  * dK and dV are gathered per column (no atomics): results are bitwise
  * reproducible for a fixed plan. */
 size_t gt_sparse_attn_bwd_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
 gt_status gt_sparse_attn_bwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
-                             const void* K, const void* V, const void* O, const void* dO, const float* LSE,
-                             float scale, void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes,
-                             hipStream_t stream);
+                             const void* K, const void* V, const void* dO, const float* LSE, float scale, void* dQ,
+                             void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* The backward in its two halves, for callers that schedule them apart (the
  * combined call above is rows then cols).
- * _rows: dQ (row-owned) and the row statistic Dstat[i, h] = <dO_i, O_i>
+ * _rows: dQ (row-owned) and the row statistic Dstat[i, h] = D_i
  *        (fp32 [n, H], written here, read by _cols).
  * _cols: dK and dV (column-owned), from Dstat of the _rows call. */
 size_t gt_sparse_attn_bwd_rows_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
 gt_status gt_sparse_attn_bwd_rows(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
-                                  const void* K, const void* V, const void* O, const void* dO, const float* LSE,
-                                  float scale, void* dQ, float* Dstat, void* ws, size_t ws_bytes, hipStream_t stream);
+                                  const void* K, const void* V, const void* dO, const float* LSE, float scale,
+                                  void* dQ, float* Dstat, void* ws, size_t ws_bytes, hipStream_t stream);
 size_t gt_sparse_attn_bwd_cols_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
 gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
                                   const void* K, const void* V, const void* dO, const float* LSE, const float* Dstat,
@@ -217,8 +219,8 @@ gt_status gt_dense_attn_fwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, con
                             const void* V, float scale, void* O, float* LSE, hipStream_t stream);
 size_t gt_dense_attn_bwd_workspace_size(int64_t n, int32_t H, int32_t d, gt_dtype dtype);
 gt_status gt_dense_attn_bwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
-                            const void* V, const void* O, const void* dO, const float* LSE, float scale, void* dQ,
-                            void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+                            const void* V, const void* dO, const float* LSE, float scale, void* dQ, void* dK,
+                            void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -209,12 +209,23 @@ __global__ __launch_bounds__(kThreads) void k_fwd_long(const int32_t* __restrict
 
 // ----------------------------------------------------------------- backward
 
-// Row pass: dQ_i = scale * sum_j dS_ij K_j
+// Row pass.  With D_i = sum_j P_ij dP_ij (which equals <dO_i, O_i> for the
+// exact output O; the stored O is rounded to the feature dtype, so D is formed
+// from the edges instead),
+//   dQ_i = scale * sum_j P_ij (dP_ij - D_i) K_j = scale * (A_i - D_i B_i),
+//   A_i = sum_j P_ij dP_ij K_j,  B_i = sum_j P_ij K_j,
+// so one pass over the row yields A, B and D together.
+template <int F>
+struct RowSums {
+    Acc<F> a, b;
+    float d = 0.f;
+};
+
 template <typename T, int D, int H>
-__device__ __forceinline__ void dq_step(Acc<EdgeCfg<T, D, H>::F>& dq, const Slice<T, EdgeCfg<T, D, H>::F>& q,
-                                        const Slice<T, EdgeCfg<T, D, H>::F>& g, float lse2, float Di,
-                                        const T* __restrict__ K, const T* __restrict__ V, int64_t j0, int64_t j1,
-                                        bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2) {
+__device__ __forceinline__ void dq_step(RowSums<EdgeCfg<T, D, H>::F>& rs, const Slice<T, EdgeCfg<T, D, H>::F>& q,
+                                        const Slice<T, EdgeCfg<T, D, H>::F>& g, float lse2, const T* __restrict__ K,
+                                        const T* __restrict__ V, int64_t j0, int64_t j1, bool ok0, bool ok1,
+                                        const Lanes<T, D, H>& ln, float sl2) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> k0, k1, v0, v1;
     k0.zero();
@@ -235,10 +246,15 @@ __device__ __forceinline__ void dq_step(Acc<EdgeCfg<T, D, H>::F>& dq, const Slic
     const float dp1 = group_sum<C::L>(g.dot(v1));
     const float p0 = ok0 ? exp2f(s0 - lse2) : 0.f;
     const float p1 = ok1 ? exp2f(s1 - lse2) : 0.f;
-    const float ds0 = p0 * (dp0 - Di);
-    const float ds1 = p1 * (dp1 - Di);
+    const float w0 = p0 * dp0;
+    const float w1 = p1 * dp1;
+    rs.d += w0 + w1;
 #pragma unroll
-    for (int f = 0; f < C::F; ++f) dq.v[f] = fmaf(ds1, k1.f(f), fmaf(ds0, k0.f(f), dq.v[f]));
+    for (int f = 0; f < C::F; ++f) {
+        const float x0 = k0.f(f), x1 = k1.f(f);
+        rs.a.v[f] = fmaf(w1, x1, fmaf(w0, x0, rs.a.v[f]));
+        rs.b.v[f] = fmaf(p1, x1, fmaf(p0, x0, rs.b.v[f]));
+    }
 }
 
 template <int F>
@@ -255,12 +271,21 @@ __device__ __forceinline__ void load_f32_slice(float (&dst)[F], const float* src
 }
 
 template <typename T, int D, int H>
+__device__ __forceinline__ void load_row_partial(RowSums<EdgeCfg<T, D, H>::F>& rs, const TilePartials& tp,
+                                                 int64_t node, int h, int64_t off) {
+    constexpr int F = EdgeCfg<T, D, H>::F;
+    load_f32_slice<F>(rs.a.v, tp.acc + off);
+    load_f32_slice<F>(rs.b.v, tp.acc2 + off);
+    rs.d = tp.m[node * H + h];
+}
+
+template <typename T, int D, int H>
 __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t* __restrict__ rp,
                                                        const int32_t* __restrict__ cl, const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V,
-                                                       const T* __restrict__ O, const T* __restrict__ dO,
-                                                       const float* __restrict__ LSE, float* __restrict__ Dv,
-                                                       float sl2, float scale, T* __restrict__ dQ, TilePartials tp) {
+                                                       const T* __restrict__ dO, const float* __restrict__ LSE,
+                                                       float* __restrict__ Dv, float sl2, float scale,
+                                                       T* __restrict__ dQ, TilePartials tp) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
     const int64_t wave = int64_t(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
@@ -278,25 +303,26 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
     Slice<T, C::F> q, g;
     q.zero();
     g.zero();
-    float lse2 = 0.f, Di = 0.f;
+    float lse2 = 0.f;
     if (live) {
-        Slice<T, C::F> o;
-        o.load(O + off);
         q.load(Q + off);
         g.load(dO + off);
         lse2 = LSE[i * H + ln.h] * kLog2e;
-        Di = group_sum<C::L>(o.dot(g));
-        if (deg >= 0 && ln.part == 0) Dv[i * H + ln.h] = Di;
     }
-    Acc<C::F> dq;
-    if (live && deg >= 0 && tp.has_row(i)) load_f32_slice<C::F>(dq.v, tp.acc + off);
+    RowSums<C::F> rs;
+    if (live && deg >= 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
     for (int t = 0; t < dmax; t += 2) {
         const bool ok0 = t < deg, ok1 = t + 1 < deg;
         const int64_t j0 = ok0 ? cl[a + t] : 0;
         const int64_t j1 = ok1 ? cl[a + t + 1] : 0;
-        dq_step<T, D, H>(dq, q, g, lse2, Di, K, V, j0, j1, ok0, ok1, ln, sl2);
+        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2);
     }
-    if (live && deg >= 0) store_slice<T, C::F>(dQ + off, dq.v, scale);
+    if (live && deg >= 0) {
+#pragma unroll
+        for (int f = 0; f < C::F; ++f) rs.a.v[f] = fmaf(-rs.d, rs.b.v[f], rs.a.v[f]);
+        store_slice<T, C::F>(dQ + off, rs.a.v, scale);
+        if (ln.part == 0) Dv[i * H + ln.h] = rs.d;
+    }
 }
 
 template <typename T, int D, int H>
@@ -304,44 +330,52 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows_long(const int32_t* __res
                                                             const int64_t* __restrict__ rp,
                                                             const int32_t* __restrict__ cl, const T* __restrict__ Q,
                                                             const T* __restrict__ K, const T* __restrict__ V,
-                                                            const T* __restrict__ O, const T* __restrict__ dO,
-                                                            const float* __restrict__ LSE, float* __restrict__ Dv,
-                                                            float sl2, float scale, T* __restrict__ dQ,
-                                                            TilePartials tp) {
+                                                            const T* __restrict__ dO, const float* __restrict__ LSE,
+                                                            float* __restrict__ Dv, float sl2, float scale,
+                                                            T* __restrict__ dQ, TilePartials tp) {
     using C = EdgeCfg<T, D, H>;
     constexpr int S = kThreads / C::G;
-    __shared__ float s_acc[S][H * D];
+    __shared__ float s_a[S][H * D];
+    __shared__ float s_b[S][H * D];
+    __shared__ float s_d[S][H];
     const Lanes<T, D, H> ln(threadIdx.x);
     const int64_t i = list[blockIdx.x];
     const int64_t a = rp[i];
     const int deg = int(rp[i + 1] - a);
     const int64_t off = ln.off(i);
-    Slice<T, C::F> q, g, o;
+    Slice<T, C::F> q, g;
     q.load(Q + off);
     g.load(dO + off);
-    o.load(O + off);
     const float lse2 = LSE[i * H + ln.h] * kLog2e;
-    const float Di = group_sum<C::L>(o.dot(g));
-    if (ln.slot == 0 && ln.part == 0) Dv[i * H + ln.h] = Di;
-    Acc<C::F> dq;
-    if (ln.slot == 0 && tp.has_row(i)) load_f32_slice<C::F>(dq.v, tp.acc + off);
+    RowSums<C::F> rs;
+    if (ln.slot == 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
     for (int t = ln.slot; t < deg; t += 2 * S) {
         const bool ok1 = t + S < deg;
         const int64_t j0 = cl[a + t];
         const int64_t j1 = ok1 ? cl[a + t + S] : 0;
-        dq_step<T, D, H>(dq, q, g, lse2, Di, K, V, j0, j1, true, ok1, ln, sl2);
+        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, true, ok1, ln, sl2);
     }
 #pragma unroll
-    for (int f = 0; f < C::F; ++f) s_acc[ln.slot][ln.h * D + ln.part * C::F + f] = dq.v[f];
+    for (int f = 0; f < C::F; ++f) {
+        s_a[ln.slot][ln.h * D + ln.part * C::F + f] = rs.a.v[f];
+        s_b[ln.slot][ln.h * D + ln.part * C::F + f] = rs.b.v[f];
+    }
+    if (ln.part == 0) s_d[ln.slot][ln.h] = rs.d;
     __syncthreads();
     for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
-        float acc = 0.f;
-        for (int s = 0; s < S; ++s) acc += s_acc[s][idx];
-        acc *= scale;
+        const int h = idx / D;
+        float sa = 0.f, sb = 0.f, sd = 0.f;
+        for (int s = 0; s < S; ++s) {
+            sa += s_a[s][idx];
+            sb += s_b[s][idx];
+            sd += s_d[s][h];
+        }
+        const float acc = fmaf(-sd, sb, sa) * scale;
         if (sizeof(T) == 2)
             reinterpret_cast<uint16_t*>(dQ)[i * H * D + idx] = f32_to_bf16(acc);
         else
             reinterpret_cast<float*>(dQ)[i * H * D + idx] = acc;
+        if (idx % D == 0) Dv[i * H + h] = sd;
     }
 }
 
@@ -527,9 +561,8 @@ gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V
 }
 
 template <typename T, int D, int H>
-gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* O,
-                       const void* dO, const float* LSE, float scale, void* dQ, float* Dv, void* ws_ptr,
-                       hipStream_t s) {
+gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
+                       const float* LSE, float scale, void* dQ, float* Dv, void* ws_ptr, hipStream_t s) {
     using C = EdgeCfg<T, D, H>;
     const int64_t n = p->n;
     if (n == 0) return GT_OK;
@@ -538,18 +571,18 @@ gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const vo
     TileBwdPartials tb = tile_partials_bwd(ws, p, H, D, true, false);
     const float sl2 = scale * kLog2e;
     const T *q = static_cast<const T*>(Q), *k = static_cast<const T*>(K), *v = static_cast<const T*>(V);
-    const T *o = static_cast<const T*>(O), *g = static_cast<const T*>(dO);
+    const T* g = static_cast<const T*>(dO);
     gt_status st;
     if (p->n_dense > 0) {
-        if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, o, g, LSE, Dv, sl2, tb.dq, s)) != GT_OK) return st;
+        if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, g, LSE, sl2, tb.dq, s)) != GT_OK) return st;
     }
     const unsigned grid = unsigned(cdiv(cdiv(n, C::NPW), kThreads / kWave));
-    k_bwd_rows<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, q, k, v, o, g, LSE, Dv, sl2, scale,
+    k_bwd_rows<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, Dv, sl2, scale,
                                                   static_cast<T*>(dQ), tb.dq);
     GT_LAUNCH_CHECK("sparse_bwd_rows");
     if (p->n_long_rows > 0) {
         k_bwd_rows_long<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
-            p->long_rows, p->sp_rowptr, p->sp_col, q, k, v, o, g, LSE, Dv, sl2, scale, static_cast<T*>(dQ), tb.dq);
+            p->long_rows, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, Dv, sl2, scale, static_cast<T*>(dQ), tb.dq);
         GT_LAUNCH_CHECK("sparse_bwd_rows_long");
     }
     return GT_OK;
@@ -586,13 +619,13 @@ gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const vo
 }
 
 template <typename T, int D, int H>
-gt_status run_bwd(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* O, const void* dO,
-                  const float* LSE, float scale, void* dQ, void* dK, void* dV, void* ws_ptr, hipStream_t s) {
+gt_status run_bwd(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO, const float* LSE,
+                  float scale, void* dQ, void* dK, void* dV, void* ws_ptr, hipStream_t s) {
     if (p->n == 0) return GT_OK;
     Ws ws(ws_ptr);
     float* Dv = ws.take<float>(size_t(p->n) * H);
     char* rest = ws.take<char>(1);
-    gt_status st = run_bwd_rows<T, D, H>(p, Q, K, V, O, dO, LSE, scale, dQ, Dv, rest, s);
+    gt_status st = run_bwd_rows<T, D, H>(p, Q, K, V, dO, LSE, scale, dQ, Dv, rest, s);
     if (st != GT_OK) return st;
     return run_bwd_cols<T, D, H>(p, Q, K, V, dO, LSE, Dv, scale, dK, dV, rest, s);
 }
@@ -668,17 +701,17 @@ extern "C" size_t gt_sparse_attn_bwd_rows_workspace_size(const gt_tiles* plan, i
 }
 
 extern "C" gt_status gt_sparse_attn_bwd_rows(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype,
-                                             const void* Q, const void* K, const void* V, const void* O,
-                                             const void* dO, const float* LSE, float scale, void* dQ, float* Dstat,
-                                             void* ws, size_t ws_bytes, hipStream_t stream) {
+                                             const void* Q, const void* K, const void* V, const void* dO,
+                                             const float* LSE, float scale, void* dQ, float* Dstat, void* ws,
+                                             size_t ws_bytes, hipStream_t stream) {
     gt_status st = check_plan("gt_sparse_attn_bwd_rows", plan);
     if (st != GT_OK) return st;
     if (!supported(H, d, dtype)) return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_bwd_rows: unsupported (H, d, dtype)");
-    if (plan->n > 0 && (!Q || !K || !V || !O || !dO || !LSE || !dQ || !Dstat || !ws))
+    if (plan->n > 0 && (!Q || !K || !V || !dO || !LSE || !dQ || !Dstat || !ws))
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_rows: null pointer");
     if (ws_bytes < bwd_part_ws(plan, H, d, true, false))
         return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_rows: workspace too small");
-    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_rows, plan, Q, K, V, O, dO, LSE, scale, dQ, Dstat, ws, stream);
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_rows, plan, Q, K, V, dO, LSE, scale, dQ, Dstat, ws, stream);
 }
 
 extern "C" size_t gt_sparse_attn_bwd_cols_workspace_size(const gt_tiles* plan, int32_t H, int32_t d,
@@ -702,14 +735,13 @@ extern "C" gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, in
 }
 
 extern "C" gt_status gt_sparse_attn_bwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
-                                        const void* K, const void* V, const void* O, const void* dO, const float* LSE,
-                                        float scale, void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes,
-                                        hipStream_t stream) {
+                                        const void* K, const void* V, const void* dO, const float* LSE, float scale,
+                                        void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream) {
     gt_status st = check_plan("gt_sparse_attn_bwd", plan);
     if (st != GT_OK) return st;
     if (!supported(H, d, dtype)) return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_bwd: unsupported (H, d, dtype)");
-    if (plan->n > 0 && (!Q || !K || !V || !O || !dO || !LSE || !dQ || !dK || !dV || !ws))
+    if (plan->n > 0 && (!Q || !K || !V || !dO || !LSE || !dQ || !dK || !dV || !ws))
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd: null pointer");
     if (ws_bytes < bwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd: workspace too small");
-    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, O, dO, LSE, scale, dQ, dK, dV, ws, stream);
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, dO, LSE, scale, dQ, dK, dV, ws, stream);
 }

@@ -13,9 +13,10 @@ namespace gt {
 struct TilePartials {
     const int64_t* ptr = nullptr;
     int tshift = 0;
-    float* m = nullptr;    // [n, H] running max (log2 domain), forward only
-    float* l = nullptr;    // [n, H] running sum, forward only
-    float* acc = nullptr;  // [n, H, d] unnormalised output / gradient sums
+    float* m = nullptr;     // [n, H] forward: running max (log2 domain); dQ: partial D sum
+    float* l = nullptr;     // [n, H] forward: running sum
+    float* acc = nullptr;   // [n, H, d] unnormalised output / gradient sums (dQ: A)
+    float* acc2 = nullptr;  // [n, H, d] dQ only: B
     __device__ __forceinline__ bool has(int64_t node) const {
         if (!ptr) return false;
         const int64_t I = node >> tshift;
@@ -50,6 +51,8 @@ inline TileBwdPartials tile_partials_bwd(Ws& ws, const gt_tiles* p, int H, int D
         b.dq.ptr = p->tile_rowptr;
         b.dq.tshift = tile_shift(p->T);
         b.dq.acc = ws.take<float>(size_t(p->n) * H * D);
+        b.dq.acc2 = ws.take<float>(size_t(p->n) * H * D);
+        b.dq.m = ws.take<float>(size_t(p->n) * H);
     }
     if (cols) {
         b.dk.ptr = b.dv.ptr = p->tileT_ptr;
@@ -67,11 +70,12 @@ gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float 
                    hipStream_t s);
 
 // Backward over the dense tiles, row-owned: for every node of a tile row with
-// dense tiles, writes D = <dO, O> into Dv and the dq sum over its dense-tile
-// edges (unscaled by `scale`; the edge kernels apply it when they finish).
+// dense tiles, the sums over its dense-tile edges of P dP K (acc), P K (acc2)
+// and P dP (m); the edge kernels add the remainder and form
+// dQ = scale (A - D B) with D the total P dP sum.
 template <typename T, int D, int H>
-gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* O, const T* dO,
-                      const float* LSE, float* Dv, float sl2, TilePartials dq, hipStream_t s);
+gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
+                      float sl2, TilePartials dq, hipStream_t s);
 
 // Backward over the dense tiles, column-owned: dk (unscaled) and dv sums over
 // the dense-tile edges of every node of a tile column with dense tiles.
@@ -80,11 +84,11 @@ gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, c
                         const float* Dv, float sl2, TilePartials dk, TilePartials dv, hipStream_t s);
 
 // The full softmax layer (every node attends to all n nodes) on the same
-// kernels: O and LSE, then dQ (and D into Dv), then dK and dV.
+// kernels: O and LSE; then dQ and D (into Dv); then dK and dV.
 template <typename T, int D, int H>
 gt_status full_fwd(int64_t n, const T* Q, const T* K, const T* V, float sl2, T* O, float* LSE, hipStream_t s);
 template <typename T, int D, int H>
-gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, const T* dO, const float* LSE,
-                   float sl2, float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s);
+gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* dO, const float* LSE, float sl2,
+                   float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s);
 
 }  // namespace gt

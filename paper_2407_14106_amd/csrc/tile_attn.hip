@@ -342,16 +342,20 @@ __global__ __launch_bounds__(2 * TT) void k_tile_fwd(int64_t n, const int64_t* _
 }
 
 // ---------------------------------------------------------------- dQ (rows)
+// dQ = scale (A - D B) with A = sum P dP K, B = sum P K and D = sum P dP over
+// the row's partners (D equals <dO, O> of the exact output).  The sparse
+// variant leaves A, B and the D sum as partials; kFull finishes dQ and writes D.
 
 template <typename T, int D, int H, int TT, bool kFull>
 __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __restrict__ tile_rowptr,
                                                      const int32_t* __restrict__ tile_col,
                                                      const uint32_t* __restrict__ tile_mask,
                                                      const T* __restrict__ Q, const T* __restrict__ K,
-                                                     const T* __restrict__ V, const T* __restrict__ O,
-                                                     const T* __restrict__ dO, const float* __restrict__ LSE,
-                                                     float* __restrict__ Dv, float sl2, float* __restrict__ pdq,
-                                                     T* __restrict__ dQ, float scale) {
+                                                     const T* __restrict__ V, const T* __restrict__ dO,
+                                                     const float* __restrict__ LSE, float sl2,
+                                                     float* __restrict__ pa, float* __restrict__ pb,
+                                                     float* __restrict__ pd, T* __restrict__ dQ,
+                                                     float* __restrict__ Dv, float scale) {
     constexpr int NT = 2 * TT;
     constexpr int KB = TT / 32;
     constexpr int W = TT / 32;
@@ -374,17 +378,14 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
     const int qlocal = 32 * wv + (lane & 31);
     const int64_t q = int64_t(I) * TT + qlocal;
     const bool qok = q < n;
-    RowFrag<T, D> qf, gf, of;
+    RowFrag<T, D> qf, gf;
     qf.load(Q + (q * H + h) * D, qok, lane);
     gf.load(dO + (q * H + h) * D, qok, lane);
-    of.load(O + (q * H + h) * D, qok, lane);
-    float Dq = gf.dot(of);
-    Dq += __shfl_xor(Dq, 32, kWave);
-    if (qok && lane < 32) Dv[q * H + h] = Dq;
     const float lse2 = qok ? LSE[q * H + h] * kLog2e : 0.f;
-    f32x16_t acc[D / 32];
+    f32x16_t accA[D / 32], accB[D / 32];
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) acc[db] = zero16();
+    for (int db = 0; db < D / 32; ++db) accA[db] = accB[db] = zero16();
+    float dsum = 0.f;
     for (int64_t k = t0; k < t1; ++k) {
         const int64_t kbase = (kFull ? k : int64_t(tile_col[k])) * TT;
         __syncthreads();
@@ -394,34 +395,42 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
         const uint32_t* mrow = tile_mask + (k * TT + qlocal) * W;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
-            f32x16_t s = prod_rows<T, D>(sK + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, qf, lane);
-            const f32x16_t dp = prod_rows<T, D>(sV + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, gf, lane);
+            f32x16_t p = prod_rows<T, D>(sK + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, qf, lane);
+            f32x16_t w = prod_rows<T, D>(sV + 32 * kb * Pad<T, D>::kRow, Pad<T, D>::kRow, gf, lane);
             const uint32_t mw = kFull ? (qok ? full_word(kbase + 32 * kb, n) : 0u) : mrow[kb];
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const float p = ((mw >> crow(i, lane)) & 1u) ? ex2(s[i] * sl2 - lse2) : 0.f;
-                s[i] = p * (dp[i] - Dq);
+                const float pv = ((mw >> crow(i, lane)) & 1u) ? ex2(p[i] * sl2 - lse2) : 0.f;
+                p[i] = pv;
+                w[i] *= pv;
+                dsum += w[i];
             }
 #pragma unroll
             for (int db = 0; db < D / 32; ++db) {
                 const T* trow = sKt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
-                acc[db] = prod_acc<T>(acc[db], trow, 32 * kb, s, lane);
+                accA[db] = prod_acc<T>(accA[db], trow, 32 * kb, w, lane);
+                accB[db] = prod_acc<T>(accB[db], trow, 32 * kb, p, lane);
             }
         }
     }
+    dsum += __shfl_xor(dsum, 32, kWave);
     if (!qok) return;
+    if (kFull && lane < 32) Dv[q * H + h] = dsum;
+    if (!kFull && lane < 32) pd[q * H + h] = dsum;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
             const int64_t o = (q * H + h) * D + 32 * db + crow(i, lane);
             if (kFull) {
+                const float v = fmaf(-dsum, accB[db][i], accA[db][i]) * scale;
                 if constexpr (Mma<T>::kBf16)
-                    dQ[o] = f32_to_bf16(acc[db][i] * scale);
+                    dQ[o] = f32_to_bf16(v);
                 else
-                    dQ[o] = acc[db][i] * scale;
+                    dQ[o] = v;
             } else {
-                pdq[o] = acc[db][i];
+                pa[o] = accA[db][i];
+                pb[o] = accB[db][i];
             }
         }
 }
@@ -574,12 +583,12 @@ gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float 
 }
 
 template <typename T, int D, int H>
-gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* O, const T* dO,
-                      const float* LSE, float* Dv, float sl2, TilePartials dq, hipStream_t s) {
+gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
+                      float sl2, TilePartials dq, hipStream_t s) {
     const dim3 grid(unsigned(p->n_row_tiles), H);
     GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
-                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, O, dO, LSE, Dv, sl2, dq.acc,
-                             nullptr, 1.f)));
+                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, dO, LSE, sl2, dq.acc,
+                             dq.acc2, dq.m, nullptr, nullptr, 1.f)));
     GT_LAUNCH_CHECK("tile_bwd_dq");
     return GT_OK;
 }
@@ -607,12 +616,12 @@ gt_status full_fwd(int64_t n, const T* Q, const T* K, const T* V, float sl2, T* 
 }
 
 template <typename T, int D, int H>
-gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, const T* dO, const float* LSE,
-                   float sl2, float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s) {
+gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* dO, const float* LSE, float sl2,
+                   float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s) {
     constexpr int TT = 128;
     const dim3 grid(unsigned(cdiv(n, TT)), H);
-    k_tile_dq<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, O, dO, LSE, Dv,
-                                                         sl2, nullptr, dQ, scale);
+    k_tile_dq<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, dO, LSE, sl2,
+                                                         nullptr, nullptr, nullptr, dQ, Dv, scale);
     GT_LAUNCH_CHECK("full_bwd_dq");
     k_tile_dkdv<T, D, H, TT, true, false><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, nullptr, Q, K, V,
                                                                   dO, LSE, Dv, sl2, nullptr, nullptr, dK, dV, scale);
@@ -623,14 +632,14 @@ gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, co
 #define GT_INST(T, D, H)                                                                                          \
     template gt_status tile_fwd<T, D, H>(const gt_tiles*, const T*, const T*, const T*, float, TilePartials,      \
                                          hipStream_t);                                                            \
-    template gt_status tile_bwd_dq<T, D, H>(const gt_tiles*, const T*, const T*, const T*, const T*, const T*,    \
-                                            const float*, float*, float, TilePartials, hipStream_t);              \
+    template gt_status tile_bwd_dq<T, D, H>(const gt_tiles*, const T*, const T*, const T*, const T*,              \
+                                            const float*, float, TilePartials, hipStream_t);                      \
     template gt_status tile_bwd_dkdv<T, D, H>(const gt_tiles*, const T*, const T*, const T*, const T*,            \
                                               const float*, const float*, float, TilePartials, TilePartials,      \
                                               hipStream_t);                                                       \
     template gt_status full_fwd<T, D, H>(int64_t, const T*, const T*, const T*, float, T*, float*, hipStream_t); \
-    template gt_status full_bwd<T, D, H>(int64_t, const T*, const T*, const T*, const T*, const T*, const float*, \
-                                         float, float, T*, T*, T*, float*, hipStream_t);
+    template gt_status full_bwd<T, D, H>(int64_t, const T*, const T*, const T*, const T*, const float*, float,   \
+                                         float, T*, T*, T*, float*, hipStream_t);
 #define GT_INST_H(T, D) GT_INST(T, D, 1) GT_INST(T, D, 2) GT_INST(T, D, 4) GT_INST(T, D, 8) GT_INST(T, D, 16)
 GT_INST_H(uint16_t, 32)
 GT_INST_H(uint16_t, 64)

@@ -63,18 +63,18 @@ SIGNATURES = {
     "gt_sparse_attn_fwd_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
     "gt_sparse_attn_fwd": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _sz, _vp]),
     "gt_sparse_attn_bwd_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
-    "gt_sparse_attn_bwd": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp,
-                                  _vp, _vp, _sz, _vp]),
+    "gt_sparse_attn_bwd": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp,
+                                  _vp, _sz, _vp]),
     "gt_sparse_attn_bwd_rows_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
-    "gt_sparse_attn_bwd_rows": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp,
-                                       _vp, _vp, _sz, _vp]),
+    "gt_sparse_attn_bwd_rows": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp,
+                                       _vp, _sz, _vp]),
     "gt_sparse_attn_bwd_cols_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
     "gt_sparse_attn_bwd_cols": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp,
                                        _vp, _vp, _sz, _vp]),
     "gt_dense_attn_fwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp]),
     "gt_dense_attn_bwd_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
-    "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
-                                 _sz, _vp]),
+    "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _sz,
+                                 _vp]),
 }
 
 _LIB = None
@@ -301,26 +301,26 @@ def sparse_attn_fwd(plan: Plan, Q: torch.Tensor, K: torch.Tensor, V: torch.Tenso
     return O, LSE
 
 
-def sparse_attn_bwd(plan: Plan, Q, K, V, O, dO, LSE, scale: float | None = None):
+def sparse_attn_bwd(plan: Plan, Q, K, V, dO, LSE, scale: float | None = None):
     """(dQ, dK, dV) of neighbourhood softmax attention."""
     lib = load_library()
-    _check_feats(plan.n, Q, K, V, O, dO)
+    _check_feats(plan.n, Q, K, V, dO)
     n, H, d = Q.shape
     _need(LSE.dtype == torch.float32 and LSE.shape == (n, H) and LSE.is_contiguous(), "LSE must be fp32 [n, H]")
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     dt = _dtype_code(Q)
     dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
     ws = _workspace(lib.gt_sparse_attn_bwd_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
-    _check(lib.gt_sparse_attn_bwd(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO),
-                                  _ptr(LSE), scale, _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(),
-                                  _stream(Q.device)), "gt_sparse_attn_bwd")
+    _check(lib.gt_sparse_attn_bwd(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(dO), _ptr(LSE),
+                                  scale, _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(), _stream(Q.device)),
+           "gt_sparse_attn_bwd")
     return dQ, dK, dV
 
 
-def sparse_attn_bwd_rows(plan: Plan, Q, K, V, O, dO, LSE, scale: float | None = None):
+def sparse_attn_bwd_rows(plan: Plan, Q, K, V, dO, LSE, scale: float | None = None):
     """(dQ, Dstat) - the row-owned half of the backward."""
     lib = load_library()
-    _check_feats(plan.n, Q, K, V, O, dO)
+    _check_feats(plan.n, Q, K, V, dO)
     n, H, d = Q.shape
     _need(LSE.dtype == torch.float32 and LSE.shape == (n, H) and LSE.is_contiguous(), "LSE must be fp32 [n, H]")
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
@@ -328,7 +328,7 @@ def sparse_attn_bwd_rows(plan: Plan, Q, K, V, O, dO, LSE, scale: float | None = 
     dQ = torch.empty_like(Q)
     Dstat = torch.empty((n, H), dtype=torch.float32, device=Q.device)
     ws = _workspace(lib.gt_sparse_attn_bwd_rows_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
-    _check(lib.gt_sparse_attn_bwd_rows(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO),
+    _check(lib.gt_sparse_attn_bwd_rows(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(dO),
                                        _ptr(LSE), scale, _ptr(dQ), _ptr(Dstat), _ptr(ws), ws.numel(),
                                        _stream(Q.device)), "gt_sparse_attn_bwd_rows")
     return dQ, Dstat
@@ -364,16 +364,15 @@ def dense_attn_fwd(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: flo
     return O, LSE
 
 
-def dense_attn_bwd(Q, K, V, O, dO, LSE, scale: float | None = None):
+def dense_attn_bwd(Q, K, V, dO, LSE, scale: float | None = None):
     """(dQ, dK, dV) of full softmax attention."""
     lib = load_library()
-    _check_feats(Q.shape[0], Q, K, V, O, dO)
+    _check_feats(Q.shape[0], Q, K, V, dO)
     n, H, d = Q.shape
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     dt = _dtype_code(Q)
     dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
     ws = _workspace(lib.gt_dense_attn_bwd_workspace_size(n, H, d, dt), Q.device)
-    _check(lib.gt_dense_attn_bwd(n, H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE), scale,
-                                 _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(), _stream(Q.device)),
-           "gt_dense_attn_bwd")
+    _check(lib.gt_dense_attn_bwd(n, H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(dO), _ptr(LSE), scale, _ptr(dQ),
+                                 _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(), _stream(Q.device)), "gt_dense_attn_bwd")
     return dQ, dK, dV

@@ -70,7 +70,7 @@ def test_argument_errors_without_device(lib):
     # unsupported head width and head count
     assert lib.gt_sparse_attn_fwd(ctypes.byref(c), 8, 48, gt.GT_BF16, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE,
                                   1 << 30, stream) == gt.GT_ERR_UNSUPPORTED
-    assert lib.gt_sparse_attn_bwd(ctypes.byref(c), 3, 32, gt.GT_F32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1.0, FAKE,
+    assert lib.gt_sparse_attn_bwd(ctypes.byref(c), 3, 32, gt.GT_F32, FAKE, FAKE, FAKE, FAKE, FAKE, 1.0, FAKE,
                                   FAKE, FAKE, FAKE, 1 << 30, stream) == gt.GT_ERR_UNSUPPORTED
     # workspace too small
     assert lib.gt_sparse_attn_fwd(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, 0,

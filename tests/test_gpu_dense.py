@@ -30,7 +30,7 @@ def test_dense_layer_full_outputs(gt, n, H, d, dtype):
     scale = 1.0 / np.sqrt(d)
     Q, K, V, dO = (dev_feat(x, dtype) for x in (q, k, v, do))
     O, L = gt.dense_attn_fwd(Q, K, V, scale)
-    dQ, dK, dV = gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
+    dQ, dK, dV = gt.dense_attn_bwd(Q, K, V, dO, L, scale)
     torch.cuda.synchronize()
     O_ref, L_ref = OA.dense_attn_fwd(q, k, v, scale)
     ref = OA.dense_attn_bwd(q, k, v, do, scale)
@@ -48,7 +48,7 @@ def test_dense_layer_65536_sampled_rows_and_sum_rules(gt):
     Q, K, V, dO = (dev_feat(x, "bf16") for x in (q, k, v, do))
     say("dense c5 full size", n, H, d)
     O, L = gt.dense_attn_fwd(Q, K, V, scale)
-    dQ, dK, dV = gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
+    dQ, dK, dV = gt.dense_attn_bwd(Q, K, V, dO, L, scale)
     torch.cuda.synchronize()
     rows = np.sort(np.random.default_rng(5).choice(n, size=64, replace=False))
     O_ref, L_ref = OA.dense_attn_fwd(q, k, v, scale, rows=rows)
