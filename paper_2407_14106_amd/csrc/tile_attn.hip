@@ -161,8 +161,9 @@ __device__ __forceinline__ f32x16_t prod_acc(f32x16_t acc, const T* trow, int co
 }
 
 // As prod_acc, but the bf16 B operand is split into hi + lo parts (two
-// products), so P keeps about 16 mantissa bits: used where a column sums many
-// large probabilities (a hub attended by many low-degree rows).
+// products), so the weights keep about 16 mantissa bits: used where sums of
+// many large weights meet (a hub attended by many low-degree rows) and where
+// two such sums are subtracted (dQ = A - D B).
 template <typename T>
 __device__ __forceinline__ f32x16_t prod_acc_split(f32x16_t acc, const T* trow, int col0, const f32x16_t& p, int lane) {
     if constexpr (Mma<T>::kBf16) {
@@ -346,7 +347,7 @@ __global__ __launch_bounds__(2 * TT) void k_tile_fwd(int64_t n, const int64_t* _
 // the row's partners (D equals <dO, O> of the exact output).  The sparse
 // variant leaves A, B and the D sum as partials; kFull finishes dQ and writes D.
 
-template <typename T, int D, int H, int TT, bool kFull>
+template <typename T, int D, int H, int TT, bool kFull, bool kSplit>
 __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __restrict__ tile_rowptr,
                                                      const int32_t* __restrict__ tile_col,
                                                      const uint32_t* __restrict__ tile_mask,
@@ -408,8 +409,13 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
 #pragma unroll
             for (int db = 0; db < D / 32; ++db) {
                 const T* trow = sKt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
-                accA[db] = prod_acc<T>(accA[db], trow, 32 * kb, w, lane);
-                accB[db] = prod_acc<T>(accB[db], trow, 32 * kb, p, lane);
+                if (kSplit) {
+                    accA[db] = prod_acc_split<T>(accA[db], trow, 32 * kb, w, lane);
+                    accB[db] = prod_acc_split<T>(accB[db], trow, 32 * kb, p, lane);
+                } else {
+                    accA[db] = prod_acc<T>(accA[db], trow, 32 * kb, w, lane);
+                    accB[db] = prod_acc<T>(accB[db], trow, 32 * kb, p, lane);
+                }
             }
         }
     }
@@ -586,7 +592,7 @@ template <typename T, int D, int H>
 gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
                       float sl2, TilePartials dq, hipStream_t s) {
     const dim3 grid(unsigned(p->n_row_tiles), H);
-    GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
+    GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
                              p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, dO, LSE, sl2, dq.acc,
                              dq.acc2, dq.m, nullptr, nullptr, 1.f)));
     GT_LAUNCH_CHECK("tile_bwd_dq");
@@ -620,7 +626,7 @@ gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* dO, c
                    float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s) {
     constexpr int TT = 128;
     const dim3 grid(unsigned(cdiv(n, TT)), H);
-    k_tile_dq<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, dO, LSE, sl2,
+    k_tile_dq<T, D, H, TT, true, false><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, dO, LSE, sl2,
                                                          nullptr, nullptr, nullptr, dQ, Dv, scale);
     GT_LAUNCH_CHECK("full_bwd_dq");
     k_tile_dkdv<T, D, H, TT, true, false><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, nullptr, Q, K, V,
