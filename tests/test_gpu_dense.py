@@ -21,7 +21,7 @@ def say(*a):
     sys.stdout.flush()
 
 
-@pytest.mark.parametrize("n,H,d,dtype", [(1, 1, 32, "f32"), (77, 2, 32, "f32"), (300, 1, 64, "f32"),
+@pytest.mark.parametrize("n,H,d,dtype", [(2, 1, 32, "f32"), (77, 2, 32, "f32"), (300, 1, 64, "f32"),
                                          (300, 8, 64, "bf16"), (1000, 4, 32, "bf16"), (4096, 8, 64, "bf16"),
                                          (129, 16, 64, "bf16")])
 def test_dense_layer_full_outputs(gt, n, H, d, dtype):
@@ -38,6 +38,21 @@ def test_dense_layer_full_outputs(gt, n, H, d, dtype):
     assert_close(L.cpu().numpy(), L_ref, dtype, "LSE")
     for name, x, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
         assert_close(host(x), r, dtype, name)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dense_layer_single_node(gt, dtype):
+    # one key: P = 1, so O = V, LSE = scale <q, k>, dV = dO, and dQ = dK = 0 up to rounding of the terms
+    q, k, v, do = (normal_tensor((1, 4, 64), (1, t), dtype) for t in range(4))
+    Q, K, V, dO = (dev_feat(x, dtype) for x in (q, k, v, do))
+    O, L = gt.dense_attn_fwd(Q, K, V, 0.125)
+    dQ, dK, dV = gt.dense_attn_bwd(Q, K, V, dO, L, 0.125)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(O), v.astype(np.float64))
+    np.testing.assert_allclose(L.cpu().numpy(), 0.125 * np.einsum("nhc,nhc->nh", q, k), rtol=1e-5, atol=1e-5)
+    np.testing.assert_allclose(host(dV), do, rtol=1e-6 if dtype == "f32" else 0, atol=1e-6)
+    term = 0.125 * np.abs(do).max() * np.abs(v).max() * max(np.abs(k).max(), np.abs(q).max())
+    assert np.abs(host(dQ)).max() <= 1e-5 * term and np.abs(host(dK)).max() <= 1e-5 * term
 
 
 def test_dense_layer_65536_sampled_rows_and_sum_rules(gt):
