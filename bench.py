@@ -109,7 +109,7 @@ def dense_layer(steps: int):
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     for _ in range(2):
         O, L = gt.dense_attn_fwd(Q, K, V, scale)
-        gt.dense_attn_bwd(Q, K, V, dO, L, scale)
+        gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
     torch.cuda.synchronize()
     fw, bw = [], []
     for _ in range(steps):
@@ -117,7 +117,7 @@ def dense_layer(steps: int):
         a.record()
         O, L = gt.dense_attn_fwd(Q, K, V, scale)
         b.record()
-        gt.dense_attn_bwd(Q, K, V, dO, L, scale)
+        gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
         c.record()
         torch.cuda.synchronize()
         fw.append(a.elapsed_time(b))

@@ -218,9 +218,11 @@ gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, int32_t d, gt
 gt_status gt_dense_attn_fwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
                             const void* V, float scale, void* O, float* LSE, hipStream_t stream);
 size_t gt_dense_attn_bwd_workspace_size(int64_t n, int32_t H, int32_t d, gt_dtype dtype);
+/* Backward of the full layer given O and LSE of its forward.  Here every
+ * weight is about 1/n, so D_i = <dO_i, O_i> is taken from the given O. */
 gt_status gt_dense_attn_bwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
-                            const void* V, const void* dO, const float* LSE, float scale, void* dQ, void* dK,
-                            void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+                            const void* V, const void* O, const void* dO, const float* LSE, float scale, void* dQ,
+                            void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

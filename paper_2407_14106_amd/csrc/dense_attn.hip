@@ -25,13 +25,13 @@ gt_status run_dense_fwd(int64_t n, const void* Q, const void* K, const void* V, 
 }
 
 template <typename T, int D, int H>
-gt_status run_dense_bwd(int64_t n, const void* Q, const void* K, const void* V, const void* dO, const float* LSE,
-                        float scale, void* dQ, void* dK, void* dV, void* ws, hipStream_t s) {
+gt_status run_dense_bwd(int64_t n, const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                        const float* LSE, float scale, void* dQ, void* dK, void* dV, void* ws, hipStream_t s) {
     if (n == 0) return GT_OK;
     Ws w(ws);
     float* Dv = w.take<float>(size_t(n) * H);
     return full_bwd<T, D, H>(n, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
-                             static_cast<const T*>(dO), LSE, scale * kLog2e, scale,
+                             static_cast<const T*>(O), static_cast<const T*>(dO), LSE, scale * kLog2e, scale,
                              static_cast<T*>(dQ), static_cast<T*>(dK), static_cast<T*>(dV), Dv, s);
 }
 
@@ -52,13 +52,13 @@ extern "C" size_t gt_dense_attn_bwd_workspace_size(int64_t n, int32_t H, int32_t
 }
 
 extern "C" gt_status gt_dense_attn_bwd(int64_t n, int32_t H, int32_t d, gt_dtype dt, const void* Q, const void* K,
-                                       const void* V, const void* dO, const float* LSE, float scale, void* dQ,
-                                       void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream) {
+                                       const void* V, const void* O, const void* dO, const float* LSE, float scale,
+                                       void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream) {
     gt_status st = dense_check("gt_dense_attn_bwd", n, H, d, dt, Q, K, V);
     if (st != GT_OK) return st;
-    if (n > 0 && (!dO || !LSE || !dQ || !dK || !dV || !ws))
+    if (n > 0 && (!O || !dO || !LSE || !dQ || !dK || !dV || !ws))
         return fail(GT_ERR_INVALID_ARG, "gt_dense_attn_bwd: null pointer");
     if (ws_bytes < gt_dense_attn_bwd_workspace_size(n, H, d, dt))
         return fail(GT_ERR_WORKSPACE, "gt_dense_attn_bwd: workspace too small");
-    return GT_DISPATCH_ATTN(dt, d, H, run_dense_bwd, n, Q, K, V, dO, LSE, scale, dQ, dK, dV, ws, stream);
+    return GT_DISPATCH_ATTN(dt, d, H, run_dense_bwd, n, Q, K, V, O, dO, LSE, scale, dQ, dK, dV, ws, stream);
 }

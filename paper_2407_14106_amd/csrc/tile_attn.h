@@ -84,11 +84,11 @@ gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, c
                         const float* Dv, float sl2, TilePartials dk, TilePartials dv, hipStream_t s);
 
 // The full softmax layer (every node attends to all n nodes) on the same
-// kernels: O and LSE; then dQ and D (into Dv); then dK and dV.
+// kernels: O and LSE; then D = <dO, O> (into Dv) and dQ; then dK and dV.
 template <typename T, int D, int H>
 gt_status full_fwd(int64_t n, const T* Q, const T* K, const T* V, float sl2, T* O, float* LSE, hipStream_t s);
 template <typename T, int D, int H>
-gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* dO, const float* LSE, float sl2,
-                   float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s);
+gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, const T* dO, const float* LSE,
+                   float sl2, float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s);
 
 }  // namespace gt

@@ -343,18 +343,21 @@ __global__ __launch_bounds__(2 * TT) void k_tile_fwd(int64_t n, const int64_t* _
 }
 
 // ---------------------------------------------------------------- dQ (rows)
-// dQ = scale (A - D B) with A = sum P dP K, B = sum P K and D = sum P dP over
-// the row's partners (D equals <dO, O> of the exact output).  The sparse
-// variant leaves A, B and the D sum as partials; kFull finishes dQ and writes D.
+// Sparse tiles: dQ = scale (A - D B) with A = sum P dP K, B = sum P K and
+// D = sum P dP over the row's partners (D equals <dO, O> of the exact output);
+// the kernel leaves A, B and the D sum as partials, with the weights of both
+// products split into bf16 hi + lo parts so that A - D B keeps its precision.
+// Full layer (kFull): every weight is about 1/n, so D = <dO, O> from the given
+// O is used directly and dQ = scale K^T (P (dP - D)) is finished here.
 
-template <typename T, int D, int H, int TT, bool kFull, bool kSplit>
+template <typename T, int D, int H, int TT, bool kFull>
 __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __restrict__ tile_rowptr,
                                                      const int32_t* __restrict__ tile_col,
                                                      const uint32_t* __restrict__ tile_mask,
                                                      const T* __restrict__ Q, const T* __restrict__ K,
-                                                     const T* __restrict__ V, const T* __restrict__ dO,
-                                                     const float* __restrict__ LSE, float sl2,
-                                                     float* __restrict__ pa, float* __restrict__ pb,
+                                                     const T* __restrict__ V, const T* __restrict__ O,
+                                                     const T* __restrict__ dO, const float* __restrict__ LSE,
+                                                     float sl2, float* __restrict__ pa, float* __restrict__ pb,
                                                      float* __restrict__ pd, T* __restrict__ dQ,
                                                      float* __restrict__ Dv, float scale) {
     constexpr int NT = 2 * TT;
@@ -383,6 +386,14 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
     qf.load(Q + (q * H + h) * D, qok, lane);
     gf.load(dO + (q * H + h) * D, qok, lane);
     const float lse2 = qok ? LSE[q * H + h] * kLog2e : 0.f;
+    float Dq = 0.f;
+    if (kFull) {
+        RowFrag<T, D> of;
+        of.load(O + (q * H + h) * D, qok, lane);
+        Dq = gf.dot(of);
+        Dq += __shfl_xor(Dq, 32, kWave);
+        if (qok && lane < 32) Dv[q * H + h] = Dq;
+    }
     f32x16_t accA[D / 32], accB[D / 32];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) accA[db] = accB[db] = zero16();
@@ -403,25 +414,27 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
             for (int i = 0; i < 16; ++i) {
                 const float pv = ((mw >> crow(i, lane)) & 1u) ? ex2(p[i] * sl2 - lse2) : 0.f;
                 p[i] = pv;
-                w[i] *= pv;
-                dsum += w[i];
+                if (kFull) {
+                    w[i] = pv * (w[i] - Dq);
+                } else {
+                    w[i] *= pv;
+                    dsum += w[i];
+                }
             }
 #pragma unroll
             for (int db = 0; db < D / 32; ++db) {
                 const T* trow = sKt + (32 * db + (lane & 31)) * PadT<T, TT>::kRow;
-                if (kSplit) {
+                if (kFull) {
+                    accA[db] = prod_acc<T>(accA[db], trow, 32 * kb, w, lane);
+                } else {
                     accA[db] = prod_acc_split<T>(accA[db], trow, 32 * kb, w, lane);
                     accB[db] = prod_acc_split<T>(accB[db], trow, 32 * kb, p, lane);
-                } else {
-                    accA[db] = prod_acc<T>(accA[db], trow, 32 * kb, w, lane);
-                    accB[db] = prod_acc<T>(accB[db], trow, 32 * kb, p, lane);
                 }
             }
         }
     }
     dsum += __shfl_xor(dsum, 32, kWave);
     if (!qok) return;
-    if (kFull && lane < 32) Dv[q * H + h] = dsum;
     if (!kFull && lane < 32) pd[q * H + h] = dsum;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -429,7 +442,7 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
         for (int i = 0; i < 16; ++i) {
             const int64_t o = (q * H + h) * D + 32 * db + crow(i, lane);
             if (kFull) {
-                const float v = fmaf(-dsum, accB[db][i], accA[db][i]) * scale;
+                const float v = accA[db][i] * scale;
                 if constexpr (Mma<T>::kBf16)
                     dQ[o] = f32_to_bf16(v);
                 else
@@ -592,9 +605,9 @@ template <typename T, int D, int H>
 gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
                       float sl2, TilePartials dq, hipStream_t s) {
     const dim3 grid(unsigned(p->n_row_tiles), H);
-    GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
-                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, dO, LSE, sl2, dq.acc,
-                             dq.acc2, dq.m, nullptr, nullptr, 1.f)));
+    GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
+                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, nullptr, dO, LSE, sl2,
+                             dq.acc, dq.acc2, dq.m, nullptr, nullptr, 1.f)));
     GT_LAUNCH_CHECK("tile_bwd_dq");
     return GT_OK;
 }
@@ -622,11 +635,11 @@ gt_status full_fwd(int64_t n, const T* Q, const T* K, const T* V, float sl2, T* 
 }
 
 template <typename T, int D, int H>
-gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* dO, const float* LSE, float sl2,
-                   float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s) {
+gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, const T* dO, const float* LSE,
+                   float sl2, float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s) {
     constexpr int TT = 128;
     const dim3 grid(unsigned(cdiv(n, TT)), H);
-    k_tile_dq<T, D, H, TT, true, false><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, dO, LSE, sl2,
+    k_tile_dq<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, O, dO, LSE, sl2,
                                                          nullptr, nullptr, nullptr, dQ, Dv, scale);
     GT_LAUNCH_CHECK("full_bwd_dq");
     k_tile_dkdv<T, D, H, TT, true, false><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, nullptr, Q, K, V,
@@ -644,8 +657,8 @@ gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* dO, c
                                               const float*, const float*, float, TilePartials, TilePartials,      \
                                               hipStream_t);                                                       \
     template gt_status full_fwd<T, D, H>(int64_t, const T*, const T*, const T*, float, T*, float*, hipStream_t); \
-    template gt_status full_bwd<T, D, H>(int64_t, const T*, const T*, const T*, const T*, const float*, float,   \
-                                         float, T*, T*, T*, float*, hipStream_t);
+    template gt_status full_bwd<T, D, H>(int64_t, const T*, const T*, const T*, const T*, const T*, const float*, \
+                                         float, float, T*, T*, T*, float*, hipStream_t);
 #define GT_INST_H(T, D) GT_INST(T, D, 1) GT_INST(T, D, 2) GT_INST(T, D, 4) GT_INST(T, D, 8) GT_INST(T, D, 16)
 GT_INST_H(uint16_t, 32)
 GT_INST_H(uint16_t, 64)

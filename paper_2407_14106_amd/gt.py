@@ -73,8 +73,8 @@ SIGNATURES = {
                                        _vp, _vp, _sz, _vp]),
     "gt_dense_attn_fwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp]),
     "gt_dense_attn_bwd_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
-    "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _sz,
-                                 _vp]),
+    "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
+                                 _sz, _vp]),
 }
 
 _LIB = None
@@ -364,15 +364,16 @@ def dense_attn_fwd(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: flo
     return O, LSE
 
 
-def dense_attn_bwd(Q, K, V, dO, LSE, scale: float | None = None):
+def dense_attn_bwd(Q, K, V, O, dO, LSE, scale: float | None = None):
     """(dQ, dK, dV) of full softmax attention."""
     lib = load_library()
-    _check_feats(Q.shape[0], Q, K, V, dO)
+    _check_feats(Q.shape[0], Q, K, V, O, dO)
     n, H, d = Q.shape
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     dt = _dtype_code(Q)
     dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
     ws = _workspace(lib.gt_dense_attn_bwd_workspace_size(n, H, d, dt), Q.device)
-    _check(lib.gt_dense_attn_bwd(n, H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(dO), _ptr(LSE), scale, _ptr(dQ),
-                                 _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(), _stream(Q.device)), "gt_dense_attn_bwd")
+    _check(lib.gt_dense_attn_bwd(n, H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE), scale,
+                                 _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(), _stream(Q.device)),
+           "gt_dense_attn_bwd")
     return dQ, dK, dV
