@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense-layer", action="store_true", help="skip the full-attention layer measurement")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB row copy (gt_gather_rows, identity order) 5 times: the reference "
+                         "for scaling hardware byte counters")
     return ap.parse_args()
 
 
@@ -79,7 +82,7 @@ def cpu_baseline(w, target_s):
         OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, scale, rows=sample)
         OA.sparse_attn_bwd_sampled(g.rowptr, g.col, q, k, v, do, scale, sample, sample)
         dt = time.perf_counter() - t0
-        if dt >= target_s / 3 or rows >= g.n:
+        if dt >= 0.6 * target_s or rows >= g.n:
             break
         rows = min(g.n, int(rows * max(2.0, min(8.0, target_s / max(dt, 1e-3)))))
     deg = np.diff(g.rowptr)[sample]
@@ -135,11 +138,31 @@ def dense_layer(steps: int):
     }
 
 
+def copy_probe():
+    """A plain copy of known size: 2^21 rows x 512 bytes (1 GiB) read and written, plus the 8 MiB order array."""
+    import torch
+
+    from paper_2407_14106_amd import gt
+
+    gt.load_library()
+    rows = 1 << 21
+    x = torch.zeros((rows, 256), dtype=torch.bfloat16, device="cuda:0")
+    perm = torch.arange(rows, dtype=torch.int32, device="cuda:0")
+    for _ in range(5):
+        gt.gather_rows(x, perm)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe": {"rows": rows, "row_bytes": 512, "bytes_read": rows * 512 + 4 * rows,
+                                     "bytes_written": rows * 512, "launches": 5, "kernel": "k_move_rows"}}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe()
+        return
     import torch
 
     from paper_2407_14106_amd import gt
