@@ -57,6 +57,17 @@ struct Slice<uint16_t, F> {
         }
         return a0 + a1;
     }
+    // acc[2i] += p * lo(w[i]), acc[2i+1] += p * hi(w[i]) with p given as the
+    // bf16 pairs (p, 0) and (0, p): one dot2 per element, no conversion.
+    __device__ __forceinline__ void axpy_w(float (&acc)[F], uint32_t p_lo, uint32_t p_hi) const {
+#pragma unroll
+        for (int i = 0; i < F / 2; ++i) {
+            const bf16x2_t x = __builtin_bit_cast(bf16x2_t, w[i]);
+            acc[2 * i] = __builtin_amdgcn_fdot2_f32_bf16(x, __builtin_bit_cast(bf16x2_t, p_lo), acc[2 * i], false);
+            acc[2 * i + 1] =
+                __builtin_amdgcn_fdot2_f32_bf16(x, __builtin_bit_cast(bf16x2_t, p_hi), acc[2 * i + 1], false);
+        }
+    }
 };
 
 template <int F>

@@ -47,6 +47,16 @@ struct Ws {
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// MI355X has 8 XCDs (each with its own L2) and hands consecutive workgroup ids
+// to them round-robin.  Kernels whose neighbouring workgroups share data
+// remap their id so that each XCD walks one contiguous range: launch a grid
+// padded to a multiple of kXcds (xcd_grid) and call xcd_block(blockIdx.x).
+constexpr int kXcds = 8;
+inline unsigned xcd_grid(int64_t blocks) { return static_cast<unsigned>(cdiv(blocks > 0 ? blocks : 1, kXcds) * kXcds); }
+__device__ __forceinline__ int64_t xcd_block(int64_t b, int64_t grid) {
+    return (b % kXcds) * (grid / kXcds) + b / kXcds;
+}
+
 inline unsigned grid_for(int64_t work, int per_block, int64_t cap = 1 << 20) {
     int64_t g = cdiv(work, per_block);
     if (g < 1) g = 1;

@@ -77,39 +77,65 @@ __device__ __forceinline__ void load_fwd_partial(Online<EdgeCfg<T, D, H>::F>& st
     }
 }
 
-// One block of two edges for the forward state.
+// The running max is a lazy reference: it moves only when a score exceeds it
+// by more than 2^8 (in the exp2 domain), so the accumulator is rescaled
+// rarely; weights stay below 2^8 and the result is unchanged.
+constexpr float kRescale = 8.f;
+
+// Weight p as the bf16 pairs (p, 0) and (0, p) for Slice::axpy_w.
+__device__ __forceinline__ void weight_pairs(float p, uint32_t& lo, uint32_t& hi) {
+    lo = uint32_t(f32_to_bf16(p));
+    hi = lo << 16;
+}
+
+// One block of two edges for the forward state.  j0/j1 are always valid
+// node ids (callers substitute a valid id for missing edges); ok0/ok1 say
+// which of the two are edges.
 template <typename T, int D, int H>
 __device__ __forceinline__ void fwd_step(Online<EdgeCfg<T, D, H>::F>& st, const Slice<T, EdgeCfg<T, D, H>::F>& q,
                                          const T* __restrict__ K, const T* __restrict__ V, int64_t j0, int64_t j1,
                                          bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> k0, k1, v0, v1;
-    k0.zero();
-    k1.zero();
-    v0.zero();
-    v1.zero();
-    if (ok0) {
-        k0.load(K + ln.off(j0));
-        v0.load(V + ln.off(j0));
-    }
-    if (ok1) {
-        k1.load(K + ln.off(j1));
-        v1.load(V + ln.off(j1));
-    }
-    float s0 = group_sum<C::L>(q.dot(k0)) * sl2;
-    float s1 = group_sum<C::L>(q.dot(k1)) * sl2;
-    s0 = ok0 ? s0 : kNegInf;
-    s1 = ok1 ? s1 : kNegInf;
+    k0.load(K + ln.off(j0));
+    k1.load(K + ln.off(j1));
+    v0.load(V + ln.off(j0));
+    v1.load(V + ln.off(j1));
+    const float s0 = ok0 ? group_sum<C::L>(q.dot(k0)) * sl2 : kNegInf;
+    const float s1 = ok1 ? group_sum<C::L>(q.dot(k1)) * sl2 : kNegInf;
     const float mb = fmaxf(s0, s1);
-    const float mn = fmaxf(st.m, mb);
-    if (mn == kNegInf) return;
-    const float alpha = exp2f(st.m - mn);
-    const float p0 = exp2f(s0 - mn);
-    const float p1 = exp2f(s1 - mn);
-    st.l = st.l * alpha + p0 + p1;
+    if (mb > st.m + kRescale) {
+        const float alpha = st.m == kNegInf ? 0.f : exp2f(st.m - mb);
+        st.l *= alpha;
 #pragma unroll
-    for (int i = 0; i < C::F; ++i) st.acc[i] = fmaf(p1, v1.f(i), fmaf(p0, v0.f(i), st.acc[i] * alpha));
-    st.m = mn;
+        for (int i = 0; i < C::F; ++i) st.acc[i] *= alpha;
+        st.m = mb;
+    }
+    const float p0 = ok0 ? exp2f(s0 - st.m) : 0.f;
+    const float p1 = ok1 ? exp2f(s1 - st.m) : 0.f;
+    st.l += p0 + p1;
+    if constexpr (sizeof(T) == 2) {
+        uint32_t a0, b0, a1, b1;
+        weight_pairs(p0, a0, b0);
+        weight_pairs(p1, a1, b1);
+        v0.axpy_w(st.acc, a0, b0);
+        v1.axpy_w(st.acc, a1, b1);
+    } else {
+#pragma unroll
+        for (int i = 0; i < C::F; ++i) st.acc[i] = fmaf(p1, v1.f(i), fmaf(p0, v0.f(i), st.acc[i]));
+    }
+}
+
+// Neighbour ids of edges t and t+1 of a row (a valid id in place of a missing edge).
+__device__ __forceinline__ void edge_pair(const int32_t* __restrict__ cl, int64_t a, int deg, int t, int64_t self,
+                                          int64_t& j0, int64_t& j1) {
+    if (deg <= 0) {
+        j0 = j1 = self;
+        return;
+    }
+    const int last = deg - 1;
+    j0 = cl[a + (t < last ? t : last)];
+    j1 = cl[a + (t + 1 < last ? t + 1 : last)];
 }
 
 // ------------------------------------------------------------------ forward
@@ -121,9 +147,10 @@ __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t*
                                                        T* __restrict__ O, float* __restrict__ LSE, TilePartials tp) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
-    const int64_t wave = int64_t(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
+    const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
     const int64_t i = wave * C::NPW + ln.slot;
     const bool live = i < n;
+    const int64_t self = live ? i : 0;
     int64_t a = 0;
     int deg = 0;
     if (live) {
@@ -132,17 +159,15 @@ __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t*
         deg = dg > GT_LONG_ROW ? -1 : int(dg);
     }
     const int dmax = wave_max(deg);
-    const int64_t off = live ? ln.off(i) : 0;
+    const int64_t off = ln.off(self);
     Slice<T, C::F> q;
-    q.zero();
-    if (live) q.load(Q + off);
+    q.load(Q + off);
     Online<C::F> st;
     if (live && deg >= 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
     for (int t = 0; t < dmax; t += 2) {
-        const bool ok0 = t < deg, ok1 = t + 1 < deg;
-        const int64_t j0 = ok0 ? cl[a + t] : 0;
-        const int64_t j1 = ok1 ? cl[a + t + 1] : 0;
-        fwd_step<T, D, H>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2);
+        int64_t j0, j1;
+        edge_pair(cl, a, deg, t, self, j0, j1);
+        fwd_step<T, D, H>(st, q, K, V, j0, j1, t < deg, t + 1 < deg, ln, sl2);
     }
     if (live && deg >= 0) {
         const float inv = st.l > 0.f ? 1.f / st.l : 0.f;
@@ -228,18 +253,10 @@ __device__ __forceinline__ void dq_step(RowSums<EdgeCfg<T, D, H>::F>& rs, const 
                                         const Lanes<T, D, H>& ln, float sl2) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> k0, k1, v0, v1;
-    k0.zero();
-    k1.zero();
-    v0.zero();
-    v1.zero();
-    if (ok0) {
-        k0.load(K + ln.off(j0));
-        v0.load(V + ln.off(j0));
-    }
-    if (ok1) {
-        k1.load(K + ln.off(j1));
-        v1.load(V + ln.off(j1));
-    }
+    k0.load(K + ln.off(j0));
+    k1.load(K + ln.off(j1));
+    v0.load(V + ln.off(j0));
+    v1.load(V + ln.off(j1));
     const float s0 = group_sum<C::L>(q.dot(k0)) * sl2;
     const float s1 = group_sum<C::L>(q.dot(k1)) * sl2;
     const float dp0 = group_sum<C::L>(g.dot(v0));
@@ -288,9 +305,10 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
                                                        T* __restrict__ dQ, TilePartials tp) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
-    const int64_t wave = int64_t(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
+    const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
     const int64_t i = wave * C::NPW + ln.slot;
     const bool live = i < n;
+    const int64_t self = live ? i : 0;
     int64_t a = 0;
     int deg = 0;
     if (live) {
@@ -299,23 +317,17 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
         deg = dg > GT_LONG_ROW ? -1 : int(dg);
     }
     const int dmax = wave_max(deg);
-    const int64_t off = live ? ln.off(i) : 0;
+    const int64_t off = ln.off(self);
     Slice<T, C::F> q, g;
-    q.zero();
-    g.zero();
-    float lse2 = 0.f;
-    if (live) {
-        q.load(Q + off);
-        g.load(dO + off);
-        lse2 = LSE[i * H + ln.h] * kLog2e;
-    }
+    q.load(Q + off);
+    g.load(dO + off);
+    const float lse2 = LSE[self * H + ln.h] * kLog2e;
     RowSums<C::F> rs;
     if (live && deg >= 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
     for (int t = 0; t < dmax; t += 2) {
-        const bool ok0 = t < deg, ok1 = t + 1 < deg;
-        const int64_t j0 = ok0 ? cl[a + t] : 0;
-        const int64_t j1 = ok1 ? cl[a + t + 1] : 0;
-        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2);
+        int64_t j0, j1;
+        edge_pair(cl, a, deg, t, self, j0, j1);
+        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, t < deg, t + 1 < deg, ln, sl2);
     }
     if (live && deg >= 0) {
 #pragma unroll
@@ -389,23 +401,14 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
                                          const Lanes<T, D, H>& ln, float sl2) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> q0, q1, g0, g1;
-    q0.zero();
-    q1.zero();
-    g0.zero();
-    g1.zero();
-    float l0 = 0.f, l1 = 0.f, D0 = 0.f, D1 = 0.f;
-    if (ok0) {
-        q0.load(Q + ln.off(i0));
-        g0.load(dO + ln.off(i0));
-        l0 = LSE[i0 * H + ln.h] * kLog2e;
-        D0 = Dv[i0 * H + ln.h];
-    }
-    if (ok1) {
-        q1.load(Q + ln.off(i1));
-        g1.load(dO + ln.off(i1));
-        l1 = LSE[i1 * H + ln.h] * kLog2e;
-        D1 = Dv[i1 * H + ln.h];
-    }
+    q0.load(Q + ln.off(i0));
+    q1.load(Q + ln.off(i1));
+    g0.load(dO + ln.off(i0));
+    g1.load(dO + ln.off(i1));
+    const float l0 = LSE[i0 * H + ln.h] * kLog2e;
+    const float l1 = LSE[i1 * H + ln.h] * kLog2e;
+    const float D0 = Dv[i0 * H + ln.h];
+    const float D1 = Dv[i1 * H + ln.h];
     const float s0 = group_sum<C::L>(q0.dot(k)) * sl2;
     const float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
     const float dp0 = group_sum<C::L>(g0.dot(v));
@@ -431,9 +434,10 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
                                                        TilePartials tpv) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
-    const int64_t wave = int64_t(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
+    const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
     const int64_t j = wave * C::NPW + ln.slot;
     const bool live = j < n;
+    const int64_t self = live ? j : 0;
     int64_t a = 0;
     int deg = 0;
     if (live) {
@@ -442,24 +446,19 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
         deg = dg > GT_LONG_ROW ? -1 : int(dg);
     }
     const int dmax = wave_max(deg);
-    const int64_t off = live ? ln.off(j) : 0;
+    const int64_t off = ln.off(self);
     Slice<T, C::F> k, v;
-    k.zero();
-    v.zero();
-    if (live) {
-        k.load(K + off);
-        v.load(V + off);
-    }
+    k.load(K + off);
+    v.load(V + off);
     Acc<C::F> dk, dv;
     if (live && deg >= 0 && tpk.has_col(j)) {
         load_f32_slice<C::F>(dk.v, tpk.acc + off);
         load_f32_slice<C::F>(dv.v, tpv.acc + off);
     }
     for (int t = 0; t < dmax; t += 2) {
-        const bool ok0 = t < deg, ok1 = t + 1 < deg;
-        const int64_t i0 = ok0 ? rw[a + t] : 0;
-        const int64_t i1 = ok1 ? rw[a + t + 1] : 0;
-        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, ok0, ok1, ln, sl2);
+        int64_t i0, i1;
+        edge_pair(rw, a, deg, t, self, i0, i1);
+        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, t < deg, t + 1 < deg, ln, sl2);
     }
     if (live && deg >= 0) {
         store_slice<T, C::F>(dK + off, dk.v, scale);
@@ -547,7 +546,7 @@ gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V
         tp = TilePartials{};
     }
     const int64_t waves = cdiv(n, C::NPW);
-    k_fwd_rows<T, D, H><<<unsigned(cdiv(waves, kThreads / kWave)), kThreads, 0, s>>>(
+    k_fwd_rows<T, D, H><<<xcd_grid(cdiv(waves, kThreads / kWave)), kThreads, 0, s>>>(
         n, p->sp_rowptr, p->sp_col, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
         sl2, static_cast<T*>(O), LSE, tp);
     GT_LAUNCH_CHECK("sparse_fwd_rows");
@@ -576,7 +575,7 @@ gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const vo
     if (p->n_dense > 0) {
         if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, g, LSE, sl2, tb.dq, s)) != GT_OK) return st;
     }
-    const unsigned grid = unsigned(cdiv(cdiv(n, C::NPW), kThreads / kWave));
+    const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
     k_bwd_rows<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, Dv, sl2, scale,
                                                   static_cast<T*>(dQ), tb.dq);
     GT_LAUNCH_CHECK("sparse_bwd_rows");
@@ -605,7 +604,7 @@ gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const vo
     if (p->n_dense > 0) {
         if ((st = tile_bwd_dkdv<T, D, H>(p, q, k, v, g, LSE, Dv, sl2, tb.dk, tb.dv, s)) != GT_OK) return st;
     }
-    const unsigned grid = unsigned(cdiv(cdiv(n, C::NPW), kThreads / kWave));
+    const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
     k_bwd_cols<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2, scale,
                                                   static_cast<T*>(dK), static_cast<T*>(dV), tb.dk, tb.dv);
     GT_LAUNCH_CHECK("sparse_bwd_cols");
