@@ -67,6 +67,32 @@ def algorithmic_bytes(n, nnz, H, d, b):
     }
 
 
+EDGE_KERNEL_SOURCES = ("common.h", "attn_common.h", "sparse_attn.hip")
+
+
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from profiles/traffic_c4_edge_kernels.txt, if the kernel source still
+    (common.h, attn_common.h, sparse_attn.hip, concatenated) still matches the hash recorded with the counters
+    (otherwise None)."""
+    import hashlib
+
+    rec = os.path.join(ROOT, "profiles", "traffic_c4_edge_kernels.txt")
+    if not os.path.exists(rec):
+        return None
+    fields = {}
+    for line in open(rec):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for name in EDGE_KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2407_14106_amd", "csrc", name), "rb").read())
+    sha = h.hexdigest()[:16]
+    if fields.get("source_sha256_prefix") != sha or kernel not in fields:
+        return None
+    return int(fields[kernel])
+
+
 def cpu_baseline(w, target_s):
     """The fp64 oracle on a bounded sample: forward and backward for a block of rows/columns."""
     from oracle import attention as OA
@@ -283,7 +309,8 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": (recorded_traffic(dom_kernel) if args.workload == "c4" and args.scale == 1.0
+                        and plan.n_dense <= 16 else None),
             "kernel": dom_kernel,
             "stage": dom,
             "algorithmic_bytes": alg[dom],

@@ -13,10 +13,12 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // Lane layout of the edge kernels: each (node, head) is owned by L = D / F
-// consecutive lanes, each holding F consecutive features.
+// consecutive lanes, each holding F consecutive features (32 bytes of bf16, 64
+// of fp32), which keeps the per-lane register footprint small enough for
+// several resident wavefronts per SIMD to overlap their gathers.
 template <typename T, int D, int H>
 struct EdgeCfg {
-    static constexpr int F = sizeof(T) == 2 ? 32 : 16;  // features per lane (64 bytes)
+    static constexpr int F = 16;                        // features per lane
     static constexpr int L = D / F;                     // lanes per (node, head)
     static constexpr int G = H * L;                     // lanes per node
     static constexpr int NPW = kWave / G;               // nodes per wavefront
@@ -116,6 +118,19 @@ __device__ __forceinline__ void store_slice<uint16_t, 32>(uint16_t* p, const flo
     uint4* q = reinterpret_cast<uint4*>(p);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+        uint4 o;
+        o.x = pack_bf16x2(v[8 * i + 0] * scale, v[8 * i + 1] * scale);
+        o.y = pack_bf16x2(v[8 * i + 2] * scale, v[8 * i + 3] * scale);
+        o.z = pack_bf16x2(v[8 * i + 4] * scale, v[8 * i + 5] * scale);
+        o.w = pack_bf16x2(v[8 * i + 6] * scale, v[8 * i + 7] * scale);
+        q[i] = o;
+    }
+}
+template <>
+__device__ __forceinline__ void store_slice<uint16_t, 16>(uint16_t* p, const float (&v)[16], float scale) {
+    uint4* q = reinterpret_cast<uint4*>(p);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
         uint4 o;
         o.x = pack_bf16x2(v[8 * i + 0] * scale, v[8 * i + 1] * scale);
         o.y = pack_bf16x2(v[8 * i + 2] * scale, v[8 * i + 3] * scale);
