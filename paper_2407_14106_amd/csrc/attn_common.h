@@ -109,42 +109,28 @@ __device__ __forceinline__ void axpy(float (&acc)[F], float p, const Slice<T, F>
     for (int i = 0; i < F; ++i) acc[i] = fmaf(p, x.f(i), acc[i]);
 }
 
-// Store F fp32 values as T (bf16: round to nearest even).
+// Store F fp32 values, times scale, as T (bf16: round to nearest even).
 template <typename T, int F>
-__device__ __forceinline__ void store_slice(T* p, const float (&v)[F], float scale);
-
-template <>
-__device__ __forceinline__ void store_slice<uint16_t, 32>(uint16_t* p, const float (&v)[32], float scale) {
-    uint4* q = reinterpret_cast<uint4*>(p);
+__device__ __forceinline__ void store_slice(T* p, const float (&v)[F], float scale) {
+    if constexpr (sizeof(T) == 2) {
+        static_assert(F % 8 == 0, "bf16 slices are stored 16 bytes at a time");
+        uint4* q = reinterpret_cast<uint4*>(p);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        uint4 o;
-        o.x = pack_bf16x2(v[8 * i + 0] * scale, v[8 * i + 1] * scale);
-        o.y = pack_bf16x2(v[8 * i + 2] * scale, v[8 * i + 3] * scale);
-        o.z = pack_bf16x2(v[8 * i + 4] * scale, v[8 * i + 5] * scale);
-        o.w = pack_bf16x2(v[8 * i + 6] * scale, v[8 * i + 7] * scale);
-        q[i] = o;
+        for (int i = 0; i < F / 8; ++i) {
+            uint4 o;
+            o.x = pack_bf16x2(v[8 * i + 0] * scale, v[8 * i + 1] * scale);
+            o.y = pack_bf16x2(v[8 * i + 2] * scale, v[8 * i + 3] * scale);
+            o.z = pack_bf16x2(v[8 * i + 4] * scale, v[8 * i + 5] * scale);
+            o.w = pack_bf16x2(v[8 * i + 6] * scale, v[8 * i + 7] * scale);
+            q[i] = o;
+        }
+    } else {
+        static_assert(F % 4 == 0, "fp32 slices are stored 16 bytes at a time");
+        float4* q = reinterpret_cast<float4*>(p);
+#pragma unroll
+        for (int i = 0; i < F / 4; ++i)
+            q[i] = make_float4(v[4 * i] * scale, v[4 * i + 1] * scale, v[4 * i + 2] * scale, v[4 * i + 3] * scale);
     }
-}
-template <>
-__device__ __forceinline__ void store_slice<uint16_t, 16>(uint16_t* p, const float (&v)[16], float scale) {
-    uint4* q = reinterpret_cast<uint4*>(p);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        uint4 o;
-        o.x = pack_bf16x2(v[8 * i + 0] * scale, v[8 * i + 1] * scale);
-        o.y = pack_bf16x2(v[8 * i + 2] * scale, v[8 * i + 3] * scale);
-        o.z = pack_bf16x2(v[8 * i + 4] * scale, v[8 * i + 5] * scale);
-        o.w = pack_bf16x2(v[8 * i + 6] * scale, v[8 * i + 7] * scale);
-        q[i] = o;
-    }
-}
-template <>
-__device__ __forceinline__ void store_slice<float, 16>(float* p, const float (&v)[16], float scale) {
-    float4* q = reinterpret_cast<float4*>(p);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) q[i] = make_float4(v[4 * i] * scale, v[4 * i + 1] * scale, v[4 * i + 2] * scale,
-                                                   v[4 * i + 3] * scale);
 }
 
 // Sum over the L lanes that share one (node, head).

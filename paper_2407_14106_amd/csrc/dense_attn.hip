@@ -1,5 +1,6 @@
 // Full softmax attention (§2.1 Eq. (1)): the interleaved fully-connected layer
-// of §3.2, on the matrix-core tile kernels with every pair attended.
+// of §3.2.  bf16 features run the streaming kernels of dense_mfma.hip; fp32
+// features run the matrix-core tile kernels with every pair attended.
 #include "tile_attn.h"
 
 using namespace gt;
@@ -20,6 +21,9 @@ template <typename T, int D, int H>
 gt_status run_dense_fwd(int64_t n, const void* Q, const void* K, const void* V, float scale, void* O, float* LSE,
                         hipStream_t s) {
     if (n == 0) return GT_OK;
+    if constexpr (sizeof(T) == 2)
+        return full_fwd_bf16<D>(n, H, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
+                                scale * kLog2e, static_cast<T*>(O), LSE, s);
     return full_fwd<T, D, H>(n, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
                              scale * kLog2e, static_cast<T*>(O), LSE, s);
 }
@@ -30,6 +34,10 @@ gt_status run_dense_bwd(int64_t n, const void* Q, const void* K, const void* V, 
     if (n == 0) return GT_OK;
     Ws w(ws);
     float* Dv = w.take<float>(size_t(n) * H);
+    if constexpr (sizeof(T) == 2)
+        return full_bwd_bf16<D>(n, H, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
+                                static_cast<const T*>(O), static_cast<const T*>(dO), LSE, scale * kLog2e, scale,
+                                static_cast<T*>(dQ), static_cast<T*>(dK), static_cast<T*>(dV), Dv, s);
     return full_bwd<T, D, H>(n, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
                              static_cast<const T*>(O), static_cast<const T*>(dO), LSE, scale * kLog2e, scale,
                              static_cast<T*>(dQ), static_cast<T*>(dK), static_cast<T*>(dV), Dv, s);

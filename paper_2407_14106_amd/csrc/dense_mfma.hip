@@ -1,0 +1,620 @@
+// Full softmax attention for bf16 features on the matrix cores: the
+// interleaved fully-connected layer of §3.2 (every node attends to every node,
+// Eq. (1) of §2.1), forward and backward, streaming over the keys with no
+// n x n buffer.
+//
+// Design (CDNA4, wave64, v_mfma_f32_32x32x16_bf16):
+//   - A workgroup is 4 wavefronts; each wavefront owns 64 rows (two 32-row
+//     MFMA blocks) of one head, so every operand fragment read from LDS feeds
+//     two products.  The partner rows stream through LDS in 64-row stages,
+//     double buffered: the next stage is loaded into registers while the
+//     current one is multiplied, then written to the other buffer, with one
+//     barrier per stage.
+//   - Scores are formed transposed (partners x owned rows), so each lane holds
+//     one owned row and 16 of its partners; per-row statistics need one
+//     v_permlane32_swap between the half-waves.  The probabilities (or dS)
+//     become the next product's B operand straight from the accumulators; the
+//     A operand of that product (V^T, K^T, dO^T, Q^T) is read from a
+//     transposed LDS copy written as 4-partner x 4-feature blocks.
+//   - The forward's running maximum is lazy: the accumulators are rescaled
+//     only when some row's block maximum exceeds it by 2^8 (exp2 domain), so
+//     weights stay below 256 and the result is unchanged.
+//   - D_i = <dO_i, O_i> from the given O: every full-layer weight is O(1/n),
+//     so no cancellation-prone sum over partners is needed.
+//   - Workgroups are remapped so that each XCD works on one range of
+//     (head, row block) pairs and shares that head's K and V in its L2.
+#include "tile_attn.h"
+
+namespace gt {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kWaves = 4;                // wavefronts per workgroup
+constexpr int kThr = kWaves * kWave;     // threads per workgroup
+constexpr int kOwn = 64;                 // owned rows per wavefront
+constexpr int kRowsWg = kWaves * kOwn;   // owned rows per workgroup
+constexpr int kStage = 64;               // partner rows per LDS stage
+constexpr int kTS = kStage + 4;          // transposed LDS row stride (elements)
+constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kLazy = 8.f;             // lazy-max slack, exp2 domain
+
+template <int D>
+struct RS {
+    static constexpr int v = D + 8;  // row-major LDS row stride (elements)
+};
+
+__device__ __forceinline__ int crow(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ f32x16_t zero16() {
+    f32x16_t z;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) z[i] = 0.f;
+    return z;
+}
+
+__device__ __forceinline__ f32x16_t mma(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// The value of x held by the partner lane (lane ^ 32) combined with x.
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// A operand from a row-major LDS tile: row r, features 16c + 8(lane/32) .. +7.
+template <int D>
+__device__ __forceinline__ bf16x8_t lds_row8(const uint16_t* s, int r, int c, int lane) {
+    return __builtin_bit_cast(bf16x8_t,
+                              *reinterpret_cast<const uint4*>(s + r * RS<D>::v + 16 * c + 8 * (lane >> 5)));
+}
+// A operand from a transposed LDS tile (row = feature f): partners
+// base + 4(lane/32) + {0..3} and base + 8 + 4(lane/32) + {0..3}, the partner
+// order of an accumulator-layout B operand (acc_b16).
+__device__ __forceinline__ bf16x8_t lds_perm8(const uint16_t* s, int f, int base, int lane) {
+    const uint16_t* p = s + f * kTS + base + 4 * (lane >> 5);
+    const uint2 a = *reinterpret_cast<const uint2*>(p);
+    const uint2 b = *reinterpret_cast<const uint2*>(p + 8);
+    return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
+}
+// Accumulator elements 8*half .. +7 as a bf16 B operand.
+__device__ __forceinline__ bf16x8_t acc_b16(const f32x16_t& c, int half) {
+    bf16x8_t o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = (__bf16)c[8 * half + t];
+    return o;
+}
+
+// B operand fragments of one owned row (global memory): features
+// 16c + 8(lane/32) .. +7 for c < D/16; zero for rows >= n.
+template <int D>
+struct Frag {
+    bf16x8_t v[D / 16];
+    __device__ __forceinline__ void load(const uint16_t* X, int64_t row, int64_t n, int H, int h, int lane) {
+        const int64_t src = row < n ? row : n - 1;
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c) {
+            uint4 x = *reinterpret_cast<const uint4*>(X + (src * H + h) * D + 16 * c + 8 * (lane >> 5));
+            if (row >= n) x = make_uint4(0, 0, 0, 0);
+            v[c] = __builtin_bit_cast(bf16x8_t, x);
+        }
+    }
+    // this lane's share of <this, o>
+    __device__ __forceinline__ float dot(const Frag& o) const {
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c)
+#pragma unroll
+            for (int t = 0; t < 8; ++t) s = fmaf(float(v[c][t]), float(o.v[c][t]), s);
+        return s;
+    }
+};
+
+// One thread's share of a 64-row stage of X[:, h, :]: a block of 4 rows x 4
+// features (8 bytes per row), kept in registers between the global load and
+// the LDS stores.  Loads are unconditional (rows past n read row n-1) so the
+// compiler can keep them in flight across the stage's products; rows >= n are
+// zeroed when stored.
+template <int D>
+struct Stager {
+    static constexpr int FG = D / 4;       // feature groups per row
+    static constexpr int kItems = 16 * FG; // (row group, feature group) blocks
+    static_assert(kItems <= kThr && kThr % kItems == 0, "stage does not fit the workgroup");
+    uint2 r[4];
+    int rg, fg;
+    uint32_t valid;  // bit j: row 4 rg + j < n
+    __device__ __forceinline__ Stager() {
+        const int t = threadIdx.x % kItems;
+        rg = t / FG;
+        fg = t % FG;
+    }
+    // Threads beyond kItems (whole wavefronts) only mirror the loads.
+    __device__ __forceinline__ bool on() const { return kItems == kThr || threadIdx.x < kItems; }
+    __device__ __forceinline__ void load(const uint16_t* __restrict__ X, int64_t base, int64_t n, int H, int h) {
+        valid = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t node = base + 4 * rg + j;
+            const int64_t src = node < n ? node : n - 1;
+            valid |= uint32_t(node < n) << j;
+            r[j] = *reinterpret_cast<const uint2*>(X + (src * H + h) * D + 4 * fg);
+        }
+    }
+    __device__ __forceinline__ uint2 row(int j) const {
+        return (valid >> j) & 1u ? r[j] : make_uint2(0, 0);
+    }
+    __device__ __forceinline__ void store_rm(uint16_t* s) const {
+        if (!on()) return;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint2*>(s + (4 * rg + j) * RS<D>::v + 4 * fg) = row(j);
+    }
+    // s[f * kTS + row]: the 4 rows of each of the 4 features as one 8-byte store.
+    __device__ __forceinline__ void store_tr(uint16_t* s) const {
+        if (!on()) return;
+        const uint2 a = row(0), b = row(1), c = row(2), d = row(3);
+        const uint32_t lo = 0xFFFFu, hi = 0xFFFF0000u;
+        uint16_t* p = s + (4 * fg) * kTS + 4 * rg;
+        *reinterpret_cast<uint2*>(p) = make_uint2((a.x & lo) | (b.x << 16), (c.x & lo) | (d.x << 16));
+        *reinterpret_cast<uint2*>(p + kTS) = make_uint2((a.x >> 16) | (b.x & hi), (c.x >> 16) | (d.x & hi));
+        *reinterpret_cast<uint2*>(p + 2 * kTS) = make_uint2((a.y & lo) | (b.y << 16), (c.y & lo) | (d.y << 16));
+        *reinterpret_cast<uint2*>(p + 3 * kTS) = make_uint2((a.y >> 16) | (b.y & hi), (c.y >> 16) | (d.y & hi));
+    }
+};
+
+// All outstanding memory operations of this wavefront are complete (so the
+// compiler's wait counting starts the streaming loop from a clean state).
+__device__ __forceinline__ void drain() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Workgroup -> (head, first owned row); false for the padding of the grid.
+__device__ __forceinline__ bool wg_coords(int64_t n, int H, int& h, int64_t& row0) {
+    const int64_t blocks = cdiv(n, kRowsWg);
+    const int64_t b = xcd_block(blockIdx.x, gridDim.x);
+    if (b >= blocks * H) return false;
+    h = int(b / blocks);
+    row0 = (b % blocks) * kRowsWg;
+    return true;
+}
+
+inline unsigned full_grid(int64_t n, int H) { return xcd_grid(cdiv(n, kRowsWg) * H); }
+
+// ------------------------------------------------------------------ forward
+
+template <int D>
+__global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const uint16_t* __restrict__ Q,
+                                                      const uint16_t* __restrict__ K,
+                                                      const uint16_t* __restrict__ V, float sl2,
+                                                      uint16_t* __restrict__ O, float* __restrict__ LSE) {
+    __shared__ __attribute__((aligned(16))) uint16_t sK[2][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sVt[2][D * kTS];
+    int h;
+    int64_t row0;
+    if (!wg_coords(n, H, h, row0)) return;
+    const int lane = lane_id();
+    const int64_t q0 = row0 + (threadIdx.x / kWave) * kOwn;
+    Frag<D> qf[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) qf[b].load(Q, q0 + 32 * b + (lane & 31), n, H, h, lane);
+    if (sl2 < 0.f) {  // keep the exp2-domain scale positive: negate Q instead (exact in bf16)
+        sl2 = -sl2;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c)
+                qf[b].v[c] = __builtin_bit_cast(bf16x8_t, __builtin_bit_cast(uint4, qf[b].v[c]) ^
+                                                              make_uint4(0x80008000u, 0x80008000u, 0x80008000u,
+                                                                         0x80008000u));
+    }
+    f32x16_t acc[2][D / 32];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
+    float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
+
+    Stager<D> gk, gv;
+    gk.load(K, 0, n, H, h);
+    gv.load(V, 0, n, H, h);
+    gk.store_rm(sK[0]);
+    gv.store_tr(sVt[0]);
+    drain();
+    __syncthreads();
+    const int64_t stages = cdiv(n, kStage);
+    for (int64_t t = 0; t < stages; ++t) {
+        const int buf = int(t & 1);
+        const int64_t kbase = t * kStage;
+        if (t + 1 < stages) {
+            gk.load(K, kbase + kStage, n, H, h);
+            gv.load(V, kbase + kStage, n, H, h);
+        }
+        const uint16_t* k_s = sK[buf];
+        const uint16_t* v_s = sVt[buf];
+#pragma unroll
+        for (int kb = 0; kb < kStage / 32; ++kb) {
+            f32x16_t s[2];
+            s[0] = s[1] = zero16();
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) {
+                const bf16x8_t a = lds_row8<D>(k_s, 32 * kb + (lane & 31), c, lane);
+                s[0] = mma(a, qf[0].v[c], s[0]);
+                s[1] = mma(a, qf[1].v[c], s[1]);
+            }
+            const int64_t key0 = kbase + 32 * kb;
+            if (key0 + 32 > n) {  // ragged last block: partners >= n take no weight
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    if (key0 + crow(i, lane) >= n) s[0][i] = s[1][i] = kNegInf;
+            }
+            bool grow = false;
+            float mt[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                float mx = s[b][0];
+#pragma unroll
+                for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[b][i]);
+                mt[b] = pair_max(mx) * sl2;
+                grow |= mt[b] > m[b] + kLazy;
+            }
+            if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const float mn = fmaxf(m[b], mt[b]);
+                    const float alpha = ex2(m[b] - mn);
+                    l[b] *= alpha;
+#pragma unroll
+                    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) acc[b][db][i] *= alpha;
+                    m[b] = mn;
+                }
+            }
+            bf16x8_t pb[2][2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                float ls = 0.f;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = ex2(fmaf(s[b][i], sl2, -m[b]));
+                    s[b][i] = p;
+                    ls += p;
+                }
+                l[b] += ls;
+                pb[b][0] = acc_b16(s[b], 0);
+                pb[b][1] = acc_b16(s[b], 1);
+            }
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    const bf16x8_t a = lds_perm8(v_s, 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
+                    acc[0][db] = mma(a, pb[0][half], acc[0][db]);
+                    acc[1][db] = mma(a, pb[1][half], acc[1][db]);
+                }
+        }
+        if (t + 1 < stages) {
+            gk.store_rm(sK[buf ^ 1]);
+            gv.store_tr(sVt[buf ^ 1]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t q = q0 + 32 * b + (lane & 31);
+        const float lt = pair_sum(l[b]);
+        if (q >= n) continue;
+        const float inv = lt > 0.f ? 1.f / lt : 0.f;
+        if (lane < 32) LSE[q * H + h] = lt > 0.f ? (m[b] + __log2f(lt)) * kLn2 : kNegInf;
+        uint16_t* o = O + (q * H + h) * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x16_t& a = acc[b][db];
+                *reinterpret_cast<uint2*>(o + 32 * db + 8 * j + 4 * (lane >> 5)) =
+                    make_uint2(pack_bf16x2(a[4 * j] * inv, a[4 * j + 1] * inv),
+                               pack_bf16x2(a[4 * j + 2] * inv, a[4 * j + 3] * inv));
+            }
+    }
+}
+
+// ---------------------------------------------------------------- dQ (rows)
+// dQ_i = scale sum_j P_ij (dP_ij - D_i) K_j with dP_ij = <dO_i, V_j>; also
+// writes D_i for the column pass.
+
+template <int D>
+__global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uint16_t* __restrict__ Q,
+                                                     const uint16_t* __restrict__ K,
+                                                     const uint16_t* __restrict__ V,
+                                                     const uint16_t* __restrict__ O,
+                                                     const uint16_t* __restrict__ dO,
+                                                     const float* __restrict__ LSE, float sl2, float scale,
+                                                     uint16_t* __restrict__ dQ, float* __restrict__ Dv) {
+    __shared__ __attribute__((aligned(16))) uint16_t sK[2][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[2][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sKt[2][D * kTS];
+    int h;
+    int64_t row0;
+    if (!wg_coords(n, H, h, row0)) return;
+    const int lane = lane_id();
+    const int64_t q0 = row0 + (threadIdx.x / kWave) * kOwn;
+    Frag<D> qf[2], gf[2];
+    float lse2[2], Dq[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t q = q0 + 32 * b + (lane & 31);
+        qf[b].load(Q, q, n, H, h, lane);
+        gf[b].load(dO, q, n, H, h, lane);
+        Frag<D> of;
+        of.load(O, q, n, H, h, lane);
+        Dq[b] = pair_sum(gf[b].dot(of));
+        lse2[b] = q < n ? LSE[q * H + h] * kLog2e : 0.f;
+        if (q < n && lane < 32) Dv[q * H + h] = Dq[b];
+    }
+    f32x16_t acc[2][D / 32];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
+
+    Stager<D> gk, gv;
+    gk.load(K, 0, n, H, h);
+    gv.load(V, 0, n, H, h);
+    gk.store_rm(sK[0]);
+    gk.store_tr(sKt[0]);
+    gv.store_rm(sV[0]);
+    drain();
+    __syncthreads();
+    const int64_t stages = cdiv(n, kStage);
+    for (int64_t t = 0; t < stages; ++t) {
+        const int buf = int(t & 1);
+        const int64_t kbase = t * kStage;
+        if (t + 1 < stages) {
+            gk.load(K, kbase + kStage, n, H, h);
+            gv.load(V, kbase + kStage, n, H, h);
+        }
+#pragma unroll
+        for (int kb = 0; kb < kStage / 32; ++kb) {
+            f32x16_t s[2], dp[2];
+            s[0] = s[1] = dp[0] = dp[1] = zero16();
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) {
+                const bf16x8_t a = lds_row8<D>(sK[buf], 32 * kb + (lane & 31), c, lane);
+                s[0] = mma(a, qf[0].v[c], s[0]);
+                s[1] = mma(a, qf[1].v[c], s[1]);
+                const bf16x8_t v = lds_row8<D>(sV[buf], 32 * kb + (lane & 31), c, lane);
+                dp[0] = mma(v, gf[0].v[c], dp[0]);
+                dp[1] = mma(v, gf[1].v[c], dp[1]);
+            }
+            const int64_t key0 = kbase + 32 * kb;
+            if (key0 + 32 > n) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    if (key0 + crow(i, lane) >= n) s[0][i] = s[1][i] = kNegInf;
+            }
+            bf16x8_t db16[2][2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = ex2(fmaf(s[b][i], sl2, -lse2[b]));
+                    s[b][i] = p * (dp[b][i] - Dq[b]);
+                }
+                db16[b][0] = acc_b16(s[b], 0);
+                db16[b][1] = acc_b16(s[b], 1);
+            }
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    const bf16x8_t a = lds_perm8(sKt[buf], 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
+                    acc[0][db] = mma(a, db16[0][half], acc[0][db]);
+                    acc[1][db] = mma(a, db16[1][half], acc[1][db]);
+                }
+        }
+        if (t + 1 < stages) {
+            gk.store_rm(sK[buf ^ 1]);
+            gk.store_tr(sKt[buf ^ 1]);
+            gv.store_rm(sV[buf ^ 1]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t q = q0 + 32 * b + (lane & 31);
+        if (q >= n) continue;
+        uint16_t* o = dQ + (q * H + h) * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x16_t& a = acc[b][db];
+                *reinterpret_cast<uint2*>(o + 32 * db + 8 * j + 4 * (lane >> 5)) =
+                    make_uint2(pack_bf16x2(a[4 * j] * scale, a[4 * j + 1] * scale),
+                               pack_bf16x2(a[4 * j + 2] * scale, a[4 * j + 3] * scale));
+            }
+    }
+}
+
+// ----------------------------------------------------------- dK, dV (cols)
+// dK_j = scale sum_i P_ij (dP_ij - D_i) Q_i and dV_j = sum_i P_ij dO_i, with
+// the wavefront owning 64 keys and the queries streaming through LDS.
+
+template <int D>
+__global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const uint16_t* __restrict__ Q,
+                                                       const uint16_t* __restrict__ K,
+                                                       const uint16_t* __restrict__ V,
+                                                       const uint16_t* __restrict__ dO,
+                                                       const float* __restrict__ LSE,
+                                                       const float* __restrict__ Dv, float sl2, float scale,
+                                                       uint16_t* __restrict__ dK, uint16_t* __restrict__ dV) {
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[2][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sG[2][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sQt[2][D * kTS];
+    __shared__ __attribute__((aligned(16))) uint16_t sGt[2][D * kTS];
+    __shared__ __attribute__((aligned(16))) float sL[2][kStage];
+    __shared__ __attribute__((aligned(16))) float sD[2][kStage];
+    int h;
+    int64_t row0;
+    if (!wg_coords(n, H, h, row0)) return;
+    const int lane = lane_id();
+    const int64_t k0 = row0 + (threadIdx.x / kWave) * kOwn;
+    Frag<D> kf[2], vf[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        kf[b].load(K, k0 + 32 * b + (lane & 31), n, H, h, lane);
+        vf[b].load(V, k0 + 32 * b + (lane & 31), n, H, h, lane);
+    }
+    f32x16_t dk[2][D / 32], dv[2][D / 32];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) dk[b][db] = dv[b][db] = zero16();
+
+    // LSE (exp2 domain) and D of the stage's queries; queries >= n get
+    // LSE = +inf so that their weights are exactly zero.
+    auto stage_rows = [&](int buf, int64_t base) {
+        if (threadIdx.x < kStage) {
+            const int64_t qn = base + threadIdx.x;
+            sL[buf][threadIdx.x] = qn < n ? LSE[qn * H + h] * kLog2e : __builtin_huge_valf();
+            sD[buf][threadIdx.x] = qn < n ? Dv[qn * H + h] : 0.f;
+        }
+    };
+    Stager<D> gq, gg;
+    gq.load(Q, 0, n, H, h);
+    gg.load(dO, 0, n, H, h);
+    gq.store_rm(sQ[0]);
+    gq.store_tr(sQt[0]);
+    gg.store_rm(sG[0]);
+    gg.store_tr(sGt[0]);
+    stage_rows(0, 0);
+    drain();
+    __syncthreads();
+    const int64_t stages = cdiv(n, kStage);
+    for (int64_t t = 0; t < stages; ++t) {
+        const int buf = int(t & 1);
+        const int64_t qbase = t * kStage;
+        if (t + 1 < stages) {
+            gq.load(Q, qbase + kStage, n, H, h);
+            gg.load(dO, qbase + kStage, n, H, h);
+        }
+#pragma unroll
+        for (int qb = 0; qb < kStage / 32; ++qb) {
+            f32x16_t s[2], dp[2];
+            s[0] = s[1] = dp[0] = dp[1] = zero16();
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) {
+                const bf16x8_t a = lds_row8<D>(sQ[buf], 32 * qb + (lane & 31), c, lane);
+                s[0] = mma(a, kf[0].v[c], s[0]);
+                s[1] = mma(a, kf[1].v[c], s[1]);
+                const bf16x8_t g = lds_row8<D>(sG[buf], 32 * qb + (lane & 31), c, lane);
+                dp[0] = mma(g, vf[0].v[c], dp[0]);
+                dp[1] = mma(g, vf[1].v[c], dp[1]);
+            }
+            // rows of accumulator element i: 32 qb + 8 (i/4) + 4 (lane/32) + i%4
+            float Lr[16], Dr[16];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 32 * qb + 8 * j + 4 * (lane >> 5);
+                const float4 lv = *reinterpret_cast<const float4*>(&sL[buf][r]);
+                const float4 dv4 = *reinterpret_cast<const float4*>(&sD[buf][r]);
+                Lr[4 * j] = lv.x, Lr[4 * j + 1] = lv.y, Lr[4 * j + 2] = lv.z, Lr[4 * j + 3] = lv.w;
+                Dr[4 * j] = dv4.x, Dr[4 * j + 1] = dv4.y, Dr[4 * j + 2] = dv4.z, Dr[4 * j + 3] = dv4.w;
+            }
+            bf16x8_t pb[2][2], sb[2][2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = ex2(fmaf(s[b][i], sl2, -Lr[i]));
+                    s[b][i] = p * (dp[b][i] - Dr[i]);
+                    dp[b][i] = p;
+                }
+                pb[b][0] = acc_b16(dp[b], 0);
+                pb[b][1] = acc_b16(dp[b], 1);
+                sb[b][0] = acc_b16(s[b], 0);
+                sb[b][1] = acc_b16(s[b], 1);
+            }
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    const bf16x8_t g = lds_perm8(sGt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
+                    dv[0][db] = mma(g, pb[0][half], dv[0][db]);
+                    dv[1][db] = mma(g, pb[1][half], dv[1][db]);
+                    const bf16x8_t a = lds_perm8(sQt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
+                    dk[0][db] = mma(a, sb[0][half], dk[0][db]);
+                    dk[1][db] = mma(a, sb[1][half], dk[1][db]);
+                }
+        }
+        if (t + 1 < stages) {
+            gq.store_rm(sQ[buf ^ 1]);
+            gq.store_tr(sQt[buf ^ 1]);
+            gg.store_rm(sG[buf ^ 1]);
+            gg.store_tr(sGt[buf ^ 1]);
+            stage_rows(buf ^ 1, qbase + kStage);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t key = k0 + 32 * b + (lane & 31);
+        if (key >= n) continue;
+        uint16_t* ok = dK + (key * H + h) * D;
+        uint16_t* ov = dV + (key * H + h) * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int f = 32 * db + 8 * j + 4 * (lane >> 5);
+                const f32x16_t& a = dk[b][db];
+                const f32x16_t& c = dv[b][db];
+                *reinterpret_cast<uint2*>(ok + f) =
+                    make_uint2(pack_bf16x2(a[4 * j] * scale, a[4 * j + 1] * scale),
+                               pack_bf16x2(a[4 * j + 2] * scale, a[4 * j + 3] * scale));
+                *reinterpret_cast<uint2*>(ov + f) =
+                    make_uint2(pack_bf16x2(c[4 * j], c[4 * j + 1]), pack_bf16x2(c[4 * j + 2], c[4 * j + 3]));
+            }
+    }
+}
+
+}  // namespace
+
+template <int D>
+gt_status full_fwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V, float sl2,
+                        uint16_t* O, float* LSE, hipStream_t s) {
+    if (n <= 0) return GT_OK;
+    k_full_fwd<D><<<full_grid(n, H), kThr, 0, s>>>(n, H, Q, K, V, sl2, O, LSE);
+    GT_LAUNCH_CHECK("full_fwd_bf16");
+    return GT_OK;
+}
+
+template <int D>
+gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        const uint16_t* O, const uint16_t* dO, const float* LSE, float sl2, float scale,
+                        uint16_t* dQ, uint16_t* dK, uint16_t* dV, float* Dv, hipStream_t s) {
+    if (n <= 0) return GT_OK;
+    k_full_dq<D><<<full_grid(n, H), kThr, 0, s>>>(n, H, Q, K, V, O, dO, LSE, sl2, scale, dQ, Dv);
+    GT_LAUNCH_CHECK("full_bwd_bf16 dq");
+    k_full_dkdv<D><<<full_grid(n, H), kThr, 0, s>>>(n, H, Q, K, V, dO, LSE, Dv, sl2, scale, dK, dV);
+    GT_LAUNCH_CHECK("full_bwd_bf16 dkdv");
+    return GT_OK;
+}
+
+template gt_status full_fwd_bf16<32>(int64_t, int, const uint16_t*, const uint16_t*, const uint16_t*, float,
+                                     uint16_t*, float*, hipStream_t);
+template gt_status full_fwd_bf16<64>(int64_t, int, const uint16_t*, const uint16_t*, const uint16_t*, float,
+                                     uint16_t*, float*, hipStream_t);
+template gt_status full_bwd_bf16<32>(int64_t, int, const uint16_t*, const uint16_t*, const uint16_t*,
+                                     const uint16_t*, const uint16_t*, const float*, float, float, uint16_t*,
+                                     uint16_t*, uint16_t*, float*, hipStream_t);
+template gt_status full_bwd_bf16<64>(int64_t, int, const uint16_t*, const uint16_t*, const uint16_t*,
+                                     const uint16_t*, const uint16_t*, const float*, float, float, uint16_t*,
+                                     uint16_t*, uint16_t*, float*, hipStream_t);
+
+}  // namespace gt

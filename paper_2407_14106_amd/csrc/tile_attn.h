@@ -91,4 +91,15 @@ template <typename T, int D, int H>
 gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, const T* dO, const float* LSE,
                    float sl2, float scale, T* dQ, T* dK, T* dV, float* Dv, hipStream_t s);
 
+// The full layer for bf16 features (dense_mfma.hip): the streaming kernels
+// with two 32-row blocks per wavefront; same results contract as full_fwd /
+// full_bwd.  H is a runtime value.
+template <int D>
+gt_status full_fwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V, float sl2,
+                        uint16_t* O, float* LSE, hipStream_t s);
+template <int D>
+gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        const uint16_t* O, const uint16_t* dO, const float* LSE, float sl2, float scale,
+                        uint16_t* dQ, uint16_t* dK, uint16_t* dV, float* Dv, hipStream_t s);
+
 }  // namespace gt
