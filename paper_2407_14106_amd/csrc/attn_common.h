@@ -133,11 +133,15 @@ __device__ __forceinline__ void store_slice(T* p, const float (&v)[F], float sca
     }
 }
 
-// Sum over the L lanes that share one (node, head).
+// Sum over the L lanes that share one (node, head).  Groups of 2 or 4 lanes sit
+// inside one DPP quad, so the exchanges are quad permutes (xor 1, xor 2) that
+// stay off the LDS; every lane of a group is active whenever one is.
 template <int L>
 __device__ __forceinline__ float group_sum(float x) {
+    if constexpr (L >= 2) x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
+    if constexpr (L >= 4) x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));
 #pragma unroll
-    for (int o = 1; o < L; o <<= 1) x += __shfl_xor(x, o, kWave);
+    for (int o = 4; o < L; o <<= 1) x += __shfl_xor(x, o, kWave);
     return x;
 }
 

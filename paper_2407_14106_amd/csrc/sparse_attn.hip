@@ -126,23 +126,50 @@ __device__ __forceinline__ void fwd_step(Online<EdgeCfg<T, D, H>::F>& st, const 
     }
 }
 
-// Neighbour ids of edges t and t+1 of a row (a valid id in place of a missing edge).
-__device__ __forceinline__ void edge_pair(const int32_t* __restrict__ cl, int64_t a, int deg, int t, int64_t self,
-                                          int64_t& j0, int64_t& j1) {
-    if (deg <= 0) {
-        j0 = j1 = self;
-        return;
+// Neighbour ids of edges t .. t+3 of a row whose list is cl[a, a + deg) in an
+// array of `len` entries: one 16-byte load where the array allows it (ids past
+// the row are read but replaced).  Missing edges get a valid id: the row's
+// edge t if it exists, else `self`.
+__device__ __forceinline__ int4 edge_quad(const int32_t* __restrict__ cl, int64_t len, int64_t a, int deg, int t,
+                                          int32_t self) {
+    if (deg <= t) return make_int4(self, self, self, self);
+    int4 v;
+    if (a + t + 4 <= len) {
+        v = *reinterpret_cast<const int4*>(cl + a + t);
+    } else {
+        const int last = deg - 1;
+        v.x = cl[a + t];
+        v.y = cl[a + (t + 1 < last ? t + 1 : last)];
+        v.z = cl[a + (t + 2 < last ? t + 2 : last)];
+        v.w = cl[a + (t + 3 < last ? t + 3 : last)];
     }
-    const int last = deg - 1;
-    j0 = cl[a + (t < last ? t : last)];
-    j1 = cl[a + (t + 1 < last ? t + 1 : last)];
+    if (t + 1 >= deg) v.y = v.x;
+    if (t + 2 >= deg) v.z = v.x;
+    if (t + 3 >= deg) v.w = v.x;
+    return v;
+}
+
+// Walk a row's edges four at a time up to the wavefront maximum dmax, the ids
+// of the next four fetched before the current four are used; step(j0, j1,
+// ok0, ok1) takes two edges.
+template <class Step>
+__device__ __forceinline__ void walk_edges(const int32_t* __restrict__ cl, int64_t len, int64_t a, int deg, int dmax,
+                                           int32_t self, Step step) {
+    int4 cur = edge_quad(cl, len, a, deg, 0, self), nxt = cur;
+    for (int t = 0; t < dmax; t += 4) {
+        if (t + 4 < dmax) nxt = edge_quad(cl, len, a, deg, t + 4, self);
+        step(cur.x, cur.y, t < deg, t + 1 < deg);
+        if (t + 2 < dmax) step(cur.z, cur.w, t + 2 < deg, t + 3 < deg);
+        cur = nxt;
+    }
 }
 
 // ------------------------------------------------------------------ forward
 
 template <typename T, int D, int H>
 __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t* __restrict__ rp,
-                                                       const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                       const int32_t* __restrict__ cl, int64_t len,
+                                                       const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V, float sl2,
                                                        T* __restrict__ O, float* __restrict__ LSE, TilePartials tp) {
     using C = EdgeCfg<T, D, H>;
@@ -164,11 +191,9 @@ __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t*
     q.load(Q + off);
     Online<C::F> st;
     if (live && deg >= 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
-    for (int t = 0; t < dmax; t += 2) {
-        int64_t j0, j1;
-        edge_pair(cl, a, deg, t, self, j0, j1);
-        fwd_step<T, D, H>(st, q, K, V, j0, j1, t < deg, t + 1 < deg, ln, sl2);
-    }
+    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, bool ok0, bool ok1) {
+        fwd_step<T, D, H>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2);
+    });
     if (live && deg >= 0) {
         const float inv = st.l > 0.f ? 1.f / st.l : 0.f;
         store_slice<T, C::F>(O + off, st.acc, inv);
@@ -298,7 +323,8 @@ __device__ __forceinline__ void load_row_partial(RowSums<EdgeCfg<T, D, H>::F>& r
 
 template <typename T, int D, int H>
 __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t* __restrict__ rp,
-                                                       const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                       const int32_t* __restrict__ cl, int64_t len,
+                                                       const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V,
                                                        const T* __restrict__ dO, const float* __restrict__ LSE,
                                                        float* __restrict__ Dv, float sl2, float scale,
@@ -324,11 +350,9 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
     const float lse2 = LSE[self * H + ln.h] * kLog2e;
     RowSums<C::F> rs;
     if (live && deg >= 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
-    for (int t = 0; t < dmax; t += 2) {
-        int64_t j0, j1;
-        edge_pair(cl, a, deg, t, self, j0, j1);
-        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, t < deg, t + 1 < deg, ln, sl2);
-    }
+    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, bool ok0, bool ok1) {
+        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2);
+    });
     if (live && deg >= 0) {
 #pragma unroll
         for (int f = 0; f < C::F; ++f) rs.a.v[f] = fmaf(-rs.d, rs.b.v[f], rs.a.v[f]);
@@ -426,7 +450,8 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
 
 template <typename T, int D, int H>
 __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t* __restrict__ cp,
-                                                       const int32_t* __restrict__ rw, const T* __restrict__ Q,
+                                                       const int32_t* __restrict__ rw, int64_t len,
+                                                       const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V,
                                                        const T* __restrict__ dO, const float* __restrict__ LSE,
                                                        const float* __restrict__ Dv, float sl2, float scale,
@@ -455,11 +480,9 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
         load_f32_slice<C::F>(dk.v, tpk.acc + off);
         load_f32_slice<C::F>(dv.v, tpv.acc + off);
     }
-    for (int t = 0; t < dmax; t += 2) {
-        int64_t i0, i1;
-        edge_pair(rw, a, deg, t, self, i0, i1);
-        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, t < deg, t + 1 < deg, ln, sl2);
-    }
+    walk_edges(rw, len, a, deg, dmax, int32_t(self), [&](int64_t i0, int64_t i1, bool ok0, bool ok1) {
+        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, ok0, ok1, ln, sl2);
+    });
     if (live && deg >= 0) {
         store_slice<T, C::F>(dK + off, dk.v, scale);
         store_slice<T, C::F>(dV + off, dv.v, 1.f);
@@ -547,8 +570,8 @@ gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V
     }
     const int64_t waves = cdiv(n, C::NPW);
     k_fwd_rows<T, D, H><<<xcd_grid(cdiv(waves, kThreads / kWave)), kThreads, 0, s>>>(
-        n, p->sp_rowptr, p->sp_col, static_cast<const T*>(Q), static_cast<const T*>(K), static_cast<const T*>(V),
-        sl2, static_cast<T*>(O), LSE, tp);
+        n, p->sp_rowptr, p->sp_col, p->nnz_sparse, static_cast<const T*>(Q), static_cast<const T*>(K),
+        static_cast<const T*>(V), sl2, static_cast<T*>(O), LSE, tp);
     GT_LAUNCH_CHECK("sparse_fwd_rows");
     if (p->n_long_rows > 0) {
         k_fwd_long<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
@@ -576,8 +599,8 @@ gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const vo
         if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, g, LSE, sl2, tb.dq, s)) != GT_OK) return st;
     }
     const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
-    k_bwd_rows<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, Dv, sl2, scale,
-                                                  static_cast<T*>(dQ), tb.dq);
+    k_bwd_rows<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, p->nnz_sparse, q, k, v, g, LSE, Dv,
+                                                  sl2, scale, static_cast<T*>(dQ), tb.dq);
     GT_LAUNCH_CHECK("sparse_bwd_rows");
     if (p->n_long_rows > 0) {
         k_bwd_rows_long<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
@@ -605,8 +628,8 @@ gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const vo
         if ((st = tile_bwd_dkdv<T, D, H>(p, q, k, v, g, LSE, Dv, sl2, tb.dk, tb.dv, s)) != GT_OK) return st;
     }
     const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
-    k_bwd_cols<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2, scale,
-                                                  static_cast<T*>(dK), static_cast<T*>(dV), tb.dk, tb.dv);
+    k_bwd_cols<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_colptr, p->sp_row, p->nnz_sparse, q, k, v, g, LSE, Dv,
+                                                  sl2, scale, static_cast<T*>(dK), static_cast<T*>(dV), tb.dk, tb.dv);
     GT_LAUNCH_CHECK("sparse_bwd_cols");
     if (p->n_long_cols > 0) {
         k_bwd_cols_long<T, D, H><<<unsigned(p->n_long_cols), kThreads, 0, s>>>(
