@@ -117,54 +117,65 @@ struct Frag {
     }
 };
 
-// One thread's share of a 64-row stage of X[:, h, :]: a block of 4 rows x 4
-// features (8 bytes per row), kept in registers between the global load and
-// the LDS stores.  Loads are unconditional (rows past n read row n-1) so the
-// compiler can keep them in flight across the stage's products; rows >= n are
-// zeroed when stored.
-template <int D>
+// One thread's share of a 64-row stage of X[:, h, :] for a workgroup of NT
+// threads: blocks of 4 rows x 4 features (8 bytes per row), kept in registers
+// between the global load and the LDS stores.  Loads are unconditional (rows
+// past n read row n-1) so the compiler can keep them in flight across the
+// stage's products; rows >= n are zeroed when stored.
+template <int D, int NT>
 struct Stager {
-    static constexpr int FG = D / 4;       // feature groups per row
-    static constexpr int kItems = 16 * FG; // (row group, feature group) blocks
-    static_assert(kItems <= kThr && kThr % kItems == 0, "stage does not fit the workgroup");
-    uint2 r[4];
-    int rg, fg;
-    uint32_t valid;  // bit j: row 4 rg + j < n
-    __device__ __forceinline__ Stager() {
-        const int t = threadIdx.x % kItems;
-        rg = t / FG;
-        fg = t % FG;
-    }
+    static constexpr int FG = D / 4;                        // feature groups per row
+    static constexpr int kItems = 16 * FG;                  // (row group, feature group) blocks
+    static constexpr int PER = kItems >= NT ? kItems / NT : 1;
+    static_assert(kItems >= NT ? kItems % NT == 0 : NT % kItems == 0, "stage does not fit the workgroup");
+    uint2 r[PER][4];
+    uint32_t valid;  // bit 4k + j: row j of block k is below n
     // Threads beyond kItems (whole wavefronts) only mirror the loads.
-    __device__ __forceinline__ bool on() const { return kItems == kThr || threadIdx.x < kItems; }
+    __device__ __forceinline__ static bool on() { return kItems >= NT || threadIdx.x < kItems; }
+    __device__ __forceinline__ static int item(int k) {
+        return kItems >= NT ? int(threadIdx.x) + k * NT : int(threadIdx.x) % kItems;
+    }
     __device__ __forceinline__ void load(const uint16_t* __restrict__ X, int64_t base, int64_t n, int H, int h) {
         valid = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t node = base + 4 * rg + j;
-            const int64_t src = node < n ? node : n - 1;
-            valid |= uint32_t(node < n) << j;
-            r[j] = *reinterpret_cast<const uint2*>(X + (src * H + h) * D + 4 * fg);
+        for (int k = 0; k < PER; ++k) {
+            const int it = item(k), rg = it / FG, fg = it % FG;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t node = base + 4 * rg + j;
+                const int64_t src = node < n ? node : n - 1;
+                valid |= uint32_t(node < n) << (4 * k + j);
+                r[k][j] = *reinterpret_cast<const uint2*>(X + (src * H + h) * D + 4 * fg);
+            }
         }
     }
-    __device__ __forceinline__ uint2 row(int j) const {
-        return (valid >> j) & 1u ? r[j] : make_uint2(0, 0);
+    __device__ __forceinline__ uint2 row(int k, int j) const {
+        return (valid >> (4 * k + j)) & 1u ? r[k][j] : make_uint2(0, 0);
     }
     __device__ __forceinline__ void store_rm(uint16_t* s) const {
         if (!on()) return;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint2*>(s + (4 * rg + j) * RS<D>::v + 4 * fg) = row(j);
+        for (int k = 0; k < PER; ++k) {
+            const int it = item(k), rg = it / FG, fg = it % FG;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                *reinterpret_cast<uint2*>(s + (4 * rg + j) * RS<D>::v + 4 * fg) = row(k, j);
+        }
     }
     // s[f * kTS + row]: the 4 rows of each of the 4 features as one 8-byte store.
     __device__ __forceinline__ void store_tr(uint16_t* s) const {
         if (!on()) return;
-        const uint2 a = row(0), b = row(1), c = row(2), d = row(3);
         const uint32_t lo = 0xFFFFu, hi = 0xFFFF0000u;
-        uint16_t* p = s + (4 * fg) * kTS + 4 * rg;
-        *reinterpret_cast<uint2*>(p) = make_uint2((a.x & lo) | (b.x << 16), (c.x & lo) | (d.x << 16));
-        *reinterpret_cast<uint2*>(p + kTS) = make_uint2((a.x >> 16) | (b.x & hi), (c.x >> 16) | (d.x & hi));
-        *reinterpret_cast<uint2*>(p + 2 * kTS) = make_uint2((a.y & lo) | (b.y << 16), (c.y & lo) | (d.y << 16));
-        *reinterpret_cast<uint2*>(p + 3 * kTS) = make_uint2((a.y >> 16) | (b.y & hi), (c.y >> 16) | (d.y & hi));
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int it = item(k), rg = it / FG, fg = it % FG;
+            const uint2 a = row(k, 0), b = row(k, 1), c = row(k, 2), d = row(k, 3);
+            uint16_t* p = s + (4 * fg) * kTS + 4 * rg;
+            *reinterpret_cast<uint2*>(p) = make_uint2((a.x & lo) | (b.x << 16), (c.x & lo) | (d.x << 16));
+            *reinterpret_cast<uint2*>(p + kTS) = make_uint2((a.x >> 16) | (b.x & hi), (c.x >> 16) | (d.x & hi));
+            *reinterpret_cast<uint2*>(p + 2 * kTS) = make_uint2((a.y & lo) | (b.y << 16), (c.y & lo) | (d.y << 16));
+            *reinterpret_cast<uint2*>(p + 3 * kTS) = make_uint2((a.y >> 16) | (b.y & hi), (c.y >> 16) | (d.y & hi));
+        }
     }
 };
 
@@ -218,7 +229,7 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
         for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
     float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
 
-    Stager<D> gk, gv;
+    Stager<D, kThr> gk, gv;
     gk.load(K, 0, n, H, h);
     gv.load(V, 0, n, H, h);
     gk.store_rm(sK[0]);
@@ -362,7 +373,7 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uin
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
 
-    Stager<D> gk, gv;
+    Stager<D, kThr> gk, gv;
     gk.load(K, 0, n, H, h);
     gv.load(V, 0, n, H, h);
     gk.store_rm(sK[0]);
@@ -485,7 +496,7 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
             sD[buf][threadIdx.x] = qn < n ? Dv[qn * H + h] : 0.f;
         }
     };
-    Stager<D> gq, gg;
+    Stager<D, kThr> gq, gg;
     gq.load(Q, 0, n, H, h);
     gg.load(dO, 0, n, H, h);
     gq.store_rm(sQ[0]);
@@ -583,6 +594,463 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
     }
 }
 
+// ------------------------------------------------------------ dense tiles
+// Sparse layers: the dense tiles of the plan (§3.4), computed whole on the
+// matrix cores with the tile's bit mask deciding which pairs are edges.  The
+// row-owned kernels walk a tile row's dense tiles, the column-owned kernel a
+// tile column's; a workgroup has T/64 wavefronts of 64 owned rows (two MFMA
+// blocks) and stages the partners 64 at a time.  Each kernel leaves fp32
+// partial sums per (node, head) for the edge kernels, which add the remainder
+// edges and finish every row and column.  A row may have no edge in a tile:
+// its weights are exactly zero (masked scores are -inf, and an all-masked
+// running maximum is treated as 0 in the exponent).
+
+// Mask words of one owned row for one tile: bit c of word w <=> key 32 w + c.
+template <int T>
+__device__ __forceinline__ void load_mask_row(uint32_t (&mw)[T / 32], const uint32_t* __restrict__ row) {
+    if constexpr (T == 128) {
+        const uint4 v = *reinterpret_cast<const uint4*>(row);
+        mw[0] = v.x, mw[1] = v.y, mw[2] = v.z, mw[3] = v.w;
+    } else {
+        const uint2 v = *reinterpret_cast<const uint2*>(row);
+        mw[0] = v.x, mw[1] = v.y;
+    }
+}
+
+template <int D, int T>
+__global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
+                                                 const int32_t* __restrict__ tile_col,
+                                                 const uint32_t* __restrict__ tile_mask,
+                                                 const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                                                 const uint16_t* __restrict__ V, float sl2, float* __restrict__ pm,
+                                                 float* __restrict__ pl, float* __restrict__ pacc) {
+    constexpr int W = T / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t sK[1][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sVt[1][D * kTS];
+    const int I = blockIdx.x, h = blockIdx.y;
+    const int64_t t0 = tile_rowptr[I], t1 = tile_rowptr[I + 1];
+    if (t0 == t1) return;
+    const int lane = lane_id();
+    const int ql0 = (threadIdx.x / kWave) * kOwn;  // first owned row inside the tile row
+    const int64_t q0 = int64_t(I) * T + ql0;
+    Frag<D> qf[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) qf[b].load(Q, q0 + 32 * b + (lane & 31), n, H, h, lane);
+    if (sl2 < 0.f) {  // keep the exp2-domain scale positive: negate Q instead (exact in bf16)
+        sl2 = -sl2;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c)
+                qf[b].v[c] = __builtin_bit_cast(bf16x8_t, __builtin_bit_cast(uint4, qf[b].v[c]) ^
+                                                              make_uint4(0x80008000u, 0x80008000u, 0x80008000u,
+                                                                         0x80008000u));
+    }
+    f32x16_t acc[2][D / 32];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
+    float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
+    // Stages run over the tile row's dense tiles, T/64 per tile.  They are
+    // single-buffered: several small workgroups per CU hide each other's
+    // loads, which a register prefetch (at one wavefront per SIMD) did not.
+    constexpr int NSG = T / kStage;
+    const int64_t stages = (t1 - t0) * NSG;
+    Stager<D, T> gk, gv;
+    uint32_t mw[2][W];
+    auto fetch = [&](int64_t g, uint32_t (&mwx)[2][W]) {
+        const int64_t k = t0 + g / NSG;
+        const int64_t kb = int64_t(tile_col[k]) * T + kStage * (g % NSG);
+        gk.load(K, kb, n, H, h);
+        gv.load(V, kb, n, H, h);
+        if (g % NSG == 0)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                load_mask_row<T>(mwx[b], tile_mask + (k * T + ql0 + 32 * b + (lane & 31)) * W);
+    };
+#pragma unroll 1
+    for (int64_t g = 0; g < stages; ++g) {
+        const int buf = 0, st = int(g % NSG);
+        fetch(g, mw);
+        __syncthreads();  // the previous stage's readers are done
+        gk.store_rm(sK[0]);
+        gv.store_tr(sVt[0]);
+        __syncthreads();
+#pragma unroll
+        for (int kb = 0; kb < kStage / 32; ++kb) {
+            f32x16_t s[2];
+            s[0] = s[1] = zero16();
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) {
+                const bf16x8_t a = lds_row8<D>(sK[buf], 32 * kb + (lane & 31), c, lane);
+                s[0] = mma(a, qf[0].v[c], s[0]);
+                s[1] = mma(a, qf[1].v[c], s[1]);
+            }
+            bool grow = false;
+            float mt[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const uint32_t w = mw[b][2 * st + kb];
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    if (!((w >> crow(i, lane)) & 1u)) s[b][i] = kNegInf;
+                float mx = s[b][0];
+#pragma unroll
+                for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[b][i]);
+                mt[b] = pair_max(mx) * sl2;
+                grow |= mt[b] > m[b] + kLazy;
+            }
+            if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const float mn = fmaxf(m[b], mt[b]);
+                    if (mn == kNegInf) continue;
+                    const float alpha = ex2(m[b] - mn);
+                    l[b] *= alpha;
+#pragma unroll
+                    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) acc[b][db][i] *= alpha;
+                    m[b] = mn;
+                }
+            }
+            bf16x8_t pb[2][2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const float mm = m[b] == kNegInf ? 0.f : m[b];
+                float ls = 0.f;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = ex2(fmaf(s[b][i], sl2, -mm));
+                    s[b][i] = p;
+                    ls += p;
+                }
+                l[b] += ls;
+                pb[b][0] = acc_b16(s[b], 0);
+                pb[b][1] = acc_b16(s[b], 1);
+            }
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    const bf16x8_t a = lds_perm8(sVt[buf], 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
+                    acc[0][db] = mma(a, pb[0][half], acc[0][db]);
+                    acc[1][db] = mma(a, pb[1][half], acc[1][db]);
+                }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t q = q0 + 32 * b + (lane & 31);
+        const float lt = pair_sum(l[b]);
+        if (q >= n) continue;
+        if (lane < 32) {
+            pm[q * H + h] = m[b];
+            pl[q * H + h] = lt;
+        }
+        float* o = pacc + (q * H + h) * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x16_t& a = acc[b][db];
+                *reinterpret_cast<float4*>(o + 32 * db + 8 * j + 4 * (lane >> 5)) =
+                    make_float4(a[4 * j], a[4 * j + 1], a[4 * j + 2], a[4 * j + 3]);
+            }
+    }
+}
+
+// Weights w as bf16 hi + lo parts (about 16 mantissa bits): B operands of
+// two products whose sum keeps the fp32 weight, for sums of many large
+// weights and for the A - D B difference of the row pass.
+__device__ __forceinline__ void split_b16(const f32x16_t& w, int half, bf16x8_t& hi, bf16x8_t& lo) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        hi[t] = (__bf16)w[8 * half + t];
+        lo[t] = (__bf16)(w[8 * half + t] - float(hi[t]));
+    }
+}
+
+// Row pass over the dense tiles: A = sum P dP K, B = sum P K and the D sum
+// sum P dP of every owned row (the edge kernels form dQ = scale (A - D B)).
+template <int D, int T>
+__global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
+                                                const int32_t* __restrict__ tile_col,
+                                                const uint32_t* __restrict__ tile_mask,
+                                                const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                                                const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
+                                                const float* __restrict__ LSE, float sl2, float* __restrict__ pa,
+                                                float* __restrict__ pb, float* __restrict__ pd) {
+    constexpr int W = T / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t sK[1][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[1][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sKt[1][D * kTS];
+    const int I = blockIdx.x, h = blockIdx.y;
+    const int64_t t0 = tile_rowptr[I], t1 = tile_rowptr[I + 1];
+    if (t0 == t1) return;
+    const int lane = lane_id();
+    const int ql0 = (threadIdx.x / kWave) * kOwn;
+    const int64_t q0 = int64_t(I) * T + ql0;
+    Frag<D> qf[2], gf[2];
+    float lse2[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t q = q0 + 32 * b + (lane & 31);
+        qf[b].load(Q, q, n, H, h, lane);
+        gf[b].load(dO, q, n, H, h, lane);
+        lse2[b] = q < n ? LSE[q * H + h] * kLog2e : 0.f;
+    }
+    f32x16_t accA[2][D / 32], accB[2][D / 32];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) accA[b][db] = accB[b][db] = zero16();
+    float dsum[2] = {0.f, 0.f};
+    constexpr int NSG = T / kStage;
+    const int64_t stages = (t1 - t0) * NSG;
+    Stager<D, T> gk, gv;
+    uint32_t mw[2][W];
+    auto fetch = [&](int64_t g, uint32_t (&mwx)[2][W]) {
+        const int64_t k = t0 + g / NSG;
+        const int64_t kb = int64_t(tile_col[k]) * T + kStage * (g % NSG);
+        gk.load(K, kb, n, H, h);
+        gv.load(V, kb, n, H, h);
+        if (g % NSG == 0)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                load_mask_row<T>(mwx[b], tile_mask + (k * T + ql0 + 32 * b + (lane & 31)) * W);
+    };
+#pragma unroll 1
+    for (int64_t g = 0; g < stages; ++g) {
+        const int buf = 0, st = int(g % NSG);
+        fetch(g, mw);
+        __syncthreads();
+        gk.store_rm(sK[0]);
+        gk.store_tr(sKt[0]);
+        gv.store_rm(sV[0]);
+        __syncthreads();
+#pragma unroll
+        for (int kb = 0; kb < kStage / 32; ++kb) {
+            f32x16_t s[2], dp[2];
+            s[0] = s[1] = dp[0] = dp[1] = zero16();
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) {
+                const bf16x8_t a = lds_row8<D>(sK[buf], 32 * kb + (lane & 31), c, lane);
+                s[0] = mma(a, qf[0].v[c], s[0]);
+                s[1] = mma(a, qf[1].v[c], s[1]);
+                const bf16x8_t v = lds_row8<D>(sV[buf], 32 * kb + (lane & 31), c, lane);
+                dp[0] = mma(v, gf[0].v[c], dp[0]);
+                dp[1] = mma(v, gf[1].v[c], dp[1]);
+            }
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const uint32_t w = mw[b][2 * st + kb];
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = (w >> crow(i, lane)) & 1u ? ex2(fmaf(s[b][i], sl2, -lse2[b])) : 0.f;
+                    s[b][i] = p;
+                    dp[b][i] *= p;
+                    dsum[b] += dp[b][i];
+                }
+            }
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    const bf16x8_t a = lds_perm8(sKt[buf], 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) {
+                        bf16x8_t hi, lo;
+                        split_b16(dp[b], half, hi, lo);
+                        accA[b][db] = mma(a, lo, mma(a, hi, accA[b][db]));
+                        split_b16(s[b], half, hi, lo);
+                        accB[b][db] = mma(a, lo, mma(a, hi, accB[b][db]));
+                    }
+                }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t q = q0 + 32 * b + (lane & 31);
+        const float ds = pair_sum(dsum[b]);
+        if (q >= n) continue;
+        if (lane < 32) pd[q * H + h] = ds;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int f = 32 * db + 8 * j + 4 * (lane >> 5);
+                const f32x16_t& x = accA[b][db];
+                const f32x16_t& y = accB[b][db];
+                *reinterpret_cast<float4*>(pa + (q * H + h) * D + f) =
+                    make_float4(x[4 * j], x[4 * j + 1], x[4 * j + 2], x[4 * j + 3]);
+                *reinterpret_cast<float4*>(pb + (q * H + h) * D + f) =
+                    make_float4(y[4 * j], y[4 * j + 1], y[4 * j + 2], y[4 * j + 3]);
+            }
+    }
+}
+
+// Column pass over the dense tiles: unscaled dK and dV sums of every owned key.
+// The stage's masks are transposed with ballots so that each lane holds, for
+// its key, one 64-bit word over the stage's 64 queries.
+template <int D, int T>
+__global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_row_tiles,
+                                                  const int64_t* __restrict__ tileT_ptr,
+                                                  const int32_t* __restrict__ tileT_idx,
+                                                  const int64_t* __restrict__ tile_rowptr,
+                                                  const uint32_t* __restrict__ tile_mask,
+                                                  const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                                                  const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
+                                                  const float* __restrict__ LSE, const float* __restrict__ Dv,
+                                                  float sl2, float* __restrict__ pdk, float* __restrict__ pdv) {
+    constexpr int W = T / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[1][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sG[1][kStage * RS<D>::v];
+    __shared__ __attribute__((aligned(16))) uint16_t sQt[1][D * kTS];
+    __shared__ __attribute__((aligned(16))) uint16_t sGt[1][D * kTS];
+    __shared__ __attribute__((aligned(16))) float sL[1][kStage];
+    __shared__ __attribute__((aligned(16))) float sD[1][kStage];
+    const int J = blockIdx.x, h = blockIdx.y;
+    const int64_t u0 = tileT_ptr[J], u1 = tileT_ptr[J + 1];
+    if (u0 == u1) return;
+    const int lane = lane_id();
+    const int kl0 = (threadIdx.x / kWave) * kOwn;  // first owned key inside the tile column
+    const int64_t k0 = int64_t(J) * T + kl0;
+    Frag<D> kf[2], vf[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        kf[b].load(K, k0 + 32 * b + (lane & 31), n, H, h, lane);
+        vf[b].load(V, k0 + 32 * b + (lane & 31), n, H, h, lane);
+    }
+    f32x16_t dk[2][D / 32], dv[2][D / 32];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) dk[b][db] = dv[b][db] = zero16();
+    constexpr int NSG = T / kStage;
+    const int64_t stages = (u1 - u0) * NSG;
+    Stager<D, T> gq, gg;
+    uint32_t mword[2];  // this lane's row of the stage: mask words of the wavefront's two key blocks
+    float2 stat;        // LSE (exp2 domain) and D of the stage's query threadIdx.x % kStage
+    auto fetch = [&](int64_t g) {
+        const int64_t k = tileT_idx[u0 + g / NSG];
+        int64_t lo = 0, hi = n_row_tiles;  // tile row of tile k: the last I with tile_rowptr[I] <= k
+        while (hi - lo > 1) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (tile_rowptr[mid] <= k) lo = mid;
+            else hi = mid;
+        }
+        const int st = int(g % NSG);
+        const int64_t qbase = lo * T + kStage * st;
+        gq.load(Q, qbase, n, H, h);
+        gg.load(dO, qbase, n, H, h);
+#pragma unroll
+        for (int b = 0; b < 2; ++b) mword[b] = tile_mask[(k * T + kStage * st + lane) * W + (kl0 / 32 + b)];
+        stat = make_float2(__builtin_huge_valf(), 0.f);  // queries >= n take no weight
+        const int64_t qn = qbase + (threadIdx.x % kStage);
+        if (qn < n) stat = make_float2(LSE[qn * H + h] * kLog2e, Dv[qn * H + h]);
+    };
+    // transposed masks: bit r of mt[b] <=> query r of the stage attends to key k0 + 32 b + lane % 32
+    uint64_t mt[2];
+    auto transpose = [&](uint64_t (&out)[2]) {
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            uint64_t mine = 0;
+#pragma unroll
+            for (int c = 0; c < 32; ++c) {
+                const uint64_t bal = __builtin_amdgcn_ballot_w64((mword[b] >> c) & 1u);
+                if ((lane & 31) == c) mine = bal;
+            }
+            out[b] = mine;
+        }
+    };
+    auto store = [&](int buf) {
+        gq.store_rm(sQ[buf]);
+        gq.store_tr(sQt[buf]);
+        gg.store_rm(sG[buf]);
+        gg.store_tr(sGt[buf]);
+        if (threadIdx.x < kStage) {
+            sL[buf][threadIdx.x] = stat.x;
+            sD[buf][threadIdx.x] = stat.y;
+        }
+    };
+#pragma unroll 1
+    for (int64_t g = 0; g < stages; ++g) {
+        const int buf = 0;
+        fetch(g);
+        transpose(mt);
+        __syncthreads();  // the previous stage's readers are done
+        store(0);
+        __syncthreads();
+#pragma unroll
+        for (int qb = 0; qb < kStage / 32; ++qb) {
+            f32x16_t s[2], dp[2];
+            s[0] = s[1] = dp[0] = dp[1] = zero16();
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) {
+                const bf16x8_t a = lds_row8<D>(sQ[buf], 32 * qb + (lane & 31), c, lane);
+                s[0] = mma(a, kf[0].v[c], s[0]);
+                s[1] = mma(a, kf[1].v[c], s[1]);
+                const bf16x8_t g8 = lds_row8<D>(sG[buf], 32 * qb + (lane & 31), c, lane);
+                dp[0] = mma(g8, vf[0].v[c], dp[0]);
+                dp[1] = mma(g8, vf[1].v[c], dp[1]);
+            }
+            float Lr[16], Dr[16];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 32 * qb + 8 * j + 4 * (lane >> 5);
+                const float4 lv = *reinterpret_cast<const float4*>(&sL[buf][r]);
+                const float4 d4 = *reinterpret_cast<const float4*>(&sD[buf][r]);
+                Lr[4 * j] = lv.x, Lr[4 * j + 1] = lv.y, Lr[4 * j + 2] = lv.z, Lr[4 * j + 3] = lv.w;
+                Dr[4 * j] = d4.x, Dr[4 * j + 1] = d4.y, Dr[4 * j + 2] = d4.z, Dr[4 * j + 3] = d4.w;
+            }
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const uint32_t w = uint32_t(mt[b] >> (32 * qb));
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = (w >> crow(i, lane)) & 1u ? ex2(fmaf(s[b][i], sl2, -Lr[i])) : 0.f;
+                    s[b][i] = p * (dp[b][i] - Dr[i]);
+                    dp[b][i] = p;
+                }
+            }
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    const bf16x8_t g8 = lds_perm8(sGt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
+                    const bf16x8_t a = lds_perm8(sQt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) {
+                        bf16x8_t hi16, lo16;
+                        split_b16(dp[b], half, hi16, lo16);
+                        dv[b][db] = mma(g8, lo16, mma(g8, hi16, dv[b][db]));
+                        split_b16(s[b], half, hi16, lo16);
+                        dk[b][db] = mma(a, lo16, mma(a, hi16, dk[b][db]));
+                    }
+                }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int64_t key = k0 + 32 * b + (lane & 31);
+        if (key >= n) continue;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int f = 32 * db + 8 * j + 4 * (lane >> 5);
+                const f32x16_t& x = dk[b][db];
+                const f32x16_t& y = dv[b][db];
+                *reinterpret_cast<float4*>(pdk + (key * H + h) * D + f) =
+                    make_float4(x[4 * j], x[4 * j + 1], x[4 * j + 2], x[4 * j + 3]);
+                *reinterpret_cast<float4*>(pdv + (key * H + h) * D + f) =
+                    make_float4(y[4 * j], y[4 * j + 1], y[4 * j + 2], y[4 * j + 3]);
+            }
+    }
+}
+
 }  // namespace
 
 template <int D>
@@ -605,6 +1073,63 @@ gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, 
     GT_LAUNCH_CHECK("full_bwd_bf16 dkdv");
     return GT_OK;
 }
+
+
+#define GT_TILES_T(CALL)                                                          \
+    do {                                                                          \
+        if (p->T == 128) {                                                        \
+            constexpr int TT = 128;                                               \
+            CALL;                                                                 \
+        } else if (p->T == 64) {                                                  \
+            constexpr int TT = 64;                                                \
+            CALL;                                                                 \
+        } else {                                                                  \
+            return fail(GT_ERR_UNSUPPORTED, "dense tiles: T must be 64 or 128");  \
+        }                                                                         \
+    } while (0)
+
+template <int D>
+gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                         float sl2, TilePartials tp, hipStream_t s) {
+    const dim3 grid(unsigned(p->n_row_tiles), unsigned(H));
+    GT_TILES_T((k_tiles_fwd<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
+                                                       sl2, tp.m, tp.l, tp.acc)));
+    GT_LAUNCH_CHECK("tiles_fwd_bf16");
+    return GT_OK;
+}
+
+template <int D>
+gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        const uint16_t* dO, const float* LSE, float sl2, TilePartials dq, hipStream_t s) {
+    const dim3 grid(unsigned(p->n_row_tiles), unsigned(H));
+    GT_TILES_T((k_tiles_dq<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
+                                                      dO, LSE, sl2, dq.acc, dq.acc2, dq.m)));
+    GT_LAUNCH_CHECK("tiles_dq_bf16");
+    return GT_OK;
+}
+
+template <int D>
+gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                          const uint16_t* dO, const float* LSE, const float* Dv, float sl2, TilePartials dk,
+                          TilePartials dv, hipStream_t s) {
+    const dim3 grid(unsigned(p->n_row_tiles), unsigned(H));
+    GT_TILES_T((k_tiles_dkdv<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->n_row_tiles, p->tileT_ptr, p->tileT_idx,
+                                                        p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv, sl2,
+                                                        dk.acc, dv.acc)));
+    GT_LAUNCH_CHECK("tiles_dkdv_bf16");
+    return GT_OK;
+}
+
+#define GT_TILES_INST(D)                                                                                        \
+    template gt_status tiles_fwd_bf16<D>(const gt_tiles*, int, const uint16_t*, const uint16_t*, const uint16_t*, \
+                                         float, TilePartials, hipStream_t);                                     \
+    template gt_status tiles_dq_bf16<D>(const gt_tiles*, int, const uint16_t*, const uint16_t*, const uint16_t*,  \
+                                        const uint16_t*, const float*, float, TilePartials, hipStream_t);       \
+    template gt_status tiles_dkdv_bf16<D>(const gt_tiles*, int, const uint16_t*, const uint16_t*,                \
+                                          const uint16_t*, const uint16_t*, const float*, const float*, float,  \
+                                          TilePartials, TilePartials, hipStream_t);
+GT_TILES_INST(32)
+GT_TILES_INST(64)
 
 template gt_status full_fwd_bf16<32>(int64_t, int, const uint16_t*, const uint16_t*, const uint16_t*, float,
                                      uint16_t*, float*, hipStream_t);

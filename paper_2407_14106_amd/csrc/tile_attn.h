@@ -102,4 +102,17 @@ gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, 
                         const uint16_t* O, const uint16_t* dO, const float* LSE, float sl2, float scale,
                         uint16_t* dQ, uint16_t* dK, uint16_t* dV, float* Dv, hipStream_t s);
 
+// The dense tiles of a plan for bf16 features (dense_mfma.hip): same partial
+// sums as tile_fwd / tile_bwd_dq / tile_bwd_dkdv, which call them for bf16.
+template <int D>
+gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                         float sl2, TilePartials tp, hipStream_t s);
+template <int D>
+gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        const uint16_t* dO, const float* LSE, float sl2, TilePartials dq, hipStream_t s);
+template <int D>
+gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                          const uint16_t* dO, const float* LSE, const float* Dv, float sl2, TilePartials dk,
+                          TilePartials dv, hipStream_t s);
+
 }  // namespace gt

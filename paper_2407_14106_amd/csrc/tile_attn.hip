@@ -593,6 +593,7 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dkdv(int64_t n, const int64_t* 
 template <typename T, int D, int H>
 gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float sl2, TilePartials tp,
                    hipStream_t s) {
+    if constexpr (Mma<T>::kBf16) return tiles_fwd_bf16<D>(p, H, Q, K, V, sl2, tp, s);
     const dim3 grid(unsigned(p->n_row_tiles), H);
     GT_TILE_SWITCH(p->T, (k_tile_fwd<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
                              p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc,
@@ -604,6 +605,7 @@ gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float 
 template <typename T, int D, int H>
 gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
                       float sl2, TilePartials dq, hipStream_t s) {
+    if constexpr (Mma<T>::kBf16) return tiles_dq_bf16<D>(p, H, Q, K, V, dO, LSE, sl2, dq, s);
     const dim3 grid(unsigned(p->n_row_tiles), H);
     GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
                              p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, nullptr, dO, LSE, sl2,
@@ -615,6 +617,7 @@ gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, con
 template <typename T, int D, int H>
 gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
                         const float* Dv, float sl2, TilePartials dk, TilePartials dv, hipStream_t s) {
+    if constexpr (Mma<T>::kBf16) return tiles_dkdv_bf16<D>(p, H, Q, K, V, dO, LSE, Dv, sl2, dk, dv, s);
     const dim3 grid(unsigned(p->n_row_tiles), H);
     GT_TILE_SWITCH(p->T, (k_tile_dkdv<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
                              p->n, p->tileT_ptr, p->tileT_idx, p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv,
