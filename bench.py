@@ -4,7 +4,10 @@ One step = forward, backward row half (dQ) and backward column half (dK, dV)
 of neighbourhood softmax attention over one synthetic graph and its Q, K, V,
 dO, all resident in HBM.  The graph is reordered (cluster order), relabelled
 and tiled once before timing; those stages are timed separately and reported
-under "preprocess".
+under "preprocess".  Also reported: the same step at density thresholds 1%,
+20% and the CSR-only control ("tau_sweep"), the interleaved full-attention
+layer ("dense_layer"), and the fp64 oracle on a bounded sample of the same
+workload on the host's cores ("cpu_baseline", timed before the GPU is used).
 
 Default workload: 1,000,000-node stochastic block model, 1,000 log-normal
 blocks, average degree 30, 5% of edges across blocks, self-loops, random node
@@ -40,8 +43,8 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--scale", type=float, default=1.0, help="shrink the workload's node count (testing only)")
     ap.add_argument("--tau", type=float, default=0.05, help="tile density threshold")
@@ -49,6 +52,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense-layer", action="store_true", help="skip the full-attention layer measurement")
+    ap.add_argument("--no-tau-sweep", action="store_true",
+                    help="skip the density-threshold sweep (1%%, 20%%, CSR only) of the default workload")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB row copy (gt_gather_rows, identity order) 5 times: the reference "
                          "for scaling hardware byte counters")
@@ -93,33 +98,71 @@ def recorded_traffic(kernel: str):
     return int(fields[kernel])
 
 
-def cpu_baseline(w, target_s):
-    """The fp64 oracle on a bounded sample: forward and backward for a block of rows/columns."""
+def _oracle_rows(args):
+    """Worker: fp64 oracle forward and backward for one chunk of sample rows (fork-shared inputs)."""
+    from threadpoolctl import threadpool_limits
+
     from oracle import attention as OA
 
+    rows = args
+    g, q, k, v, do, scale = _ORACLE_INPUTS
+    with threadpool_limits(1):
+        OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, scale, rows=rows)
+        if do is not None:
+            OA.sparse_attn_bwd_sampled(g.rowptr, g.col, q, k, v, do, scale, rows, rows)
+    return len(rows)
+
+
+_ORACLE_INPUTS = None
+
+
+def cpu_baseline(w, q, k, v, do, target_s):
+    """The fp64 oracle on a bounded sample of the same workload: forward, dQ of the sample rows and dK/dV of the
+    same node ids as columns.  Timed once on one core (BLAS limited to one thread) and once over a process pool
+    on the host's cores; runs before the process touches the GPU, so the pool can fork."""
+    import multiprocessing as mp
+
+    from threadpoolctl import threadpool_limits
+
+    from oracle import attention as OA
+
+    global _ORACLE_INPUTS
     g = w.graph
-    q, k, v, do = w.tensors()
     scale = 1.0 / math.sqrt(w.dim)
+    _ORACLE_INPUTS = (g, q, k, v, do, scale)
     rng = np.random.default_rng(0)
     rows = 64
-    while True:
-        sample = np.sort(rng.choice(g.n, size=rows, replace=False))
+    with threadpool_limits(1):
+        while True:
+            sample = np.sort(rng.choice(g.n, size=rows, replace=False))
+            t0 = time.perf_counter()
+            OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, scale, rows=sample)
+            if do is not None:
+                OA.sparse_attn_bwd_sampled(g.rowptr, g.col, q, k, v, do, scale, sample, sample)
+            dt1 = time.perf_counter() - t0
+            if dt1 >= 0.4 * target_s or rows >= g.n:
+                break
+            rows = min(g.n, int(rows * max(2.0, min(8.0, 0.5 * target_s / max(dt1, 1e-3)))))
+    edge_heads = float(np.diff(g.rowptr)[sample].sum()) * w.heads
+    cores = min(16, len(os.sched_getaffinity(0)))
+    big = np.sort(rng.choice(g.n, size=min(g.n, rows * cores // 2), replace=False))
+    chunks = np.array_split(big, cores * 4)
+    ctx = mp.get_context("fork")
+    with ctx.Pool(cores) as pool:
         t0 = time.perf_counter()
-        OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, scale, rows=sample)
-        OA.sparse_attn_bwd_sampled(g.rowptr, g.col, q, k, v, do, scale, sample, sample)
-        dt = time.perf_counter() - t0
-        if dt >= 0.6 * target_s or rows >= g.n:
-            break
-        rows = min(g.n, int(rows * max(2.0, min(8.0, target_s / max(dt, 1e-3)))))
-    deg = np.diff(g.rowptr)[sample]
-    edge_heads = float(deg.sum()) * w.heads
+        pool.map(_oracle_rows, chunks)
+        dtn = time.perf_counter() - t0
+    edge_heads_n = float(np.diff(g.rowptr)[big].sum()) * w.heads
+    _ORACLE_INPUTS = None
     return {
-        "value": edge_heads / dt,
+        "value": edge_heads_n / dtn,
         "unit": "edge-head scores/s",
-        "cores": 1,
+        "cores": cores,
         "kind": "oracle",
-        "sample": f"{rows} random rows (their {int(deg.sum())} edges x {w.heads} heads): fp64 forward of the rows, "
-                  f"dQ of the rows, dK/dV of the same node ids as columns; {dt:.1f} s",
+        "sample": f"{len(big)} random rows of the workload (their {int(edge_heads_n / w.heads)} edges x {w.heads} "
+                  f"heads) over {cores} processes, {dtn:.1f} s: fp64 forward of the rows, dQ of the rows, dK/dV "
+                  f"of the same node ids as columns",
+        "single_core": {"value": edge_heads / dt1, "cores": 1, "rows": rows, "seconds": round(dt1, 2)},
     }
 
 
@@ -164,6 +207,45 @@ def dense_layer(steps: int):
     }
 
 
+def tau_sweep(gt, rp, cl, Q, K, V, dO, scale, args, edge_heads, T):
+    """Same step at other density thresholds: 1% (the diagonal tiles of the clusters go to the matrix cores),
+    20% (none do) and above 1 (the CSR-only control: no tile can qualify)."""
+    import torch
+
+    out = {}
+    for tau in (0.01, 0.20, 1.01):
+        plan = gt.build_tiles(rp, cl, T, gt.tau_to_ppm(tau))
+        for _ in range(3):
+            O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
+            dQ, Dst = gt.sparse_attn_bwd_rows(plan, Q, K, V, dO, L, scale)
+            gt.sparse_attn_bwd_cols(plan, Q, K, V, dO, L, Dst, scale)
+        torch.cuda.synchronize()
+        steps = 10
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        f = r = c = 0.0
+        for _ in range(steps):
+            ev[0].record()
+            O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
+            ev[1].record()
+            dQ, Dst = gt.sparse_attn_bwd_rows(plan, Q, K, V, dO, L, scale)
+            ev[2].record()
+            gt.sparse_attn_bwd_cols(plan, Q, K, V, dO, L, Dst, scale)
+            ev[3].record()
+            torch.cuda.synchronize()
+            f += ev[0].elapsed_time(ev[1])
+            r += ev[1].elapsed_time(ev[2])
+            c += ev[2].elapsed_time(ev[3])
+        ms = (f + r + c) / steps
+        out[f"{tau:g}"] = {
+            "dense_tiles": int(plan.n_dense), "remainder_edges": int(plan.nnz_sparse),
+            "ms_per_step": round(ms, 4), "value": edge_heads / (ms / 1e3),
+            "stages_ms": {"fwd": round(f / steps, 4), "bwd_rows": round(r / steps, 4), "bwd_cols": round(c / steps, 4)},
+            "dense_tile_flops_fwd": 4.0 * T * T * Q.shape[2] * Q.shape[1] * int(plan.n_dense),
+        }
+        del plan
+    return out
+
+
 def copy_probe():
     """A plain copy of known size: 2^21 rows x 512 bytes (1 GiB) read and written, plus the 8 MiB order array."""
     import torch
@@ -195,13 +277,17 @@ def main():
     from synth import make_workload
     from synth.tensors import bf16_bits
 
-    gt.load_library()
-    dev = torch.device("cuda:0")
     t0 = time.perf_counter()
     w = make_workload(args.workload, args.scale)
     g = w.graph
     q, k, v, do = w.tensors()
     log(f"workload {w.name}: {w.description}, nnz={g.nnz}, generated in {time.perf_counter() - t0:.1f}s")
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle sample (before the GPU is touched) ...")
+        cpu = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
+    gt.load_library()
+    dev = torch.device("cuda:0")
 
     def up(x):
         if w.dtype == "bf16":
@@ -273,6 +359,7 @@ def main():
         stages["bwd_rows"].append(e[1].elapsed_time(e[2]))
         stages["bwd_cols"].append(e[2].elapsed_time(e[3]))
     avg = {k: float(np.mean(v)) for k, v in stages.items()}
+    med = {k: float(np.median(v)) for k, v in stages.items()}
 
     nnz, H, d = g.nnz, w.heads, w.dim
     b = 2 if w.dtype == "bf16" else 4
@@ -317,17 +404,20 @@ def main():
             "avg_launch_ms": round(avg[dom], 4),
         },
         "stages_ms": {k: round(v, 4) for k, v in avg.items()},
+        "stages_median_ms": {k: round(v, 4) for k, v in med.items()},
         "stages_alg_GBps": stage_gbs,
         "step_alg_GBps": round(sum(alg.values()) / (ms_per_step / 1e3) / 1e9, 1),
         "preprocess": pre,
         "wall_s_timed": round(t_wall, 3),
     }
+    if not args.no_tau_sweep and args.workload == "c4":
+        log("density-threshold sweep ...")
+        result["tau_sweep"] = tau_sweep(gt, rp2, cl2, Q, K, V, dO, scale, args, edge_heads, args.tile)
     if not args.no_dense_layer:
         log("timing the full-attention layer ...")
         result["dense_layer"] = dense_layer(5)
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle sample ...")
-        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    if cpu is not None:
+        result["cpu_baseline"] = cpu
     print(json.dumps(result), flush=True)
 
 
