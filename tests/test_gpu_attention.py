@@ -158,3 +158,37 @@ def test_pipeline_reorder_then_attention_is_equivariant(gt):
     assert_close(gt.scatter_rows(L, perm).cpu().numpy(), L_ref, "bf16", "LSE")
     for name, x, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
         assert_close(host(gt.scatter_rows(x, perm)), r, "bf16", name)
+
+
+@pytest.mark.parametrize("name,tau", [("c2", 10_000), ("c3", 10_000), ("c4", 50_000), ("c4", 10_000),
+                                      ("c5", 10_000)])
+def test_full_size_workloads_sampled(gt, name, tau):
+    # The workloads at their full sizes through the library's whole pipeline, in the launch configuration the
+    # benchmark times (reorder, relabel, 128-wide tiles at the workload's threshold, row gather, forward and
+    # both backward passes), with the outputs scattered back to the input order.  The oracle computes 192
+    # random rows (forward, dQ) and columns (dK, dV) one by one on the original graph, plus the eight rows of
+    # largest degree (hubs on the power-law graph).
+    w = make_workload(name)
+    g = w.graph
+    q, k, v, do = w.tensors()
+    scale = 1.0 / np.sqrt(w.dim)
+    say("full size", name, g.n, g.nnz, tau)
+    rp, cl = dev_csr(g.rowptr, g.col)
+    perm, iperm, _ = gt.reorder(rp, cl)
+    rp2, cl2 = gt.permute_csr(rp, cl, perm, iperm)
+    plan = gt.build_tiles(rp2, cl2, 128, tau)
+    Q, K, V, dO = (gt.gather_rows(dev_feat(x, w.dtype), perm) for x in (q, k, v, do))
+    O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
+    dQ, dK, dV = gt.sparse_attn_bwd(plan, Q, K, V, dO, L, scale)
+    outs = [gt.scatter_rows(x, perm) for x in (O, L, dQ, dK, dV)]
+    torch.cuda.synchronize()
+    say("  dense tiles", plan.n_dense, "long rows", plan.c.n_long_rows, "long cols", plan.c.n_long_cols)
+    rng = np.random.default_rng(11)
+    deg = np.diff(g.rowptr)
+    rows = np.unique(np.concatenate([rng.choice(g.n, size=192, replace=False), np.argsort(deg)[-8:]]))
+    O_ref, L_ref = OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, scale, rows=rows)
+    dq_ref, dk_ref, dv_ref = OA.sparse_attn_bwd_sampled(g.rowptr, g.col, q, k, v, do, scale, rows, rows)
+    idx = torch.from_numpy(rows).cuda()
+    for nm, x, r in zip(("O", "dQ", "dK", "dV"), (outs[0], outs[2], outs[3], outs[4]), (O_ref, dq_ref, dk_ref, dv_ref)):
+        assert_close(host(x[idx]), r, w.dtype, f"{name} {nm}")
+    assert_close(outs[1][idx].cpu().numpy(), L_ref, w.dtype, f"{name} LSE")

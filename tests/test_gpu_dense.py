@@ -56,6 +56,8 @@ def test_dense_layer_single_node(gt, dtype):
 
 
 def test_dense_layer_65536_sampled_rows_and_sum_rules(gt):
+    # 1,024 sampled rows of O, LSE and dQ against the oracle (each needs only its own scores against all
+    # keys); dK and dV, which need every row's softmax, are checked through the sum rules.
     w = make_workload("c5")
     n, H, d = w.graph.n, w.heads, w.dim
     q, k, v, do = w.tensors()
@@ -65,7 +67,7 @@ def test_dense_layer_65536_sampled_rows_and_sum_rules(gt):
     O, L = gt.dense_attn_fwd(Q, K, V, scale)
     dQ, dK, dV = gt.dense_attn_bwd(Q, K, V, O, dO, L, scale)
     torch.cuda.synchronize()
-    rows = np.sort(np.random.default_rng(5).choice(n, size=64, replace=False))
+    rows = np.sort(np.random.default_rng(5).choice(n, size=1024, replace=False))
     O_ref, L_ref = OA.dense_attn_fwd(q, k, v, scale, rows=rows)
     dq_ref = OA.dense_attn_dq_rows(q, k, v, do, scale, rows)
     idx = torch.from_numpy(rows).cuda()
