@@ -43,6 +43,19 @@ def _f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
+class _Widen:
+    """Rows of a feature array as fp64 on selection.  The inputs hold fp32 (or bf16-rounded) values, which
+    fp64 holds exactly, so widening the selected rows equals widening the whole array first; large arrays are
+    never copied whole."""
+
+    def __init__(self, x):
+        self.x = x.x if isinstance(x, _Widen) else np.asarray(x)
+        self.shape = self.x.shape
+
+    def __getitem__(self, key):
+        return np.asarray(self.x[key], dtype=np.float64)
+
+
 def _row_chunks(rowptr: np.ndarray, rows: np.ndarray, per_edge: int):
     """Split the row list into consecutive chunks holding about _EDGE_BUDGET elements."""
     deg = rowptr[rows + 1] - rowptr[rows]
@@ -51,7 +64,8 @@ def _row_chunks(rowptr: np.ndarray, rows: np.ndarray, per_edge: int):
     start = 0
     while start < len(rows):
         base = cum[start - 1] if start else 0
-        stop = int(np.searchsorted(cum, base + budget, side="left")) + 1
+        # rows while the chunk stays within the budget; a row above the budget on its own is a chunk alone
+        stop = int(np.searchsorted(cum, base + budget, side="right"))
         stop = min(max(stop, start + 1), len(rows))
         yield rows[start:stop]
         start = stop
@@ -68,14 +82,25 @@ def _edges_of(rowptr, col, rows):
     return local, col[idx].astype(np.int64), deg
 
 
+def _segments(local, n_rows):
+    """Rows with at least one edge and the offset of each one's first edge; ``local`` is non-decreasing (the
+    edges of a row are contiguous in CSR order)."""
+    counts = np.bincount(local, minlength=n_rows)
+    nz = np.nonzero(counts)[0]
+    first = np.concatenate([[0], np.cumsum(counts)[:-1]])
+    return nz, first[nz]
+
+
 def _segment_softmax_stats(s, local, n_rows):
     """Per local row and head: max and log-sum-exp of the scores s[e, h] of its edges."""
     H = s.shape[1]
     m = np.full((n_rows, H), -np.inf)
-    np.maximum.at(m, local, s)
-    p = np.exp(s - m[local])
     total = np.zeros((n_rows, H))
-    np.add.at(total, local, p)
+    if len(s):
+        nz, first = _segments(local, n_rows)
+        m[nz] = np.maximum.reduceat(s, first, axis=0)
+        p = np.exp(s - m[local])
+        total[nz] = np.add.reduceat(p, first, axis=0)
     with np.errstate(divide="ignore"):
         lse = m + np.log(total)
     return lse
@@ -83,7 +108,7 @@ def _segment_softmax_stats(s, local, n_rows):
 
 def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
     """O[rows], LSE[rows] of neighbourhood softmax attention (all rows when ``rows`` is None)."""
-    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    Q, K, V = _Widen(Q), _Widen(K), _Widen(V)
     N, H, d = Q.shape
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
@@ -94,13 +119,26 @@ def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
     for chunk in _row_chunks(rowptr, rows, H * d):
         local, nbr, _ = _edges_of(rowptr, col, chunk)
         n = len(chunk)
-        if len(nbr):
+        if n == 1 and len(nbr) > 4096:
+            # one long row (a hub, a global token): the same definition per head, as contractions over its
+            # partners without edge-major temporaries
+            r = chunk[0]
+            Kn, Vn = K[nbr], V[nbr]
+            for h in range(H):
+                s = scale * (Kn[:, h, :] @ Q[r, h, :])
+                m = s.max()
+                p = np.exp(s - m)
+                tot = p.sum()
+                O[pos, h] = (p @ Vn[:, h, :]) / tot
+                LSE[pos, h] = m + np.log(tot)
+        elif len(nbr):
             i = chunk[local]
             s = scale * np.einsum("ehc,ehc->eh", Q[i], K[nbr])
             lse = _segment_softmax_stats(s, local, n)
             p = np.exp(s - lse[local])
             o = np.zeros((n, H, d))
-            np.add.at(o, local, p[:, :, None] * V[nbr])
+            nz, first = _segments(local, n)
+            o[nz] = np.add.reduceat(p[:, :, None] * V[nbr], first, axis=0)
             O[pos:pos + n] = o
             LSE[pos:pos + n] = lse
         pos += n
@@ -150,15 +188,21 @@ def sparse_attn_bwd_sampled(rowptr, col, Q, K, V, dO, scale, rows, cols):
     dQ_i needs row i alone; dK_j and dV_j need every row i that has j as a
     neighbour (with that row's LSE_i and D_i, each row-local).
     """
-    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    Q, K, V, dO = _Widen(Q), _Widen(K), _Widen(V), _Widen(dO)
     N, H, d = Q.shape
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
     rows = np.asarray(rows, dtype=np.int64)
     cols = np.asarray(cols, dtype=np.int64)
 
-    O_r, L_r = sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=rows)
-    D_r = np.einsum("nhc,nhc->nh", dO[rows], O_r)
+    colptr, inrow = _csc(rowptr, col, N)
+    # LSE_i and D_i of the sampled rows and of every source row a sampled column needs, each computed once
+    need = np.unique(np.concatenate([rows] + [inrow[colptr[jj]:colptr[jj + 1]] for jj in cols]))
+    slot = np.full(N, -1, dtype=np.int64)
+    slot[need] = np.arange(len(need))
+    O_n, L_n = sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=need)
+    D_n = np.einsum("nhc,nhc->nh", dO[need], O_n)
+    L_r, D_r = L_n[slot[rows]], D_n[slot[rows]]
     dQ = np.zeros((len(rows), H, d))
     local, j, _ = _edges_of(rowptr, col, rows)
     if len(j):
@@ -167,17 +211,16 @@ def sparse_attn_bwd_sampled(rowptr, col, Q, K, V, dO, scale, rows, cols):
         p = np.exp(s - L_r[local])
         dp = np.einsum("ehc,ehc->eh", dO[i], V[j])
         ds = p * (dp - D_r[local])
-        np.add.at(dQ, local, scale * ds[:, :, None] * K[j])
+        nz, first = _segments(local, len(rows))
+        dQ[nz] = np.add.reduceat(scale * ds[:, :, None] * K[j], first, axis=0)
 
-    colptr, inrow = _csc(rowptr, col, N)
     dK = np.zeros((len(cols), H, d))
     dV = np.zeros((len(cols), H, d))
     for k, jj in enumerate(cols):
         srcs = inrow[colptr[jj]:colptr[jj + 1]]
         if not len(srcs):
             continue
-        O_s, L_s = sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=srcs)
-        D_s = np.einsum("nhc,nhc->nh", dO[srcs], O_s)
+        L_s, D_s = L_n[slot[srcs]], D_n[slot[srcs]]
         s = scale * np.einsum("ehc,hc->eh", Q[srcs], K[jj])
         p = np.exp(s - L_s)
         dp = np.einsum("ehc,hc->eh", dO[srcs], V[jj])

@@ -18,6 +18,7 @@
 // The backward never uses atomics: dQ is gathered per row over the CSR, dK and
 // dV per column over the remainder's transpose.
 #include "attn_common.h"
+#include "prim.h"
 #include "tile_attn.h"
 
 namespace gt {
@@ -201,62 +202,6 @@ __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t*
     }
 }
 
-// One workgroup per long row; lane groups take edges round-robin, then the
-// per-group states are merged through LDS.
-template <typename T, int D, int H>
-__global__ __launch_bounds__(kThreads) void k_fwd_long(const int32_t* __restrict__ list,
-                                                       const int64_t* __restrict__ rp,
-                                                       const int32_t* __restrict__ cl, const T* __restrict__ Q,
-                                                       const T* __restrict__ K, const T* __restrict__ V, float sl2,
-                                                       T* __restrict__ O, float* __restrict__ LSE, TilePartials tp) {
-    using C = EdgeCfg<T, D, H>;
-    constexpr int S = kThreads / C::G;  // lane groups per workgroup
-    __shared__ float s_m[S][H];
-    __shared__ float s_l[S][H];
-    __shared__ float s_acc[S][H * D];
-    const Lanes<T, D, H> ln(threadIdx.x);
-    const int64_t i = list[blockIdx.x];
-    const int64_t a = rp[i];
-    const int deg = int(rp[i + 1] - a);
-    const int64_t off = ln.off(i);
-    Slice<T, C::F> q;
-    q.load(Q + off);
-    Online<C::F> st;
-    if (ln.slot == 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
-    for (int t = ln.slot; t < deg; t += 2 * S) {
-        const bool ok1 = t + S < deg;
-        const int64_t j0 = cl[a + t];
-        const int64_t j1 = ok1 ? cl[a + t + S] : 0;
-        fwd_step<T, D, H>(st, q, K, V, j0, j1, true, ok1, ln, sl2);
-    }
-    if (ln.part == 0) {
-        s_m[ln.slot][ln.h] = st.m;
-        s_l[ln.slot][ln.h] = st.l;
-    }
-#pragma unroll
-    for (int f = 0; f < C::F; ++f) s_acc[ln.slot][ln.h * D + ln.part * C::F + f] = st.acc[f];
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
-        const int h = idx / D;
-        float M = kNegInf;
-        for (int s = 0; s < S; ++s) M = fmaxf(M, s_m[s][h]);
-        float lsum = 0.f, o = 0.f;
-        if (M != kNegInf) {
-            for (int s = 0; s < S; ++s) {
-                const float w = exp2f(s_m[s][h] - M);
-                lsum += s_l[s][h] * w;
-                o += s_acc[s][idx] * w;
-            }
-        }
-        const float val = lsum > 0.f ? o / lsum : 0.f;
-        if (sizeof(T) == 2)
-            reinterpret_cast<uint16_t*>(O)[i * H * D + idx] = f32_to_bf16(val);
-        else
-            reinterpret_cast<float*>(O)[i * H * D + idx] = val;
-        if (idx % D == 0) LSE[i * H + h] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : kNegInf;
-    }
-}
-
 // ----------------------------------------------------------------- backward
 
 // Row pass.  With D_i = sum_j P_ij dP_ij (which equals <dO_i, O_i> for the
@@ -361,60 +306,6 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
     }
 }
 
-template <typename T, int D, int H>
-__global__ __launch_bounds__(kThreads) void k_bwd_rows_long(const int32_t* __restrict__ list,
-                                                            const int64_t* __restrict__ rp,
-                                                            const int32_t* __restrict__ cl, const T* __restrict__ Q,
-                                                            const T* __restrict__ K, const T* __restrict__ V,
-                                                            const T* __restrict__ dO, const float* __restrict__ LSE,
-                                                            float* __restrict__ Dv, float sl2, float scale,
-                                                            T* __restrict__ dQ, TilePartials tp) {
-    using C = EdgeCfg<T, D, H>;
-    constexpr int S = kThreads / C::G;
-    __shared__ float s_a[S][H * D];
-    __shared__ float s_b[S][H * D];
-    __shared__ float s_d[S][H];
-    const Lanes<T, D, H> ln(threadIdx.x);
-    const int64_t i = list[blockIdx.x];
-    const int64_t a = rp[i];
-    const int deg = int(rp[i + 1] - a);
-    const int64_t off = ln.off(i);
-    Slice<T, C::F> q, g;
-    q.load(Q + off);
-    g.load(dO + off);
-    const float lse2 = LSE[i * H + ln.h] * kLog2e;
-    RowSums<C::F> rs;
-    if (ln.slot == 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
-    for (int t = ln.slot; t < deg; t += 2 * S) {
-        const bool ok1 = t + S < deg;
-        const int64_t j0 = cl[a + t];
-        const int64_t j1 = ok1 ? cl[a + t + S] : 0;
-        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, true, ok1, ln, sl2);
-    }
-#pragma unroll
-    for (int f = 0; f < C::F; ++f) {
-        s_a[ln.slot][ln.h * D + ln.part * C::F + f] = rs.a.v[f];
-        s_b[ln.slot][ln.h * D + ln.part * C::F + f] = rs.b.v[f];
-    }
-    if (ln.part == 0) s_d[ln.slot][ln.h] = rs.d;
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
-        const int h = idx / D;
-        float sa = 0.f, sb = 0.f, sd = 0.f;
-        for (int s = 0; s < S; ++s) {
-            sa += s_a[s][idx];
-            sb += s_b[s][idx];
-            sd += s_d[s][h];
-        }
-        const float acc = fmaf(-sd, sb, sa) * scale;
-        if (sizeof(T) == 2)
-            reinterpret_cast<uint16_t*>(dQ)[i * H * D + idx] = f32_to_bf16(acc);
-        else
-            reinterpret_cast<float*>(dQ)[i * H * D + idx] = acc;
-        if (idx % D == 0) Dv[i * H + h] = sd;
-    }
-}
-
 // Column pass: dK_j = scale * sum_i dS_ij Q_i, dV_j = sum_i P_ij dO_i over the in-edges of j.
 template <typename T, int D, int H>
 __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeCfg<T, D, H>::F>& dv,
@@ -489,36 +380,280 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
     }
 }
 
+// ------------------------------------------------------------- long rows
+// Remainder rows (columns) with more than GT_LONG_ROW edges, up to a row that
+// attends to every node: each is cut into chunks of kChunk edges, one
+// workgroup per chunk leaves a partial state (its lane groups take the edges
+// round-robin and merge in LDS), and one workgroup per long row merges its
+// chunks with the row's dense-tile partial and writes the result.  The chunk
+// table is built on the device; the chunk grid is launched at its upper bound
+// (one chunk per long row plus one per kChunk remainder edges) and surplus
+// workgroups return at once.
+constexpr int kChunk = 2048;
+
+template <int H, int D>
+constexpr int64_t FwdLongF = int64_t(H) * D + 2 * H;  // floats per chunk: m[H], l[H], acc[H D]
+template <int H, int D>
+constexpr int64_t RowLongF = 2 * int64_t(H) * D + H;  // a[H D], b[H D], d[H]
+template <int H, int D>
+constexpr int64_t ColLongF = 2 * int64_t(H) * D;      // dk[H D], dv[H D]
+
+struct LongPlan {
+    int32_t* counts = nullptr;     // [n_long]: chunks of each long row
+    int64_t* chunk_off = nullptr;  // [n_long + 1]: exclusive scan of counts
+    float* part = nullptr;         // [max_chunks, floats per chunk]
+    int64_t max_chunks = 0;
+    ScanTmp scan;
+};
+
+inline LongPlan long_plan_take(Ws& ws, int64_t n_long, int64_t nnz, int64_t per_chunk) {
+    LongPlan lp;
+    if (n_long <= 0) return lp;
+    lp.max_chunks = n_long + nnz / kChunk + 1;
+    lp.counts = ws.take<int32_t>(size_t(n_long));
+    lp.chunk_off = ws.take<int64_t>(size_t(n_long + 1));
+    lp.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n_long)));
+    lp.part = ws.take<float>(size_t(lp.max_chunks * per_chunk));
+    return lp;
+}
+
+__global__ void k_long_counts(const int32_t* __restrict__ list, int64_t n_long, const int64_t* __restrict__ ptr,
+                              int32_t* __restrict__ counts) {
+    const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= n_long) return;
+    const int64_t i = list[r];
+    counts[r] = int32_t(cdiv(ptr[i + 1] - ptr[i], kChunk));
+}
+
+gt_status long_chunks(const int32_t* list, int64_t n_long, const int64_t* ptr, const LongPlan& lp, hipStream_t s) {
+    k_long_counts<<<grid_for(n_long, 256), 256, 0, s>>>(list, n_long, ptr, lp.counts);
+    GT_LAUNCH_CHECK("long_counts");
+    return exclusive_scan_i32(lp.counts, n_long, lp.chunk_off, lp.scan, s);
+}
+
+// Chunk b -> (long row r, chunk c of that row, its edge range [e0, e1) inside
+// the row); false for the surplus of the grid.
+__device__ __forceinline__ bool chunk_of(const int64_t* __restrict__ off, int64_t n_long, int64_t b, int64_t& r,
+                                         int& e0) {
+    if (b >= off[n_long]) return false;
+    int64_t lo = 0, hi = n_long;  // the last r with off[r] <= b
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (off[mid] <= b) lo = mid;
+        else hi = mid;
+    }
+    r = lo;
+    e0 = int(b - off[lo]) * kChunk;
+    return true;
+}
+
 template <typename T, int D, int H>
-__global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __restrict__ list,
+__global__ __launch_bounds__(kThreads) void k_fwd_long(const int32_t* __restrict__ list, int64_t n_long,
+                                                       const int64_t* __restrict__ chunk_off,
+                                                       const int64_t* __restrict__ rp,
+                                                       const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                       const T* __restrict__ K, const T* __restrict__ V, float sl2,
+                                                       float* __restrict__ part) {
+    using C = EdgeCfg<T, D, H>;
+    constexpr int S = kThreads / C::G;  // lane groups per workgroup
+    __shared__ float s_m[S][H];
+    __shared__ float s_l[S][H];
+    __shared__ float s_acc[S][H * D];
+    int64_t r;
+    int e0;
+    if (!chunk_of(chunk_off, n_long, blockIdx.x, r, e0)) return;
+    const Lanes<T, D, H> ln(threadIdx.x);
+    const int64_t i = list[r];
+    const int64_t a = rp[i];
+    const int deg = int(rp[i + 1] - a);
+    const int e1 = e0 + kChunk < deg ? e0 + kChunk : deg;
+    const int64_t off = ln.off(i);
+    Slice<T, C::F> q;
+    q.load(Q + off);
+    Online<C::F> st;
+    for (int t = e0 + ln.slot; t < e1; t += 2 * S) {
+        const bool ok1 = t + S < e1;
+        const int64_t j0 = cl[a + t];
+        const int64_t j1 = ok1 ? cl[a + t + S] : j0;
+        fwd_step<T, D, H>(st, q, K, V, j0, j1, true, ok1, ln, sl2);
+    }
+    if (ln.part == 0) {
+        s_m[ln.slot][ln.h] = st.m;
+        s_l[ln.slot][ln.h] = st.l;
+    }
+#pragma unroll
+    for (int f = 0; f < C::F; ++f) s_acc[ln.slot][ln.h * D + ln.part * C::F + f] = st.acc[f];
+    __syncthreads();
+    float* out = part + blockIdx.x * FwdLongF<H, D>;
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        const int h = idx / D;
+        float M = kNegInf;
+        for (int g = 0; g < S; ++g) M = fmaxf(M, s_m[g][h]);
+        float lsum = 0.f, o = 0.f;
+        if (M != kNegInf) {
+            for (int g = 0; g < S; ++g) {
+                const float w = exp2f(s_m[g][h] - M);
+                lsum += s_l[g][h] * w;
+                o += s_acc[g][idx] * w;
+            }
+        }
+        out[2 * H + idx] = o;
+        if (idx % D == 0) {
+            out[h] = M;
+            out[H + h] = lsum;
+        }
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_fwd_long_merge(const int32_t* __restrict__ list,
+                                                             const int64_t* __restrict__ chunk_off,
+                                                             const float* __restrict__ part, TilePartials tp,
+                                                             T* __restrict__ O, float* __restrict__ LSE) {
+    const int64_t i = list[blockIdx.x];
+    const int64_t c0 = chunk_off[blockIdx.x], c1 = chunk_off[blockIdx.x + 1];
+    const bool tile = tp.has_row(i);
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        const int h = idx / D;
+        float M = tile ? tp.m[i * H + h] : kNegInf;
+        for (int64_t c = c0; c < c1; ++c) M = fmaxf(M, part[c * FwdLongF<H, D> + h]);
+        float lsum = 0.f, o = 0.f;
+        if (M != kNegInf) {
+            if (tile) {
+                const float w = exp2f(tp.m[i * H + h] - M);
+                lsum = tp.l[i * H + h] * w;
+                o = tp.acc[i * H * D + idx] * w;
+            }
+            for (int64_t c = c0; c < c1; ++c) {
+                const float* pc = part + c * FwdLongF<H, D>;
+                const float w = exp2f(pc[h] - M);
+                lsum += pc[H + h] * w;
+                o += pc[2 * H + idx] * w;
+            }
+        }
+        const float val = lsum > 0.f ? o / lsum : 0.f;
+        if (sizeof(T) == 2)
+            reinterpret_cast<uint16_t*>(O)[i * H * D + idx] = f32_to_bf16(val);
+        else
+            reinterpret_cast<float*>(O)[i * H * D + idx] = val;
+        if (idx % D == 0) LSE[i * H + h] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : kNegInf;
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_rows_long(const int32_t* __restrict__ list, int64_t n_long,
+                                                            const int64_t* __restrict__ chunk_off,
+                                                            const int64_t* __restrict__ rp,
+                                                            const int32_t* __restrict__ cl, const T* __restrict__ Q,
+                                                            const T* __restrict__ K, const T* __restrict__ V,
+                                                            const T* __restrict__ dO, const float* __restrict__ LSE,
+                                                            float sl2, float* __restrict__ part) {
+    using C = EdgeCfg<T, D, H>;
+    constexpr int S = kThreads / C::G;
+    __shared__ float s_a[S][H * D];
+    __shared__ float s_b[S][H * D];
+    __shared__ float s_d[S][H];
+    int64_t r;
+    int e0;
+    if (!chunk_of(chunk_off, n_long, blockIdx.x, r, e0)) return;
+    const Lanes<T, D, H> ln(threadIdx.x);
+    const int64_t i = list[r];
+    const int64_t a = rp[i];
+    const int deg = int(rp[i + 1] - a);
+    const int e1 = e0 + kChunk < deg ? e0 + kChunk : deg;
+    const int64_t off = ln.off(i);
+    Slice<T, C::F> q, g;
+    q.load(Q + off);
+    g.load(dO + off);
+    const float lse2 = LSE[i * H + ln.h] * kLog2e;
+    RowSums<C::F> rs;
+    for (int t = e0 + ln.slot; t < e1; t += 2 * S) {
+        const bool ok1 = t + S < e1;
+        const int64_t j0 = cl[a + t];
+        const int64_t j1 = ok1 ? cl[a + t + S] : j0;
+        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, true, ok1, ln, sl2);
+    }
+#pragma unroll
+    for (int f = 0; f < C::F; ++f) {
+        s_a[ln.slot][ln.h * D + ln.part * C::F + f] = rs.a.v[f];
+        s_b[ln.slot][ln.h * D + ln.part * C::F + f] = rs.b.v[f];
+    }
+    if (ln.part == 0) s_d[ln.slot][ln.h] = rs.d;
+    __syncthreads();
+    float* out = part + blockIdx.x * RowLongF<H, D>;
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        const int h = idx / D;
+        float sa = 0.f, sb = 0.f, sd = 0.f;
+        for (int gi = 0; gi < S; ++gi) {
+            sa += s_a[gi][idx];
+            sb += s_b[gi][idx];
+            sd += s_d[gi][h];
+        }
+        out[idx] = sa;
+        out[H * D + idx] = sb;
+        if (idx % D == 0) out[2 * H * D + h] = sd;
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_rows_long_merge(const int32_t* __restrict__ list,
+                                                                  const int64_t* __restrict__ chunk_off,
+                                                                  const float* __restrict__ part, TilePartials tp,
+                                                                  float scale, T* __restrict__ dQ,
+                                                                  float* __restrict__ Dv) {
+    const int64_t i = list[blockIdx.x];
+    const int64_t c0 = chunk_off[blockIdx.x], c1 = chunk_off[blockIdx.x + 1];
+    const bool tile = tp.has_row(i);
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        const int h = idx / D;
+        float sa = tile ? tp.acc[i * H * D + idx] : 0.f;
+        float sb = tile ? tp.acc2[i * H * D + idx] : 0.f;
+        float sd = tile ? tp.m[i * H + h] : 0.f;
+        for (int64_t c = c0; c < c1; ++c) {
+            const float* pc = part + c * RowLongF<H, D>;
+            sa += pc[idx];
+            sb += pc[H * D + idx];
+            sd += pc[2 * H * D + h];
+        }
+        const float v = fmaf(-sd, sb, sa) * scale;
+        if (sizeof(T) == 2)
+            reinterpret_cast<uint16_t*>(dQ)[i * H * D + idx] = f32_to_bf16(v);
+        else
+            reinterpret_cast<float*>(dQ)[i * H * D + idx] = v;
+        if (idx % D == 0) Dv[i * H + h] = sd;
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __restrict__ list, int64_t n_long,
+                                                            const int64_t* __restrict__ chunk_off,
                                                             const int64_t* __restrict__ cp,
                                                             const int32_t* __restrict__ rw, const T* __restrict__ Q,
                                                             const T* __restrict__ K, const T* __restrict__ V,
                                                             const T* __restrict__ dO, const float* __restrict__ LSE,
-                                                            const float* __restrict__ Dv, float sl2, float scale,
-                                                            T* __restrict__ dK, T* __restrict__ dV, TilePartials tpk,
-                                                            TilePartials tpv) {
+                                                            const float* __restrict__ Dv, float sl2,
+                                                            float* __restrict__ part) {
     using C = EdgeCfg<T, D, H>;
     constexpr int S = kThreads / C::G;
     __shared__ float s_k[S][H * D];
     __shared__ float s_v[S][H * D];
+    int64_t r;
+    int e0;
+    if (!chunk_of(chunk_off, n_long, blockIdx.x, r, e0)) return;
     const Lanes<T, D, H> ln(threadIdx.x);
-    const int64_t j = list[blockIdx.x];
+    const int64_t j = list[r];
     const int64_t a = cp[j];
     const int deg = int(cp[j + 1] - a);
+    const int e1 = e0 + kChunk < deg ? e0 + kChunk : deg;
     const int64_t off = ln.off(j);
     Slice<T, C::F> k, v;
     k.load(K + off);
     v.load(V + off);
     Acc<C::F> dk, dv;
-    if (ln.slot == 0 && tpk.has_col(j)) {
-        load_f32_slice<C::F>(dk.v, tpk.acc + off);
-        load_f32_slice<C::F>(dv.v, tpv.acc + off);
-    }
-    for (int t = ln.slot; t < deg; t += 2 * S) {
-        const bool ok1 = t + S < deg;
+    for (int t = e0 + ln.slot; t < e1; t += 2 * S) {
+        const bool ok1 = t + S < e1;
         const int64_t i0 = rw[a + t];
-        const int64_t i1 = ok1 ? rw[a + t + S] : 0;
+        const int64_t i1 = ok1 ? rw[a + t + S] : i0;
         dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, true, ok1, ln, sl2);
     }
 #pragma unroll
@@ -527,11 +662,34 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __res
         s_v[ln.slot][ln.h * D + ln.part * C::F + f] = dv.v[f];
     }
     __syncthreads();
+    float* out = part + blockIdx.x * ColLongF<H, D>;
     for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
         float ak = 0.f, av = 0.f;
-        for (int s = 0; s < S; ++s) {
-            ak += s_k[s][idx];
-            av += s_v[s][idx];
+        for (int g = 0; g < S; ++g) {
+            ak += s_k[g][idx];
+            av += s_v[g][idx];
+        }
+        out[idx] = ak;
+        out[H * D + idx] = av;
+    }
+}
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_bwd_cols_long_merge(const int32_t* __restrict__ list,
+                                                                  const int64_t* __restrict__ chunk_off,
+                                                                  const float* __restrict__ part, TilePartials tpk,
+                                                                  TilePartials tpv, float scale,
+                                                                  T* __restrict__ dK, T* __restrict__ dV) {
+    const int64_t j = list[blockIdx.x];
+    const int64_t c0 = chunk_off[blockIdx.x], c1 = chunk_off[blockIdx.x + 1];
+    const bool tile = tpk.has_col(j);
+    for (int idx = threadIdx.x; idx < H * D; idx += kThreads) {
+        float ak = tile ? tpk.acc[j * H * D + idx] : 0.f;
+        float av = tile ? tpv.acc[j * H * D + idx] : 0.f;
+        for (int64_t c = c0; c < c1; ++c) {
+            const float* pc = part + c * ColLongF<H, D>;
+            ak += pc[idx];
+            av += pc[H * D + idx];
         }
         ak *= scale;
         if (sizeof(T) == 2) {
@@ -559,6 +717,7 @@ gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V
     Ws ws(ws_ptr);
     ws.take<char>(256);
     TilePartials tp = tile_partials_fwd(ws, p, H, D);
+    LongPlan lp = long_plan_take(ws, p->n_long_rows, p->nnz_sparse, FwdLongF<H, D>);
     const float sl2 = scale * kLog2e;
     gt_status st;
     if (p->n_dense > 0) {
@@ -574,10 +733,14 @@ gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V
         static_cast<const T*>(V), sl2, static_cast<T*>(O), LSE, tp);
     GT_LAUNCH_CHECK("sparse_fwd_rows");
     if (p->n_long_rows > 0) {
-        k_fwd_long<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
-            p->long_rows, p->sp_rowptr, p->sp_col, static_cast<const T*>(Q), static_cast<const T*>(K),
-            static_cast<const T*>(V), sl2, static_cast<T*>(O), LSE, tp);
+        if ((st = long_chunks(p->long_rows, p->n_long_rows, p->sp_rowptr, lp, s)) != GT_OK) return st;
+        k_fwd_long<T, D, H><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
+            p->long_rows, p->n_long_rows, lp.chunk_off, p->sp_rowptr, p->sp_col, static_cast<const T*>(Q),
+            static_cast<const T*>(K), static_cast<const T*>(V), sl2, lp.part);
         GT_LAUNCH_CHECK("sparse_fwd_long");
+        k_fwd_long_merge<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
+            p->long_rows, lp.chunk_off, lp.part, tp, static_cast<T*>(O), LSE);
+        GT_LAUNCH_CHECK("sparse_fwd_long_merge");
     }
     return GT_OK;
 }
@@ -591,6 +754,7 @@ gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const vo
     Ws ws(ws_ptr);
     ws.take<char>(256);
     TileBwdPartials tb = tile_partials_bwd(ws, p, H, D, true, false);
+    LongPlan lp = long_plan_take(ws, p->n_long_rows, p->nnz_sparse, RowLongF<H, D>);
     const float sl2 = scale * kLog2e;
     const T *q = static_cast<const T*>(Q), *k = static_cast<const T*>(K), *v = static_cast<const T*>(V);
     const T* g = static_cast<const T*>(dO);
@@ -603,9 +767,13 @@ gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const vo
                                                   sl2, scale, static_cast<T*>(dQ), tb.dq);
     GT_LAUNCH_CHECK("sparse_bwd_rows");
     if (p->n_long_rows > 0) {
-        k_bwd_rows_long<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
-            p->long_rows, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, Dv, sl2, scale, static_cast<T*>(dQ), tb.dq);
+        if ((st = long_chunks(p->long_rows, p->n_long_rows, p->sp_rowptr, lp, s)) != GT_OK) return st;
+        k_bwd_rows_long<T, D, H><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
+            p->long_rows, p->n_long_rows, lp.chunk_off, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, sl2, lp.part);
         GT_LAUNCH_CHECK("sparse_bwd_rows_long");
+        k_bwd_rows_long_merge<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
+            p->long_rows, lp.chunk_off, lp.part, tb.dq, scale, static_cast<T*>(dQ), Dv);
+        GT_LAUNCH_CHECK("sparse_bwd_rows_long_merge");
     }
     return GT_OK;
 }
@@ -620,6 +788,7 @@ gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const vo
     Ws ws(ws_ptr);
     ws.take<char>(256);
     TileBwdPartials tb = tile_partials_bwd(ws, p, H, D, false, true);
+    LongPlan lp = long_plan_take(ws, p->n_long_cols, p->nnz_sparse, ColLongF<H, D>);
     const float sl2 = scale * kLog2e;
     const T *q = static_cast<const T*>(Q), *k = static_cast<const T*>(K), *v = static_cast<const T*>(V);
     const T* g = static_cast<const T*>(dO);
@@ -632,10 +801,14 @@ gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const vo
                                                   sl2, scale, static_cast<T*>(dK), static_cast<T*>(dV), tb.dk, tb.dv);
     GT_LAUNCH_CHECK("sparse_bwd_cols");
     if (p->n_long_cols > 0) {
-        k_bwd_cols_long<T, D, H><<<unsigned(p->n_long_cols), kThreads, 0, s>>>(
-            p->long_cols, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2, scale, static_cast<T*>(dK),
-            static_cast<T*>(dV), tb.dk, tb.dv);
+        if ((st = long_chunks(p->long_cols, p->n_long_cols, p->sp_colptr, lp, s)) != GT_OK) return st;
+        k_bwd_cols_long<T, D, H><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
+            p->long_cols, p->n_long_cols, lp.chunk_off, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2,
+            lp.part);
         GT_LAUNCH_CHECK("sparse_bwd_cols_long");
+        k_bwd_cols_long_merge<T, D, H><<<unsigned(p->n_long_cols), kThreads, 0, s>>>(
+            p->long_cols, lp.chunk_off, lp.part, tb.dk, tb.dv, scale, static_cast<T*>(dK), static_cast<T*>(dV));
+        GT_LAUNCH_CHECK("sparse_bwd_cols_long_merge");
     }
     return GT_OK;
 }
@@ -673,12 +846,15 @@ size_t fwd_ws(const gt_tiles* p, int32_t H, int32_t d) {
     Ws ws(nullptr);
     ws.take<char>(256);
     tile_partials_fwd(ws, p, H, d);
+    long_plan_take(ws, p->n_long_rows, p->nnz_sparse, int64_t(H) * d + 2 * H);
     return ws.size();
 }
 size_t bwd_part_ws(const gt_tiles* p, int32_t H, int32_t d, bool rows, bool cols) {
     Ws ws(nullptr);
     ws.take<char>(256);
     tile_partials_bwd(ws, p, H, d, rows, cols);
+    if (rows) long_plan_take(ws, p->n_long_rows, p->nnz_sparse, 2 * int64_t(H) * d + H);
+    if (cols) long_plan_take(ws, p->n_long_cols, p->nnz_sparse, 2 * int64_t(H) * d);
     return ws.size();
 }
 size_t bwd_ws(const gt_tiles* p, int32_t H, int32_t d) {

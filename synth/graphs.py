@@ -179,3 +179,48 @@ def chung_lu_graph(n: int, gamma: float, avg_degree: float, max_degree: float, s
             "max_degree_cap": max_degree, "pairs_drawn": m, "seed": seed,
             "n_at_cap": int((w >= max_degree).sum())}
     return Graph(n=n, rowptr=rowptr, col=col, block=None, info=info)
+
+
+def batched_graphs(sizes, avg_degree: float, seed: int, global_token: bool = False,
+                   self_loops: bool = True) -> Graph:
+    """Many small graphs as one block-diagonal graph (graph-level batching).
+
+    Graph g gets ``sizes[g]`` consecutive node ids.  Each is a random spanning
+    tree (every node links to a uniformly chosen earlier node, so the graph is
+    connected) plus extra uniformly random in-graph pairs up to
+    ``round(size * avg_degree / 2)`` pairs in total (molecule-like rings when
+    avg_degree is near 2).  With ``global_token`` one more node (the last id)
+    is linked to every node in both directions, a degree-N row and column.
+    Nodes keep the batch order: each graph is contiguous.
+    """
+    rng = _rng(seed)
+    sizes = np.asarray(sizes, dtype=np.int64)
+    starts = np.concatenate([[0], np.cumsum(sizes)[:-1]])
+    n_real = int(sizes.sum())
+    us, vs = [], []
+    # spanning trees: node k > 0 of a graph links to a uniform earlier node of the same graph
+    local = np.arange(n_real, dtype=np.int64) - np.repeat(starts, sizes)
+    first = local > 0
+    parent_local = (rng.random(n_real) * np.maximum(local, 1)).astype(np.int64)
+    node = np.arange(n_real, dtype=np.int64)
+    us.append(node[first])
+    vs.append((node - local + parent_local)[first])
+    # extra in-graph pairs
+    extra = np.maximum(0, np.round(sizes * avg_degree / 2.0).astype(np.int64) - (sizes - 1))
+    g_of = np.repeat(np.arange(len(sizes)), extra)
+    a = starts[g_of] + (rng.random(len(g_of)) * sizes[g_of]).astype(np.int64)
+    b = starts[g_of] + (rng.random(len(g_of)) * sizes[g_of]).astype(np.int64)
+    keep = a != b
+    us.append(a[keep])
+    vs.append(b[keep])
+    n = n_real + (1 if global_token else 0)
+    if global_token:
+        us.append(np.full(n_real, n_real, dtype=np.int64))
+        vs.append(np.arange(n_real, dtype=np.int64))
+    rowptr, col = csr_from_pairs(n, np.concatenate(us), np.concatenate(vs), symmetric=True, self_loops=self_loops)
+    block = np.repeat(np.arange(len(sizes)), sizes)
+    if global_token:
+        block = np.concatenate([block, [-1]])
+    info = {"kind": "batched", "graphs": len(sizes), "mean_size": float(sizes.mean()),
+            "avg_degree_nominal": avg_degree, "global_token": global_token, "seed": seed}
+    return Graph(n=n, rowptr=rowptr, col=col, block=block, info=info)

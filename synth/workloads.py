@@ -1,6 +1,8 @@
-"""The five named workloads (graph + tensor recipes) and scaled-down variants.
+"""The named workloads (graph + tensor recipes) and scaled-down variants.
 
-Recipes (seed = 1000 + workload number; node order shuffled in every graph):
+Recipes (seed = 1000 + workload number for the c workloads, 2000 + number for
+the b workloads; node order shuffled in every c graph, batch order kept in the
+b graphs):
 
 * ``c1``: SBM, 4,096 nodes, 16 equal blocks, average degree 8, 10% of pairs
   across blocks; Q,K,V fp32 [4096, 1, 64]; forward only.
@@ -12,6 +14,12 @@ Recipes (seed = 1000 + workload number; node order shuffled in every graph):
   30, 5% across; bf16 [1M, 8, 32]; 128-wide tiles at densities 1%, 5%, 20%.
 * ``c5``: SBM, 65,536 nodes, 256 equal blocks, degree 20, 10% across;
   bf16 [65536, 8, 64]; a sparse layer then a full dense layer.
+* ``b1``: graph-level batch of molecule-sized graphs (23 to 26 nodes, degree
+  2.2: a spanning tree plus a few ring closures), 40,000 graphs, plus a
+  global token attending to and attended by every node; bf16 [N, 8, 32].
+* ``b2``: graph-level batch of call-graph-sized graphs (log-normal sizes with
+  mean 15,378 nodes, degree 4.57), 64 graphs, plus a global token; bf16
+  [N, 8, 32].
 
 ``scale`` shrinks the node count (and block count, keeping block sizes) so the
 same recipe can run at oracle-friendly sizes.
@@ -23,7 +31,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .graphs import Graph, chung_lu_graph, lognormal_block_sizes, sbm_graph
+from .graphs import Graph, batched_graphs, chung_lu_graph, lognormal_block_sizes, sbm_graph
 from .tensors import normal_tensor
 
 
@@ -68,13 +76,17 @@ WORKLOADS = {
                dim=32, dtype="bf16", backward=True, tile=128, taus=(0.01, 0.05, 0.20)),
     "c5": dict(n=65_536, kind="sbm", blocks=256, degree=20, cross=0.10, heads=8, dim=64, dtype="bf16",
                backward=True, tile=128, taus=(0.01,)),
+    "b1": dict(n=1_000_000, kind="batched", graphs=40_000, size_lo=23, size_hi=26, degree=2.2, token=True,
+               heads=8, dim=32, dtype="bf16", backward=True, tile=128, taus=(0.01, 0.05)),
+    "b2": dict(n=1_000_000, kind="batched_lognormal", graphs=64, size_mean=15_378, sigma=0.8, degree=4.57,
+               token=True, heads=8, dim=32, dtype="bf16", backward=True, tile=128, taus=(0.05,)),
 }
 
 
 def make_workload(name: str, scale: float = 1.0) -> Workload:
     """Build workload ``name``; ``scale < 1`` shrinks N (blocks shrink in number, not size)."""
     spec = WORKLOADS[name]
-    seed = 1000 + int(name[1:])
+    seed = (1000 if name[0] == "c" else 2000) + int(name[1:])
     n = max(64, int(round(spec["n"] * scale)))
     kind = spec["kind"]
     if kind == "sbm":
@@ -90,6 +102,21 @@ def make_workload(name: str, scale: float = 1.0) -> Workload:
         cap = min(spec["cap"], max(2, n // 50))
         g = chung_lu_graph(n, spec["gamma"], spec["degree"], cap, seed)
         desc = f"Chung-Lu n={n} gamma={spec['gamma']} deg={spec['degree']} cap={cap}"
+    elif kind == "batched":
+        rng = np.random.Generator(np.random.PCG64(seed + 1))
+        ng = max(1, int(round(spec["graphs"] * scale)))
+        sizes = rng.integers(spec["size_lo"], spec["size_hi"] + 1, size=ng)
+        g = batched_graphs(sizes, spec["degree"], seed, global_token=spec["token"])
+        desc = (f"batch of {ng} graphs of {spec['size_lo']}-{spec['size_hi']} nodes, deg={spec['degree']}"
+                f"{', global token' if spec['token'] else ''}")
+    elif kind == "batched_lognormal":
+        rng = np.random.Generator(np.random.PCG64(seed + 1))
+        ng = max(1, int(round(spec["graphs"] * scale)))
+        mu = np.log(spec["size_mean"]) - spec["sigma"] ** 2 / 2
+        sizes = np.maximum(2, np.round(rng.lognormal(mu, spec["sigma"], size=ng))).astype(np.int64)
+        g = batched_graphs(sizes, spec["degree"], seed, global_token=spec["token"])
+        desc = (f"batch of {ng} graphs, log-normal sizes mean {spec['size_mean']} sigma {spec['sigma']}, "
+                f"deg={spec['degree']}{', global token' if spec['token'] else ''}")
     else:
         raise ValueError(kind)
     return Workload(name=name, graph=g, heads=spec["heads"], dim=spec["dim"], dtype=spec["dtype"],

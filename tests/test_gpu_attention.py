@@ -161,13 +161,15 @@ def test_pipeline_reorder_then_attention_is_equivariant(gt):
 
 
 @pytest.mark.parametrize("name,tau", [("c2", 10_000), ("c3", 10_000), ("c4", 50_000), ("c4", 10_000),
-                                      ("c5", 10_000)])
+                                      ("c5", 10_000), ("b1", 10_000), ("b2", 50_000)])
 def test_full_size_workloads_sampled(gt, name, tau):
     # The workloads at their full sizes through the library's whole pipeline, in the launch configuration the
     # benchmark times (reorder, relabel, 128-wide tiles at the workload's threshold, row gather, forward and
     # both backward passes), with the outputs scattered back to the input order.  The oracle computes 192
     # random rows (forward, dQ) and columns (dK, dV) one by one on the original graph, plus the eight rows of
-    # largest degree (hubs on the power-law graph).
+    # largest degree (hubs on the power-law graph, the global token of the batched graphs).  A column attended
+    # by more than 65,536 rows (the global token's) is left to the small batched test, which checks it in
+    # full: its dK and dV need the softmax statistics of every row.
     w = make_workload(name)
     g = w.graph
     q, k, v, do = w.tensors()
@@ -186,9 +188,24 @@ def test_full_size_workloads_sampled(gt, name, tau):
     rng = np.random.default_rng(11)
     deg = np.diff(g.rowptr)
     rows = np.unique(np.concatenate([rng.choice(g.n, size=192, replace=False), np.argsort(deg)[-8:]]))
+    cols = rows[deg[rows] <= 65_536]
+    say("  oracle on", len(rows), "rows and", len(cols), "columns")
     O_ref, L_ref = OA.sparse_attn_fwd(g.rowptr, g.col, q, k, v, scale, rows=rows)
-    dq_ref, dk_ref, dv_ref = OA.sparse_attn_bwd_sampled(g.rowptr, g.col, q, k, v, do, scale, rows, rows)
+    dq_ref, dk_ref, dv_ref = OA.sparse_attn_bwd_sampled(g.rowptr, g.col, q, k, v, do, scale, rows, cols)
+    say("  oracle done")
     idx = torch.from_numpy(rows).cuda()
-    for nm, x, r in zip(("O", "dQ", "dK", "dV"), (outs[0], outs[2], outs[3], outs[4]), (O_ref, dq_ref, dk_ref, dv_ref)):
+    cdx = torch.from_numpy(cols).cuda()
+    for nm, x, r in zip(("O", "dQ"), (outs[0], outs[2]), (O_ref, dq_ref)):
         assert_close(host(x[idx]), r, w.dtype, f"{name} {nm}")
+    for nm, x, r in zip(("dK", "dV"), (outs[3], outs[4]), (dk_ref, dv_ref)):
+        assert_close(host(x[cdx]), r, w.dtype, f"{name} {nm}")
     assert_close(outs[1][idx].cpu().numpy(), L_ref, w.dtype, f"{name} LSE")
+
+
+def test_batched_small_graphs_with_global_token(gt):
+    # Graph-level batching: 400 molecule-sized graphs as one block-diagonal graph plus a global token whose
+    # row and column hold every node (a 9,809-edge row and column, cut into chunks), every tile plan.
+    w = make_workload("b1", 0.01)
+    g = w.graph
+    run_case(gt, g.rowptr, g.col, 8, 32, "bf16", taus=SWEEP, seed=21)
+    run_case(gt, g.rowptr, g.col, 2, 64, "f32", taus=(10_000, CSR_ONLY), seed=22)

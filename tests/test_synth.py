@@ -58,3 +58,50 @@ def test_bf16_rounding_matches_torch():
     ref = torch.from_numpy(x).to(torch.bfloat16).float().numpy()
     np.testing.assert_array_equal(bf16_round(x), ref)
     np.testing.assert_array_equal(bf16_to_f32(bf16_bits(x)), ref)
+
+
+def test_batched_graphs_block_diagonal_connected_with_global_token():
+    from synth import batched_graphs
+
+    sizes = np.array([3, 25, 24, 1, 26])
+    g = batched_graphs(sizes, 2.2, seed=7, global_token=True)
+    n_real = int(sizes.sum())
+    assert g.n == n_real + 1
+    rp, cl = g.rowptr, g.col
+    starts = np.concatenate([[0], np.cumsum(sizes)])
+    token = n_real
+    # symmetric, sorted, self-loops, token row/column complete
+    dense = np.zeros((g.n, g.n), dtype=bool)
+    for i in range(g.n):
+        row = cl[rp[i]:rp[i + 1]]
+        assert np.all(np.diff(row) > 0)
+        dense[i, row] = True
+    assert np.array_equal(dense, dense.T)
+    assert dense.diagonal().all()
+    assert dense[token].all() and dense[:, token].all()
+    # block-diagonal apart from the token, and every small graph connected
+    for a, b in zip(starts[:-1], starts[1:]):
+        blk = dense[a:b, a:b]
+        outside = dense[a:b, :n_real].copy()
+        outside[:, a:b] = False
+        assert not outside.any()
+        seen = {0}
+        frontier = [0]
+        while frontier:
+            u = frontier.pop()
+            for v in np.nonzero(blk[u])[0]:
+                if v not in seen:
+                    seen.add(int(v))
+                    frontier.append(int(v))
+        assert len(seen) == b - a
+
+
+def test_batched_workloads_shapes():
+    from synth import make_workload
+
+    w = make_workload("b1", 0.01)
+    deg = np.diff(w.graph.rowptr)
+    assert deg.max() == w.graph.n  # the global token attends to every node, itself included
+    assert w.graph.info["graphs"] == 400
+    w2 = make_workload("b2", 0.05)
+    assert w2.graph.info["global_token"] and w2.graph.n > 3 * 2
