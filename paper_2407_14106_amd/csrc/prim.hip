@@ -303,29 +303,57 @@ gt_status radix_sort_u64(uint64_t* keys, uint32_t* values, int64_t n, int key_bi
 
 // =========================================================== CSR validation
 
+// Rows of up to kValidateShort entries are checked by one thread each; the
+// wavefront takes every longer row of its batch together, its lanes striding
+// the row 64 entries apart and comparing each entry with the one before it
+// in memory, so a row that holds every node is not left to one thread.
+constexpr int64_t kValidateShort = 256;
+
 __global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
                                uint32_t* flags) {
     uint32_t f = 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         if (rowptr[0] != 0 || rowptr[n] != nnz) f |= kOutOfRange;
     }
-    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
-        const int64_t a = rowptr[i], b = rowptr[i + 1];
-        if (a > b) {
-            f |= kUnsorted;
-            continue;
+    const int lane = lane_id();
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    // wave-uniform loop: every lane of a wavefront runs the same number of rounds
+    for (int64_t base = int64_t(blockIdx.x) * blockDim.x + (threadIdx.x - lane); base < n; base += stride) {
+        const int64_t i = base + lane;
+        bool long_row = false;
+        int64_t a = 0, b = 0;
+        if (i < n) {
+            a = rowptr[i];
+            b = rowptr[i + 1];
+            if (a > b) f |= kUnsorted;
+            else if (a < 0 || b > nnz) f |= kOutOfRange;
+            else if (b - a > kValidateShort) long_row = true;
+            else {
+                int64_t prev = -1;
+                for (int64_t e = a; e < b; ++e) {
+                    const int64_t c = col[e];
+                    if (c < 0 || c >= n) f |= kOutOfRange;
+                    if (c == prev) f |= kDuplicate;
+                    else if (c < prev) f |= kUnsorted;
+                    prev = c;
+                }
+            }
         }
-        if (a < 0 || b > nnz) {
-            f |= kOutOfRange;
-            continue;
-        }
-        int64_t prev = -1;
-        for (int64_t e = a; e < b; ++e) {
-            const int64_t c = col[e];
-            if (c < 0 || c >= n) f |= kOutOfRange;
-            if (c == prev) f |= kDuplicate;
-            else if (c < prev) f |= kUnsorted;
-            prev = c;
+        uint64_t pending = __ballot(long_row);
+        while (pending) {
+            const int src = __builtin_ctzll(pending);
+            pending &= pending - 1;
+            const int64_t ra = __shfl(a, src, kWave), rb = __shfl(b, src, kWave);
+#pragma unroll 4
+            for (int64_t e = ra + lane; e < rb; e += kWave) {
+                const int64_t c = col[e];
+                if (c < 0 || c >= n) f |= kOutOfRange;
+                if (e > ra) {
+                    const int64_t prev = col[e - 1];
+                    if (c == prev) f |= kDuplicate;
+                    else if (c < prev) f |= kUnsorted;
+                }
+            }
         }
     }
     if (f) atomicOr(flags, f);
