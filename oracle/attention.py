@@ -28,6 +28,13 @@ Backward, for an upstream gradient dO:
     dK_j  = scale * sum_{i : j in N(i)} dS_ij Q[i,h]
     dV_j  = sum_{i : j in N(i)} P_ij dO[i,h]
 
+With a per-edge bias b (the graph encoding of §2.1 Eq. (3), added to the
+scaled product; it shares the attention's sparse layout, §3.3), given as
+[nnz, H] in CSR order:
+
+    s_ij  = scale * <Q[i,h], K[j,h]> + b_ij[h]
+    dB_ij = dS_ij
+
 All arrays are [N, H, d] (node, head, feature); LSE and D are [N, H].
 Inputs are upcast to fp64; bfloat16 workloads pass the already-rounded values.
 """
@@ -71,14 +78,16 @@ def _row_chunks(rowptr: np.ndarray, rows: np.ndarray, per_edge: int):
         start = stop
 
 
-def _edges_of(rowptr, col, rows):
-    """Edge list (local row index, neighbour id) for the given rows, in CSR order."""
+def _edges_of(rowptr, col, rows, with_pos=False):
+    """Edge list (local row index, neighbour id) for the given rows, in CSR order (and the CSR positions)."""
     deg = (rowptr[rows + 1] - rowptr[rows]).astype(np.int64)
     local = np.repeat(np.arange(len(rows)), deg)
     first = np.zeros(len(rows), dtype=np.int64)
     if len(rows):
         np.cumsum(deg[:-1], out=first[1:])
     idx = np.arange(int(deg.sum()), dtype=np.int64) - np.repeat(first, deg) + np.repeat(rowptr[rows], deg)
+    if with_pos:
+        return local, col[idx].astype(np.int64), deg, idx
     return local, col[idx].astype(np.int64), deg
 
 
@@ -106,9 +115,11 @@ def _segment_softmax_stats(s, local, n_rows):
     return lse
 
 
-def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
-    """O[rows], LSE[rows] of neighbourhood softmax attention (all rows when ``rows`` is None)."""
+def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None, bias=None):
+    """O[rows], LSE[rows] of neighbourhood softmax attention (all rows when ``rows`` is None); ``bias`` is the
+    optional per-edge term [nnz, H] in CSR order."""
     Q, K, V = _Widen(Q), _Widen(K), _Widen(V)
+    B = None if bias is None else np.asarray(bias, dtype=np.float64)
     N, H, d = Q.shape
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
@@ -117,7 +128,7 @@ def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
     LSE = np.full((len(rows), H), -np.inf)
     pos = 0
     for chunk in _row_chunks(rowptr, rows, H * d):
-        local, nbr, _ = _edges_of(rowptr, col, chunk)
+        local, nbr, _, epos = _edges_of(rowptr, col, chunk, with_pos=True)
         n = len(chunk)
         if n == 1 and len(nbr) > 4096:
             # one long row (a hub, a global token): the same definition per head, as contractions over its
@@ -126,6 +137,8 @@ def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
             Kn, Vn = K[nbr], V[nbr]
             for h in range(H):
                 s = scale * (Kn[:, h, :] @ Q[r, h, :])
+                if B is not None:
+                    s = s + B[epos, h]
                 m = s.max()
                 p = np.exp(s - m)
                 tot = p.sum()
@@ -134,6 +147,8 @@ def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
         elif len(nbr):
             i = chunk[local]
             s = scale * np.einsum("ehc,ehc->eh", Q[i], K[nbr])
+            if B is not None:
+                s = s + B[epos]
             lse = _segment_softmax_stats(s, local, n)
             p = np.exp(s - lse[local])
             o = np.zeros((n, H, d))
@@ -145,72 +160,90 @@ def sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=None):
     return O, LSE
 
 
-def _csc(rowptr, col, N):
-    """In-neighbour lists: for each column j, the rows i with j in N(i), ascending."""
+def _csc(rowptr, col, N, with_pos=False):
+    """In-neighbour lists: for each column j, the rows i with j in N(i), ascending (and each entry's CSR
+    position)."""
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
     rows = np.repeat(np.arange(N), np.diff(rowptr))
     order = np.argsort(col, kind="stable")
     colptr = np.zeros(N + 1, dtype=np.int64)
     np.cumsum(np.bincount(col, minlength=N), out=colptr[1:])
+    if with_pos:
+        return colptr, rows[order], order
     return colptr, rows[order]
 
 
-def sparse_attn_bwd(rowptr, col, Q, K, V, dO, scale):
-    """dQ, dK, dV of neighbourhood softmax attention for the whole graph."""
+def sparse_attn_bwd(rowptr, col, Q, K, V, dO, scale, bias=None):
+    """dQ, dK, dV of neighbourhood softmax attention for the whole graph (and dB [nnz, H] with a bias)."""
     Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
     N, H, d = Q.shape
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
-    O, LSE = sparse_attn_fwd(rowptr, col, Q, K, V, scale)
+    B = None if bias is None else np.asarray(bias, dtype=np.float64)
+    O, LSE = sparse_attn_fwd(rowptr, col, Q, K, V, scale, bias=B)
     D = np.einsum("nhc,nhc->nh", dO, O)
     dQ = np.zeros_like(Q)
     dK = np.zeros_like(K)
     dV = np.zeros_like(V)
+    dB = None if B is None else np.zeros_like(B)
     for chunk in _row_chunks(rowptr, np.arange(N), H * d):
-        local, j, _ = _edges_of(rowptr, col, chunk)
+        local, j, _, epos = _edges_of(rowptr, col, chunk, with_pos=True)
         if not len(j):
             continue
         i = chunk[local]
         s = scale * np.einsum("ehc,ehc->eh", Q[i], K[j])
+        if B is not None:
+            s = s + B[epos]
         p = np.exp(s - LSE[i])
         dp = np.einsum("ehc,ehc->eh", dO[i], V[j])
         ds = p * (dp - D[i])
+        if dB is not None:
+            dB[epos] = ds
         np.add.at(dQ, i, scale * ds[:, :, None] * K[j])
         np.add.at(dK, j, scale * ds[:, :, None] * Q[i])
         np.add.at(dV, j, p[:, :, None] * dO[i])
+    if dB is not None:
+        return dQ, dK, dV, dB
     return dQ, dK, dV
 
 
-def sparse_attn_bwd_sampled(rowptr, col, Q, K, V, dO, scale, rows, cols):
+def sparse_attn_bwd_sampled(rowptr, col, Q, K, V, dO, scale, rows, cols, bias=None):
     """dQ[rows], dK[cols], dV[cols] computed from only the rows they depend on.
 
     dQ_i needs row i alone; dK_j and dV_j need every row i that has j as a
-    neighbour (with that row's LSE_i and D_i, each row-local).
+    neighbour (with that row's LSE_i and D_i, each row-local).  With a bias, a
+    fourth result (positions, dB) holds dB of the sampled rows' edges with their
+    CSR positions.
     """
     Q, K, V, dO = _Widen(Q), _Widen(K), _Widen(V), _Widen(dO)
+    B = None if bias is None else np.asarray(bias, dtype=np.float64)
     N, H, d = Q.shape
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
     rows = np.asarray(rows, dtype=np.int64)
     cols = np.asarray(cols, dtype=np.int64)
 
-    colptr, inrow = _csc(rowptr, col, N)
+    colptr, inrow, inpos = _csc(rowptr, col, N, with_pos=True)
     # LSE_i and D_i of the sampled rows and of every source row a sampled column needs, each computed once
     need = np.unique(np.concatenate([rows] + [inrow[colptr[jj]:colptr[jj + 1]] for jj in cols]))
     slot = np.full(N, -1, dtype=np.int64)
     slot[need] = np.arange(len(need))
-    O_n, L_n = sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=need)
+    O_n, L_n = sparse_attn_fwd(rowptr, col, Q, K, V, scale, rows=need, bias=B)
     D_n = np.einsum("nhc,nhc->nh", dO[need], O_n)
     L_r, D_r = L_n[slot[rows]], D_n[slot[rows]]
     dQ = np.zeros((len(rows), H, d))
-    local, j, _ = _edges_of(rowptr, col, rows)
+    local, j, _, epos = _edges_of(rowptr, col, rows, with_pos=True)
+    dB_r = np.zeros((len(j), H))
     if len(j):
         i = rows[local]
         s = scale * np.einsum("ehc,ehc->eh", Q[i], K[j])
+        if B is not None:
+            s = s + B[epos]
         p = np.exp(s - L_r[local])
         dp = np.einsum("ehc,ehc->eh", dO[i], V[j])
         ds = p * (dp - D_r[local])
+        dB_r = ds
         nz, first = _segments(local, len(rows))
         dQ[nz] = np.add.reduceat(scale * ds[:, :, None] * K[j], first, axis=0)
 
@@ -222,11 +255,15 @@ def sparse_attn_bwd_sampled(rowptr, col, Q, K, V, dO, scale, rows, cols):
             continue
         L_s, D_s = L_n[slot[srcs]], D_n[slot[srcs]]
         s = scale * np.einsum("ehc,hc->eh", Q[srcs], K[jj])
+        if B is not None:
+            s = s + B[inpos[colptr[jj]:colptr[jj + 1]]]
         p = np.exp(s - L_s)
         dp = np.einsum("ehc,hc->eh", dO[srcs], V[jj])
         ds = p * (dp - D_s)
         dK[k] = scale * np.einsum("eh,ehc->hc", ds, Q[srcs])
         dV[k] = np.einsum("eh,ehc->hc", p, dO[srcs])
+    if B is not None:
+        return dQ, dK, dV, (epos, dB_r)
     return dQ, dK, dV
 
 

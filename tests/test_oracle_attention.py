@@ -238,3 +238,116 @@ def test_dense_bwd_matches_torch_and_sampled_rows():
     O_all, L_all = A.dense_attn_fwd(Q, K, V, scale)
     np.testing.assert_allclose(O, O_all[rows], rtol=1e-13)
     np.testing.assert_allclose(L, L_all[rows], rtol=1e-13)
+
+
+# ---------------------------------------------------------------- per-edge bias (§2.1 Eq. (3), §3.3)
+
+def dense_bias(rowptr, col, bias, n):
+    """The [H, n, n] dense form of a per-edge bias (0 outside the graph; masked anyway)."""
+    H = bias.shape[1]
+    B = np.zeros((H, n, n))
+    for i in range(n):
+        for e in range(rowptr[i], rowptr[i + 1]):
+            B[:, i, col[e]] = bias[e]
+    return B
+
+
+def test_bias_matches_torch_autograd_of_dense_masked_formulation():
+    # a different formulation: dense scores + dense bias, -inf outside the graph, torch softmax and autograd
+    n, H, d = 23, 2, 8
+    rowptr, col = random_graph(n, 0.25, seed=41)
+    Q, K, V, dO = qkv(n, H, d, seed=42)
+    bias = np.random.default_rng(43).standard_normal((len(col), H))
+    mask = torch.from_numpy(to_dense(rowptr, col, n))
+    q, k, v = (torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (Q, K, V))
+    b = torch.tensor(dense_bias(rowptr, col, bias, n), dtype=torch.float64, requires_grad=True)
+    s = 0.3 * torch.einsum("ihc,jhc->hij", q, k) + b
+    s = s.masked_fill(~mask, float("-inf"))
+    o = torch.einsum("hij,jhc->ihc", torch.softmax(s, dim=-1), v)
+    (o * torch.from_numpy(dO)).sum().backward()
+    O, L = A.sparse_attn_fwd(rowptr, col, Q, K, V, 0.3, bias=bias)
+    np.testing.assert_allclose(O, o.detach().numpy(), rtol=1e-12, atol=1e-12)
+    dQ, dK, dV, dB = A.sparse_attn_bwd(rowptr, col, Q, K, V, dO, 0.3, bias=bias)
+    np.testing.assert_allclose(dQ, q.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dK, k.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dV, v.grad.numpy(), rtol=1e-10, atol=1e-12)
+    gb = b.grad.numpy()
+    for i in range(n):
+        for e in range(rowptr[i], rowptr[i + 1]):
+            np.testing.assert_allclose(dB[e], gb[:, i, col[e]], rtol=1e-10, atol=1e-12)
+
+
+def test_bias_zero_is_the_plain_attention_and_row_constant_shifts_only_lse():
+    n, H, d = 31, 3, 4
+    rowptr, col = random_graph(n, 0.2, seed=44)
+    Q, K, V, dO = qkv(n, H, d, seed=45)
+    O0, L0 = A.sparse_attn_fwd(rowptr, col, Q, K, V, 0.5)
+    g0 = A.sparse_attn_bwd(rowptr, col, Q, K, V, dO, 0.5)
+    zero = np.zeros((len(col), H))
+    O1, L1 = A.sparse_attn_fwd(rowptr, col, Q, K, V, 0.5, bias=zero)
+    assert np.array_equal(O0, O1) and np.array_equal(L0, L1)
+    g1 = A.sparse_attn_bwd(rowptr, col, Q, K, V, dO, 0.5, bias=zero)
+    for a, b in zip(g0, g1[:3]):
+        assert np.array_equal(a, b)
+    # a constant per (row, head): softmax is shift invariant, LSE moves by the constant, dB sums to 0 per row
+    c = np.random.default_rng(46).standard_normal((n, H))
+    rows = np.repeat(np.arange(n), np.diff(rowptr))
+    O2, L2 = A.sparse_attn_fwd(rowptr, col, Q, K, V, 0.5, bias=c[rows])
+    np.testing.assert_allclose(O2, O0, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(L2, L0 + c, rtol=1e-12, atol=1e-12)
+    dQ, dK, dV, dB = A.sparse_attn_bwd(rowptr, col, Q, K, V, dO, 0.5, bias=c[rows])
+    for a, b in zip(g0, (dQ, dK, dV)):
+        np.testing.assert_allclose(a, b, rtol=1e-10, atol=1e-12)
+    row_sums = np.add.reduceat(dB, rowptr[:-1], axis=0)
+    np.testing.assert_allclose(row_sums, 0.0, atol=1e-12)
+
+
+def test_bias_minus_infinity_removes_the_edge():
+    n, H, d = 27, 2, 6
+    rowptr, col = random_graph(n, 0.3, seed=47)
+    Q, K, V, dO = qkv(n, H, d, seed=48)
+    rng = np.random.default_rng(49)
+    rows = np.repeat(np.arange(n), np.diff(rowptr))
+    cut = (rng.random(len(col)) < 0.3) & (rows != col)  # keep every self-loop
+    bias = np.where(cut[:, None], -np.inf, 0.0) * np.ones((1, H))
+    keep = ~cut
+    u, v = rows[keep], col[keep]
+    rp2, cl2 = csr_from_pairs(n, u, v, symmetric=False, self_loops=False)
+    O, L = A.sparse_attn_fwd(rowptr, col, Q, K, V, 0.4, bias=bias)
+    O2, L2 = A.sparse_attn_fwd(rp2, cl2, Q, K, V, 0.4)
+    np.testing.assert_allclose(O, O2, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(L, L2, rtol=1e-12, atol=1e-13)
+    dQ, dK, dV, dB = A.sparse_attn_bwd(rowptr, col, Q, K, V, dO, 0.4, bias=bias)
+    for a, b in zip((dQ, dK, dV), A.sparse_attn_bwd(rp2, cl2, Q, K, V, dO, 0.4)):
+        np.testing.assert_allclose(a, b, rtol=1e-10, atol=1e-12)
+    assert np.all(dB[cut] == 0.0)
+
+
+def test_bias_gradient_central_finite_differences():
+    n, H, d = 9, 1, 3
+    rowptr, col = random_graph(n, 0.4, seed=50)
+    Q, K, V, dO = qkv(n, H, d, seed=51)
+    bias = np.random.default_rng(52).standard_normal((len(col), H))
+    _, _, _, dB = A.sparse_attn_bwd(rowptr, col, Q, K, V, dO, 0.7, bias=bias)
+    eps = 1e-6
+    for e in range(0, len(col), 3):
+        bp, bm = bias.copy(), bias.copy()
+        bp[e, 0] += eps
+        bm[e, 0] -= eps
+        lp = (A.sparse_attn_fwd(rowptr, col, Q, K, V, 0.7, bias=bp)[0] * dO).sum()
+        lm = (A.sparse_attn_fwd(rowptr, col, Q, K, V, 0.7, bias=bm)[0] * dO).sum()
+        assert abs((lp - lm) / (2 * eps) - dB[e, 0]) < 1e-7
+
+
+def test_bias_bwd_sampled_equals_full():
+    n, H, d = 40, 2, 4
+    rowptr, col = random_graph(n, 0.15, seed=53)
+    Q, K, V, dO = qkv(n, H, d, seed=54)
+    bias = np.random.default_rng(55).standard_normal((len(col), H))
+    full = A.sparse_attn_bwd(rowptr, col, Q, K, V, dO, 0.6, bias=bias)
+    rows = np.array([0, 5, 17, 39])
+    dq, dk, dv, (pos, db) = A.sparse_attn_bwd_sampled(rowptr, col, Q, K, V, dO, 0.6, rows, rows, bias=bias)
+    np.testing.assert_allclose(dq, full[0][rows], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dk, full[1][rows], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dv, full[2][rows], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(db, full[3][pos], rtol=1e-12, atol=1e-13)
