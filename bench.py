@@ -8,7 +8,8 @@ under "preprocess".  Also reported: the interleaved full-attention layer
 ("dense_layer"), the fp64 oracle on a bounded sample of the same workload on
 the host's cores ("cpu_baseline", timed before the GPU is used) and, with
 --tau-sweep, the same step at density thresholds 1%, 20% and the CSR-only
-control ("tau_sweep").
+control ("tau_sweep"); with --bias, the step with a per-edge additive bias
+("edge_bias").
 
 Default workload: 1,000,000-node stochastic block model, 1,000 log-normal
 blocks, average degree 30, 5% of edges across blocks, self-loops, random node
@@ -56,6 +57,9 @@ def parse():
     ap.add_argument("--tau-sweep", action="store_true",
                     help="also time the step at density thresholds 1%%, 20%% and CSR only (c4); off by default so "
                          "that a kernel trace of the default command holds the headline launches only")
+    ap.add_argument("--bias", action="store_true",
+                    help="also time the step with a per-edge additive bias (all-remainder plan) and the plain "
+                         "step on the same plan")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB row copy (gt_gather_rows, identity order) 5 times: the reference "
                          "for scaling hardware byte counters")
@@ -78,8 +82,8 @@ EDGE_KERNEL_SOURCES = ("common.h", "attn_common.h", "sparse_attn.hip")
 
 
 def recorded_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from profiles/traffic_c4_edge_kernels.txt, if the kernel source still
-    (common.h, attn_common.h, sparse_attn.hip, concatenated) still matches the hash recorded with the counters
+    """HBM bytes per launch of `kernel` from profiles/traffic_c4_edge_kernels.txt, if the kernel sources
+    (common.h, attn_common.h, sparse_attn.hip, concatenated) still match the hash recorded with the counters
     (otherwise None)."""
     import hashlib
 
@@ -246,6 +250,43 @@ def tau_sweep(gt, rp, cl, Q, K, V, dO, scale, args, edge_heads, T):
         }
         del plan
     return out
+
+
+def bias_step(gt, w, rp, cl, perm, iperm, Q, K, V, dO, scale, edge_heads):
+    """The step with the graph-encoding bias (fp32 [nnz, H], N(0,1)): relabelled with its edges, on the
+    all-remainder plan the bias requires, against the plain step on that same plan."""
+    import torch
+
+    rp2, cl2, src = gt.permute_csr_edges(rp, cl, perm, iperm)
+    plan = gt.build_tiles(rp2, cl2, 128, gt.tau_to_ppm(1.01))
+    bias = gt.gather_rows(torch.from_numpy(w.edge_bias()).to(Q.device), src)
+    csc = gt.edge_map(plan)
+    del src
+
+    def timed(fn, steps=10):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    def with_bias():
+        O, L = gt.sparse_attn_fwd_bias(plan, Q, K, V, bias, scale)
+        gt.sparse_attn_bwd_bias(plan, csc, Q, K, V, bias, dO, L, scale)
+
+    def plain():
+        O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
+        gt.sparse_attn_bwd(plan, Q, K, V, dO, L, scale)
+
+    mb, mp = timed(with_bias), timed(plain)
+    return {"ms_per_step": round(mb, 4), "value": edge_heads / (mb / 1e3), "plain_same_plan_ms": round(mp, 4),
+            "bias_bytes_per_step": int(3 * 4 * bias.numel() + 4 * csc.numel()),
+            "note": "fwd + bwd with bias (bwd also writes dB); bias read by fwd, bwd rows, bwd cols"}
 
 
 def copy_probe():
@@ -415,6 +456,9 @@ def main():
     if args.tau_sweep and args.workload == "c4":
         log("density-threshold sweep ...")
         result["tau_sweep"] = tau_sweep(gt, rp2, cl2, Q, K, V, dO, scale, args, edge_heads, args.tile)
+    if args.bias:
+        log("step with a per-edge bias ...")
+        result["edge_bias"] = bias_step(gt, w, rp, cl, perm, iperm, Q, K, V, dO, scale, edge_heads)
     if not args.no_dense_layer:
         log("timing the full-attention layer ...")
         result["dense_layer"] = dense_layer(5)

@@ -115,6 +115,15 @@ size_t gt_permute_workspace_size(int64_t n, int64_t nnz);
 gt_status gt_permute_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, const int32_t* perm,
                          const int32_t* iperm, int64_t* rowptr_out, int32_t* col_out, void* ws, size_t ws_bytes,
                          hipStream_t stream);
+/* gt_permute_csr that also returns, for every edge e of the output,
+ * src_pos[e] = its position in the input CSR (int32[nnz], device), so that
+ * per-edge values (a bias, §2.1 Eq. (3)) follow their edges:
+ * gt_gather_rows(nnz, bytes per edge, values, src_pos, values_out).
+ * nnz < 2^31.  Same validation and errors as gt_permute_csr. */
+size_t gt_permute_edges_workspace_size(int64_t n, int64_t nnz);
+gt_status gt_permute_csr_edges(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                               const int32_t* perm, const int32_t* iperm, int64_t* rowptr_out, int32_t* col_out,
+                               int32_t* src_pos, void* ws, size_t ws_bytes, hipStream_t stream);
 /* dst row r = src row perm[r] (rows of row_bytes bytes, a multiple of 4). */
 gt_status gt_gather_rows(int64_t n, int64_t row_bytes, const void* src, const int32_t* perm, void* dst,
                          hipStream_t stream);
@@ -209,6 +218,27 @@ size_t gt_sparse_attn_bwd_cols_workspace_size(const gt_tiles* plan, int32_t H, i
 gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
                                   const void* K, const void* V, const void* dO, const float* LSE, const float* Dstat,
                                   float scale, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* With a per-edge additive bias, §2.1 Eq. (3) (the graph's structural
+ * encoding, stored in the attention's sparse layout per §3.3):
+ *   s_ij = scale*<Q[i,h],K[j,h]> + bias[e,h],
+ * e the position of edge (i, j) in the plan's remainder CSR (sp_rowptr /
+ * sp_col); bias and dbias are fp32 [nnz_sparse, H] device arrays.  The
+ * backward also writes dbias[e,h] = dS_ij (every entry written).  The bias is
+ * defined on remainder edges only, so a plan with dense tiles returns
+ * GT_ERR_UNSUPPORTED: build the plan with tau_ppm > 10^6.  nnz_sparse < 2^31.
+ * Workspaces are those of gt_sparse_attn_fwd / gt_sparse_attn_bwd.
+ * csc_pos (int32[nnz_sparse], device) comes from gt_edge_map for this plan:
+ * csc_pos[c] is the remainder-CSR position of the c-th entry of sp_row. */
+size_t gt_edge_map_workspace_size(const gt_tiles* plan);
+gt_status gt_edge_map(const gt_tiles* plan, int32_t* csc_pos, void* ws, size_t ws_bytes, hipStream_t stream);
+gt_status gt_sparse_attn_fwd_bias(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
+                                  const void* K, const void* V, const float* bias, float scale, void* O, float* LSE,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
+gt_status gt_sparse_attn_bwd_bias(const gt_tiles* plan, const int32_t* csc_pos, int32_t H, int32_t d, gt_dtype dtype,
+                                  const void* Q, const void* K, const void* V, const float* bias, const void* dO,
+                                  const float* LSE, float scale, void* dQ, void* dK, void* dV, float* dbias,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Full softmax attention, §2.1 Eq. (1) (the interleaved dense layer of §3.2).*/

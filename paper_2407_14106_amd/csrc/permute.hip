@@ -34,6 +34,21 @@ __global__ void k_key_cols(int64_t nnz, const uint64_t* keys, uint64_t mask, int
         col_out[e] = int32_t(keys[e] & mask);
 }
 
+// Rows of fewer than 32 dwords (per-edge values): one lane per dword.
+template <bool kGather>
+__global__ __launch_bounds__(256) void k_move_small_rows(int64_t n, int32_t words, const uint32_t* src,
+                                                         const int32_t* perm, uint32_t* dst) {
+    const int64_t total = n * words;
+    for (int64_t x = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; x < total; x += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t r = x / words, w = x - r * words;
+        const int64_t p = perm[r];
+        if (kGather)
+            dst[x] = src[p * words + w];
+        else
+            dst[p * words + w] = src[x];
+    }
+}
+
 // One wavefront per row; dwords per lane.
 template <bool kGather>
 __global__ __launch_bounds__(256) void k_move_rows(int64_t n, int64_t words, const uint32_t* src,
@@ -52,43 +67,38 @@ struct PermuteWs {
     uint32_t* flags;
     int64_t* deg_new;
     uint64_t* keys;
+    uint32_t* vals;  // source positions (edge map only)
     ScanTmp scan;
     SortTmp sort;
 };
 
-PermuteWs carve(Ws& ws, int64_t n, int64_t nnz) {
+PermuteWs carve(Ws& ws, int64_t n, int64_t nnz, bool with_map) {
     PermuteWs p;
     const int64_t n1 = n > 0 ? n : 1, e1 = nnz > 0 ? nnz : 1;
     p.flags = ws.take<uint32_t>(1);
     p.deg_new = ws.take<int64_t>(n1);
     p.keys = ws.take<uint64_t>(e1);
+    p.vals = with_map ? ws.take<uint32_t>(e1) : nullptr;
     p.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1)));
-    p.sort = sort_tmp(ws, e1, 8, false);
+    p.sort = sort_tmp(ws, e1, 8, with_map);
     return p;
 }
 
-}  // namespace
-}  // namespace gt
-
-using namespace gt;
-
-extern "C" size_t gt_permute_workspace_size(int64_t n, int64_t nnz) {
-    Ws ws(nullptr);
-    carve(ws, n, nnz);
-    return ws.size();
-}
-
-extern "C" gt_status gt_permute_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
-                                    const int32_t* perm, const int32_t* iperm, int64_t* rowptr_out,
-                                    int32_t* col_out, void* ws_ptr, size_t ws_bytes, hipStream_t stream) {
-    if (n < 0 || nnz < 0 || n >= (int64_t(1) << 31) || nnz >= (int64_t(1) << 32))
-        return fail(GT_ERR_INVALID_ARG, "gt_permute_csr: n or nnz out of range");
+// Relabelled CSR; with src_pos, also the old CSR position of every new edge
+// (the sort carries it as the value), so per-edge values follow the edges.
+gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                  const int32_t* perm, const int32_t* iperm, int64_t* rowptr_out, int32_t* col_out, int32_t* src_pos,
+                  void* ws_ptr, size_t ws_bytes, hipStream_t stream) {
+    const bool with_map = src_pos != nullptr;
+    if (n < 0 || nnz < 0 || n >= (int64_t(1) << 31) || nnz >= (int64_t(1) << (with_map ? 31 : 32)))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": n or nnz out of range");
     if (!rowptr || !rowptr_out || (nnz > 0 && (!col || !col_out)) || (n > 0 && (!perm || !iperm)) || !ws_ptr)
-        return fail(GT_ERR_INVALID_ARG, "gt_permute_csr: null pointer");
-    if (ws_bytes < gt_permute_workspace_size(n, nnz))
-        return fail(GT_ERR_WORKSPACE, "gt_permute_csr: workspace too small");
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": null pointer");
+    Ws need(nullptr);
+    carve(need, n, nnz, with_map);
+    if (ws_bytes < need.size()) return fail(GT_ERR_WORKSPACE, std::string(who) + ": workspace too small");
     Ws ws(ws_ptr);
-    PermuteWs p = carve(ws, n, nnz);
+    PermuteWs p = carve(ws, n, nnz, with_map);
     gt_status st;
     if (n == 0) return fill_i64(rowptr_out, 1, 0, stream);
     if ((st = launch_validate_csr(n, nnz, rowptr, col, p.flags, stream)) != GT_OK) return st;
@@ -101,10 +111,47 @@ extern "C" gt_status gt_permute_csr(int64_t n, int64_t nnz, const int64_t* rowpt
     const int bits = bits_for(n);
     k_edge_keys<<<grid_for(n, 4, 65536), 256, 0, stream>>>(n, rowptr, col, iperm, bits, p.keys);
     GT_LAUNCH_CHECK("permute_keys");
-    if ((st = radix_sort_u64(p.keys, nullptr, nnz, 2 * bits, p.sort, stream)) != GT_OK) return st;
+    if (with_map && (st = iota_u32(p.vals, nnz, stream)) != GT_OK) return st;
+    if ((st = radix_sort_u64(p.keys, p.vals, nnz, 2 * bits, p.sort, stream)) != GT_OK) return st;
     k_key_cols<<<grid_for(nnz, 256, 16384), 256, 0, stream>>>(nnz, p.keys, (uint64_t(1) << bits) - 1, col_out);
     GT_LAUNCH_CHECK("permute_cols");
+    if (with_map) {
+        if ((st = copy_bytes(src_pos, p.vals, nnz * 4, stream)) != GT_OK) return st;
+    }
     return GT_OK;
+}
+
+}  // namespace
+}  // namespace gt
+
+using namespace gt;
+
+extern "C" size_t gt_permute_workspace_size(int64_t n, int64_t nnz) {
+    Ws ws(nullptr);
+    carve(ws, n, nnz, false);
+    return ws.size();
+}
+
+extern "C" gt_status gt_permute_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                                    const int32_t* perm, const int32_t* iperm, int64_t* rowptr_out,
+                                    int32_t* col_out, void* ws_ptr, size_t ws_bytes, hipStream_t stream) {
+    return permute("gt_permute_csr", n, nnz, rowptr, col, perm, iperm, rowptr_out, col_out, nullptr, ws_ptr,
+                   ws_bytes, stream);
+}
+
+extern "C" size_t gt_permute_edges_workspace_size(int64_t n, int64_t nnz) {
+    Ws ws(nullptr);
+    carve(ws, n, nnz, true);
+    return ws.size();
+}
+
+extern "C" gt_status gt_permute_csr_edges(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                                          const int32_t* perm, const int32_t* iperm, int64_t* rowptr_out,
+                                          int32_t* col_out, int32_t* src_pos, void* ws_ptr, size_t ws_bytes,
+                                          hipStream_t stream) {
+    if (nnz > 0 && !src_pos) return fail(GT_ERR_INVALID_ARG, "gt_permute_csr_edges: null src_pos");
+    return permute("gt_permute_csr_edges", n, nnz, rowptr, col, perm, iperm, rowptr_out, col_out, src_pos, ws_ptr,
+                   ws_bytes, stream);
 }
 
 static gt_status move_rows(bool gather, int64_t n, int64_t row_bytes, const void* src, const int32_t* perm,
@@ -113,6 +160,18 @@ static gt_status move_rows(bool gather, int64_t n, int64_t row_bytes, const void
         return fail(GT_ERR_INVALID_ARG, "gt_gather_rows/gt_scatter_rows: bad n or row_bytes (must be a multiple of 4)");
     if (n == 0 || row_bytes == 0) return GT_OK;
     if (!src || !dst || !perm) return fail(GT_ERR_INVALID_ARG, "gt_gather_rows/gt_scatter_rows: null pointer");
+    if (row_bytes < 128) {
+        const int32_t words = int32_t(row_bytes / 4);
+        const unsigned gs = grid_for(n * words, 256, 65536);
+        if (gather)
+            k_move_small_rows<true><<<gs, 256, 0, stream>>>(n, words, static_cast<const uint32_t*>(src), perm,
+                                                              static_cast<uint32_t*>(dst));
+        else
+            k_move_small_rows<false><<<gs, 256, 0, stream>>>(n, words, static_cast<const uint32_t*>(src), perm,
+                                                               static_cast<uint32_t*>(dst));
+        GT_LAUNCH_CHECK("move_small_rows");
+        return GT_OK;
+    }
     const unsigned g = grid_for(n, 4, 65536);
     if (gather)
         k_move_rows<true><<<g, 256, 0, stream>>>(n, row_bytes / 4, static_cast<const uint32_t*>(src), perm,

@@ -39,6 +39,18 @@ struct Lanes {
     __device__ __forceinline__ int64_t off(int64_t node) const { return (node * H + h) * D + part * C::F; }
 };
 
+// Per-edge additive bias (the graph encoding added to the scaled product,
+// §2.1 Eq. (3); it shares the attention's sparse layout, §3.3): fp32
+// [nnz, H] indexed by remainder-CSR position.  The column pass finds an
+// in-edge's CSR position through csc_pos and writes dB = dS there.
+struct EdgeBias {
+    const float* b = nullptr;
+    const int32_t* csc_pos = nullptr;
+    float* db = nullptr;
+    // bias of CSR position pos, head h, in the exp2 domain
+    __device__ __forceinline__ float at(int64_t pos, int H, int h) const { return b[pos * H + h] * kLog2e; }
+};
+
 // F fp32 accumulators of one (node, head) slice.
 template <int F>
 struct Acc {
@@ -92,18 +104,23 @@ __device__ __forceinline__ void weight_pairs(float p, uint32_t& lo, uint32_t& hi
 // One block of two edges for the forward state.  j0/j1 are always valid
 // node ids (callers substitute a valid id for missing edges); ok0/ok1 say
 // which of the two are edges.
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias = false>
 __device__ __forceinline__ void fwd_step(Online<EdgeCfg<T, D, H>::F>& st, const Slice<T, EdgeCfg<T, D, H>::F>& q,
                                          const T* __restrict__ K, const T* __restrict__ V, int64_t j0, int64_t j1,
-                                         bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2) {
+                                         bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2, float b0 = 0.f,
+                                         float b1 = 0.f) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> k0, k1, v0, v1;
     k0.load(K + ln.off(j0));
     k1.load(K + ln.off(j1));
     v0.load(V + ln.off(j0));
     v1.load(V + ln.off(j1));
-    const float s0 = ok0 ? group_sum<C::L>(q.dot(k0)) * sl2 : kNegInf;
-    const float s1 = ok1 ? group_sum<C::L>(q.dot(k1)) * sl2 : kNegInf;
+    float s0 = ok0 ? group_sum<C::L>(q.dot(k0)) * sl2 : kNegInf;
+    float s1 = ok1 ? group_sum<C::L>(q.dot(k1)) * sl2 : kNegInf;
+    if constexpr (kBias) {
+        s0 += b0;
+        s1 += b1;
+    }
     const float mb = fmaxf(s0, s1);
     if (mb > st.m + kRescale) {
         const float alpha = st.m == kNegInf ? 0.f : exp2f(st.m - mb);
@@ -151,28 +168,37 @@ __device__ __forceinline__ int4 edge_quad(const int32_t* __restrict__ cl, int64_
 }
 
 // Walk a row's edges four at a time up to the wavefront maximum dmax, the ids
-// of the next four fetched before the current four are used; step(j0, j1,
-// ok0, ok1) takes two edges.
+// of the next four fetched before the current four are used; step(j0, j1, t,
+// ok0, ok1) takes two edges, the row's edges t and t + 1.
 template <class Step>
 __device__ __forceinline__ void walk_edges(const int32_t* __restrict__ cl, int64_t len, int64_t a, int deg, int dmax,
                                            int32_t self, Step step) {
     int4 cur = edge_quad(cl, len, a, deg, 0, self), nxt = cur;
     for (int t = 0; t < dmax; t += 4) {
         if (t + 4 < dmax) nxt = edge_quad(cl, len, a, deg, t + 4, self);
-        step(cur.x, cur.y, t < deg, t + 1 < deg);
-        if (t + 2 < dmax) step(cur.z, cur.w, t + 2 < deg, t + 3 < deg);
+        step(cur.x, cur.y, t, t < deg, t + 1 < deg);
+        if (t + 2 < dmax) step(cur.z, cur.w, t + 2, t + 2 < deg, t + 3 < deg);
         cur = nxt;
     }
 }
 
+// Bias (exp2 domain) of a row's edges t and t + 1 at CSR offset a; 0 where
+// the edge is missing.
+__device__ __forceinline__ void bias_pair(const EdgeBias& eb, int64_t a, int t, bool ok0, bool ok1, int H, int h,
+                                          float& b0, float& b1) {
+    b0 = ok0 ? eb.at(a + t, H, h) : 0.f;
+    b1 = ok1 ? eb.at(a + t + 1, H, h) : 0.f;
+}
+
 // ------------------------------------------------------------------ forward
 
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias>
 __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t* __restrict__ rp,
                                                        const int32_t* __restrict__ cl, int64_t len,
                                                        const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V, float sl2,
-                                                       T* __restrict__ O, float* __restrict__ LSE, TilePartials tp) {
+                                                       T* __restrict__ O, float* __restrict__ LSE, TilePartials tp,
+                                                       EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
     const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
@@ -192,8 +218,10 @@ __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t*
     q.load(Q + off);
     Online<C::F> st;
     if (live && deg >= 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
-    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, bool ok0, bool ok1) {
-        fwd_step<T, D, H>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2);
+    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
+        float b0 = 0.f, b1 = 0.f;
+        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln.h, b0, b1);
+        fwd_step<T, D, H, kBias>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
     });
     if (live && deg >= 0) {
         const float inv = st.l > 0.f ? 1.f / st.l : 0.f;
@@ -216,19 +244,23 @@ struct RowSums {
     float d = 0.f;
 };
 
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias = false>
 __device__ __forceinline__ void dq_step(RowSums<EdgeCfg<T, D, H>::F>& rs, const Slice<T, EdgeCfg<T, D, H>::F>& q,
                                         const Slice<T, EdgeCfg<T, D, H>::F>& g, float lse2, const T* __restrict__ K,
                                         const T* __restrict__ V, int64_t j0, int64_t j1, bool ok0, bool ok1,
-                                        const Lanes<T, D, H>& ln, float sl2) {
+                                        const Lanes<T, D, H>& ln, float sl2, float b0 = 0.f, float b1 = 0.f) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> k0, k1, v0, v1;
     k0.load(K + ln.off(j0));
     k1.load(K + ln.off(j1));
     v0.load(V + ln.off(j0));
     v1.load(V + ln.off(j1));
-    const float s0 = group_sum<C::L>(q.dot(k0)) * sl2;
-    const float s1 = group_sum<C::L>(q.dot(k1)) * sl2;
+    float s0 = group_sum<C::L>(q.dot(k0)) * sl2;
+    float s1 = group_sum<C::L>(q.dot(k1)) * sl2;
+    if constexpr (kBias) {
+        s0 += b0;
+        s1 += b1;
+    }
     const float dp0 = group_sum<C::L>(g.dot(v0));
     const float dp1 = group_sum<C::L>(g.dot(v1));
     const float p0 = ok0 ? exp2f(s0 - lse2) : 0.f;
@@ -266,14 +298,14 @@ __device__ __forceinline__ void load_row_partial(RowSums<EdgeCfg<T, D, H>::F>& r
     rs.d = tp.m[node * H + h];
 }
 
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias>
 __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t* __restrict__ rp,
                                                        const int32_t* __restrict__ cl, int64_t len,
                                                        const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V,
                                                        const T* __restrict__ dO, const float* __restrict__ LSE,
                                                        float* __restrict__ Dv, float sl2, float scale,
-                                                       T* __restrict__ dQ, TilePartials tp) {
+                                                       T* __restrict__ dQ, TilePartials tp, EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
     const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
@@ -295,8 +327,10 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
     const float lse2 = LSE[self * H + ln.h] * kLog2e;
     RowSums<C::F> rs;
     if (live && deg >= 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
-    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, bool ok0, bool ok1) {
-        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2);
+    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
+        float b0 = 0.f, b1 = 0.f;
+        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln.h, b0, b1);
+        dq_step<T, D, H, kBias>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
     });
     if (live && deg >= 0) {
 #pragma unroll
@@ -307,13 +341,16 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
 }
 
 // Column pass: dK_j = scale * sum_i dS_ij Q_i, dV_j = sum_i P_ij dO_i over the in-edges of j.
-template <typename T, int D, int H>
+// With a bias, c0/c1 are the two in-edges' CSC positions; the bias is read and
+// dB = dS written at their CSR positions.
+template <typename T, int D, int H, bool kBias = false>
 __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeCfg<T, D, H>::F>& dv,
                                          const Slice<T, EdgeCfg<T, D, H>::F>& k,
                                          const Slice<T, EdgeCfg<T, D, H>::F>& v, const T* __restrict__ Q,
                                          const T* __restrict__ dO, const float* __restrict__ LSE,
                                          const float* __restrict__ Dv, int64_t i0, int64_t i1, bool ok0, bool ok1,
-                                         const Lanes<T, D, H>& ln, float sl2) {
+                                         const Lanes<T, D, H>& ln, float sl2, const EdgeBias& eb = EdgeBias{},
+                                         int64_t c0 = 0, int64_t c1 = 0) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> q0, q1, g0, g1;
     q0.load(Q + ln.off(i0));
@@ -324,14 +361,27 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
     const float l1 = LSE[i1 * H + ln.h] * kLog2e;
     const float D0 = Dv[i0 * H + ln.h];
     const float D1 = Dv[i1 * H + ln.h];
-    const float s0 = group_sum<C::L>(q0.dot(k)) * sl2;
-    const float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
+    float s0 = group_sum<C::L>(q0.dot(k)) * sl2;
+    float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
+    int64_t e0 = 0, e1 = 0;
+    if constexpr (kBias) {
+        e0 = ok0 ? eb.csc_pos[c0] : 0;
+        e1 = ok1 ? eb.csc_pos[c1] : 0;
+        if (ok0) s0 += eb.at(e0, H, ln.h);
+        if (ok1) s1 += eb.at(e1, H, ln.h);
+    }
     const float dp0 = group_sum<C::L>(g0.dot(v));
     const float dp1 = group_sum<C::L>(g1.dot(v));
     const float p0 = ok0 ? exp2f(s0 - l0) : 0.f;
     const float p1 = ok1 ? exp2f(s1 - l1) : 0.f;
     const float ds0 = p0 * (dp0 - D0);
     const float ds1 = p1 * (dp1 - D1);
+    if constexpr (kBias) {
+        if (ln.part == 0) {
+            if (ok0) eb.db[e0 * H + ln.h] = ds0;
+            if (ok1) eb.db[e1 * H + ln.h] = ds1;
+        }
+    }
 #pragma unroll
     for (int f = 0; f < C::F; ++f) {
         dk.v[f] = fmaf(ds1, q1.f(f), fmaf(ds0, q0.f(f), dk.v[f]));
@@ -339,7 +389,7 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
     }
 }
 
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias>
 __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t* __restrict__ cp,
                                                        const int32_t* __restrict__ rw, int64_t len,
                                                        const T* __restrict__ Q,
@@ -347,7 +397,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
                                                        const T* __restrict__ dO, const float* __restrict__ LSE,
                                                        const float* __restrict__ Dv, float sl2, float scale,
                                                        T* __restrict__ dK, T* __restrict__ dV, TilePartials tpk,
-                                                       TilePartials tpv) {
+                                                       TilePartials tpv, EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
     const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
@@ -371,8 +421,8 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
         load_f32_slice<C::F>(dk.v, tpk.acc + off);
         load_f32_slice<C::F>(dv.v, tpv.acc + off);
     }
-    walk_edges(rw, len, a, deg, dmax, int32_t(self), [&](int64_t i0, int64_t i1, bool ok0, bool ok1) {
-        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, ok0, ok1, ln, sl2);
+    walk_edges(rw, len, a, deg, dmax, int32_t(self), [&](int64_t i0, int64_t i1, int t, bool ok0, bool ok1) {
+        dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, ok0, ok1, ln, sl2, eb, a + t, a + t + 1);
     });
     if (live && deg >= 0) {
         store_slice<T, C::F>(dK + off, dk.v, scale);
@@ -447,13 +497,13 @@ __device__ __forceinline__ bool chunk_of(const int64_t* __restrict__ off, int64_
     return true;
 }
 
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias>
 __global__ __launch_bounds__(kThreads) void k_fwd_long(const int32_t* __restrict__ list, int64_t n_long,
                                                        const int64_t* __restrict__ chunk_off,
                                                        const int64_t* __restrict__ rp,
                                                        const int32_t* __restrict__ cl, const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V, float sl2,
-                                                       float* __restrict__ part) {
+                                                       float* __restrict__ part, EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     constexpr int S = kThreads / C::G;  // lane groups per workgroup
     __shared__ float s_m[S][H];
@@ -475,7 +525,12 @@ __global__ __launch_bounds__(kThreads) void k_fwd_long(const int32_t* __restrict
         const bool ok1 = t + S < e1;
         const int64_t j0 = cl[a + t];
         const int64_t j1 = ok1 ? cl[a + t + S] : j0;
-        fwd_step<T, D, H>(st, q, K, V, j0, j1, true, ok1, ln, sl2);
+        float b0 = 0.f, b1 = 0.f;
+        if constexpr (kBias) {
+            b0 = eb.at(a + t, H, ln.h);
+            b1 = ok1 ? eb.at(a + t + S, H, ln.h) : 0.f;
+        }
+        fwd_step<T, D, H, kBias>(st, q, K, V, j0, j1, true, ok1, ln, sl2, b0, b1);
     }
     if (ln.part == 0) {
         s_m[ln.slot][ln.h] = st.m;
@@ -540,14 +595,14 @@ __global__ __launch_bounds__(kThreads) void k_fwd_long_merge(const int32_t* __re
     }
 }
 
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias>
 __global__ __launch_bounds__(kThreads) void k_bwd_rows_long(const int32_t* __restrict__ list, int64_t n_long,
                                                             const int64_t* __restrict__ chunk_off,
                                                             const int64_t* __restrict__ rp,
                                                             const int32_t* __restrict__ cl, const T* __restrict__ Q,
                                                             const T* __restrict__ K, const T* __restrict__ V,
                                                             const T* __restrict__ dO, const float* __restrict__ LSE,
-                                                            float sl2, float* __restrict__ part) {
+                                                            float sl2, float* __restrict__ part, EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     constexpr int S = kThreads / C::G;
     __shared__ float s_a[S][H * D];
@@ -571,7 +626,12 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows_long(const int32_t* __res
         const bool ok1 = t + S < e1;
         const int64_t j0 = cl[a + t];
         const int64_t j1 = ok1 ? cl[a + t + S] : j0;
-        dq_step<T, D, H>(rs, q, g, lse2, K, V, j0, j1, true, ok1, ln, sl2);
+        float b0 = 0.f, b1 = 0.f;
+        if constexpr (kBias) {
+            b0 = eb.at(a + t, H, ln.h);
+            b1 = ok1 ? eb.at(a + t + S, H, ln.h) : 0.f;
+        }
+        dq_step<T, D, H, kBias>(rs, q, g, lse2, K, V, j0, j1, true, ok1, ln, sl2, b0, b1);
     }
 #pragma unroll
     for (int f = 0; f < C::F; ++f) {
@@ -624,7 +684,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows_long_merge(const int32_t*
     }
 }
 
-template <typename T, int D, int H>
+template <typename T, int D, int H, bool kBias>
 __global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __restrict__ list, int64_t n_long,
                                                             const int64_t* __restrict__ chunk_off,
                                                             const int64_t* __restrict__ cp,
@@ -632,7 +692,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __res
                                                             const T* __restrict__ K, const T* __restrict__ V,
                                                             const T* __restrict__ dO, const float* __restrict__ LSE,
                                                             const float* __restrict__ Dv, float sl2,
-                                                            float* __restrict__ part) {
+                                                            float* __restrict__ part, EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     constexpr int S = kThreads / C::G;
     __shared__ float s_k[S][H * D];
@@ -654,7 +714,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __res
         const bool ok1 = t + S < e1;
         const int64_t i0 = rw[a + t];
         const int64_t i1 = ok1 ? rw[a + t + S] : i0;
-        dkv_step<T, D, H>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, true, ok1, ln, sl2);
+        dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, true, ok1, ln, sl2, eb, a + t, a + t + S);
     }
 #pragma unroll
     for (int f = 0; f < C::F; ++f) {
@@ -708,9 +768,9 @@ struct FwdWs {
     TilePartials tp;
 };
 
-template <typename T, int D, int H>
-gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V, float scale, void* O, float* LSE,
-                  void* ws_ptr, hipStream_t s) {
+template <typename T, int D, int H, bool kBias>
+gt_status run_fwd_t(const gt_tiles* p, const void* Q, const void* K, const void* V, float scale, void* O, float* LSE,
+                    void* ws_ptr, EdgeBias eb, hipStream_t s) {
     using C = EdgeCfg<T, D, H>;
     const int64_t n = p->n;
     if (n == 0) return GT_OK;
@@ -728,15 +788,15 @@ gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V
         tp = TilePartials{};
     }
     const int64_t waves = cdiv(n, C::NPW);
-    k_fwd_rows<T, D, H><<<xcd_grid(cdiv(waves, kThreads / kWave)), kThreads, 0, s>>>(
+    k_fwd_rows<T, D, H, kBias><<<xcd_grid(cdiv(waves, kThreads / kWave)), kThreads, 0, s>>>(
         n, p->sp_rowptr, p->sp_col, p->nnz_sparse, static_cast<const T*>(Q), static_cast<const T*>(K),
-        static_cast<const T*>(V), sl2, static_cast<T*>(O), LSE, tp);
+        static_cast<const T*>(V), sl2, static_cast<T*>(O), LSE, tp, eb);
     GT_LAUNCH_CHECK("sparse_fwd_rows");
     if (p->n_long_rows > 0) {
         if ((st = long_chunks(p->long_rows, p->n_long_rows, p->sp_rowptr, lp, s)) != GT_OK) return st;
-        k_fwd_long<T, D, H><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
+        k_fwd_long<T, D, H, kBias><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
             p->long_rows, p->n_long_rows, lp.chunk_off, p->sp_rowptr, p->sp_col, static_cast<const T*>(Q),
-            static_cast<const T*>(K), static_cast<const T*>(V), sl2, lp.part);
+            static_cast<const T*>(K), static_cast<const T*>(V), sl2, lp.part, eb);
         GT_LAUNCH_CHECK("sparse_fwd_long");
         k_fwd_long_merge<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
             p->long_rows, lp.chunk_off, lp.part, tp, static_cast<T*>(O), LSE);
@@ -746,8 +806,16 @@ gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V
 }
 
 template <typename T, int D, int H>
-gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
-                       const float* LSE, float scale, void* dQ, float* Dv, void* ws_ptr, hipStream_t s) {
+gt_status run_fwd(const gt_tiles* p, const void* Q, const void* K, const void* V, float scale, void* O, float* LSE,
+                  void* ws_ptr, EdgeBias eb, hipStream_t s) {
+    return eb.b ? run_fwd_t<T, D, H, true>(p, Q, K, V, scale, O, LSE, ws_ptr, eb, s)
+                : run_fwd_t<T, D, H, false>(p, Q, K, V, scale, O, LSE, ws_ptr, eb, s);
+}
+
+template <typename T, int D, int H, bool kBias>
+gt_status run_bwd_rows_t(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
+                         const float* LSE, float scale, void* dQ, float* Dv, void* ws_ptr, EdgeBias eb,
+                         hipStream_t s) {
     using C = EdgeCfg<T, D, H>;
     const int64_t n = p->n;
     if (n == 0) return GT_OK;
@@ -763,13 +831,13 @@ gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const vo
         if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, g, LSE, sl2, tb.dq, s)) != GT_OK) return st;
     }
     const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
-    k_bwd_rows<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, p->nnz_sparse, q, k, v, g, LSE, Dv,
-                                                  sl2, scale, static_cast<T*>(dQ), tb.dq);
+    k_bwd_rows<T, D, H, kBias><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, p->nnz_sparse, q, k, v, g,
+                                                         LSE, Dv, sl2, scale, static_cast<T*>(dQ), tb.dq, eb);
     GT_LAUNCH_CHECK("sparse_bwd_rows");
     if (p->n_long_rows > 0) {
         if ((st = long_chunks(p->long_rows, p->n_long_rows, p->sp_rowptr, lp, s)) != GT_OK) return st;
-        k_bwd_rows_long<T, D, H><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
-            p->long_rows, p->n_long_rows, lp.chunk_off, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, sl2, lp.part);
+        k_bwd_rows_long<T, D, H, kBias><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
+            p->long_rows, p->n_long_rows, lp.chunk_off, p->sp_rowptr, p->sp_col, q, k, v, g, LSE, sl2, lp.part, eb);
         GT_LAUNCH_CHECK("sparse_bwd_rows_long");
         k_bwd_rows_long_merge<T, D, H><<<unsigned(p->n_long_rows), kThreads, 0, s>>>(
             p->long_rows, lp.chunk_off, lp.part, tb.dq, scale, static_cast<T*>(dQ), Dv);
@@ -779,9 +847,16 @@ gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const vo
 }
 
 template <typename T, int D, int H>
-gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
-                       const float* LSE, const float* Dv, float scale, void* dK, void* dV, void* ws_ptr,
-                       hipStream_t s) {
+gt_status run_bwd_rows(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
+                       const float* LSE, float scale, void* dQ, float* Dv, void* ws_ptr, EdgeBias eb, hipStream_t s) {
+    return eb.b ? run_bwd_rows_t<T, D, H, true>(p, Q, K, V, dO, LSE, scale, dQ, Dv, ws_ptr, eb, s)
+                : run_bwd_rows_t<T, D, H, false>(p, Q, K, V, dO, LSE, scale, dQ, Dv, ws_ptr, eb, s);
+}
+
+template <typename T, int D, int H, bool kBias>
+gt_status run_bwd_cols_t(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
+                         const float* LSE, const float* Dv, float scale, void* dK, void* dV, void* ws_ptr,
+                         EdgeBias eb, hipStream_t s) {
     using C = EdgeCfg<T, D, H>;
     const int64_t n = p->n;
     if (n == 0) return GT_OK;
@@ -797,14 +872,15 @@ gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const vo
         if ((st = tile_bwd_dkdv<T, D, H>(p, q, k, v, g, LSE, Dv, sl2, tb.dk, tb.dv, s)) != GT_OK) return st;
     }
     const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
-    k_bwd_cols<T, D, H><<<grid, kThreads, 0, s>>>(n, p->sp_colptr, p->sp_row, p->nnz_sparse, q, k, v, g, LSE, Dv,
-                                                  sl2, scale, static_cast<T*>(dK), static_cast<T*>(dV), tb.dk, tb.dv);
+    k_bwd_cols<T, D, H, kBias><<<grid, kThreads, 0, s>>>(n, p->sp_colptr, p->sp_row, p->nnz_sparse, q, k, v, g,
+                                                         LSE, Dv, sl2, scale, static_cast<T*>(dK),
+                                                         static_cast<T*>(dV), tb.dk, tb.dv, eb);
     GT_LAUNCH_CHECK("sparse_bwd_cols");
     if (p->n_long_cols > 0) {
         if ((st = long_chunks(p->long_cols, p->n_long_cols, p->sp_colptr, lp, s)) != GT_OK) return st;
-        k_bwd_cols_long<T, D, H><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
+        k_bwd_cols_long<T, D, H, kBias><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
             p->long_cols, p->n_long_cols, lp.chunk_off, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2,
-            lp.part);
+            lp.part, eb);
         GT_LAUNCH_CHECK("sparse_bwd_cols_long");
         k_bwd_cols_long_merge<T, D, H><<<unsigned(p->n_long_cols), kThreads, 0, s>>>(
             p->long_cols, lp.chunk_off, lp.part, tb.dk, tb.dv, scale, static_cast<T*>(dK), static_cast<T*>(dV));
@@ -814,15 +890,23 @@ gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const vo
 }
 
 template <typename T, int D, int H>
+gt_status run_bwd_cols(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO,
+                       const float* LSE, const float* Dv, float scale, void* dK, void* dV, void* ws_ptr, EdgeBias eb,
+                       hipStream_t s) {
+    return eb.b ? run_bwd_cols_t<T, D, H, true>(p, Q, K, V, dO, LSE, Dv, scale, dK, dV, ws_ptr, eb, s)
+                : run_bwd_cols_t<T, D, H, false>(p, Q, K, V, dO, LSE, Dv, scale, dK, dV, ws_ptr, eb, s);
+}
+
+template <typename T, int D, int H>
 gt_status run_bwd(const gt_tiles* p, const void* Q, const void* K, const void* V, const void* dO, const float* LSE,
-                  float scale, void* dQ, void* dK, void* dV, void* ws_ptr, hipStream_t s) {
+                  float scale, void* dQ, void* dK, void* dV, void* ws_ptr, EdgeBias eb, hipStream_t s) {
     if (p->n == 0) return GT_OK;
     Ws ws(ws_ptr);
     float* Dv = ws.take<float>(size_t(p->n) * H);
     char* rest = ws.take<char>(1);
-    gt_status st = run_bwd_rows<T, D, H>(p, Q, K, V, dO, LSE, scale, dQ, Dv, rest, s);
+    gt_status st = run_bwd_rows<T, D, H>(p, Q, K, V, dO, LSE, scale, dQ, Dv, rest, eb, s);
     if (st != GT_OK) return st;
-    return run_bwd_cols<T, D, H>(p, Q, K, V, dO, LSE, Dv, scale, dK, dV, rest, s);
+    return run_bwd_cols<T, D, H>(p, Q, K, V, dO, LSE, Dv, scale, dK, dV, rest, eb, s);
 }
 
 bool supported(int32_t H, int32_t d, gt_dtype dt) {
@@ -884,7 +968,7 @@ extern "C" gt_status gt_sparse_attn_fwd(const gt_tiles* plan, int32_t H, int32_t
     if (plan->n > 0 && (!Q || !K || !V || !O || !LSE || !ws))
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_fwd: null pointer");
     if (ws_bytes < fwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_fwd: workspace too small");
-    return GT_DISPATCH_ATTN(dtype, d, H, run_fwd, plan, Q, K, V, scale, O, LSE, ws, stream);
+    return GT_DISPATCH_ATTN(dtype, d, H, run_fwd, plan, Q, K, V, scale, O, LSE, ws, EdgeBias{}, stream);
 }
 
 extern "C" size_t gt_sparse_attn_bwd_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype) {
@@ -909,7 +993,8 @@ extern "C" gt_status gt_sparse_attn_bwd_rows(const gt_tiles* plan, int32_t H, in
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_rows: null pointer");
     if (ws_bytes < bwd_part_ws(plan, H, d, true, false))
         return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_rows: workspace too small");
-    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_rows, plan, Q, K, V, dO, LSE, scale, dQ, Dstat, ws, stream);
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_rows, plan, Q, K, V, dO, LSE, scale, dQ, Dstat, ws, EdgeBias{},
+                            stream);
 }
 
 extern "C" size_t gt_sparse_attn_bwd_cols_workspace_size(const gt_tiles* plan, int32_t H, int32_t d,
@@ -929,7 +1014,8 @@ extern "C" gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, in
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_cols: null pointer");
     if (ws_bytes < bwd_part_ws(plan, H, d, false, true))
         return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_cols: workspace too small");
-    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_cols, plan, Q, K, V, dO, LSE, Dstat, scale, dK, dV, ws, stream);
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd_cols, plan, Q, K, V, dO, LSE, Dstat, scale, dK, dV, ws,
+                            EdgeBias{}, stream);
 }
 
 extern "C" gt_status gt_sparse_attn_bwd(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
@@ -941,5 +1027,61 @@ extern "C" gt_status gt_sparse_attn_bwd(const gt_tiles* plan, int32_t H, int32_t
     if (plan->n > 0 && (!Q || !K || !V || !dO || !LSE || !dQ || !dK || !dV || !ws))
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd: null pointer");
     if (ws_bytes < bwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd: workspace too small");
-    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, dO, LSE, scale, dQ, dK, dV, ws, stream);
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, dO, LSE, scale, dQ, dK, dV, ws, EdgeBias{}, stream);
+}
+
+// ------------------------------------------------------------ with a bias
+// The bias is defined on the plan's remainder edges, so a plan with dense
+// tiles is refused (build it with tau_ppm above 10^6 to keep every edge in the
+// remainder).
+
+static gt_status check_bias(const char* who, const gt_tiles* plan, const float* bias) {
+    if (plan->n_dense > 0)
+        return fail(GT_ERR_UNSUPPORTED, std::string(who) + ": the plan has dense tiles (bias needs an all-remainder plan)");
+    if (plan->nnz_sparse >= (int64_t(1) << 31))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": more than 2^31 - 1 edges");
+    if (plan->nnz_sparse > 0 && !bias) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": null bias");
+    return GT_OK;
+}
+
+extern "C" gt_status gt_sparse_attn_fwd_bias(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype,
+                                             const void* Q, const void* K, const void* V, const float* bias,
+                                             float scale, void* O, float* LSE, void* ws, size_t ws_bytes,
+                                             hipStream_t stream) {
+    gt_status st = check_plan("gt_sparse_attn_fwd_bias", plan);
+    if (st != GT_OK) return st;
+    if ((st = check_bias("gt_sparse_attn_fwd_bias", plan, bias)) != GT_OK) return st;
+    if (!supported(H, d, dtype))
+        return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_fwd_bias: unsupported (H, d, dtype)");
+    if (plan->n > 0 && (!Q || !K || !V || !O || !LSE || !ws))
+        return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_fwd_bias: null pointer");
+    if (ws_bytes < fwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_fwd_bias: workspace too small");
+    EdgeBias eb;
+    eb.b = bias;
+    if (plan->nnz_sparse == 0) eb.b = nullptr;
+    return GT_DISPATCH_ATTN(dtype, d, H, run_fwd, plan, Q, K, V, scale, O, LSE, ws, eb, stream);
+}
+
+extern "C" gt_status gt_sparse_attn_bwd_bias(const gt_tiles* plan, const int32_t* csc_pos, int32_t H, int32_t d,
+                                             gt_dtype dtype, const void* Q, const void* K, const void* V,
+                                             const float* bias, const void* dO, const float* LSE, float scale,
+                                             void* dQ, void* dK, void* dV, float* dbias, void* ws, size_t ws_bytes,
+                                             hipStream_t stream) {
+    gt_status st = check_plan("gt_sparse_attn_bwd_bias", plan);
+    if (st != GT_OK) return st;
+    if ((st = check_bias("gt_sparse_attn_bwd_bias", plan, bias)) != GT_OK) return st;
+    if (!supported(H, d, dtype))
+        return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_bwd_bias: unsupported (H, d, dtype)");
+    if (plan->n > 0 && (!Q || !K || !V || !dO || !LSE || !dQ || !dK || !dV || !ws))
+        return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_bias: null pointer");
+    if (plan->nnz_sparse > 0 && (!csc_pos || !dbias))
+        return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_bias: null csc_pos or dbias");
+    if (ws_bytes < bwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_bias: workspace too small");
+    EdgeBias eb;
+    if (plan->nnz_sparse > 0) {
+        eb.b = bias;
+        eb.csc_pos = csc_pos;
+        eb.db = dbias;
+    }
+    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, dO, LSE, scale, dQ, dK, dV, ws, eb, stream);
 }

@@ -334,3 +334,41 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     if ((st = exclusive_scan_u32(t.counts, R, plan->tileT_ptr, t.scan, stream)) != GT_OK) return st;
     return GT_OK;
 }
+
+// CSC -> CSR position map of the remainder: the same stable sort by column
+// that orders the transpose, carrying each edge's CSR position.
+static size_t edge_map_ws(int64_t m) {
+    Ws ws(nullptr);
+    const int64_t e1 = m > 0 ? m : 1;
+    ws.take<uint32_t>(e1);
+    ws.take<uint32_t>(e1);
+    sort_tmp(ws, e1, 4, true);
+    return ws.size();
+}
+
+extern "C" size_t gt_edge_map_workspace_size(const gt_tiles* plan) {
+    if (!plan) return 0;
+    return edge_map_ws(plan->nnz_sparse);
+}
+
+extern "C" gt_status gt_edge_map(const gt_tiles* plan, int32_t* csc_pos, void* ws_ptr, size_t ws_bytes,
+                                 hipStream_t stream) {
+    if (!plan) return fail(GT_ERR_INVALID_ARG, "gt_edge_map: null plan");
+    const int64_t n = plan->n, m = plan->nnz_sparse;
+    if (n < 0 || n >= (int64_t(1) << 31) || m < 0 || m >= (int64_t(1) << 31))
+        return fail(GT_ERR_INVALID_ARG, "gt_edge_map: n or nnz_sparse out of range");
+    if (m == 0) return GT_OK;
+    if (!plan->sp_col || !csc_pos || !ws_ptr) return fail(GT_ERR_INVALID_ARG, "gt_edge_map: null pointer");
+    if (ws_bytes < edge_map_ws(m)) return fail(GT_ERR_WORKSPACE, "gt_edge_map: workspace too small");
+    Ws ws(ws_ptr);
+    uint32_t* keys = ws.take<uint32_t>(m);
+    uint32_t* vals = ws.take<uint32_t>(m);
+    SortTmp sort = sort_tmp(ws, m, 4, true);
+    gt_status st;
+    if ((st = copy_bytes(keys, plan->sp_col, m * 4, stream)) != GT_OK) return st;
+    if ((st = iota_u32(vals, m, stream)) != GT_OK) return st;
+    if ((st = radix_sort_u32(keys, vals, m, bits_for(n), sort, stream)) != GT_OK) return st;
+    k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, vals, csc_pos);
+    GT_LAUNCH_CHECK("edge_map");
+    return GT_OK;
+}

@@ -55,6 +55,8 @@ SIGNATURES = {
     "gt_reorder": (_i32, [_i64, _i64, _vp, _vp, _i32, _u64, _vp, _vp, _vp, _P(_i32), _vp, _sz, _vp]),
     "gt_permute_workspace_size": (_sz, [_i64, _i64]),
     "gt_permute_csr": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gt_permute_edges_workspace_size": (_sz, [_i64, _i64]),
+    "gt_permute_csr_edges": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "gt_gather_rows": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp]),
     "gt_scatter_rows": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp]),
     "gt_tiles_workspace_size": (_sz, [_i64, _i64, _i32]),
@@ -71,6 +73,12 @@ SIGNATURES = {
     "gt_sparse_attn_bwd_cols_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
     "gt_sparse_attn_bwd_cols": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp,
                                        _vp, _vp, _sz, _vp]),
+    "gt_edge_map_workspace_size": (_sz, [_P(GtTiles)]),
+    "gt_edge_map": (_i32, [_P(GtTiles), _vp, _vp, _sz, _vp]),
+    "gt_sparse_attn_fwd_bias": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp,
+                                       _sz, _vp]),
+    "gt_sparse_attn_bwd_bias": (_i32, [_P(GtTiles), _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32,
+                                       _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "gt_dense_attn_fwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp]),
     "gt_dense_attn_bwd_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
     "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
@@ -172,6 +180,23 @@ def permute_csr(rowptr: torch.Tensor, col: torch.Tensor, perm: torch.Tensor, ipe
     _check(lib.gt_permute_csr(n, nnz, _ptr(rowptr), _ptr(col), _ptr(perm), _ptr(iperm), _ptr(rp), _ptr(cl),
                               _ptr(ws), ws.numel(), _stream(dev)), "gt_permute_csr")
     return rp, cl
+
+
+def permute_csr_edges(rowptr: torch.Tensor, col: torch.Tensor, perm: torch.Tensor, iperm: torch.Tensor):
+    """(rowptr_out, col_out, src_pos): the relabelled CSR and, per new edge, its old CSR position."""
+    lib = load_library()
+    _check_csr(rowptr, col)
+    n, nnz = rowptr.numel() - 1, col.numel()
+    _need(perm.dtype == torch.int32 and iperm.dtype == torch.int32 and perm.numel() == n == iperm.numel(),
+          "perm/iperm must be int32[n]")
+    dev = rowptr.device
+    rp = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    cl = torch.empty(nnz, dtype=torch.int32, device=dev)
+    src = torch.empty(nnz, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.gt_permute_edges_workspace_size(n, nnz), dev)
+    _check(lib.gt_permute_csr_edges(n, nnz, _ptr(rowptr), _ptr(col), _ptr(perm), _ptr(iperm), _ptr(rp), _ptr(cl),
+                                    _ptr(src), _ptr(ws), ws.numel(), _stream(dev)), "gt_permute_csr_edges")
+    return rp, cl, src
 
 
 def _row_bytes(x: torch.Tensor) -> int:
@@ -349,6 +374,57 @@ def sparse_attn_bwd_cols(plan: Plan, Q, K, V, dO, LSE, Dstat, scale: float | Non
                                        _ptr(Dstat), scale, _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(),
                                        _stream(Q.device)), "gt_sparse_attn_bwd_cols")
     return dK, dV
+
+
+def edge_map(plan: Plan) -> torch.Tensor:
+    """csc_pos[c]: the remainder-CSR position of the c-th entry of the plan's transpose (sp_row)."""
+    lib = load_library()
+    dev = plan.arrays["sp_rowptr"].device
+    out = torch.empty(plan.nnz_sparse, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.gt_edge_map_workspace_size(ctypes.byref(plan.c)), dev)
+    _check(lib.gt_edge_map(ctypes.byref(plan.c), _ptr(out), _ptr(ws), ws.numel(), _stream(dev)), "gt_edge_map")
+    return out
+
+
+def _check_bias(plan: Plan, bias: torch.Tensor, H: int):
+    _need(bias.dtype == torch.float32 and bias.shape == (plan.nnz_sparse, H) and bias.is_contiguous()
+          and bias.is_cuda, "bias must be a contiguous fp32 GPU tensor [nnz_sparse, H]")
+
+
+def sparse_attn_fwd_bias(plan: Plan, Q, K, V, bias, scale: float | None = None):
+    """(O, LSE) with the per-edge additive bias (remainder-CSR order, fp32 [nnz_sparse, H])."""
+    lib = load_library()
+    _check_feats(plan.n, Q, K, V)
+    n, H, d = Q.shape
+    _check_bias(plan, bias, H)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    O = torch.empty_like(Q)
+    LSE = torch.empty((n, H), dtype=torch.float32, device=Q.device)
+    ws = _workspace(lib.gt_sparse_attn_fwd_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    _check(lib.gt_sparse_attn_fwd_bias(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(bias), scale,
+                                       _ptr(O), _ptr(LSE), _ptr(ws), ws.numel(), _stream(Q.device)),
+           "gt_sparse_attn_fwd_bias")
+    return O, LSE
+
+
+def sparse_attn_bwd_bias(plan: Plan, csc_pos, Q, K, V, bias, dO, LSE, scale: float | None = None):
+    """(dQ, dK, dV, dbias) with the per-edge additive bias; csc_pos from edge_map(plan)."""
+    lib = load_library()
+    _check_feats(plan.n, Q, K, V, dO)
+    n, H, d = Q.shape
+    _check_bias(plan, bias, H)
+    _need(csc_pos.dtype == torch.int32 and csc_pos.numel() == plan.nnz_sparse, "csc_pos must be int32[nnz_sparse]")
+    _need(LSE.dtype == torch.float32 and LSE.shape == (n, H) and LSE.is_contiguous(), "LSE must be fp32 [n, H]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    dB = torch.empty_like(bias)
+    ws = _workspace(lib.gt_sparse_attn_bwd_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    _check(lib.gt_sparse_attn_bwd_bias(ctypes.byref(plan.c), _ptr(csc_pos), H, d, dt, _ptr(Q), _ptr(K), _ptr(V),
+                                       _ptr(bias), _ptr(dO), _ptr(LSE), scale, _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(dB),
+                                       _ptr(ws), ws.numel(), _stream(Q.device)), "gt_sparse_attn_bwd_bias")
+    return dQ, dK, dV, dB
 
 
 def dense_attn_fwd(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: float | None = None):

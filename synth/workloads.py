@@ -58,6 +58,10 @@ class Workload:
         do = normal_tensor(shape, (self.seed, 3), self.dtype) if want else None
         return q, k, v, do
 
+    def edge_bias(self) -> np.ndarray:
+        """A per-edge, per-head additive bias: fp32 N(0, 1) draws [nnz, heads] in the graph's CSR order."""
+        return normal_tensor((self.graph.nnz, self.heads), (self.seed, 4), "f32")
+
 
 def _equal_blocks(n: int, nb: int) -> np.ndarray:
     base = np.full(nb, n // nb, dtype=np.int64)

@@ -35,7 +35,28 @@ def host(x: torch.Tensor) -> np.ndarray:
     return x.float().cpu().numpy().astype(np.float64)
 
 
-def assert_close(x, r, dtype: str, name: str):
+def grad_term_rms(rowptr, col, q, k, v, do, scale):
+    """Root-mean-square size of one term of each fp32 gradient, over every (edge, head):
+    scale |dP_ij| |K_j| for dQ_i, scale |dP_ij| |Q_i| for dK_j, |dO_i| for dV_j and |dP_ij| for
+    dS_ij = P_ij (dP_ij - D_i) (P_ij <= 1).
+
+    A gradient that is zero through exact cancellation (a row with one edge has dS = 0) still carries the fp32
+    rounding of its terms, so on graphs where most rows cancel these are the floors rho to use instead of the
+    result's own size."""
+    rows = np.repeat(np.arange(len(rowptr) - 1), np.diff(rowptr))
+    col = np.asarray(col, dtype=np.int64)
+    if not len(col):
+        return 0.0, 0.0, 0.0, 0.0
+    q, k, v, do = (np.asarray(x, dtype=np.float64) for x in (q, k, v, do))
+    dp = np.abs(np.einsum("ehc,ehc->eh", do[rows], v[col]))
+    nk, nq, ndo = (np.linalg.norm(x, axis=-1) for x in (k[col], q[rows], do[rows]))
+    rms = lambda t: float(np.sqrt(np.mean(t * t)))
+    return rms(scale * dp * nk), rms(scale * dp * nq), rms(ndo), rms(dp)
+
+
+def assert_close(x, r, dtype: str, name: str, rho: float | None = None):
+    """``rho``: for fp32, a floor for the tolerance's scale: used in place of the RMS of the reference's vector
+    norms ([n, H, d] tensors) or of 1 (per-entry values) when larger."""
     x = np.asarray(x, dtype=np.float64)
     r = np.asarray(r, dtype=np.float64)
     assert x.shape == r.shape, (name, x.shape, r.shape)
@@ -45,13 +66,13 @@ def assert_close(x, r, dtype: str, name: str):
     if dtype == "f32":
         if r.ndim == 3:  # [n, H, d]: normwise per (node, head)
             rn = np.linalg.norm(r, axis=-1)
-            rho = np.sqrt(np.mean(rn * rn)) if rn.size else 0.0
+            rho = max(np.sqrt(np.mean(rn * rn)) if rn.size else 0.0, rho or 0.0)
             err = np.linalg.norm(x - r, axis=-1)
             tol = 1e-5 * (rn + rho)
         else:
             x, r = x[fin], r[fin]
             err = np.abs(x - r)
-            tol = 1e-5 * np.maximum(1.0, np.abs(r))
+            tol = 1e-5 * np.maximum(max(1.0, rho or 0.0), np.abs(r))
     else:
         x, r = x[fin], r[fin]
         err = np.abs(x - r)
