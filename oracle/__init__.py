@@ -16,6 +16,8 @@ Modules:
   label-propagation reading used instead of METIS.
 * ``plan`` - relabelled CSR and the tile classification of §3.4 (cluster
   sparsity, transfer threshold), as plain integer array code.
+* ``ecr`` - the paper's lossy reformation of sparse clusters into sub-blocks
+  and the Auto Tuner that walks its transfer threshold (§3.4).
 """
 
-from . import attention, plan, reorder  # noqa: F401
+from . import attention, ecr, plan, reorder  # noqa: F401
