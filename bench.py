@@ -9,7 +9,8 @@ under "preprocess".  Also reported: the interleaved full-attention layer
 the host's cores ("cpu_baseline", timed before the GPU is used) and, with
 --tau-sweep, the same step at density thresholds 1%, 20% and the CSR-only
 control ("tau_sweep"); with --bias, the step with a per-edge additive bias
-("edge_bias").
+("edge_bias"); with --ecr, the paper's lossy cluster reformation and the step
+on the rewritten graph ("ecr").
 
 Default workload: 1,000,000-node stochastic block model, 1,000 log-normal
 blocks, average degree 30, 5% of edges across blocks, self-loops, random node
@@ -60,6 +61,9 @@ def parse():
     ap.add_argument("--bias", action="store_true",
                     help="also time the step with a per-edge additive bias (all-remainder plan) and the plain "
                          "step on the same plan")
+    ap.add_argument("--ecr", action="store_true",
+                    help="also time the paper's lossy cluster reformation (k = 8, d_b = 16) at 1x and 5x the graph "
+                         "density and the step on the rewritten graph")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB row copy (gt_gather_rows, identity order) 5 times: the reference "
                          "for scaling hardware byte counters")
@@ -289,6 +293,47 @@ def bias_step(gt, w, rp, cl, perm, iperm, Q, K, V, dO, scale, edge_heads):
             "note": "fwd + bwd with bias (bwd also writes dB); bias read by fwd, bwd rows, bwd cols"}
 
 
+def ecr_step(gt, rp, cl, Q, K, V, dO, scale, H, tau_ppm, T):
+    """The lossy reformation (k = 8 clusters per side, 16 x 16 sub-blocks) of the reordered graph at thresholds
+    beta_G and 5 beta_G, and the fwd + bwd step on the rewritten graph."""
+    import torch
+
+    n, nnz = rp.numel() - 1, cl.numel()
+    out = {}
+    for mult in (1, 5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        gt.ecr_compact(rp, cl, 8, 16, mult * nnz, n * n)  # warm-up
+        torch.cuda.synchronize()
+        a.record()
+        rp2, cl2, moved = gt.ecr_compact(rp, cl, 8, 16, mult * nnz, n * n)
+        b.record()
+        torch.cuda.synchronize()
+        compact_ms = a.elapsed_time(b)
+        plan = gt.build_tiles(rp2, cl2, T, tau_ppm)
+
+        def step():
+            O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
+            dQ, Dst = gt.sparse_attn_bwd_rows(plan, Q, K, V, dO, L, scale)
+            gt.sparse_attn_bwd_cols(plan, Q, K, V, dO, L, Dst, scale)
+
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(10):
+            step()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / 10
+        out[f"{mult}x_beta_G"] = {
+            "compact_ms": round(compact_ms, 3), "transferred_clusters": moved, "nnz_rewritten": int(cl2.numel()),
+            "dense_tiles": int(plan.n_dense), "ms_per_step": round(ms, 4),
+            "value": int(cl2.numel()) * H / (ms / 1e3),
+        }
+        del plan, rp2, cl2
+    return out
+
+
 def copy_probe():
     """A plain copy of known size: 2^21 rows x 512 bytes (1 GiB) read and written, plus the 8 MiB order array."""
     import torch
@@ -459,6 +504,9 @@ def main():
     if args.bias:
         log("step with a per-edge bias ...")
         result["edge_bias"] = bias_step(gt, w, rp, cl, perm, iperm, Q, K, V, dO, scale, edge_heads)
+    if args.ecr:
+        log("lossy reformation ...")
+        result["ecr"] = ecr_step(gt, rp2, cl2, Q, K, V, dO, scale, w.heads, tau_ppm, args.tile)
     if not args.no_dense_layer:
         log("timing the full-attention layer ...")
         result["dense_layer"] = dense_layer(5)

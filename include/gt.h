@@ -180,6 +180,57 @@ gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowptr, const in
                          uint32_t tau_ppm, gt_tiles* plan, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* The paper's lossy reformation, §3.4 (cluster sparsity, transfer strategy). */
+/* ------------------------------------------------------------------------ */
+/* An opt-in rewrite of the (clustered) graph into E'; the attention calls then
+ * run exactly on E'.  With c = ceil(n/k), cluster (I, J) holds the edges (i, j)
+ * with i/c = I, j/c = J; cnt counts them, area = rows(I)*rows(J) with
+ * rows(I) = min(c, n - I*c).  The cluster is transferred iff cnt >= 1 and
+ * cnt*den < num*area (density below num/den, exact).  In a transferred cluster
+ * the self-loops stay and its other `moved` edges are replaced by
+ * m = ceil(moved / d_b^2) full d_b x d_b sub-blocks: the cluster is cut into
+ * d_b x d_b blocks from its corner (clipped at its edge) and the m blocks that
+ * held the most moved edges are chosen, ties to the smaller (block row, block
+ * column).  Edges of other clusters are kept.  rowptr_out int64[n+1] and
+ * col_out int32[cap] receive E' (sorted, no duplicates); *nnz_out (host) its
+ * size.  cap must be at least gt_ecr_max_nnz(nnz, k, d_b); 1 <= k <= 64,
+ * 1 <= d_b <= 256.  *n_transferred (host, may be NULL) counts the transferred
+ * clusters.  SYNC: validates the CSR first and reads back counts. */
+int64_t gt_ecr_max_nnz(int64_t nnz, int32_t k, int32_t d_b);
+size_t gt_ecr_workspace_size(int64_t n, int64_t nnz, int32_t k, int32_t d_b);
+gt_status gt_ecr_compact(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t k, int32_t d_b,
+                         uint64_t num, uint64_t den, int64_t* rowptr_out, int32_t* col_out, int64_t cap,
+                         int64_t* nnz_out, int32_t* n_transferred, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Auto Tuner of the transfer threshold, §3.4 (hyperparameter modeling).  Host
+ * only (no device memory, no stream).  The caller owns the state.  Running
+ * loss F_t = 0.9 F_{t-1} + 0.1 L_t (F_0 = L_0); loss descent rate
+ * LDR_t = (F_t - F_{t-1}) / et_t (et_t the epoch's time); the threshold walks the
+ * ladder {0, bG, 1.5 bG, 5 bG, 7 bG, 10 bG, 1}, bG = nnz/n^2, each capped at 1,
+ * starting at bG.  At epoch t, once LDR_{t-delta} exists and delta epochs have
+ * passed since the last change, LDR_t >= LDR_{t-delta} moves one rung up and
+ * LDR_t < LDR_{t-delta} one rung down (clamped).  Each rung is the exact
+ * fraction num/den to pass to gt_ecr_compact. */
+#define GT_AUTOTUNER_RUNGS 7
+#define GT_AUTOTUNER_HISTORY 64
+typedef struct gt_autotuner {
+    double F;                             /* running loss */
+    double ldr[GT_AUTOTUNER_HISTORY];     /* LDR_t at t mod GT_AUTOTUNER_HISTORY */
+    int64_t t;                            /* index of the last epoch fed (-1 before the first) */
+    int64_t last_change;                  /* epoch of the last rung change (0 at the start) */
+    int32_t level;                        /* current rung, 0 .. GT_AUTOTUNER_RUNGS-1 */
+    int32_t delta;                        /* comparison distance, 1 .. GT_AUTOTUNER_HISTORY-1 */
+    uint64_t num[GT_AUTOTUNER_RUNGS];     /* ladder numerators */
+    uint64_t den[GT_AUTOTUNER_RUNGS];     /* ladder denominators */
+} gt_autotuner;
+/* n >= 1, 0 <= nnz < 2^32 (the graph bG refers to). */
+gt_status gt_autotuner_init(gt_autotuner* state, int64_t n, int64_t nnz, int32_t delta);
+/* Feed epoch t's loss (finite) and time (> 0); returns the rung for the next
+ * epoch in *level and its threshold *num / *den (each output may be NULL). */
+gt_status gt_autotuner_step(gt_autotuner* state, double loss, double epoch_seconds, int32_t* level, uint64_t* num,
+                            uint64_t* den);
+
+/* ------------------------------------------------------------------------ */
 /* Neighbourhood softmax attention, §3.2, over a plan (reordered index space).*/
 /* ------------------------------------------------------------------------ */
 /* For each node i and head h, over j in N(i) (the dense tiles plus the remainder):

@@ -50,8 +50,10 @@ def cluster_edge(n: int, k: int) -> int:
     return max(1, -(-int(n) // int(k)))
 
 
-def ecr_compact(rowptr, col, k: int, d_b: int, num: int, den: int):
-    """E' of the lossy reformation: (rowptr', col', info) with info the per-cluster counts and choices."""
+def ecr_compact(rowptr, col, k: int, d_b: int, num: int, den: int, progress=None):
+    """E' of the lossy reformation: (rowptr', col', info) with info the per-cluster counts and choices.
+    ``progress`` (optional) is called with a short text after each stage."""
+    say = progress or (lambda *_: None)
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
     n = len(rowptr) - 1
@@ -68,35 +70,43 @@ def ecr_compact(rowptr, col, k: int, d_b: int, num: int, den: int):
     transfer = np.array([cnt[x] >= 1 and int(cnt[x]) * int(den) < int(num) * int(area[x]) for x in range(k * k)],
                         dtype=bool)
 
+    say("clusters counted")
     self_loop = rows == col
     moved = transfer[cid] & ~self_loop
     keep = ~moved
     out_r = [rows[keep]]
     out_c = [col[keep]]
-    chosen = {}
-    m_of = {}
-    for x in np.flatnonzero(transfer):
-        sel = moved & (cid == x)
-        cm = int(sel.sum())
-        m = -(-cm // (d_b * d_b))
-        m_of[int(x)] = m
-        if m == 0:
-            chosen[int(x)] = []
-            continue
-        Ix, Jx = divmod(int(x), k)
-        a = (rows[sel] - Ix * c) // d_b
-        b = (col[sel] - Jx * c) // d_b
-        blocks, counts = np.unique(np.stack([a, b], axis=1), axis=0, return_counts=True)
-        order = np.lexsort((blocks[:, 1], blocks[:, 0], -counts))
-        pick = [tuple(int(v) for v in blocks[o]) for o in order[:m]]
-        chosen[int(x)] = pick
-        r_hi, c_hi = Ix * c + size[Ix], Jx * c + size[Jx]
-        for (aa, bb) in pick:
-            r0, c0 = Ix * c + aa * d_b, Jx * c + bb * d_b
-            rr = np.arange(r0, min(r0 + d_b, r_hi), dtype=np.int64)
-            cc = np.arange(c0, min(c0 + d_b, c_hi), dtype=np.int64)
-            out_r.append(np.repeat(rr, len(cc)))
-            out_c.append(np.tile(cc, len(rr)))
+    # moved edges per transferred cluster and its sub-block count m
+    mcnt = np.bincount(cid[moved], minlength=k * k)
+    m_of = {int(x): -(-int(mcnt[x]) // (d_b * d_b)) for x in np.flatnonzero(transfer)}
+    # edges per block (cluster, block row a, block column b) of the moved edges
+    nb = -(-c // d_b)
+    mc = cid[moved]
+    a = (rows[moved] - I[moved] * c) // d_b
+    b = (col[moved] - J[moved] * c) // d_b
+    bkey, counts = np.unique((mc * nb + a) * nb + b, return_counts=True)
+    say(f"{len(bkey)} blocks counted")
+    bc, ba, bb = bkey // (nb * nb), (bkey // nb) % nb, bkey % nb
+    # inside each cluster: most edges first, ties to the smaller (a, b); the first m are chosen
+    order = np.lexsort((bb, ba, -counts, bc))
+    bc, ba, bb = bc[order], ba[order], bb[order]
+    first = np.searchsorted(bc, bc, side="left")
+    rank = np.arange(len(bc)) - first
+    m_arr = np.zeros(k * k, dtype=np.int64)
+    for x, m in m_of.items():
+        m_arr[x] = m
+    pick = rank < m_arr[bc]
+    say(f"{int(pick.sum())} sub-blocks chosen")
+    chosen = {x: [] for x in m_of}
+    for x, aa, bbb in zip(bc[pick].tolist(), ba[pick].tolist(), bb[pick].tolist()):
+        chosen[x].append((aa, bbb))
+        Ix, Jx = divmod(x, k)
+        r0, c0 = Ix * c + aa * d_b, Jx * c + bbb * d_b
+        rr = np.arange(r0, min(r0 + d_b, Ix * c + size[Ix]), dtype=np.int64)
+        cc = np.arange(c0, min(c0 + d_b, Jx * c + size[Jx]), dtype=np.int64)
+        out_r.append(np.repeat(rr, len(cc)))
+        out_c.append(np.tile(cc, len(rr)))
+    say("cells emitted")
     R = np.concatenate(out_r)
     C = np.concatenate(out_c)
     key = np.unique(R * max(n, 1) + C)

@@ -44,6 +44,18 @@ class GtTiles(ctypes.Structure):
     ]
 
 
+GT_AUTOTUNER_RUNGS = 7
+GT_AUTOTUNER_HISTORY = 64
+_f64 = ctypes.c_double
+
+
+class GtAutotuner(ctypes.Structure):
+    _fields_ = [
+        ("F", _f64), ("ldr", _f64 * GT_AUTOTUNER_HISTORY), ("t", _i64), ("last_change", _i64), ("level", _i32),
+        ("delta", _i32), ("num", _u64 * GT_AUTOTUNER_RUNGS), ("den", _u64 * GT_AUTOTUNER_RUNGS),
+    ]
+
+
 _P = ctypes.POINTER
 SIGNATURES = {
     "gt_abi_version": (_i32, []),
@@ -79,6 +91,12 @@ SIGNATURES = {
                                        _sz, _vp]),
     "gt_sparse_attn_bwd_bias": (_i32, [_P(GtTiles), _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32,
                                        _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gt_ecr_max_nnz": (_i64, [_i64, _i32, _i32]),
+    "gt_ecr_workspace_size": (_sz, [_i64, _i64, _i32, _i32]),
+    "gt_ecr_compact": (_i32, [_i64, _i64, _vp, _vp, _i32, _i32, _u64, _u64, _vp, _vp, _i64, _P(_i64), _P(_i32), _vp,
+                              _sz, _vp]),
+    "gt_autotuner_init": (_i32, [_P(GtAutotuner), _i64, _i64, _i32]),
+    "gt_autotuner_step": (_i32, [_P(GtAutotuner), _f64, _f64, _P(_i32), _P(_u64), _P(_u64)]),
     "gt_dense_attn_fwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp]),
     "gt_dense_attn_bwd_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
     "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
@@ -221,6 +239,41 @@ def scatter_rows(x: torch.Tensor, perm: torch.Tensor) -> torch.Tensor:
     _check(lib.gt_scatter_rows(x.shape[0], _row_bytes(x), _ptr(x), _ptr(perm), _ptr(out), _stream(x.device)),
            "gt_scatter_rows")
     return out
+
+
+def ecr_compact(rowptr: torch.Tensor, col: torch.Tensor, k: int, d_b: int, num: int, den: int):
+    """(rowptr', col', n_transferred): the graph after the lossy cluster reformation at threshold num/den."""
+    lib = load_library()
+    _check_csr(rowptr, col)
+    n, nnz = rowptr.numel() - 1, col.numel()
+    dev = rowptr.device
+    cap = lib.gt_ecr_max_nnz(nnz, k, d_b)
+    _need(cap >= 0, "k must be in [1, 64] and d_b in [1, 256]")
+    rp = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    cl = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    ws = _workspace(lib.gt_ecr_workspace_size(n, nnz, k, d_b), dev)
+    out = ctypes.c_int64(0)
+    moved = ctypes.c_int32(0)
+    _check(lib.gt_ecr_compact(n, nnz, _ptr(rowptr), _ptr(col), k, d_b, ctypes.c_uint64(num), ctypes.c_uint64(den),
+                              _ptr(rp), _ptr(cl), cap, ctypes.byref(out), ctypes.byref(moved), _ptr(ws), ws.numel(),
+                              _stream(dev)), "gt_ecr_compact")
+    return rp, cl[:out.value].clone(), moved.value
+
+
+class AutoTuner:
+    """The transfer-threshold controller of the lossy reformation (state held in the C struct)."""
+
+    def __init__(self, n: int, nnz: int, delta: int = 10):
+        self.lib = load_library()
+        self.c = GtAutotuner()
+        _check(self.lib.gt_autotuner_init(ctypes.byref(self.c), n, nnz, delta), "gt_autotuner_init")
+
+    def step(self, loss: float, epoch_seconds: float):
+        """Returns (level, num, den) for the next epoch."""
+        lv, num, den = ctypes.c_int32(0), ctypes.c_uint64(0), ctypes.c_uint64(0)
+        _check(self.lib.gt_autotuner_step(ctypes.byref(self.c), float(loss), float(epoch_seconds), ctypes.byref(lv),
+                                          ctypes.byref(num), ctypes.byref(den)), "gt_autotuner_step")
+        return lv.value, num.value, den.value
 
 
 @dataclass
