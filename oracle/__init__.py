@@ -18,6 +18,8 @@ Modules:
   sparsity, transfer threshold), as plain integer array code.
 * ``ecr`` - the paper's lossy reformation of sparse clusters into sub-blocks
   and the Auto Tuner that walks its transfer threshold (§3.4).
+* ``interleave`` - the checks of conditions C1-C3 that decide when a dense
+  layer is interleaved (§3.2).
 """
 
-from . import attention, ecr, plan, reorder  # noqa: F401
+from . import attention, ecr, interleave, plan, reorder  # noqa: F401
