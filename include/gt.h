@@ -231,6 +231,41 @@ gt_status gt_autotuner_step(gt_autotuner* state, double loss, double epoch_secon
                             uint64_t* den);
 
 /* ------------------------------------------------------------------------ */
+/* Interleave decision, §3.2 (conditions C1-C3 for the sparse pattern alone). */
+/* ------------------------------------------------------------------------ */
+/* The CSR is read as an undirected graph (symmetric); reach follows out-edges.
+ *   C1: every row holds its self-loop (exact): missing_self_loops == 0.
+ *   C2: a Hamiltonian path, confirmed by Dirac's condition on min_degree (the
+ *       minimum degree without self-loops): 2*min_degree >= n for n >= 3; n <= 1
+ *       holds; n = 2 holds iff min_degree >= 1; otherwise 0 (not confirmed).
+ *   C3: every node within L hops of every node.  Breadth-first search from
+ *       node 0 cut at depth L+1 gives ecc_root and reached (nodes within the
+ *       cut).  ecc_root > L or reached < n: 0.  2*ecc_root <= L: 1.  Otherwise a
+ *       second search from the smallest-id node at depth ecc_root gives ecc_far:
+ *       ecc_far > L or a node beyond the cut: 0, else -1 (undetermined).
+ * c1, c2, c3 are 1 (holds), 0 (does not) or -1 (undetermined); use_sparse is 1
+ * iff all three are 1, else a fully connected layer should be interleaved.
+ * ecc_far is -1 when the second search is not run.  levels (int32[n], may be
+ * NULL) receives the first search's depths (-1 beyond the cut).  0 <= L < 2^30.
+ * SYNC: validates the CSR first and reads back a count per depth. */
+typedef struct gt_interleave_report {
+    int64_t n;
+    int64_t missing_self_loops;
+    int64_t min_degree;
+    int64_t reached;
+    int32_t ecc_root;
+    int32_t ecc_far;
+    int32_t c1;
+    int32_t c2;
+    int32_t c3;
+    int32_t use_sparse;
+} gt_interleave_report;
+size_t gt_interleave_workspace_size(int64_t n);
+gt_status gt_interleave_check(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t L,
+                              gt_interleave_report* report, int32_t* levels, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Neighbourhood softmax attention, §3.2, over a plan (reordered index space).*/
 /* ------------------------------------------------------------------------ */
 /* For each node i and head h, over j in N(i) (the dense tiles plus the remainder):

@@ -56,6 +56,13 @@ class GtAutotuner(ctypes.Structure):
     ]
 
 
+class GtInterleaveReport(ctypes.Structure):
+    _fields_ = [
+        ("n", _i64), ("missing_self_loops", _i64), ("min_degree", _i64), ("reached", _i64), ("ecc_root", _i32),
+        ("ecc_far", _i32), ("c1", _i32), ("c2", _i32), ("c3", _i32), ("use_sparse", _i32),
+    ]
+
+
 _P = ctypes.POINTER
 SIGNATURES = {
     "gt_abi_version": (_i32, []),
@@ -97,6 +104,8 @@ SIGNATURES = {
                               _sz, _vp]),
     "gt_autotuner_init": (_i32, [_P(GtAutotuner), _i64, _i64, _i32]),
     "gt_autotuner_step": (_i32, [_P(GtAutotuner), _f64, _f64, _P(_i32), _P(_u64), _P(_u64)]),
+    "gt_interleave_workspace_size": (_sz, [_i64]),
+    "gt_interleave_check": (_i32, [_i64, _i64, _vp, _vp, _i32, _P(GtInterleaveReport), _vp, _vp, _sz, _vp]),
     "gt_dense_attn_fwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp]),
     "gt_dense_attn_bwd_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
     "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
@@ -258,6 +267,21 @@ def ecr_compact(rowptr: torch.Tensor, col: torch.Tensor, k: int, d_b: int, num: 
                               _ptr(rp), _ptr(cl), cap, ctypes.byref(out), ctypes.byref(moved), _ptr(ws), ws.numel(),
                               _stream(dev)), "gt_ecr_compact")
     return rp, cl[:out.value].clone(), moved.value
+
+
+def interleave_check(rowptr: torch.Tensor, col: torch.Tensor, L: int, want_levels: bool = False):
+    """The C1-C3 report of the interleave decision as a dict (and the first search's depths if asked)."""
+    lib = load_library()
+    _check_csr(rowptr, col)
+    n, nnz = rowptr.numel() - 1, col.numel()
+    dev = rowptr.device
+    ws = _workspace(lib.gt_interleave_workspace_size(n), dev)
+    rep = GtInterleaveReport()
+    lev = torch.empty(n, dtype=torch.int32, device=dev) if want_levels else None
+    _check(lib.gt_interleave_check(n, nnz, _ptr(rowptr), _ptr(col), int(L), ctypes.byref(rep), _ptr(lev), _ptr(ws),
+                                   ws.numel(), _stream(dev)), "gt_interleave_check")
+    out = {name: getattr(rep, name) for name, _ in GtInterleaveReport._fields_}
+    return (out, lev) if want_levels else out
 
 
 class AutoTuner:
