@@ -347,20 +347,19 @@ template <typename T, int D, int H, bool kBias = false>
 __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeCfg<T, D, H>::F>& dv,
                                          const Slice<T, EdgeCfg<T, D, H>::F>& k,
                                          const Slice<T, EdgeCfg<T, D, H>::F>& v, const T* __restrict__ Q,
-                                         const T* __restrict__ dO, const float* __restrict__ LSE,
-                                         const float* __restrict__ Dv, int64_t i0, int64_t i1, bool ok0, bool ok1,
-                                         const Lanes<T, D, H>& ln, float sl2, const EdgeBias& eb = EdgeBias{},
-                                         int64_t c0 = 0, int64_t c1 = 0) {
+                                         const T* __restrict__ dO, const float2* __restrict__ stat, int64_t i0,
+                                         int64_t i1, bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2,
+                                         const EdgeBias& eb = EdgeBias{}, int64_t c0 = 0, int64_t c1 = 0) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> q0, q1, g0, g1;
     q0.load(Q + ln.off(i0));
     q1.load(Q + ln.off(i1));
     g0.load(dO + ln.off(i0));
     g1.load(dO + ln.off(i1));
-    const float l0 = LSE[i0 * H + ln.h] * kLog2e;
-    const float l1 = LSE[i1 * H + ln.h] * kLog2e;
-    const float D0 = Dv[i0 * H + ln.h];
-    const float D1 = Dv[i1 * H + ln.h];
+    const float2 st0 = stat[i0 * H + ln.h];
+    const float2 st1 = stat[i1 * H + ln.h];
+    const float l0 = st0.x, D0 = st0.y;
+    const float l1 = st1.x, D1 = st1.y;
     float s0 = group_sum<C::L>(q0.dot(k)) * sl2;
     float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
     int64_t e0 = 0, e1 = 0;
@@ -394,10 +393,10 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
                                                        const int32_t* __restrict__ rw, int64_t len,
                                                        const T* __restrict__ Q,
                                                        const T* __restrict__ K, const T* __restrict__ V,
-                                                       const T* __restrict__ dO, const float* __restrict__ LSE,
-                                                       const float* __restrict__ Dv, float sl2, float scale,
-                                                       T* __restrict__ dK, T* __restrict__ dV, TilePartials tpk,
-                                                       TilePartials tpv, EdgeBias eb) {
+                                                       const T* __restrict__ dO, const float2* __restrict__ stat,
+                                                       float sl2, float scale, T* __restrict__ dK,
+                                                       T* __restrict__ dV, TilePartials tpk, TilePartials tpv,
+                                                       EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     const Lanes<T, D, H> ln(lane_id());
     const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
@@ -422,7 +421,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
         load_f32_slice<C::F>(dv.v, tpv.acc + off);
     }
     walk_edges(rw, len, a, deg, dmax, int32_t(self), [&](int64_t i0, int64_t i1, int t, bool ok0, bool ok1) {
-        dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, ok0, ok1, ln, sl2, eb, a + t, a + t + 1);
+        dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, stat, i0, i1, ok0, ok1, ln, sl2, eb, a + t, a + t + 1);
     });
     if (live && deg >= 0) {
         store_slice<T, C::F>(dK + off, dk.v, scale);
@@ -690,8 +689,8 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __res
                                                             const int64_t* __restrict__ cp,
                                                             const int32_t* __restrict__ rw, const T* __restrict__ Q,
                                                             const T* __restrict__ K, const T* __restrict__ V,
-                                                            const T* __restrict__ dO, const float* __restrict__ LSE,
-                                                            const float* __restrict__ Dv, float sl2,
+                                                            const T* __restrict__ dO,
+                                                            const float2* __restrict__ stat, float sl2,
                                                             float* __restrict__ part, EdgeBias eb) {
     using C = EdgeCfg<T, D, H>;
     constexpr int S = kThreads / C::G;
@@ -714,7 +713,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols_long(const int32_t* __res
         const bool ok1 = t + S < e1;
         const int64_t i0 = rw[a + t];
         const int64_t i1 = ok1 ? rw[a + t + S] : i0;
-        dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, LSE, Dv, i0, i1, true, ok1, ln, sl2, eb, a + t, a + t + S);
+        dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, stat, i0, i1, true, ok1, ln, sl2, eb, a + t, a + t + S);
     }
 #pragma unroll
     for (int f = 0; f < C::F; ++f) {
@@ -760,6 +759,14 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols_long_merge(const int32_t*
             reinterpret_cast<float*>(dV)[j * H * D + idx] = av;
         }
     }
+}
+
+// The column pass reads each in-edge's row statistics as one (LSE log2 e, D)
+// pair: one 8-byte gather per edge instead of two 4-byte ones.
+__global__ void k_pack_stats(int64_t m, const float* __restrict__ LSE, const float* __restrict__ Dv,
+                             float2* __restrict__ out) {
+    for (int64_t x = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; x < m; x += int64_t(gridDim.x) * blockDim.x)
+        out[x] = make_float2(LSE[x] * kLog2e, Dv[x]);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -864,6 +871,7 @@ gt_status run_bwd_cols_t(const gt_tiles* p, const void* Q, const void* K, const 
     ws.take<char>(256);
     TileBwdPartials tb = tile_partials_bwd(ws, p, H, D, false, true);
     LongPlan lp = long_plan_take(ws, p->n_long_cols, p->nnz_sparse, ColLongF<H, D>);
+    float2* stat = ws.take<float2>(size_t(n) * H);
     const float sl2 = scale * kLog2e;
     const T *q = static_cast<const T*>(Q), *k = static_cast<const T*>(K), *v = static_cast<const T*>(V);
     const T* g = static_cast<const T*>(dO);
@@ -871,16 +879,18 @@ gt_status run_bwd_cols_t(const gt_tiles* p, const void* Q, const void* K, const 
     if (p->n_dense > 0) {
         if ((st = tile_bwd_dkdv<T, D, H>(p, q, k, v, g, LSE, Dv, sl2, tb.dk, tb.dv, s)) != GT_OK) return st;
     }
+    k_pack_stats<<<grid_for(n * H, 256, 8192), 256, 0, s>>>(n * H, LSE, Dv, stat);
+    GT_LAUNCH_CHECK("sparse_bwd_pack_stats");
     const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
     k_bwd_cols<T, D, H, kBias><<<grid, kThreads, 0, s>>>(n, p->sp_colptr, p->sp_row, p->nnz_sparse, q, k, v, g,
-                                                         LSE, Dv, sl2, scale, static_cast<T*>(dK),
+                                                         stat, sl2, scale, static_cast<T*>(dK),
                                                          static_cast<T*>(dV), tb.dk, tb.dv, eb);
     GT_LAUNCH_CHECK("sparse_bwd_cols");
     if (p->n_long_cols > 0) {
         if ((st = long_chunks(p->long_cols, p->n_long_cols, p->sp_colptr, lp, s)) != GT_OK) return st;
         k_bwd_cols_long<T, D, H, kBias><<<unsigned(lp.max_chunks), kThreads, 0, s>>>(
-            p->long_cols, p->n_long_cols, lp.chunk_off, p->sp_colptr, p->sp_row, q, k, v, g, LSE, Dv, sl2,
-            lp.part, eb);
+            p->long_cols, p->n_long_cols, lp.chunk_off, p->sp_colptr, p->sp_row, q, k, v, g, stat, sl2, lp.part,
+            eb);
         GT_LAUNCH_CHECK("sparse_bwd_cols_long");
         k_bwd_cols_long_merge<T, D, H><<<unsigned(p->n_long_cols), kThreads, 0, s>>>(
             p->long_cols, lp.chunk_off, lp.part, tb.dk, tb.dv, scale, static_cast<T*>(dK), static_cast<T*>(dV));
@@ -938,7 +948,10 @@ size_t bwd_part_ws(const gt_tiles* p, int32_t H, int32_t d, bool rows, bool cols
     ws.take<char>(256);
     tile_partials_bwd(ws, p, H, d, rows, cols);
     if (rows) long_plan_take(ws, p->n_long_rows, p->nnz_sparse, 2 * int64_t(H) * d + H);
-    if (cols) long_plan_take(ws, p->n_long_cols, p->nnz_sparse, 2 * int64_t(H) * d);
+    if (cols) {
+        long_plan_take(ws, p->n_long_cols, p->nnz_sparse, 2 * int64_t(H) * d);
+        ws.take<float2>(size_t(p->n > 0 ? p->n : 1) * H);
+    }
     return ws.size();
 }
 size_t bwd_ws(const gt_tiles* p, int32_t H, int32_t d) {
