@@ -449,6 +449,19 @@ def main():
     avg = {k: float(np.mean(v)) for k, v in stages.items()}
     med = {k: float(np.median(v)) for k, v in stages.items()}
 
+    # the gather ceiling of this plan: the forward's partner-row reads with no arithmetic
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    for _ in range(3):
+        gt.gather_probe(plan, K, V, sink)
+    pa, pb = ev(), ev()
+    torch.cuda.synchronize()
+    pa.record()
+    for _ in range(20):
+        gt.gather_probe(plan, K, V, sink)
+    pb.record()
+    torch.cuda.synchronize()
+    probe_ms = pa.elapsed_time(pb) / 20
+
     nnz, H, d = g.nnz, w.heads, w.dim
     b = 2 if w.dtype == "bf16" else 4
     edge_heads = nnz * H
@@ -494,6 +507,13 @@ def main():
         "stages_ms": {k: round(v, 4) for k, v in avg.items()},
         "stages_median_ms": {k: round(v, 4) for k, v in med.items()},
         "stages_alg_GBps": stage_gbs,
+        "gather_probe": {
+            "ms": round(probe_ms, 4),
+            "row_gather_TBps": round(plan.nnz_sparse * 2 * H * d * b / (probe_ms / 1e3) / 1e12, 2),
+            "probe_over_stage": {k: round(probe_ms / v, 3) for k, v in avg.items()},
+            "note": "gt_gather_probe: the forward's two partner-row reads per remainder edge with no arithmetic; "
+                    "probe_over_stage = probe time / stage time",
+        },
         "step_alg_GBps": round(sum(alg.values()) / (ms_per_step / 1e3) / 1e9, 1),
         "preprocess": pre,
         "wall_s_timed": round(t_wall, 3),

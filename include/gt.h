@@ -326,6 +326,15 @@ gt_status gt_sparse_attn_bwd_bias(const gt_tiles* plan, const int32_t* csc_pos, 
                                   const float* LSE, float scale, void* dQ, void* dK, void* dV, float* dbias,
                                   void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Measurement only (not part of the method): the remainder forward's data
+ * movement with no arithmetic.  Every remainder edge (i, j) of a row with at
+ * most GT_LONG_ROW edges reads row j of A and of B ([n, H, d], dtype) with the
+ * lanes and edge walk of gt_sparse_attn_fwd; the values are only XORed.  Used
+ * to time the rate the gather path allows for a plan.  sink: device uint32[1],
+ * written only if the XOR of a lane's words hits a fixed constant (ignore it). */
+gt_status gt_gather_probe(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* A, const void* B,
+                          uint32_t* sink, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Full softmax attention, §2.1 Eq. (1) (the interleaved dense layer of §3.2).*/
 /* ------------------------------------------------------------------------ */

@@ -769,6 +769,70 @@ __global__ void k_pack_stats(int64_t m, const float* __restrict__ LSE, const flo
         out[x] = make_float2(LSE[x] * kLog2e, Dv[x]);
 }
 
+// ------------------------------------------------------------ gather probe
+// Measurement only: the forward edge kernel's data movement (every remainder
+// edge of a row of at most GT_LONG_ROW edges reads its partner's two feature
+// rows, same lanes, same edge walk) with no arithmetic but an XOR, so the rate
+// the gather path allows for a plan can be timed beside the real kernels.
+template <int F>
+__device__ __forceinline__ uint32_t xor_words(const Slice<uint16_t, F>& x) {
+    uint32_t r = 0;
+#pragma unroll
+    for (int i = 0; i < F / 2; ++i) r ^= x.w[i];
+    return r;
+}
+template <int F>
+__device__ __forceinline__ uint32_t xor_words(const Slice<float, F>& x) {
+    uint32_t r = 0;
+#pragma unroll
+    for (int i = 0; i < F; ++i) r ^= __float_as_uint(x.w[i]);
+    return r;
+}
+
+constexpr uint32_t kProbeSinkKey = 0x9E3779B9u;
+
+template <typename T, int D, int H>
+__global__ __launch_bounds__(kThreads) void k_gather_probe(int64_t n, const int64_t* __restrict__ rp,
+                                                           const int32_t* __restrict__ cl, int64_t len,
+                                                           const T* __restrict__ A, const T* __restrict__ B,
+                                                           uint32_t* __restrict__ sink) {
+    using C = EdgeCfg<T, D, H>;
+    const Lanes<T, D, H> ln(lane_id());
+    const int64_t wave = xcd_block(blockIdx.x, gridDim.x) * (kThreads / kWave) + threadIdx.x / kWave;
+    const int64_t i = wave * C::NPW + ln.slot;
+    const bool live = i < n;
+    const int64_t self = live ? i : 0;
+    int64_t a = 0;
+    int deg = 0;
+    if (live) {
+        a = rp[i];
+        const int64_t dg = rp[i + 1] - a;
+        deg = dg > GT_LONG_ROW ? -1 : int(dg);
+    }
+    const int dmax = wave_max(deg);
+    uint32_t acc = 0;
+    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int, bool, bool) {
+        Slice<T, C::F> a0, a1, b0, b1;
+        a0.load(A + ln.off(j0));
+        a1.load(A + ln.off(j1));
+        b0.load(B + ln.off(j0));
+        b1.load(B + ln.off(j1));
+        acc ^= xor_words(a0) ^ xor_words(a1) ^ xor_words(b0) ^ xor_words(b1);
+    });
+    if (acc == kProbeSinkKey) sink[0] = acc;  // keeps the loads; practically never taken
+}
+
+template <typename T, int D, int H>
+gt_status run_probe(const gt_tiles* p, const void* A, const void* B, uint32_t* sink, hipStream_t s) {
+    using C = EdgeCfg<T, D, H>;
+    if (p->n == 0) return GT_OK;
+    const unsigned grid = xcd_grid(cdiv(cdiv(p->n, C::NPW), kThreads / kWave));
+    k_gather_probe<T, D, H><<<grid, kThreads, 0, s>>>(p->n, p->sp_rowptr, p->sp_col, p->nnz_sparse,
+                                                      static_cast<const T*>(A), static_cast<const T*>(B), sink);
+    GT_LAUNCH_CHECK("gather_probe");
+    return GT_OK;
+}
+
 // ---------------------------------------------------------------- launchers
 
 struct FwdWs {
@@ -1097,4 +1161,13 @@ extern "C" gt_status gt_sparse_attn_bwd_bias(const gt_tiles* plan, const int32_t
         eb.db = dbias;
     }
     return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, dO, LSE, scale, dQ, dK, dV, ws, eb, stream);
+}
+
+extern "C" gt_status gt_gather_probe(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* A,
+                                     const void* B, uint32_t* sink, hipStream_t stream) {
+    gt_status st = check_plan("gt_gather_probe", plan);
+    if (st != GT_OK) return st;
+    if (!supported(H, d, dtype)) return fail(GT_ERR_UNSUPPORTED, "gt_gather_probe: unsupported (H, d, dtype)");
+    if (plan->n > 0 && (!A || !B || !sink)) return fail(GT_ERR_INVALID_ARG, "gt_gather_probe: null pointer");
+    return GT_DISPATCH_ATTN(dtype, d, H, run_probe, plan, A, B, sink, stream);
 }

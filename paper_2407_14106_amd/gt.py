@@ -98,6 +98,7 @@ SIGNATURES = {
                                        _sz, _vp]),
     "gt_sparse_attn_bwd_bias": (_i32, [_P(GtTiles), _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32,
                                        _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gt_gather_probe": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "gt_ecr_max_nnz": (_i64, [_i64, _i32, _i32]),
     "gt_ecr_workspace_size": (_sz, [_i64, _i64, _i32, _i32]),
     "gt_ecr_compact": (_i32, [_i64, _i64, _vp, _vp, _i32, _i32, _u64, _u64, _vp, _vp, _i64, _P(_i64), _P(_i32), _vp,
@@ -451,6 +452,17 @@ def sparse_attn_bwd_cols(plan: Plan, Q, K, V, dO, LSE, Dstat, scale: float | Non
                                        _ptr(Dstat), scale, _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(),
                                        _stream(Q.device)), "gt_sparse_attn_bwd_cols")
     return dK, dV
+
+
+def gather_probe(plan: Plan, A: torch.Tensor, B: torch.Tensor, sink: torch.Tensor | None = None) -> torch.Tensor:
+    """Measurement only: the forward's partner-row gathers of A and B over the plan, no arithmetic."""
+    lib = load_library()
+    _check_feats(plan.n, A, B)
+    n, H, d = A.shape
+    sink = torch.zeros(1, dtype=torch.int32, device=A.device) if sink is None else sink
+    _check(lib.gt_gather_probe(ctypes.byref(plan.c), H, d, _dtype_code(A), _ptr(A), _ptr(B), _ptr(sink),
+                               _stream(A.device)), "gt_gather_probe")
+    return sink
 
 
 def edge_map(plan: Plan) -> torch.Tensor:

@@ -209,3 +209,17 @@ def test_batched_small_graphs_with_global_token(gt):
     g = w.graph
     run_case(gt, g.rowptr, g.col, 8, 32, "bf16", taus=SWEEP, seed=21)
     run_case(gt, g.rowptr, g.col, 2, 64, "f32", taus=(10_000, CSR_ONLY), seed=22)
+
+
+def test_gather_probe_runs_on_every_shape(gt):
+    # measurement-only entry point: must run (in bounds) for every supported shape and leave the features alone
+    g = make_workload("c1", 0.1).graph
+    rp, cl = dev_csr(g.rowptr, g.col)
+    plan = gt.build_tiles(rp, cl, 128, CSR_ONLY)
+    for dtype in ("f32", "bf16"):
+        for H, d in ((1, 32), (8, 32), (16, 64)):
+            a, b = (dev_feat(x, dtype) for x in feats(g.n, H, d, dtype, 7)[:2])
+            a0, b0 = a.clone(), b.clone()
+            gt.gather_probe(plan, a, b)
+            torch.cuda.synchronize()
+            assert torch.equal(a, a0) and torch.equal(b, b0)
