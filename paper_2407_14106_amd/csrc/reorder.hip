@@ -5,7 +5,10 @@
 //   deg <= 64          one wavefront per row, one neighbour label per lane;
 //                      multiplicities by an in-register all-pairs compare.
 //   64 < deg <= 4096   one workgroup per row, open-addressing count table in LDS.
-//   deg > 4096         one workgroup per row, count table in the workspace.
+//   deg > 4096         the whole grid per row (a hub, a global token attending
+//                      to every node): count table in the workspace filled by
+//                      every workgroup, then reduced by every workgroup in
+//                      three passes (best count, smallest hash, smallest label).
 // All three compute the same function of the neighbour-label multiset.
 #include <limits.h>
 
@@ -22,6 +25,7 @@ constexpr int kLdsTable = 8192;      // entries (int32 key + uint32 count): 64 K
 constexpr int kLdsRowMax = kLdsTable / 2;
 constexpr int kBlock = 256;
 constexpr int kMaxSweeps = 1000;
+constexpr int kBigGrid = 1024;  // workgroups sharing each very long row
 
 __device__ __forceinline__ bool is_active(int64_t v, uint64_t key) {
     return (mix64(uint64_t(v) ^ key ^ kActivitySalt) >> 61) != 0;
@@ -153,21 +157,14 @@ __device__ __forceinline__ uint64_t block_min_u64(uint64_t v, uint64_t* s) {
     return r;
 }
 
-template <bool kGlobal>
-__device__ __forceinline__ int tab_load(const int* p) {
-    if (kGlobal) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return *p;
-}
 
-// One workgroup per listed row.  Table: keys (label or -1) and counts.
-template <bool kGlobal>
+// One workgroup per listed row.  LDS table: keys (label or -1) and counts.
 __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const int64_t* list_len,
                                                      const int64_t* rowptr, const int32_t* col,
                                                      const int32_t* lab_in, int32_t* lab_out, uint64_t key,
-                                                     const uint32_t* flag_prev, uint32_t* flag_next,
-                                                     int* gkeys, int* gcnts, const int64_t* big_off) {
-    __shared__ int s_keys[kGlobal ? 1 : kLdsTable];
-    __shared__ int s_cnts[kGlobal ? 1 : kLdsTable];
+                                                     const uint32_t* flag_prev, uint32_t* flag_next) {
+    __shared__ int s_keys[kLdsTable];
+    __shared__ int s_cnts[kLdsTable];
     __shared__ int s_red[kBlock / kWave];
     __shared__ uint64_t s_red64[kBlock / kWave];
     const bool converged = *flag_prev == 0;
@@ -183,13 +180,12 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
         const int64_t deg = b - a;
         int64_t cap = 1;
         while (cap < 2 * deg) cap <<= 1;
-        int* tk = kGlobal ? gkeys + big_off[idx] : s_keys;
-        int* tc = kGlobal ? gcnts + big_off[idx] : s_cnts;
+        int* tk = s_keys;
+        int* tc = s_cnts;
         for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
             tk[s] = -1;
             tc[s] = 0;
         }
-        if (kGlobal) __threadfence();
         __syncthreads();
         for (int64_t e = a + threadIdx.x; e < b; e += kBlock) {
             const int c = col[e];
@@ -205,13 +201,12 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
                 slot = (slot + 1) & (cap - 1);
             }
         }
-        if (kGlobal) __threadfence();
         __syncthreads();
         int best = 0, own_cnt = 0;
         for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
-            const int k = tab_load<kGlobal>(&tk[s]);
+            const int k = tk[s];
             if (k < 0) continue;
-            const int c = tab_load<kGlobal>(&tc[s]);
+            const int c = tc[s];
             best = c > best ? c : best;
             if (k == own) own_cnt = c;
         }
@@ -221,16 +216,16 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
         if (best > 0 && own_cnt != best) {
             uint64_t hbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
-                const int k = tab_load<kGlobal>(&tk[s]);
-                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
+                const int k = tk[s];
+                if (k < 0 || tc[s] != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 hbest = h < hbest ? h : hbest;
             }
             hbest = block_min_u64(hbest, s_red64);
             uint64_t lbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
-                const int k = tab_load<kGlobal>(&tk[s]);
-                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
+                const int k = tk[s];
+                if (k < 0 || tc[s] != best) continue;
                 if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
                 lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
             }
@@ -241,6 +236,184 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
             if (cand != own) *flag_next = 1u;
         }
         __syncthreads();
+    }
+}
+
+// -------------------------------------------------------------- very long rows
+// Every workgroup takes a strided slice of each listed row (edges, then table
+// slots), so a row of a million edges is spread over the chip.  Per-row
+// results: best count, own label's count, smallest hash among the best, and the
+// smallest label with that hash, combined with atomics (max / min: the result
+// does not depend on the order).
+
+struct BigRows {
+    const int32_t* list;
+    const int64_t* len;
+    const int64_t* off;   // table offset of each listed row
+    int* keys;
+    int* cnts;
+    int* best;            // [listed rows]
+    int* own_cnt;
+    unsigned long long* hbest;
+    unsigned long long* lbest;
+};
+
+__device__ __forceinline__ int64_t table_cap(int64_t deg) {
+    int64_t cap = 1;
+    while (cap < 2 * deg) cap <<= 1;
+    return cap;
+}
+
+__global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t* rowptr, const uint32_t* flag_prev) {
+    if (*flag_prev == 0) return;
+    const int64_t len = *br.len;
+    const int64_t stride = int64_t(gridDim.x) * kBlock, start = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    for (int64_t idx = 0; idx < len; ++idx) {
+        const int64_t v = br.list[idx];
+        const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
+        int* tk = br.keys + br.off[idx];
+        int* tc = br.cnts + br.off[idx];
+        for (int64_t s = start; s < cap; s += stride) {
+            tk[s] = -1;
+            tc[s] = 0;
+        }
+    }
+    for (int64_t idx = start; idx < len; idx += stride) {
+        br.best[idx] = 0;
+        br.own_cnt[idx] = 0;
+        br.hbest[idx] = ~0ull;
+        br.lbest[idx] = ~0ull;
+    }
+}
+
+// Chunks of kLdsRowMax edges of every listed row, dealt round-robin over the
+// workgroups: each chunk is counted in an LDS table first, then its distinct
+// labels are added to the row's table in the workspace (far fewer global
+// atomics where neighbour labels repeat, as they do once clusters form).
+__global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t* rowptr, const int32_t* col,
+                                                       const int32_t* lab_in, const uint32_t* flag_prev) {
+    __shared__ int s_keys[kLdsTable];
+    __shared__ int s_cnts[kLdsTable];
+    if (*flag_prev == 0) return;
+    const int64_t len = *br.len;
+    int64_t chunk0 = 0;  // global index of the current row's first chunk
+    for (int64_t idx = 0; idx < len; ++idx) {
+        const int64_t v = br.list[idx];
+        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        const int64_t cap = table_cap(b - a);
+        const int64_t chunks = cdiv(b - a, kLdsRowMax);
+        int* tk = br.keys + br.off[idx];
+        int* tc = br.cnts + br.off[idx];
+        // first chunk of this row owned by this workgroup
+        int64_t c = (int64_t(blockIdx.x) - chunk0 % gridDim.x + gridDim.x) % gridDim.x;
+        for (; c < chunks; c += gridDim.x) {
+            for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
+                s_keys[x] = -1;
+                s_cnts[x] = 0;
+            }
+            __syncthreads();
+            const int64_t e0 = a + c * kLdsRowMax;
+            const int64_t e1 = e0 + kLdsRowMax < b ? e0 + kLdsRowMax : b;
+            for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
+                const int cc = col[e];
+                if (cc == v) continue;
+                const int L = lab_in[cc];
+                int slot = int(mix64(uint64_t(uint32_t(L))) & uint64_t(kLdsTable - 1));
+                while (true) {
+                    const int prev = atomicCAS(&s_keys[slot], -1, L);
+                    if (prev == -1 || prev == L) {
+                        atomicAdd(&s_cnts[slot], 1);
+                        break;
+                    }
+                    slot = (slot + 1) & (kLdsTable - 1);
+                }
+            }
+            __syncthreads();
+            for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
+                const int L = s_keys[x];
+                if (L < 0) continue;
+                int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
+                while (true) {
+                    const int prev = atomicCAS(&tk[slot], -1, L);
+                    if (prev == -1 || prev == L) {
+                        atomicAdd(&tc[slot], s_cnts[x]);
+                        break;
+                    }
+                    slot = (slot + 1) & (cap - 1);
+                }
+            }
+            __syncthreads();
+        }
+        chunk0 += chunks;
+    }
+}
+
+// pass 0: best count and the own label's count; 1: smallest hash among the
+// best labels; 2: smallest label with that hash (passes 1-2 only where the own
+// label is not among the best).
+template <int kPass>
+__global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t* rowptr, const int32_t* lab_in,
+                                                       uint64_t key, const uint32_t* flag_prev) {
+    __shared__ int s_red[kBlock / kWave];
+    __shared__ uint64_t s_red64[kBlock / kWave];
+    if (*flag_prev == 0) return;
+    const int64_t len = *br.len;
+    const int64_t stride = int64_t(gridDim.x) * kBlock, start = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    for (int64_t idx = 0; idx < len; ++idx) {
+        const int64_t v = br.list[idx];
+        const int own = lab_in[v];
+        const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
+        const int* tk = br.keys + br.off[idx];
+        const int* tc = br.cnts + br.off[idx];
+        if (kPass == 0) {
+            int best = 0, oc = 0;
+            for (int64_t s = start; s < cap; s += stride) {
+                const int k = tk[s];
+                if (k < 0) continue;
+                const int c = tc[s];
+                best = c > best ? c : best;
+                if (k == own) oc = c;
+            }
+            best = block_max_i32(best, s_red);
+            oc = block_max_i32(oc, s_red);
+            if (threadIdx.x == 0) {
+                if (best) atomicMax(&br.best[idx], best);
+                if (oc) atomicMax(&br.own_cnt[idx], oc);
+            }
+        } else {
+            const int best = br.best[idx];
+            if (best == 0 || br.own_cnt[idx] == best) continue;  // uniform across the workgroup
+            const uint64_t hb = kPass == 2 ? br.hbest[idx] : 0;
+            uint64_t r = ~0ull;
+            for (int64_t s = start; s < cap; s += stride) {
+                const int k = tk[s];
+                if (k < 0 || tc[s] != best) continue;
+                const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
+                if (kPass == 1) r = h < r ? h : r;
+                else if (h == hb) r = uint64_t(uint32_t(k)) < r ? uint64_t(uint32_t(k)) : r;
+            }
+            r = block_min_u64(r, s_red64);
+            if (threadIdx.x == 0 && r != ~0ull) atomicMin(kPass == 1 ? &br.hbest[idx] : &br.lbest[idx], r);
+        }
+    }
+}
+
+__global__ void k_big_decide(BigRows br, const int32_t* lab_in, int32_t* lab_out, uint64_t key,
+                             const uint32_t* flag_prev, uint32_t* flag_next) {
+    const bool converged = *flag_prev == 0;
+    const int64_t len = *br.len;
+    for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < len;
+         idx += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t v = br.list[idx];
+        const int own = lab_in[v];
+        if (converged) {
+            lab_out[v] = own;
+            continue;
+        }
+        const int best = br.best[idx];
+        const int cand = (best > 0 && br.own_cnt[idx] != best) ? int(br.lbest[idx]) : own;
+        lab_out[v] = is_active(v, key) ? cand : own;
+        if (cand != own) *flag_next = 1u;
     }
 }
 
@@ -276,6 +449,10 @@ struct ReorderWs {
     int64_t* big_off;
     int* tab_keys;
     int* tab_cnts;
+    int* big_best;
+    int* big_own;
+    unsigned long long* big_hbest;
+    unsigned long long* big_lbest;
     uint64_t* sort_keys;
     uint32_t* sort_vals;
     ScanTmp scan;
@@ -302,6 +479,10 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     const int64_t tab = 4 * (nnz > 0 ? nnz : 1);  // sum over big rows of cap <= 4 * deg
     r.tab_keys = ws.take<int>(size_t(tab));
     r.tab_cnts = ws.take<int>(size_t(tab));
+    r.big_best = ws.take<int>(n1);
+    r.big_own = ws.take<int>(n1);
+    r.big_hbest = ws.take<unsigned long long>(n1);
+    r.big_lbest = ws.take<unsigned long long>(n1);
     r.sort_keys = ws.take<uint64_t>(n1);
     r.sort_vals = ws.take<uint32_t>(n1);
     r.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1)));
@@ -356,6 +537,11 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if ((st = fill_u32(r.flags, iters + 1, 0, stream)) != GT_OK) return st;
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
+    int64_t n_big = 0;
+    GT_HIP(hipMemcpyAsync(&n_big, r.pos_big + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipStreamSynchronize(stream));
+    BigRows br{r.big_list, r.pos_big + n, r.big_off, r.tab_keys, r.tab_cnts, r.big_best, r.big_own,
+               r.big_hbest, r.big_lbest};
     const unsigned gw = grid_for(n, kBlock / kWave, 65536);
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
@@ -363,13 +549,22 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         int32_t* out = r.lab[(t + 1) & 1];
         k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
         GT_LAUNCH_CHECK("reorder_lp_wave");
-        k_lp_block<false><<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
-                                                       r.flags + t, r.flags + t + 1, nullptr, nullptr, nullptr);
+        k_lp_block<<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key, r.flags + t,
+                                                r.flags + t + 1);
         GT_LAUNCH_CHECK("reorder_lp_lds");
-        k_lp_block<true><<<256, kBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in, out, key,
-                                                     r.flags + t, r.flags + t + 1, r.tab_keys, r.tab_cnts,
-                                                     r.big_off);
-        GT_LAUNCH_CHECK("reorder_lp_global");
+        if (n_big > 0) {
+            const uint32_t* fp = r.flags + t;
+            k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp);
+            GT_LAUNCH_CHECK("reorder_big_clear");
+            k_big_insert<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, in, fp);
+            GT_LAUNCH_CHECK("reorder_big_insert");
+            k_big_reduce<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+            k_big_reduce<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+            k_big_reduce<2><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+            GT_LAUNCH_CHECK("reorder_big_reduce");
+            k_big_decide<<<grid_for(n_big, 256, 1024), 256, 0, stream>>>(br, in, out, key, fp, r.flags + t + 1);
+            GT_LAUNCH_CHECK("reorder_big_decide");
+        }
     }
     const int32_t* final_lab = r.lab[iters & 1];
     k_order_keys<<<g, 256, 0, stream>>>(n, final_lab, r.deg_off, r.sort_keys);

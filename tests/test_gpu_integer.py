@@ -35,7 +35,15 @@ def small_graphs():
     u2, v2 = np.nonzero(np.random.default_rng(3).random((n, 8)) < 0.5)
     out.append(("hubs_6000", *csr_from_pairs(n, np.concatenate([u, u2 % n]),
                                              np.concatenate([v, (u2 * 7 + v2 * 131) % n]))))
-    for name, sc in (("c1", 1.0), ("c2", 0.05), ("c3", 0.02), ("c4", 0.02), ("c5", 0.1)):
+    # several rows above 4096 entries at once (each spread over the whole grid), of different table sizes
+    n = 30000
+    hubs = [(0, 4500), (7, 9000), (29999, 20000)]
+    u = np.concatenate([np.full(d, h, np.int64) for h, d in hubs])
+    v = np.concatenate([(np.arange(1, d + 1) * 13 + h) % n for h, d in hubs])
+    u2 = rng.integers(0, n, 60000)
+    v2 = (u2 + rng.integers(1, 50, 60000)) % n
+    out.append(("three_hubs_30000", *csr_from_pairs(n, np.concatenate([u, u2]), np.concatenate([v, v2]))))
+    for name, sc in (("c1", 1.0), ("c2", 0.05), ("c3", 0.02), ("c4", 0.02), ("c5", 0.1), ("b1", 0.02)):
         g = make_workload(name, sc).graph
         out.append((f"{name}@{sc}", g.rowptr, g.col))
     return out
