@@ -182,6 +182,14 @@ __device__ __forceinline__ void walk_edges(const int32_t* __restrict__ cl, int64
     }
 }
 
+// The value of lane 0 of each L-lane group, in every lane of the group.
+template <int L>
+__device__ __forceinline__ float group_bcast0(float x) {
+    if constexpr (L == 2) return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xA0, 0xF, 0xF, false));
+    if constexpr (L == 4) return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x00, 0xF, 0xF, false));
+    return x;
+}
+
 // Bias (exp2 domain) of a row's edges t and t + 1 at CSR offset a; 0 where
 // the edge is missing.
 __device__ __forceinline__ void bias_pair(const EdgeBias& eb, int64_t a, int t, bool ok0, bool ok1, int H, int h,
@@ -356,10 +364,14 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
     q1.load(Q + ln.off(i1));
     g0.load(dO + ln.off(i0));
     g1.load(dO + ln.off(i1));
-    const float2 st0 = stat[i0 * H + ln.h];
-    const float2 st1 = stat[i1 * H + ln.h];
-    const float l0 = st0.x, D0 = st0.y;
-    const float l1 = st1.x, D1 = st1.y;
+    // one lane of each (node, head) group reads the pair; the others take it by DPP
+    float2 st0 = make_float2(0.f, 0.f), st1 = make_float2(0.f, 0.f);
+    if (ln.part == 0) {
+        st0 = stat[i0 * H + ln.h];
+        st1 = stat[i1 * H + ln.h];
+    }
+    const float l0 = group_bcast0<C::L>(st0.x), D0 = group_bcast0<C::L>(st0.y);
+    const float l1 = group_bcast0<C::L>(st1.x), D1 = group_bcast0<C::L>(st1.y);
     float s0 = group_sum<C::L>(q0.dot(k)) * sl2;
     float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
     int64_t e0 = 0, e1 = 0;
