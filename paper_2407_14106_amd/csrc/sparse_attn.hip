@@ -190,12 +190,30 @@ __device__ __forceinline__ float group_bcast0(float x) {
     return x;
 }
 
+// The value of the first lane of each G-lane group (one node's lanes), in
+// every lane of the group.
+template <int G>
+__device__ __forceinline__ int group_first(int x) {
+    if constexpr (G == 1) return x;
+    else if constexpr (G == 2) return __builtin_amdgcn_mov_dpp(x, 0xA0, 0xF, 0xF, false);  // quad_perm 0,0,2,2
+    else if constexpr (G == 4) return __builtin_amdgcn_mov_dpp(x, 0x00, 0xF, 0xF, false);  // quad_perm 0,0,0,0
+    else if constexpr (G == 16) return __builtin_amdgcn_mov_dpp(x, 0x150, 0xF, 0xF, false);  // row_newbcast:0
+    else if constexpr (G == 64) return __builtin_amdgcn_readfirstlane(x);
+    else return __shfl(x, lane_id() & ~(G - 1), kWave);
+}
+
 // Bias (exp2 domain) of a row's edges t and t + 1 at CSR offset a; 0 where
-// the edge is missing.
-__device__ __forceinline__ void bias_pair(const EdgeBias& eb, int64_t a, int t, bool ok0, bool ok1, int H, int h,
-                                          float& b0, float& b1) {
-    b0 = ok0 ? eb.at(a + t, H, h) : 0.f;
-    b1 = ok1 ? eb.at(a + t + 1, H, h) : 0.f;
+// the edge is missing.  One lane of each (node, head) group reads it.
+template <typename LN>
+__device__ __forceinline__ void bias_pair(const EdgeBias& eb, int64_t a, int t, bool ok0, bool ok1, int H,
+                                          const LN& ln, float& b0, float& b1) {
+    float x0 = 0.f, x1 = 0.f;
+    if (ln.part == 0) {
+        x0 = ok0 ? eb.at(a + t, H, ln.h) : 0.f;
+        x1 = ok1 ? eb.at(a + t + 1, H, ln.h) : 0.f;
+    }
+    b0 = group_bcast0<LN::C::L>(x0);
+    b1 = group_bcast0<LN::C::L>(x1);
 }
 
 // ------------------------------------------------------------------ forward
@@ -228,7 +246,7 @@ __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t*
     if (live && deg >= 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
     walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
         float b0 = 0.f, b1 = 0.f;
-        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln.h, b0, b1);
+        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln, b0, b1);
         fwd_step<T, D, H, kBias>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
     });
     if (live && deg >= 0) {
@@ -337,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
     if (live && deg >= 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
     walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
         float b0 = 0.f, b1 = 0.f;
-        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln.h, b0, b1);
+        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln, b0, b1);
         dq_step<T, D, H, kBias>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
     });
     if (live && deg >= 0) {
@@ -376,10 +394,21 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
     float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
     int64_t e0 = 0, e1 = 0;
     if constexpr (kBias) {
-        e0 = ok0 ? eb.csc_pos[c0] : 0;
-        e1 = ok1 ? eb.csc_pos[c1] : 0;
-        if (ok0) s0 += eb.at(e0, H, ln.h);
-        if (ok1) s1 += eb.at(e1, H, ln.h);
+        // the node's first lane reads the CSR positions, one lane per head the bias
+        int p0 = 0, p1 = 0;
+        if ((lane_id() & (C::G - 1)) == 0) {
+            p0 = ok0 ? eb.csc_pos[c0] : 0;
+            p1 = ok1 ? eb.csc_pos[c1] : 0;
+        }
+        e0 = group_first<C::G>(p0);
+        e1 = group_first<C::G>(p1);
+        float x0 = 0.f, x1 = 0.f;
+        if (ln.part == 0) {
+            x0 = ok0 ? eb.at(e0, H, ln.h) : 0.f;
+            x1 = ok1 ? eb.at(e1, H, ln.h) : 0.f;
+        }
+        s0 += group_bcast0<C::L>(x0);
+        s1 += group_bcast0<C::L>(x1);
     }
     const float dp0 = group_sum<C::L>(g0.dot(v));
     const float dp1 = group_sum<C::L>(g1.dot(v));
