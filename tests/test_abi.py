@@ -108,3 +108,46 @@ def test_python_binding_rejects_cpu_tensors(lib):
     cl = torch.zeros(0, dtype=torch.int32)
     with pytest.raises(ValueError):
         gt.build_tiles(rp, cl)
+
+
+def test_extension_entry_points_reject_bad_arguments(lib):
+    stream = None
+    c = gt.GtTiles(n=100, T=128, n_row_tiles=1, nnz_sparse=50)
+    for name in ("tile_rowptr", "sp_rowptr", "sp_colptr", "tileT_ptr", "sp_col", "sp_row"):
+        setattr(c, name, 0x1000)
+    ws = 1 << 30
+    # bias calls: a plan with dense tiles is refused, a null bias too
+    c.n_dense = 3
+    c.tile_col = c.tile_mask = c.tileT_idx = 0x1000
+    assert lib.gt_sparse_attn_fwd_bias(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE,
+                                       FAKE, ws, stream) == gt.GT_ERR_UNSUPPORTED
+    c.n_dense = 0
+    assert lib.gt_sparse_attn_fwd_bias(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, None, 1.0, FAKE, FAKE,
+                                       FAKE, ws, stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_sparse_attn_bwd_bias(ctypes.byref(c), None, 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                       1.0, FAKE, FAKE, FAKE, FAKE, FAKE, ws, stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_sparse_attn_bwd_bias(ctypes.byref(c), FAKE, 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                       1.0, FAKE, FAKE, FAKE, None, FAKE, ws, stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_sparse_attn_fwd_bias(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE,
+                                       FAKE, 0, stream) == gt.GT_ERR_WORKSPACE
+    # edge map / probe / relabel with edge positions
+    assert lib.gt_edge_map(None, FAKE, FAKE, ws, stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_edge_map(ctypes.byref(c), FAKE, FAKE, 0, stream) == gt.GT_ERR_WORKSPACE
+    assert lib.gt_gather_probe(ctypes.byref(c), 8, 48, gt.GT_BF16, FAKE, FAKE, FAKE, stream) == gt.GT_ERR_UNSUPPORTED
+    assert lib.gt_gather_probe(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, None, FAKE, stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_permute_csr_edges(100, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws,
+                                    stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_permute_edges_workspace_size(100, 10) > lib.gt_permute_workspace_size(100, 10)
+    # interleave check
+    rep = gt.GtInterleaveReport()
+    assert lib.gt_interleave_check(100, 10, FAKE, FAKE, -1, ctypes.byref(rep), None, FAKE, ws,
+                                   stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_interleave_check(100, 10, FAKE, FAKE, 4, None, None, FAKE, ws, stream) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_interleave_check(100, 10, FAKE, FAKE, 4, ctypes.byref(rep), None, FAKE, 0,
+                                   stream) == gt.GT_ERR_WORKSPACE
+    assert lib.gt_interleave_workspace_size(100) > 0
+
+
+def test_report_and_tuner_layouts_match_header():
+    assert ctypes.sizeof(gt.GtInterleaveReport) == 8 * 4 + 4 * 6
+    assert ctypes.sizeof(gt.GtAutotuner) == 8 + 8 * gt.GT_AUTOTUNER_HISTORY + 8 + 8 + 4 + 4 + 2 * 8 * gt.GT_AUTOTUNER_RUNGS
