@@ -5,10 +5,11 @@
 //   deg <= 64          one wavefront per row, one neighbour label per lane;
 //                      multiplicities by an in-register all-pairs compare.
 //   64 < deg <= 4096   one workgroup per row, open-addressing count table in LDS.
-//   deg > 4096         the whole grid per row (a hub, a global token attending
-//                      to every node): count table in the workspace filled by
-//                      every workgroup, then reduced by every workgroup in
-//                      three passes (best count, smallest hash, smallest label).
+//   4096 < deg <= 2^16 one workgroup per row, count table in the workspace.
+//   deg > 2^16         the whole grid (a global token attending to every node):
+//                      count table in the workspace filled by every workgroup,
+//                      then reduced by every workgroup in three passes (best
+//                      count, smallest hash, smallest label).
 // All three compute the same function of the neighbour-label multiset.
 #include <limits.h>
 
@@ -26,6 +27,7 @@ constexpr int kLdsRowMax = kLdsTable / 2;
 constexpr int kBlock = 256;
 constexpr int kMaxSweeps = 1000;
 constexpr int kBigGrid = 1024;  // workgroups sharing each very long row
+constexpr int64_t kHugeRow = int64_t(1) << 16;
 
 __device__ __forceinline__ bool is_active(int64_t v, uint64_t key) {
     return (mix64(uint64_t(v) ^ key ^ kActivitySalt) >> 61) != 0;
@@ -56,7 +58,7 @@ __device__ __forceinline__ int wave_min_i32(int v) {
 // -------------------------------------------------------------- per-row classes
 
 __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
-                           int32_t* is_med, int32_t* is_big, int64_t* big_cap) {
+                           int32_t* is_med, int32_t* is_big, int32_t* is_huge, int64_t* big_cap) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         // self-loop present?  rows are sorted: binary search for v.
@@ -71,21 +73,27 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
         deg_off[v] = uint32_t(deg - (self ? 1 : 0));
         is_med[v] = (deg > kWaveRowMax && deg <= kLdsRowMax) ? 1 : 0;
         const bool big = deg > kLdsRowMax;
-        is_big[v] = big ? 1 : 0;
+        is_big[v] = big && deg <= kHugeRow ? 1 : 0;
+        is_huge[v] = deg > kHugeRow ? 1 : 0;
         int64_t cap = 1;
         while (cap < 2 * deg) cap <<= 1;
         big_cap[v] = big ? cap : 0;
     }
 }
 
-__global__ void k_compact(int64_t n, const int32_t* is_med, const int32_t* is_big, const int64_t* pos_med,
-                          const int64_t* pos_big, const int64_t* cap_off, int32_t* med_list, int32_t* big_list,
-                          int64_t* big_off) {
+__global__ void k_compact(int64_t n, const int32_t* is_med, const int32_t* is_big, const int32_t* is_huge,
+                          const int64_t* pos_med, const int64_t* pos_big, const int64_t* pos_huge,
+                          const int64_t* cap_off, int32_t* med_list, int32_t* big_list, int64_t* big_off,
+                          int32_t* huge_list, int64_t* huge_off) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         if (is_med[v]) med_list[pos_med[v]] = int32_t(v);
         if (is_big[v]) {
             big_list[pos_big[v]] = int32_t(v);
             big_off[pos_big[v]] = cap_off[v];
+        }
+        if (is_huge[v]) {
+            huge_list[pos_huge[v]] = int32_t(v);
+            huge_off[pos_huge[v]] = cap_off[v];
         }
     }
 }
@@ -158,13 +166,22 @@ __device__ __forceinline__ uint64_t block_min_u64(uint64_t v, uint64_t* s) {
 }
 
 
-// One workgroup per listed row.  LDS table: keys (label or -1) and counts.
+template <bool kGlobal>
+__device__ __forceinline__ int tab_load(const int* p) {
+    if (kGlobal) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return *p;
+}
+
+// One workgroup per listed row.  Table: keys (label or -1) and counts, in LDS
+// (rows up to kLdsRowMax) or in the workspace (up to kHugeRow).
+template <bool kGlobal>
 __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const int64_t* list_len,
                                                      const int64_t* rowptr, const int32_t* col,
                                                      const int32_t* lab_in, int32_t* lab_out, uint64_t key,
-                                                     const uint32_t* flag_prev, uint32_t* flag_next) {
-    __shared__ int s_keys[kLdsTable];
-    __shared__ int s_cnts[kLdsTable];
+                                                     const uint32_t* flag_prev, uint32_t* flag_next,
+                                                     int* gkeys, int* gcnts, const int64_t* big_off) {
+    __shared__ int s_keys[kGlobal ? 1 : kLdsTable];
+    __shared__ int s_cnts[kGlobal ? 1 : kLdsTable];
     __shared__ int s_red[kBlock / kWave];
     __shared__ uint64_t s_red64[kBlock / kWave];
     const bool converged = *flag_prev == 0;
@@ -180,12 +197,13 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
         const int64_t deg = b - a;
         int64_t cap = 1;
         while (cap < 2 * deg) cap <<= 1;
-        int* tk = s_keys;
-        int* tc = s_cnts;
+        int* tk = kGlobal ? gkeys + big_off[idx] : s_keys;
+        int* tc = kGlobal ? gcnts + big_off[idx] : s_cnts;
         for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
             tk[s] = -1;
             tc[s] = 0;
         }
+        if (kGlobal) __threadfence();
         __syncthreads();
         for (int64_t e = a + threadIdx.x; e < b; e += kBlock) {
             const int c = col[e];
@@ -201,12 +219,13 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
                 slot = (slot + 1) & (cap - 1);
             }
         }
+        if (kGlobal) __threadfence();
         __syncthreads();
         int best = 0, own_cnt = 0;
         for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
-            const int k = tk[s];
+            const int k = tab_load<kGlobal>(&tk[s]);
             if (k < 0) continue;
-            const int c = tc[s];
+            const int c = tab_load<kGlobal>(&tc[s]);
             best = c > best ? c : best;
             if (k == own) own_cnt = c;
         }
@@ -216,16 +235,16 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
         if (best > 0 && own_cnt != best) {
             uint64_t hbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
-                const int k = tk[s];
-                if (k < 0 || tc[s] != best) continue;
+                const int k = tab_load<kGlobal>(&tk[s]);
+                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 hbest = h < hbest ? h : hbest;
             }
             hbest = block_min_u64(hbest, s_red64);
             uint64_t lbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
-                const int k = tk[s];
-                if (k < 0 || tc[s] != best) continue;
+                const int k = tab_load<kGlobal>(&tk[s]);
+                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
                 if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
                 lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
             }
@@ -240,8 +259,9 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
 }
 
 // -------------------------------------------------------------- very long rows
-// Every workgroup takes a strided slice of each listed row (edges, then table
-// slots), so a row of a million edges is spread over the chip.  Per-row
+// The edges and the table slots of each listed row are cut into chunks dealt
+// round-robin over the workgroups, so a row of a million edges is spread over
+// the chip and many long rows share it.  Per-row
 // results: best count, own label's count, smallest hash among the best, and the
 // smallest label with that hash, combined with atomics (max / min: the result
 // does not depend on the order).
@@ -264,20 +284,35 @@ __device__ __forceinline__ int64_t table_cap(int64_t deg) {
     return cap;
 }
 
+// Table slots of every listed row in chunks of kSlotChunk, dealt round-robin
+// over the workgroups like the edge chunks below: every row gets as many
+// workgroups as its table needs.
+constexpr int64_t kSlotChunk = 8192;
+
+__device__ __forceinline__ int64_t first_chunk(int64_t chunk0) {
+    return (int64_t(blockIdx.x) - chunk0 % gridDim.x + gridDim.x) % gridDim.x;
+}
+
 __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t* rowptr, const uint32_t* flag_prev) {
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
-    const int64_t stride = int64_t(gridDim.x) * kBlock, start = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    int64_t chunk0 = 0;
     for (int64_t idx = 0; idx < len; ++idx) {
         const int64_t v = br.list[idx];
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
+        const int64_t chunks = cdiv(cap, kSlotChunk);
         int* tk = br.keys + br.off[idx];
         int* tc = br.cnts + br.off[idx];
-        for (int64_t s = start; s < cap; s += stride) {
-            tk[s] = -1;
-            tc[s] = 0;
+        for (int64_t c = first_chunk(chunk0); c < chunks; c += gridDim.x) {
+            const int64_t s1 = (c + 1) * kSlotChunk < cap ? (c + 1) * kSlotChunk : cap;
+            for (int64_t s = c * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
+                tk[s] = -1;
+                tc[s] = 0;
+            }
         }
+        chunk0 += chunks;
     }
+    const int64_t stride = int64_t(gridDim.x) * kBlock, start = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     for (int64_t idx = start; idx < len; idx += stride) {
         br.best[idx] = 0;
         br.own_cnt[idx] = 0;
@@ -304,9 +339,7 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
         const int64_t chunks = cdiv(b - a, kLdsRowMax);
         int* tk = br.keys + br.off[idx];
         int* tc = br.cnts + br.off[idx];
-        // first chunk of this row owned by this workgroup
-        int64_t c = (int64_t(blockIdx.x) - chunk0 % gridDim.x + gridDim.x) % gridDim.x;
-        for (; c < chunks; c += gridDim.x) {
+        for (int64_t c = first_chunk(chunk0); c < chunks; c += gridDim.x) {
             for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
                 s_keys[x] = -1;
                 s_cnts[x] = 0;
@@ -358,21 +391,28 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
     __shared__ uint64_t s_red64[kBlock / kWave];
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
-    const int64_t stride = int64_t(gridDim.x) * kBlock, start = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    int64_t chunk0 = 0;
     for (int64_t idx = 0; idx < len; ++idx) {
         const int64_t v = br.list[idx];
-        const int own = lab_in[v];
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
+        const int64_t chunks = cdiv(cap, kSlotChunk);
+        const int64_t c_first = first_chunk(chunk0);
+        chunk0 += chunks;
+        if (c_first >= chunks) continue;  // uniform across the workgroup
+        const int own = lab_in[v];
         const int* tk = br.keys + br.off[idx];
         const int* tc = br.cnts + br.off[idx];
         if (kPass == 0) {
             int best = 0, oc = 0;
-            for (int64_t s = start; s < cap; s += stride) {
-                const int k = tk[s];
-                if (k < 0) continue;
-                const int c = tc[s];
-                best = c > best ? c : best;
-                if (k == own) oc = c;
+            for (int64_t c = c_first; c < chunks; c += gridDim.x) {
+                const int64_t s1 = (c + 1) * kSlotChunk < cap ? (c + 1) * kSlotChunk : cap;
+                for (int64_t s = c * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
+                    const int k = tk[s];
+                    if (k < 0) continue;
+                    const int cnt = tc[s];
+                    best = cnt > best ? cnt : best;
+                    if (k == own) oc = cnt;
+                }
             }
             best = block_max_i32(best, s_red);
             oc = block_max_i32(oc, s_red);
@@ -385,12 +425,15 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
             if (best == 0 || br.own_cnt[idx] == best) continue;  // uniform across the workgroup
             const uint64_t hb = kPass == 2 ? br.hbest[idx] : 0;
             uint64_t r = ~0ull;
-            for (int64_t s = start; s < cap; s += stride) {
-                const int k = tk[s];
-                if (k < 0 || tc[s] != best) continue;
-                const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
-                if (kPass == 1) r = h < r ? h : r;
-                else if (h == hb) r = uint64_t(uint32_t(k)) < r ? uint64_t(uint32_t(k)) : r;
+            for (int64_t c = c_first; c < chunks; c += gridDim.x) {
+                const int64_t s1 = (c + 1) * kSlotChunk < cap ? (c + 1) * kSlotChunk : cap;
+                for (int64_t s = c * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
+                    const int k = tk[s];
+                    if (k < 0 || tc[s] != best) continue;
+                    const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
+                    if (kPass == 1) r = h < r ? h : r;
+                    else if (h == hb) r = uint64_t(uint32_t(k)) < r ? uint64_t(uint32_t(k)) : r;
+                }
             }
             r = block_min_u64(r, s_red64);
             if (threadIdx.x == 0 && r != ~0ull) atomicMin(kPass == 1 ? &br.hbest[idx] : &br.lbest[idx], r);
@@ -440,13 +483,17 @@ struct ReorderWs {
     uint32_t* deg_off;
     int32_t* is_med;
     int32_t* is_big;
+    int32_t* is_huge;
     int64_t* big_cap;
     int64_t* pos_med;
     int64_t* pos_big;
+    int64_t* pos_huge;
     int64_t* cap_off;
     int32_t* med_list;
     int32_t* big_list;
     int64_t* big_off;
+    int32_t* huge_list;
+    int64_t* huge_off;
     int* tab_keys;
     int* tab_cnts;
     int* big_best;
@@ -469,13 +516,17 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.deg_off = ws.take<uint32_t>(n1);
     r.is_med = ws.take<int32_t>(n1);
     r.is_big = ws.take<int32_t>(n1);
+    r.is_huge = ws.take<int32_t>(n1);
     r.big_cap = ws.take<int64_t>(n1);
     r.pos_med = ws.take<int64_t>(n1 + 1);
     r.pos_big = ws.take<int64_t>(n1 + 1);
+    r.pos_huge = ws.take<int64_t>(n1 + 1);
     r.cap_off = ws.take<int64_t>(n1 + 1);
     r.med_list = ws.take<int32_t>(n1);
     r.big_list = ws.take<int32_t>(n1);
     r.big_off = ws.take<int64_t>(n1);
+    r.huge_list = ws.take<int32_t>(n1);
+    r.huge_off = ws.take<int64_t>(n1);
     const int64_t tab = 4 * (nnz > 0 ? nnz : 1);  // sum over big rows of cap <= 4 * deg
     r.tab_keys = ws.take<int>(size_t(tab));
     r.tab_cnts = ws.take<int>(size_t(tab));
@@ -524,23 +575,24 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if (st != GT_OK) return st;
 
     const unsigned g = grid_for(n, 256, 8192);
-    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_med, r.is_big, r.big_cap);
+    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_med, r.is_big, r.is_huge, r.big_cap);
     GT_LAUNCH_CHECK("reorder_classify");
     if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_big, n, r.pos_big, r.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(r.is_huge, n, r.pos_huge, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
-    k_compact<<<g, 256, 0, stream>>>(n, r.is_med, r.is_big, r.pos_med, r.pos_big, r.cap_off, r.med_list,
-                                     r.big_list, r.big_off);
+    k_compact<<<g, 256, 0, stream>>>(n, r.is_med, r.is_big, r.is_huge, r.pos_med, r.pos_big, r.pos_huge, r.cap_off,
+                                     r.med_list, r.big_list, r.big_off, r.huge_list, r.huge_off);
     GT_LAUNCH_CHECK("reorder_compact");
 
     if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
     if ((st = fill_u32(r.flags, iters + 1, 0, stream)) != GT_OK) return st;
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
-    int64_t n_big = 0;
-    GT_HIP(hipMemcpyAsync(&n_big, r.pos_big + n, 8, hipMemcpyDeviceToHost, stream));
+    int64_t n_huge = 0;
+    GT_HIP(hipMemcpyAsync(&n_huge, r.pos_huge + n, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
-    BigRows br{r.big_list, r.pos_big + n, r.big_off, r.tab_keys, r.tab_cnts, r.big_best, r.big_own,
+    BigRows br{r.huge_list, r.pos_huge + n, r.huge_off, r.tab_keys, r.tab_cnts, r.big_best, r.big_own,
                r.big_hbest, r.big_lbest};
     const unsigned gw = grid_for(n, kBlock / kWave, 65536);
     for (int t = 0; t < iters; ++t) {
@@ -549,10 +601,14 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         int32_t* out = r.lab[(t + 1) & 1];
         k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
         GT_LAUNCH_CHECK("reorder_lp_wave");
-        k_lp_block<<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key, r.flags + t,
-                                                r.flags + t + 1);
+        k_lp_block<false><<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
+                                                       r.flags + t, r.flags + t + 1, nullptr, nullptr, nullptr);
         GT_LAUNCH_CHECK("reorder_lp_lds");
-        if (n_big > 0) {
+        k_lp_block<true><<<256, kBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in, out, key,
+                                                     r.flags + t, r.flags + t + 1, r.tab_keys, r.tab_cnts,
+                                                     r.big_off);
+        GT_LAUNCH_CHECK("reorder_lp_global");
+        if (n_huge > 0) {
             const uint32_t* fp = r.flags + t;
             k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp);
             GT_LAUNCH_CHECK("reorder_big_clear");
@@ -562,7 +618,7 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             k_big_reduce<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
             k_big_reduce<2><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
             GT_LAUNCH_CHECK("reorder_big_reduce");
-            k_big_decide<<<grid_for(n_big, 256, 1024), 256, 0, stream>>>(br, in, out, key, fp, r.flags + t + 1);
+            k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, in, out, key, fp, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_big_decide");
         }
     }

@@ -43,7 +43,8 @@ def small_graphs():
     u2 = rng.integers(0, n, 60000)
     v2 = (u2 + rng.integers(1, 50, 60000)) % n
     out.append(("three_hubs_30000", *csr_from_pairs(n, np.concatenate([u, u2]), np.concatenate([v, v2]))))
-    for name, sc in (("c1", 1.0), ("c2", 0.05), ("c3", 0.02), ("c4", 0.02), ("c5", 0.1), ("b1", 0.02)):
+    # b1 at 10%: the global token's row (about 98,000 entries) takes the whole-grid path (rows above 2^16)
+    for name, sc in (("c1", 1.0), ("c2", 0.05), ("c3", 0.02), ("c4", 0.02), ("c5", 0.1), ("b1", 0.02), ("b1", 0.1)):
         g = make_workload(name, sc).graph
         out.append((f"{name}@{sc}", g.rowptr, g.col))
     return out
