@@ -617,19 +617,216 @@ __device__ __forceinline__ void load_mask_row(uint32_t (&mw)[T / 32], const uint
     }
 }
 
+// ---- chunks of the dense tiles of each tile row (column)
+
+__global__ void k_tile_chunk_counts(int64_t R, const int64_t* __restrict__ ptr, int CH, int32_t* __restrict__ counts,
+                                    int32_t* __restrict__ ecounts) {
+    for (int64_t I = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; I < R; I += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t c = cdiv(ptr[I + 1] - ptr[I], CH);
+        counts[I] = int32_t(c);
+        ecounts[I] = int32_t(c > 0 ? c - 1 : 0);
+    }
+}
+
+// Workgroup b -> tile row (column) I, its list range [t0, t1) and the output
+// slot (-1: the partial state of the row; else an extra slot); false for the
+// surplus of the grid.
+__device__ __forceinline__ bool tile_chunk(const TileChunks& ck, const int64_t* __restrict__ ptr, int64_t R,
+                                           int64_t b, int64_t& I, int64_t& t0, int64_t& t1, int64_t& slot) {
+    if (b >= ck.chunk_off[R]) return false;
+    int64_t lo = 0, hi = R;  // the last I with chunk_off[I] <= b
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (ck.chunk_off[mid] <= b) lo = mid;
+        else hi = mid;
+    }
+    I = lo;
+    const int64_t j = b - ck.chunk_off[lo];
+    t0 = ptr[lo] + j * ck.CH;
+    t1 = t0 + ck.CH < ptr[lo + 1] ? t0 + ck.CH : ptr[lo + 1];
+    slot = j == 0 ? -1 : ck.extra_off[lo] + j - 1;
+    return true;
+}
+
+// Output row of node q (tile row I) for a chunk writing `slot`.
+__device__ __forceinline__ int64_t out_row(int64_t q, int64_t I, int64_t slot, int T) {
+    return slot < 0 ? q : slot * T + (q - I * T);
+}
+
+// Both offsets in one workgroup (plans of up to kPlanOneBlock tile rows): each
+// thread sums a contiguous run of rows, an LDS scan over the threads, then the
+// runs are written out.
+constexpr int kPlanThreads = 1024;
+constexpr int64_t kPlanOneBlock = int64_t(1) << 16;
+
+__global__ __launch_bounds__(kPlanThreads) void k_tile_chunk_plan1(int64_t R, const int64_t* __restrict__ ptr,
+                                                                   int CH, int64_t* __restrict__ chunk_off,
+                                                                   int64_t* __restrict__ extra_off) {
+    __shared__ int64_t s_c[kPlanThreads], s_e[kPlanThreads];
+    const int t = threadIdx.x;
+    const int64_t per = cdiv(R, int64_t(kPlanThreads));
+    const int64_t a = t * per < R ? t * per : R, b = a + per < R ? a + per : R;
+    int64_t c = 0, e = 0;
+    for (int64_t I = a; I < b; ++I) {
+        const int64_t k = cdiv(ptr[I + 1] - ptr[I], CH);
+        c += k;
+        e += k > 0 ? k - 1 : 0;
+    }
+    s_c[t] = c;
+    s_e[t] = e;
+    __syncthreads();
+    for (int o = 1; o < kPlanThreads; o <<= 1) {  // inclusive Hillis-Steele scan
+        const int64_t xc = t >= o ? s_c[t - o] : 0, xe = t >= o ? s_e[t - o] : 0;
+        __syncthreads();
+        s_c[t] += xc;
+        s_e[t] += xe;
+        __syncthreads();
+    }
+    c = s_c[t] - c;
+    e = s_e[t] - e;
+    for (int64_t I = a; I < b; ++I) {
+        chunk_off[I] = c;
+        extra_off[I] = e;
+        const int64_t k = cdiv(ptr[I + 1] - ptr[I], CH);
+        c += k;
+        e += k > 0 ? k - 1 : 0;
+    }
+    if (t == kPlanThreads - 1) {
+        chunk_off[R] = s_c[t];
+        extra_off[R] = s_e[t];
+    }
+}
+
+gt_status tile_chunk_plan(const gt_tiles* p, const int64_t* ptr, const TileChunks& ck, hipStream_t s) {
+    const int64_t R = p->n_row_tiles;
+    if (R <= kPlanOneBlock) {
+        k_tile_chunk_plan1<<<1, kPlanThreads, 0, s>>>(R, ptr, ck.CH, ck.chunk_off, ck.extra_off);
+        GT_LAUNCH_CHECK("tile_chunk_plan");
+        return GT_OK;
+    }
+    k_tile_chunk_counts<<<grid_for(R, 256, 1024), 256, 0, s>>>(R, ptr, ck.CH, ck.counts, ck.ecounts);
+    GT_LAUNCH_CHECK("tile_chunk_counts");
+    gt_status st = exclusive_scan_i32(ck.counts, R, ck.chunk_off, ck.scan, s);
+    if (st != GT_OK) return st;
+    return exclusive_scan_i32(ck.ecounts, R, ck.extra_off, ck.scan, s);
+}
+
+// Fold the extra slots of each tile row into its partial state.  A workgroup
+// takes kMergeRows<D> rows of one (tile row, head), D / 4 consecutive lanes per
+// row, one float4 each, so every slot row is read as whole cache lines.
+constexpr int kMergeThreads = 256;
+template <int D>
+constexpr int kMergeRows = kMergeThreads / (D / 4);
+
+inline dim3 merge_grid(int64_t R, int H, int T, int D) {
+    return dim3(unsigned(R), unsigned(H), unsigned(T / (kMergeThreads / (D / 4))));
+}
+
+// ... the forward's online-softmax states (m, l, acc) ...
+template <int D, int T>
+__global__ __launch_bounds__(kMergeThreads) void k_tiles_merge_fwd(int64_t n, int H, TileChunks ck,
+                                                                   float* __restrict__ pm, float* __restrict__ pl,
+                                                                   float* __restrict__ pacc) {
+    const int64_t I = blockIdx.x;
+    const int h = blockIdx.y;
+    const int64_t e0 = ck.extra_off[I], e1 = ck.extra_off[I + 1];
+    if (e0 == e1) return;
+    const int lr = blockIdx.z * kMergeRows<D> + threadIdx.x / (D / 4);
+    const int f = 4 * (threadIdx.x % (D / 4));
+    const int64_t q = I * T + lr;
+    if (q >= n) return;
+    const int64_t row = q * H + h;
+    const float m0 = pm[row];
+    float M = m0;
+    for (int64_t e = e0; e < e1; ++e) M = fmaxf(M, ck.m[(e * T + lr) * H + h]);
+    if (M == -__builtin_huge_valf()) return;  // no dense-tile edge in any chunk
+    const float w0 = m0 == -__builtin_huge_valf() ? 0.f : ex2(m0 - M);
+    float lsum = pl[row] * w0;
+    float4* out = reinterpret_cast<float4*>(pacc + row * D + f);
+    float4 acc = *out;
+    acc.x *= w0;
+    acc.y *= w0;
+    acc.z *= w0;
+    acc.w *= w0;
+#pragma unroll 2
+    for (int64_t e = e0; e < e1; ++e) {
+        const int64_t xr = (e * T + lr) * H + h;
+        const float me = ck.m[xr];
+        if (me == -__builtin_huge_valf()) continue;
+        const float w = ex2(me - M);
+        lsum += ck.l[xr] * w;
+        const float4 x = *reinterpret_cast<const float4*>(ck.acc + xr * D + f);
+        acc.x += x.x * w;
+        acc.y += x.y * w;
+        acc.z += x.z * w;
+        acc.w += x.w * w;
+    }
+    *out = acc;
+    if (f == 0) {
+        pm[row] = M;
+        pl[row] = lsum;
+    }
+}
+
+// ... and plain sums (the backward's A, B, D and dK, dV).
+template <int D, int T>
+__global__ __launch_bounds__(kMergeThreads) void k_tiles_merge_sum(int64_t n, int H, TileChunks ck,
+                                                                   float* __restrict__ a, float* __restrict__ b,
+                                                                   float* __restrict__ m) {
+    const int64_t I = blockIdx.x;
+    const int h = blockIdx.y;
+    const int64_t e0 = ck.extra_off[I], e1 = ck.extra_off[I + 1];
+    if (e0 == e1) return;
+    const int lr = blockIdx.z * kMergeRows<D> + threadIdx.x / (D / 4);
+    const int f = 4 * (threadIdx.x % (D / 4));
+    const int64_t q = I * T + lr;
+    if (q >= n) return;
+    const int64_t row = q * H + h;
+    float4* pa = reinterpret_cast<float4*>(a + row * D + f);
+    float4* pb = b ? reinterpret_cast<float4*>(b + row * D + f) : nullptr;
+    float4 sa = *pa, sb = pb ? *pb : make_float4(0.f, 0.f, 0.f, 0.f);
+    float sm = (m && f == 0) ? m[row] : 0.f;
+#pragma unroll 2
+    for (int64_t e = e0; e < e1; ++e) {
+        const int64_t xr = (e * T + lr) * H + h;
+        const float4 x = *reinterpret_cast<const float4*>(ck.acc + xr * D + f);
+        sa.x += x.x;
+        sa.y += x.y;
+        sa.z += x.z;
+        sa.w += x.w;
+        if (pb) {
+            const float4 y = *reinterpret_cast<const float4*>(ck.acc2 + xr * D + f);
+            sb.x += y.x;
+            sb.y += y.y;
+            sb.z += y.z;
+            sb.w += y.w;
+        }
+        if (m && f == 0) sm += ck.m[xr];
+    }
+    *pa = sa;
+    if (pb) *pb = sb;
+    if (m && f == 0) m[row] = sm;
+}
+
 template <int D, int T>
 __global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
                                                  const int32_t* __restrict__ tile_col,
                                                  const uint32_t* __restrict__ tile_mask,
                                                  const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                                  const uint16_t* __restrict__ V, float sl2, float* __restrict__ pm,
-                                                 float* __restrict__ pl, float* __restrict__ pacc) {
+                                                 float* __restrict__ pl, float* __restrict__ pacc, int64_t R,
+                                                 TileChunks ck) {
     constexpr int W = T / 32;
     __shared__ __attribute__((aligned(16))) uint16_t sK[1][kStage * RS<D>::v];
     __shared__ __attribute__((aligned(16))) uint16_t sVt[1][D * kTS];
-    const int I = blockIdx.x, h = blockIdx.y;
-    const int64_t t0 = tile_rowptr[I], t1 = tile_rowptr[I + 1];
-    if (t0 == t1) return;
+    const int h = blockIdx.y;
+    int64_t I, t0, t1, slot;
+    if (!tile_chunk(ck, tile_rowptr, R, blockIdx.x, I, t0, t1, slot)) return;
+    if (slot >= 0) {
+        pm = ck.m;
+        pl = ck.l;
+        pacc = ck.acc;
+    }
     const int lane = lane_id();
     const int ql0 = (threadIdx.x / kWave) * kOwn;  // first owned row inside the tile row
     const int64_t q0 = int64_t(I) * T + ql0;
@@ -745,11 +942,12 @@ __global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t
         const int64_t q = q0 + 32 * b + (lane & 31);
         const float lt = pair_sum(l[b]);
         if (q >= n) continue;
+        const int64_t orow = out_row(q, I, slot, T);
         if (lane < 32) {
-            pm[q * H + h] = m[b];
-            pl[q * H + h] = lt;
+            pm[orow * H + h] = m[b];
+            pl[orow * H + h] = lt;
         }
-        float* o = pacc + (q * H + h) * D;
+        float* o = pacc + (orow * H + h) * D;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -781,14 +979,20 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
                                                 const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                                 const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
                                                 const float* __restrict__ LSE, float sl2, float* __restrict__ pa,
-                                                float* __restrict__ pb, float* __restrict__ pd) {
+                                                float* __restrict__ pb, float* __restrict__ pd, int64_t R,
+                                                TileChunks ck) {
     constexpr int W = T / 32;
     __shared__ __attribute__((aligned(16))) uint16_t sK[1][kStage * RS<D>::v];
     __shared__ __attribute__((aligned(16))) uint16_t sV[1][kStage * RS<D>::v];
     __shared__ __attribute__((aligned(16))) uint16_t sKt[1][D * kTS];
-    const int I = blockIdx.x, h = blockIdx.y;
-    const int64_t t0 = tile_rowptr[I], t1 = tile_rowptr[I + 1];
-    if (t0 == t1) return;
+    const int h = blockIdx.y;
+    int64_t I, t0, t1, slot;
+    if (!tile_chunk(ck, tile_rowptr, R, blockIdx.x, I, t0, t1, slot)) return;
+    if (slot >= 0) {
+        pa = ck.acc;
+        pb = ck.acc2;
+        pd = ck.m;
+    }
     const int lane = lane_id();
     const int ql0 = (threadIdx.x / kWave) * kOwn;
     const int64_t q0 = int64_t(I) * T + ql0;
@@ -875,7 +1079,8 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
         const int64_t q = q0 + 32 * b + (lane & 31);
         const float ds = pair_sum(dsum[b]);
         if (q >= n) continue;
-        if (lane < 32) pd[q * H + h] = ds;
+        const int64_t orow = out_row(q, I, slot, T);
+        if (lane < 32) pd[orow * H + h] = ds;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -883,9 +1088,9 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
                 const int f = 32 * db + 8 * j + 4 * (lane >> 5);
                 const f32x16_t& x = accA[b][db];
                 const f32x16_t& y = accB[b][db];
-                *reinterpret_cast<float4*>(pa + (q * H + h) * D + f) =
+                *reinterpret_cast<float4*>(pa + (orow * H + h) * D + f) =
                     make_float4(x[4 * j], x[4 * j + 1], x[4 * j + 2], x[4 * j + 3]);
-                *reinterpret_cast<float4*>(pb + (q * H + h) * D + f) =
+                *reinterpret_cast<float4*>(pb + (orow * H + h) * D + f) =
                     make_float4(y[4 * j], y[4 * j + 1], y[4 * j + 2], y[4 * j + 3]);
             }
     }
@@ -903,7 +1108,8 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
                                                   const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                                   const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
                                                   const float* __restrict__ LSE, const float* __restrict__ Dv,
-                                                  float sl2, float* __restrict__ pdk, float* __restrict__ pdv) {
+                                                  float sl2, float* __restrict__ pdk, float* __restrict__ pdv,
+                                                  TileChunks ck) {
     constexpr int W = T / 32;
     __shared__ __attribute__((aligned(16))) uint16_t sQ[1][kStage * RS<D>::v];
     __shared__ __attribute__((aligned(16))) uint16_t sG[1][kStage * RS<D>::v];
@@ -911,9 +1117,13 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
     __shared__ __attribute__((aligned(16))) uint16_t sGt[1][D * kTS];
     __shared__ __attribute__((aligned(16))) float sL[1][kStage];
     __shared__ __attribute__((aligned(16))) float sD[1][kStage];
-    const int J = blockIdx.x, h = blockIdx.y;
-    const int64_t u0 = tileT_ptr[J], u1 = tileT_ptr[J + 1];
-    if (u0 == u1) return;
+    const int h = blockIdx.y;
+    int64_t J, u0, u1, slot;
+    if (!tile_chunk(ck, tileT_ptr, n_row_tiles, blockIdx.x, J, u0, u1, slot)) return;
+    if (slot >= 0) {
+        pdk = ck.acc;
+        pdv = ck.acc2;
+    }
     const int lane = lane_id();
     const int kl0 = (threadIdx.x / kWave) * kOwn;  // first owned key inside the tile column
     const int64_t k0 = int64_t(J) * T + kl0;
@@ -1036,6 +1246,7 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
     for (int b = 0; b < 2; ++b) {
         const int64_t key = k0 + 32 * b + (lane & 31);
         if (key >= n) continue;
+        const int64_t orow = out_row(key, J, slot, T);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -1043,9 +1254,9 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
                 const int f = 32 * db + 8 * j + 4 * (lane >> 5);
                 const f32x16_t& x = dk[b][db];
                 const f32x16_t& y = dv[b][db];
-                *reinterpret_cast<float4*>(pdk + (key * H + h) * D + f) =
+                *reinterpret_cast<float4*>(pdk + (orow * H + h) * D + f) =
                     make_float4(x[4 * j], x[4 * j + 1], x[4 * j + 2], x[4 * j + 3]);
-                *reinterpret_cast<float4*>(pdv + (key * H + h) * D + f) =
+                *reinterpret_cast<float4*>(pdv + (orow * H + h) * D + f) =
                     make_float4(y[4 * j], y[4 * j + 1], y[4 * j + 2], y[4 * j + 3]);
             }
     }
@@ -1091,20 +1302,30 @@ gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, 
 template <int D>
 gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                          float sl2, TilePartials tp, hipStream_t s) {
-    const dim3 grid(unsigned(p->n_row_tiles), unsigned(H));
+    gt_status st = tile_chunk_plan(p, p->tile_rowptr, tp.ck, s);
+    if (st != GT_OK) return st;
+    const dim3 grid(unsigned(tp.ck.max_chunks), unsigned(H));
     GT_TILES_T((k_tiles_fwd<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
-                                                       sl2, tp.m, tp.l, tp.acc)));
+                                                       sl2, tp.m, tp.l, tp.acc, p->n_row_tiles, tp.ck)));
     GT_LAUNCH_CHECK("tiles_fwd_bf16");
+    GT_TILES_T((k_tiles_merge_fwd<D, TT><<<merge_grid(p->n_row_tiles, H, TT, D), kMergeThreads, 0, s>>>(
+        p->n, H, tp.ck, tp.m, tp.l, tp.acc)));
+    GT_LAUNCH_CHECK("tiles_merge_fwd_bf16");
     return GT_OK;
 }
 
 template <int D>
 gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                         const uint16_t* dO, const float* LSE, float sl2, TilePartials dq, hipStream_t s) {
-    const dim3 grid(unsigned(p->n_row_tiles), unsigned(H));
+    gt_status st = tile_chunk_plan(p, p->tile_rowptr, dq.ck, s);
+    if (st != GT_OK) return st;
+    const dim3 grid(unsigned(dq.ck.max_chunks), unsigned(H));
     GT_TILES_T((k_tiles_dq<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
-                                                      dO, LSE, sl2, dq.acc, dq.acc2, dq.m)));
+                                                      dO, LSE, sl2, dq.acc, dq.acc2, dq.m, p->n_row_tiles, dq.ck)));
     GT_LAUNCH_CHECK("tiles_dq_bf16");
+    GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(p->n_row_tiles, H, TT, D), kMergeThreads, 0, s>>>(
+        p->n, H, dq.ck, dq.acc, dq.acc2, dq.m)));
+    GT_LAUNCH_CHECK("tiles_merge_dq_bf16");
     return GT_OK;
 }
 
@@ -1112,11 +1333,16 @@ template <int D>
 gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                           const uint16_t* dO, const float* LSE, const float* Dv, float sl2, TilePartials dk,
                           TilePartials dv, hipStream_t s) {
-    const dim3 grid(unsigned(p->n_row_tiles), unsigned(H));
+    gt_status st = tile_chunk_plan(p, p->tileT_ptr, dk.ck, s);
+    if (st != GT_OK) return st;
+    const dim3 grid(unsigned(dk.ck.max_chunks), unsigned(H));
     GT_TILES_T((k_tiles_dkdv<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->n_row_tiles, p->tileT_ptr, p->tileT_idx,
                                                         p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv, sl2,
-                                                        dk.acc, dv.acc)));
+                                                        dk.acc, dv.acc, dk.ck)));
     GT_LAUNCH_CHECK("tiles_dkdv_bf16");
+    GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(p->n_row_tiles, H, TT, D), kMergeThreads, 0, s>>>(
+        p->n, H, dk.ck, dk.acc, dv.acc, nullptr)));
+    GT_LAUNCH_CHECK("tiles_merge_dkdv_bf16");
     return GT_OK;
 }
 

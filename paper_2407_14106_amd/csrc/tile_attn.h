@@ -4,8 +4,31 @@
 #pragma once
 
 #include "attn_common.h"
+#include "prim.h"
 
 namespace gt {
+
+// The dense tiles of a tile row (tile column) are dealt out in chunks of CH
+// tiles, one workgroup each, so a row of many dense tiles (the hubs of a
+// power-law graph) is spread over the chip.  The first chunk of a row writes
+// the row's partial state; the others write extra slots, which a merge then
+// folds in (in slot order, so the result is deterministic).
+struct TileChunks {
+    int64_t* chunk_off = nullptr;  // [R + 1]: first chunk of each tile row (column)
+    int64_t* extra_off = nullptr;  // [R + 1]: first extra slot of each tile row (column)
+    int32_t* counts = nullptr;     // [R]: chunks per row
+    int32_t* ecounts = nullptr;    // [R]: extra slots per row
+    ScanTmp scan;
+    int CH = 1;
+    int64_t max_chunks = 0;
+    float* m = nullptr;     // extra slots: [slots, T, H] (forward max, or the dQ pass's D sum)
+    float* l = nullptr;     // [slots, T, H] forward only
+    float* acc = nullptr;   // [slots, T, H, d]
+    float* acc2 = nullptr;  // [slots, T, H, d] dQ pass only
+};
+
+constexpr int kTileChunkMin = 4;        // tiles per chunk, at least
+constexpr int64_t kTileChunks = 512;    // the chunk size grows so that extra slots stay below this
 
 // Per-(node, head) partial state left by the dense tiles of a tile row (or
 // tile column).  `ptr` is tile_rowptr (or tileT_ptr): a node has a partial iff
@@ -17,6 +40,7 @@ struct TilePartials {
     float* l = nullptr;     // [n, H] forward: running sum
     float* acc = nullptr;   // [n, H, d] unnormalised output / gradient sums (dQ: A)
     float* acc2 = nullptr;  // [n, H, d] dQ only: B
+    TileChunks ck;
     __device__ __forceinline__ bool has(int64_t node) const {
         if (!ptr) return false;
         const int64_t I = node >> tshift;
@@ -32,6 +56,28 @@ struct TileBwdPartials {
 
 inline int tile_shift(int T) { return T == 128 ? 7 : 6; }
 
+// Carve the chunk plan and its extra slots (floats per slot row: per_row) out of the workspace.
+inline TileChunks tile_chunks(Ws& ws, const gt_tiles* p, int64_t per_row_m, int64_t per_row_acc, bool with_l,
+                              bool with_acc2) {
+    TileChunks c;
+    const int64_t R = p->n_row_tiles > 0 ? p->n_row_tiles : 1;
+    const int64_t nd = p->n_dense;
+    c.CH = int(cdiv(nd, kTileChunks) > kTileChunkMin ? cdiv(nd, kTileChunks) : kTileChunkMin);
+    const int64_t slots = nd / c.CH + 1;
+    c.max_chunks = (R < nd ? R : nd) + nd / c.CH + 1;
+    c.chunk_off = ws.take<int64_t>(R + 1);
+    c.extra_off = ws.take<int64_t>(R + 1);
+    c.counts = ws.take<int32_t>(R);
+    c.ecounts = ws.take<int32_t>(R);
+    c.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(R)));
+    const int64_t rows = slots * p->T;
+    c.m = ws.take<float>(size_t(rows * per_row_m));
+    if (with_l) c.l = ws.take<float>(size_t(rows * per_row_m));
+    c.acc = ws.take<float>(size_t(rows * per_row_acc));
+    if (with_acc2) c.acc2 = ws.take<float>(size_t(rows * per_row_acc));
+    return c;
+}
+
 // Carve the partial buffers out of the workspace (nothing when no tile is dense).
 inline TilePartials tile_partials_fwd(Ws& ws, const gt_tiles* p, int H, int D) {
     TilePartials t;
@@ -41,6 +87,7 @@ inline TilePartials tile_partials_fwd(Ws& ws, const gt_tiles* p, int H, int D) {
     t.m = ws.take<float>(size_t(p->n) * H);
     t.l = ws.take<float>(size_t(p->n) * H);
     t.acc = ws.take<float>(size_t(p->n) * H * D);
+    t.ck = tile_chunks(ws, p, H, int64_t(H) * D, true, false);
     return t;
 }
 
@@ -53,12 +100,14 @@ inline TileBwdPartials tile_partials_bwd(Ws& ws, const gt_tiles* p, int H, int D
         b.dq.acc = ws.take<float>(size_t(p->n) * H * D);
         b.dq.acc2 = ws.take<float>(size_t(p->n) * H * D);
         b.dq.m = ws.take<float>(size_t(p->n) * H);
+        b.dq.ck = tile_chunks(ws, p, H, int64_t(H) * D, false, true);
     }
     if (cols) {
         b.dk.ptr = b.dv.ptr = p->tileT_ptr;
         b.dk.tshift = b.dv.tshift = tile_shift(p->T);
         b.dk.acc = ws.take<float>(size_t(p->n) * H * D);
         b.dv.acc = ws.take<float>(size_t(p->n) * H * D);
+        b.dk.ck = tile_chunks(ws, p, 0, int64_t(H) * D, false, true);  // acc: dk slots, acc2: dv slots
     }
     return b;
 }

@@ -121,6 +121,25 @@ def test_long_rows_and_columns(gt):
         run_case(gt, rowptr, col, H, d, dtype, taus=(0, 5000, CSR_ONLY), seed=H + d)
 
 
+def test_hub_tile_rows_and_columns_in_chunks(gt):
+    # 96 hub rows attend to half of all nodes and 64 hub columns are attended by half of all rows, over a sparse
+    # background; n = 2117 is ragged for both tile sizes.  Each hub tile row (column) holds ~17-34 dense tiles,
+    # so its dense tiles are dealt out to several workgroups whose partial states are merged.
+    n = 2117
+    rng = np.random.default_rng(5)
+    hub_r = np.repeat(np.arange(96), n // 2)
+    hub_rc = rng.integers(0, n, size=len(hub_r))
+    hub_c = np.repeat(np.arange(200, 264), n // 2)
+    hub_cr = rng.integers(0, n, size=len(hub_c))
+    bu, bv = rng.integers(0, n, size=6 * n), rng.integers(0, n, size=6 * n)
+    u = np.concatenate([hub_r, hub_cr, bu])
+    v = np.concatenate([hub_rc, hub_c, bv])
+    rowptr, col = csr_from_pairs(n, u, v, symmetric=False, self_loops=True)
+    for T in (64, 128):
+        run_case(gt, rowptr, col, 4, 64, "bf16", taus=(0, 50_000), T=T, seed=T + 1)
+    run_case(gt, rowptr, col, 8, 32, "bf16", taus=(10_000,), T=128, seed=9)
+
+
 def test_bitwise_deterministic(gt):
     w = make_workload("c4", 0.01)
     g = w.graph
