@@ -18,14 +18,32 @@ __global__ void k_new_degrees(int64_t n, const int64_t* rowptr, const int32_t* p
 }
 
 // One wavefront per old row: every edge (u, c) becomes key (iperm[u] << B) | iperm[c].
+// Rows of more than kLongRow edges are left to k_edge_keys_long.
 __global__ __launch_bounds__(256) void k_edge_keys(int64_t n, const int64_t* rowptr, const int32_t* col,
                                                    const int32_t* iperm, int bits, uint64_t* keys) {
     const int lane = lane_id();
     const int64_t waves = int64_t(gridDim.x) * 4;
     for (int64_t u = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; u < n; u += waves) {
         const int64_t a = rowptr[u], b = rowptr[u + 1];
+        if (b - a > kLongRow) continue;
         const uint64_t hi = uint64_t(uint32_t(iperm[u])) << bits;
         for (int64_t e = a + lane; e < b; e += kWave) keys[e] = hi | uint64_t(uint32_t(iperm[col[e]]));
+    }
+}
+
+// The long rows' keys, chunk by chunk over the grid.
+__global__ __launch_bounds__(256) void k_edge_keys_long(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                                        const int32_t* col, const int32_t* iperm, int bits,
+                                                        uint64_t* keys) {
+    const int64_t chunks = long_chunks_of(nnz);
+    for (int64_t c = blockIdx.x; c < chunks; c += gridDim.x) {
+        LongSeg seg[2];
+        const int k = long_segments(rowptr, n, nnz, c, seg);
+        for (int j = 0; j < k; ++j) {
+            const uint64_t hi = uint64_t(uint32_t(iperm[seg[j].row])) << bits;
+            for (int64_t e = seg[j].a + threadIdx.x; e < seg[j].b; e += blockDim.x)
+                keys[e] = hi | uint64_t(uint32_t(iperm[col[e]]));
+        }
     }
 }
 
@@ -111,6 +129,12 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     const int bits = bits_for(n);
     k_edge_keys<<<grid_for(n, 4, 65536), 256, 0, stream>>>(n, rowptr, col, iperm, bits, p.keys);
     GT_LAUNCH_CHECK("permute_keys");
+    if (nnz > kLongRow) {
+        const int64_t ch = long_chunks_of(nnz);
+        k_edge_keys_long<<<unsigned(ch < 8192 ? ch : 8192), 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits,
+                                                                               p.keys);
+        GT_LAUNCH_CHECK("permute_keys_long");
+    }
     if (with_map && (st = iota_u32(p.vals, nnz, stream)) != GT_OK) return st;
     if ((st = radix_sort_u64(p.keys, p.vals, nnz, 2 * bits, p.sort, stream)) != GT_OK) return st;
     k_key_cols<<<grid_for(nnz, 256, 16384), 256, 0, stream>>>(nnz, p.keys, (uint64_t(1) << bits) - 1, col_out);

@@ -48,6 +48,58 @@ inline int bits_for(int64_t n) {
     return b;
 }
 
+// ---- long rows, spread over the grid.
+// Rows of more than kLongRow entries are handled by a pass of their own that cuts
+// the CSR's entry range into chunks of kLongRow entries.  A long row is longer
+// than a chunk, so at most two long rows overlap a chunk: the row of its first
+// entry and the row of its last entry.
+constexpr int64_t kLongRow = 2048;
+
+__host__ __device__ inline int64_t long_chunks_of(int64_t nnz) { return (nnz + kLongRow - 1) / kLongRow; }
+
+// The row r with rowptr[r] <= e < rowptr[r + 1], for 0 <= e < rowptr[n]
+// (empty rows are skipped); stays in [0, n - 1] for any rowptr.
+__device__ __forceinline__ int64_t row_of(const int64_t* __restrict__ rowptr, int64_t n, int64_t e) {
+    int64_t lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (rowptr[mid] <= e) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+struct LongSeg {
+    int64_t row;   // the row
+    int64_t a, b;  // its entries inside the chunk, [a, b)
+    int s;         // 0: the row of the chunk's first entry, 1: of its last
+};
+
+// The segments of long rows inside chunk c of a CSR with nnz entries; returns
+// their number (0, 1 or 2).  Entry bounds are clamped to the chunk, so an
+// invalid rowptr still only yields entries in [0, nnz).
+__device__ __forceinline__ int long_segments(const int64_t* __restrict__ rowptr, int64_t n, int64_t nnz, int64_t c,
+                                             LongSeg seg[2]) {
+    const int64_t e0 = c * kLongRow, e1 = e0 + kLongRow < nnz ? e0 + kLongRow : nnz;
+    int k = 0;
+    if (e0 >= e1 || n <= 0) return 0;
+    const int64_t ra = row_of(rowptr, n, e0), rb = row_of(rowptr, n, e1 - 1);
+    const int64_t rows[2] = {ra, rb};
+    for (int s = 0; s < 2; ++s) {
+        const int64_t r = rows[s];
+        if (s == 1 && rb == ra) break;
+        const int64_t p = rowptr[r], q = rowptr[r + 1];
+        if (q - p <= kLongRow) continue;
+        LongSeg g;
+        g.row = r;
+        g.a = p > e0 ? p : e0;
+        g.b = q < e1 ? q : e1;
+        g.s = s;
+        if (g.a < g.b) seg[k++] = g;
+    }
+    return k;
+}
+
 // ---- CSR validation: accumulates error bits into *flags (one uint32, zeroed by the caller).
 enum : uint32_t { kBadRowptr = 1u, kOutOfRange = 2u, kUnsorted = 4u, kDuplicate = 8u };
 gt_status launch_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, uint32_t* flags,

@@ -304,9 +304,10 @@ gt_status radix_sort_u64(uint64_t* keys, uint32_t* values, int64_t n, int key_bi
 // =========================================================== CSR validation
 
 // Rows of up to kValidateShort entries are checked by one thread each; the
-// wavefront takes every longer row of its batch together, its lanes striding
-// the row 64 entries apart and comparing each entry with the one before it
-// in memory, so a row that holds every node is not left to one thread.
+// wavefront takes every longer row of its batch up to kLongRow entries
+// together, its lanes striding the row 64 entries apart and comparing each
+// entry with the one before it in memory.  Longer rows (a node adjacent to
+// every node) are checked chunk by chunk over the whole grid.
 constexpr int64_t kValidateShort = 256;
 
 __global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
@@ -320,14 +321,16 @@ __global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, co
     // wave-uniform loop: every lane of a wavefront runs the same number of rounds
     for (int64_t base = int64_t(blockIdx.x) * blockDim.x + (threadIdx.x - lane); base < n; base += stride) {
         const int64_t i = base + lane;
-        bool long_row = false;
+        bool mid_row = false;
         int64_t a = 0, b = 0;
         if (i < n) {
             a = rowptr[i];
             b = rowptr[i + 1];
             if (a > b) f |= kUnsorted;
             else if (a < 0 || b > nnz) f |= kOutOfRange;
-            else if (b - a > kValidateShort) long_row = true;
+            else if (b - a > kLongRow) {
+                // checked by k_validate_long
+            } else if (b - a > kValidateShort) mid_row = true;
             else {
                 int64_t prev = -1;
                 for (int64_t e = a; e < b; ++e) {
@@ -339,7 +342,7 @@ __global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, co
                 }
             }
         }
-        uint64_t pending = __ballot(long_row);
+        uint64_t pending = __ballot(mid_row);
         while (pending) {
             const int src = __builtin_ctzll(pending);
             pending &= pending - 1;
@@ -359,12 +362,41 @@ __global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, co
     if (f) atomicOr(flags, f);
 }
 
+// Rows of more than kLongRow entries, one chunk of the entry range per round.
+__global__ __launch_bounds__(256) void k_validate_long(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                                       const int32_t* col, uint32_t* flags) {
+    uint32_t f = 0;
+    const int64_t chunks = long_chunks_of(nnz);
+    for (int64_t c = blockIdx.x; c < chunks; c += gridDim.x) {
+        LongSeg seg[2];
+        const int k = long_segments(rowptr, n, nnz, c, seg);
+        for (int j = 0; j < k; ++j) {
+            const int64_t first = rowptr[seg[j].row];  // the row's first entry (negative only if rowptr is bad)
+            for (int64_t e = seg[j].a + threadIdx.x; e < seg[j].b; e += blockDim.x) {
+                const int64_t x = col[e];
+                if (x < 0 || x >= n) f |= kOutOfRange;
+                if (e > first && e > 0) {
+                    const int64_t prev = col[e - 1];
+                    if (x == prev) f |= kDuplicate;
+                    else if (x < prev) f |= kUnsorted;
+                }
+            }
+        }
+    }
+    if (f) atomicOr(flags, f);
+}
+
 gt_status launch_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, uint32_t* flags,
                               hipStream_t s) {
     gt_status st = fill_u32(flags, 1, 0, s);
     if (st != GT_OK) return st;
     k_validate_csr<<<grid_for(n > 0 ? n : 1, 256, 4096), 256, 0, s>>>(n, nnz, rowptr, col, flags);
     GT_LAUNCH_CHECK("validate_csr");
+    if (n > 0 && nnz > kLongRow) {
+        k_validate_long<<<unsigned(long_chunks_of(nnz) < 4096 ? long_chunks_of(nnz) : 4096), 256, 0, s>>>(
+            n, nnz, rowptr, col, flags);
+        GT_LAUNCH_CHECK("validate_long");
+    }
     return GT_OK;
 }
 

@@ -5,8 +5,12 @@
 // in LDS (R <= 16384 columns: 64 KiB), so counting touches only the edges of
 // the tile row.  The same kernel, run a second time with the output offsets
 // known, writes the (I, J)-sorted dense tile list, the tile bit masks and the
-// remainder CSR.  The remainder's transpose and the column-grouped tile list
-// come from stable radix sorts, so every output is deterministic.
+// remainder CSR.  Rows of more than kLongRow edges (hubs, a global token) are
+// left out of the tile row's workgroup: the count pass publishes each tile
+// row's dense/sparse split as a bit set, and their edges are counted and
+// written chunk by chunk over the whole grid.  The remainder's transpose and
+// the column-grouped tile list come from stable radix sorts, so every output
+// is deterministic.
 #include "prim.h"
 
 namespace gt {
@@ -15,6 +19,28 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kMaxR = 16384;
 constexpr uint32_t kDense = 0x80000000u;
+constexpr int kHash = 256;  // LDS slots that gather the remainder column counts of a workgroup
+constexpr uint32_t kEmpty = 0xFFFFFFFFu;
+
+__device__ __forceinline__ int hash_slot(uint32_t c) { return int((c * 2654435761u) >> 24); }
+
+// Exclusive prefix of a 0/1 flag over the workgroup, in thread order; *total = the sum.
+__device__ __forceinline__ int64_t block_flag_scan(bool flag, int64_t* s, int64_t* total) {
+    const uint64_t b = __ballot(flag);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) s[w] = __popcll(b);
+    __syncthreads();
+    int64_t before = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kThreads / kWave; ++i) {
+        const int64_t t = s[i];
+        if (i < w) before += t;
+        tot += t;
+    }
+    __syncthreads();
+    *total = tot;
+    return before + __popcll(b & lanemask_lt());
+}
 
 __device__ __forceinline__ int64_t block_exscan_i64(int64_t v, int64_t* s, int64_t* total) {
     const int lane = lane_id();
@@ -41,16 +67,27 @@ __device__ __forceinline__ int64_t block_exscan_i64(int64_t v, int64_t* s, int64
 
 // kFill = false: dense tiles per tile row, remainder degree per row.
 // kFill = true: the plan arrays (offsets from the count pass).
+// The count pass also publishes the split of tile row I for the long rows:
+// bit J of dense_bits[I * W + J / 32] marks a dense tile, dense_pre[I * W + w]
+// counts the dense tiles in words before w (W = ceil(R / 32)).
 template <bool kFill>
 __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* rowptr, const int32_t* col, int T,
                                                     int R, uint32_t tau_ppm, int32_t* dense_per_tilerow,
                                                     int32_t* sp_deg, const int64_t* tile_rowptr, int32_t* tile_col,
                                                     int32_t* tile_nnz, uint32_t* tile_mask,
                                                     const int64_t* sp_rowptr, int32_t* sp_col,
-                                                    uint32_t* sp_colkey, uint32_t* sp_rowval, uint32_t* sp_colcnt) {
+                                                    uint32_t* sp_colkey, uint32_t* sp_rowval, uint32_t* sp_colcnt,
+                                                    int W, uint32_t* dense_bits, uint32_t* dense_pre) {
     __shared__ uint32_t s_cnt[kMaxR];
     __shared__ int64_t s_red[kThreads / kWave];
+    __shared__ uint32_t s_hkey[kHash], s_hval[kHash];
     const int I = blockIdx.x;
+    if (!kFill) {
+        for (int j = threadIdx.x; j < kHash; j += kThreads) {
+            s_hkey[j] = kEmpty;
+            s_hval[j] = 0;
+        }
+    }
     const int64_t r0 = int64_t(I) * T;
     const int64_t r1 = r0 + T < n ? r0 + T : n;
     const int64_t rows = r1 - r0;
@@ -77,6 +114,25 @@ __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* ro
     const int64_t before = block_exscan_i64(mine, s_red, &total);
     if (!kFill) {
         if (threadIdx.x == 0) dense_per_tilerow[I] = int32_t(total);
+        __syncthreads();  // every classification is in s_cnt
+        // words 2t and 2t + 1 of the tile row's bit set (W <= 512)
+        uint32_t wd[2] = {0u, 0u};
+        for (int q = 0; q < 2; ++q) {
+            const int w = 2 * threadIdx.x + q;
+            if (w >= W) break;
+            for (int b = 0; b < 32; ++b) {
+                const int J = 32 * w + b;
+                if (J < R && (s_cnt[J] & kDense)) wd[q] |= 1u << b;
+            }
+        }
+        int64_t tot2;
+        const int64_t pre = block_exscan_i64(__popc(wd[0]) + __popc(wd[1]), s_red, &tot2);
+        for (int q = 0; q < 2; ++q) {
+            const int w = 2 * threadIdx.x + q;
+            if (w >= W) break;
+            dense_bits[int64_t(I) * W + w] = wd[q];
+            dense_pre[int64_t(I) * W + w] = uint32_t(pre + (q ? __popc(wd[0]) : 0));
+        }
     } else {
         const int64_t base = tile_rowptr[I];
         int64_t k = before;
@@ -98,6 +154,10 @@ __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* ro
     for (int64_t rl = threadIdx.x / kWave; rl < rows; rl += kThreads / kWave) {
         const int64_t i = r0 + rl;
         const int64_t a = rowptr[i], b = rowptr[i + 1];
+        if (b - a > kLongRow) {  // counted and written by the long-row kernels
+            if (!kFill && lane == 0) sp_deg[i] = 0;
+            continue;
+        }
         int64_t sp = 0;
         for (int64_t eb = a; eb < b; eb += kWave) {
             const int64_t e = eb + lane;
@@ -122,10 +182,133 @@ __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* ro
                     sp_rowval[pos] = uint32_t(i);
                 }
             }
-            if (!kFill && sparse) atomicAdd(&sp_colcnt[c], 1u);
+            if (!kFill && sparse) {
+                const int slot = hash_slot(uint32_t(c));
+                uint32_t k = s_hkey[slot];
+                if (k == kEmpty) k = atomicCAS(&s_hkey[slot], kEmpty, uint32_t(c));
+                if (k == kEmpty || k == uint32_t(c)) atomicAdd(&s_hval[slot], 1u);
+                else atomicAdd(&sp_colcnt[c], 1u);
+            }
             sp += __popcll(sb);
         }
         if (!kFill && lane == 0) sp_deg[i] = int32_t(sp);
+    }
+    if (!kFill) {
+        __syncthreads();
+        for (int j = threadIdx.x; j < kHash; j += kThreads)
+            if (s_hval[j]) atomicAdd(&sp_colcnt[s_hkey[j]], s_hval[j]);
+    }
+}
+
+__device__ __forceinline__ bool tile_is_dense(const uint32_t* __restrict__ bits, int J) {
+    return (bits[J >> 5] >> (J & 31)) & 1u;
+}
+
+// Count pass of the long rows: remainder degree (added to the zero the tile
+// row's workgroup left) and remainder column counts.
+__global__ __launch_bounds__(kThreads) void k_tiles_long_count(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                                               const int32_t* col, int T, int W,
+                                                               const uint32_t* dense_bits, int32_t* sp_deg,
+                                                               uint32_t* sp_colcnt) {
+    __shared__ int64_t s_red[kThreads / kWave];
+    const int64_t chunks = long_chunks_of(nnz);
+    for (int64_t ch = blockIdx.x; ch < chunks; ch += gridDim.x) {
+        LongSeg seg[2];
+        const int k = long_segments(rowptr, n, nnz, ch, seg);
+        for (int j = 0; j < k; ++j) {
+            const int64_t r = seg[j].row;
+            const uint32_t* bits = dense_bits + (r / T) * W;
+            int64_t total = 0;
+            for (int64_t e0 = seg[j].a; e0 < seg[j].b; e0 += kThreads) {
+                const int64_t e = e0 + threadIdx.x;
+                bool sparse = false;
+                if (e < seg[j].b) {
+                    const int c = col[e];
+                    sparse = !tile_is_dense(bits, c / T);
+                    if (sparse) atomicAdd(&sp_colcnt[c], 1u);
+                }
+                int64_t t;
+                block_flag_scan(sparse, s_red, &t);
+                total += t;
+            }
+            if (threadIdx.x == 0 && total) atomicAdd(&sp_deg[r], int32_t(total));
+        }
+    }
+}
+
+// Fill pass of the long rows, first step: remainder edges per (chunk, segment).
+__global__ __launch_bounds__(kThreads) void k_tiles_long_segs(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                                              const int32_t* col, int T, int W,
+                                                              const uint32_t* dense_bits, int32_t* segcnt) {
+    __shared__ int64_t s_red[kThreads / kWave];
+    const int64_t chunks = long_chunks_of(nnz);
+    for (int64_t ch = blockIdx.x; ch < chunks; ch += gridDim.x) {
+        LongSeg seg[2];
+        const int k = long_segments(rowptr, n, nnz, ch, seg);
+        for (int j = 0; j < k; ++j) {
+            const uint32_t* bits = dense_bits + (seg[j].row / T) * W;
+            int64_t total = 0;
+            for (int64_t e0 = seg[j].a; e0 < seg[j].b; e0 += kThreads) {
+                const int64_t e = e0 + threadIdx.x;
+                const bool sparse = e < seg[j].b && !tile_is_dense(bits, col[e] / T);
+                int64_t t;
+                block_flag_scan(sparse, s_red, &t);
+                total += t;
+            }
+            if (threadIdx.x == 0) segcnt[2 * ch + seg[j].s] = int32_t(total);
+        }
+    }
+}
+
+// Fill pass of the long rows, second step: mask bits and remainder entries.
+// segoff is the exclusive scan of segcnt; a row's entries before a segment are
+// segoff[segment] - segoff[the row's first segment].
+__global__ __launch_bounds__(kThreads) void k_tiles_long_fill(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                                              const int32_t* col, int T, int W,
+                                                              const uint32_t* dense_bits,
+                                                              const uint32_t* dense_pre, const int64_t* segoff,
+                                                              const int64_t* tile_rowptr, uint32_t* tile_mask,
+                                                              const int64_t* sp_rowptr, int32_t* sp_col,
+                                                              uint32_t* sp_colkey, uint32_t* sp_rowval) {
+    __shared__ int64_t s_red[kThreads / kWave];
+    const int64_t chunks = long_chunks_of(nnz);
+    const int wpr = T / 32;
+    for (int64_t ch = blockIdx.x; ch < chunks; ch += gridDim.x) {
+        LongSeg seg[2];
+        const int k = long_segments(rowptr, n, nnz, ch, seg);
+        for (int j = 0; j < k; ++j) {
+            const int64_t r = seg[j].row;
+            const int64_t I = r / T;
+            const uint32_t* bits = dense_bits + I * W;
+            const uint32_t* pre = dense_pre + I * W;
+            const int64_t first = rowptr[r];
+            const int64_t c0 = first / kLongRow;
+            const int s0 = first == c0 * kLongRow ? 0 : 1;
+            int64_t base = sp_rowptr[r] + segoff[2 * ch + seg[j].s] - segoff[2 * c0 + s0];
+            for (int64_t e0 = seg[j].a; e0 < seg[j].b; e0 += kThreads) {
+                const int64_t e = e0 + threadIdx.x;
+                const bool valid = e < seg[j].b;
+                const int c = valid ? col[e] : 0;
+                const int J = c / T;
+                const bool dense = valid && tile_is_dense(bits, J);
+                const bool sparse = valid && !dense;
+                int64_t t;
+                const int64_t before = block_flag_scan(sparse, s_red, &t);
+                if (dense) {
+                    const uint32_t wd = bits[J >> 5];
+                    const int64_t kk = tile_rowptr[I] + pre[J >> 5] + __popc(wd & ((1u << (J & 31)) - 1u));
+                    const int cl = c - J * T;
+                    atomicOr(&tile_mask[kk * int64_t(T) * wpr + (r - I * T) * wpr + cl / 32], 1u << (cl & 31));
+                }
+                if (sparse) {
+                    const int64_t pos = base + before;
+                    sp_col[pos] = c;
+                    sp_colkey[pos] = uint32_t(c);
+                    sp_rowval[pos] = uint32_t(r);
+                }
+                base += t;
+            }
+        }
     }
 }
 
@@ -160,6 +343,11 @@ struct TilesWs {
     int32_t* long_col_flag;
     int64_t* long_row_pos;
     int64_t* long_col_pos;
+    uint32_t* dense_bits;  // [R, W]: the dense/sparse split of each tile row
+    uint32_t* dense_pre;   // [R, W]: dense tiles before each word
+    int32_t* segcnt;       // [2 * long chunks]: remainder edges of each long-row segment
+    int64_t* segoff;       // [2 * long chunks + 1]
+    int W;
     ScanTmp scan;
     SortTmp sort;
 };
@@ -181,7 +369,13 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
     t.long_col_flag = ws.take<int32_t>(n1);
     t.long_row_pos = ws.take<int64_t>(n1 + 1);
     t.long_col_pos = ws.take<int64_t>(n1 + 1);
-    t.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1)));
+    t.W = int(cdiv(R, 32));
+    t.dense_bits = ws.take<uint32_t>(size_t(R * t.W));
+    t.dense_pre = ws.take<uint32_t>(size_t(R * t.W));
+    const int64_t segs = 2 * long_chunks_of(e1);
+    t.segcnt = ws.take<int32_t>(size_t(segs));
+    t.segoff = ws.take<int64_t>(size_t(segs + 1));
+    t.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1 > segs + 1 ? n1 + 1 : segs + 1)));
     t.sort = sort_tmp(ws, e1, 4, true);
     return t;
 }
@@ -202,15 +396,25 @@ gt_status check_common(const char* who, int64_t n, int64_t nnz, const int64_t* r
 // Count pass shared by gt_tiles_count and gt_build_tiles: dense tiles per tile
 // row (scanned into tile_rowptr), remainder degrees (scanned into sp_rowptr)
 // and the long-row / long-column flags and positions.
-gt_status count_pass(int64_t n, const int64_t* rowptr, const int32_t* col, int32_t T, uint32_t tau_ppm,
+inline unsigned long_grid(int64_t nnz) {
+    const int64_t c = long_chunks_of(nnz);
+    return unsigned(c < 8192 ? c : 8192);
+}
+
+gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T, uint32_t tau_ppm,
                      TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, hipStream_t stream) {
     gt_status st;
     const int R = int(cdiv(n, T));
     if ((st = fill_u32(t.colcnt, n, 0u, stream)) != GT_OK) return st;
     k_tiles<false><<<R, kThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg, nullptr,
                                                nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                               t.colcnt);
+                                               t.colcnt, t.W, t.dense_bits, t.dense_pre);
     GT_LAUNCH_CHECK("tiles_count");
+    if (nnz > kLongRow) {
+        k_tiles_long_count<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
+                                                                   t.sp_deg, t.colcnt);
+        GT_LAUNCH_CHECK("tiles_long_count");
+    }
     if ((st = exclusive_scan_i32(t.dense_per_tilerow, R, tile_rowptr, t.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(t.sp_deg, n, sp_rowptr, t.scan, stream)) != GT_OK) return st;
     const unsigned g = grid_for(n, 256, 8192);
@@ -249,7 +453,7 @@ extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowpt
     TilesWs t = carve(ws, n, nnz, T);
     if ((st = launch_validate_csr(n, nnz, rowptr, col, t.flags, stream)) != GT_OK) return st;
     if ((st = read_validation(t.flags, stream)) != GT_OK) return st;
-    if ((st = count_pass(n, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
+    if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
         return st;
     const int64_t R = plan->n_row_tiles;
     int64_t h[4] = {0, 0, 0, 0};
@@ -291,7 +495,7 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     }
     Ws ws(ws_ptr);
     TilesWs t = carve(ws, n, nnz, T);
-    if ((st = count_pass(n, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) != GT_OK)
+    if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) != GT_OK)
         return st;
     {
         const unsigned g = grid_for(n, 256, 8192);
@@ -308,18 +512,29 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     if ((st = fill_u32(plan->tile_mask, words, 0u, stream)) != GT_OK) return st;
     k_tiles<true><<<R, kThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
                                               plan->tile_col, plan->tile_nnz, plan->tile_mask, plan->sp_rowptr,
-                                              plan->sp_col, t.keys, t.vals, nullptr);
+                                              plan->sp_col, t.keys, t.vals, nullptr, t.W, nullptr, nullptr);
     GT_LAUNCH_CHECK("tiles_fill");
-    // remainder transpose: stable sort of (column, row) pairs by column
+    if (nnz > kLongRow) {
+        const int64_t segs = 2 * long_chunks_of(nnz);
+        if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.segcnt), segs, 0u, stream)) != GT_OK) return st;
+        k_tiles_long_segs<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
+                                                                  t.segcnt);
+        GT_LAUNCH_CHECK("tiles_long_segs");
+        if ((st = exclusive_scan_i32(t.segcnt, segs, t.segoff, t.scan, stream)) != GT_OK) return st;
+        k_tiles_long_fill<<<long_grid(nnz), kThreads, 0, stream>>>(
+            n, nnz, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.segoff, plan->tile_rowptr, plan->tile_mask,
+            plan->sp_rowptr, plan->sp_col, t.keys, t.vals);
+        GT_LAUNCH_CHECK("tiles_long_fill");
+    }
+    // remainder transpose: stable sort of (column, row) pairs by column; the
+    // count pass left the column counts in colcnt
     const int64_t m = plan->nnz_sparse;
-    if ((st = fill_u32(t.counts, n, 0u, stream)) != GT_OK) return st;
     if (m > 0) {
-        if ((st = count_keys(reinterpret_cast<const int32_t*>(t.keys), m, t.counts, stream)) != GT_OK) return st;
         if ((st = radix_sort_u32(t.keys, t.vals, m, bits_for(n), t.sort, stream)) != GT_OK) return st;
         k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, t.vals, plan->sp_row);
         GT_LAUNCH_CHECK("tiles_sp_row");
     }
-    if ((st = exclusive_scan_u32(t.counts, n, plan->sp_colptr, t.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_u32(t.colcnt, n, plan->sp_colptr, t.scan, stream)) != GT_OK) return st;
     // tiles grouped by column: stable sort of (J, tile index) by J
     const int64_t d = plan->n_dense;
     if ((st = fill_u32(t.counts, R, 0u, stream)) != GT_OK) return st;

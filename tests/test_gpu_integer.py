@@ -155,6 +155,30 @@ def test_validation_errors(gt):
     gt.validate_csr(rp, cl)
 
 
+def test_validation_errors_in_long_rows(gt):
+    # rows above 2,048 entries are checked chunk by chunk over the grid: plant each error at a chunk boundary
+    # (entries 2047/2048 of the CSR) or inside a long row that starts in the middle of a chunk
+    n = 6000
+    deg = np.zeros(n, np.int64)
+    deg[0], deg[1], deg[2] = 5000, 7, 3000
+    rowptr = np.concatenate([[0], np.cumsum(deg)])
+    good = np.concatenate([np.arange(5000), np.arange(7) * 3, np.arange(3000) * 2]).astype(np.int32)
+    rp, cl = dev_csr(rowptr, good)
+    gt.validate_csr(rp, cl)
+    b = int(rowptr[2])  # row 2 starts at entry 5007, inside the third chunk
+    cases = []
+    bad = good.copy(); bad[2047], bad[2048] = bad[2048], bad[2047]; cases.append((bad, gt.GT_ERR_UNSORTED))
+    bad = good.copy(); bad[2048] = bad[2047]; cases.append((bad, gt.GT_ERR_DUPLICATE))
+    bad = good.copy(); bad[b + 1] = bad[b]; cases.append((bad, gt.GT_ERR_DUPLICATE))
+    bad = good.copy(); bad[b + 2999] = 1; cases.append((bad, gt.GT_ERR_UNSORTED))
+    bad = good.copy(); bad[4999] = n + 5; cases.append((bad, gt.GT_ERR_OUT_OF_RANGE))
+    for col, code in cases:
+        rp, cl = dev_csr(rowptr, col)
+        with pytest.raises(gt.GtError) as e:
+            gt.validate_csr(rp, cl)
+        assert e.value.status == code
+
+
 def test_gather_scatter_rows(gt):
     x = torch.randn(1000, 8, 32, device="cuda").to(torch.bfloat16)
     perm = torch.randperm(1000, device="cuda").to(torch.int32)
