@@ -4,7 +4,9 @@
 // Rows are handled by size:
 //   deg <= 64          one wavefront per row, one neighbour label per lane;
 //                      multiplicities by an in-register all-pairs compare.
-//   64 < deg <= 4096   one workgroup per row, open-addressing count table in LDS.
+//   64 < deg <= 512    one wavefront per row, open-addressing count table in
+//                      the wavefront's share of LDS (no workgroup barriers).
+//   512 < deg <= 4096  one workgroup per row, open-addressing count table in LDS.
 //   4096 < deg <= 2^16 one workgroup per row, count table in the workspace.
 //   deg > 2^16         the whole grid (a global token attending to every node):
 //                      count table in the workspace filled by every workgroup,
@@ -22,6 +24,8 @@ namespace {
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kActivitySalt = 0xD6E8FEB86659FD93ull;
 constexpr int kWaveRowMax = 64;
+constexpr int kWaveTabRowMax = 512;
+constexpr int kWaveTab = 2 * kWaveTabRowMax;  // per-wavefront table entries
 constexpr int kLdsTable = 8192;      // entries (int32 key + uint32 count): 64 KiB
 constexpr int kLdsRowMax = kLdsTable / 2;
 constexpr int kBlock = 256;
@@ -58,7 +62,7 @@ __device__ __forceinline__ int wave_min_i32(int v) {
 // -------------------------------------------------------------- per-row classes
 
 __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
-                           int32_t* is_med, int32_t* is_big, int32_t* is_huge, int64_t* big_cap) {
+                           int32_t* is_wmed, int32_t* is_med, int32_t* is_big, int32_t* is_huge, int64_t* big_cap) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         // self-loop present?  rows are sorted: binary search for v.
@@ -71,7 +75,8 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
         const bool self = lo < b && col[lo] == v;
         const int64_t deg = b - a;
         deg_off[v] = uint32_t(deg - (self ? 1 : 0));
-        is_med[v] = (deg > kWaveRowMax && deg <= kLdsRowMax) ? 1 : 0;
+        is_wmed[v] = (deg > kWaveRowMax && deg <= kWaveTabRowMax) ? 1 : 0;
+        is_med[v] = (deg > kWaveTabRowMax && deg <= kLdsRowMax) ? 1 : 0;
         const bool big = deg > kLdsRowMax;
         is_big[v] = big && deg <= kHugeRow ? 1 : 0;
         is_huge[v] = deg > kHugeRow ? 1 : 0;
@@ -81,11 +86,13 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
     }
 }
 
-__global__ void k_compact(int64_t n, const int32_t* is_med, const int32_t* is_big, const int32_t* is_huge,
-                          const int64_t* pos_med, const int64_t* pos_big, const int64_t* pos_huge,
-                          const int64_t* cap_off, int32_t* med_list, int32_t* big_list, int64_t* big_off,
+__global__ void k_compact(int64_t n, const int32_t* is_wmed, const int32_t* is_med, const int32_t* is_big,
+                          const int32_t* is_huge, const int64_t* pos_wmed, const int64_t* pos_med,
+                          const int64_t* pos_big, const int64_t* pos_huge, const int64_t* cap_off,
+                          int32_t* wmed_list, int32_t* med_list, int32_t* big_list, int64_t* big_off,
                           int32_t* huge_list, int64_t* huge_off) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
+        if (is_wmed[v]) wmed_list[pos_wmed[v]] = int32_t(v);
         if (is_med[v]) med_list[pos_med[v]] = int32_t(v);
         if (is_big[v]) {
             big_list[pos_big[v]] = int32_t(v);
@@ -172,6 +179,37 @@ __device__ __forceinline__ int tab_load(const int* p) {
     return *p;
 }
 
+// Adds k to the count of label L in an open-addressing table of cap slots.
+__device__ __forceinline__ void tab_add(int* tk, int* tc, int64_t cap, int L, int k) {
+    int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
+    while (true) {
+        const int prev = atomicCAS(&tk[slot], -1, L);
+        if (prev == -1 || prev == L) {
+            atomicAdd(&tc[slot], k);
+            return;
+        }
+        slot = (slot + 1) & (cap - 1);
+    }
+}
+
+// Inserts the labels of one wavefront's 64 edges (L valid where `valid`): the
+// most frequent labels of the slice (once clusters form, most neighbours share
+// one) are peeled off by ballot and added once each, the rest lane by lane.
+// Must be reached by the whole wavefront.
+__device__ __forceinline__ void tab_add_wave(int* tk, int* tc, int64_t cap, bool valid, int L) {
+    bool pending = valid;
+    for (int it = 0; it < 3; ++it) {
+        const uint64_t m = __ballot(pending);
+        if (!m) return;
+        const int leader = __builtin_ctzll(m);
+        const int Ld = __shfl(L, leader, kWave);
+        const uint64_t same = __ballot(pending && L == Ld);
+        if (lane_id() == leader) tab_add(tk, tc, cap, Ld, __popcll(same));
+        if (pending && L == Ld) pending = false;
+    }
+    if (pending) tab_add(tk, tc, cap, L, 1);
+}
+
 // One workgroup per listed row.  Table: keys (label or -1) and counts, in LDS
 // (rows up to kLdsRowMax) or in the workspace (up to kHugeRow).
 template <bool kGlobal>
@@ -205,19 +243,12 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
         }
         if (kGlobal) __threadfence();
         __syncthreads();
-        for (int64_t e = a + threadIdx.x; e < b; e += kBlock) {
-            const int c = col[e];
-            if (c == v) continue;
-            const int L = lab_in[c];
-            int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
-            while (true) {
-                const int prev = atomicCAS(&tk[slot], -1, L);
-                if (prev == -1 || prev == L) {
-                    atomicAdd(&tc[slot], 1);
-                    break;
-                }
-                slot = (slot + 1) & (cap - 1);
-            }
+        // wave-uniform rounds: each wavefront takes 64 consecutive edges per round
+        for (int64_t base = a + (threadIdx.x & ~(kWave - 1)); base < b; base += kBlock) {
+            const int64_t e = base + lane_id();
+            const int c = e < b ? col[e] : int(v);
+            const bool valid = c != v;
+            tab_add_wave(tk, tc, cap, valid, valid ? lab_in[c] : -1);
         }
         if (kGlobal) __threadfence();
         __syncthreads();
@@ -255,6 +286,86 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
             if (cand != own) *flag_next = 1u;
         }
         __syncthreads();
+    }
+}
+
+// One wavefront per listed row (64 < deg <= kWaveTabRowMax), the same
+// function as k_lp_block with the count table in the wavefront's own slice of
+// LDS: the lanes of one wavefront meet only at wavefront-scope fences.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, const int64_t* list_len,
+                                                       const int64_t* rowptr, const int32_t* col,
+                                                       const int32_t* lab_in, int32_t* lab_out, uint64_t key,
+                                                       const uint32_t* flag_prev, uint32_t* flag_next) {
+    __shared__ int s_keys[kBlock / kWave][kWaveTab];
+    __shared__ int s_cnts[kBlock / kWave][kWaveTab];
+    const int w = threadIdx.x / kWave, lane = lane_id();
+    int* tk = s_keys[w];
+    int* tc = s_cnts[w];
+    const bool converged = *flag_prev == 0;
+    const int64_t len = *list_len;
+    const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
+    for (int64_t idx = int64_t(blockIdx.x) * (kBlock / kWave) + w; idx < len; idx += waves) {
+        const int64_t v = list[idx];
+        const int own = lab_in[v];
+        if (converged) {
+            if (lane == 0) lab_out[v] = own;
+            continue;
+        }
+        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        int cap = 1;
+        while (cap < 2 * (b - a)) cap <<= 1;  // <= kWaveTab
+        for (int s2 = lane; s2 < cap; s2 += kWave) {
+            tk[s2] = -1;
+            tc[s2] = 0;
+        }
+        wave_lds_sync();
+        for (int64_t base = a; base < b; base += kWave) {
+            const int64_t e = base + lane;
+            const int c = e < b ? col[e] : int(v);
+            const bool valid = c != v;
+            tab_add_wave(tk, tc, cap, valid, valid ? lab_in[c] : -1);
+        }
+        wave_lds_sync();
+        int best = 0, own_cnt = 0;
+        for (int s2 = lane; s2 < cap; s2 += kWave) {
+            const int k = tk[s2];
+            if (k < 0) continue;
+            const int c = tc[s2];
+            best = c > best ? c : best;
+            if (k == own) own_cnt = c;
+        }
+        best = wave_max(best);
+        own_cnt = wave_max(own_cnt);
+        int cand = own;
+        if (best > 0 && own_cnt != best) {
+            uint64_t hbest = ~0ull;
+            for (int s2 = lane; s2 < cap; s2 += kWave) {
+                const int k = tk[s2];
+                if (k < 0 || tc[s2] != best) continue;
+                const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
+                hbest = h < hbest ? h : hbest;
+            }
+            hbest = wave_min_u64(hbest);
+            int lbest = INT_MAX;
+            for (int s2 = lane; s2 < cap; s2 += kWave) {
+                const int k = tk[s2];
+                if (k < 0 || tc[s2] != best) continue;
+                if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
+                lbest = k < lbest ? k : lbest;
+            }
+            cand = wave_min_i32(lbest);
+        }
+        if (lane == 0) {
+            lab_out[v] = is_active(v, key) ? cand : own;
+            if (cand != own) *flag_next = 1u;
+        }
+        wave_lds_sync();  // every lane is done with the table before the next row clears it
     }
 }
 
@@ -347,19 +458,11 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
             __syncthreads();
             const int64_t e0 = a + c * kLdsRowMax;
             const int64_t e1 = e0 + kLdsRowMax < b ? e0 + kLdsRowMax : b;
-            for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-                const int cc = col[e];
-                if (cc == v) continue;
-                const int L = lab_in[cc];
-                int slot = int(mix64(uint64_t(uint32_t(L))) & uint64_t(kLdsTable - 1));
-                while (true) {
-                    const int prev = atomicCAS(&s_keys[slot], -1, L);
-                    if (prev == -1 || prev == L) {
-                        atomicAdd(&s_cnts[slot], 1);
-                        break;
-                    }
-                    slot = (slot + 1) & (kLdsTable - 1);
-                }
+            for (int64_t base = e0 + (threadIdx.x & ~(kWave - 1)); base < e1; base += kBlock) {
+                const int64_t e = base + lane_id();
+                const int cc = e < e1 ? col[e] : int(v);
+                const bool valid = cc != v;
+                tab_add_wave(s_keys, s_cnts, kLdsTable, valid, valid ? lab_in[cc] : -1);
             }
             __syncthreads();
             for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
@@ -481,14 +584,17 @@ struct ReorderWs {
     uint32_t* flags;
     int32_t* lab[2];
     uint32_t* deg_off;
+    int32_t* is_wmed;
     int32_t* is_med;
     int32_t* is_big;
     int32_t* is_huge;
     int64_t* big_cap;
+    int64_t* pos_wmed;
     int64_t* pos_med;
     int64_t* pos_big;
     int64_t* pos_huge;
     int64_t* cap_off;
+    int32_t* wmed_list;
     int32_t* med_list;
     int32_t* big_list;
     int64_t* big_off;
@@ -514,14 +620,17 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.lab[0] = ws.take<int32_t>(n1);
     r.lab[1] = ws.take<int32_t>(n1);
     r.deg_off = ws.take<uint32_t>(n1);
+    r.is_wmed = ws.take<int32_t>(n1);
     r.is_med = ws.take<int32_t>(n1);
     r.is_big = ws.take<int32_t>(n1);
     r.is_huge = ws.take<int32_t>(n1);
     r.big_cap = ws.take<int64_t>(n1);
+    r.pos_wmed = ws.take<int64_t>(n1 + 1);
     r.pos_med = ws.take<int64_t>(n1 + 1);
     r.pos_big = ws.take<int64_t>(n1 + 1);
     r.pos_huge = ws.take<int64_t>(n1 + 1);
     r.cap_off = ws.take<int64_t>(n1 + 1);
+    r.wmed_list = ws.take<int32_t>(n1);
     r.med_list = ws.take<int32_t>(n1);
     r.big_list = ws.take<int32_t>(n1);
     r.big_off = ws.take<int64_t>(n1);
@@ -575,14 +684,17 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if (st != GT_OK) return st;
 
     const unsigned g = grid_for(n, 256, 8192);
-    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_med, r.is_big, r.is_huge, r.big_cap);
+    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_wmed, r.is_med, r.is_big, r.is_huge,
+                                      r.big_cap);
     GT_LAUNCH_CHECK("reorder_classify");
+    if ((st = exclusive_scan_i32(r.is_wmed, n, r.pos_wmed, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_big, n, r.pos_big, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_huge, n, r.pos_huge, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
-    k_compact<<<g, 256, 0, stream>>>(n, r.is_med, r.is_big, r.is_huge, r.pos_med, r.pos_big, r.pos_huge, r.cap_off,
-                                     r.med_list, r.big_list, r.big_off, r.huge_list, r.huge_off);
+    k_compact<<<g, 256, 0, stream>>>(n, r.is_wmed, r.is_med, r.is_big, r.is_huge, r.pos_wmed, r.pos_med, r.pos_big,
+                                     r.pos_huge, r.cap_off, r.wmed_list, r.med_list, r.big_list, r.big_off,
+                                     r.huge_list, r.huge_off);
     GT_LAUNCH_CHECK("reorder_compact");
 
     if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
@@ -601,6 +713,9 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         int32_t* out = r.lab[(t + 1) & 1];
         k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
         GT_LAUNCH_CHECK("reorder_lp_wave");
+        k_lp_wavetab<<<1024, kBlock, 0, stream>>>(r.wmed_list, r.pos_wmed + n, rowptr, col, in, out, key,
+                                                  r.flags + t, r.flags + t + 1);
+        GT_LAUNCH_CHECK("reorder_lp_wavetab");
         k_lp_block<false><<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
                                                        r.flags + t, r.flags + t + 1, nullptr, nullptr, nullptr);
         GT_LAUNCH_CHECK("reorder_lp_lds");
