@@ -16,7 +16,8 @@
 namespace gt {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;      // the long-row kernels
+constexpr int kTileThreads = 1024;  // one workgroup per tile row: 16 wavefronts share its LDS count table
 constexpr int kMaxR = 16384;
 constexpr uint32_t kDense = 0x80000000u;
 constexpr int kHash = 256;  // LDS slots that gather the remainder column counts of a workgroup
@@ -55,7 +56,7 @@ __device__ __forceinline__ int64_t block_exscan_i64(int64_t v, int64_t* s, int64
     __syncthreads();
     int64_t before = 0, tot = 0;
 #pragma unroll
-    for (int i = 0; i < kThreads / kWave; ++i) {
+    for (int i = 0; i < kTileThreads / kWave; ++i) {
         const int64_t t = s[i];
         if (i < w) before += t;
         tot += t;
@@ -71,7 +72,7 @@ __device__ __forceinline__ int64_t block_exscan_i64(int64_t v, int64_t* s, int64
 // bit J of dense_bits[I * W + J / 32] marks a dense tile, dense_pre[I * W + w]
 // counts the dense tiles in words before w (W = ceil(R / 32)).
 template <bool kFill>
-__global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* rowptr, const int32_t* col, int T,
+__global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t* rowptr, const int32_t* col, int T,
                                                     int R, uint32_t tau_ppm, int32_t* dense_per_tilerow,
                                                     int32_t* sp_deg, const int64_t* tile_rowptr, int32_t* tile_col,
                                                     int32_t* tile_nnz, uint32_t* tile_mask,
@@ -79,11 +80,11 @@ __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* ro
                                                     uint32_t* sp_colkey, uint32_t* sp_rowval, uint32_t* sp_colcnt,
                                                     int W, uint32_t* dense_bits, uint32_t* dense_pre) {
     __shared__ uint32_t s_cnt[kMaxR];
-    __shared__ int64_t s_red[kThreads / kWave];
+    __shared__ int64_t s_red[kTileThreads / kWave];
     __shared__ uint32_t s_hkey[kHash], s_hval[kHash];
     const int I = blockIdx.x;
     if (!kFill) {
-        for (int j = threadIdx.x; j < kHash; j += kThreads) {
+        for (int j = threadIdx.x; j < kHash; j += kTileThreads) {
             s_hkey[j] = kEmpty;
             s_hval[j] = 0;
         }
@@ -91,14 +92,14 @@ __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* ro
     const int64_t r0 = int64_t(I) * T;
     const int64_t r1 = r0 + T < n ? r0 + T : n;
     const int64_t rows = r1 - r0;
-    for (int J = threadIdx.x; J < R; J += kThreads) s_cnt[J] = 0;
+    for (int J = threadIdx.x; J < R; J += kTileThreads) s_cnt[J] = 0;
     __syncthreads();
     const int64_t e0 = rowptr[r0], e1 = rowptr[r1];
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += kThreads) atomicAdd(&s_cnt[col[e] / T], 1u);
+    for (int64_t e = e0 + threadIdx.x; e < e1; e += kTileThreads) atomicAdd(&s_cnt[col[e] / T], 1u);
     __syncthreads();
     // classify; keep the count in the low bits
     int64_t mine = 0;
-    const int chunk = (R + kThreads - 1) / kThreads;
+    const int chunk = (R + kTileThreads - 1) / kTileThreads;
     const int j0 = threadIdx.x * chunk;
     const int j1 = j0 + chunk < R ? j0 + chunk : R;
     for (int J = j0; J < j1; ++J) {
@@ -151,7 +152,7 @@ __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* ro
     const int lane = lane_id();
     const uint64_t lt = lanemask_lt();
     const int wpr = T / 32;  // mask words per tile row
-    for (int64_t rl = threadIdx.x / kWave; rl < rows; rl += kThreads / kWave) {
+    for (int64_t rl = threadIdx.x / kWave; rl < rows; rl += kTileThreads / kWave) {
         const int64_t i = r0 + rl;
         const int64_t a = rowptr[i], b = rowptr[i + 1];
         if (b - a > kLongRow) {  // counted and written by the long-row kernels
@@ -195,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void k_tiles(int64_t n, const int64_t* ro
     }
     if (!kFill) {
         __syncthreads();
-        for (int j = threadIdx.x; j < kHash; j += kThreads)
+        for (int j = threadIdx.x; j < kHash; j += kTileThreads)
             if (s_hval[j]) atomicAdd(&sp_colcnt[s_hkey[j]], s_hval[j]);
     }
 }
@@ -406,7 +407,7 @@ gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_
     gt_status st;
     const int R = int(cdiv(n, T));
     if ((st = fill_u32(t.colcnt, n, 0u, stream)) != GT_OK) return st;
-    k_tiles<false><<<R, kThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg, nullptr,
+    k_tiles<false><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg, nullptr,
                                                nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                                t.colcnt, t.W, t.dense_bits, t.dense_pre);
     GT_LAUNCH_CHECK("tiles_count");
@@ -510,7 +511,7 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     }
     const int64_t words = plan->n_dense * int64_t(T) * (T / 32);
     if ((st = fill_u32(plan->tile_mask, words, 0u, stream)) != GT_OK) return st;
-    k_tiles<true><<<R, kThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
+    k_tiles<true><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
                                               plan->tile_col, plan->tile_nnz, plan->tile_mask, plan->sp_rowptr,
                                               plan->sp_col, t.keys, t.vals, nullptr, t.W, nullptr, nullptr);
     GT_LAUNCH_CHECK("tiles_fill");
