@@ -2,7 +2,8 @@
 // hashed partial activation, then a stable sort by (label, -degree, id).
 //
 // Rows are handled by size:
-//   deg <= 64          one wavefront per row, one neighbour label per lane;
+//   deg <= 16 / 32     four / two rows per wavefront, 16 / 32 lanes each;
+//   32 < deg <= 64     one wavefront per row; one neighbour label per lane,
 //                      multiplicities by an in-register all-pairs compare.
 //   64 < deg <= 512    one wavefront per row, open-addressing count table in
 //                      the wavefront's share of LDS (no workgroup barriers).
@@ -24,6 +25,7 @@ namespace {
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kActivitySalt = 0xD6E8FEB86659FD93ull;
 constexpr int kWaveRowMax = 64;
+constexpr int kSub16 = 16, kSub32 = 32;  // rows of up to 16 / 32 edges share a wavefront
 constexpr int kWaveTabRowMax = 512;
 constexpr int kWaveTab = 2 * kWaveTabRowMax;  // per-wavefront table entries
 constexpr int kLdsTable = 8192;      // entries (int32 key + uint32 count): 64 KiB
@@ -62,7 +64,8 @@ __device__ __forceinline__ int wave_min_i32(int v) {
 // -------------------------------------------------------------- per-row classes
 
 __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
-                           int32_t* is_wmed, int32_t* is_med, int32_t* is_big, int32_t* is_huge, int64_t* big_cap) {
+                           int32_t* is_s16, int32_t* is_s32, int32_t* is_wmed, int32_t* is_med, int32_t* is_big,
+                           int32_t* is_huge, int64_t* big_cap) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         // self-loop present?  rows are sorted: binary search for v.
@@ -75,6 +78,8 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
         const bool self = lo < b && col[lo] == v;
         const int64_t deg = b - a;
         deg_off[v] = uint32_t(deg - (self ? 1 : 0));
+        is_s16[v] = deg <= kSub16 ? 1 : 0;
+        is_s32[v] = (deg > kSub16 && deg <= kSub32) ? 1 : 0;
         is_wmed[v] = (deg > kWaveRowMax && deg <= kWaveTabRowMax) ? 1 : 0;
         is_med[v] = (deg > kWaveTabRowMax && deg <= kLdsRowMax) ? 1 : 0;
         const bool big = deg > kLdsRowMax;
@@ -86,12 +91,16 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
     }
 }
 
-__global__ void k_compact(int64_t n, const int32_t* is_wmed, const int32_t* is_med, const int32_t* is_big,
-                          const int32_t* is_huge, const int64_t* pos_wmed, const int64_t* pos_med,
-                          const int64_t* pos_big, const int64_t* pos_huge, const int64_t* cap_off,
-                          int32_t* wmed_list, int32_t* med_list, int32_t* big_list, int64_t* big_off,
-                          int32_t* huge_list, int64_t* huge_off) {
+__global__ void k_compact(int64_t n, const int32_t* is_s16, const int32_t* is_s32, const int32_t* is_wmed,
+                          const int32_t* is_med, const int32_t* is_big, const int32_t* is_huge,
+                          const int64_t* pos_s16, const int64_t* pos_s32, const int64_t* pos_wmed,
+                          const int64_t* pos_med, const int64_t* pos_big, const int64_t* pos_huge,
+                          const int64_t* cap_off, int32_t* s16_list, int32_t* s32_list, int32_t* wmed_list,
+                          int32_t* med_list, int32_t* big_list, int64_t* big_off, int32_t* huge_list,
+                          int64_t* huge_off) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
+        if (is_s16[v]) s16_list[pos_s16[v]] = int32_t(v);
+        if (is_s32[v]) s32_list[pos_s32[v]] = int32_t(v);
         if (is_wmed[v]) wmed_list[pos_wmed[v]] = int32_t(v);
         if (is_med[v]) med_list[pos_med[v]] = int32_t(v);
         if (is_big[v]) {
@@ -121,7 +130,7 @@ __global__ __launch_bounds__(kBlock) void k_lp_wave(int64_t n, const int64_t* ro
         }
         const int64_t a = rowptr[v];
         const int deg = int(rowptr[v + 1] - a);
-        if (deg > kWaveRowMax) continue;  // handled by the workgroup kernels
+        if (deg <= kSub32 || deg > kWaveRowMax) continue;  // handled by k_lp_sub and the workgroup kernels
         int c = lane < deg ? col[a + lane] : -1;
         const bool valid = lane < deg && c != v;
         const int L = valid ? lab_in[c] : -1;
@@ -143,6 +152,87 @@ __global__ __launch_bounds__(kBlock) void k_lp_wave(int64_t n, const int64_t* ro
             }
         }
         if (lane == 0) {
+            lab_out[v] = is_active(v, key) ? cand : own;
+            if (cand != own) *flag_next = 1u;
+        }
+    }
+}
+
+// Rows of at most S edges (S = 16 or 32), 64 / S rows per wavefront: the same
+// function as k_lp_wave with every reduction confined to the row's S lanes.
+template <int S>
+__device__ __forceinline__ int group_max_i32(int v) {
+#pragma unroll
+    for (int o = S / 2; o > 0; o >>= 1) {
+        const int w = __shfl_xor(v, o, kWave);
+        v = w > v ? w : v;
+    }
+    return v;
+}
+template <int S>
+__device__ __forceinline__ int group_min_i32(int v) {
+#pragma unroll
+    for (int o = S / 2; o > 0; o >>= 1) {
+        const int w = __shfl_xor(v, o, kWave);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+template <int S>
+__device__ __forceinline__ uint64_t group_min_u64(uint64_t v) {
+#pragma unroll
+    for (int o = S / 2; o > 0; o >>= 1) {
+        const uint64_t w = shfl_xor_u64(v, o);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+
+template <int S>
+__global__ __launch_bounds__(kBlock) void k_lp_sub(const int32_t* list, const int64_t* list_len,
+                                                   const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
+                                                   int32_t* lab_out, uint64_t key, const uint32_t* flag_prev,
+                                                   uint32_t* flag_next) {
+    constexpr int G = kWave / S;
+    const bool converged = *flag_prev == 0;
+    const int lane = lane_id(), sub = lane / S, sl = lane % S;
+    const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
+    const int64_t len = *list_len;
+    const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
+    for (int64_t base = (int64_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave) * G; base < len;
+         base += waves * G) {
+        const int64_t idx = base + sub;
+        const bool live = idx < len;
+        const int64_t v = live ? list[idx] : 0;
+        const int own = live ? lab_in[v] : -1;
+        if (converged) {
+            if (live && sl == 0) lab_out[v] = own;
+            continue;
+        }
+        int64_t a = 0;
+        int deg = 0;
+        if (live) {
+            a = rowptr[v];
+            deg = int(rowptr[v + 1] - a);
+        }
+        const int c = sl < deg ? col[a + sl] : -1;
+        const bool valid = sl < deg && c != v;
+        const int L = valid ? lab_in[c] : -1;
+        const int dmax = wave_max(deg);
+        int cnt = 0;
+        for (int k = 0; k < dmax; ++k) {
+            const int Lk = __shfl(L, sub * S + k, kWave);
+            cnt += (Lk == L) ? 1 : 0;
+        }
+        if (!valid) cnt = 0;
+        const int best = group_max_i32<S>(cnt);
+        const int own_cnt = __popcll(__ballot(valid && L == own) & gmask);
+        const bool top = valid && cnt == best && best > 0 && own_cnt != best;
+        const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
+        const uint64_t hmin = group_min_u64<S>(h);
+        const int lmin = group_min_i32<S>((top && h == hmin) ? L : INT_MAX);
+        const int cand = (best > 0 && own_cnt != best) ? lmin : own;
+        if (live && sl == 0) {
             lab_out[v] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
         }
@@ -584,16 +674,22 @@ struct ReorderWs {
     uint32_t* flags;
     int32_t* lab[2];
     uint32_t* deg_off;
+    int32_t* is_s16;
+    int32_t* is_s32;
     int32_t* is_wmed;
     int32_t* is_med;
     int32_t* is_big;
     int32_t* is_huge;
     int64_t* big_cap;
+    int64_t* pos_s16;
+    int64_t* pos_s32;
     int64_t* pos_wmed;
     int64_t* pos_med;
     int64_t* pos_big;
     int64_t* pos_huge;
     int64_t* cap_off;
+    int32_t* s16_list;
+    int32_t* s32_list;
     int32_t* wmed_list;
     int32_t* med_list;
     int32_t* big_list;
@@ -620,16 +716,22 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.lab[0] = ws.take<int32_t>(n1);
     r.lab[1] = ws.take<int32_t>(n1);
     r.deg_off = ws.take<uint32_t>(n1);
+    r.is_s16 = ws.take<int32_t>(n1);
+    r.is_s32 = ws.take<int32_t>(n1);
     r.is_wmed = ws.take<int32_t>(n1);
     r.is_med = ws.take<int32_t>(n1);
     r.is_big = ws.take<int32_t>(n1);
     r.is_huge = ws.take<int32_t>(n1);
     r.big_cap = ws.take<int64_t>(n1);
+    r.pos_s16 = ws.take<int64_t>(n1 + 1);
+    r.pos_s32 = ws.take<int64_t>(n1 + 1);
     r.pos_wmed = ws.take<int64_t>(n1 + 1);
     r.pos_med = ws.take<int64_t>(n1 + 1);
     r.pos_big = ws.take<int64_t>(n1 + 1);
     r.pos_huge = ws.take<int64_t>(n1 + 1);
     r.cap_off = ws.take<int64_t>(n1 + 1);
+    r.s16_list = ws.take<int32_t>(n1);
+    r.s32_list = ws.take<int32_t>(n1);
     r.wmed_list = ws.take<int32_t>(n1);
     r.med_list = ws.take<int32_t>(n1);
     r.big_list = ws.take<int32_t>(n1);
@@ -684,17 +786,20 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if (st != GT_OK) return st;
 
     const unsigned g = grid_for(n, 256, 8192);
-    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_wmed, r.is_med, r.is_big, r.is_huge,
-                                      r.big_cap);
+    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_s16, r.is_s32, r.is_wmed, r.is_med, r.is_big,
+                                      r.is_huge, r.big_cap);
     GT_LAUNCH_CHECK("reorder_classify");
+    if ((st = exclusive_scan_i32(r.is_s16, n, r.pos_s16, r.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(r.is_s32, n, r.pos_s32, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_wmed, n, r.pos_wmed, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_big, n, r.pos_big, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_huge, n, r.pos_huge, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
-    k_compact<<<g, 256, 0, stream>>>(n, r.is_wmed, r.is_med, r.is_big, r.is_huge, r.pos_wmed, r.pos_med, r.pos_big,
-                                     r.pos_huge, r.cap_off, r.wmed_list, r.med_list, r.big_list, r.big_off,
-                                     r.huge_list, r.huge_off);
+    k_compact<<<g, 256, 0, stream>>>(n, r.is_s16, r.is_s32, r.is_wmed, r.is_med, r.is_big, r.is_huge, r.pos_s16,
+                                     r.pos_s32, r.pos_wmed, r.pos_med, r.pos_big, r.pos_huge, r.cap_off, r.s16_list,
+                                     r.s32_list, r.wmed_list, r.med_list, r.big_list, r.big_off, r.huge_list,
+                                     r.huge_off);
     GT_LAUNCH_CHECK("reorder_compact");
 
     if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
@@ -707,12 +812,19 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     BigRows br{r.huge_list, r.pos_huge + n, r.huge_off, r.tab_keys, r.tab_cnts, r.big_best, r.big_own,
                r.big_hbest, r.big_lbest};
     const unsigned gw = grid_for(n, kBlock / kWave, 65536);
+    const unsigned gs = grid_for(n, kBlock / kWave * 2, 16384);
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
         const int32_t* in = r.lab[t & 1];
         int32_t* out = r.lab[(t + 1) & 1];
         k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
         GT_LAUNCH_CHECK("reorder_lp_wave");
+        k_lp_sub<kSub16><<<gs, kBlock, 0, stream>>>(r.s16_list, r.pos_s16 + n, rowptr, col, in, out, key,
+                                                    r.flags + t, r.flags + t + 1);
+        GT_LAUNCH_CHECK("reorder_lp_sub16");
+        k_lp_sub<kSub32><<<gs, kBlock, 0, stream>>>(r.s32_list, r.pos_s32 + n, rowptr, col, in, out, key,
+                                                    r.flags + t, r.flags + t + 1);
+        GT_LAUNCH_CHECK("reorder_lp_sub32");
         k_lp_wavetab<<<1024, kBlock, 0, stream>>>(r.wmed_list, r.pos_wmed + n, rowptr, col, in, out, key,
                                                   r.flags + t, r.flags + t + 1);
         GT_LAUNCH_CHECK("reorder_lp_wavetab");
