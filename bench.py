@@ -10,7 +10,8 @@ the host's cores ("cpu_baseline", timed before the GPU is used) and, with
 --tau-sweep, the same step at density thresholds 1%, 20% and the CSR-only
 control ("tau_sweep"); with --bias, the step with a per-edge additive bias
 ("edge_bias"); with --ecr, the paper's lossy cluster reformation and the step
-on the rewritten graph ("ecr").
+on the rewritten graph ("ecr").  "peaks" holds measured denominators beside
+the published ones (a 1 GiB device copy, a bf16 8192^3 matrix product).
 
 Default workload: 1,000,000-node stochastic block model, 1,000 log-normal
 blocks, average degree 30, 5% of edges across blocks, self-loops, random node
@@ -64,6 +65,7 @@ def parse():
     ap.add_argument("--ecr", action="store_true",
                     help="also time the paper's lossy cluster reformation (k = 8, d_b = 16) at 1x and 5x the graph "
                          "density and the step on the rewritten graph")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured copy and matrix-product rates")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB row copy (gt_gather_rows, identity order) 5 times: the reference "
                          "for scaling hardware byte counters")
@@ -217,6 +219,54 @@ def dense_layer(steps: int):
     }
 
 
+def measured_peaks():
+    """Measured denominators beside the published ones: a 1 GiB device-to-device copy (the library's row move in
+    identity order, and torch's copy) and a bf16 8192^3 matrix product through torch (hipBLASLt)."""
+    import torch
+
+    from paper_2407_14106_amd import gt
+
+    dev = torch.device("cuda:0")
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    def best_ms(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        out = []
+        for _ in range(reps):
+            a, b = ev(), ev()
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            out.append(a.elapsed_time(b))
+        return min(out)
+
+    rows = 1 << 21
+    x = torch.ones((rows, 256), dtype=torch.bfloat16, device=dev)
+    y = torch.empty_like(x)
+    perm = torch.arange(rows, dtype=torch.int32, device=dev)
+    moved = 2.0 * x.numel() * 2
+    lib_ms = best_ms(lambda: gt.gather_rows(x, perm))
+    torch_ms = best_ms(lambda: y.copy_(x))
+    del x, y, perm
+    m = 8192
+    A = torch.randn((m, m), device=dev).to(torch.bfloat16)
+    B = torch.randn((m, m), device=dev).to(torch.bfloat16)
+    mm_ms = best_ms(lambda: torch.matmul(A, B))
+    del A, B
+    return {
+        "hbm_spec_GBps": HBM_PEAK_GBS,
+        "hbm_copy_GBps": round(moved / (min(lib_ms, torch_ms) / 1e3) / 1e9, 1),
+        "copy_GBps_library_row_move": round(moved / (lib_ms / 1e3) / 1e9, 1),
+        "copy_GBps_torch": round(moved / (torch_ms / 1e3) / 1e9, 1),
+        "mfma_bf16_spec_TFLOPs": 2500.0,
+        "mfma_bf16_matmul_TFLOPs": round(2.0 * m ** 3 / (mm_ms / 1e3) / 1e12, 1),
+        "note": "copy: 1 GiB read + 1 GiB written, best of 5; matmul: torch.matmul bf16 8192^3 (hipBLASLt), best "
+                "of 5. The roofline fractions use the published peaks.",
+    }
+
+
 def tau_sweep(gt, rp, cl, Q, K, V, dO, scale, args, edge_heads, T):
     """Same step at other density thresholds: 1% (the diagonal tiles of the clusters go to the matrix cores),
     20% (none do) and above 1 (the CSR-only control: no tile can qualify)."""
@@ -348,7 +398,7 @@ def copy_probe():
         gt.gather_rows(x, perm)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe": {"rows": rows, "row_bytes": 512, "bytes_read": rows * 512 + 4 * rows,
-                                     "bytes_written": rows * 512, "launches": 5, "kernel": "k_move_rows"}}))
+                                     "bytes_written": rows * 512, "launches": 5, "kernel": "k_move_rows16"}}))
 
 
 def main():
@@ -537,6 +587,13 @@ def main():
     if not args.no_dense_layer:
         log("timing the full-attention layer ...")
         result["dense_layer"] = dense_layer(5)
+    if not args.no_peaks:
+        log("measuring copy and matrix-product rates ...")
+        pk = measured_peaks()
+        pk["roofline_achieved_over_copy"] = round(achieved / pk["hbm_copy_GBps"], 4)
+        if "dense_layer" in result:
+            pk["dense_fwd_over_matmul"] = round(result["dense_layer"]["fwd_TFLOPs"] / pk["mfma_bf16_matmul_TFLOPs"], 4)
+        result["peaks"] = pk
     if cpu is not None:
         result["cpu_baseline"] = cpu
     print(json.dumps(result), flush=True)

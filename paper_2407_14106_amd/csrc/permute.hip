@@ -67,6 +67,23 @@ __global__ __launch_bounds__(256) void k_move_small_rows(int64_t n, int32_t word
     }
 }
 
+// Rows of a multiple of 16 bytes: one 16-byte vector per lane, consecutive lanes
+// on consecutive vectors of a row (rows of 512 bytes: two per wavefront).
+template <bool kGather, typename I>
+__global__ __launch_bounds__(256) void k_move_rows16(I n, I vpr, const uint4* __restrict__ src,
+                                                     const int32_t* __restrict__ perm, uint4* __restrict__ dst) {
+    const I total = n * vpr;
+    const I stride = I(gridDim.x) * I(blockDim.x);
+    for (I x = I(blockIdx.x) * I(blockDim.x) + I(threadIdx.x); x < total; x += stride) {
+        const I r = x / vpr, w = x - r * vpr;
+        const I p = I(perm[r]);
+        if (kGather)
+            dst[x] = src[p * vpr + w];
+        else
+            dst[p * vpr + w] = src[x];
+    }
+}
+
 // One wavefront per row; dwords per lane.
 template <bool kGather>
 __global__ __launch_bounds__(256) void k_move_rows(int64_t n, int64_t words, const uint32_t* src,
@@ -194,6 +211,23 @@ static gt_status move_rows(bool gather, int64_t n, int64_t row_bytes, const void
             k_move_small_rows<false><<<gs, 256, 0, stream>>>(n, words, static_cast<const uint32_t*>(src), perm,
                                                                static_cast<uint32_t*>(dst));
         GT_LAUNCH_CHECK("move_small_rows");
+        return GT_OK;
+    }
+    const bool aligned = (reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 16 == 0;
+    if (row_bytes % 16 == 0 && aligned) {
+        const int64_t vpr = row_bytes / 16, total = n * vpr;
+        const unsigned gv = grid_for(total, 256, 16384);
+        const uint4* s4 = static_cast<const uint4*>(src);
+        uint4* d4 = static_cast<uint4*>(dst);
+        if (total < (int64_t(1) << 32)) {
+            const uint32_t n32 = uint32_t(n), v32 = uint32_t(vpr);
+            if (gather) k_move_rows16<true, uint32_t><<<gv, 256, 0, stream>>>(n32, v32, s4, perm, d4);
+            else k_move_rows16<false, uint32_t><<<gv, 256, 0, stream>>>(n32, v32, s4, perm, d4);
+        } else {
+            if (gather) k_move_rows16<true, int64_t><<<gv, 256, 0, stream>>>(n, vpr, s4, perm, d4);
+            else k_move_rows16<false, int64_t><<<gv, 256, 0, stream>>>(n, vpr, s4, perm, d4);
+        }
+        GT_LAUNCH_CHECK("move_rows16");
         return GT_OK;
     }
     const unsigned g = grid_for(n, 4, 65536);
