@@ -653,54 +653,91 @@ __device__ __forceinline__ int64_t out_row(int64_t q, int64_t I, int64_t slot, i
     return slot < 0 ? q : slot * T + (q - I * T);
 }
 
-// Both offsets in one workgroup (plans of up to kPlanOneBlock tile rows): each
-// thread sums a contiguous run of rows, an LDS scan over the threads, then the
-// runs are written out.
+// The plan in one workgroup (plans of up to kPlanOneBlock tile rows): each
+// thread sums a contiguous run of rows (chunks, extra slots, rows with extra
+// slots), a wavefront scan plus one pass over the wavefront totals, then the
+// runs are written out with the list of rows that have extra slots.
 constexpr int kPlanThreads = 1024;
+constexpr int kPlanWaves = kPlanThreads / kWave;
 constexpr int64_t kPlanOneBlock = int64_t(1) << 16;
+
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t x) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int64_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
 
 __global__ __launch_bounds__(kPlanThreads) void k_tile_chunk_plan1(int64_t R, const int64_t* __restrict__ ptr,
                                                                    int CH, int64_t* __restrict__ chunk_off,
-                                                                   int64_t* __restrict__ extra_off) {
-    __shared__ int64_t s_c[kPlanThreads], s_e[kPlanThreads];
-    const int t = threadIdx.x;
+                                                                   int64_t* __restrict__ extra_off,
+                                                                   int32_t* __restrict__ merge_rows,
+                                                                   uint32_t* __restrict__ merge_cnt) {
+    __shared__ int64_t s_w[3][kPlanWaves];
+    const int t = threadIdx.x, w = t / kWave, lane = lane_id();
     const int64_t per = cdiv(R, int64_t(kPlanThreads));
     const int64_t a = t * per < R ? t * per : R, b = a + per < R ? a + per : R;
-    int64_t c = 0, e = 0;
+    int64_t c = 0, e = 0, m = 0;
     for (int64_t I = a; I < b; ++I) {
         const int64_t k = cdiv(ptr[I + 1] - ptr[I], CH);
         c += k;
-        e += k > 0 ? k - 1 : 0;
+        e += k > 1 ? k - 1 : 0;
+        m += k > 1 ? 1 : 0;
     }
-    s_c[t] = c;
-    s_e[t] = e;
+    const int64_t ic = wave_incl_scan(c), ie = wave_incl_scan(e), im = wave_incl_scan(m);
+    if (lane == kWave - 1) {
+        s_w[0][w] = ic;
+        s_w[1][w] = ie;
+        s_w[2][w] = im;
+    }
     __syncthreads();
-    for (int o = 1; o < kPlanThreads; o <<= 1) {  // inclusive Hillis-Steele scan
-        const int64_t xc = t >= o ? s_c[t - o] : 0, xe = t >= o ? s_e[t - o] : 0;
-        __syncthreads();
-        s_c[t] += xc;
-        s_e[t] += xe;
-        __syncthreads();
+    int64_t bc = 0, be = 0, bm = 0, tc = 0, te = 0, tm = 0;
+    for (int x = 0; x < kPlanWaves; ++x) {
+        if (x < w) {
+            bc += s_w[0][x];
+            be += s_w[1][x];
+            bm += s_w[2][x];
+        }
+        tc += s_w[0][x];
+        te += s_w[1][x];
+        tm += s_w[2][x];
     }
-    c = s_c[t] - c;
-    e = s_e[t] - e;
+    c = bc + ic - c;
+    e = be + ie - e;
+    m = bm + im - m;
     for (int64_t I = a; I < b; ++I) {
         chunk_off[I] = c;
         extra_off[I] = e;
         const int64_t k = cdiv(ptr[I + 1] - ptr[I], CH);
         c += k;
-        e += k > 0 ? k - 1 : 0;
+        if (k > 1) {
+            e += k - 1;
+            merge_rows[m++] = int32_t(I);
+        }
     }
-    if (t == kPlanThreads - 1) {
-        chunk_off[R] = s_c[t];
-        extra_off[R] = s_e[t];
+    if (t == 0) {
+        chunk_off[R] = tc;
+        extra_off[R] = te;
+        *merge_cnt = uint32_t(tm);
     }
+}
+
+// Larger plans: rows with extra slots listed in any order (each is merged on
+// its own, so the order does not change any result).
+__global__ void k_tile_merge_list(int64_t R, const int32_t* __restrict__ ecounts, int32_t* __restrict__ merge_rows,
+                                  uint32_t* __restrict__ merge_cnt) {
+    for (int64_t I = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; I < R; I += int64_t(gridDim.x) * blockDim.x)
+        if (ecounts[I] > 0) merge_rows[atomicAdd(merge_cnt, 1u)] = int32_t(I);
 }
 
 gt_status tile_chunk_plan(const gt_tiles* p, const int64_t* ptr, const TileChunks& ck, hipStream_t s) {
     const int64_t R = p->n_row_tiles;
     if (R <= kPlanOneBlock) {
-        k_tile_chunk_plan1<<<1, kPlanThreads, 0, s>>>(R, ptr, ck.CH, ck.chunk_off, ck.extra_off);
+        k_tile_chunk_plan1<<<1, kPlanThreads, 0, s>>>(R, ptr, ck.CH, ck.chunk_off, ck.extra_off, ck.merge_rows,
+                                                      ck.merge_cnt);
         GT_LAUNCH_CHECK("tile_chunk_plan");
         return GT_OK;
     }
@@ -708,7 +745,11 @@ gt_status tile_chunk_plan(const gt_tiles* p, const int64_t* ptr, const TileChunk
     GT_LAUNCH_CHECK("tile_chunk_counts");
     gt_status st = exclusive_scan_i32(ck.counts, R, ck.chunk_off, ck.scan, s);
     if (st != GT_OK) return st;
-    return exclusive_scan_i32(ck.ecounts, R, ck.extra_off, ck.scan, s);
+    if ((st = exclusive_scan_i32(ck.ecounts, R, ck.extra_off, ck.scan, s)) != GT_OK) return st;
+    if ((st = fill_u32(ck.merge_cnt, 1, 0u, s)) != GT_OK) return st;
+    k_tile_merge_list<<<grid_for(R, 256, 1024), 256, 0, s>>>(R, ck.ecounts, ck.merge_rows, ck.merge_cnt);
+    GT_LAUNCH_CHECK("tile_merge_list");
+    return GT_OK;
 }
 
 // Fold the extra slots of each tile row into its partial state.  A workgroup
@@ -718,8 +759,8 @@ constexpr int kMergeThreads = 256;
 template <int D>
 constexpr int kMergeRows = kMergeThreads / (D / 4);
 
-inline dim3 merge_grid(int64_t R, int H, int T, int D) {
-    return dim3(unsigned(R), unsigned(H), unsigned(T / (kMergeThreads / (D / 4))));
+inline dim3 merge_grid(const TileChunks& ck, int H, int T, int D) {
+    return dim3(unsigned(ck.max_merge), unsigned(H), unsigned(T / (kMergeThreads / (D / 4))));
 }
 
 // ... the forward's online-softmax states (m, l, acc) ...
@@ -727,10 +768,10 @@ template <int D, int T>
 __global__ __launch_bounds__(kMergeThreads) void k_tiles_merge_fwd(int64_t n, int H, TileChunks ck,
                                                                    float* __restrict__ pm, float* __restrict__ pl,
                                                                    float* __restrict__ pacc) {
-    const int64_t I = blockIdx.x;
+    if (blockIdx.x >= *ck.merge_cnt) return;
+    const int64_t I = ck.merge_rows[blockIdx.x];
     const int h = blockIdx.y;
     const int64_t e0 = ck.extra_off[I], e1 = ck.extra_off[I + 1];
-    if (e0 == e1) return;
     const int lr = blockIdx.z * kMergeRows<D> + threadIdx.x / (D / 4);
     const int f = 4 * (threadIdx.x % (D / 4));
     const int64_t q = I * T + lr;
@@ -773,10 +814,10 @@ template <int D, int T>
 __global__ __launch_bounds__(kMergeThreads) void k_tiles_merge_sum(int64_t n, int H, TileChunks ck,
                                                                    float* __restrict__ a, float* __restrict__ b,
                                                                    float* __restrict__ m) {
-    const int64_t I = blockIdx.x;
+    if (blockIdx.x >= *ck.merge_cnt) return;
+    const int64_t I = ck.merge_rows[blockIdx.x];
     const int h = blockIdx.y;
     const int64_t e0 = ck.extra_off[I], e1 = ck.extra_off[I + 1];
-    if (e0 == e1) return;
     const int lr = blockIdx.z * kMergeRows<D> + threadIdx.x / (D / 4);
     const int f = 4 * (threadIdx.x % (D / 4));
     const int64_t q = I * T + lr;
@@ -1308,7 +1349,7 @@ gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint
     GT_TILES_T((k_tiles_fwd<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
                                                        sl2, tp.m, tp.l, tp.acc, p->n_row_tiles, tp.ck)));
     GT_LAUNCH_CHECK("tiles_fwd_bf16");
-    GT_TILES_T((k_tiles_merge_fwd<D, TT><<<merge_grid(p->n_row_tiles, H, TT, D), kMergeThreads, 0, s>>>(
+    GT_TILES_T((k_tiles_merge_fwd<D, TT><<<merge_grid(tp.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, tp.ck, tp.m, tp.l, tp.acc)));
     GT_LAUNCH_CHECK("tiles_merge_fwd_bf16");
     return GT_OK;
@@ -1323,7 +1364,7 @@ gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint1
     GT_TILES_T((k_tiles_dq<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
                                                       dO, LSE, sl2, dq.acc, dq.acc2, dq.m, p->n_row_tiles, dq.ck)));
     GT_LAUNCH_CHECK("tiles_dq_bf16");
-    GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(p->n_row_tiles, H, TT, D), kMergeThreads, 0, s>>>(
+    GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(dq.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, dq.ck, dq.acc, dq.acc2, dq.m)));
     GT_LAUNCH_CHECK("tiles_merge_dq_bf16");
     return GT_OK;
@@ -1340,7 +1381,7 @@ gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uin
                                                         p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv, sl2,
                                                         dk.acc, dv.acc, dk.ck)));
     GT_LAUNCH_CHECK("tiles_dkdv_bf16");
-    GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(p->n_row_tiles, H, TT, D), kMergeThreads, 0, s>>>(
+    GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(dk.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, dk.ck, dk.acc, dv.acc, nullptr)));
     GT_LAUNCH_CHECK("tiles_merge_dkdv_bf16");
     return GT_OK;

@@ -19,8 +19,11 @@ struct TileChunks {
     int32_t* counts = nullptr;     // [R]: chunks per row
     int32_t* ecounts = nullptr;    // [R]: extra slots per row
     ScanTmp scan;
+    int32_t* merge_rows = nullptr;  // tile rows (columns) with extra slots, the first *merge_cnt entries
+    uint32_t* merge_cnt = nullptr;
     int CH = 1;
     int64_t max_chunks = 0;
+    int64_t max_merge = 0;  // bound on the rows with extra slots
     float* m = nullptr;     // extra slots: [slots, T, H] (forward max, or the dQ pass's D sum)
     float* l = nullptr;     // [slots, T, H] forward only
     float* acc = nullptr;   // [slots, T, H, d]
@@ -70,6 +73,9 @@ inline TileChunks tile_chunks(Ws& ws, const gt_tiles* p, int64_t per_row_m, int6
     c.counts = ws.take<int32_t>(R);
     c.ecounts = ws.take<int32_t>(R);
     c.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(R)));
+    c.max_merge = R < slots ? R : slots;
+    c.merge_rows = ws.take<int32_t>(size_t(c.max_merge));
+    c.merge_cnt = ws.take<uint32_t>(1);
     const int64_t rows = slots * p->T;
     c.m = ws.take<float>(size_t(rows * per_row_m));
     if (with_l) c.l = ws.take<float>(size_t(rows * per_row_m));
