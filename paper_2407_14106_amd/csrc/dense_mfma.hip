@@ -619,15 +619,6 @@ __device__ __forceinline__ void load_mask_row(uint32_t (&mw)[T / 32], const uint
 
 // ---- chunks of the dense tiles of each tile row (column)
 
-__global__ void k_tile_chunk_counts(int64_t R, const int64_t* __restrict__ ptr, int CH, int32_t* __restrict__ counts,
-                                    int32_t* __restrict__ ecounts) {
-    for (int64_t I = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; I < R; I += int64_t(gridDim.x) * blockDim.x) {
-        const int64_t c = cdiv(ptr[I + 1] - ptr[I], CH);
-        counts[I] = int32_t(c);
-        ecounts[I] = int32_t(c > 0 ? c - 1 : 0);
-    }
-}
-
 // Workgroup b -> tile row (column) I, its list range [t0, t1) and the output
 // slot (-1: the partial state of the row; else an extra slot); false for the
 // surplus of the grid.
@@ -653,13 +644,13 @@ __device__ __forceinline__ int64_t out_row(int64_t q, int64_t I, int64_t slot, i
     return slot < 0 ? q : slot * T + (q - I * T);
 }
 
-// The plan in one workgroup (plans of up to kPlanOneBlock tile rows): each
+// The plan in one workgroup (a tile plan has at most 16,384 tile rows): each
 // thread sums a contiguous run of rows (chunks, extra slots, rows with extra
 // slots), a wavefront scan plus one pass over the wavefront totals, then the
 // runs are written out with the list of rows that have extra slots.
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / kWave;
-constexpr int64_t kPlanOneBlock = int64_t(1) << 16;
+constexpr int64_t kPlanMaxRows = 16384;
 
 __device__ __forceinline__ int64_t wave_incl_scan(int64_t x) {
     const int lane = lane_id();
@@ -725,30 +716,12 @@ __global__ __launch_bounds__(kPlanThreads) void k_tile_chunk_plan1(int64_t R, co
     }
 }
 
-// Larger plans: rows with extra slots listed in any order (each is merged on
-// its own, so the order does not change any result).
-__global__ void k_tile_merge_list(int64_t R, const int32_t* __restrict__ ecounts, int32_t* __restrict__ merge_rows,
-                                  uint32_t* __restrict__ merge_cnt) {
-    for (int64_t I = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; I < R; I += int64_t(gridDim.x) * blockDim.x)
-        if (ecounts[I] > 0) merge_rows[atomicAdd(merge_cnt, 1u)] = int32_t(I);
-}
-
 gt_status tile_chunk_plan(const gt_tiles* p, const int64_t* ptr, const TileChunks& ck, hipStream_t s) {
     const int64_t R = p->n_row_tiles;
-    if (R <= kPlanOneBlock) {
-        k_tile_chunk_plan1<<<1, kPlanThreads, 0, s>>>(R, ptr, ck.CH, ck.chunk_off, ck.extra_off, ck.merge_rows,
-                                                      ck.merge_cnt);
-        GT_LAUNCH_CHECK("tile_chunk_plan");
-        return GT_OK;
-    }
-    k_tile_chunk_counts<<<grid_for(R, 256, 1024), 256, 0, s>>>(R, ptr, ck.CH, ck.counts, ck.ecounts);
-    GT_LAUNCH_CHECK("tile_chunk_counts");
-    gt_status st = exclusive_scan_i32(ck.counts, R, ck.chunk_off, ck.scan, s);
-    if (st != GT_OK) return st;
-    if ((st = exclusive_scan_i32(ck.ecounts, R, ck.extra_off, ck.scan, s)) != GT_OK) return st;
-    if ((st = fill_u32(ck.merge_cnt, 1, 0u, s)) != GT_OK) return st;
-    k_tile_merge_list<<<grid_for(R, 256, 1024), 256, 0, s>>>(R, ck.ecounts, ck.merge_rows, ck.merge_cnt);
-    GT_LAUNCH_CHECK("tile_merge_list");
+    if (R > kPlanMaxRows) return fail(GT_ERR_UNSUPPORTED, "dense tiles: more than 16384 tile rows");
+    k_tile_chunk_plan1<<<1, kPlanThreads, 0, s>>>(R, ptr, ck.CH, ck.chunk_off, ck.extra_off, ck.merge_rows,
+                                                  ck.merge_cnt);
+    GT_LAUNCH_CHECK("tile_chunk_plan");
     return GT_OK;
 }
 

@@ -4,7 +4,6 @@
 #pragma once
 
 #include "attn_common.h"
-#include "prim.h"
 
 namespace gt {
 
@@ -16,9 +15,6 @@ namespace gt {
 struct TileChunks {
     int64_t* chunk_off = nullptr;  // [R + 1]: first chunk of each tile row (column)
     int64_t* extra_off = nullptr;  // [R + 1]: first extra slot of each tile row (column)
-    int32_t* counts = nullptr;     // [R]: chunks per row
-    int32_t* ecounts = nullptr;    // [R]: extra slots per row
-    ScanTmp scan;
     int32_t* merge_rows = nullptr;  // tile rows (columns) with extra slots, the first *merge_cnt entries
     uint32_t* merge_cnt = nullptr;
     int CH = 1;
@@ -70,9 +66,6 @@ inline TileChunks tile_chunks(Ws& ws, const gt_tiles* p, int64_t per_row_m, int6
     c.max_chunks = (R < nd ? R : nd) + nd / c.CH + 1;
     c.chunk_off = ws.take<int64_t>(R + 1);
     c.extra_off = ws.take<int64_t>(R + 1);
-    c.counts = ws.take<int32_t>(R);
-    c.ecounts = ws.take<int32_t>(R);
-    c.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(R)));
     c.max_merge = R < slots ? R : slots;
     c.merge_rows = ws.take<int32_t>(size_t(c.max_merge));
     c.merge_cnt = ws.take<uint32_t>(1);
