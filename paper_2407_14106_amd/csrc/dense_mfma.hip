@@ -729,6 +729,7 @@ gt_status tile_chunk_plan(const gt_tiles* p, const int64_t* ptr, const TileChunk
 // takes kMergeRows<D> rows of one (tile row, head), D / 4 consecutive lanes per
 // row, one float4 each, so every slot row is read as whole cache lines.
 constexpr int kMergeThreads = 256;
+constexpr int kTileNB = 1;  // 32-row blocks per wavefront in the dense-tile kernels
 template <int D>
 constexpr int kMergeRows = kMergeThreads / (D / 4);
 
@@ -822,8 +823,15 @@ __global__ __launch_bounds__(kMergeThreads) void k_tiles_merge_sum(int64_t n, in
     if (m && f == 0) m[row] = sm;
 }
 
-template <int D, int T>
-__global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
+// NB 32-row blocks per wavefront (2: every K and V fragment read from LDS
+// feeds two products; 1: half the registers, twice the wavefronts).  The
+// tiles are launched with NB = 1 (kTileNB): a chunk holds only a few tiles, so
+// the kernels are latency-bound and more resident wavefronts pay more than
+// the operand reuse; the occupancy hints keep the accumulators out of the
+// AGPRs (forward: 4 wavefronts per SIMD at d = 32 and 64; dQ, dK/dV: 2-3).
+template <int D, int T, int NB>
+__global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(D >= 64 ? 3 : 4))) void k_tiles_fwd(
+    int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
                                                  const int32_t* __restrict__ tile_col,
                                                  const uint32_t* __restrict__ tile_mask,
                                                  const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
@@ -842,42 +850,46 @@ __global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t
         pacc = ck.acc;
     }
     const int lane = lane_id();
-    const int ql0 = (threadIdx.x / kWave) * kOwn;  // first owned row inside the tile row
+    constexpr int NT = T * 2 / NB;
+    const int ql0 = (threadIdx.x / kWave) * 32 * NB;  // first owned row inside the tile row
     const int64_t q0 = int64_t(I) * T + ql0;
-    Frag<D> qf[2];
+    Frag<D> qf[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) qf[b].load(Q, q0 + 32 * b + (lane & 31), n, H, h, lane);
+    for (int b = 0; b < NB; ++b) qf[b].load(Q, q0 + 32 * b + (lane & 31), n, H, h, lane);
     if (sl2 < 0.f) {  // keep the exp2-domain scale positive: negate Q instead (exact in bf16)
         sl2 = -sl2;
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int c = 0; c < D / 16; ++c)
                 qf[b].v[c] = __builtin_bit_cast(bf16x8_t, __builtin_bit_cast(uint4, qf[b].v[c]) ^
                                                               make_uint4(0x80008000u, 0x80008000u, 0x80008000u,
                                                                          0x80008000u));
     }
-    f32x16_t acc[2][D / 32];
+    f32x16_t acc[NB][D / 32];
+    float m[NB], l[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b) {
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
-    float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
+        m[b] = kNegInf;
+        l[b] = 0.f;
+    }
     // Stages run over the tile row's dense tiles, T/64 per tile.  They are
     // single-buffered: several small workgroups per CU hide each other's
     // loads, which a register prefetch (at one wavefront per SIMD) did not.
     constexpr int NSG = T / kStage;
     const int64_t stages = (t1 - t0) * NSG;
-    Stager<D, T> gk, gv;
-    uint32_t mw[2][W];
-    auto fetch = [&](int64_t g, uint32_t (&mwx)[2][W]) {
+    Stager<D, NT> gk, gv;
+    uint32_t mw[NB][W];
+    auto fetch = [&](int64_t g, uint32_t (&mwx)[NB][W]) {
         const int64_t k = t0 + g / NSG;
         const int64_t kb = int64_t(tile_col[k]) * T + kStage * (g % NSG);
         gk.load(K, kb, n, H, h);
         gv.load(V, kb, n, H, h);
         if (g % NSG == 0)
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
+            for (int b = 0; b < NB; ++b)
                 load_mask_row<T>(mwx[b], tile_mask + (k * T + ql0 + 32 * b + (lane & 31)) * W);
     };
 #pragma unroll 1
@@ -890,18 +902,19 @@ __global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t
         __syncthreads();
 #pragma unroll
         for (int kb = 0; kb < kStage / 32; ++kb) {
-            f32x16_t s[2];
-            s[0] = s[1] = zero16();
+            f32x16_t s[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) s[b] = zero16();
 #pragma unroll
             for (int c = 0; c < D / 16; ++c) {
                 const bf16x8_t a = lds_row8<D>(sK[buf], 32 * kb + (lane & 31), c, lane);
-                s[0] = mma(a, qf[0].v[c], s[0]);
-                s[1] = mma(a, qf[1].v[c], s[1]);
+#pragma unroll
+                for (int b = 0; b < NB; ++b) s[b] = mma(a, qf[b].v[c], s[b]);
             }
             bool grow = false;
-            float mt[2];
+            float mt[NB];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+            for (int b = 0; b < NB; ++b) {
                 const uint32_t w = mw[b][2 * st + kb];
 #pragma unroll
                 for (int i = 0; i < 16; ++i)
@@ -914,7 +927,7 @@ __global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t
             }
             if (__builtin_amdgcn_ballot_w64(grow)) {
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
+                for (int b = 0; b < NB; ++b) {
                     const float mn = fmaxf(m[b], mt[b]);
                     if (mn == kNegInf) continue;
                     const float alpha = ex2(m[b] - mn);
@@ -926,9 +939,9 @@ __global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t
                     m[b] = mn;
                 }
             }
-            bf16x8_t pb[2][2];
+            bf16x8_t pb[NB][2];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+            for (int b = 0; b < NB; ++b) {
                 const float mm = m[b] == kNegInf ? 0.f : m[b];
                 float ls = 0.f;
 #pragma unroll
@@ -946,13 +959,13 @@ __global__ __launch_bounds__(T) void k_tiles_fwd(int64_t n, int H, const int64_t
 #pragma unroll
                 for (int half = 0; half < 2; ++half) {
                     const bf16x8_t a = lds_perm8(sVt[buf], 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
-                    acc[0][db] = mma(a, pb[0][half], acc[0][db]);
-                    acc[1][db] = mma(a, pb[1][half], acc[1][db]);
+#pragma unroll
+                    for (int b = 0; b < NB; ++b) acc[b][db] = mma(a, pb[b][half], acc[b][db]);
                 }
         }
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t q = q0 + 32 * b + (lane & 31);
         const float lt = pair_sum(l[b]);
         if (q >= n) continue;
@@ -986,8 +999,9 @@ __device__ __forceinline__ void split_b16(const f32x16_t& w, int half, bf16x8_t&
 
 // Row pass over the dense tiles: A = sum P dP K, B = sum P K and the D sum
 // sum P dP of every owned row (the edge kernels form dQ = scale (A - D B)).
-template <int D, int T>
-__global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
+template <int D, int T, int NB>
+__global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 2 : 1))) void k_tiles_dq(
+    int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
                                                 const int32_t* __restrict__ tile_col,
                                                 const uint32_t* __restrict__ tile_mask,
                                                 const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
@@ -1008,35 +1022,38 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
         pd = ck.m;
     }
     const int lane = lane_id();
-    const int ql0 = (threadIdx.x / kWave) * kOwn;
+    constexpr int NT = T * 2 / NB;
+    const int ql0 = (threadIdx.x / kWave) * 32 * NB;
     const int64_t q0 = int64_t(I) * T + ql0;
-    Frag<D> qf[2], gf[2];
-    float lse2[2];
+    Frag<D> qf[NB], gf[NB];
+    float lse2[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t q = q0 + 32 * b + (lane & 31);
         qf[b].load(Q, q, n, H, h, lane);
         gf[b].load(dO, q, n, H, h, lane);
         lse2[b] = q < n ? LSE[q * H + h] * kLog2e : 0.f;
     }
-    f32x16_t accA[2][D / 32], accB[2][D / 32];
+    f32x16_t accA[NB][D / 32], accB[NB][D / 32];
+    float dsum[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b) {
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) accA[b][db] = accB[b][db] = zero16();
-    float dsum[2] = {0.f, 0.f};
+        dsum[b] = 0.f;
+    }
     constexpr int NSG = T / kStage;
     const int64_t stages = (t1 - t0) * NSG;
-    Stager<D, T> gk, gv;
-    uint32_t mw[2][W];
-    auto fetch = [&](int64_t g, uint32_t (&mwx)[2][W]) {
+    Stager<D, NT> gk, gv;
+    uint32_t mw[NB][W];
+    auto fetch = [&](int64_t g, uint32_t (&mwx)[NB][W]) {
         const int64_t k = t0 + g / NSG;
         const int64_t kb = int64_t(tile_col[k]) * T + kStage * (g % NSG);
         gk.load(K, kb, n, H, h);
         gv.load(V, kb, n, H, h);
         if (g % NSG == 0)
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
+            for (int b = 0; b < NB; ++b)
                 load_mask_row<T>(mwx[b], tile_mask + (k * T + ql0 + 32 * b + (lane & 31)) * W);
     };
 #pragma unroll 1
@@ -1050,19 +1067,20 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
         __syncthreads();
 #pragma unroll
         for (int kb = 0; kb < kStage / 32; ++kb) {
-            f32x16_t s[2], dp[2];
-            s[0] = s[1] = dp[0] = dp[1] = zero16();
+            f32x16_t s[NB], dp[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) s[b] = dp[b] = zero16();
 #pragma unroll
             for (int c = 0; c < D / 16; ++c) {
                 const bf16x8_t a = lds_row8<D>(sK[buf], 32 * kb + (lane & 31), c, lane);
-                s[0] = mma(a, qf[0].v[c], s[0]);
-                s[1] = mma(a, qf[1].v[c], s[1]);
+#pragma unroll
+                for (int b = 0; b < NB; ++b) s[b] = mma(a, qf[b].v[c], s[b]);
                 const bf16x8_t v = lds_row8<D>(sV[buf], 32 * kb + (lane & 31), c, lane);
-                dp[0] = mma(v, gf[0].v[c], dp[0]);
-                dp[1] = mma(v, gf[1].v[c], dp[1]);
+#pragma unroll
+                for (int b = 0; b < NB; ++b) dp[b] = mma(v, gf[b].v[c], dp[b]);
             }
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+            for (int b = 0; b < NB; ++b) {
                 const uint32_t w = mw[b][2 * st + kb];
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
@@ -1078,7 +1096,7 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
                 for (int half = 0; half < 2; ++half) {
                     const bf16x8_t a = lds_perm8(sKt[buf], 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
 #pragma unroll
-                    for (int b = 0; b < 2; ++b) {
+                    for (int b = 0; b < NB; ++b) {
                         bf16x8_t hi, lo;
                         split_b16(dp[b], half, hi, lo);
                         accA[b][db] = mma(a, lo, mma(a, hi, accA[b][db]));
@@ -1089,7 +1107,7 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
         }
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t q = q0 + 32 * b + (lane & 31);
         const float ds = pair_sum(dsum[b]);
         if (q >= n) continue;
@@ -1113,8 +1131,9 @@ __global__ __launch_bounds__(T) void k_tiles_dq(int64_t n, int H, const int64_t*
 // Column pass over the dense tiles: unscaled dK and dV sums of every owned key.
 // The stage's masks are transposed with ballots so that each lane holds, for
 // its key, one 64-bit word over the stage's 64 queries.
-template <int D, int T>
-__global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_row_tiles,
+template <int D, int T, int NB>
+__global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 2 : 1))) void k_tiles_dkdv(
+    int64_t n, int H, int64_t n_row_tiles,
                                                   const int64_t* __restrict__ tileT_ptr,
                                                   const int32_t* __restrict__ tileT_idx,
                                                   const int64_t* __restrict__ tile_rowptr,
@@ -1139,23 +1158,24 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
         pdv = ck.acc2;
     }
     const int lane = lane_id();
-    const int kl0 = (threadIdx.x / kWave) * kOwn;  // first owned key inside the tile column
+    constexpr int NT = T * 2 / NB;
+    const int kl0 = (threadIdx.x / kWave) * 32 * NB;  // first owned key inside the tile column
     const int64_t k0 = int64_t(J) * T + kl0;
-    Frag<D> kf[2], vf[2];
+    Frag<D> kf[NB], vf[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         kf[b].load(K, k0 + 32 * b + (lane & 31), n, H, h, lane);
         vf[b].load(V, k0 + 32 * b + (lane & 31), n, H, h, lane);
     }
-    f32x16_t dk[2][D / 32], dv[2][D / 32];
+    f32x16_t dk[NB][D / 32], dv[NB][D / 32];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) dk[b][db] = dv[b][db] = zero16();
     constexpr int NSG = T / kStage;
     const int64_t stages = (u1 - u0) * NSG;
-    Stager<D, T> gq, gg;
-    uint32_t mword[2];  // this lane's row of the stage: mask words of the wavefront's two key blocks
+    Stager<D, NT> gq, gg;
+    uint32_t mword[NB];  // this lane's row of the stage: mask words of the wavefront's key blocks
     float2 stat;        // LSE (exp2 domain) and D of the stage's query threadIdx.x % kStage
     auto fetch = [&](int64_t g) {
         const int64_t k = tileT_idx[u0 + g / NSG];
@@ -1170,16 +1190,16 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
         gq.load(Q, qbase, n, H, h);
         gg.load(dO, qbase, n, H, h);
 #pragma unroll
-        for (int b = 0; b < 2; ++b) mword[b] = tile_mask[(k * T + kStage * st + lane) * W + (kl0 / 32 + b)];
+        for (int b = 0; b < NB; ++b) mword[b] = tile_mask[(k * T + kStage * st + lane) * W + (kl0 / 32 + b)];
         stat = make_float2(__builtin_huge_valf(), 0.f);  // queries >= n take no weight
         const int64_t qn = qbase + (threadIdx.x % kStage);
         if (qn < n) stat = make_float2(LSE[qn * H + h] * kLog2e, Dv[qn * H + h]);
     };
     // transposed masks: bit r of mt[b] <=> query r of the stage attends to key k0 + 32 b + lane % 32
-    uint64_t mt[2];
-    auto transpose = [&](uint64_t (&out)[2]) {
+    uint64_t mt[NB];
+    auto transpose = [&](uint64_t (&out)[NB]) {
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
+        for (int b = 0; b < NB; ++b) {
             uint64_t mine = 0;
 #pragma unroll
             for (int c = 0; c < 32; ++c) {
@@ -1209,16 +1229,17 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
         __syncthreads();
 #pragma unroll
         for (int qb = 0; qb < kStage / 32; ++qb) {
-            f32x16_t s[2], dp[2];
-            s[0] = s[1] = dp[0] = dp[1] = zero16();
+            f32x16_t s[NB], dp[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) s[b] = dp[b] = zero16();
 #pragma unroll
             for (int c = 0; c < D / 16; ++c) {
                 const bf16x8_t a = lds_row8<D>(sQ[buf], 32 * qb + (lane & 31), c, lane);
-                s[0] = mma(a, kf[0].v[c], s[0]);
-                s[1] = mma(a, kf[1].v[c], s[1]);
+#pragma unroll
+                for (int b = 0; b < NB; ++b) s[b] = mma(a, kf[b].v[c], s[b]);
                 const bf16x8_t g8 = lds_row8<D>(sG[buf], 32 * qb + (lane & 31), c, lane);
-                dp[0] = mma(g8, vf[0].v[c], dp[0]);
-                dp[1] = mma(g8, vf[1].v[c], dp[1]);
+#pragma unroll
+                for (int b = 0; b < NB; ++b) dp[b] = mma(g8, vf[b].v[c], dp[b]);
             }
             float Lr[16], Dr[16];
 #pragma unroll
@@ -1230,7 +1251,7 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
                 Dr[4 * j] = d4.x, Dr[4 * j + 1] = d4.y, Dr[4 * j + 2] = d4.z, Dr[4 * j + 3] = d4.w;
             }
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+            for (int b = 0; b < NB; ++b) {
                 const uint32_t w = uint32_t(mt[b] >> (32 * qb));
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
@@ -1246,7 +1267,7 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
                     const bf16x8_t g8 = lds_perm8(sGt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
                     const bf16x8_t a = lds_perm8(sQt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
 #pragma unroll
-                    for (int b = 0; b < 2; ++b) {
+                    for (int b = 0; b < NB; ++b) {
                         bf16x8_t hi16, lo16;
                         split_b16(dp[b], half, hi16, lo16);
                         dv[b][db] = mma(g8, lo16, mma(g8, hi16, dv[b][db]));
@@ -1257,7 +1278,7 @@ __global__ __launch_bounds__(T) void k_tiles_dkdv(int64_t n, int H, int64_t n_ro
         }
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t key = k0 + 32 * b + (lane & 31);
         if (key >= n) continue;
         const int64_t orow = out_row(key, J, slot, T);
@@ -1319,8 +1340,10 @@ gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint
     gt_status st = tile_chunk_plan(p, p->tile_rowptr, tp.ck, s);
     if (st != GT_OK) return st;
     const dim3 grid(unsigned(tp.ck.max_chunks), unsigned(H));
-    GT_TILES_T((k_tiles_fwd<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
-                                                       sl2, tp.m, tp.l, tp.acc, p->n_row_tiles, tp.ck)));
+    constexpr int NB = kTileNB;
+    GT_TILES_T((k_tiles_fwd<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col,
+                                                                    p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc,
+                                                                    p->n_row_tiles, tp.ck)));
     GT_LAUNCH_CHECK("tiles_fwd_bf16");
     GT_TILES_T((k_tiles_merge_fwd<D, TT><<<merge_grid(tp.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, tp.ck, tp.m, tp.l, tp.acc)));
@@ -1334,8 +1357,10 @@ gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint1
     gt_status st = tile_chunk_plan(p, p->tile_rowptr, dq.ck, s);
     if (st != GT_OK) return st;
     const dim3 grid(unsigned(dq.ck.max_chunks), unsigned(H));
-    GT_TILES_T((k_tiles_dq<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V,
-                                                      dO, LSE, sl2, dq.acc, dq.acc2, dq.m, p->n_row_tiles, dq.ck)));
+    constexpr int NB = kTileNB;
+    GT_TILES_T((k_tiles_dq<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col,
+                                                                   p->tile_mask, Q, K, V, dO, LSE, sl2, dq.acc,
+                                                                   dq.acc2, dq.m, p->n_row_tiles, dq.ck)));
     GT_LAUNCH_CHECK("tiles_dq_bf16");
     GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(dq.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, dq.ck, dq.acc, dq.acc2, dq.m)));
@@ -1350,9 +1375,11 @@ gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uin
     gt_status st = tile_chunk_plan(p, p->tileT_ptr, dk.ck, s);
     if (st != GT_OK) return st;
     const dim3 grid(unsigned(dk.ck.max_chunks), unsigned(H));
-    GT_TILES_T((k_tiles_dkdv<D, TT><<<grid, TT, 0, s>>>(p->n, H, p->n_row_tiles, p->tileT_ptr, p->tileT_idx,
-                                                        p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv, sl2,
-                                                        dk.acc, dv.acc, dk.ck)));
+    constexpr int NB = kTileNB;
+    GT_TILES_T((k_tiles_dkdv<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->n_row_tiles, p->tileT_ptr,
+                                                                     p->tileT_idx, p->tile_rowptr, p->tile_mask, Q,
+                                                                     K, V, dO, LSE, Dv, sl2, dk.acc, dv.acc,
+                                                                     dk.ck)));
     GT_LAUNCH_CHECK("tiles_dkdv_bf16");
     GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(dk.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, dk.ck, dk.acc, dv.acc, nullptr)));
