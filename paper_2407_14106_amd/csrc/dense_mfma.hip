@@ -4,9 +4,11 @@
 // n x n buffer.
 //
 // Design (CDNA4, wave64, v_mfma_f32_32x32x16_bf16):
-//   - A workgroup is 4 wavefronts; each wavefront owns 64 rows (two 32-row
-//     MFMA blocks) of one head, so every operand fragment read from LDS feeds
-//     two products.  The partner rows stream through LDS in 64-row stages,
+//   - A workgroup owns 256 rows of one head.  In the forward each wavefront
+//     owns 64 of them (two 32-row MFMA blocks), so every operand fragment read
+//     from LDS feeds two products; the backward passes give each wavefront one
+//     block (8 wavefronts), which halves their registers and leaves 2-3
+//     wavefronts per SIMD.  The partner rows stream through LDS in 64-row stages,
 //     double buffered: the next stage is loaded into registers while the
 //     current one is multiplied, then written to the other buffer, with one
 //     barrier per stage.
@@ -31,10 +33,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kWaves = 4;                // wavefronts per workgroup
-constexpr int kThr = kWaves * kWave;     // threads per workgroup
-constexpr int kOwn = 64;                 // owned rows per wavefront
-constexpr int kRowsWg = kWaves * kOwn;   // owned rows per workgroup
+constexpr int kRowsWg = 256;             // owned rows per workgroup of the full layer
 constexpr int kStage = 64;               // partner rows per LDS stage
 constexpr int kTS = kStage + 4;          // transposed LDS row stride (elements)
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -195,10 +194,20 @@ __device__ __forceinline__ bool wg_coords(int64_t n, int H, int& h, int64_t& row
 
 inline unsigned full_grid(int64_t n, int H) { return xcd_grid(cdiv(n, kRowsWg) * H); }
 
+// 32-row MFMA blocks per wavefront in the full layer (the kernels are
+// templated on it) and the threads per workgroup that hold kRowsWg rows.  The
+// forward keeps two blocks (every K and V fragment read from LDS feeds two
+// products; measured faster: 10.9 against 13.7 ms at 65,536 x 8 x 64); the
+// backward passes take one, which leaves them 2-3 wavefronts per SIMD instead
+// of one (44.1 -> 35.3 ms).
+constexpr int kFullFwdNB = 2, kFullBwdNB = 1;
+constexpr int kFullFwdThr = kRowsWg / (32 * kFullFwdNB) * kWave;
+constexpr int kFullBwdThr = kRowsWg / (32 * kFullBwdNB) * kWave;
+
 // ------------------------------------------------------------------ forward
 
-template <int D>
-__global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const uint16_t* __restrict__ Q,
+template <int D, int NB>
+__global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 3 : 2))) void k_full_fwd(int64_t n, int H, const uint16_t* __restrict__ Q,
                                                       const uint16_t* __restrict__ K,
                                                       const uint16_t* __restrict__ V, float sl2,
                                                       uint16_t* __restrict__ O, float* __restrict__ LSE) {
@@ -208,28 +217,33 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
     int64_t row0;
     if (!wg_coords(n, H, h, row0)) return;
     const int lane = lane_id();
-    const int64_t q0 = row0 + (threadIdx.x / kWave) * kOwn;
-    Frag<D> qf[2];
+    const int64_t q0 = row0 + (threadIdx.x / kWave) * 32 * NB;
+    Frag<D> qf[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) qf[b].load(Q, q0 + 32 * b + (lane & 31), n, H, h, lane);
+    for (int b = 0; b < NB; ++b) qf[b].load(Q, q0 + 32 * b + (lane & 31), n, H, h, lane);
     if (sl2 < 0.f) {  // keep the exp2-domain scale positive: negate Q instead (exact in bf16)
         sl2 = -sl2;
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int c = 0; c < D / 16; ++c)
                 qf[b].v[c] = __builtin_bit_cast(bf16x8_t, __builtin_bit_cast(uint4, qf[b].v[c]) ^
                                                               make_uint4(0x80008000u, 0x80008000u, 0x80008000u,
                                                                          0x80008000u));
     }
-    f32x16_t acc[2][D / 32];
+    f32x16_t acc[NB][D / 32];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
-    float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
+    float m[NB], l[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        m[b] = kNegInf;
+        l[b] = 0.f;
+    }
 
-    Stager<D, kThr> gk, gv;
+    Stager<D, kRowsWg / (32 * NB) * kWave> gk, gv;
     gk.load(K, 0, n, H, h);
     gv.load(V, 0, n, H, h);
     gk.store_rm(sK[0]);
@@ -248,24 +262,27 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
         const uint16_t* v_s = sVt[buf];
 #pragma unroll
         for (int kb = 0; kb < kStage / 32; ++kb) {
-            f32x16_t s[2];
-            s[0] = s[1] = zero16();
+            f32x16_t s[NB];
+            #pragma unroll
+            for (int b = 0; b < NB; ++b) s[b] = zero16();
 #pragma unroll
             for (int c = 0; c < D / 16; ++c) {
                 const bf16x8_t a = lds_row8<D>(k_s, 32 * kb + (lane & 31), c, lane);
-                s[0] = mma(a, qf[0].v[c], s[0]);
-                s[1] = mma(a, qf[1].v[c], s[1]);
+                #pragma unroll
+                for (int b = 0; b < NB; ++b) s[b] = mma(a, qf[b].v[c], s[b]);
             }
             const int64_t key0 = kbase + 32 * kb;
             if (key0 + 32 > n) {  // ragged last block: partners >= n take no weight
 #pragma unroll
                 for (int i = 0; i < 16; ++i)
-                    if (key0 + crow(i, lane) >= n) s[0][i] = s[1][i] = kNegInf;
+                    if (key0 + crow(i, lane) >= n)
+#pragma unroll
+                        for (int b = 0; b < NB; ++b) s[b][i] = kNegInf;
             }
             bool grow = false;
-            float mt[2];
+            float mt[NB];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+            for (int b = 0; b < NB; ++b) {
                 float mx = s[b][0];
 #pragma unroll
                 for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[b][i]);
@@ -274,7 +291,7 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
             }
             if (__builtin_amdgcn_ballot_w64(grow)) {
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
+                for (int b = 0; b < NB; ++b) {
                     const float mn = fmaxf(m[b], mt[b]);
                     const float alpha = ex2(m[b] - mn);
                     l[b] *= alpha;
@@ -285,9 +302,9 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
                     m[b] = mn;
                 }
             }
-            bf16x8_t pb[2][2];
+            bf16x8_t pb[NB][2];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+            for (int b = 0; b < NB; ++b) {
                 float ls = 0.f;
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
@@ -304,8 +321,8 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
 #pragma unroll
                 for (int half = 0; half < 2; ++half) {
                     const bf16x8_t a = lds_perm8(v_s, 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
-                    acc[0][db] = mma(a, pb[0][half], acc[0][db]);
-                    acc[1][db] = mma(a, pb[1][half], acc[1][db]);
+                    #pragma unroll
+                    for (int b = 0; b < NB; ++b) acc[b][db] = mma(a, pb[b][half], acc[b][db]);
                 }
         }
         if (t + 1 < stages) {
@@ -315,7 +332,7 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
         __syncthreads();
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t q = q0 + 32 * b + (lane & 31);
         const float lt = pair_sum(l[b]);
         if (q >= n) continue;
@@ -338,8 +355,8 @@ __global__ __launch_bounds__(kThr, 2) void k_full_fwd(int64_t n, int H, const ui
 // dQ_i = scale sum_j P_ij (dP_ij - D_i) K_j with dP_ij = <dO_i, V_j>; also
 // writes D_i for the column pass.
 
-template <int D>
-__global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uint16_t* __restrict__ Q,
+template <int D, int NB>
+__global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 2 : 1))) void k_full_dq(int64_t n, int H, const uint16_t* __restrict__ Q,
                                                      const uint16_t* __restrict__ K,
                                                      const uint16_t* __restrict__ V,
                                                      const uint16_t* __restrict__ O,
@@ -353,11 +370,11 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uin
     int64_t row0;
     if (!wg_coords(n, H, h, row0)) return;
     const int lane = lane_id();
-    const int64_t q0 = row0 + (threadIdx.x / kWave) * kOwn;
-    Frag<D> qf[2], gf[2];
-    float lse2[2], Dq[2];
+    const int64_t q0 = row0 + (threadIdx.x / kWave) * 32 * NB;
+    Frag<D> qf[NB], gf[NB];
+    float lse2[NB], Dq[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t q = q0 + 32 * b + (lane & 31);
         qf[b].load(Q, q, n, H, h, lane);
         gf[b].load(dO, q, n, H, h, lane);
@@ -367,13 +384,13 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uin
         lse2[b] = q < n ? LSE[q * H + h] * kLog2e : 0.f;
         if (q < n && lane < 32) Dv[q * H + h] = Dq[b];
     }
-    f32x16_t acc[2][D / 32];
+    f32x16_t acc[NB][D / 32];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) acc[b][db] = zero16();
 
-    Stager<D, kThr> gk, gv;
+    Stager<D, kRowsWg / (32 * NB) * kWave> gk, gv;
     gk.load(K, 0, n, H, h);
     gv.load(V, 0, n, H, h);
     gk.store_rm(sK[0]);
@@ -391,26 +408,29 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uin
         }
 #pragma unroll
         for (int kb = 0; kb < kStage / 32; ++kb) {
-            f32x16_t s[2], dp[2];
-            s[0] = s[1] = dp[0] = dp[1] = zero16();
+            f32x16_t s[NB], dp[NB];
+            #pragma unroll
+            for (int b = 0; b < NB; ++b) s[b] = dp[b] = zero16();
 #pragma unroll
             for (int c = 0; c < D / 16; ++c) {
                 const bf16x8_t a = lds_row8<D>(sK[buf], 32 * kb + (lane & 31), c, lane);
-                s[0] = mma(a, qf[0].v[c], s[0]);
-                s[1] = mma(a, qf[1].v[c], s[1]);
+                #pragma unroll
+                for (int b = 0; b < NB; ++b) s[b] = mma(a, qf[b].v[c], s[b]);
                 const bf16x8_t v = lds_row8<D>(sV[buf], 32 * kb + (lane & 31), c, lane);
-                dp[0] = mma(v, gf[0].v[c], dp[0]);
-                dp[1] = mma(v, gf[1].v[c], dp[1]);
+                #pragma unroll
+                for (int b = 0; b < NB; ++b) dp[b] = mma(v, gf[b].v[c], dp[b]);
             }
             const int64_t key0 = kbase + 32 * kb;
             if (key0 + 32 > n) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i)
-                    if (key0 + crow(i, lane) >= n) s[0][i] = s[1][i] = kNegInf;
-            }
-            bf16x8_t db16[2][2];
+                    if (key0 + crow(i, lane) >= n)
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+                        for (int b = 0; b < NB; ++b) s[b][i] = kNegInf;
+            }
+            bf16x8_t db16[NB][2];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const float p = ex2(fmaf(s[b][i], sl2, -lse2[b]));
@@ -424,8 +444,8 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uin
 #pragma unroll
                 for (int half = 0; half < 2; ++half) {
                     const bf16x8_t a = lds_perm8(sKt[buf], 32 * db + (lane & 31), 32 * kb + 16 * half, lane);
-                    acc[0][db] = mma(a, db16[0][half], acc[0][db]);
-                    acc[1][db] = mma(a, db16[1][half], acc[1][db]);
+                    #pragma unroll
+                    for (int b = 0; b < NB; ++b) acc[b][db] = mma(a, db16[b][half], acc[b][db]);
                 }
         }
         if (t + 1 < stages) {
@@ -436,7 +456,7 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uin
         __syncthreads();
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t q = q0 + 32 * b + (lane & 31);
         if (q >= n) continue;
         uint16_t* o = dQ + (q * H + h) * D;
@@ -454,10 +474,10 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dq(int64_t n, int H, const uin
 
 // ----------------------------------------------------------- dK, dV (cols)
 // dK_j = scale sum_i P_ij (dP_ij - D_i) Q_i and dV_j = sum_i P_ij dO_i, with
-// the wavefront owning 64 keys and the queries streaming through LDS.
+// the wavefront owning 32 NB keys and the queries streaming through LDS.
 
-template <int D>
-__global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const uint16_t* __restrict__ Q,
+template <int D, int NB>
+__global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 2 : 1))) void k_full_dkdv(int64_t n, int H, const uint16_t* __restrict__ Q,
                                                        const uint16_t* __restrict__ K,
                                                        const uint16_t* __restrict__ V,
                                                        const uint16_t* __restrict__ dO,
@@ -474,16 +494,16 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
     int64_t row0;
     if (!wg_coords(n, H, h, row0)) return;
     const int lane = lane_id();
-    const int64_t k0 = row0 + (threadIdx.x / kWave) * kOwn;
-    Frag<D> kf[2], vf[2];
+    const int64_t k0 = row0 + (threadIdx.x / kWave) * 32 * NB;
+    Frag<D> kf[NB], vf[NB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         kf[b].load(K, k0 + 32 * b + (lane & 31), n, H, h, lane);
         vf[b].load(V, k0 + 32 * b + (lane & 31), n, H, h, lane);
     }
-    f32x16_t dk[2][D / 32], dv[2][D / 32];
+    f32x16_t dk[NB][D / 32], dv[NB][D / 32];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) dk[b][db] = dv[b][db] = zero16();
 
@@ -496,7 +516,7 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
             sD[buf][threadIdx.x] = qn < n ? Dv[qn * H + h] : 0.f;
         }
     };
-    Stager<D, kThr> gq, gg;
+    Stager<D, kRowsWg / (32 * NB) * kWave> gq, gg;
     gq.load(Q, 0, n, H, h);
     gg.load(dO, 0, n, H, h);
     gq.store_rm(sQ[0]);
@@ -516,16 +536,17 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
         }
 #pragma unroll
         for (int qb = 0; qb < kStage / 32; ++qb) {
-            f32x16_t s[2], dp[2];
-            s[0] = s[1] = dp[0] = dp[1] = zero16();
+            f32x16_t s[NB], dp[NB];
+            #pragma unroll
+            for (int b = 0; b < NB; ++b) s[b] = dp[b] = zero16();
 #pragma unroll
             for (int c = 0; c < D / 16; ++c) {
                 const bf16x8_t a = lds_row8<D>(sQ[buf], 32 * qb + (lane & 31), c, lane);
-                s[0] = mma(a, kf[0].v[c], s[0]);
-                s[1] = mma(a, kf[1].v[c], s[1]);
+                #pragma unroll
+                for (int b = 0; b < NB; ++b) s[b] = mma(a, kf[b].v[c], s[b]);
                 const bf16x8_t g = lds_row8<D>(sG[buf], 32 * qb + (lane & 31), c, lane);
-                dp[0] = mma(g, vf[0].v[c], dp[0]);
-                dp[1] = mma(g, vf[1].v[c], dp[1]);
+                #pragma unroll
+                for (int b = 0; b < NB; ++b) dp[b] = mma(g, vf[b].v[c], dp[b]);
             }
             // rows of accumulator element i: 32 qb + 8 (i/4) + 4 (lane/32) + i%4
             float Lr[16], Dr[16];
@@ -537,9 +558,9 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
                 Lr[4 * j] = lv.x, Lr[4 * j + 1] = lv.y, Lr[4 * j + 2] = lv.z, Lr[4 * j + 3] = lv.w;
                 Dr[4 * j] = dv4.x, Dr[4 * j + 1] = dv4.y, Dr[4 * j + 2] = dv4.z, Dr[4 * j + 3] = dv4.w;
             }
-            bf16x8_t pb[2][2], sb[2][2];
+            bf16x8_t pb[NB][2], sb[NB][2];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
+            for (int b = 0; b < NB; ++b) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const float p = ex2(fmaf(s[b][i], sl2, -Lr[i]));
@@ -556,11 +577,11 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
 #pragma unroll
                 for (int half = 0; half < 2; ++half) {
                     const bf16x8_t g = lds_perm8(sGt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
-                    dv[0][db] = mma(g, pb[0][half], dv[0][db]);
-                    dv[1][db] = mma(g, pb[1][half], dv[1][db]);
+                    #pragma unroll
+                    for (int b = 0; b < NB; ++b) dv[b][db] = mma(g, pb[b][half], dv[b][db]);
                     const bf16x8_t a = lds_perm8(sQt[buf], 32 * db + (lane & 31), 32 * qb + 16 * half, lane);
-                    dk[0][db] = mma(a, sb[0][half], dk[0][db]);
-                    dk[1][db] = mma(a, sb[1][half], dk[1][db]);
+                    #pragma unroll
+                    for (int b = 0; b < NB; ++b) dk[b][db] = mma(a, sb[b][half], dk[b][db]);
                 }
         }
         if (t + 1 < stages) {
@@ -573,7 +594,7 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
         __syncthreads();
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < NB; ++b) {
         const int64_t key = k0 + 32 * b + (lane & 31);
         if (key >= n) continue;
         uint16_t* ok = dK + (key * H + h) * D;
@@ -598,8 +619,9 @@ __global__ __launch_bounds__(kThr, 1) void k_full_dkdv(int64_t n, int H, const u
 // Sparse layers: the dense tiles of the plan (§3.4), computed whole on the
 // matrix cores with the tile's bit mask deciding which pairs are edges.  The
 // row-owned kernels walk a tile row's dense tiles, the column-owned kernel a
-// tile column's; a workgroup has T/64 wavefronts of 64 owned rows (two MFMA
-// blocks) and stages the partners 64 at a time.  Each kernel leaves fp32
+// tile column's (in chunks of tiles); a workgroup has T/32 wavefronts of 32
+// owned rows (one MFMA block each, kTileNB) and stages the partners 64 at a
+// time.  Each kernel leaves fp32
 // partial sums per (node, head) for the edge kernels, which add the remainder
 // edges and finish every row and column.  A row may have no edge in a tile:
 // its weights are exactly zero (masked scores are -inf, and an all-masked
@@ -1303,7 +1325,7 @@ template <int D>
 gt_status full_fwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V, float sl2,
                         uint16_t* O, float* LSE, hipStream_t s) {
     if (n <= 0) return GT_OK;
-    k_full_fwd<D><<<full_grid(n, H), kThr, 0, s>>>(n, H, Q, K, V, sl2, O, LSE);
+    k_full_fwd<D, kFullFwdNB><<<full_grid(n, H), kFullFwdThr, 0, s>>>(n, H, Q, K, V, sl2, O, LSE);
     GT_LAUNCH_CHECK("full_fwd_bf16");
     return GT_OK;
 }
@@ -1313,9 +1335,9 @@ gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, 
                         const uint16_t* O, const uint16_t* dO, const float* LSE, float sl2, float scale,
                         uint16_t* dQ, uint16_t* dK, uint16_t* dV, float* Dv, hipStream_t s) {
     if (n <= 0) return GT_OK;
-    k_full_dq<D><<<full_grid(n, H), kThr, 0, s>>>(n, H, Q, K, V, O, dO, LSE, sl2, scale, dQ, Dv);
+    k_full_dq<D, kFullBwdNB><<<full_grid(n, H), kFullBwdThr, 0, s>>>(n, H, Q, K, V, O, dO, LSE, sl2, scale, dQ, Dv);
     GT_LAUNCH_CHECK("full_bwd_bf16 dq");
-    k_full_dkdv<D><<<full_grid(n, H), kThr, 0, s>>>(n, H, Q, K, V, dO, LSE, Dv, sl2, scale, dK, dV);
+    k_full_dkdv<D, kFullBwdNB><<<full_grid(n, H), kFullBwdThr, 0, s>>>(n, H, Q, K, V, dO, LSE, Dv, sl2, scale, dK, dV);
     GT_LAUNCH_CHECK("full_bwd_bf16 dkdv");
     return GT_OK;
 }
