@@ -138,6 +138,9 @@ def test_hub_tile_rows_and_columns_in_chunks(gt):
     for T in (64, 128):
         run_case(gt, rowptr, col, 4, 64, "bf16", taus=(0, 50_000), T=T, seed=T + 1)
     run_case(gt, rowptr, col, 8, 32, "bf16", taus=(10_000,), T=128, seed=9)
+    # every merge geometry: D / 4 lanes per row, T / (256 / (D / 4)) row blocks per (tile row, head)
+    for H, d, T in ((16, 64, 64), (1, 32, 64), (2, 64, 128), (16, 32, 128)):
+        run_case(gt, rowptr, col, H, d, "bf16", taus=(0,), T=T, seed=H * d + T, bwd=True)
 
 
 def test_bitwise_deterministic(gt):
