@@ -404,7 +404,7 @@ def copy_probe():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "the library runs on one GPU; --gpus must be 1 (the sharded path is a design, not built)"}))
         sys.exit(2)
     if args.copy_probe:
         copy_probe()

@@ -9,7 +9,7 @@ CSR}, ascending.
 
 Tiles (§3.4, cluster sparsity and transfer strategy).  The paper cuts the
 clustered S x S layout into a grid of square blocks and treats each block by
-how full it is, the fullness being the share of non-zero entries.  This build
+how full it is, the fullness being the share of non-zero entries.  The library
 reads that as an exact execution plan on T x T tiles:
 
 * R = ceil(N / T) tile rows and columns; tile (I, J) holds the edges (i, j) with

@@ -4,7 +4,7 @@ Oracle - test infrastructure only (see the package docstring).
 
 §3.3 (utilisation of graph cluster) reorders the nodes so that each cluster's
 nodes get neighbouring ids, using METIS.  METIS is a third-party multilevel
-partitioner whose output cannot be reproduced bit for bit, so this build reads
+partitioner whose output cannot be reproduced bit for bit, so the library reads
 the step as "any deterministic community-finding node order" and fixes one:
 label propagation with hashed tie-breaks and hashed partial activation,
 followed by a sort by (label, -degree, id).  The definition:
