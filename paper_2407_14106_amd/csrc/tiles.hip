@@ -20,10 +20,12 @@ constexpr int kThreads = 256;      // the long-row kernels
 constexpr int kTileThreads = 1024;  // one workgroup per tile row: 16 wavefronts share its LDS count table
 constexpr int kMaxR = 16384;
 constexpr uint32_t kDense = 0x80000000u;
-constexpr int kHash = 256;  // LDS slots that gather the remainder column counts of a workgroup
+// LDS slots that gather the remainder column counts of a workgroup (the most
+// that keeps two tile-row workgroups per CU beside the 64 KiB count table)
+constexpr int kHash = 1024;
 constexpr uint32_t kEmpty = 0xFFFFFFFFu;
 
-__device__ __forceinline__ int hash_slot(uint32_t c) { return int((c * 2654435761u) >> 24); }
+__device__ __forceinline__ int hash_slot(uint32_t c) { return int((c * 2654435761u) >> 22); }
 
 // Exclusive prefix of a 0/1 flag over the workgroup, in thread order; *total = the sum.
 __device__ __forceinline__ int64_t block_flag_scan(bool flag, int64_t* s, int64_t* total) {
