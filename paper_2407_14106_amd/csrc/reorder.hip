@@ -31,6 +31,7 @@ constexpr int kWaveTab = 2 * kWaveTabRowMax;  // per-wavefront table entries
 constexpr int kLdsTable = 8192;      // entries (int32 key + uint32 count): 64 KiB
 constexpr int kLdsRowMax = kLdsTable / 2;
 constexpr int kBlock = 256;
+constexpr int kBigRowBlock = 1024;  // threads per row of 4,097 to 2^16 edges (a few rows, one workgroup each)
 constexpr int kMaxSweeps = 1000;
 constexpr int kBigGrid = 1024;  // workgroups sharing each very long row
 constexpr int64_t kHugeRow = int64_t(1) << 16;
@@ -241,23 +242,25 @@ __global__ __launch_bounds__(kBlock) void k_lp_sub(const int32_t* list, const in
 
 // ------------------------------------------------------------- workgroup rows
 
+template <int BS = kBlock>
 __device__ __forceinline__ int block_max_i32(int v, int* s) {
     v = wave_max(v);
     const int w = threadIdx.x / kWave;
     if (lane_id() == 0) s[w] = v;
     __syncthreads();
     int r = s[0];
-    for (int i = 1; i < kBlock / kWave; ++i) r = s[i] > r ? s[i] : r;
+    for (int i = 1; i < BS / kWave; ++i) r = s[i] > r ? s[i] : r;
     __syncthreads();
     return r;
 }
+template <int BS = kBlock>
 __device__ __forceinline__ uint64_t block_min_u64(uint64_t v, uint64_t* s) {
     v = wave_min_u64(v);
     const int w = threadIdx.x / kWave;
     if (lane_id() == 0) s[w] = v;
     __syncthreads();
     uint64_t r = s[0];
-    for (int i = 1; i < kBlock / kWave; ++i) r = s[i] < r ? s[i] : r;
+    for (int i = 1; i < BS / kWave; ++i) r = s[i] < r ? s[i] : r;
     __syncthreads();
     return r;
 }
@@ -302,16 +305,16 @@ __device__ __forceinline__ void tab_add_wave(int* tk, int* tc, int64_t cap, bool
 
 // One workgroup per listed row.  Table: keys (label or -1) and counts, in LDS
 // (rows up to kLdsRowMax) or in the workspace (up to kHugeRow).
-template <bool kGlobal>
-__global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const int64_t* list_len,
+template <bool kGlobal, int BS>
+__global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int64_t* list_len,
                                                      const int64_t* rowptr, const int32_t* col,
                                                      const int32_t* lab_in, int32_t* lab_out, uint64_t key,
                                                      const uint32_t* flag_prev, uint32_t* flag_next,
                                                      int* gkeys, int* gcnts, const int64_t* big_off) {
     __shared__ int s_keys[kGlobal ? 1 : kLdsTable];
     __shared__ int s_cnts[kGlobal ? 1 : kLdsTable];
-    __shared__ int s_red[kBlock / kWave];
-    __shared__ uint64_t s_red64[kBlock / kWave];
+    __shared__ int s_red[BS / kWave];
+    __shared__ uint64_t s_red64[BS / kWave];
     const bool converged = *flag_prev == 0;
     const int64_t len = *list_len;
     for (int64_t idx = blockIdx.x; idx < len; idx += gridDim.x) {
@@ -327,14 +330,14 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
         while (cap < 2 * deg) cap <<= 1;
         int* tk = kGlobal ? gkeys + big_off[idx] : s_keys;
         int* tc = kGlobal ? gcnts + big_off[idx] : s_cnts;
-        for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+        for (int64_t s = threadIdx.x; s < cap; s += BS) {
             tk[s] = -1;
             tc[s] = 0;
         }
         if (kGlobal) __threadfence();
         __syncthreads();
         // wave-uniform rounds: each wavefront takes 64 consecutive edges per round
-        for (int64_t base = a + (threadIdx.x & ~(kWave - 1)); base < b; base += kBlock) {
+        for (int64_t base = a + (threadIdx.x & ~(kWave - 1)); base < b; base += BS) {
             const int64_t e = base + lane_id();
             const int c = e < b ? col[e] : int(v);
             const bool valid = c != v;
@@ -343,33 +346,33 @@ __global__ __launch_bounds__(kBlock) void k_lp_block(const int32_t* list, const 
         if (kGlobal) __threadfence();
         __syncthreads();
         int best = 0, own_cnt = 0;
-        for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+        for (int64_t s = threadIdx.x; s < cap; s += BS) {
             const int k = tab_load<kGlobal>(&tk[s]);
             if (k < 0) continue;
             const int c = tab_load<kGlobal>(&tc[s]);
             best = c > best ? c : best;
             if (k == own) own_cnt = c;
         }
-        best = block_max_i32(best, s_red);
-        own_cnt = block_max_i32(own_cnt, s_red);
+        best = block_max_i32<BS>(best, s_red);
+        own_cnt = block_max_i32<BS>(own_cnt, s_red);
         int cand = own;
         if (best > 0 && own_cnt != best) {
             uint64_t hbest = ~0ull;
-            for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+            for (int64_t s = threadIdx.x; s < cap; s += BS) {
                 const int k = tab_load<kGlobal>(&tk[s]);
                 if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 hbest = h < hbest ? h : hbest;
             }
-            hbest = block_min_u64(hbest, s_red64);
+            hbest = block_min_u64<BS>(hbest, s_red64);
             uint64_t lbest = ~0ull;
-            for (int64_t s = threadIdx.x; s < cap; s += kBlock) {
+            for (int64_t s = threadIdx.x; s < cap; s += BS) {
                 const int k = tab_load<kGlobal>(&tk[s]);
                 if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
                 if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
                 lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
             }
-            cand = int(block_min_u64(lbest, s_red64));
+            cand = int(block_min_u64<BS>(lbest, s_red64));
         }
         if (threadIdx.x == 0) {
             lab_out[v] = is_active(v, key) ? cand : own;
@@ -828,10 +831,10 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         k_lp_wavetab<<<1024, kBlock, 0, stream>>>(r.wmed_list, r.pos_wmed + n, rowptr, col, in, out, key,
                                                   r.flags + t, r.flags + t + 1);
         GT_LAUNCH_CHECK("reorder_lp_wavetab");
-        k_lp_block<false><<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
+        k_lp_block<false, kBlock><<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
                                                        r.flags + t, r.flags + t + 1, nullptr, nullptr, nullptr);
         GT_LAUNCH_CHECK("reorder_lp_lds");
-        k_lp_block<true><<<256, kBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in, out, key,
+        k_lp_block<true, kBigRowBlock><<<256, kBigRowBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in, out, key,
                                                      r.flags + t, r.flags + t + 1, r.tab_keys, r.tab_cnts,
                                                      r.big_off);
         GT_LAUNCH_CHECK("reorder_lp_global");
