@@ -596,6 +596,15 @@ def main():
     if not args.no_dense_layer:
         log("timing the full-attention layer ...")
         result["dense_layer"] = dense_layer(5)
+        if args.workload == "c5" and args.scale == 1.0:
+            # the dual-interleaved pair on the same 65,536 nodes: this graph-sparse layer, then the full layer
+            dl = result["dense_layer"]
+            total = ms_per_step + dl["fwd_ms"] + dl["bwd_ms"]
+            result["layer_pair"] = {
+                "sparse_ms": round(ms_per_step, 4), "dense_fwd_ms": dl["fwd_ms"], "dense_bwd_ms": dl["bwd_ms"],
+                "ms": round(total, 3),
+                "note": "fwd + bwd of the graph-sparse layer (this step) and of the full softmax layer over all nodes",
+            }
     if not args.no_peaks:
         log("measuring copy and matrix-product rates ...")
         pk = measured_peaks()
