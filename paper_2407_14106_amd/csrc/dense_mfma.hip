@@ -421,7 +421,10 @@ __global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_
                 for (int b = 0; b < NB; ++b) dp[b] = mma(v, gf[b].v[c], dp[b]);
             }
             const int64_t key0 = kbase + 32 * kb;
-            if (key0 + 32 > n) {
+            // ragged last block; marked unlikely so that the compiler keeps the masking
+            // out of the other blocks (measured: the backward 1.4% faster, the
+            // forward no faster)
+            if (__builtin_expect(key0 + 32 > n, 0)) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i)
                     if (key0 + crow(i, lane) >= n)
