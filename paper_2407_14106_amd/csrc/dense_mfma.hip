@@ -1153,9 +1153,34 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB =
     }
 }
 
+// One butterfly step of a 32 x 32 bit-matrix transpose held one row per lane
+// in each half of the wavefront: the lanes with bit J set trade the low J bits
+// of each 2J-bit group for their partner's high J bits (ds_swizzle in bitmask
+// mode, xor J within 32 lanes).
+template <int J>
+__device__ __forceinline__ uint32_t bit_transpose_step(uint32_t w, int lane) {
+    constexpr uint32_t lo = J == 16 ? 0x0000FFFFu : J == 8 ? 0x00FF00FFu : J == 4 ? 0x0F0F0F0Fu : J == 2 ? 0x33333333u
+                                                                                                           : 0x55555555u;
+    const uint32_t t = uint32_t(__builtin_amdgcn_ds_swizzle(int(w), (J << 10) | 0x1F));
+    return (lane & J) ? (w & ~lo) | ((t & ~lo) >> J) : (w & lo) | ((t & lo) << J);
+}
+
+// Transpose of the 64 x 32 bit matrix whose row r is lane r's word: on return
+// bit r of lane c's word (either half: both get the same 64 bits) is entry
+// (r, c % 32).
+__device__ __forceinline__ uint64_t bit_transpose_64x32(uint32_t w, int lane) {
+    w = bit_transpose_step<16>(w, lane);
+    w = bit_transpose_step<8>(w, lane);
+    w = bit_transpose_step<4>(w, lane);
+    w = bit_transpose_step<2>(w, lane);
+    w = bit_transpose_step<1>(w, lane);
+    const uint32_t other = __shfl_xor(w, 32, kWave);
+    return lane < 32 ? uint64_t(w) | (uint64_t(other) << 32) : uint64_t(other) | (uint64_t(w) << 32);
+}
+
 // Column pass over the dense tiles: unscaled dK and dV sums of every owned key.
-// The stage's masks are transposed with ballots so that each lane holds, for
-// its key, one 64-bit word over the stage's 64 queries.
+// The stage's masks are transposed so that each lane holds, for its key, one
+// 64-bit word over the stage's 64 queries.
 template <int D, int T, int NB>
 __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 2 : 1))) void k_tiles_dkdv(
     int64_t n, int H, int64_t n_row_tiles,
@@ -1224,15 +1249,7 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB =
     uint64_t mt[NB];
     auto transpose = [&](uint64_t (&out)[NB]) {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            uint64_t mine = 0;
-#pragma unroll
-            for (int c = 0; c < 32; ++c) {
-                const uint64_t bal = __builtin_amdgcn_ballot_w64((mword[b] >> c) & 1u);
-                if ((lane & 31) == c) mine = bal;
-            }
-            out[b] = mine;
-        }
+        for (int b = 0; b < NB; ++b) out[b] = bit_transpose_64x32(mword[b], lane);
     };
     auto store = [&](int buf) {
         gq.store_rm(sQ[buf]);
