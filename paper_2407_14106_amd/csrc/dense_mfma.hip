@@ -669,21 +669,38 @@ __device__ __forceinline__ int64_t out_row(int64_t q, int64_t I, int64_t slot, i
     return slot < 0 ? q : slot * T + (q - I * T);
 }
 
-// The plan in one workgroup (a tile plan has at most 16,384 tile rows): each
-// thread sums a contiguous run of rows (chunks, extra slots, rows with extra
-// slots), a wavefront scan plus one pass over the wavefront totals, then the
-// runs are written out with the list of rows that have extra slots.
+// The plan in one workgroup (a tile plan has at most 16,384 tile rows).
+// Wavefront w owns rows [1024 w, 1024 w + 1024) in 16 rounds of 64 consecutive
+// rows (one per lane), so every load and store is coalesced: the wavefront
+// totals give each wavefront its base, then each round's wavefront scan, plus
+// the running total of the rounds before it, gives every row its chunk
+// offset, extra-slot offset and place in the list of rows with extra slots.
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / kWave;
 constexpr int64_t kPlanMaxRows = 16384;
+constexpr int kPlanRounds = int(kPlanMaxRows / kPlanThreads);
 
-__device__ __forceinline__ int64_t wave_incl_scan(int64_t x) {
-    const int lane = lane_id();
+// Inclusive wavefront sum scan on DPP moves (no LDS round trips): shifts by
+// 1, 2, 4 and 8 lanes scan each 16-lane row; broadcasting lane 15 into rows 1
+// and 3, then lane 31 into rows 2 and 3, adds the totals of the rows before.
+// Lanes a move does not reach take 0 (the `old` operand).
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+    return uint32_t(__builtin_amdgcn_update_dpp(0, int(x), Ctrl, RowMask, 0xF, false));
+}
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
+    x += dpp_u32<0x111, 0xF>(x);  // row_shr:1
+    x += dpp_u32<0x112, 0xF>(x);  // row_shr:2
+    x += dpp_u32<0x114, 0xF>(x);  // row_shr:4
+    x += dpp_u32<0x118, 0xF>(x);  // row_shr:8
+    x += dpp_u32<0x142, 0xA>(x);  // row_bcast:15 into rows 1, 3
+    x += dpp_u32<0x143, 0xC>(x);  // row_bcast:31 into rows 2, 3
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
 #pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const int64_t y = __shfl_up(x, o, kWave);
-        if (lane >= o) x += y;
-    }
+    for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
     return x;
 }
 
@@ -692,25 +709,34 @@ __global__ __launch_bounds__(kPlanThreads) void k_tile_chunk_plan1(int64_t R, co
                                                                    int64_t* __restrict__ extra_off,
                                                                    int32_t* __restrict__ merge_rows,
                                                                    uint32_t* __restrict__ merge_cnt) {
-    __shared__ int64_t s_w[3][kPlanWaves];
+    // Counts fit in 32 bits: at most R <= 16,384 tiles per row and R rows.
+    __shared__ uint32_t s_w[3][kPlanWaves];
     const int t = threadIdx.x, w = t / kWave, lane = lane_id();
-    const int64_t per = cdiv(R, int64_t(kPlanThreads));
-    const int64_t a = t * per < R ? t * per : R, b = a + per < R ? a + per : R;
-    int64_t c = 0, e = 0, m = 0;
-    for (int64_t I = a; I < b; ++I) {
-        const int64_t k = cdiv(ptr[I + 1] - ptr[I], CH);
-        c += k;
-        e += k > 1 ? k - 1 : 0;
-        m += k > 1 ? 1 : 0;
+    const int64_t base = int64_t(w) * (kPlanRounds * kWave);
+    uint32_t k[kPlanRounds];  // chunks of row base + 64 j + lane
+#pragma unroll
+    for (int j = 0; j < kPlanRounds; ++j) {
+        const int64_t I = base + kWave * j + lane;
+        k[j] = I < R ? (uint32_t(ptr[I + 1] - ptr[I]) + uint32_t(CH) - 1u) / uint32_t(CH) : 0u;
     }
-    const int64_t ic = wave_incl_scan(c), ie = wave_incl_scan(e), im = wave_incl_scan(m);
-    if (lane == kWave - 1) {
-        s_w[0][w] = ic;
-        s_w[1][w] = ie;
-        s_w[2][w] = im;
+    uint32_t c = 0, e = 0, m = 0;
+#pragma unroll
+    for (int j = 0; j < kPlanRounds; ++j) {
+        c += k[j];
+        e += k[j] > 1u ? k[j] - 1u : 0u;
+        m += k[j] > 1u ? 1u : 0u;
+    }
+    c = wave_sum_u32(c);
+    e = wave_sum_u32(e);
+    m = wave_sum_u32(m);
+    if (lane == 0) {
+        s_w[0][w] = c;
+        s_w[1][w] = e;
+        s_w[2][w] = m;
     }
     __syncthreads();
-    int64_t bc = 0, be = 0, bm = 0, tc = 0, te = 0, tm = 0;
+    uint32_t bc = 0, be = 0, bm = 0, tc = 0, te = 0, tm = 0;
+#pragma unroll 1
     for (int x = 0; x < kPlanWaves; ++x) {
         if (x < w) {
             bc += s_w[0][x];
@@ -721,23 +747,24 @@ __global__ __launch_bounds__(kPlanThreads) void k_tile_chunk_plan1(int64_t R, co
         te += s_w[1][x];
         tm += s_w[2][x];
     }
-    c = bc + ic - c;
-    e = be + ie - e;
-    m = bm + im - m;
-    for (int64_t I = a; I < b; ++I) {
-        chunk_off[I] = c;
-        extra_off[I] = e;
-        const int64_t k = cdiv(ptr[I + 1] - ptr[I], CH);
-        c += k;
-        if (k > 1) {
-            e += k - 1;
-            merge_rows[m++] = int32_t(I);
+#pragma unroll
+    for (int j = 0; j < kPlanRounds; ++j) {
+        const int64_t I = base + kWave * j + lane;
+        const uint32_t xe = k[j] > 1u ? k[j] - 1u : 0u, xm = k[j] > 1u ? 1u : 0u;
+        const uint32_t ic = wave_incl_scan_u32(k[j]), ie = wave_incl_scan_u32(xe), im = wave_incl_scan_u32(xm);
+        if (I < R) {
+            chunk_off[I] = int64_t(bc + ic - k[j]);
+            extra_off[I] = int64_t(be + ie - xe);
+            if (xm) merge_rows[bm + im - 1u] = int32_t(I);
         }
+        bc += uint32_t(__builtin_amdgcn_readlane(int(ic), kWave - 1));
+        be += uint32_t(__builtin_amdgcn_readlane(int(ie), kWave - 1));
+        bm += uint32_t(__builtin_amdgcn_readlane(int(im), kWave - 1));
     }
     if (t == 0) {
-        chunk_off[R] = tc;
-        extra_off[R] = te;
-        *merge_cnt = uint32_t(tm);
+        chunk_off[R] = int64_t(tc);
+        extra_off[R] = int64_t(te);
+        *merge_cnt = tm;
     }
 }
 
