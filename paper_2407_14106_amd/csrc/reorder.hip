@@ -16,6 +16,8 @@
 // All three compute the same function of the neighbour-label multiset.
 #include <limits.h>
 
+#include <mutex>
+
 #include "prim.h"
 
 namespace gt {
@@ -701,6 +703,7 @@ struct ReorderWs {
     int64_t* huge_off;
     int* tab_keys;
     int* tab_cnts;
+    int64_t* class_cnt;  // [kClasses]: rows of each list class, for the host
     int* big_best;
     int* big_own;
     unsigned long long* big_hbest;
@@ -710,6 +713,48 @@ struct ReorderWs {
     ScanTmp scan;
     SortTmp sort;
 };
+
+// The row counts of the list classes (the totals of their scans), gathered
+// so that one copy brings them to the host.
+enum { kClsS16, kClsS32, kClsWmed, kClsMed, kClsBig, kClsHuge, kClasses };
+__global__ void k_class_counts(int64_t n, const int64_t* s16, const int64_t* s32, const int64_t* wmed,
+                               const int64_t* med, const int64_t* big, const int64_t* huge, int64_t* out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    out[kClsS16] = s16[n];
+    out[kClsS32] = s32[n];
+    out[kClsWmed] = wmed[n];
+    out[kClsMed] = med[n];
+    out[kClsBig] = big[n];
+    out[kClsHuge] = huge[n];
+}
+
+// A second stream per device for the rows of more than 4,096 edges: their
+// workgroups run long on a few CUs while the other classes of a sweep run
+// beside them (every class reads the sweep's input labels and writes only its
+// own rows).  The stream and its fork/join events are created on first use and
+// kept for the life of the process; a call holds `mu` while it records and
+// waits on them, so calls from several host threads do not interleave.
+struct SideStream {
+    std::mutex mu;
+    hipStream_t s = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    bool ready() {  // with mu held
+        if (!s && hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) s = nullptr;
+        if (!fork && hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess) fork = nullptr;
+        if (!join && hipEventCreateWithFlags(&join, hipEventDisableTiming) != hipSuccess) join = nullptr;
+        return s && fork && join;
+    }
+};
+constexpr int kMaxDevices = 64;
+SideStream& side_stream(int dev) {
+    static SideStream per_dev[kMaxDevices];
+    return per_dev[dev];
+}
+
+inline unsigned grid_cap(int64_t rows, int64_t per_block, unsigned cap) {
+    const int64_t g = cdiv(rows, per_block);
+    return unsigned(g < 1 ? 1 : (g > cap ? cap : g));
+}
 
 ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     ReorderWs r;
@@ -744,6 +789,7 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     const int64_t tab = 4 * (nnz > 0 ? nnz : 1);  // sum over big rows of cap <= 4 * deg
     r.tab_keys = ws.take<int>(size_t(tab));
     r.tab_cnts = ws.take<int>(size_t(tab));
+    r.class_cnt = ws.take<int64_t>(kClasses);
     r.big_best = ws.take<int>(n1);
     r.big_own = ws.take<int>(n1);
     r.big_hbest = ws.take<unsigned long long>(n1);
@@ -809,48 +855,86 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if ((st = fill_u32(r.flags, iters + 1, 0, stream)) != GT_OK) return st;
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
-    int64_t n_huge = 0;
-    GT_HIP(hipMemcpyAsync(&n_huge, r.pos_huge + n, 8, hipMemcpyDeviceToHost, stream));
+    // the class sizes on the host: empty classes are not launched and grids fit the lists
+    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s16, r.pos_s32, r.pos_wmed, r.pos_med, r.pos_big, r.pos_huge,
+                                         r.class_cnt);
+    GT_LAUNCH_CHECK("reorder_class_counts");
+    int64_t cnt[kClasses] = {};
+    GT_HIP(hipMemcpyAsync(cnt, r.class_cnt, sizeof(cnt), hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
+    const int64_t n_huge = cnt[kClsHuge], n_big = cnt[kClsBig];
     BigRows br{r.huge_list, r.pos_huge + n, r.huge_off, r.tab_keys, r.tab_cnts, r.big_best, r.big_own,
                r.big_hbest, r.big_lbest};
     const unsigned gw = grid_for(n, kBlock / kWave, 65536);
-    const unsigned gs = grid_for(n, kBlock / kWave * 2, 16384);
+    const unsigned g16 = grid_cap(cnt[kClsS16], kBlock / kSub16, 16384);
+    const unsigned g32 = grid_cap(cnt[kClsS32], kBlock / kSub32, 16384);
+    const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
+    const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
+    const unsigned gbig = grid_cap(n_big, 1, 256);
+    // rows of more than 4,096 edges go to the side stream when there is one
+    SideStream* ss = nullptr;
+    std::unique_lock<std::mutex> side_lock;
+    int dev = -1;
+    if ((n_big > 0 || n_huge > 0) && hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kMaxDevices) {
+        SideStream& x = side_stream(dev);
+        side_lock = std::unique_lock<std::mutex>(x.mu);
+        if (x.ready()) ss = &x;
+        else side_lock.unlock();
+    }
+    const hipStream_t side = ss ? ss->s : nullptr;
+    const hipStream_t bs = side ? side : stream;
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
         const int32_t* in = r.lab[t & 1];
         int32_t* out = r.lab[(t + 1) & 1];
-        k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
-        GT_LAUNCH_CHECK("reorder_lp_wave");
-        k_lp_sub<kSub16><<<gs, kBlock, 0, stream>>>(r.s16_list, r.pos_s16 + n, rowptr, col, in, out, key,
-                                                    r.flags + t, r.flags + t + 1);
-        GT_LAUNCH_CHECK("reorder_lp_sub16");
-        k_lp_sub<kSub32><<<gs, kBlock, 0, stream>>>(r.s32_list, r.pos_s32 + n, rowptr, col, in, out, key,
-                                                    r.flags + t, r.flags + t + 1);
-        GT_LAUNCH_CHECK("reorder_lp_sub32");
-        k_lp_wavetab<<<1024, kBlock, 0, stream>>>(r.wmed_list, r.pos_wmed + n, rowptr, col, in, out, key,
-                                                  r.flags + t, r.flags + t + 1);
-        GT_LAUNCH_CHECK("reorder_lp_wavetab");
-        k_lp_block<false, kBlock><<<1024, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
-                                                       r.flags + t, r.flags + t + 1, nullptr, nullptr, nullptr);
-        GT_LAUNCH_CHECK("reorder_lp_lds");
-        k_lp_block<true, kBigRowBlock><<<256, kBigRowBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in, out, key,
-                                                     r.flags + t, r.flags + t + 1, r.tab_keys, r.tab_cnts,
-                                                     r.big_off);
-        GT_LAUNCH_CHECK("reorder_lp_global");
+        if (side) {
+            GT_HIP(hipEventRecord(ss->fork, stream));
+            GT_HIP(hipStreamWaitEvent(side, ss->fork, 0));
+        }
+        if (n_big > 0) {
+            k_lp_block<true, kBigRowBlock><<<gbig, kBigRowBlock, 0, bs>>>(r.big_list, r.pos_big + n, rowptr, col, in,
+                                                                       out, key, r.flags + t, r.flags + t + 1,
+                                                                       r.tab_keys, r.tab_cnts, r.big_off);
+            GT_LAUNCH_CHECK("reorder_lp_global");
+        }
         if (n_huge > 0) {
             const uint32_t* fp = r.flags + t;
-            k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp);
+            k_big_clear<<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, fp);
             GT_LAUNCH_CHECK("reorder_big_clear");
-            k_big_insert<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, in, fp);
+            k_big_insert<<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, col, in, fp);
             GT_LAUNCH_CHECK("reorder_big_insert");
-            k_big_reduce<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
-            k_big_reduce<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
-            k_big_reduce<2><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+            k_big_reduce<0><<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, in, key, fp);
+            k_big_reduce<1><<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, in, key, fp);
+            k_big_reduce<2><<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, in, key, fp);
             GT_LAUNCH_CHECK("reorder_big_reduce");
-            k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, in, out, key, fp, r.flags + t + 1);
+            k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, bs>>>(br, in, out, key, fp, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_big_decide");
         }
+        if (side) GT_HIP(hipEventRecord(ss->join, side));
+        k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
+        GT_LAUNCH_CHECK("reorder_lp_wave");
+        if (cnt[kClsS16] > 0) {
+            k_lp_sub<kSub16><<<g16, kBlock, 0, stream>>>(r.s16_list, r.pos_s16 + n, rowptr, col, in, out, key,
+                                                         r.flags + t, r.flags + t + 1);
+            GT_LAUNCH_CHECK("reorder_lp_sub16");
+        }
+        if (cnt[kClsS32] > 0) {
+            k_lp_sub<kSub32><<<g32, kBlock, 0, stream>>>(r.s32_list, r.pos_s32 + n, rowptr, col, in, out, key,
+                                                         r.flags + t, r.flags + t + 1);
+            GT_LAUNCH_CHECK("reorder_lp_sub32");
+        }
+        if (cnt[kClsWmed] > 0) {
+            k_lp_wavetab<<<gwt, kBlock, 0, stream>>>(r.wmed_list, r.pos_wmed + n, rowptr, col, in, out, key,
+                                                     r.flags + t, r.flags + t + 1);
+            GT_LAUNCH_CHECK("reorder_lp_wavetab");
+        }
+        if (cnt[kClsMed] > 0) {
+            k_lp_block<false, kBlock><<<gmed, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out,
+                                                                   key, r.flags + t, r.flags + t + 1, nullptr,
+                                                                   nullptr, nullptr);
+            GT_LAUNCH_CHECK("reorder_lp_lds");
+        }
+        if (side) GT_HIP(hipStreamWaitEvent(stream, ss->join, 0));
     }
     const int32_t* final_lab = r.lab[iters & 1];
     k_order_keys<<<g, 256, 0, stream>>>(n, final_lab, r.deg_off, r.sort_keys);
