@@ -303,12 +303,15 @@ gt_status radix_sort_u64(uint64_t* keys, uint32_t* values, int64_t n, int key_bi
 
 // =========================================================== CSR validation
 
-// Rows of up to kValidateShort entries are checked by one thread each; the
-// wavefront takes every longer row of its batch up to kLongRow entries
-// together, its lanes striding the row 64 entries apart and comparing each
-// entry with the one before it in memory.  Longer rows (a node adjacent to
-// every node) are checked chunk by chunk over the whole grid.
+// Rows of up to kValidateShort entries are checked by one thread each, which
+// loads kValidateBatch entries at a time before comparing them (one memory
+// latency per batch, not per entry); the wavefront takes every longer row of
+// its batch up to kLongRow entries together, its lanes striding the row 64
+// entries apart and comparing each entry with the one before it in memory.
+// Longer rows (a node adjacent to every node) are checked chunk by chunk over
+// the whole grid.
 constexpr int64_t kValidateShort = 256;
+constexpr int kValidateBatch = 8;
 
 __global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
                                uint32_t* flags) {
@@ -333,12 +336,18 @@ __global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, co
             } else if (b - a > kValidateShort) mid_row = true;
             else {
                 int64_t prev = -1;
-                for (int64_t e = a; e < b; ++e) {
-                    const int64_t c = col[e];
-                    if (c < 0 || c >= n) f |= kOutOfRange;
-                    if (c == prev) f |= kDuplicate;
-                    else if (c < prev) f |= kUnsorted;
-                    prev = c;
+                for (int64_t e0 = a; e0 < b; e0 += kValidateBatch) {
+                    int64_t c[kValidateBatch];
+#pragma unroll
+                    for (int k = 0; k < kValidateBatch; ++k) c[k] = e0 + k < b ? int64_t(col[e0 + k]) : 0;
+#pragma unroll
+                    for (int k = 0; k < kValidateBatch; ++k) {
+                        if (e0 + k >= b) break;
+                        if (c[k] < 0 || c[k] >= n) f |= kOutOfRange;
+                        if (c[k] == prev) f |= kDuplicate;
+                        else if (c[k] < prev) f |= kUnsorted;
+                        prev = c[k];
+                    }
                 }
             }
         }

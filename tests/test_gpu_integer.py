@@ -185,3 +185,33 @@ def test_gather_scatter_rows(gt):
     y = gt.gather_rows(x, perm)
     assert torch.equal(y, x[perm.long()])
     assert torch.equal(gt.scatter_rows(y, perm), x)
+
+
+def test_validation_errors_in_short_rows(gt):
+    # rows of up to 256 entries are checked by one thread in batches of 8 loads: plant each error on either side
+    # of a batch boundary and at the ends of rows of several lengths, next to rows that are valid
+    lens = [1, 7, 8, 9, 15, 16, 17, 100, 256]
+    rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    n = 300
+    good = np.concatenate([np.arange(L, dtype=np.int32) * 1 + (i % 5) for i, L in enumerate(lens)])
+    rp_n = np.concatenate([rp, np.full(n - len(lens), rp[-1])]).astype(np.int64)  # n rows, the last ones empty
+    gt.validate_csr(*dev_csr(rp_n, good))
+    for r, L in enumerate(lens):
+        a = int(rp[r])
+        for k in sorted({0, 6, 7, 8, 9, 15, 16, L - 1}):
+            if k >= L:
+                continue
+            cases = [(n + 3, gt.GT_ERR_OUT_OF_RANGE), (-1, gt.GT_ERR_OUT_OF_RANGE)]
+            if k > 0:
+                cases.append((int(good[a + k - 1]), gt.GT_ERR_DUPLICATE))
+                cases.append((int(good[a + k - 1]) - 1, gt.GT_ERR_UNSORTED))
+            for val, code in cases:
+                bad = good.copy()
+                bad[a + k] = val
+                if code == gt.GT_ERR_UNSORTED and val < 0:
+                    continue
+                say("validate short", L, k, val)
+                rp_d, cl_d = dev_csr(rp_n, bad)
+                with pytest.raises(gt.GtError) as e:
+                    gt.validate_csr(rp_d, cl_d)
+                assert e.value.status == code, (L, k, val)
