@@ -98,7 +98,11 @@ gt_status gt_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const i
  *   labels int32[n] out (may be NULL): final label of each (old) node
  *   sweeps_done (host, may be NULL): SYNC if given; sweeps that changed a label.
  * The CSR must satisfy the input convention (see gt_validate_csr); it is
- * validated here first (SYNC) and an invalid CSR returns its error code. */
+ * validated here first (SYNC) and an invalid CSR returns its error code.
+ * Rows of more than 4,096 entries are processed on a second stream of the
+ * library's own (one per device, default priority, kept for the life of the
+ * process), forked from and joined back to `stream` with events every sweep:
+ * the results are ordered on `stream` as for any other call. */
 size_t gt_reorder_workspace_size(int64_t n, int64_t nnz);
 gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
                      uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels, int32_t* sweeps_done,
