@@ -179,7 +179,11 @@ gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowptr, const in
 /* Fills every array of *plan.  The size fields must be those set by
  * gt_tiles_count for the same arguments and every array pointer a caller
  * allocation of the size given above.  The CSR is the one gt_tiles_count
- * validated. */
+ * validated.  When ws is the workspace gt_tiles_count used with the same
+ * arguments, its count results are taken from there if a checksum of them
+ * (recorded by gt_tiles_count, recomputed here: SYNC) still matches; any other
+ * workspace, or one written to in between, is counted again.  Either way the
+ * plan is the same. */
 gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
                          uint32_t tau_ppm, gt_tiles* plan, void* ws, size_t ws_bytes, hipStream_t stream);
 

@@ -11,6 +11,9 @@
 // written chunk by chunk over the whole grid.  The remainder's transpose and
 // the column-grouped tile list come from stable radix sorts, so every output
 // is deterministic.
+#include <mutex>
+#include <vector>
+
 #include "prim.h"
 
 namespace gt {
@@ -334,6 +337,10 @@ __global__ void k_u32_to_i32(int64_t m, const uint32_t* src, int32_t* dst) {
 
 struct TilesWs {
     uint32_t* flags;
+    unsigned long long* csum;  // checksum of the count results (kept below)
+    // The count results, one contiguous range [kept_begin, kept_end) of the
+    // workspace, so that gt_build_tiles can take them from gt_tiles_count's
+    // workspace: dense_per_tilerow .. dense_pre.
     int32_t* dense_per_tilerow;
     int32_t* sp_deg;
     int64_t* tmp_tile_rowptr;
@@ -350,6 +357,8 @@ struct TilesWs {
     uint32_t* dense_pre;   // [R, W]: dense tiles before each word
     int32_t* segcnt;       // [2 * long chunks]: remainder edges of each long-row segment
     int64_t* segoff;       // [2 * long chunks + 1]
+    const uint64_t* kept_begin;
+    int64_t kept_words;    // 8-byte words of the count results' range
     int W;
     ScanTmp scan;
     SortTmp sort;
@@ -360,27 +369,102 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
     const int64_t n1 = n > 0 ? n : 1, e1 = nnz > 0 ? nnz : 1;
     const int64_t R = cdiv(n1, T > 0 ? T : 1);
     t.flags = ws.take<uint32_t>(1);
+    t.csum = ws.take<unsigned long long>(1);
+    t.W = int(cdiv(R, 32));
     t.dense_per_tilerow = ws.take<int32_t>(R);
     t.sp_deg = ws.take<int32_t>(n1);
     t.tmp_tile_rowptr = ws.take<int64_t>(R + 1);
     t.tmp_sp_rowptr = ws.take<int64_t>(n1 + 1);
-    t.keys = ws.take<uint32_t>(e1);
-    t.vals = ws.take<uint32_t>(e1);
-    t.counts = ws.take<uint32_t>(n1 + 1);
     t.colcnt = ws.take<uint32_t>(n1);
     t.long_row_flag = ws.take<int32_t>(n1);
     t.long_col_flag = ws.take<int32_t>(n1);
     t.long_row_pos = ws.take<int64_t>(n1 + 1);
     t.long_col_pos = ws.take<int64_t>(n1 + 1);
-    t.W = int(cdiv(R, 32));
     t.dense_bits = ws.take<uint32_t>(size_t(R * t.W));
-    t.dense_pre = ws.take<uint32_t>(size_t(R * t.W));
+    t.dense_pre = ws.take<uint32_t>(size_t(R * t.W + 1));  // + 1: the range ends on an 8-byte word
+    {
+        const char* b = reinterpret_cast<const char*>(t.dense_per_tilerow);
+        const char* e = reinterpret_cast<const char*>(t.dense_pre + R * t.W + 1);
+        t.kept_begin = reinterpret_cast<const uint64_t*>(t.dense_per_tilerow);
+        t.kept_words = int64_t((e - b) / 8);
+    }
+    t.keys = ws.take<uint32_t>(e1);
+    t.vals = ws.take<uint32_t>(e1);
+    t.counts = ws.take<uint32_t>(n1 + 1);
     const int64_t segs = 2 * long_chunks_of(e1);
     t.segcnt = ws.take<int32_t>(size_t(segs));
     t.segoff = ws.take<int64_t>(size_t(segs + 1));
     t.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1 > segs + 1 ? n1 + 1 : segs + 1)));
     t.sort = sort_tmp(ws, e1, 4, true);
     return t;
+}
+
+// Checksum of the count results: the sum over the range's 8-byte words w_i of
+// mix64(w_i + i * 0x9E3779B97F4A7C15) (mod 2^64, so the order of the sums does
+// not matter); a changed or moved word changes it.
+__global__ __launch_bounds__(256) void k_ws_checksum(const uint64_t* __restrict__ p, int64_t words,
+                                                     unsigned long long* __restrict__ out) {
+    uint64_t acc = 0;
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < words; i += stride)
+        acc += mix64(p[i] + uint64_t(i) * 0x9E3779B97F4A7C15ull);
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const uint32_t lo = __shfl_xor(uint32_t(acc), o, kWave), hi = __shfl_xor(uint32_t(acc >> 32), o, kWave);
+        acc += (uint64_t(hi) << 32) | lo;
+    }
+    if (lane_id() == 0 && acc) atomicAdd(out, (unsigned long long)acc);
+}
+
+gt_status ws_checksum(const TilesWs& t, hipStream_t s) {
+    gt_status st = fill_u32(reinterpret_cast<uint32_t*>(t.csum), 2, 0u, s);
+    if (st != GT_OK) return st;
+    k_ws_checksum<<<grid_for(t.kept_words, 256, 2048), 256, 0, s>>>(t.kept_begin, t.kept_words, t.csum);
+    GT_LAUNCH_CHECK("tiles_checksum");
+    return GT_OK;
+}
+
+// What the last gt_tiles_count left in a workspace: its arguments and the
+// checksum of its count results.  gt_build_tiles with the same workspace and
+// arguments takes the counts from there when the checksum still matches.
+struct CountRecord {
+    const void* ws;
+    int64_t n, nnz;
+    const int64_t* rowptr;
+    const int32_t* col;
+    int32_t T;
+    uint32_t tau_ppm;
+    uint64_t sum;
+};
+std::mutex g_count_mu;
+std::vector<CountRecord> g_counts;  // at most kCountRecords, oldest first
+constexpr size_t kCountRecords = 16;
+
+void count_record_put(const CountRecord& r) {
+    std::lock_guard<std::mutex> lock(g_count_mu);
+    for (size_t i = 0; i < g_counts.size(); ++i)
+        if (g_counts[i].ws == r.ws) {
+            g_counts.erase(g_counts.begin() + i);
+            break;
+        }
+    if (g_counts.size() >= kCountRecords) g_counts.erase(g_counts.begin());
+    g_counts.push_back(r);
+}
+
+// Removes and returns the record of `ws` if its arguments match.
+bool count_record_take(const void* ws, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
+                       uint32_t tau_ppm, uint64_t& sum) {
+    std::lock_guard<std::mutex> lock(g_count_mu);
+    for (size_t i = 0; i < g_counts.size(); ++i) {
+        const CountRecord& r = g_counts[i];
+        if (r.ws != ws) continue;
+        const bool same = r.n == n && r.nnz == nnz && r.rowptr == rowptr && r.col == col && r.T == T &&
+                          r.tau_ppm == tau_ppm;
+        sum = r.sum;
+        g_counts.erase(g_counts.begin() + i);
+        return same;
+    }
+    return false;
 }
 
 gt_status check_common(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
@@ -458,17 +542,20 @@ extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowpt
     if ((st = read_validation(t.flags, stream)) != GT_OK) return st;
     if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
         return st;
+    if ((st = ws_checksum(t, stream)) != GT_OK) return st;
     const int64_t R = plan->n_row_tiles;
-    int64_t h[4] = {0, 0, 0, 0};
+    int64_t h[5] = {0, 0, 0, 0, 0};
     GT_HIP(hipMemcpyAsync(&h[0], t.tmp_tile_rowptr + R, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipMemcpyAsync(&h[1], t.tmp_sp_rowptr + n, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipMemcpyAsync(&h[2], t.long_row_pos + n, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipMemcpyAsync(&h[3], t.long_col_pos + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipMemcpyAsync(&h[4], t.csum, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
     plan->n_dense = h[0];
     plan->nnz_sparse = h[1];
     plan->n_long_rows = h[2];
     plan->n_long_cols = h[3];
+    count_record_put({ws_ptr, n, nnz, rowptr, col, T, tau_ppm, uint64_t(h[4])});
     return GT_OK;
 }
 
@@ -498,8 +585,24 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     }
     Ws ws(ws_ptr);
     TilesWs t = carve(ws, n, nnz, T);
-    if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) != GT_OK)
+    // the counts of the gt_tiles_count call that used this workspace with these
+    // arguments, if they are still there unchanged; else count again
+    bool reuse = false;
+    uint64_t want = 0;
+    if (count_record_take(ws_ptr, n, nnz, rowptr, col, T, tau_ppm, want)) {
+        if ((st = ws_checksum(t, stream)) != GT_OK) return st;
+        uint64_t have = 0;
+        GT_HIP(hipMemcpyAsync(&have, t.csum, 8, hipMemcpyDeviceToHost, stream));
+        GT_HIP(hipStreamSynchronize(stream));
+        reuse = have == want;
+    }
+    if (reuse) {
+        if ((st = copy_bytes(plan->tile_rowptr, t.tmp_tile_rowptr, size_t(R + 1) * 8, stream)) != GT_OK) return st;
+        if ((st = copy_bytes(plan->sp_rowptr, t.tmp_sp_rowptr, size_t(n + 1) * 8, stream)) != GT_OK) return st;
+    } else if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) !=
+               GT_OK) {
         return st;
+    }
     {
         const unsigned g = grid_for(n, 256, 8192);
         if (plan->n_long_rows > 0) {

@@ -335,8 +335,13 @@ def tau_to_ppm(tau: float) -> int:
     return int(round(float(tau) * 1e6))
 
 
-def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: int = 10000) -> Plan:
-    """Tile plan of the CSR at tile edge T and density threshold tau_ppm (parts per million)."""
+def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: int = 10000, *,
+                build_ws: torch.Tensor | None = None, between=None) -> Plan:
+    """Tile plan of the CSR at tile edge T and density threshold tau_ppm (parts per million).
+
+    gt_tiles_count and gt_build_tiles share one workspace, so the build takes the counts from it.  build_ws
+    gives the build call a workspace of its own instead, and between(ws) runs between the two calls; with
+    either, the build counts again (the library checks the workspace)."""
     lib = load_library()
     _check_csr(rowptr, col)
     n, nnz = rowptr.numel() - 1, col.numel()
@@ -365,6 +370,11 @@ def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: 
     }
     for k, v in arrays.items():
         setattr(c, k, v.data_ptr())
+    if between is not None:
+        between(ws)
+    if build_ws is not None:
+        _need(build_ws.numel() >= ws.numel() and build_ws.device == ws.device, "build_ws too small")
+        ws = build_ws
     _check(lib.gt_build_tiles(n, nnz, _ptr(rowptr), _ptr(col), T, tau_ppm, ctypes.byref(c), _ptr(ws), ws.numel(), st),
            "gt_build_tiles")
     arrays["tile_mask"] = arrays["tile_mask"].view(torch.int32)

@@ -105,6 +105,29 @@ def test_tiles_bit_exact(gt, name, rowptr, col, T):
     assert n >= 1
 
 
+@pytest.mark.parametrize("name", ["hubs_6000", "three_hubs_30000", "c3@0.02", "b1@0.1"])
+def test_tiles_counts_taken_or_recounted(gt, name):
+    # gt_build_tiles takes gt_tiles_count's counts from the shared workspace only while they are unchanged
+    # there: a workspace of its own, or one overwritten in between, makes it count again; every way gives the
+    # oracle's plan
+    rowptr, col = next((g[1], g[2]) for g in GRAPHS if g[0] == name)
+    rp, cl = dev_csr(rowptr, col)
+    for T, tau in ((64, 10000), (128, 50000)):
+        ref = OP.build_tiles(rowptr, col, T, tau)
+        ws_bytes = gt.load_library().gt_tiles_workspace_size(len(rowptr) - 1, len(col), T)
+        ways = {
+            "shared": {},
+            "own workspace": {"build_ws": torch.full((max(ws_bytes, 256),), 0x5A, dtype=torch.uint8,
+                                                     device=rp.device)},
+            "overwritten": {"between": lambda ws: ws.fill_(0xA5)},
+            "one byte changed": {"between": lambda ws: ws[ws.numel() // 3].add_(1)},
+        }
+        for way, kw in ways.items():
+            say("tiles counts", name, T, tau, way)
+            plan = gt.build_tiles(rp, cl, T, tau, **kw)
+            compare_plan(plan.to_numpy(), ref)
+
+
 def test_tiles_threshold_equality(gt):
     # a 64x64 tile with exactly 64 edges (density 1/64 = 15625 ppm): dense at 15625, sparse at 15626
     u = np.arange(64)
