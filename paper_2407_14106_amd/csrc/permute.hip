@@ -2,9 +2,12 @@
 // reorganised by cluster once the full sequence is on the device), and row
 // gathers/scatters of feature tensors.
 //
-// The relabelled CSR is produced by one stable radix sort of the packed keys
-// (iperm[row] << B) | iperm[col]: after sorting, the keys are grouped by new
-// row and ascending inside each row, which is exactly the new CSR order.
+// Rows move whole to their new place, so only each row's relabelled columns
+// need sorting.  A row of at most kShortRow entries is sorted by one wavefront
+// (a bitonic network across the lanes) and written straight to its place.
+// The longer rows' edges are packed as keys (new row << B) | new column and
+// put in order by one stable radix sort: sorted, they are grouped by new row
+// and ascending inside each row, each at its rank inside the row.
 #include "prim.h"
 
 namespace gt {
@@ -17,39 +20,113 @@ __global__ void k_new_degrees(int64_t n, const int64_t* rowptr, const int32_t* p
     }
 }
 
-// One wavefront per old row: every edge (u, c) becomes key (iperm[u] << B) | iperm[c].
-// Rows of more than kLongRow edges are left to k_edge_keys_long.
-__global__ __launch_bounds__(256) void k_edge_keys(int64_t n, const int64_t* rowptr, const int32_t* col,
-                                                   const int32_t* iperm, int bits, uint64_t* keys) {
+constexpr int kShortRow = 64;  // rows sorted inside one wavefront
+
+// One wavefront per new row r (old row u = perm[r]) of 1 to kShortRow entries:
+// lane l holds iperm of the row's l-th column (padding sorts last) and, for
+// the edge map, its old CSR position; a bitonic network over the next power
+// of two of lanes sorts them ascending (the columns of a row are distinct).
+template <bool kMap>
+__global__ __launch_bounds__(256) void k_relabel_short(int64_t n, const int64_t* __restrict__ rowptr,
+                                                       const int32_t* __restrict__ col,
+                                                       const int32_t* __restrict__ perm,
+                                                       const int32_t* __restrict__ iperm,
+                                                       const int64_t* __restrict__ rowptr_out,
+                                                       int32_t* __restrict__ col_out, int32_t* __restrict__ src_pos) {
     const int lane = lane_id();
     const int64_t waves = int64_t(gridDim.x) * 4;
-    for (int64_t u = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; u < n; u += waves) {
-        const int64_t a = rowptr[u], b = rowptr[u + 1];
-        if (b - a > kLongRow) continue;
-        const uint64_t hi = uint64_t(uint32_t(iperm[u])) << bits;
-        for (int64_t e = a + lane; e < b; e += kWave) keys[e] = hi | uint64_t(uint32_t(iperm[col[e]]));
+    for (int64_t r = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; r < n; r += waves) {
+        const int64_t u = perm[r];
+        const int64_t a = rowptr[u], dl = rowptr[u + 1] - a;
+        if (dl == 0 || dl > kShortRow) continue;
+        const int d = int(dl);
+        uint32_t key = 0xFFFFFFFFu, pos = 0u;
+        if (lane < d) {
+            key = uint32_t(iperm[col[a + lane]]);
+            pos = uint32_t(a + lane);
+        }
+        int P = 1;
+        while (P < d) P <<= 1;
+        for (int k = 2; k <= P; k <<= 1) {
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                const uint32_t ok = __shfl_xor(key, j, kWave);
+                const uint32_t op = kMap ? __shfl_xor(pos, j, kWave) : 0u;
+                const bool take_min = ((lane & j) == 0) == ((lane & k) == 0);
+                if (take_min ? ok < key : ok > key) {
+                    key = ok;
+                    pos = op;
+                }
+            }
+        }
+        if (lane < d) {
+            const int64_t o = rowptr_out[r] + lane;
+            col_out[o] = int32_t(key);
+            if (kMap) src_pos[o] = int32_t(pos);
+        }
     }
 }
 
-// The long rows' keys, chunk by chunk over the grid.
+// Entries of each new row that go to the radix sort: its degree when it is
+// longer than kShortRow, else 0.
+__global__ void k_sort_degrees(int64_t n, const int64_t* deg_new, int64_t* sdeg) {
+    for (int64_t r = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; r < n; r += int64_t(gridDim.x) * blockDim.x)
+        sdeg[r] = deg_new[r] > kShortRow ? deg_new[r] : 0;
+}
+
+// Keys of the rows of kShortRow + 1 to kLongRow entries, one wavefront per new
+// row, at the row's offset soff[r] among the sorted rows' entries; for the
+// edge map, the old CSR position as the value.
+template <bool kMap>
+__global__ __launch_bounds__(256) void k_edge_keys(int64_t n, const int64_t* rowptr, const int32_t* col,
+                                                   const int32_t* perm, const int32_t* iperm, int bits,
+                                                   const int64_t* soff, uint64_t* keys, uint32_t* vals) {
+    const int lane = lane_id();
+    const int64_t waves = int64_t(gridDim.x) * 4;
+    for (int64_t r = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; r < n; r += waves) {
+        const int64_t u = perm[r];
+        const int64_t a = rowptr[u], d = rowptr[u + 1] - a;
+        if (d <= kShortRow || d > kLongRow) continue;
+        const uint64_t hi = uint64_t(r) << bits;
+        const int64_t base = soff[r];
+        for (int64_t e = lane; e < d; e += kWave) {
+            keys[base + e] = hi | uint64_t(uint32_t(iperm[col[a + e]]));
+            if (kMap) vals[base + e] = uint32_t(a + e);
+        }
+    }
+}
+
+// The keys of the rows of more than kLongRow entries, chunk by chunk over the grid.
+template <bool kMap>
 __global__ __launch_bounds__(256) void k_edge_keys_long(int64_t n, int64_t nnz, const int64_t* rowptr,
                                                         const int32_t* col, const int32_t* iperm, int bits,
-                                                        uint64_t* keys) {
+                                                        const int64_t* soff, uint64_t* keys, uint32_t* vals) {
     const int64_t chunks = long_chunks_of(nnz);
     for (int64_t c = blockIdx.x; c < chunks; c += gridDim.x) {
         LongSeg seg[2];
         const int k = long_segments(rowptr, n, nnz, c, seg);
         for (int j = 0; j < k; ++j) {
-            const uint64_t hi = uint64_t(uint32_t(iperm[seg[j].row])) << bits;
-            for (int64_t e = seg[j].a + threadIdx.x; e < seg[j].b; e += blockDim.x)
-                keys[e] = hi | uint64_t(uint32_t(iperm[col[e]]));
+            const int64_t r = iperm[seg[j].row];
+            const uint64_t hi = uint64_t(r) << bits;
+            const int64_t shift = soff[r] - rowptr[seg[j].row];  // key position = soff[r] + (e - row start)
+            for (int64_t e = seg[j].a + threadIdx.x; e < seg[j].b; e += blockDim.x) {
+                keys[shift + e] = hi | uint64_t(uint32_t(iperm[col[e]]));
+                if (kMap) vals[shift + e] = uint32_t(e);
+            }
         }
     }
 }
 
-__global__ void k_key_cols(int64_t nnz, const uint64_t* keys, uint64_t mask, int32_t* col_out) {
-    for (int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; e < nnz; e += int64_t(gridDim.x) * blockDim.x)
-        col_out[e] = int32_t(keys[e] & mask);
+// Sorted key i of new row r goes to rank i - soff[r] inside the row.
+__global__ void k_place_sorted(int64_t m, const uint64_t* keys, const uint32_t* vals, int bits, const int64_t* soff,
+                               const int64_t* rowptr_out, int32_t* col_out, int32_t* src_pos) {
+    const uint64_t mask = (uint64_t(1) << bits) - 1;
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < m; i += int64_t(gridDim.x) * blockDim.x) {
+        const uint64_t key = keys[i];
+        const int64_t r = int64_t(key >> bits);
+        const int64_t o = rowptr_out[r] + (i - soff[r]);
+        col_out[o] = int32_t(key & mask);
+        if (src_pos) src_pos[o] = int32_t(vals[i]);
+    }
 }
 
 // Rows of fewer than 32 dwords (per-edge values): one lane per dword.
@@ -101,6 +178,8 @@ __global__ __launch_bounds__(256) void k_move_rows(int64_t n, int64_t words, con
 struct PermuteWs {
     uint32_t* flags;
     int64_t* deg_new;
+    int64_t* sdeg;  // entries of each new row that go to the radix sort
+    int64_t* soff;  // [n + 1]: their exclusive scan
     uint64_t* keys;
     uint32_t* vals;  // source positions (edge map only)
     ScanTmp scan;
@@ -112,6 +191,8 @@ PermuteWs carve(Ws& ws, int64_t n, int64_t nnz, bool with_map) {
     const int64_t n1 = n > 0 ? n : 1, e1 = nnz > 0 ? nnz : 1;
     p.flags = ws.take<uint32_t>(1);
     p.deg_new = ws.take<int64_t>(n1);
+    p.sdeg = ws.take<int64_t>(n1);
+    p.soff = ws.take<int64_t>(n1 + 1);
     p.keys = ws.take<uint64_t>(e1);
     p.vals = with_map ? ws.take<uint32_t>(e1) : nullptr;
     p.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1)));
@@ -143,22 +224,40 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     GT_LAUNCH_CHECK("permute_degrees");
     if ((st = exclusive_scan_i64(p.deg_new, n, rowptr_out, p.scan, stream)) != GT_OK) return st;
     if (nnz == 0) return GT_OK;
+    const unsigned gw = grid_for(n, 4, 65536);
+    if (with_map)
+        k_relabel_short<true><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, rowptr_out, col_out, src_pos);
+    else
+        k_relabel_short<false><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, rowptr_out, col_out, nullptr);
+    GT_LAUNCH_CHECK("permute_short_rows");
+    // the rows of more than kShortRow entries: packed keys, one radix sort
+    k_sort_degrees<<<g, 256, 0, stream>>>(n, p.deg_new, p.sdeg);
+    GT_LAUNCH_CHECK("permute_sort_degrees");
+    if ((st = exclusive_scan_i64(p.sdeg, n, p.soff, p.scan, stream)) != GT_OK) return st;
+    int64_t m = 0;
+    GT_HIP(hipMemcpyAsync(&m, p.soff + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipStreamSynchronize(stream));
+    if (m == 0) return GT_OK;
     const int bits = bits_for(n);
-    k_edge_keys<<<grid_for(n, 4, 65536), 256, 0, stream>>>(n, rowptr, col, iperm, bits, p.keys);
+    if (with_map)
+        k_edge_keys<true><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, bits, p.soff, p.keys, p.vals);
+    else
+        k_edge_keys<false><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, bits, p.soff, p.keys, nullptr);
     GT_LAUNCH_CHECK("permute_keys");
     if (nnz > kLongRow) {
         const int64_t ch = long_chunks_of(nnz);
-        k_edge_keys_long<<<unsigned(ch < 8192 ? ch : 8192), 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits,
-                                                                               p.keys);
+        const unsigned gl = unsigned(ch < 8192 ? ch : 8192);
+        if (with_map)
+            k_edge_keys_long<true><<<gl, 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits, p.soff, p.keys, p.vals);
+        else
+            k_edge_keys_long<false><<<gl, 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits, p.soff, p.keys,
+                                                             nullptr);
         GT_LAUNCH_CHECK("permute_keys_long");
     }
-    if (with_map && (st = iota_u32(p.vals, nnz, stream)) != GT_OK) return st;
-    if ((st = radix_sort_u64(p.keys, p.vals, nnz, 2 * bits, p.sort, stream)) != GT_OK) return st;
-    k_key_cols<<<grid_for(nnz, 256, 16384), 256, 0, stream>>>(nnz, p.keys, (uint64_t(1) << bits) - 1, col_out);
-    GT_LAUNCH_CHECK("permute_cols");
-    if (with_map) {
-        if ((st = copy_bytes(src_pos, p.vals, nnz * 4, stream)) != GT_OK) return st;
-    }
+    if ((st = radix_sort_u64(p.keys, p.vals, m, 2 * bits, p.sort, stream)) != GT_OK) return st;
+    k_place_sorted<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, p.keys, p.vals, bits, p.soff, rowptr_out, col_out,
+                                                                with_map ? src_pos : nullptr);
+    GT_LAUNCH_CHECK("permute_place");
     return GT_OK;
 }
 
