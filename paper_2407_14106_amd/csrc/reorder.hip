@@ -4,7 +4,7 @@
 // Rows are handled by size:
 //   deg <= 16 / 32     four / two rows per wavefront, 16 / 32 lanes each;
 //   32 < deg <= 64     one wavefront per row; one neighbour label per lane,
-//                      multiplicities by an in-register all-pairs compare.
+//                      multiplicities by an all-pairs compare (readlane).
 //   64 < deg <= 512    one wavefront per row, open-addressing count table in
 //                      the wavefront's share of LDS (no workgroup barriers).
 //   512 < deg <= 4096  one workgroup per row, open-addressing count table in LDS.
@@ -67,8 +67,8 @@ __device__ __forceinline__ int wave_min_i32(int v) {
 // -------------------------------------------------------------- per-row classes
 
 __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
-                           int32_t* is_s16, int32_t* is_s32, int32_t* is_wmed, int32_t* is_med, int32_t* is_big,
-                           int32_t* is_huge, int64_t* big_cap) {
+                           int32_t* is_s16, int32_t* is_s32, int32_t* is_wav, int32_t* is_wmed, int32_t* is_med,
+                           int32_t* is_big, int32_t* is_huge, int64_t* big_cap) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         // self-loop present?  rows are sorted: binary search for v.
@@ -83,6 +83,7 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
         deg_off[v] = uint32_t(deg - (self ? 1 : 0));
         is_s16[v] = deg <= kSub16 ? 1 : 0;
         is_s32[v] = (deg > kSub16 && deg <= kSub32) ? 1 : 0;
+        is_wav[v] = (deg > kSub32 && deg <= kWaveRowMax) ? 1 : 0;
         is_wmed[v] = (deg > kWaveRowMax && deg <= kWaveTabRowMax) ? 1 : 0;
         is_med[v] = (deg > kWaveTabRowMax && deg <= kLdsRowMax) ? 1 : 0;
         const bool big = deg > kLdsRowMax;
@@ -94,16 +95,17 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
     }
 }
 
-__global__ void k_compact(int64_t n, const int32_t* is_s16, const int32_t* is_s32, const int32_t* is_wmed,
-                          const int32_t* is_med, const int32_t* is_big, const int32_t* is_huge,
-                          const int64_t* pos_s16, const int64_t* pos_s32, const int64_t* pos_wmed,
-                          const int64_t* pos_med, const int64_t* pos_big, const int64_t* pos_huge,
-                          const int64_t* cap_off, int32_t* s16_list, int32_t* s32_list, int32_t* wmed_list,
-                          int32_t* med_list, int32_t* big_list, int64_t* big_off, int32_t* huge_list,
-                          int64_t* huge_off) {
+__global__ void k_compact(int64_t n, const int32_t* is_s16, const int32_t* is_s32, const int32_t* is_wav,
+                          const int32_t* is_wmed, const int32_t* is_med, const int32_t* is_big,
+                          const int32_t* is_huge, const int64_t* pos_s16, const int64_t* pos_s32,
+                          const int64_t* pos_wav, const int64_t* pos_wmed, const int64_t* pos_med,
+                          const int64_t* pos_big, const int64_t* pos_huge, const int64_t* cap_off, int32_t* s16_list,
+                          int32_t* s32_list, int32_t* wav_list, int32_t* wmed_list, int32_t* med_list,
+                          int32_t* big_list, int64_t* big_off, int32_t* huge_list, int64_t* huge_off) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         if (is_s16[v]) s16_list[pos_s16[v]] = int32_t(v);
         if (is_s32[v]) s32_list[pos_s32[v]] = int32_t(v);
+        if (is_wav[v]) wav_list[pos_wav[v]] = int32_t(v);
         if (is_wmed[v]) wmed_list[pos_wmed[v]] = int32_t(v);
         if (is_med[v]) med_list[pos_med[v]] = int32_t(v);
         if (is_big[v]) {
@@ -119,13 +121,19 @@ __global__ void k_compact(int64_t n, const int32_t* is_s16, const int32_t* is_s3
 
 // ------------------------------------------------------------------ wave rows
 
-__global__ __launch_bounds__(kBlock) void k_lp_wave(int64_t n, const int64_t* rowptr, const int32_t* col,
+// Rows of kSub32 + 1 to kWaveRowMax edges, one wavefront each: every lane
+// counts how many of the row's labels equal its own, reading the others with
+// readlane (the lane index is uniform over the wavefront).
+__global__ __launch_bounds__(kBlock) void k_lp_wave(const int32_t* list, const int64_t* list_len,
+                                                    const int64_t* rowptr, const int32_t* col,
                                                     const int32_t* lab_in, int32_t* lab_out, uint64_t key,
                                                     const uint32_t* flag_prev, uint32_t* flag_next) {
     const bool converged = *flag_prev == 0;
     const int lane = lane_id();
+    const int64_t len = *list_len;
     const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
-    for (int64_t v = int64_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave; v < n; v += waves) {
+    for (int64_t idx = int64_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave; idx < len; idx += waves) {
+        const int64_t v = list[idx];
         const int own = lab_in[v];
         if (converged) {
             if (lane == 0) lab_out[v] = own;
@@ -133,15 +141,11 @@ __global__ __launch_bounds__(kBlock) void k_lp_wave(int64_t n, const int64_t* ro
         }
         const int64_t a = rowptr[v];
         const int deg = int(rowptr[v + 1] - a);
-        if (deg <= kSub32 || deg > kWaveRowMax) continue;  // handled by k_lp_sub and the workgroup kernels
         int c = lane < deg ? col[a + lane] : -1;
         const bool valid = lane < deg && c != v;
         const int L = valid ? lab_in[c] : -1;
         int cnt = 0;
-        for (int k = 0; k < deg; ++k) {
-            const int Lk = __shfl(L, k, kWave);
-            cnt += (Lk == L) ? 1 : 0;
-        }
+        for (int k = 0; k < deg; ++k) cnt += (__builtin_amdgcn_readlane(L, k) == L) ? 1 : 0;
         if (!valid) cnt = 0;
         const int best = wave_max(cnt);
         int cand = own;
@@ -224,7 +228,13 @@ __global__ __launch_bounds__(kBlock) void k_lp_sub(const int32_t* list, const in
         const int dmax = wave_max(deg);
         int cnt = 0;
         for (int k = 0; k < dmax; ++k) {
-            const int Lk = __shfl(L, sub * S + k, kWave);
+            // lane sub * S + k of each group, by readlane (k is uniform over the wavefront)
+            int Lk = __builtin_amdgcn_readlane(L, k);
+#pragma unroll
+            for (int g = 1; g < G; ++g) {
+                const int x = __builtin_amdgcn_readlane(L, g * S + k);
+                Lk = sub == g ? x : Lk;
+            }
             cnt += (Lk == L) ? 1 : 0;
         }
         if (!valid) cnt = 0;
@@ -681,6 +691,7 @@ struct ReorderWs {
     uint32_t* deg_off;
     int32_t* is_s16;
     int32_t* is_s32;
+    int32_t* is_wav;
     int32_t* is_wmed;
     int32_t* is_med;
     int32_t* is_big;
@@ -688,6 +699,7 @@ struct ReorderWs {
     int64_t* big_cap;
     int64_t* pos_s16;
     int64_t* pos_s32;
+    int64_t* pos_wav;
     int64_t* pos_wmed;
     int64_t* pos_med;
     int64_t* pos_big;
@@ -695,6 +707,7 @@ struct ReorderWs {
     int64_t* cap_off;
     int32_t* s16_list;
     int32_t* s32_list;
+    int32_t* wav_list;
     int32_t* wmed_list;
     int32_t* med_list;
     int32_t* big_list;
@@ -716,12 +729,14 @@ struct ReorderWs {
 
 // The row counts of the list classes (the totals of their scans), gathered
 // so that one copy brings them to the host.
-enum { kClsS16, kClsS32, kClsWmed, kClsMed, kClsBig, kClsHuge, kClasses };
-__global__ void k_class_counts(int64_t n, const int64_t* s16, const int64_t* s32, const int64_t* wmed,
-                               const int64_t* med, const int64_t* big, const int64_t* huge, int64_t* out) {
+enum { kClsS16, kClsS32, kClsWav, kClsWmed, kClsMed, kClsBig, kClsHuge, kClasses };
+__global__ void k_class_counts(int64_t n, const int64_t* s16, const int64_t* s32, const int64_t* wav,
+                               const int64_t* wmed, const int64_t* med, const int64_t* big, const int64_t* huge,
+                               int64_t* out) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     out[kClsS16] = s16[n];
     out[kClsS32] = s32[n];
+    out[kClsWav] = wav[n];
     out[kClsWmed] = wmed[n];
     out[kClsMed] = med[n];
     out[kClsBig] = big[n];
@@ -766,6 +781,7 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.deg_off = ws.take<uint32_t>(n1);
     r.is_s16 = ws.take<int32_t>(n1);
     r.is_s32 = ws.take<int32_t>(n1);
+    r.is_wav = ws.take<int32_t>(n1);
     r.is_wmed = ws.take<int32_t>(n1);
     r.is_med = ws.take<int32_t>(n1);
     r.is_big = ws.take<int32_t>(n1);
@@ -773,6 +789,7 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.big_cap = ws.take<int64_t>(n1);
     r.pos_s16 = ws.take<int64_t>(n1 + 1);
     r.pos_s32 = ws.take<int64_t>(n1 + 1);
+    r.pos_wav = ws.take<int64_t>(n1 + 1);
     r.pos_wmed = ws.take<int64_t>(n1 + 1);
     r.pos_med = ws.take<int64_t>(n1 + 1);
     r.pos_big = ws.take<int64_t>(n1 + 1);
@@ -780,6 +797,7 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.cap_off = ws.take<int64_t>(n1 + 1);
     r.s16_list = ws.take<int32_t>(n1);
     r.s32_list = ws.take<int32_t>(n1);
+    r.wav_list = ws.take<int32_t>(n1);
     r.wmed_list = ws.take<int32_t>(n1);
     r.med_list = ws.take<int32_t>(n1);
     r.big_list = ws.take<int32_t>(n1);
@@ -835,20 +853,21 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if (st != GT_OK) return st;
 
     const unsigned g = grid_for(n, 256, 8192);
-    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_s16, r.is_s32, r.is_wmed, r.is_med, r.is_big,
-                                      r.is_huge, r.big_cap);
+    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med,
+                                      r.is_big, r.is_huge, r.big_cap);
     GT_LAUNCH_CHECK("reorder_classify");
     if ((st = exclusive_scan_i32(r.is_s16, n, r.pos_s16, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_s32, n, r.pos_s32, r.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(r.is_wav, n, r.pos_wav, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_wmed, n, r.pos_wmed, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_big, n, r.pos_big, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_huge, n, r.pos_huge, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
-    k_compact<<<g, 256, 0, stream>>>(n, r.is_s16, r.is_s32, r.is_wmed, r.is_med, r.is_big, r.is_huge, r.pos_s16,
-                                     r.pos_s32, r.pos_wmed, r.pos_med, r.pos_big, r.pos_huge, r.cap_off, r.s16_list,
-                                     r.s32_list, r.wmed_list, r.med_list, r.big_list, r.big_off, r.huge_list,
-                                     r.huge_off);
+    k_compact<<<g, 256, 0, stream>>>(n, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med, r.is_big, r.is_huge,
+                                     r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_big, r.pos_huge,
+                                     r.cap_off, r.s16_list, r.s32_list, r.wav_list, r.wmed_list, r.med_list,
+                                     r.big_list, r.big_off, r.huge_list, r.huge_off);
     GT_LAUNCH_CHECK("reorder_compact");
 
     if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
@@ -856,8 +875,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
     // the class sizes on the host: empty classes are not launched and grids fit the lists
-    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s16, r.pos_s32, r.pos_wmed, r.pos_med, r.pos_big, r.pos_huge,
-                                         r.class_cnt);
+    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_big,
+                                         r.pos_huge, r.class_cnt);
     GT_LAUNCH_CHECK("reorder_class_counts");
     int64_t cnt[kClasses] = {};
     GT_HIP(hipMemcpyAsync(cnt, r.class_cnt, sizeof(cnt), hipMemcpyDeviceToHost, stream));
@@ -865,7 +884,7 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     const int64_t n_huge = cnt[kClsHuge], n_big = cnt[kClsBig];
     BigRows br{r.huge_list, r.pos_huge + n, r.huge_off, r.tab_keys, r.tab_cnts, r.big_best, r.big_own,
                r.big_hbest, r.big_lbest};
-    const unsigned gw = grid_for(n, kBlock / kWave, 65536);
+    const unsigned gw = grid_cap(cnt[kClsWav], kBlock / kWave, 65536);
     const unsigned g16 = grid_cap(cnt[kClsS16], kBlock / kSub16, 16384);
     const unsigned g32 = grid_cap(cnt[kClsS32], kBlock / kSub32, 16384);
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
@@ -911,8 +930,11 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             GT_LAUNCH_CHECK("reorder_big_decide");
         }
         if (side) GT_HIP(hipEventRecord(ss->join, side));
-        k_lp_wave<<<gw, kBlock, 0, stream>>>(n, rowptr, col, in, out, key, r.flags + t, r.flags + t + 1);
-        GT_LAUNCH_CHECK("reorder_lp_wave");
+        if (cnt[kClsWav] > 0) {
+            k_lp_wave<<<gw, kBlock, 0, stream>>>(r.wav_list, r.pos_wav + n, rowptr, col, in, out, key, r.flags + t,
+                                                 r.flags + t + 1);
+            GT_LAUNCH_CHECK("reorder_lp_wave");
+        }
         if (cnt[kClsS16] > 0) {
             k_lp_sub<kSub16><<<g16, kBlock, 0, stream>>>(r.s16_list, r.pos_s16 + n, rowptr, col, in, out, key,
                                                          r.flags + t, r.flags + t + 1);
