@@ -338,9 +338,9 @@ __global__ void k_u32_to_i32(int64_t m, const uint32_t* src, int32_t* dst) {
 struct TilesWs {
     uint32_t* flags;
     unsigned long long* csum;  // checksum of the count results (kept below)
-    // The count results, one contiguous range [kept_begin, kept_end) of the
-    // workspace, so that gt_build_tiles can take them from gt_tiles_count's
-    // workspace: dense_per_tilerow .. dense_pre.
+    // The count results, one contiguous range of the workspace (kept_words
+    // 8-byte words from kept_begin: dense_per_tilerow .. dense_pre), so that
+    // gt_build_tiles can take them from gt_tiles_count's workspace.
     int32_t* dense_per_tilerow;
     int32_t* sp_deg;
     int64_t* tmp_tile_rowptr;
