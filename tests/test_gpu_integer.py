@@ -66,6 +66,46 @@ def test_reorder_bit_exact(gt, name, rowptr, col):
     assert sweeps == done
 
 
+def test_reorder_concurrent_calls(gt):
+    # rows above 4,096 entries run on a second stream of the library's own, shared by every call on the device:
+    # two host threads reordering at once, each on a stream of its own (default priority), both get the oracle's
+    # order, call after call
+    import threading
+
+    cases = [g for g in GRAPHS if g[0] in ("three_hubs_30000", "b1@0.1")]
+    refs = {}
+    for name, rowptr, col in cases:
+        lab_ref, _ = OR.lp_labels(rowptr, col, iters=20, seed=5)
+        refs[name] = OR.cluster_order(rowptr, col, lab_ref)
+    dev_graphs = {name: dev_csr(rowptr, col) for name, rowptr, col in cases}
+    torch.cuda.synchronize()
+    results, errors = {}, []
+
+    def work(name):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                rp, cl = dev_graphs[name]
+                for _ in range(3):
+                    perm, iperm, _lab = gt.reorder(rp, cl, iters=20, seed=5)
+                    results.setdefault(name, []).append((perm.cpu().numpy(), iperm.cpu().numpy()))
+        except Exception as e:  # reported below, in the test's own thread
+            errors.append(e)
+
+    say("reorder concurrent", ", ".join(dev_graphs))
+    threads = [threading.Thread(target=work, args=(name,)) for name in dev_graphs]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for name, (perm_ref, iperm_ref) in refs.items():
+        assert len(results[name]) == 3
+        for perm, iperm in results[name]:
+            np.testing.assert_array_equal(perm, perm_ref)
+            np.testing.assert_array_equal(iperm, iperm_ref)
+
+
 @pytest.mark.parametrize("name,rowptr,col", GRAPHS, ids=[g[0] for g in GRAPHS])
 def test_permute_bit_exact(gt, name, rowptr, col):
     say("permute", name)
