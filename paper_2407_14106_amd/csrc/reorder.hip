@@ -240,11 +240,15 @@ __global__ __launch_bounds__(kBlock) void k_lp_sub(const int32_t* list, const in
         if (!valid) cnt = 0;
         const int best = group_max_i32<S>(cnt);
         const int own_cnt = __popcll(__ballot(valid && L == own) & gmask);
-        const bool top = valid && cnt == best && best > 0 && own_cnt != best;
-        const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
-        const uint64_t hmin = group_min_u64<S>(h);
-        const int lmin = group_min_i32<S>((top && h == hmin) ? L : INT_MAX);
-        const int cand = (best > 0 && own_cnt != best) ? lmin : own;
+        const bool moves = best > 0 && own_cnt != best;
+        int cand = own;
+        if (__ballot(moves)) {  // the tie-break, unless every row of the wavefront keeps its label
+            const bool top = valid && cnt == best && moves;
+            const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
+            const uint64_t hmin = group_min_u64<S>(h);
+            const int lmin = group_min_i32<S>((top && h == hmin) ? L : INT_MAX);
+            if (moves) cand = lmin;
+        }
         if (live && sl == 0) {
             lab_out[v] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
