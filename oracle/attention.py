@@ -333,3 +333,31 @@ def dense_attn_dq_rows(Q, K, V, dO, scale, rows):
             ds = p * (dp - Dv)
             dQ[a:a + len(r), h, :] = scale * ds @ K[:, h, :]
     return dQ
+
+
+def dense_attn_row_stats(Q, K, V, dO, scale):
+    """LSE_i and D_i = <dO_i, O_i> of every row of full softmax attention ([N, H] each), O in fp64."""
+    dO = _f64(dO)
+    O, LSE = dense_attn_fwd(Q, K, V, scale)
+    return LSE, np.einsum("nhc,nhc->nh", dO, O)
+
+
+def dense_attn_dkdv_cols(Q, K, V, dO, scale, cols, stats=None):
+    """dK[cols], dV[cols] of full softmax attention: column j gathers dS_ij Q_i and P_ij dO_i over all N rows,
+    with P_ij = exp(s_ij - LSE_i) and dS_ij = P_ij (dP_ij - D_i), so it needs every row's LSE and D
+    (``stats`` = dense_attn_row_stats(...), computed here when not given)."""
+    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    N, H, d = Q.shape
+    cols = np.asarray(cols, dtype=np.int64)
+    LSE, Dv = stats if stats is not None else dense_attn_row_stats(Q, K, V, dO, scale)
+    dK = np.zeros((len(cols), H, d))
+    dV = np.zeros((len(cols), H, d))
+    step = max(1, (1 << 22) // max(1, N))
+    for a in range(0, len(cols), step):
+        c = cols[a:a + step]
+        for h in range(H):
+            p = np.exp(scale * (Q[:, h, :] @ K[c, h, :].T) - LSE[:, h:h + 1])  # [N, C]
+            ds = p * (dO[:, h, :] @ V[c, h, :].T - Dv[:, h:h + 1])
+            dK[a:a + len(c), h, :] = scale * ds.T @ Q[:, h, :]
+            dV[a:a + len(c), h, :] = p.T @ dO[:, h, :]
+    return dK, dV

@@ -240,6 +240,25 @@ def test_dense_bwd_matches_torch_and_sampled_rows():
     np.testing.assert_allclose(L, L_all[rows], rtol=1e-13)
 
 
+def test_dense_sampled_columns_match_torch_autograd():
+    # dK, dV of chosen columns (every row's softmax statistics needed) against torch's fp64 autograd of the
+    # full layer, on a ragged column set in an order of its own, and with the statistics passed in
+    n, H, d = 70, 3, 8
+    Q, K, V, dO = qkv(n, H, d, 47)
+    scale = 1.0 / np.sqrt(d)
+    _, rk, rv = torch_masked_grads(np.ones((n, n), bool), Q, K, V, dO, scale)
+    cols = np.array([69, 0, 33, 34, 7])
+    dk, dv = A.dense_attn_dkdv_cols(Q, K, V, dO, scale, cols)
+    np.testing.assert_allclose(dk, rk[cols], rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dv, rv[cols], rtol=1e-10, atol=1e-12)
+    stats = A.dense_attn_row_stats(Q, K, V, dO, scale)
+    dk2, dv2 = A.dense_attn_dkdv_cols(Q, K, V, dO, scale, np.arange(n), stats=stats)
+    np.testing.assert_allclose(dk2, rk, rtol=1e-10, atol=1e-12)
+    # softmax Jacobian sum rules over all columns: sum_j dK_j = 0, sum_j dV_j = sum_i dO_i
+    np.testing.assert_allclose(dk2.sum(axis=0), 0.0, atol=1e-11)
+    np.testing.assert_allclose(dv2.sum(axis=0), dO.sum(axis=0), rtol=1e-12, atol=1e-12)
+
+
 # ---------------------------------------------------------------- per-edge bias (§2.1 Eq. (3), §3.3)
 
 def dense_bias(rowptr, col, bias, n):

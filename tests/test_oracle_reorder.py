@@ -110,3 +110,55 @@ def test_recovers_planted_blocks_about_as_well_as_planted_order():
     ref = _dense_edge_share(g, planted, ip)
     assert ref > 0.8
     assert ours >= 0.95 * ref
+
+
+def test_cluster_order_key_worked_by_hand():
+    # The order after propagation sorts by (label, -degree, id), the degree counting a row's entries other than
+    # its self-loop.  Six nodes in two clusters, labels given; rows chosen so that each part of the key decides
+    # somewhere (worked by hand):
+    #   node: 0      1        2      3        4    5
+    #   row : {0,2}  {1,3,5}  {0,4}  {0,1,2}  {4}  {1,3}
+    #   deg : 1      2        2      3        0    2      (self-loops of 0, 1, 4 not counted)
+    #   lab : 5      2        5      2        5    2
+    # cluster 2 first: 3 (deg 3), then 1 and 5 (deg 2, by id); cluster 5: 2 (deg 2), 0 (deg 1), 4 (deg 0).
+    # Counting self-loops would give [1, 3, 5, 0, 2, 4]; an ascending degree [1, 5, 3, 4, 0, 2]; no label
+    # [3, 1, 2, 5, 0, 4]; ties by descending id [3, 5, 1, 2, 0, 4].
+    rows = [[0, 2], [1, 3, 5], [0, 4], [0, 1, 2], [4], [1, 3]]
+    rowptr = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int64)
+    col = np.concatenate(rows).astype(np.int32)
+    labels = np.array([5, 2, 5, 2, 5, 2])
+    perm, iperm = R.cluster_order(rowptr, col, labels)
+    assert perm.tolist() == [3, 1, 5, 2, 0, 4]
+    assert iperm.tolist() == [4, 1, 3, 0, 5, 2]
+
+
+def test_reorder_orders_unequal_degree_clusters_by_degree():
+    # End to end through propagation: two disjoint graphs, a 5-clique with two pendant nodes on member a and
+    # one on member b, and a triangle with one pendant.  Each component converges to one label (checked), and
+    # inside a component the nodes come out by falling degree (self-loops, added by csr_from_pairs, ignored),
+    # ties by id.
+    rng = np.random.default_rng(8)
+    n = 12
+    ids = rng.permutation(n)
+    k5 = ids[:5]
+    pend = ids[5:8]
+    tri = ids[8:11]
+    tri_pend = ids[11]
+    u, v = [], []
+    for a in range(5):
+        for b in range(a + 1, 5):
+            u.append(k5[a]); v.append(k5[b])
+    u += [k5[0], k5[0], k5[1]]; v += [pend[0], pend[1], pend[2]]
+    u += [tri[0], tri[0], tri[1], tri[2]]; v += [tri[1], tri[2], tri[2], tri_pend]
+    rowptr, col = csr_from_pairs(n, u, v)
+    perm, iperm, lab = R.reorder(rowptr, col)
+    comp1 = set(k5.tolist()) | set(pend.tolist())
+    comp2 = set(tri.tolist()) | {int(tri_pend)}
+    assert len({int(lab[x]) for x in comp1}) == 1 and len({int(lab[x]) for x in comp2}) == 1
+    deg = {int(x): 0 for x in range(n)}
+    for a, b in zip(u, v):
+        deg[int(a)] += 1
+        deg[int(b)] += 1
+    first, second = (comp1, comp2) if lab[k5[0]] < lab[tri[0]] else (comp2, comp1)
+    expect = sorted(first, key=lambda x: (-deg[x], x)) + sorted(second, key=lambda x: (-deg[x], x))
+    assert perm.tolist() == expect
