@@ -16,8 +16,10 @@
  *
  * Conventions shared by every entry point:
  *   - Every pointer is device memory unless its comment says "host".  All
- *     memory is owned by the caller; the library allocates nothing and keeps
- *     no state between calls except the thread-local error text.
+ *     memory is owned by the caller; the library allocates nothing, creates no
+ *     stream or event, and keeps no state between calls except the
+ *     thread-local error text (what one call leaves for another, such as the
+ *     tile counts, stays in the caller's workspace).
  *   - Scratch memory comes from a caller workspace `ws` of at least the size
  *     returned by the matching *_workspace_size() function (256-byte aligned
  *     base).  A smaller workspace gives GT_ERR_WORKSPACE.
@@ -29,9 +31,15 @@
  *     (gt_last_error() gives the reason).
  *   - Feature tensors Q, K, V, O, dO, dQ, dK, dV are [n, H, d] row-major
  *     (node, head, feature) in the element type `dtype`; LSE is [n, H] fp32.
- *     Supported: d in {32, 64}; H in {1, 2, 4, 8, 16}; dtype GT_F32 or GT_BF16
- *     (bf16 storage, fp32 arithmetic and accumulation, bf16 results rounded to
- *     nearest even).
+ *     Supported: d in {32, 64}; H in {1, 2, 4, 8, 16}; dtype GT_F32 or GT_BF16.
+ *     bf16: bf16 storage, scores, softmax statistics and every sum accumulated
+ *     in fp32, bf16 results rounded to nearest even; where a softmax weight
+ *     multiplies a bf16 row (the value sums, and the dense tiles' products of
+ *     weights or score gradients with K, Q or dO) the weight is rounded to
+ *     bf16 first, kept as a bf16 hi + lo pair where many large weights are
+ *     summed or two such sums are subtracted (a relative error of about 2^-9
+ *     per single-part weight); the softmax denominator sums the fp32 weights.
+ *     GT_F32 keeps every weight in fp32.
  *   - CSR: rowptr int64[n+1] with rowptr[0] = 0 and rowptr[n] = nnz; col
  *     int32[nnz], 0 <= col < n, strictly increasing inside each row.  Row i
  *     attends to the columns of row i (its out-neighbours).  The library adds
@@ -99,10 +107,7 @@ gt_status gt_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const i
  *   sweeps_done (host, may be NULL): SYNC if given; sweeps that changed a label.
  * The CSR must satisfy the input convention (see gt_validate_csr); it is
  * validated here first (SYNC) and an invalid CSR returns its error code.
- * Rows of more than 4,096 entries are processed on a second stream of the
- * library's own (one per device, default priority, kept for the life of the
- * process), forked from and joined back to `stream` with events every sweep:
- * the results are ordered on `stream` as for any other call. */
+ * Every kernel runs on `stream`. */
 size_t gt_reorder_workspace_size(int64_t n, int64_t nnz);
 gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
                      uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels, int32_t* sweeps_done,
@@ -179,11 +184,13 @@ gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowptr, const in
 /* Fills every array of *plan.  The size fields must be those set by
  * gt_tiles_count for the same arguments and every array pointer a caller
  * allocation of the size given above.  The CSR is the one gt_tiles_count
- * validated.  When ws is the workspace gt_tiles_count used with the same
- * arguments, its count results are taken from there if a checksum of them
- * (recorded by gt_tiles_count, recomputed here: SYNC) still matches; any other
- * workspace, or one written to in between, is counted again.  Either way the
- * plan is the same. */
+ * validated.  gt_tiles_count leaves in its workspace a record of its
+ * arguments and a checksum of its count results.  SYNC: this call reads that
+ * record back and recomputes the checksum; when ws holds the record of a
+ * gt_tiles_count with the same arguments and the checksum still matches, the
+ * counts are taken from there, otherwise (another workspace, or one written to
+ * in between) they are counted again.  The record is cleared once read.
+ * Either way the plan is the same. */
 gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
                          uint32_t tau_ppm, gt_tiles* plan, void* ws, size_t ws_bytes, hipStream_t stream);
 

@@ -16,8 +16,6 @@
 // All three compute the same function of the neighbour-label multiset.
 #include <limits.h>
 
-#include <mutex>
-
 #include "prim.h"
 
 namespace gt {
@@ -747,29 +745,6 @@ __global__ void k_class_counts(int64_t n, const int64_t* s16, const int64_t* s32
     out[kClsHuge] = huge[n];
 }
 
-// A second stream per device for the rows of more than 4,096 edges: their
-// workgroups run long on a few CUs while the other classes of a sweep run
-// beside them (every class reads the sweep's input labels and writes only its
-// own rows).  The stream and its fork/join events are created on first use and
-// kept for the life of the process; a call holds `mu` while it records and
-// waits on them, so calls from several host threads do not interleave.
-struct SideStream {
-    std::mutex mu;
-    hipStream_t s = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
-    bool ready() {  // with mu held
-        if (!s && hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) s = nullptr;
-        if (!fork && hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess) fork = nullptr;
-        if (!join && hipEventCreateWithFlags(&join, hipEventDisableTiming) != hipSuccess) join = nullptr;
-        return s && fork && join;
-    }
-};
-constexpr int kMaxDevices = 64;
-SideStream& side_stream(int dev) {
-    static SideStream per_dev[kMaxDevices];
-    return per_dev[dev];
-}
-
 inline unsigned grid_cap(int64_t rows, int64_t per_block, unsigned cap) {
     const int64_t g = cdiv(rows, per_block);
     return unsigned(g < 1 ? 1 : (g > cap ? cap : g));
@@ -894,46 +869,29 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
     const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
     const unsigned gbig = grid_cap(n_big, 1, 256);
-    // rows of more than 4,096 edges go to the side stream when there is one
-    SideStream* ss = nullptr;
-    std::unique_lock<std::mutex> side_lock;
-    int dev = -1;
-    if ((n_big > 0 || n_huge > 0) && hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kMaxDevices) {
-        SideStream& x = side_stream(dev);
-        side_lock = std::unique_lock<std::mutex>(x.mu);
-        if (x.ready()) ss = &x;
-        else side_lock.unlock();
-    }
-    const hipStream_t side = ss ? ss->s : nullptr;
-    const hipStream_t bs = side ? side : stream;
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
         const int32_t* in = r.lab[t & 1];
         int32_t* out = r.lab[(t + 1) & 1];
-        if (side) {
-            GT_HIP(hipEventRecord(ss->fork, stream));
-            GT_HIP(hipStreamWaitEvent(side, ss->fork, 0));
-        }
         if (n_big > 0) {
-            k_lp_block<true, kBigRowBlock><<<gbig, kBigRowBlock, 0, bs>>>(r.big_list, r.pos_big + n, rowptr, col, in,
+            k_lp_block<true, kBigRowBlock><<<gbig, kBigRowBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in,
                                                                        out, key, r.flags + t, r.flags + t + 1,
                                                                        r.tab_keys, r.tab_cnts, r.big_off);
             GT_LAUNCH_CHECK("reorder_lp_global");
         }
         if (n_huge > 0) {
             const uint32_t* fp = r.flags + t;
-            k_big_clear<<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, fp);
+            k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp);
             GT_LAUNCH_CHECK("reorder_big_clear");
-            k_big_insert<<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, col, in, fp);
+            k_big_insert<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, in, fp);
             GT_LAUNCH_CHECK("reorder_big_insert");
-            k_big_reduce<0><<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, in, key, fp);
-            k_big_reduce<1><<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, in, key, fp);
-            k_big_reduce<2><<<kBigGrid, kBlock, 0, bs>>>(br, rowptr, in, key, fp);
+            k_big_reduce<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+            k_big_reduce<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+            k_big_reduce<2><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
             GT_LAUNCH_CHECK("reorder_big_reduce");
-            k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, bs>>>(br, in, out, key, fp, r.flags + t + 1);
+            k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, in, out, key, fp, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_big_decide");
         }
-        if (side) GT_HIP(hipEventRecord(ss->join, side));
         if (cnt[kClsWav] > 0) {
             k_lp_wave<<<gw, kBlock, 0, stream>>>(r.wav_list, r.pos_wav + n, rowptr, col, in, out, key, r.flags + t,
                                                  r.flags + t + 1);
@@ -960,7 +918,6 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
                                                                    nullptr, nullptr);
             GT_LAUNCH_CHECK("reorder_lp_lds");
         }
-        if (side) GT_HIP(hipStreamWaitEvent(stream, ss->join, 0));
     }
     const int32_t* final_lab = r.lab[iters & 1];
     k_order_keys<<<g, 256, 0, stream>>>(n, final_lab, r.deg_off, r.sort_keys);

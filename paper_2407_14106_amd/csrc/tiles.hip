@@ -11,8 +11,6 @@
 // written chunk by chunk over the whole grid.  The remainder's transpose and
 // the column-grouped tile list come from stable radix sorts, so every output
 // is deterministic.
-#include <mutex>
-#include <vector>
 
 #include "prim.h"
 
@@ -335,9 +333,12 @@ __global__ void k_u32_to_i32(int64_t m, const uint32_t* src, int32_t* dst) {
         dst[e] = int32_t(src[e]);
 }
 
+constexpr int kRecordWords = 8;
+
 struct TilesWs {
     uint32_t* flags;
     unsigned long long* csum;  // checksum of the count results (kept below)
+    uint64_t* record;          // [kRecordWords]: what gt_tiles_count left here (CountRecord)
     // The count results, one contiguous range of the workspace (kept_words
     // 8-byte words from kept_begin: dense_per_tilerow .. dense_pre), so that
     // gt_build_tiles can take them from gt_tiles_count's workspace.
@@ -370,6 +371,7 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
     const int64_t R = cdiv(n1, T > 0 ? T : 1);
     t.flags = ws.take<uint32_t>(1);
     t.csum = ws.take<unsigned long long>(1);
+    t.record = ws.take<uint64_t>(kRecordWords);
     t.W = int(cdiv(R, 32));
     t.dense_per_tilerow = ws.take<int32_t>(R);
     t.sp_deg = ws.take<int32_t>(n1);
@@ -424,47 +426,36 @@ gt_status ws_checksum(const TilesWs& t, hipStream_t s) {
     return GT_OK;
 }
 
-// What the last gt_tiles_count left in a workspace: its arguments and the
-// checksum of its count results.  gt_build_tiles with the same workspace and
-// arguments takes the counts from there when the checksum still matches.
+// What gt_tiles_count leaves in its workspace, next to the count results: its
+// arguments and the checksum of those results, written by the device after the
+// checksum kernel.  gt_build_tiles with the same workspace and arguments takes
+// the counts from there when the checksum still matches, and clears the
+// record's tag (a record is used once).  The record lives in the caller's
+// memory, so the library keeps nothing between the two calls.
+constexpr uint64_t kRecordTag = 0x67745F74696C6573ull;
 struct CountRecord {
-    const void* ws;
-    int64_t n, nnz;
-    const int64_t* rowptr;
-    const int32_t* col;
-    int32_t T;
-    uint32_t tau_ppm;
-    uint64_t sum;
+    uint64_t w[kRecordWords];  // tag, n, nnz, rowptr, col, T << 32 | tau_ppm, checksum, unused
 };
-std::mutex g_count_mu;
-std::vector<CountRecord> g_counts;  // at most kCountRecords, oldest first
-constexpr size_t kCountRecords = 16;
 
-void count_record_put(const CountRecord& r) {
-    std::lock_guard<std::mutex> lock(g_count_mu);
-    for (size_t i = 0; i < g_counts.size(); ++i)
-        if (g_counts[i].ws == r.ws) {
-            g_counts.erase(g_counts.begin() + i);
-            break;
-        }
-    if (g_counts.size() >= kCountRecords) g_counts.erase(g_counts.begin());
-    g_counts.push_back(r);
+__global__ void k_put_record(uint64_t* __restrict__ rec, int64_t n, int64_t nnz, const int64_t* rowptr,
+                             const int32_t* col, int32_t T, uint32_t tau_ppm, const unsigned long long* __restrict__ sum) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    rec[0] = kRecordTag;
+    rec[1] = uint64_t(n);
+    rec[2] = uint64_t(nnz);
+    rec[3] = uint64_t(reinterpret_cast<uintptr_t>(rowptr));
+    rec[4] = uint64_t(reinterpret_cast<uintptr_t>(col));
+    rec[5] = (uint64_t(uint32_t(T)) << 32) | tau_ppm;
+    rec[6] = uint64_t(*sum);
+    rec[7] = 0;
 }
 
-// Removes and returns the record of `ws` if its arguments match.
-bool count_record_take(const void* ws, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
-                       uint32_t tau_ppm, uint64_t& sum) {
-    std::lock_guard<std::mutex> lock(g_count_mu);
-    for (size_t i = 0; i < g_counts.size(); ++i) {
-        const CountRecord& r = g_counts[i];
-        if (r.ws != ws) continue;
-        const bool same = r.n == n && r.nnz == nnz && r.rowptr == rowptr && r.col == col && r.T == T &&
-                          r.tau_ppm == tau_ppm;
-        sum = r.sum;
-        g_counts.erase(g_counts.begin() + i);
-        return same;
-    }
-    return false;
+bool record_matches(const CountRecord& r, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                    int32_t T, uint32_t tau_ppm) {
+    return r.w[0] == kRecordTag && r.w[1] == uint64_t(n) && r.w[2] == uint64_t(nnz) &&
+           r.w[3] == uint64_t(reinterpret_cast<uintptr_t>(rowptr)) &&
+           r.w[4] == uint64_t(reinterpret_cast<uintptr_t>(col)) &&
+           r.w[5] == ((uint64_t(uint32_t(T)) << 32) | tau_ppm);
 }
 
 gt_status check_common(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T,
@@ -543,19 +534,19 @@ extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowpt
     if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
         return st;
     if ((st = ws_checksum(t, stream)) != GT_OK) return st;
+    k_put_record<<<1, 64, 0, stream>>>(t.record, n, nnz, rowptr, col, T, tau_ppm, t.csum);
+    GT_LAUNCH_CHECK("tiles_count_record");
     const int64_t R = plan->n_row_tiles;
-    int64_t h[5] = {0, 0, 0, 0, 0};
+    int64_t h[4] = {0, 0, 0, 0};
     GT_HIP(hipMemcpyAsync(&h[0], t.tmp_tile_rowptr + R, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipMemcpyAsync(&h[1], t.tmp_sp_rowptr + n, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipMemcpyAsync(&h[2], t.long_row_pos + n, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipMemcpyAsync(&h[3], t.long_col_pos + n, 8, hipMemcpyDeviceToHost, stream));
-    GT_HIP(hipMemcpyAsync(&h[4], t.csum, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
     plan->n_dense = h[0];
     plan->nnz_sparse = h[1];
     plan->n_long_rows = h[2];
     plan->n_long_cols = h[3];
-    count_record_put({ws_ptr, n, nnz, rowptr, col, T, tau_ppm, uint64_t(h[4])});
     return GT_OK;
 }
 
@@ -588,13 +579,16 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     // the counts of the gt_tiles_count call that used this workspace with these
     // arguments, if they are still there unchanged; else count again
     bool reuse = false;
-    uint64_t want = 0;
-    if (count_record_take(ws_ptr, n, nnz, rowptr, col, T, tau_ppm, want)) {
+    {
         if ((st = ws_checksum(t, stream)) != GT_OK) return st;
+        CountRecord rec;
         uint64_t have = 0;
+        GT_HIP(hipMemcpyAsync(&rec, t.record, sizeof(rec), hipMemcpyDeviceToHost, stream));
         GT_HIP(hipMemcpyAsync(&have, t.csum, 8, hipMemcpyDeviceToHost, stream));
         GT_HIP(hipStreamSynchronize(stream));
-        reuse = have == want;
+        reuse = record_matches(rec, n, nnz, rowptr, col, T, tau_ppm) && rec.w[6] == have;
+        if (rec.w[0] == kRecordTag && (st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK)
+            return st;
     }
     if (reuse) {
         if ((st = copy_bytes(plan->tile_rowptr, t.tmp_tile_rowptr, size_t(R + 1) * 8, stream)) != GT_OK) return st;

@@ -36,6 +36,20 @@ def test_every_declared_symbol_is_exported(lib):
     assert set(names) == set(gt.SIGNATURES), "binding signatures out of sync with the header"
 
 
+def test_library_creates_no_runtime_objects(lib):
+    # The library keeps no state between calls and owns no device memory: it imports no HIP call that creates
+    # streams or events or that allocates or frees memory (the symbol table of the built library).
+    import subprocess
+
+    out = subprocess.run(["nm", "-D", "--undefined-only", gt.LIB_PATH], capture_output=True, text=True, check=True)
+    imported = {line.split()[-1].split("@")[0] for line in out.stdout.splitlines() if line.strip()}
+    hip = {name for name in imported if name.startswith("hip")}
+    forbidden = re.compile(r"^hip(Stream|Event|Graph)Create|^hip(Ext)?Malloc|^hipFree|^hipHost(Malloc|Register)"
+                           r"|^hipMemset|^hipMallocManaged")
+    assert "hipLaunchKernel" in hip
+    assert not sorted(n for n in hip if forbidden.search(n)), hip
+
+
 def test_version_and_status_strings(lib):
     assert lib.gt_abi_version() == 1
     assert lib.gt_status_string(gt.GT_OK) == b"ok"

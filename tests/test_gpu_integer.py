@@ -67,9 +67,8 @@ def test_reorder_bit_exact(gt, name, rowptr, col):
 
 
 def test_reorder_concurrent_calls(gt):
-    # rows above 4,096 entries run on a second stream of the library's own, shared by every call on the device:
     # two host threads reordering at once, each on a stream of its own (default priority), both get the oracle's
-    # order, call after call
+    # order, call after call (the library keeps nothing between or across calls)
     import threading
 
     cases = [g for g in GRAPHS if g[0] in ("three_hubs_30000", "b1@0.1")]
