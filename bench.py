@@ -156,7 +156,10 @@ def cpu_baseline(w, q, k, v, do, target_s):
                 break
             rows = min(g.n, int(rows * max(2.0, min(8.0, 0.5 * target_s / max(dt1, 1e-3)))))
     edge_heads = float(np.diff(g.rowptr)[sample].sum()) * w.heads
-    cores = min(16, len(os.sched_getaffinity(0)))
+    # the pool is sized to this GPU's share of the host (16 cores per GPU on these machines), never above the
+    # cores the process may run on; the host's own count is recorded beside it
+    host_cores, allowed = os.cpu_count() or 1, len(os.sched_getaffinity(0))
+    cores = min(16, allowed)
     big = np.sort(rng.choice(g.n, size=min(g.n, rows * cores // 2), replace=False))
     chunks = np.array_split(big, cores * 4)
     ctx = mp.get_context("fork")
@@ -170,6 +173,8 @@ def cpu_baseline(w, q, k, v, do, target_s):
         "value": edge_heads_n / dtn,
         "unit": "edge-head scores/s",
         "cores": cores,
+        "host_cpu_count": host_cores,
+        "host_cores_allowed": allowed,
         "kind": "oracle",
         "sample": f"{len(big)} random rows of the workload (their {int(edge_heads_n / w.heads)} edges x {w.heads} "
                   f"heads) over {cores} processes, {dtn:.1f} s: fp64 forward of the rows, dQ of the rows, dK/dV "
