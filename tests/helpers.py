@@ -54,6 +54,28 @@ def grad_term_rms(rowptr, col, q, k, v, do, scale):
     return rms(scale * dp * nk), rms(scale * dp * nq), rms(ndo), rms(dp)
 
 
+# Elementwise figures of every fp32 comparison, reported at the end of the session (conftest): the largest
+# |x - r| / (1e-5 |r| + 1e-5 rms(r)) (above 1 means the elementwise reading of the fp32 bar would fail there) and
+# the largest |x - r| / |r| over entries with |r| >= rms(r).
+FP32_ELEMENTWISE: list[tuple[str, float, float]] = []
+
+
+def _record_fp32_elementwise(x: np.ndarray, r: np.ndarray, name: str) -> None:
+    fin = np.isfinite(r)
+    x, r = x[fin], r[fin]
+    if r.size == 0:
+        return
+    rms = float(np.sqrt(np.mean(r * r)))
+    err = np.abs(x - r)
+    ratio = float(np.max(err / (1e-5 * np.abs(r) + 1e-5 * rms))) if rms > 0 else float(err.max() > 0) * np.inf
+    big = np.abs(r) >= rms
+    rel = float(np.max(err[big] / np.abs(r[big]))) if big.any() else 0.0
+    import os
+
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0].split("::")[-1]
+    FP32_ELEMENTWISE.append((f"{test} {name}".strip(), ratio, rel))
+
+
 def assert_close(x, r, dtype: str, name: str, rho: float | None = None):
     """``rho``: for fp32, a floor for the tolerance's scale: used in place of the RMS of the reference's vector
     norms ([n, H, d] tensors) or of 1 (per-entry values) when larger."""
@@ -64,6 +86,7 @@ def assert_close(x, r, dtype: str, name: str, rho: float | None = None):
     assert np.array_equal(np.isfinite(x), fin), f"{name}: non-finite pattern differs"
     assert np.array_equal(x[~fin], r[~fin]), f"{name}: infinite values differ"
     if dtype == "f32":
+        _record_fp32_elementwise(x, r, name)
         if r.ndim == 3:  # [n, H, d]: normwise per (node, head)
             rn = np.linalg.norm(r, axis=-1)
             rho = max(np.sqrt(np.mean(rn * rn)) if rn.size else 0.0, rho or 0.0)

@@ -52,6 +52,15 @@ def run_case(gt, rowptr, col, H, d, dtype, taus=(CSR_ONLY,), T=128, seed=0, bwd=
             torch.cuda.synchronize()
             for name, x, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), grads_ref):
                 assert_close(host(x), r, dtype, f"{name} tau={tau}")
+            # the two halves as the benchmark calls them (the row pass's statistic handed to the column pass):
+            # D against the oracle's <dO_i, O_i>, the gradients equal to the combined call's bit for bit
+            dQ2, Dst = gt.sparse_attn_bwd_rows(plan, Q, K, V, dO, L, scale)
+            dK2, dV2 = gt.sparse_attn_bwd_cols(plan, Q, K, V, dO, L, Dst, scale)
+            torch.cuda.synchronize()
+            assert_close(Dst.cpu().numpy(), np.einsum("nhc,nhc->nh", np.asarray(do, np.float64), O_ref), dtype,
+                         f"D tau={tau}")
+            for name, a, b in zip(("dQ", "dK", "dV"), (dQ, dK, dV), (dQ2, dK2, dV2)):
+                assert torch.equal(a, b), f"{name} of the split backward differs from the combined call, tau={tau}"
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -186,8 +195,8 @@ def test_pipeline_reorder_then_attention_is_equivariant(gt):
                                       ("c5", 10_000), ("b1", 10_000), ("b2", 50_000)])
 def test_full_size_workloads_sampled(gt, name, tau):
     # The workloads at their full sizes through the library's whole pipeline, in the launch configuration the
-    # benchmark times (reorder, relabel, 128-wide tiles at the workload's threshold, row gather, forward and
-    # both backward passes), with the outputs scattered back to the input order.  The oracle computes 192
+    # benchmark times (reorder, relabel, 128-wide tiles at the workload's threshold, row gather, the forward,
+    # then the backward's row and column calls), with the outputs scattered back to the input order.  The oracle computes 192
     # random rows (forward, dQ) and columns (dK, dV) one by one on the original graph, plus the eight rows of
     # largest degree (hubs on the power-law graph, the global token of the batched graphs).  A column attended
     # by more than 65,536 rows (the global token's) is left to the small batched test, which checks it in
@@ -203,7 +212,8 @@ def test_full_size_workloads_sampled(gt, name, tau):
     plan = gt.build_tiles(rp2, cl2, 128, tau)
     Q, K, V, dO = (gt.gather_rows(dev_feat(x, w.dtype), perm) for x in (q, k, v, do))
     O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
-    dQ, dK, dV = gt.sparse_attn_bwd(plan, Q, K, V, dO, L, scale)
+    dQ, Dst = gt.sparse_attn_bwd_rows(plan, Q, K, V, dO, L, scale)
+    dK, dV = gt.sparse_attn_bwd_cols(plan, Q, K, V, dO, L, Dst, scale)
     outs = [gt.scatter_rows(x, perm) for x in (O, L, dQ, dK, dV)]
     torch.cuda.synchronize()
     say("  dense tiles", plan.n_dense, "long rows", plan.c.n_long_rows, "long cols", plan.c.n_long_cols)
