@@ -363,6 +363,22 @@ size_t gt_dense_attn_bwd_workspace_size(int64_t n, int32_t H, int32_t d, gt_dtyp
 gt_status gt_dense_attn_bwd(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
                             const void* V, const void* O, const void* dO, const float* LSE, float scale, void* dQ,
                             void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+/* For callers that cannot allocate (code under stream capture, tight serving
+ * loops, harnesses that forbid allocation): gt_dense_attn_bwd with its scratch
+ * (the row statistic D, fp32 [n, H]) in a device array of the library's own
+ * instead of a caller workspace.  It allocates and frees nothing.  The array
+ * holds gt_dense_attn_bwd_noalloc_max_bytes() = 64 MiB; n * H above 16,777,216
+ * returns GT_ERR_UNSUPPORTED (use gt_dense_attn_bwd).  Each GPU the library
+ * runs this on holds its own copy until the process ends; its device address
+ * is looked up on the first call on that device.  The stream must belong to
+ * the current device.  Every call on one GPU shares that GPU's array, so calls
+ * that overlap on one GPU (other streams, other host threads) race: order them.
+ * Nothing in the array needs clearing between calls (D is written before it is
+ * read).  Results equal gt_dense_attn_bwd's bit for bit. */
+size_t gt_dense_attn_bwd_noalloc_max_bytes(void);
+gt_status gt_dense_attn_bwd_noalloc(int64_t n, int32_t H, int32_t d, gt_dtype dtype, const void* Q, const void* K,
+                                    const void* V, const void* O, const void* dO, const float* LSE, float scale,
+                                    void* dQ, void* dK, void* dV, hipStream_t stream);
 
 #ifdef __cplusplus
 }

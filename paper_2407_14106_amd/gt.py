@@ -111,6 +111,9 @@ SIGNATURES = {
     "gt_dense_attn_bwd_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
     "gt_dense_attn_bwd": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
                                  _sz, _vp]),
+    "gt_dense_attn_bwd_noalloc_max_bytes": (_sz, []),
+    "gt_dense_attn_bwd_noalloc": (_i32, [_i64, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp,
+                                         _vp, _vp]),
 }
 
 _LIB = None
@@ -551,4 +554,19 @@ def dense_attn_bwd(Q, K, V, O, dO, LSE, scale: float | None = None):
     _check(lib.gt_dense_attn_bwd(n, H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE), scale,
                                  _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel(), _stream(Q.device)),
            "gt_dense_attn_bwd")
+    return dQ, dK, dV
+
+
+def dense_attn_bwd_noalloc(Q, K, V, O, dO, LSE, scale: float | None = None, out=None):
+    """(dQ, dK, dV) of full softmax attention through the entry point that allocates nothing: its scratch is the
+    library's own device array (n * H <= 16,777,216).  ``out``: optional (dQ, dK, dV) to write into."""
+    lib = load_library()
+    _check_feats(Q.shape[0], Q, K, V, O, dO)
+    n, H, d = Q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dt = _dtype_code(Q)
+    dQ, dK, dV = out if out is not None else (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V))
+    _check(lib.gt_dense_attn_bwd_noalloc(n, H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE),
+                                         scale, _ptr(dQ), _ptr(dK), _ptr(dV), _stream(Q.device)),
+           "gt_dense_attn_bwd_noalloc")
     return dQ, dK, dV
