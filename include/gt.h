@@ -19,7 +19,9 @@
  *     memory is owned by the caller; the library allocates nothing, creates no
  *     stream or event, and keeps no state between calls except the
  *     thread-local error text (what one call leaves for another, such as the
- *     tile counts, stays in the caller's workspace).
+ *     tile counts, stays in the caller's workspace) and, for the one entry
+ *     point that takes no workspace (gt_dense_attn_bwd_noalloc), its device
+ *     scratch array and that array's address on each device.
  *   - Scratch memory comes from a caller workspace `ws` of at least the size
  *     returned by the matching *_workspace_size() function (256-byte aligned
  *     base).  A smaller workspace gives GT_ERR_WORKSPACE.
