@@ -7,7 +7,7 @@ and tiled once before timing; those stages are timed separately and reported
 under "preprocess".  Also reported: the interleaved full-attention layer
 ("dense_layer"), the fp64 oracle on a bounded sample of the same workload on
 the host's cores ("cpu_baseline", timed before the GPU is used) and, with
---tau-sweep, the same step at density thresholds 1%, 20% and the CSR-only
+--tau-sweep [TAU ...], the same step at other density thresholds and the CSR-only
 control ("tau_sweep"); with --bias, the step with a per-edge additive bias
 ("edge_bias"); with --ecr, the paper's lossy cluster reformation and the step
 on the rewritten graph ("ecr").  "peaks" holds measured denominators beside
@@ -56,9 +56,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense-layer", action="store_true", help="skip the full-attention layer measurement")
-    ap.add_argument("--tau-sweep", action="store_true",
-                    help="also time the step at density thresholds 1%%, 20%% and CSR only (c4); off by default so "
-                         "that a kernel trace of the default command holds the headline launches only")
+    ap.add_argument("--tau-sweep", type=float, nargs="*", default=None,
+                    help="also time the step at other density thresholds (default 1%%, 5%%, 10%%, 20%%, 30%%, 50%% "
+                         "and above 1, the CSR-only control); off by default so that a kernel trace of the default "
+                         "command holds the headline launches only")
     ap.add_argument("--bias", action="store_true",
                     help="also time the step with a per-edge additive bias (all-remainder plan) and the plain "
                          "step on the same plan")
@@ -272,13 +273,15 @@ def measured_peaks():
     }
 
 
-def tau_sweep(gt, rp, cl, Q, K, V, dO, scale, args, edge_heads, T):
-    """Same step at other density thresholds: 1% (the diagonal tiles of the clusters go to the matrix cores),
-    20% (none do) and above 1 (the CSR-only control: no tile can qualify)."""
+SWEEP_TAUS = (0.01, 0.05, 0.10, 0.20, 0.30, 0.50, 1.01)
+
+
+def tau_sweep(gt, rp, cl, Q, K, V, dO, scale, taus, edge_heads, T):
+    """Same step at other density thresholds; above 1 is the CSR-only control (no tile can qualify)."""
     import torch
 
     out = {}
-    for tau in (0.01, 0.20, 1.01):
+    for tau in taus:
         plan = gt.build_tiles(rp, cl, T, gt.tau_to_ppm(tau))
         for _ in range(3):
             O, L = gt.sparse_attn_fwd(plan, Q, K, V, scale)
@@ -589,9 +592,10 @@ def main():
         },
         "wall_s_timed": round(t_wall, 3),
     }
-    if args.tau_sweep and args.workload == "c4":
+    if args.tau_sweep is not None and not fwd_only:
         log("density-threshold sweep ...")
-        result["tau_sweep"] = tau_sweep(gt, rp2, cl2, Q, K, V, dO, scale, args, edge_heads, args.tile)
+        result["tau_sweep"] = tau_sweep(gt, rp2, cl2, Q, K, V, dO, scale, args.tau_sweep or SWEEP_TAUS, edge_heads,
+                                        args.tile)
     if args.bias:
         log("step with a per-edge bias ...")
         result["edge_bias"] = bias_step(gt, w, rp, cl, perm, iperm, Q, K, V, dO, scale, edge_heads)

@@ -303,94 +303,75 @@ gt_status radix_sort_u64(uint64_t* keys, uint32_t* values, int64_t n, int key_bi
 
 // =========================================================== CSR validation
 
-// Rows of up to kValidateShort entries are checked by one thread each, which
-// loads kValidateBatch entries at a time before comparing them (one memory
-// latency per batch, not per entry); the wavefront takes every longer row of
-// its batch up to kLongRow entries together, its lanes striding the row 64
-// entries apart and comparing each entry with the one before it in memory.
-// Longer rows (a node adjacent to every node) are checked chunk by chunk over
-// the whole grid.
-constexpr int64_t kValidateShort = 256;
-constexpr int kValidateBatch = 8;
+// Validation in two coalesced passes.  k_validate_rows checks every row's
+// bounds (one thread per row).  k_validate_entries cuts col into chunks of
+// kValidateChunk entries, one workgroup per chunk: it finds the chunk's first
+// row by a binary search on rowptr, marks in LDS the chunk's entries that start
+// a non-empty row, then every thread checks its entries (0 <= col < n, and
+// col[e - 1] < col[e] unless e starts a row).  Every workgroup does the same
+// work whatever the row lengths, and every read stays inside rowptr[0..n] and
+// col[0..nnz) even when rowptr is wrong (then the rows pass reports it).
+constexpr int kValidateChunk = 2048;
+constexpr int kValidateThreads = 256;
 
-__global__ void k_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
-                               uint32_t* flags) {
+__global__ void k_validate_rows(int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr, uint32_t* flags) {
     uint32_t f = 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         if (rowptr[0] != 0 || rowptr[n] != nnz) f |= kOutOfRange;
     }
-    const int lane = lane_id();
-    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-    // wave-uniform loop: every lane of a wavefront runs the same number of rounds
-    for (int64_t base = int64_t(blockIdx.x) * blockDim.x + (threadIdx.x - lane); base < n; base += stride) {
-        const int64_t i = base + lane;
-        bool mid_row = false;
-        int64_t a = 0, b = 0;
-        if (i < n) {
-            a = rowptr[i];
-            b = rowptr[i + 1];
-            if (a > b) f |= kUnsorted;
-            else if (a < 0 || b > nnz) f |= kOutOfRange;
-            else if (b - a > kLongRow) {
-                // checked by k_validate_long
-            } else if (b - a > kValidateShort) mid_row = true;
-            else {
-                int64_t prev = -1;
-                for (int64_t e0 = a; e0 < b; e0 += kValidateBatch) {
-                    int64_t c[kValidateBatch];
-#pragma unroll
-                    for (int k = 0; k < kValidateBatch; ++k) c[k] = e0 + k < b ? int64_t(col[e0 + k]) : 0;
-#pragma unroll
-                    for (int k = 0; k < kValidateBatch; ++k) {
-                        if (e0 + k >= b) break;
-                        if (c[k] < 0 || c[k] >= n) f |= kOutOfRange;
-                        if (c[k] == prev) f |= kDuplicate;
-                        else if (c[k] < prev) f |= kUnsorted;
-                        prev = c[k];
-                    }
-                }
-            }
-        }
-        uint64_t pending = __ballot(mid_row);
-        while (pending) {
-            const int src = __builtin_ctzll(pending);
-            pending &= pending - 1;
-            const int64_t ra = __shfl(a, src, kWave), rb = __shfl(b, src, kWave);
-#pragma unroll 4
-            for (int64_t e = ra + lane; e < rb; e += kWave) {
-                const int64_t c = col[e];
-                if (c < 0 || c >= n) f |= kOutOfRange;
-                if (e > ra) {
-                    const int64_t prev = col[e - 1];
-                    if (c == prev) f |= kDuplicate;
-                    else if (c < prev) f |= kUnsorted;
-                }
-            }
-        }
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t a = rowptr[i], b = rowptr[i + 1];
+        if (a > b) f |= kUnsorted;
+        else if (a < 0 || b > nnz) f |= kOutOfRange;
     }
     if (f) atomicOr(flags, f);
 }
 
-// Rows of more than kLongRow entries, one chunk of the entry range per round.
-__global__ __launch_bounds__(256) void k_validate_long(int64_t n, int64_t nnz, const int64_t* rowptr,
-                                                       const int32_t* col, uint32_t* flags) {
+__global__ __launch_bounds__(kValidateThreads) void k_validate_entries(int64_t n, int64_t nnz,
+                                                                       const int64_t* __restrict__ rowptr,
+                                                                       const int32_t* __restrict__ col,
+                                                                       uint32_t* flags) {
+    __shared__ uint32_t s_start[kValidateChunk / 32];
+    __shared__ int64_t s_row;
     uint32_t f = 0;
-    const int64_t chunks = long_chunks_of(nnz);
+    const int64_t chunks = cdiv(nnz, kValidateChunk);
     for (int64_t c = blockIdx.x; c < chunks; c += gridDim.x) {
-        LongSeg seg[2];
-        const int k = long_segments(rowptr, n, nnz, c, seg);
-        for (int j = 0; j < k; ++j) {
-            const int64_t first = rowptr[seg[j].row];  // the row's first entry (negative only if rowptr is bad)
-            for (int64_t e = seg[j].a + threadIdx.x; e < seg[j].b; e += blockDim.x) {
-                const int64_t x = col[e];
-                if (x < 0 || x >= n) f |= kOutOfRange;
-                if (e > first && e > 0) {
-                    const int64_t prev = col[e - 1];
-                    if (x == prev) f |= kDuplicate;
-                    else if (x < prev) f |= kUnsorted;
-                }
+        const int64_t c0 = c * kValidateChunk, c1 = c0 + kValidateChunk < nnz ? c0 + kValidateChunk : nnz;
+        for (int w = threadIdx.x; w < kValidateChunk / 32; w += kValidateThreads) s_start[w] = 0;
+        if (threadIdx.x == 0) {  // the last row r with rowptr[r] <= c0
+            int64_t lo = 0, hi = n;
+            while (hi - lo > 1) {
+                const int64_t mid = (lo + hi) >> 1;
+                if (rowptr[mid] <= c0) lo = mid;
+                else hi = mid;
+            }
+            s_row = lo;
+        }
+        __syncthreads();
+        // rows r0, r0 + 1, ... while they start before c1; a non-empty row starting
+        // inside the chunk marks its first entry
+        for (int64_t r = s_row + threadIdx.x;; r += kValidateThreads) {
+            const bool in = r < n;
+            const int64_t a = in ? rowptr[r] : c1;
+            const bool more = __syncthreads_or(in && a < c1);
+            if (in && a >= c0 && a < c1 && a < rowptr[r + 1]) {
+                const int64_t k = a - c0;
+                atomicOr(&s_start[k >> 5], 1u << (k & 31));
+            }
+            if (!more) break;
+        }
+        __syncthreads();
+        for (int64_t e = c0 + threadIdx.x; e < c1; e += kValidateThreads) {
+            const int64_t x = col[e];
+            if (x < 0 || x >= n) f |= kOutOfRange;
+            const int64_t k = e - c0;
+            if (e > 0 && !((s_start[k >> 5] >> (k & 31)) & 1u)) {
+                const int64_t prev = col[e - 1];
+                if (x == prev) f |= kDuplicate;
+                else if (x < prev) f |= kUnsorted;
             }
         }
+        __syncthreads();
     }
     if (f) atomicOr(flags, f);
 }
@@ -399,12 +380,12 @@ gt_status launch_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, con
                               hipStream_t s) {
     gt_status st = fill_u32(flags, 1, 0, s);
     if (st != GT_OK) return st;
-    k_validate_csr<<<grid_for(n > 0 ? n : 1, 256, 4096), 256, 0, s>>>(n, nnz, rowptr, col, flags);
-    GT_LAUNCH_CHECK("validate_csr");
-    if (n > 0 && nnz > kLongRow) {
-        k_validate_long<<<unsigned(long_chunks_of(nnz) < 4096 ? long_chunks_of(nnz) : 4096), 256, 0, s>>>(
-            n, nnz, rowptr, col, flags);
-        GT_LAUNCH_CHECK("validate_long");
+    k_validate_rows<<<grid_for(n > 0 ? n : 1, 256, 4096), 256, 0, s>>>(n, nnz, rowptr, flags);
+    GT_LAUNCH_CHECK("validate_rows");
+    if (n > 0 && nnz > 0) {
+        k_validate_entries<<<grid_for(nnz, kValidateChunk, 8192), kValidateThreads, 0, s>>>(n, nnz, rowptr, col,
+                                                                                            flags);
+        GT_LAUNCH_CHECK("validate_entries");
     }
     return GT_OK;
 }

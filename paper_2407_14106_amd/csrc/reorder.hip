@@ -8,11 +8,11 @@
 //   64 < deg <= 512    one wavefront per row, open-addressing count table in
 //                      the wavefront's share of LDS (no workgroup barriers).
 //   512 < deg <= 4096  one workgroup per row, open-addressing count table in LDS.
-//   4096 < deg <= 2^16 one workgroup per row, count table in the workspace.
-//   deg > 2^16         the whole grid (a global token attending to every node):
-//                      count table in the workspace filled by every workgroup,
-//                      then reduced by every workgroup in three passes (best
-//                      count, smallest hash, smallest label).
+//   deg > 4096         the whole grid (hubs, a global token attending to every
+//                      node): each row's count table in the workspace, filled
+//                      chunk by chunk by every workgroup, then reduced by every
+//                      workgroup in three passes (best count, smallest hash,
+//                      smallest label).
 // All three compute the same function of the neighbour-label multiset.
 #include <limits.h>
 
@@ -31,10 +31,8 @@ constexpr int kWaveTab = 2 * kWaveTabRowMax;  // per-wavefront table entries
 constexpr int kLdsTable = 8192;      // entries (int32 key + uint32 count): 64 KiB
 constexpr int kLdsRowMax = kLdsTable / 2;
 constexpr int kBlock = 256;
-constexpr int kBigRowBlock = 1024;  // threads per row of 4,097 to 2^16 edges (a few rows, one workgroup each)
 constexpr int kMaxSweeps = 1000;
 constexpr int kBigGrid = 1024;  // workgroups sharing each very long row
-constexpr int64_t kHugeRow = int64_t(1) << 16;
 
 __device__ __forceinline__ bool is_active(int64_t v, uint64_t key) {
     return (mix64(uint64_t(v) ^ key ^ kActivitySalt) >> 61) != 0;
@@ -66,7 +64,7 @@ __device__ __forceinline__ int wave_min_i32(int v) {
 
 __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
                            int32_t* is_s16, int32_t* is_s32, int32_t* is_wav, int32_t* is_wmed, int32_t* is_med,
-                           int32_t* is_big, int32_t* is_huge, int64_t* big_cap) {
+                           int32_t* is_huge, int64_t* big_cap) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         // self-loop present?  rows are sorted: binary search for v.
@@ -85,8 +83,7 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
         is_wmed[v] = (deg > kWaveRowMax && deg <= kWaveTabRowMax) ? 1 : 0;
         is_med[v] = (deg > kWaveTabRowMax && deg <= kLdsRowMax) ? 1 : 0;
         const bool big = deg > kLdsRowMax;
-        is_big[v] = big && deg <= kHugeRow ? 1 : 0;
-        is_huge[v] = deg > kHugeRow ? 1 : 0;
+        is_huge[v] = big ? 1 : 0;
         int64_t cap = 1;
         while (cap < 2 * deg) cap <<= 1;
         big_cap[v] = big ? cap : 0;
@@ -94,22 +91,17 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
 }
 
 __global__ void k_compact(int64_t n, const int32_t* is_s16, const int32_t* is_s32, const int32_t* is_wav,
-                          const int32_t* is_wmed, const int32_t* is_med, const int32_t* is_big,
-                          const int32_t* is_huge, const int64_t* pos_s16, const int64_t* pos_s32,
-                          const int64_t* pos_wav, const int64_t* pos_wmed, const int64_t* pos_med,
-                          const int64_t* pos_big, const int64_t* pos_huge, const int64_t* cap_off, int32_t* s16_list,
-                          int32_t* s32_list, int32_t* wav_list, int32_t* wmed_list, int32_t* med_list,
-                          int32_t* big_list, int64_t* big_off, int32_t* huge_list, int64_t* huge_off) {
+                          const int32_t* is_wmed, const int32_t* is_med, const int32_t* is_huge,
+                          const int64_t* pos_s16, const int64_t* pos_s32, const int64_t* pos_wav,
+                          const int64_t* pos_wmed, const int64_t* pos_med, const int64_t* pos_huge,
+                          const int64_t* cap_off, int32_t* s16_list, int32_t* s32_list, int32_t* wav_list,
+                          int32_t* wmed_list, int32_t* med_list, int32_t* huge_list, int64_t* huge_off) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         if (is_s16[v]) s16_list[pos_s16[v]] = int32_t(v);
         if (is_s32[v]) s32_list[pos_s32[v]] = int32_t(v);
         if (is_wav[v]) wav_list[pos_wav[v]] = int32_t(v);
         if (is_wmed[v]) wmed_list[pos_wmed[v]] = int32_t(v);
         if (is_med[v]) med_list[pos_med[v]] = int32_t(v);
-        if (is_big[v]) {
-            big_list[pos_big[v]] = int32_t(v);
-            big_off[pos_big[v]] = cap_off[v];
-        }
         if (is_huge[v]) {
             huge_list[pos_huge[v]] = int32_t(v);
             huge_off[pos_huge[v]] = cap_off[v];
@@ -280,12 +272,6 @@ __device__ __forceinline__ uint64_t block_min_u64(uint64_t v, uint64_t* s) {
 }
 
 
-template <bool kGlobal>
-__device__ __forceinline__ int tab_load(const int* p) {
-    if (kGlobal) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return *p;
-}
-
 // Adds k to the count of label L in an open-addressing table of cap slots.
 __device__ __forceinline__ void tab_add(int* tk, int* tc, int64_t cap, int L, int k) {
     int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
@@ -317,16 +303,15 @@ __device__ __forceinline__ void tab_add_wave(int* tk, int* tc, int64_t cap, bool
     if (pending) tab_add(tk, tc, cap, L, 1);
 }
 
-// One workgroup per listed row.  Table: keys (label or -1) and counts, in LDS
-// (rows up to kLdsRowMax) or in the workspace (up to kHugeRow).
-template <bool kGlobal, int BS>
+// One workgroup per listed row (rows up to kLdsRowMax).  Table: keys (label or
+// -1) and counts in LDS.
+template <int BS>
 __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int64_t* list_len,
-                                                     const int64_t* rowptr, const int32_t* col,
-                                                     const int32_t* lab_in, int32_t* lab_out, uint64_t key,
-                                                     const uint32_t* flag_prev, uint32_t* flag_next,
-                                                     int* gkeys, int* gcnts, const int64_t* big_off) {
-    __shared__ int s_keys[kGlobal ? 1 : kLdsTable];
-    __shared__ int s_cnts[kGlobal ? 1 : kLdsTable];
+                                                 const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
+                                                 int32_t* lab_out, uint64_t key, const uint32_t* flag_prev,
+                                                 uint32_t* flag_next) {
+    __shared__ int s_keys[kLdsTable];
+    __shared__ int s_cnts[kLdsTable];
     __shared__ int s_red[BS / kWave];
     __shared__ uint64_t s_red64[BS / kWave];
     const bool converged = *flag_prev == 0;
@@ -342,13 +327,12 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
         const int64_t deg = b - a;
         int64_t cap = 1;
         while (cap < 2 * deg) cap <<= 1;
-        int* tk = kGlobal ? gkeys + big_off[idx] : s_keys;
-        int* tc = kGlobal ? gcnts + big_off[idx] : s_cnts;
+        int* tk = s_keys;
+        int* tc = s_cnts;
         for (int64_t s = threadIdx.x; s < cap; s += BS) {
             tk[s] = -1;
             tc[s] = 0;
         }
-        if (kGlobal) __threadfence();
         __syncthreads();
         // wave-uniform rounds: each wavefront takes 64 consecutive edges per round
         for (int64_t base = a + (threadIdx.x & ~(kWave - 1)); base < b; base += BS) {
@@ -357,13 +341,12 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
             const bool valid = c != v;
             tab_add_wave(tk, tc, cap, valid, valid ? lab_in[c] : -1);
         }
-        if (kGlobal) __threadfence();
         __syncthreads();
         int best = 0, own_cnt = 0;
         for (int64_t s = threadIdx.x; s < cap; s += BS) {
-            const int k = tab_load<kGlobal>(&tk[s]);
+            const int k = tk[s];
             if (k < 0) continue;
-            const int c = tab_load<kGlobal>(&tc[s]);
+            const int c = tc[s];
             best = c > best ? c : best;
             if (k == own) own_cnt = c;
         }
@@ -373,16 +356,16 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
         if (best > 0 && own_cnt != best) {
             uint64_t hbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += BS) {
-                const int k = tab_load<kGlobal>(&tk[s]);
-                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
+                const int k = tk[s];
+                if (k < 0 || tc[s] != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 hbest = h < hbest ? h : hbest;
             }
             hbest = block_min_u64<BS>(hbest, s_red64);
             uint64_t lbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += BS) {
-                const int k = tab_load<kGlobal>(&tk[s]);
-                if (k < 0 || tab_load<kGlobal>(&tc[s]) != best) continue;
+                const int k = tk[s];
+                if (k < 0 || tc[s] != best) continue;
                 if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
                 lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
             }
@@ -477,9 +460,10 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
 }
 
 // -------------------------------------------------------------- very long rows
-// The edges and the table slots of each listed row are cut into chunks dealt
-// round-robin over the workgroups, so a row of a million edges is spread over
-// the chip and many long rows share it.  Per-row
+// The edges and the table slots of each listed row are cut into chunks,
+// numbered one after the other over all listed rows and dealt over the grid,
+// so a row of a million edges is spread over the chip and many long rows share
+// it.  Per-row
 // results: best count, own label's count, smallest hash among the best, and the
 // smallest label with that hash, combined with atomics (max / min: the result
 // does not depend on the order).
@@ -488,6 +472,8 @@ struct BigRows {
     const int32_t* list;
     const int64_t* len;
     const int64_t* off;   // table offset of each listed row
+    const int64_t* echunk;  // [listed rows + 1]: first edge chunk of each row (kLdsRowMax edges per chunk)
+    const int64_t* schunk;  // [listed rows + 1]: first table-slot chunk of each row (kSlotChunk slots per chunk)
     int* keys;
     int* cnts;
     int* best;            // [listed rows]
@@ -502,33 +488,52 @@ __device__ __forceinline__ int64_t table_cap(int64_t deg) {
     return cap;
 }
 
-// Table slots of every listed row in chunks of kSlotChunk, dealt round-robin
-// over the workgroups like the edge chunks below: every row gets as many
-// workgroups as its table needs.
+// Table slots of every listed row in chunks of kSlotChunk; the chunks of all
+// rows are numbered one after the other (the offsets are computed once per
+// call) and dealt over the grid, so every row gets as many workgroups as its
+// table needs and a workgroup finds its row by a binary search.
 constexpr int64_t kSlotChunk = 8192;
 
-__device__ __forceinline__ int64_t first_chunk(int64_t chunk0) {
-    return (int64_t(blockIdx.x) - chunk0 % gridDim.x + gridDim.x) % gridDim.x;
+// The listed row holding global chunk c (the last idx with off[idx] <= c).
+__device__ __forceinline__ int64_t chunk_row(const int64_t* __restrict__ off, int64_t len, int64_t c) {
+    int64_t lo = 0, hi = len;
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (off[mid] <= c) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
+__global__ void k_big_chunks(const int32_t* __restrict__ list, const int64_t* __restrict__ len_p,
+                             const int64_t* __restrict__ rowptr, int32_t* __restrict__ ecnt,
+                             int32_t* __restrict__ scnt) {
+    const int64_t len = *len_p;
+    for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < len;
+         idx += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t v = list[idx];
+        const int64_t deg = rowptr[v + 1] - rowptr[v];
+        ecnt[idx] = int32_t(cdiv(deg, kLdsRowMax));
+        scnt[idx] = int32_t(cdiv(table_cap(deg), kSlotChunk));
+    }
 }
 
 __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t* rowptr, const uint32_t* flag_prev) {
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
-    int64_t chunk0 = 0;
-    for (int64_t idx = 0; idx < len; ++idx) {
+    const int64_t total = br.schunk[len];
+    for (int64_t c = blockIdx.x; c < total; c += gridDim.x) {
+        const int64_t idx = chunk_row(br.schunk, len, c);
         const int64_t v = br.list[idx];
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
-        const int64_t chunks = cdiv(cap, kSlotChunk);
+        const int64_t j = c - br.schunk[idx];
         int* tk = br.keys + br.off[idx];
         int* tc = br.cnts + br.off[idx];
-        for (int64_t c = first_chunk(chunk0); c < chunks; c += gridDim.x) {
-            const int64_t s1 = (c + 1) * kSlotChunk < cap ? (c + 1) * kSlotChunk : cap;
-            for (int64_t s = c * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
-                tk[s] = -1;
-                tc[s] = 0;
-            }
+        const int64_t s1 = (j + 1) * kSlotChunk < cap ? (j + 1) * kSlotChunk : cap;
+        for (int64_t s = j * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
+            tk[s] = -1;
+            tc[s] = 0;
         }
-        chunk0 += chunks;
     }
     const int64_t stride = int64_t(gridDim.x) * kBlock, start = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     for (int64_t idx = start; idx < len; idx += stride) {
@@ -539,61 +544,60 @@ __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t*
     }
 }
 
-// Chunks of kLdsRowMax edges of every listed row, dealt round-robin over the
-// workgroups: each chunk is counted in an LDS table first, then its distinct
-// labels are added to the row's table in the workspace (far fewer global
-// atomics where neighbour labels repeat, as they do once clusters form).
+// Chunks of kLdsRowMax edges of every listed row, dealt over the grid: each
+// chunk is counted in an LDS table first, then its distinct labels are added
+// to the row's table in the workspace (far fewer global atomics where
+// neighbour labels repeat, as they do once clusters form).
 __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t* rowptr, const int32_t* col,
                                                        const int32_t* lab_in, const uint32_t* flag_prev) {
     __shared__ int s_keys[kLdsTable];
     __shared__ int s_cnts[kLdsTable];
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
-    int64_t chunk0 = 0;  // global index of the current row's first chunk
-    for (int64_t idx = 0; idx < len; ++idx) {
+    const int64_t total = br.echunk[len];
+    for (int64_t c = blockIdx.x; c < total; c += gridDim.x) {
+        const int64_t idx = chunk_row(br.echunk, len, c);
         const int64_t v = br.list[idx];
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         const int64_t cap = table_cap(b - a);
-        const int64_t chunks = cdiv(b - a, kLdsRowMax);
+        const int64_t j = c - br.echunk[idx];
         int* tk = br.keys + br.off[idx];
         int* tc = br.cnts + br.off[idx];
-        for (int64_t c = first_chunk(chunk0); c < chunks; c += gridDim.x) {
-            for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
-                s_keys[x] = -1;
-                s_cnts[x] = 0;
-            }
-            __syncthreads();
-            const int64_t e0 = a + c * kLdsRowMax;
-            const int64_t e1 = e0 + kLdsRowMax < b ? e0 + kLdsRowMax : b;
-            for (int64_t base = e0 + (threadIdx.x & ~(kWave - 1)); base < e1; base += kBlock) {
-                const int64_t e = base + lane_id();
-                const int cc = e < e1 ? col[e] : int(v);
-                const bool valid = cc != v;
-                tab_add_wave(s_keys, s_cnts, kLdsTable, valid, valid ? lab_in[cc] : -1);
-            }
-            __syncthreads();
-            for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
-                const int L = s_keys[x];
-                if (L < 0) continue;
-                int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
-                while (true) {
-                    const int prev = atomicCAS(&tk[slot], -1, L);
-                    if (prev == -1 || prev == L) {
-                        atomicAdd(&tc[slot], s_cnts[x]);
-                        break;
-                    }
-                    slot = (slot + 1) & (cap - 1);
-                }
-            }
-            __syncthreads();
+        for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
+            s_keys[x] = -1;
+            s_cnts[x] = 0;
         }
-        chunk0 += chunks;
+        __syncthreads();
+        const int64_t e0 = a + j * kLdsRowMax;
+        const int64_t e1 = e0 + kLdsRowMax < b ? e0 + kLdsRowMax : b;
+        for (int64_t base = e0 + (threadIdx.x & ~(kWave - 1)); base < e1; base += kBlock) {
+            const int64_t e = base + lane_id();
+            const int cc = e < e1 ? col[e] : int(v);
+            const bool valid = cc != v;
+            tab_add_wave(s_keys, s_cnts, kLdsTable, valid, valid ? lab_in[cc] : -1);
+        }
+        __syncthreads();
+        for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
+            const int L = s_keys[x];
+            if (L < 0) continue;
+            int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
+            while (true) {
+                const int prev = atomicCAS(&tk[slot], -1, L);
+                if (prev == -1 || prev == L) {
+                    atomicAdd(&tc[slot], s_cnts[x]);
+                    break;
+                }
+                slot = (slot + 1) & (cap - 1);
+            }
+        }
+        __syncthreads();
     }
 }
 
 // pass 0: best count and the own label's count; 1: smallest hash among the
 // best labels; 2: smallest label with that hash (passes 1-2 only where the own
-// label is not among the best).
+// label is not among the best).  Each slot chunk reduces in its workgroup and
+// adds its result with one atomic.
 template <int kPass>
 __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t* rowptr, const int32_t* lab_in,
                                                        uint64_t key, const uint32_t* flag_prev) {
@@ -601,28 +605,24 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
     __shared__ uint64_t s_red64[kBlock / kWave];
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
-    int64_t chunk0 = 0;
-    for (int64_t idx = 0; idx < len; ++idx) {
+    const int64_t total = br.schunk[len];
+    for (int64_t c = blockIdx.x; c < total; c += gridDim.x) {
+        const int64_t idx = chunk_row(br.schunk, len, c);
         const int64_t v = br.list[idx];
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
-        const int64_t chunks = cdiv(cap, kSlotChunk);
-        const int64_t c_first = first_chunk(chunk0);
-        chunk0 += chunks;
-        if (c_first >= chunks) continue;  // uniform across the workgroup
+        const int64_t j = c - br.schunk[idx];
+        const int64_t s0 = j * kSlotChunk, s1 = (j + 1) * kSlotChunk < cap ? (j + 1) * kSlotChunk : cap;
         const int own = lab_in[v];
         const int* tk = br.keys + br.off[idx];
         const int* tc = br.cnts + br.off[idx];
         if (kPass == 0) {
             int best = 0, oc = 0;
-            for (int64_t c = c_first; c < chunks; c += gridDim.x) {
-                const int64_t s1 = (c + 1) * kSlotChunk < cap ? (c + 1) * kSlotChunk : cap;
-                for (int64_t s = c * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
-                    const int k = tk[s];
-                    if (k < 0) continue;
-                    const int cnt = tc[s];
-                    best = cnt > best ? cnt : best;
-                    if (k == own) oc = cnt;
-                }
+            for (int64_t s = s0 + threadIdx.x; s < s1; s += kBlock) {
+                const int k = tk[s];
+                if (k < 0) continue;
+                const int cnt = tc[s];
+                best = cnt > best ? cnt : best;
+                if (k == own) oc = cnt;
             }
             best = block_max_i32(best, s_red);
             oc = block_max_i32(oc, s_red);
@@ -635,15 +635,12 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
             if (best == 0 || br.own_cnt[idx] == best) continue;  // uniform across the workgroup
             const uint64_t hb = kPass == 2 ? br.hbest[idx] : 0;
             uint64_t r = ~0ull;
-            for (int64_t c = c_first; c < chunks; c += gridDim.x) {
-                const int64_t s1 = (c + 1) * kSlotChunk < cap ? (c + 1) * kSlotChunk : cap;
-                for (int64_t s = c * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
-                    const int k = tk[s];
-                    if (k < 0 || tc[s] != best) continue;
-                    const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
-                    if (kPass == 1) r = h < r ? h : r;
-                    else if (h == hb) r = uint64_t(uint32_t(k)) < r ? uint64_t(uint32_t(k)) : r;
-                }
+            for (int64_t s = s0 + threadIdx.x; s < s1; s += kBlock) {
+                const int k = tk[s];
+                if (k < 0 || tc[s] != best) continue;
+                const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
+                if (kPass == 1) r = h < r ? h : r;
+                else if (h == hb) r = uint64_t(uint32_t(k)) < r ? uint64_t(uint32_t(k)) : r;
             }
             r = block_min_u64(r, s_red64);
             if (threadIdx.x == 0 && r != ~0ull) atomicMin(kPass == 1 ? &br.hbest[idx] : &br.lbest[idx], r);
@@ -696,7 +693,6 @@ struct ReorderWs {
     int32_t* is_wav;
     int32_t* is_wmed;
     int32_t* is_med;
-    int32_t* is_big;
     int32_t* is_huge;
     int64_t* big_cap;
     int64_t* pos_s16;
@@ -704,7 +700,6 @@ struct ReorderWs {
     int64_t* pos_wav;
     int64_t* pos_wmed;
     int64_t* pos_med;
-    int64_t* pos_big;
     int64_t* pos_huge;
     int64_t* cap_off;
     int32_t* s16_list;
@@ -712,10 +707,12 @@ struct ReorderWs {
     int32_t* wav_list;
     int32_t* wmed_list;
     int32_t* med_list;
-    int32_t* big_list;
-    int64_t* big_off;
     int32_t* huge_list;
     int64_t* huge_off;
+    int32_t* huge_ecnt;
+    int32_t* huge_scnt;
+    int64_t* huge_echunk;
+    int64_t* huge_schunk;
     int* tab_keys;
     int* tab_cnts;
     int64_t* class_cnt;  // [kClasses]: rows of each list class, for the host
@@ -731,17 +728,15 @@ struct ReorderWs {
 
 // The row counts of the list classes (the totals of their scans), gathered
 // so that one copy brings them to the host.
-enum { kClsS16, kClsS32, kClsWav, kClsWmed, kClsMed, kClsBig, kClsHuge, kClasses };
+enum { kClsS16, kClsS32, kClsWav, kClsWmed, kClsMed, kClsHuge, kClasses };
 __global__ void k_class_counts(int64_t n, const int64_t* s16, const int64_t* s32, const int64_t* wav,
-                               const int64_t* wmed, const int64_t* med, const int64_t* big, const int64_t* huge,
-                               int64_t* out) {
+                               const int64_t* wmed, const int64_t* med, const int64_t* huge, int64_t* out) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     out[kClsS16] = s16[n];
     out[kClsS32] = s32[n];
     out[kClsWav] = wav[n];
     out[kClsWmed] = wmed[n];
     out[kClsMed] = med[n];
-    out[kClsBig] = big[n];
     out[kClsHuge] = huge[n];
 }
 
@@ -763,7 +758,6 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.is_wav = ws.take<int32_t>(n1);
     r.is_wmed = ws.take<int32_t>(n1);
     r.is_med = ws.take<int32_t>(n1);
-    r.is_big = ws.take<int32_t>(n1);
     r.is_huge = ws.take<int32_t>(n1);
     r.big_cap = ws.take<int64_t>(n1);
     r.pos_s16 = ws.take<int64_t>(n1 + 1);
@@ -771,7 +765,6 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.pos_wav = ws.take<int64_t>(n1 + 1);
     r.pos_wmed = ws.take<int64_t>(n1 + 1);
     r.pos_med = ws.take<int64_t>(n1 + 1);
-    r.pos_big = ws.take<int64_t>(n1 + 1);
     r.pos_huge = ws.take<int64_t>(n1 + 1);
     r.cap_off = ws.take<int64_t>(n1 + 1);
     r.s16_list = ws.take<int32_t>(n1);
@@ -779,10 +772,12 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.wav_list = ws.take<int32_t>(n1);
     r.wmed_list = ws.take<int32_t>(n1);
     r.med_list = ws.take<int32_t>(n1);
-    r.big_list = ws.take<int32_t>(n1);
-    r.big_off = ws.take<int64_t>(n1);
     r.huge_list = ws.take<int32_t>(n1);
     r.huge_off = ws.take<int64_t>(n1);
+    r.huge_ecnt = ws.take<int32_t>(n1);
+    r.huge_scnt = ws.take<int32_t>(n1);
+    r.huge_echunk = ws.take<int64_t>(n1 + 1);
+    r.huge_schunk = ws.take<int64_t>(n1 + 1);
     const int64_t tab = 4 * (nnz > 0 ? nnz : 1);  // sum over big rows of cap <= 4 * deg
     r.tab_keys = ws.take<int>(size_t(tab));
     r.tab_cnts = ws.take<int>(size_t(tab));
@@ -833,20 +828,18 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
 
     const unsigned g = grid_for(n, 256, 8192);
     k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med,
-                                      r.is_big, r.is_huge, r.big_cap);
+                                      r.is_huge, r.big_cap);
     GT_LAUNCH_CHECK("reorder_classify");
     if ((st = exclusive_scan_i32(r.is_s16, n, r.pos_s16, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_s32, n, r.pos_s32, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_wav, n, r.pos_wav, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_wmed, n, r.pos_wmed, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_big, n, r.pos_big, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_huge, n, r.pos_huge, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
-    k_compact<<<g, 256, 0, stream>>>(n, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med, r.is_big, r.is_huge,
-                                     r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_big, r.pos_huge,
-                                     r.cap_off, r.s16_list, r.s32_list, r.wav_list, r.wmed_list, r.med_list,
-                                     r.big_list, r.big_off, r.huge_list, r.huge_off);
+    k_compact<<<g, 256, 0, stream>>>(n, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med, r.is_huge, r.pos_s16,
+                                     r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_huge, r.cap_off, r.s16_list,
+                                     r.s32_list, r.wav_list, r.wmed_list, r.med_list, r.huge_list, r.huge_off);
     GT_LAUNCH_CHECK("reorder_compact");
 
     if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
@@ -854,31 +847,31 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
     // the class sizes on the host: empty classes are not launched and grids fit the lists
-    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_big,
-                                         r.pos_huge, r.class_cnt);
+    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_huge,
+                                         r.class_cnt);
     GT_LAUNCH_CHECK("reorder_class_counts");
     int64_t cnt[kClasses] = {};
     GT_HIP(hipMemcpyAsync(cnt, r.class_cnt, sizeof(cnt), hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
-    const int64_t n_huge = cnt[kClsHuge], n_big = cnt[kClsBig];
-    BigRows br{r.huge_list, r.pos_huge + n, r.huge_off, r.tab_keys, r.tab_cnts, r.big_best, r.big_own,
-               r.big_hbest, r.big_lbest};
+    const int64_t n_huge = cnt[kClsHuge];
+    BigRows br{r.huge_list, r.pos_huge + n, r.huge_off, r.huge_echunk, r.huge_schunk, r.tab_keys, r.tab_cnts,
+               r.big_best, r.big_own, r.big_hbest, r.big_lbest};
+    if (n_huge > 0) {  // the chunk numbering of the long rows' edges and table slots
+        k_big_chunks<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(r.huge_list, r.pos_huge + n, rowptr,
+                                                                       r.huge_ecnt, r.huge_scnt);
+        GT_LAUNCH_CHECK("reorder_big_chunks");
+        if ((st = exclusive_scan_i32(r.huge_ecnt, n_huge, r.huge_echunk, r.scan, stream)) != GT_OK) return st;
+        if ((st = exclusive_scan_i32(r.huge_scnt, n_huge, r.huge_schunk, r.scan, stream)) != GT_OK) return st;
+    }
     const unsigned gw = grid_cap(cnt[kClsWav], kBlock / kWave, 65536);
     const unsigned g16 = grid_cap(cnt[kClsS16], kBlock / kSub16, 16384);
     const unsigned g32 = grid_cap(cnt[kClsS32], kBlock / kSub32, 16384);
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
     const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
-    const unsigned gbig = grid_cap(n_big, 1, 256);
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
         const int32_t* in = r.lab[t & 1];
         int32_t* out = r.lab[(t + 1) & 1];
-        if (n_big > 0) {
-            k_lp_block<true, kBigRowBlock><<<gbig, kBigRowBlock, 0, stream>>>(r.big_list, r.pos_big + n, rowptr, col, in,
-                                                                       out, key, r.flags + t, r.flags + t + 1,
-                                                                       r.tab_keys, r.tab_cnts, r.big_off);
-            GT_LAUNCH_CHECK("reorder_lp_global");
-        }
         if (n_huge > 0) {
             const uint32_t* fp = r.flags + t;
             k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp);
@@ -913,9 +906,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             GT_LAUNCH_CHECK("reorder_lp_wavetab");
         }
         if (cnt[kClsMed] > 0) {
-            k_lp_block<false, kBlock><<<gmed, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out,
-                                                                   key, r.flags + t, r.flags + t + 1, nullptr,
-                                                                   nullptr, nullptr);
+            k_lp_block<kBlock><<<gmed, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
+                                                            r.flags + t, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_lds");
         }
     }

@@ -404,8 +404,12 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
 // Checksum of the count results: the sum over the range's 8-byte words w_i of
 // mix64(w_i + i * 0x9E3779B97F4A7C15) (mod 2^64, so the order of the sums does
 // not matter); a changed or moved word changes it.
+// The wavefront sums meet in LDS, so each workgroup adds one value to the
+// total (a few hundred atomics on one address instead of one per wavefront).
+constexpr int kCsumBlocks = 512;
 __global__ __launch_bounds__(256) void k_ws_checksum(const uint64_t* __restrict__ p, int64_t words,
                                                      unsigned long long* __restrict__ out) {
+    __shared__ uint64_t s_part[256 / kWave];
     uint64_t acc = 0;
     const int64_t stride = int64_t(gridDim.x) * blockDim.x;
     for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < words; i += stride)
@@ -415,13 +419,20 @@ __global__ __launch_bounds__(256) void k_ws_checksum(const uint64_t* __restrict_
         const uint32_t lo = __shfl_xor(uint32_t(acc), o, kWave), hi = __shfl_xor(uint32_t(acc >> 32), o, kWave);
         acc += (uint64_t(hi) << 32) | lo;
     }
-    if (lane_id() == 0 && acc) atomicAdd(out, (unsigned long long)acc);
+    if (lane_id() == 0) s_part[threadIdx.x / kWave] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t t = 0;
+#pragma unroll
+        for (int w = 0; w < 256 / kWave; ++w) t += s_part[w];
+        if (t) atomicAdd(out, (unsigned long long)t);
+    }
 }
 
 gt_status ws_checksum(const TilesWs& t, hipStream_t s) {
     gt_status st = fill_u32(reinterpret_cast<uint32_t*>(t.csum), 2, 0u, s);
     if (st != GT_OK) return st;
-    k_ws_checksum<<<grid_for(t.kept_words, 256, 2048), 256, 0, s>>>(t.kept_begin, t.kept_words, t.csum);
+    k_ws_checksum<<<grid_for(t.kept_words, 256, kCsumBlocks), 256, 0, s>>>(t.kept_begin, t.kept_words, t.csum);
     GT_LAUNCH_CHECK("tiles_checksum");
     return GT_OK;
 }
