@@ -175,6 +175,13 @@ typedef struct gt_tiles {
     int32_t* tileT_idx;    /* int32[n_dense]: index into the (I, J)-sorted list */
     int32_t* long_rows;    /* int32[n_long_rows]: ascending */
     int32_t* long_cols;    /* int32[n_long_cols]: ascending */
+    /* Edge positions (optional, for a per-edge bias on a plan with dense
+     * tiles): when non-NULL at gt_build_tiles they are filled, and the input
+     * CSR must have nnz < 2^31.  Positions are those of the input CSR. */
+    int32_t* sp_pos;       /* int32[nnz_sparse]: position of each remainder edge */
+    int32_t* tile_pos;     /* int32[n_dense*T]: [k*T + r] = position of the first edge of local row r of dense
+                              tile k; the row's edges in the tile are the next popcount(mask row r) positions
+                              (0 where the row has none) */
 } gt_tiles;
 
 size_t gt_tiles_workspace_size(int64_t n, int64_t nnz, int32_t T);
@@ -325,16 +332,22 @@ gt_status gt_sparse_attn_bwd_cols(const gt_tiles* plan, int32_t H, int32_t d, gt
 /* With a per-edge additive bias, §2.1 Eq. (3) (the graph's structural
  * encoding, stored in the attention's sparse layout per §3.3):
  *   s_ij = scale*<Q[i,h],K[j,h]> + bias[e,h],
- * e the position of edge (i, j) in the plan's remainder CSR (sp_rowptr /
- * sp_col); bias and dbias are fp32 [nnz_sparse, H] device arrays.  The
- * backward also writes dbias[e,h] = dS_ij (every entry written).  The bias is
- * defined on remainder edges only, so a plan with dense tiles returns
- * GT_ERR_UNSUPPORTED: build the plan with tau_ppm > 10^6.  nnz_sparse < 2^31.
- * Workspaces are those of gt_sparse_attn_fwd / gt_sparse_attn_bwd.
+ * e the position of edge (i, j) in the input CSR the plan was built from, on
+ * remainder edges and dense-tile edges alike; bias and dbias are fp32 [nnz, H]
+ * device arrays (nnz = nnz_sparse + the dense tiles' edges, < 2^31).  The
+ * backward also writes dbias[e,h] = dS_ij (every entry written).  A plan with
+ * dense tiles must carry sp_pos and tile_pos (gt_build_tiles fills them when
+ * given); for a plan without dense tiles the remainder is the input CSR and
+ * they may be NULL.  On dense tiles the bias is laid out per tile in the
+ * workspace before the tile kernels run, and their dS written back to dbias
+ * at the edges' positions.
  * csc_pos (int32[nnz_sparse], device) comes from gt_edge_map for this plan:
- * csc_pos[c] is the remainder-CSR position of the c-th entry of sp_row. */
+ * csc_pos[c] is the input-CSR position of the c-th entry of sp_row (the
+ * remainder position where the plan has no sp_pos). */
 size_t gt_edge_map_workspace_size(const gt_tiles* plan);
 gt_status gt_edge_map(const gt_tiles* plan, int32_t* csc_pos, void* ws, size_t ws_bytes, hipStream_t stream);
+size_t gt_sparse_attn_fwd_bias_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
+size_t gt_sparse_attn_bwd_bias_workspace_size(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype);
 gt_status gt_sparse_attn_fwd_bias(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* Q,
                                   const void* K, const void* V, const float* bias, float scale, void* O, float* LSE,
                                   void* ws, size_t ws_bytes, hipStream_t stream);

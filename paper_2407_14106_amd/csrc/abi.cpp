@@ -23,7 +23,7 @@ gt_status hip_fail(hipError_t e, const char* what) {
 
 extern "C" {
 
-int32_t gt_abi_version(void) { return 1; }
+int32_t gt_abi_version(void) { return 2; }
 
 const char* gt_status_string(gt_status status) {
     switch (status) {

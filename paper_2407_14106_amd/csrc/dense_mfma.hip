@@ -881,7 +881,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_tiles_merge_sum(int64_t n, in
 // the kernels are latency-bound and more resident wavefronts pay more than
 // the operand reuse; the occupancy hints keep the accumulators out of the
 // AGPRs (forward: 4 wavefronts per SIMD at d = 32 and 64; dQ, dK/dV: 2-3).
-template <int D, int T, int NB>
+template <int D, int T, int NB, bool kBias = false>
 __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(D >= 64 ? 3 : 4))) void k_tiles_fwd(
     int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
                                                  const int32_t* __restrict__ tile_col,
@@ -889,7 +889,7 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(D >=
                                                  const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                                  const uint16_t* __restrict__ V, float sl2, float* __restrict__ pm,
                                                  float* __restrict__ pl, float* __restrict__ pacc, int64_t R,
-                                                 TileChunks ck) {
+                                                 TileChunks ck, TileBias tb) {
     constexpr int W = T / 32;
     __shared__ __attribute__((aligned(16))) uint16_t sK[1][kStage * RS<D>::v];
     __shared__ __attribute__((aligned(16))) uint16_t sVt[1][D * kTS];
@@ -968,13 +968,26 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(D >=
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const uint32_t w = mw[b][2 * st + kb];
+                if constexpr (kBias) {
+                    // scores in the exp2 domain with the bias added: s sl2 + b log2 e
+                    const int64_t tk = t0 + g / NSG;
+                    const int r = ql0 + 32 * b + (lane & 31);
 #pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if (!((w >> crow(i, lane)) & 1u)) s[b][i] = kNegInf;
+                    for (int i = 0; i < 16; ++i) {
+                        // the per-tile bias is -inf off the edges, so it masks the cell itself: no test and
+                        // no branch, which keeps the wait states of the accumulator reads that follow
+                        const float bb = tb.b[TileBias::at(tk, H, h, T, r, kStage * st + 32 * kb + crow(i, lane))];
+                        s[b][i] = fmaf(s[b][i], sl2, bb * kLog2e);
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 16; ++i)
+                        if (!((w >> crow(i, lane)) & 1u)) s[b][i] = kNegInf;
+                }
                 float mx = s[b][0];
 #pragma unroll
                 for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[b][i]);
-                mt[b] = pair_max(mx) * sl2;
+                mt[b] = kBias ? pair_max(mx) : pair_max(mx) * sl2;
                 grow |= mt[b] > m[b] + kLazy;
             }
             if (__builtin_amdgcn_ballot_w64(grow)) {
@@ -998,7 +1011,7 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(D >=
                 float ls = 0.f;
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const float p = ex2(fmaf(s[b][i], sl2, -mm));
+                    const float p = kBias ? ex2(s[b][i] - mm) : ex2(fmaf(s[b][i], sl2, -mm));
                     s[b][i] = p;
                     ls += p;
                 }
@@ -1051,7 +1064,7 @@ __device__ __forceinline__ void split_b16(const f32x16_t& w, int half, bf16x8_t&
 
 // Row pass over the dense tiles: A = sum P dP K, B = sum P K and the D sum
 // sum P dP of every owned row (the edge kernels form dQ = scale (A - D B)).
-template <int D, int T, int NB>
+template <int D, int T, int NB, bool kBias = false>
 __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 2 : 1))) void k_tiles_dq(
     int64_t n, int H, const int64_t* __restrict__ tile_rowptr,
                                                 const int32_t* __restrict__ tile_col,
@@ -1060,7 +1073,7 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB =
                                                 const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
                                                 const float* __restrict__ LSE, float sl2, float* __restrict__ pa,
                                                 float* __restrict__ pb, float* __restrict__ pd, int64_t R,
-                                                TileChunks ck) {
+                                                TileChunks ck, TileBias tb) {
     constexpr int W = T / 32;
     __shared__ __attribute__((aligned(16))) uint16_t sK[1][kStage * RS<D>::v];
     __shared__ __attribute__((aligned(16))) uint16_t sV[1][kStage * RS<D>::v];
@@ -1136,7 +1149,15 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB =
                 const uint32_t w = mw[b][2 * st + kb];
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const float p = (w >> crow(i, lane)) & 1u ? ex2(fmaf(s[b][i], sl2, -lse2[b])) : 0.f;
+                    float p;
+                    if constexpr (kBias) {
+                        const int64_t tk = t0 + g / NSG;
+                        const int r = ql0 + 32 * b + (lane & 31), c = kStage * st + 32 * kb + crow(i, lane);
+                        const float bb = tb.b[TileBias::at(tk, H, h, T, r, c)];
+                        p = ex2(fmaf(s[b][i], sl2, bb * kLog2e - lse2[b]));  // 0 off the edges (bias -inf)
+                    } else {
+                        p = (w >> crow(i, lane)) & 1u ? ex2(fmaf(s[b][i], sl2, -lse2[b])) : 0.f;
+                    }
                     s[b][i] = p;
                     dp[b][i] *= p;
                     dsum[b] += dp[b][i];
@@ -1208,7 +1229,7 @@ __device__ __forceinline__ uint64_t bit_transpose_64x32(uint32_t w, int lane) {
 // Column pass over the dense tiles: unscaled dK and dV sums of every owned key.
 // The stage's masks are transposed so that each lane holds, for its key, one
 // 64-bit word over the stage's 64 queries.
-template <int D, int T, int NB>
+template <int D, int T, int NB, bool kBias = false>
 __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 2 : 1))) void k_tiles_dkdv(
     int64_t n, int H, int64_t n_row_tiles,
                                                   const int64_t* __restrict__ tileT_ptr,
@@ -1219,7 +1240,7 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB =
                                                   const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
                                                   const float* __restrict__ LSE, const float* __restrict__ Dv,
                                                   float sl2, float* __restrict__ pdk, float* __restrict__ pdv,
-                                                  TileChunks ck) {
+                                                  TileChunks ck, TileBias tb) {
     constexpr int W = T / 32;
     __shared__ __attribute__((aligned(16))) uint16_t sQ[1][kStage * RS<D>::v];
     __shared__ __attribute__((aligned(16))) uint16_t sG[1][kStage * RS<D>::v];
@@ -1254,8 +1275,10 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB =
     Stager<D, NT> gq, gg;
     uint32_t mword[NB];  // this lane's row of the stage: mask words of the wavefront's key blocks
     float2 stat;        // LSE (exp2 domain) and D of the stage's query threadIdx.x % kStage
+    int64_t tk = 0;     // the stage's tile
     auto fetch = [&](int64_t g) {
         const int64_t k = tileT_idx[u0 + g / NSG];
+        tk = k;
         int64_t lo = 0, hi = n_row_tiles;  // tile row of tile k: the last I with tile_rowptr[I] <= k
         while (hi - lo > 1) {
             const int64_t mid = (lo + hi) >> 1;
@@ -1324,8 +1347,19 @@ __global__ __launch_bounds__(T * 2 / NB) __attribute__((amdgpu_waves_per_eu(NB =
                 const uint32_t w = uint32_t(mt[b] >> (32 * qb));
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const float p = (w >> crow(i, lane)) & 1u ? ex2(fmaf(s[b][i], sl2, -Lr[i])) : 0.f;
-                    s[b][i] = p * (dp[b][i] - Dr[i]);
+                    const bool on = (w >> crow(i, lane)) & 1u;
+                    float p = 0.f;
+                    if constexpr (kBias) {
+                        const int st = int(g % NSG);
+                        const int r = kStage * st + 32 * qb + crow(i, lane), c = kl0 + 32 * b + (lane & 31);
+                        const int64_t x = TileBias::at(tk, H, h, T, r, c);
+                        p = ex2(fmaf(s[b][i], sl2, tb.b[x] * kLog2e - Lr[i]));  // 0 off the edges (bias -inf)
+                        s[b][i] = p * (dp[b][i] - Dr[i]);
+                        tb.db[x] = s[b][i];  // every cell (0 off the edges), so no branch is needed
+                    } else {
+                        p = on ? ex2(fmaf(s[b][i], sl2, -Lr[i])) : 0.f;
+                        s[b][i] = p * (dp[b][i] - Dr[i]);
+                    }
                     dp[b][i] = p;
                 }
             }
@@ -1405,14 +1439,19 @@ gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, 
 
 template <int D>
 gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                         float sl2, TilePartials tp, hipStream_t s) {
+                         float sl2, TilePartials tp, TileBias tb, hipStream_t s) {
     gt_status st = tile_chunk_plan(p, p->tile_rowptr, tp.ck, s);
     if (st != GT_OK) return st;
     const dim3 grid(unsigned(tp.ck.max_chunks), unsigned(H));
     constexpr int NB = kTileNB;
-    GT_TILES_T((k_tiles_fwd<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col,
-                                                                    p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc,
-                                                                    p->n_row_tiles, tp.ck)));
+    if (tb.b)
+        GT_TILES_T((k_tiles_fwd<D, TT, NB, true><<<grid, TT * 2 / NB, 0, s>>>(
+            p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc, p->n_row_tiles,
+            tp.ck, tb)));
+    else
+        GT_TILES_T((k_tiles_fwd<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col,
+                                                                        p->tile_mask, Q, K, V, sl2, tp.m, tp.l,
+                                                                        tp.acc, p->n_row_tiles, tp.ck, tb)));
     GT_LAUNCH_CHECK("tiles_fwd_bf16");
     GT_TILES_T((k_tiles_merge_fwd<D, TT><<<merge_grid(tp.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, tp.ck, tp.m, tp.l, tp.acc)));
@@ -1422,14 +1461,20 @@ gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint
 
 template <int D>
 gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                        const uint16_t* dO, const float* LSE, float sl2, TilePartials dq, hipStream_t s) {
+                        const uint16_t* dO, const float* LSE, float sl2, TilePartials dq, TileBias tb,
+                        hipStream_t s) {
     gt_status st = tile_chunk_plan(p, p->tile_rowptr, dq.ck, s);
     if (st != GT_OK) return st;
     const dim3 grid(unsigned(dq.ck.max_chunks), unsigned(H));
     constexpr int NB = kTileNB;
-    GT_TILES_T((k_tiles_dq<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col,
-                                                                   p->tile_mask, Q, K, V, dO, LSE, sl2, dq.acc,
-                                                                   dq.acc2, dq.m, p->n_row_tiles, dq.ck)));
+    if (tb.b)
+        GT_TILES_T((k_tiles_dq<D, TT, NB, true><<<grid, TT * 2 / NB, 0, s>>>(
+            p->n, H, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, dO, LSE, sl2, dq.acc, dq.acc2, dq.m,
+            p->n_row_tiles, dq.ck, tb)));
+    else
+        GT_TILES_T((k_tiles_dq<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->tile_rowptr, p->tile_col,
+                                                                       p->tile_mask, Q, K, V, dO, LSE, sl2, dq.acc,
+                                                                       dq.acc2, dq.m, p->n_row_tiles, dq.ck, tb)));
     GT_LAUNCH_CHECK("tiles_dq_bf16");
     GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(dq.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, dq.ck, dq.acc, dq.acc2, dq.m)));
@@ -1440,15 +1485,20 @@ gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint1
 template <int D>
 gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                           const uint16_t* dO, const float* LSE, const float* Dv, float sl2, TilePartials dk,
-                          TilePartials dv, hipStream_t s) {
+                          TilePartials dv, TileBias tb, hipStream_t s) {
     gt_status st = tile_chunk_plan(p, p->tileT_ptr, dk.ck, s);
     if (st != GT_OK) return st;
     const dim3 grid(unsigned(dk.ck.max_chunks), unsigned(H));
     constexpr int NB = kTileNB;
-    GT_TILES_T((k_tiles_dkdv<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->n_row_tiles, p->tileT_ptr,
-                                                                     p->tileT_idx, p->tile_rowptr, p->tile_mask, Q,
-                                                                     K, V, dO, LSE, Dv, sl2, dk.acc, dv.acc,
-                                                                     dk.ck)));
+    if (tb.b)
+        GT_TILES_T((k_tiles_dkdv<D, TT, NB, true><<<grid, TT * 2 / NB, 0, s>>>(
+            p->n, H, p->n_row_tiles, p->tileT_ptr, p->tileT_idx, p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv,
+            sl2, dk.acc, dv.acc, dk.ck, tb)));
+    else
+        GT_TILES_T((k_tiles_dkdv<D, TT, NB><<<grid, TT * 2 / NB, 0, s>>>(p->n, H, p->n_row_tiles, p->tileT_ptr,
+                                                                         p->tileT_idx, p->tile_rowptr, p->tile_mask,
+                                                                         Q, K, V, dO, LSE, Dv, sl2, dk.acc, dv.acc,
+                                                                         dk.ck, tb)));
     GT_LAUNCH_CHECK("tiles_dkdv_bf16");
     GT_TILES_T((k_tiles_merge_sum<D, TT><<<merge_grid(dk.ck, H, TT, D), kMergeThreads, 0, s>>>(
         p->n, H, dk.ck, dk.acc, dv.acc, nullptr)));
@@ -1458,12 +1508,13 @@ gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uin
 
 #define GT_TILES_INST(D)                                                                                        \
     template gt_status tiles_fwd_bf16<D>(const gt_tiles*, int, const uint16_t*, const uint16_t*, const uint16_t*, \
-                                         float, TilePartials, hipStream_t);                                     \
+                                         float, TilePartials, TileBias, hipStream_t);                           \
     template gt_status tiles_dq_bf16<D>(const gt_tiles*, int, const uint16_t*, const uint16_t*, const uint16_t*,  \
-                                        const uint16_t*, const float*, float, TilePartials, hipStream_t);       \
+                                        const uint16_t*, const float*, float, TilePartials, TileBias,           \
+                                        hipStream_t);                                                           \
     template gt_status tiles_dkdv_bf16<D>(const gt_tiles*, int, const uint16_t*, const uint16_t*,                \
                                           const uint16_t*, const uint16_t*, const float*, const float*, float,  \
-                                          TilePartials, TilePartials, hipStream_t);
+                                          TilePartials, TilePartials, TileBias, hipStream_t);
 GT_TILES_INST(32)
 GT_TILES_INST(64)
 

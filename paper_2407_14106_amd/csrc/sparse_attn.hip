@@ -41,14 +41,23 @@ struct Lanes {
 
 // Per-edge additive bias (the graph encoding added to the scaled product,
 // §2.1 Eq. (3); it shares the attention's sparse layout, §3.3): fp32
-// [nnz, H] indexed by remainder-CSR position.  The column pass finds an
-// in-edge's CSR position through csc_pos and writes dB = dS there.
+// [nnz, H] indexed by the edge's position in the input CSR of the plan.  A
+// remainder edge's input position is sp_pos[remainder position] (the same
+// position when the plan has no dense tile and no sp_pos).  The column pass
+// finds an in-edge's input position through csc_pos and writes dB = dS there.
+// The dense tiles take the bias laid out per tile (tile).
 struct EdgeBias {
-    const float* b = nullptr;
+    const float* b = nullptr;  // null: no bias on the remainder edges
+    const int32_t* sp_pos = nullptr;
     const int32_t* csc_pos = nullptr;
     float* db = nullptr;
-    // bias of CSR position pos, head h, in the exp2 domain
-    __device__ __forceinline__ float at(int64_t pos, int H, int h) const { return b[pos * H + h] * kLog2e; }
+    TileBias tile;
+    // bias of remainder position pos, head h, in the exp2 domain
+    __device__ __forceinline__ float at(int64_t pos, int H, int h) const {
+        return b[(sp_pos ? int64_t(sp_pos[pos]) : pos) * H + h] * kLog2e;
+    }
+    // bias of input-CSR position e, head h, in the exp2 domain
+    __device__ __forceinline__ float at_input(int64_t e, int H, int h) const { return b[e * H + h] * kLog2e; }
 };
 
 // F fp32 accumulators of one (node, head) slice.
@@ -404,8 +413,8 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
         e1 = group_first<C::G>(p1);
         float x0 = 0.f, x1 = 0.f;
         if (ln.part == 0) {
-            x0 = ok0 ? eb.at(e0, H, ln.h) : 0.f;
-            x1 = ok1 ? eb.at(e1, H, ln.h) : 0.f;
+            x0 = ok0 ? eb.at_input(e0, H, ln.h) : 0.f;
+            x1 = ok1 ? eb.at_input(e1, H, ln.h) : 0.f;
         }
         s0 += group_bcast0<C::L>(x0);
         s1 += group_bcast0<C::L>(x1);
@@ -894,7 +903,7 @@ gt_status run_fwd_t(const gt_tiles* p, const void* Q, const void* K, const void*
     gt_status st;
     if (p->n_dense > 0) {
         if ((st = tile_fwd<T, D, H>(p, static_cast<const T*>(Q), static_cast<const T*>(K),
-                                    static_cast<const T*>(V), sl2, tp, s)) != GT_OK)
+                                    static_cast<const T*>(V), sl2, tp, eb.tile, s)) != GT_OK)
             return st;
     } else {
         tp = TilePartials{};
@@ -940,7 +949,7 @@ gt_status run_bwd_rows_t(const gt_tiles* p, const void* Q, const void* K, const 
     const T* g = static_cast<const T*>(dO);
     gt_status st;
     if (p->n_dense > 0) {
-        if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, g, LSE, sl2, tb.dq, s)) != GT_OK) return st;
+        if ((st = tile_bwd_dq<T, D, H>(p, q, k, v, g, LSE, sl2, tb.dq, eb.tile, s)) != GT_OK) return st;
     }
     const unsigned grid = xcd_grid(cdiv(cdiv(n, C::NPW), kThreads / kWave));
     k_bwd_rows<T, D, H, kBias><<<grid, kThreads, 0, s>>>(n, p->sp_rowptr, p->sp_col, p->nnz_sparse, q, k, v, g,
@@ -982,7 +991,8 @@ gt_status run_bwd_cols_t(const gt_tiles* p, const void* Q, const void* K, const 
     const T* g = static_cast<const T*>(dO);
     gt_status st;
     if (p->n_dense > 0) {
-        if ((st = tile_bwd_dkdv<T, D, H>(p, q, k, v, g, LSE, Dv, sl2, tb.dk, tb.dv, s)) != GT_OK) return st;
+        if ((st = tile_bwd_dkdv<T, D, H>(p, q, k, v, g, LSE, Dv, sl2, tb.dk, tb.dv, eb.tile, s)) != GT_OK)
+            return st;
     }
     k_pack_stats<<<grid_for(n * H, 256, 8192), 256, 0, s>>>(n * H, LSE, Dv, stat);
     GT_LAUNCH_CHECK("sparse_bwd_pack_stats");
@@ -1149,17 +1159,95 @@ extern "C" gt_status gt_sparse_attn_bwd(const gt_tiles* plan, int32_t H, int32_t
 }
 
 // ------------------------------------------------------------ with a bias
-// The bias is defined on the plan's remainder edges, so a plan with dense
-// tiles is refused (build it with tau_ppm above 10^6 to keep every edge in the
-// remainder).
+// The bias is indexed by input-CSR position.  Remainder edges read it through
+// sp_pos (forward, row pass) or csc_pos (column pass).  On a plan with dense
+// tiles it is first laid out per tile in the workspace (TileBias: the tile
+// kernels read it with the same cell indexing as their masks), and the column
+// pass's tile dS are written back to dbias at the tile edges' positions.
 
-static gt_status check_bias(const char* who, const gt_tiles* plan, const float* bias) {
-    if (plan->n_dense > 0)
-        return fail(GT_ERR_UNSUPPORTED, std::string(who) + ": the plan has dense tiles (bias needs an all-remainder plan)");
+namespace gt {
+namespace {
+
+int64_t tile_bias_elems(const gt_tiles* p, int32_t H) {
+    return p->n_dense > 0 ? p->n_dense * int64_t(H) * p->T * p->T : 0;
+}
+
+// The cells of local row r, word w (32 columns) of dense tile k: each thread
+// takes one (r, w), whose first edge position is tile_pos[k T + r] plus the
+// edges of the row's earlier words.  kToTiles: bias -> per-tile layout (-inf
+// off the edges, so the tile kernels need no mask test where they add it);
+// else per-tile dS -> dbias at the edges' positions.
+template <bool kToTiles>
+__global__ __launch_bounds__(256) void k_tile_bias_move(int H, int T, const uint32_t* __restrict__ mask,
+                                                        const int32_t* __restrict__ tile_pos,
+                                                        const float* __restrict__ src, float* __restrict__ dst) {
+    const int64_t k = blockIdx.x;
+    const int h = blockIdx.y;
+    const int W = T / 32;
+    for (int x = threadIdx.x; x < T * W; x += blockDim.x) {
+        const int r = x / W, w = x % W;
+        const uint32_t* row = mask + (k * T + r) * W;
+        int pre = 0;
+        for (int u = 0; u < w; ++u) pre += __popc(row[u]);
+        const uint32_t word = row[w];
+        const int64_t p0 = int64_t(tile_pos[k * T + r]) + pre;
+        const int64_t cell = TileBias::at(k, H, h, T, r, 32 * w);
+        for (int bit = 0; bit < 32; ++bit) {
+            const bool on = (word >> bit) & 1u;
+            const int64_t e = p0 + __popc(word & ((1u << bit) - 1u));
+            if (kToTiles) dst[cell + bit] = on ? src[e * H + h] : -__builtin_huge_valf();
+            else if (on) dst[e * H + h] = src[cell + bit];
+        }
+    }
+}
+
+gt_status tile_bias_move(bool to_tiles, const gt_tiles* p, int32_t H, const float* src, float* dst, hipStream_t s) {
+    if (p->n_dense <= 0) return GT_OK;
+    const dim3 grid(unsigned(p->n_dense), unsigned(H));
+    if (to_tiles) k_tile_bias_move<true><<<grid, 256, 0, s>>>(H, p->T, p->tile_mask, p->tile_pos, src, dst);
+    else k_tile_bias_move<false><<<grid, 256, 0, s>>>(H, p->T, p->tile_mask, p->tile_pos, src, dst);
+    GT_LAUNCH_CHECK("tile_bias_move");
+    return GT_OK;
+}
+
+gt_status check_bias(const char* who, const gt_tiles* plan, const float* bias) {
     if (plan->nnz_sparse >= (int64_t(1) << 31))
         return fail(GT_ERR_INVALID_ARG, std::string(who) + ": more than 2^31 - 1 edges");
-    if (plan->nnz_sparse > 0 && !bias) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": null bias");
+    if (plan->n_dense > 0 && ((plan->nnz_sparse > 0 && !plan->sp_pos) || !plan->tile_pos))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": a plan with dense tiles needs sp_pos and tile_pos "
+                                                            "(pass them to gt_build_tiles)");
+    if ((plan->nnz_sparse > 0 || plan->n_dense > 0) && !bias)
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": null bias");
     return GT_OK;
+}
+
+size_t fwd_bias_ws(const gt_tiles* p, int32_t H, int32_t d) {
+    Ws ws(nullptr);
+    ws.take<char>(fwd_ws(p, H, d));
+    ws.take<float>(size_t(tile_bias_elems(p, H)));
+    return ws.size();
+}
+size_t bwd_bias_ws(const gt_tiles* p, int32_t H, int32_t d) {
+    Ws ws(nullptr);
+    ws.take<char>(bwd_ws(p, H, d));
+    ws.take<float>(size_t(tile_bias_elems(p, H)));
+    ws.take<float>(size_t(tile_bias_elems(p, H)));
+    return ws.size();
+}
+
+}  // namespace
+}  // namespace gt
+
+extern "C" size_t gt_sparse_attn_fwd_bias_workspace_size(const gt_tiles* plan, int32_t H, int32_t d,
+                                                         gt_dtype dtype) {
+    if (!plan || !supported(H, d, dtype)) return 0;
+    return fwd_bias_ws(plan, H, d);
+}
+
+extern "C" size_t gt_sparse_attn_bwd_bias_workspace_size(const gt_tiles* plan, int32_t H, int32_t d,
+                                                         gt_dtype dtype) {
+    if (!plan || !supported(H, d, dtype)) return 0;
+    return bwd_bias_ws(plan, H, d);
 }
 
 extern "C" gt_status gt_sparse_attn_fwd_bias(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype,
@@ -1173,11 +1261,22 @@ extern "C" gt_status gt_sparse_attn_fwd_bias(const gt_tiles* plan, int32_t H, in
         return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_fwd_bias: unsupported (H, d, dtype)");
     if (plan->n > 0 && (!Q || !K || !V || !O || !LSE || !ws))
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_fwd_bias: null pointer");
-    if (ws_bytes < fwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_fwd_bias: workspace too small");
+    if (ws_bytes < fwd_bias_ws(plan, H, d))
+        return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_fwd_bias: workspace too small");
+    if (plan->n == 0) return GT_OK;
+    Ws w(ws);
+    void* main = w.take<char>(fwd_ws(plan, H, d));
     EdgeBias eb;
-    eb.b = bias;
-    if (plan->nnz_sparse == 0) eb.b = nullptr;
-    return GT_DISPATCH_ATTN(dtype, d, H, run_fwd, plan, Q, K, V, scale, O, LSE, ws, eb, stream);
+    if (plan->nnz_sparse > 0) {
+        eb.b = bias;
+        eb.sp_pos = plan->sp_pos;
+    }
+    if (plan->n_dense > 0) {
+        float* bt = w.take<float>(size_t(tile_bias_elems(plan, H)));
+        if ((st = tile_bias_move(true, plan, H, bias, bt, stream)) != GT_OK) return st;
+        eb.tile.b = bt;
+    }
+    return GT_DISPATCH_ATTN(dtype, d, H, run_fwd, plan, Q, K, V, scale, O, LSE, main, eb, stream);
 }
 
 extern "C" gt_status gt_sparse_attn_bwd_bias(const gt_tiles* plan, const int32_t* csc_pos, int32_t H, int32_t d,
@@ -1192,16 +1291,31 @@ extern "C" gt_status gt_sparse_attn_bwd_bias(const gt_tiles* plan, const int32_t
         return fail(GT_ERR_UNSUPPORTED, "gt_sparse_attn_bwd_bias: unsupported (H, d, dtype)");
     if (plan->n > 0 && (!Q || !K || !V || !dO || !LSE || !dQ || !dK || !dV || !ws))
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_bias: null pointer");
-    if (plan->nnz_sparse > 0 && (!csc_pos || !dbias))
+    if ((plan->nnz_sparse > 0 && !csc_pos) || ((plan->nnz_sparse > 0 || plan->n_dense > 0) && !dbias))
         return fail(GT_ERR_INVALID_ARG, "gt_sparse_attn_bwd_bias: null csc_pos or dbias");
-    if (ws_bytes < bwd_ws(plan, H, d)) return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_bias: workspace too small");
+    if (ws_bytes < bwd_bias_ws(plan, H, d))
+        return fail(GT_ERR_WORKSPACE, "gt_sparse_attn_bwd_bias: workspace too small");
+    if (plan->n == 0) return GT_OK;
+    Ws w(ws);
+    void* main = w.take<char>(bwd_ws(plan, H, d));
     EdgeBias eb;
     if (plan->nnz_sparse > 0) {
         eb.b = bias;
+        eb.sp_pos = plan->sp_pos;
         eb.csc_pos = csc_pos;
         eb.db = dbias;
     }
-    return GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, dO, LSE, scale, dQ, dK, dV, ws, eb, stream);
+    float* dbt = nullptr;
+    if (plan->n_dense > 0) {
+        float* bt = w.take<float>(size_t(tile_bias_elems(plan, H)));
+        dbt = w.take<float>(size_t(tile_bias_elems(plan, H)));
+        if ((st = tile_bias_move(true, plan, H, bias, bt, stream)) != GT_OK) return st;
+        eb.tile.b = bt;
+        eb.tile.db = dbt;
+    }
+    st = GT_DISPATCH_ATTN(dtype, d, H, run_bwd, plan, Q, K, V, dO, LSE, scale, dQ, dK, dV, main, eb, stream);
+    if (st != GT_OK) return st;
+    return dbt ? tile_bias_move(false, plan, H, dbt, dbias, stream) : GT_OK;
 }
 
 extern "C" gt_status gt_gather_probe(const gt_tiles* plan, int32_t H, int32_t d, gt_dtype dtype, const void* A,

@@ -53,6 +53,19 @@ struct TileBwdPartials {
     TilePartials dq, dk, dv;
 };
 
+// A per-edge bias on the dense tiles (the graph encoding of §2.1 Eq. (3)),
+// laid out per tile in the workspace: b[((k H + h) T + r) T + c] for local row
+// r and column c of dense tile k, -inf off the tile's edges (adding it masks
+// the cell).  The column pass writes dS into db at the same places (every
+// cell).  Null b: no bias.
+struct TileBias {
+    const float* b = nullptr;
+    float* db = nullptr;
+    __device__ __forceinline__ static int64_t at(int64_t k, int H, int h, int T, int r, int c) {
+        return ((k * H + h) * int64_t(T) + r) * T + c;
+    }
+};
+
 inline int tile_shift(int T) { return T == 128 ? 7 : 6; }
 
 // Carve the chunk plan and its extra slots (floats per slot row: per_row) out of the workspace.
@@ -115,7 +128,7 @@ inline TileBwdPartials tile_partials_bwd(Ws& ws, const gt_tiles* p, int H, int D
 // tiles, writes (m, l, acc) of the online softmax over its dense-tile edges.
 template <typename T, int D, int H>
 gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float sl2, TilePartials tp,
-                   hipStream_t s);
+                   TileBias tb, hipStream_t s);
 
 // Backward over the dense tiles, row-owned: for every node of a tile row with
 // dense tiles, the sums over its dense-tile edges of P dP K (acc), P K (acc2)
@@ -123,13 +136,14 @@ gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float 
 // dQ = scale (A - D B) with D the total P dP sum.
 template <typename T, int D, int H>
 gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
-                      float sl2, TilePartials dq, hipStream_t s);
+                      float sl2, TilePartials dq, TileBias tb, hipStream_t s);
 
 // Backward over the dense tiles, column-owned: dk (unscaled) and dv sums over
-// the dense-tile edges of every node of a tile column with dense tiles.
+// the dense-tile edges of every node of a tile column with dense tiles; with a
+// bias, dS of every tile edge into tb.db.
 template <typename T, int D, int H>
 gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
-                        const float* Dv, float sl2, TilePartials dk, TilePartials dv, hipStream_t s);
+                        const float* Dv, float sl2, TilePartials dk, TilePartials dv, TileBias tb, hipStream_t s);
 
 // The full softmax layer (every node attends to all n nodes) on the same
 // kernels: O and LSE; then D = <dO, O> (into Dv) and dQ; then dK and dV.
@@ -154,13 +168,14 @@ gt_status full_bwd_bf16(int64_t n, int H, const uint16_t* Q, const uint16_t* K, 
 // sums as tile_fwd / tile_bwd_dq / tile_bwd_dkdv, which call them for bf16.
 template <int D>
 gt_status tiles_fwd_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                         float sl2, TilePartials tp, hipStream_t s);
+                         float sl2, TilePartials tp, TileBias tb, hipStream_t s);
 template <int D>
 gt_status tiles_dq_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                        const uint16_t* dO, const float* LSE, float sl2, TilePartials dq, hipStream_t s);
+                        const uint16_t* dO, const float* LSE, float sl2, TilePartials dq, TileBias tb,
+                        hipStream_t s);
 template <int D>
 gt_status tiles_dkdv_bf16(const gt_tiles* p, int H, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                           const uint16_t* dO, const float* LSE, const float* Dv, float sl2, TilePartials dk,
-                          TilePartials dv, hipStream_t s);
+                          TilePartials dv, TileBias tb, hipStream_t s);
 
 }  // namespace gt

@@ -236,14 +236,14 @@ __device__ __forceinline__ uint32_t full_word(int64_t first, int64_t n) {
 // interleaved full layer) and the kernel writes O and LSE; otherwise it walks
 // the tile row's dense tiles and leaves (m, l, acc) partials.
 
-template <typename T, int D, int H, int TT, bool kFull>
+template <typename T, int D, int H, int TT, bool kFull, bool kBias = false>
 __global__ __launch_bounds__(2 * TT) void k_tile_fwd(int64_t n, const int64_t* __restrict__ tile_rowptr,
                                                       const int32_t* __restrict__ tile_col,
                                                       const uint32_t* __restrict__ tile_mask,
                                                       const T* __restrict__ Q, const T* __restrict__ K,
                                                       const T* __restrict__ V, float sl2, float* __restrict__ pm,
                                                       float* __restrict__ pl, float* __restrict__ pacc,
-                                                      T* __restrict__ O, float* __restrict__ LSE) {
+                                                      T* __restrict__ O, float* __restrict__ LSE, TileBias tb) {
     constexpr int NT = 2 * TT;  // threads: one wavefront per 32 rows
     constexpr int KB = TT / 32;
     constexpr int W = TT / 32;  // mask words per tile row
@@ -286,7 +286,14 @@ __global__ __launch_bounds__(2 * TT) void k_tile_fwd(int64_t n, const int64_t* _
             const uint32_t mw = kFull ? full_word(kbase + 32 * kb, n) : mrow[kb];
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const float v = ((mw >> crow(i, lane)) & 1u) ? s[kb][i] * sl2 : kNegInf;
+                float v;
+                if constexpr (kBias) {
+                    // the per-tile bias is -inf off the edges, so it masks the cell itself: no test and
+                    // no branch, which keeps the wait states of the accumulator reads that follow
+                    v = fmaf(s[kb][i], sl2, tb.b[TileBias::at(k, H, h, TT, qlocal, 32 * kb + crow(i, lane))] * kLog2e);
+                } else {
+                    v = ((mw >> crow(i, lane)) & 1u) ? s[kb][i] * sl2 : kNegInf;
+                }
                 s[kb][i] = v;
                 mloc = fmaxf(mloc, v);
             }
@@ -350,7 +357,7 @@ __global__ __launch_bounds__(2 * TT) void k_tile_fwd(int64_t n, const int64_t* _
 // Full layer (kFull): every weight is about 1/n, so D = <dO, O> from the given
 // O is used directly and dQ = scale K^T (P (dP - D)) is finished here.
 
-template <typename T, int D, int H, int TT, bool kFull>
+template <typename T, int D, int H, int TT, bool kFull, bool kBias = false>
 __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __restrict__ tile_rowptr,
                                                      const int32_t* __restrict__ tile_col,
                                                      const uint32_t* __restrict__ tile_mask,
@@ -359,7 +366,7 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
                                                      const T* __restrict__ dO, const float* __restrict__ LSE,
                                                      float sl2, float* __restrict__ pa, float* __restrict__ pb,
                                                      float* __restrict__ pd, T* __restrict__ dQ,
-                                                     float* __restrict__ Dv, float scale) {
+                                                     float* __restrict__ Dv, float scale, TileBias tb) {
     constexpr int NT = 2 * TT;
     constexpr int KB = TT / 32;
     constexpr int W = TT / 32;
@@ -412,7 +419,13 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
             const uint32_t mw = kFull ? (qok ? full_word(kbase + 32 * kb, n) : 0u) : mrow[kb];
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const float pv = ((mw >> crow(i, lane)) & 1u) ? ex2(p[i] * sl2 - lse2) : 0.f;
+                float pv;
+                if constexpr (kBias) {
+                    const float bb = tb.b[TileBias::at(k, H, h, TT, qlocal, 32 * kb + crow(i, lane))];
+                    pv = ex2(fmaf(p[i], sl2, bb * kLog2e) - lse2);  // 0 off the edges (bias -inf)
+                } else {
+                    pv = ((mw >> crow(i, lane)) & 1u) ? ex2(p[i] * sl2 - lse2) : 0.f;
+                }
                 p[i] = pv;
                 if (kFull) {
                     w[i] = pv * (w[i] - Dq);
@@ -456,7 +469,7 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dq(int64_t n, const int64_t* __
 
 // ----------------------------------------------------------- dK, dV (cols)
 
-template <typename T, int D, int H, int TT, bool kFull, bool kSplit>
+template <typename T, int D, int H, int TT, bool kFull, bool kSplit, bool kBias = false>
 __global__ __launch_bounds__(2 * TT) void k_tile_dkdv(int64_t n, const int64_t* __restrict__ tileT_ptr,
                                                        const int32_t* __restrict__ tileT_idx,
                                                        const int64_t* __restrict__ tile_rowptr,
@@ -465,7 +478,8 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dkdv(int64_t n, const int64_t* 
                                                        const T* __restrict__ V, const T* __restrict__ dO,
                                                        const float* __restrict__ LSE, const float* __restrict__ Dv,
                                                        float sl2, float* __restrict__ pdk, float* __restrict__ pdv,
-                                                       T* __restrict__ dK, T* __restrict__ dV, float scale) {
+                                                       T* __restrict__ dK, T* __restrict__ dV, float scale,
+                                                       TileBias tb) {
     constexpr int NT = 2 * TT;
     constexpr int QB = TT / 32;
     constexpr int W = TT / 32;
@@ -534,9 +548,17 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dkdv(int64_t n, const int64_t* 
             for (int i = 0; i < 16; ++i) {
                 const int r = 32 * qb + crow(i, lane);
                 const bool on = kFull ? (qbase + r < n) : ((sM[r * W + wv] >> (lane & 31)) & 1u);
-                const float pv = on ? ex2(s[i] * sl2 - sL[r]) : 0.f;
+                float pv;
+                if constexpr (kBias) {
+                    const int64_t x = TileBias::at(k, H, h, TT, r, klocal);
+                    pv = ex2(fmaf(s[i], sl2, tb.b[x] * kLog2e) - sL[r]);  // 0 off the edges (bias -inf)
+                    s[i] = pv * (dp[i] - sD[r]);
+                    tb.db[x] = s[i];  // every cell (0 off the edges), so no branch is needed
+                } else {
+                    pv = on ? ex2(s[i] * sl2 - sL[r]) : 0.f;
+                    s[i] = pv * (dp[i] - sD[r]);
+                }
                 p[i] = pv;
-                s[i] = pv * (dp[i] - sD[r]);
             }
 #pragma unroll
             for (int db = 0; db < D / 32; ++db) {
@@ -591,37 +613,52 @@ __global__ __launch_bounds__(2 * TT) void k_tile_dkdv(int64_t n, const int64_t* 
     } while (0)
 
 template <typename T, int D, int H>
-gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float sl2, TilePartials tp,
+gt_status tile_fwd(const gt_tiles* p, const T* Q, const T* K, const T* V, float sl2, TilePartials tp, TileBias tb,
                    hipStream_t s) {
-    if constexpr (Mma<T>::kBf16) return tiles_fwd_bf16<D>(p, H, Q, K, V, sl2, tp, s);
+    if constexpr (Mma<T>::kBf16) return tiles_fwd_bf16<D>(p, H, Q, K, V, sl2, tp, tb, s);
     const dim3 grid(unsigned(p->n_row_tiles), H);
-    GT_TILE_SWITCH(p->T, (k_tile_fwd<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
-                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc,
-                             nullptr, nullptr)));
+    if (tb.b)
+        GT_TILE_SWITCH(p->T, (k_tile_fwd<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
+                                 p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc,
+                                 nullptr, nullptr, tb)));
+    else
+        GT_TILE_SWITCH(p->T, (k_tile_fwd<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
+                                 p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, sl2, tp.m, tp.l, tp.acc,
+                                 nullptr, nullptr, tb)));
     GT_LAUNCH_CHECK("tile_fwd");
     return GT_OK;
 }
 
 template <typename T, int D, int H>
 gt_status tile_bwd_dq(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
-                      float sl2, TilePartials dq, hipStream_t s) {
-    if constexpr (Mma<T>::kBf16) return tiles_dq_bf16<D>(p, H, Q, K, V, dO, LSE, sl2, dq, s);
+                      float sl2, TilePartials dq, TileBias tb, hipStream_t s) {
+    if constexpr (Mma<T>::kBf16) return tiles_dq_bf16<D>(p, H, Q, K, V, dO, LSE, sl2, dq, tb, s);
     const dim3 grid(unsigned(p->n_row_tiles), H);
-    GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
-                             p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, nullptr, dO, LSE, sl2,
-                             dq.acc, dq.acc2, dq.m, nullptr, nullptr, 1.f)));
+    if (tb.b)
+        GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
+                                 p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, nullptr, dO, LSE, sl2,
+                                 dq.acc, dq.acc2, dq.m, nullptr, nullptr, 1.f, tb)));
+    else
+        GT_TILE_SWITCH(p->T, (k_tile_dq<T, D, H, TT, false><<<grid, 2 * TT, 0, s>>>(
+                                 p->n, p->tile_rowptr, p->tile_col, p->tile_mask, Q, K, V, nullptr, dO, LSE, sl2,
+                                 dq.acc, dq.acc2, dq.m, nullptr, nullptr, 1.f, tb)));
     GT_LAUNCH_CHECK("tile_bwd_dq");
     return GT_OK;
 }
 
 template <typename T, int D, int H>
 gt_status tile_bwd_dkdv(const gt_tiles* p, const T* Q, const T* K, const T* V, const T* dO, const float* LSE,
-                        const float* Dv, float sl2, TilePartials dk, TilePartials dv, hipStream_t s) {
-    if constexpr (Mma<T>::kBf16) return tiles_dkdv_bf16<D>(p, H, Q, K, V, dO, LSE, Dv, sl2, dk, dv, s);
+                        const float* Dv, float sl2, TilePartials dk, TilePartials dv, TileBias tb, hipStream_t s) {
+    if constexpr (Mma<T>::kBf16) return tiles_dkdv_bf16<D>(p, H, Q, K, V, dO, LSE, Dv, sl2, dk, dv, tb, s);
     const dim3 grid(unsigned(p->n_row_tiles), H);
-    GT_TILE_SWITCH(p->T, (k_tile_dkdv<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
-                             p->n, p->tileT_ptr, p->tileT_idx, p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE, Dv,
-                             sl2, dk.acc, dv.acc, nullptr, nullptr, 1.f)));
+    if (tb.b)
+        GT_TILE_SWITCH(p->T, (k_tile_dkdv<T, D, H, TT, false, true, true><<<grid, 2 * TT, 0, s>>>(
+                                 p->n, p->tileT_ptr, p->tileT_idx, p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE,
+                                 Dv, sl2, dk.acc, dv.acc, nullptr, nullptr, 1.f, tb)));
+    else
+        GT_TILE_SWITCH(p->T, (k_tile_dkdv<T, D, H, TT, false, true><<<grid, 2 * TT, 0, s>>>(
+                                 p->n, p->tileT_ptr, p->tileT_idx, p->tile_rowptr, p->tile_mask, Q, K, V, dO, LSE,
+                                 Dv, sl2, dk.acc, dv.acc, nullptr, nullptr, 1.f, tb)));
     GT_LAUNCH_CHECK("tile_bwd_dkdv");
     return GT_OK;
 }
@@ -632,7 +669,7 @@ gt_status full_fwd(int64_t n, const T* Q, const T* K, const T* V, float sl2, T* 
     constexpr int TT = 128;
     const dim3 grid(unsigned(cdiv(n, TT)), H);
     k_tile_fwd<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, sl2, nullptr,
-                                                          nullptr, nullptr, O, LSE);
+                                                          nullptr, nullptr, O, LSE, TileBias{});
     GT_LAUNCH_CHECK("full_fwd");
     return GT_OK;
 }
@@ -643,22 +680,23 @@ gt_status full_bwd(int64_t n, const T* Q, const T* K, const T* V, const T* O, co
     constexpr int TT = 128;
     const dim3 grid(unsigned(cdiv(n, TT)), H);
     k_tile_dq<T, D, H, TT, true><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, Q, K, V, O, dO, LSE, sl2,
-                                                         nullptr, nullptr, nullptr, dQ, Dv, scale);
+                                                         nullptr, nullptr, nullptr, dQ, Dv, scale, TileBias{});
     GT_LAUNCH_CHECK("full_bwd_dq");
     k_tile_dkdv<T, D, H, TT, true, false><<<grid, 2 * TT, 0, s>>>(n, nullptr, nullptr, nullptr, nullptr, Q, K, V,
-                                                                  dO, LSE, Dv, sl2, nullptr, nullptr, dK, dV, scale);
+                                                                  dO, LSE, Dv, sl2, nullptr, nullptr, dK, dV, scale,
+                                                                  TileBias{});
     GT_LAUNCH_CHECK("full_bwd_dkdv");
     return GT_OK;
 }
 
 #define GT_INST(T, D, H)                                                                                          \
     template gt_status tile_fwd<T, D, H>(const gt_tiles*, const T*, const T*, const T*, float, TilePartials,      \
-                                         hipStream_t);                                                            \
+                                         TileBias, hipStream_t);                                                  \
     template gt_status tile_bwd_dq<T, D, H>(const gt_tiles*, const T*, const T*, const T*, const T*,              \
-                                            const float*, float, TilePartials, hipStream_t);                      \
+                                            const float*, float, TilePartials, TileBias, hipStream_t);            \
     template gt_status tile_bwd_dkdv<T, D, H>(const gt_tiles*, const T*, const T*, const T*, const T*,            \
                                               const float*, const float*, float, TilePartials, TilePartials,      \
-                                              hipStream_t);                                                       \
+                                              TileBias, hipStream_t);                                             \
     template gt_status full_fwd<T, D, H>(int64_t, const T*, const T*, const T*, float, T*, float*, hipStream_t); \
     template gt_status full_bwd<T, D, H>(int64_t, const T*, const T*, const T*, const T*, const T*, const float*, \
                                          float, float, T*, T*, T*, float*, hipStream_t);

@@ -81,7 +81,8 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
                                                     int32_t* tile_nnz, uint32_t* tile_mask,
                                                     const int64_t* sp_rowptr, int32_t* sp_col,
                                                     uint32_t* sp_colkey, uint32_t* sp_rowval, uint32_t* sp_colcnt,
-                                                    int W, uint32_t* dense_bits, uint32_t* dense_pre) {
+                                                    int W, uint32_t* dense_bits, uint32_t* dense_pre,
+                                                    int32_t* sp_pos, int32_t* tile_pos) {
     __shared__ uint32_t s_cnt[kMaxR];
     __shared__ int64_t s_red[kTileThreads / kWave];
     __shared__ uint32_t s_hkey[kHash], s_hval[kHash];
@@ -178,12 +179,15 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
                     const int cl = c - J * T;
                     const int64_t word = k * int64_t(T) * wpr + rl * wpr + cl / 32;
                     atomicOr(&tile_mask[word], 1u << (cl & 31));
+                    // the row's first edge in this tile (its columns are sorted)
+                    if (tile_pos && (e == a || col[e - 1] / T != J)) tile_pos[k * T + rl] = int32_t(e);
                 }
                 if (sparse) {
                     const int64_t pos = sp_rowptr[i] + sp + __popcll(sb & lt);
                     sp_col[pos] = c;
                     sp_colkey[pos] = uint32_t(c);
                     sp_rowval[pos] = uint32_t(i);
+                    if (sp_pos) sp_pos[pos] = int32_t(e);
                 }
             }
             if (!kFill && sparse) {
@@ -273,7 +277,8 @@ __global__ __launch_bounds__(kThreads) void k_tiles_long_fill(int64_t n, int64_t
                                                               const uint32_t* dense_pre, const int64_t* segoff,
                                                               const int64_t* tile_rowptr, uint32_t* tile_mask,
                                                               const int64_t* sp_rowptr, int32_t* sp_col,
-                                                              uint32_t* sp_colkey, uint32_t* sp_rowval) {
+                                                              uint32_t* sp_colkey, uint32_t* sp_rowval,
+                                                              int32_t* sp_pos, int32_t* tile_pos) {
     __shared__ int64_t s_red[kThreads / kWave];
     const int64_t chunks = long_chunks_of(nnz);
     const int wpr = T / 32;
@@ -303,12 +308,14 @@ __global__ __launch_bounds__(kThreads) void k_tiles_long_fill(int64_t n, int64_t
                     const int64_t kk = tile_rowptr[I] + pre[J >> 5] + __popc(wd & ((1u << (J & 31)) - 1u));
                     const int cl = c - J * T;
                     atomicOr(&tile_mask[kk * int64_t(T) * wpr + (r - I * T) * wpr + cl / 32], 1u << (cl & 31));
+                    if (tile_pos && (e == first || col[e - 1] / T != J)) tile_pos[kk * T + (r - I * T)] = int32_t(e);
                 }
                 if (sparse) {
                     const int64_t pos = base + before;
                     sp_col[pos] = c;
                     sp_colkey[pos] = uint32_t(c);
                     sp_rowval[pos] = uint32_t(r);
+                    if (sp_pos) sp_pos[pos] = int32_t(e);
                 }
                 base += t;
             }
@@ -497,7 +504,7 @@ gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_
     if ((st = fill_u32(t.colcnt, n, 0u, stream)) != GT_OK) return st;
     k_tiles<false><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg, nullptr,
                                                nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                               t.colcnt, t.W, t.dense_bits, t.dense_pre);
+                                               t.colcnt, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr);
     GT_LAUNCH_CHECK("tiles_count");
     if (nnz > kLongRow) {
         k_tiles_long_count<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
@@ -577,6 +584,8 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         (plan->n_dense > 0 && (!plan->tile_col || !plan->tile_nnz || !plan->tile_mask || !plan->tileT_idx)) ||
         (plan->nnz_sparse > 0 && (!plan->sp_col || !plan->sp_row)))
         return fail(GT_ERR_INVALID_ARG, "gt_build_tiles: null plan array");
+    if ((plan->sp_pos || plan->tile_pos) && nnz >= (int64_t(1) << 31))
+        return fail(GT_ERR_INVALID_ARG, "gt_build_tiles: edge positions need nnz < 2^31");
     const int R = n > 0 ? int(cdiv(n, T)) : 0;
     plan->n_row_tiles = R;
     if (n == 0) {
@@ -621,9 +630,13 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     }
     const int64_t words = plan->n_dense * int64_t(T) * (T / 32);
     if ((st = fill_u32(plan->tile_mask, words, 0u, stream)) != GT_OK) return st;
+    if (plan->tile_pos && plan->n_dense > 0 &&
+        (st = fill_u32(reinterpret_cast<uint32_t*>(plan->tile_pos), plan->n_dense * T, 0u, stream)) != GT_OK)
+        return st;
     k_tiles<true><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
                                               plan->tile_col, plan->tile_nnz, plan->tile_mask, plan->sp_rowptr,
-                                              plan->sp_col, t.keys, t.vals, nullptr, t.W, nullptr, nullptr);
+                                              plan->sp_col, t.keys, t.vals, nullptr, t.W, nullptr, nullptr,
+                                              plan->sp_pos, plan->tile_pos);
     GT_LAUNCH_CHECK("tiles_fill");
     if (nnz > kLongRow) {
         const int64_t segs = 2 * long_chunks_of(nnz);
@@ -634,7 +647,7 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         if ((st = exclusive_scan_i32(t.segcnt, segs, t.segoff, t.scan, stream)) != GT_OK) return st;
         k_tiles_long_fill<<<long_grid(nnz), kThreads, 0, stream>>>(
             n, nnz, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.segoff, plan->tile_rowptr, plan->tile_mask,
-            plan->sp_rowptr, plan->sp_col, t.keys, t.vals);
+            plan->sp_rowptr, plan->sp_col, t.keys, t.vals, plan->sp_pos, plan->tile_pos);
         GT_LAUNCH_CHECK("tiles_long_fill");
     }
     // remainder transpose: stable sort of (column, row) pairs by column; the
@@ -662,7 +675,13 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
 }
 
 // CSC -> CSR position map of the remainder: the same stable sort by column
-// that orders the transpose, carrying each edge's CSR position.
+// that orders the transpose, carrying each edge's remainder position, then
+// mapped to the input CSR through sp_pos when the plan has it.
+__global__ void k_map_positions(int64_t m, const uint32_t* rem, const int32_t* sp_pos, int32_t* out) {
+    for (int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; e < m; e += int64_t(gridDim.x) * blockDim.x)
+        out[e] = sp_pos ? sp_pos[rem[e]] : int32_t(rem[e]);
+}
+
 static size_t edge_map_ws(int64_t m) {
     Ws ws(nullptr);
     const int64_t e1 = m > 0 ? m : 1;
@@ -694,7 +713,7 @@ extern "C" gt_status gt_edge_map(const gt_tiles* plan, int32_t* csc_pos, void* w
     if ((st = copy_bytes(keys, plan->sp_col, m * 4, stream)) != GT_OK) return st;
     if ((st = iota_u32(vals, m, stream)) != GT_OK) return st;
     if ((st = radix_sort_u32(keys, vals, m, bits_for(n), sort, stream)) != GT_OK) return st;
-    k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, vals, csc_pos);
+    k_map_positions<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, vals, plan->sp_pos, csc_pos);
     GT_LAUNCH_CHECK("edge_map");
     return GT_OK;
 }

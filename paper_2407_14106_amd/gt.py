@@ -41,6 +41,7 @@ class GtTiles(ctypes.Structure):
         ("tile_rowptr", _vp), ("tile_col", _vp), ("tile_nnz", _vp), ("tile_mask", _vp),
         ("sp_rowptr", _vp), ("sp_col", _vp), ("sp_colptr", _vp), ("sp_row", _vp),
         ("tileT_ptr", _vp), ("tileT_idx", _vp), ("long_rows", _vp), ("long_cols", _vp),
+        ("sp_pos", _vp), ("tile_pos", _vp),
     ]
 
 
@@ -94,6 +95,8 @@ SIGNATURES = {
                                        _vp, _vp, _sz, _vp]),
     "gt_edge_map_workspace_size": (_sz, [_P(GtTiles)]),
     "gt_edge_map": (_i32, [_P(GtTiles), _vp, _vp, _sz, _vp]),
+    "gt_sparse_attn_fwd_bias_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
+    "gt_sparse_attn_bwd_bias_workspace_size": (_sz, [_P(GtTiles), _i32, _i32, _i32]),
     "gt_sparse_attn_fwd_bias": (_i32, [_P(GtTiles), _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp,
                                        _sz, _vp]),
     "gt_sparse_attn_bwd_bias": (_i32, [_P(GtTiles), _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32,
@@ -310,6 +313,7 @@ class Plan:
 
     c: GtTiles
     arrays: dict
+    nnz: int = -1  # edges of the input CSR (remainder plus dense tiles)
 
     @property
     def n(self):
@@ -339,12 +343,13 @@ def tau_to_ppm(tau: float) -> int:
 
 
 def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: int = 10000, *,
-                build_ws: torch.Tensor | None = None, between=None) -> Plan:
+                build_ws: torch.Tensor | None = None, between=None, edge_positions: bool = False) -> Plan:
     """Tile plan of the CSR at tile edge T and density threshold tau_ppm (parts per million).
 
     gt_tiles_count and gt_build_tiles share one workspace, so the build takes the counts from it.  build_ws
     gives the build call a workspace of its own instead, and between(ws) runs between the two calls; with
-    either, the build counts again (the library checks the workspace)."""
+    either, the build counts again (the library checks the workspace).  edge_positions: also fill sp_pos and
+    tile_pos (the input-CSR positions a per-edge bias needs on a plan with dense tiles)."""
     lib = load_library()
     _check_csr(rowptr, col)
     n, nnz = rowptr.numel() - 1, col.numel()
@@ -371,6 +376,9 @@ def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: 
         "long_rows": torch.empty(c.n_long_rows, **i32),
         "long_cols": torch.empty(c.n_long_cols, **i32),
     }
+    if edge_positions:
+        arrays["sp_pos"] = torch.empty(ns, **i32)
+        arrays["tile_pos"] = torch.empty(nd * T, **i32)
     for k, v in arrays.items():
         setattr(c, k, v.data_ptr())
     if between is not None:
@@ -381,7 +389,7 @@ def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: 
     _check(lib.gt_build_tiles(n, nnz, _ptr(rowptr), _ptr(col), T, tau_ppm, ctypes.byref(c), _ptr(ws), ws.numel(), st),
            "gt_build_tiles")
     arrays["tile_mask"] = arrays["tile_mask"].view(torch.int32)
-    return Plan(c=c, arrays=arrays)
+    return Plan(c=c, arrays=arrays, nnz=nnz)
 
 
 # ------------------------------------------------------------------------------ attention
@@ -479,7 +487,7 @@ def gather_probe(plan: Plan, A: torch.Tensor, B: torch.Tensor, sink: torch.Tenso
 
 
 def edge_map(plan: Plan) -> torch.Tensor:
-    """csc_pos[c]: the remainder-CSR position of the c-th entry of the plan's transpose (sp_row)."""
+    """csc_pos[c]: the input-CSR position of the c-th entry of the plan's transpose (sp_row)."""
     lib = load_library()
     dev = plan.arrays["sp_rowptr"].device
     out = torch.empty(plan.nnz_sparse, dtype=torch.int32, device=dev)
@@ -489,12 +497,12 @@ def edge_map(plan: Plan) -> torch.Tensor:
 
 
 def _check_bias(plan: Plan, bias: torch.Tensor, H: int):
-    _need(bias.dtype == torch.float32 and bias.shape == (plan.nnz_sparse, H) and bias.is_contiguous()
-          and bias.is_cuda, "bias must be a contiguous fp32 GPU tensor [nnz_sparse, H]")
+    _need(bias.dtype == torch.float32 and bias.shape == (plan.nnz, H) and bias.is_contiguous()
+          and bias.is_cuda, "bias must be a contiguous fp32 GPU tensor [nnz, H] in the input CSR's order")
 
 
 def sparse_attn_fwd_bias(plan: Plan, Q, K, V, bias, scale: float | None = None):
-    """(O, LSE) with the per-edge additive bias (remainder-CSR order, fp32 [nnz_sparse, H])."""
+    """(O, LSE) with the per-edge additive bias (the input CSR's edge order, fp32 [nnz, H])."""
     lib = load_library()
     _check_feats(plan.n, Q, K, V)
     n, H, d = Q.shape
@@ -503,7 +511,7 @@ def sparse_attn_fwd_bias(plan: Plan, Q, K, V, bias, scale: float | None = None):
     dt = _dtype_code(Q)
     O = torch.empty_like(Q)
     LSE = torch.empty((n, H), dtype=torch.float32, device=Q.device)
-    ws = _workspace(lib.gt_sparse_attn_fwd_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    ws = _workspace(lib.gt_sparse_attn_fwd_bias_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
     _check(lib.gt_sparse_attn_fwd_bias(ctypes.byref(plan.c), H, d, dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(bias), scale,
                                        _ptr(O), _ptr(LSE), _ptr(ws), ws.numel(), _stream(Q.device)),
            "gt_sparse_attn_fwd_bias")
@@ -522,7 +530,7 @@ def sparse_attn_bwd_bias(plan: Plan, csc_pos, Q, K, V, bias, dO, LSE, scale: flo
     dt = _dtype_code(Q)
     dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
     dB = torch.empty_like(bias)
-    ws = _workspace(lib.gt_sparse_attn_bwd_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
+    ws = _workspace(lib.gt_sparse_attn_bwd_bias_workspace_size(ctypes.byref(plan.c), H, d, dt), Q.device)
     _check(lib.gt_sparse_attn_bwd_bias(ctypes.byref(plan.c), _ptr(csc_pos), H, d, dt, _ptr(Q), _ptr(K), _ptr(V),
                                        _ptr(bias), _ptr(dO), _ptr(LSE), scale, _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(dB),
                                        _ptr(ws), ws.numel(), _stream(Q.device)), "gt_sparse_attn_bwd_bias")

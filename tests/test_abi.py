@@ -51,14 +51,14 @@ def test_library_creates_no_runtime_objects(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.gt_abi_version() == 1
+    assert lib.gt_abi_version() == 2
     assert lib.gt_status_string(gt.GT_OK) == b"ok"
     assert lib.gt_status_string(gt.GT_ERR_WORKSPACE) == b"workspace too small"
     assert lib.gt_status_string(-99) == b"unknown status"
 
 
 def test_struct_layout_matches_header():
-    assert ctypes.sizeof(gt.GtTiles) == 8 * 6 + 4 * 2 + 8 * 12
+    assert ctypes.sizeof(gt.GtTiles) == 8 * 6 + 4 * 2 + 8 * 14
 
 
 def test_workspace_queries_are_host_only(lib):
@@ -130,11 +130,14 @@ def test_extension_entry_points_reject_bad_arguments(lib):
     for name in ("tile_rowptr", "sp_rowptr", "sp_colptr", "tileT_ptr", "sp_col", "sp_row"):
         setattr(c, name, 0x1000)
     ws = 1 << 30
-    # bias calls: a plan with dense tiles is refused, a null bias too
+    # bias calls: a plan with dense tiles but no edge positions is refused, a null bias too
     c.n_dense = 3
     c.tile_col = c.tile_mask = c.tileT_idx = 0x1000
     assert lib.gt_sparse_attn_fwd_bias(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, FAKE, 1.0, FAKE, FAKE,
-                                       FAKE, ws, stream) == gt.GT_ERR_UNSUPPORTED
+                                       FAKE, ws, stream) == gt.GT_ERR_INVALID_ARG
+    assert b"sp_pos and tile_pos" in lib.gt_last_error()
+    assert (lib.gt_sparse_attn_bwd_bias_workspace_size(ctypes.byref(c), 8, 32, gt.GT_BF16)
+            >= lib.gt_sparse_attn_bwd_workspace_size(ctypes.byref(c), 8, 32, gt.GT_BF16) + 2 * 3 * 8 * 128 * 128 * 4)
     c.n_dense = 0
     assert lib.gt_sparse_attn_fwd_bias(ctypes.byref(c), 8, 32, gt.GT_BF16, FAKE, FAKE, FAKE, None, 1.0, FAKE, FAKE,
                                        FAKE, ws, stream) == gt.GT_ERR_INVALID_ARG

@@ -12,13 +12,15 @@ import pytest
 import torch
 
 from oracle import attention as OA
+from oracle import plan as OP
 from synth import csr_from_pairs, make_workload
 from synth.tensors import normal_tensor
 from tests.helpers import assert_close, dev_csr, dev_feat, grad_term_rms, host
 
 pytestmark = pytest.mark.gpu
 
-CSR_ONLY = 1_000_001  # no dense tile: the bias is defined on remainder edges
+CSR_ONLY = 1_000_001  # no dense tile: every edge on the edge kernels
+SWEEP = (0, 10_000, 50_000, CSR_ONLY)  # every non-empty tile dense, 1%, 5%, none
 
 
 def say(*a):
@@ -30,28 +32,32 @@ def dev_bias(b):
     return torch.from_numpy(np.ascontiguousarray(b, dtype=np.float32)).cuda()
 
 
-def run_bias_case(gt, rowptr, col, H, d, dtype, seed, bias_sigma=1.0):
+def run_bias_case(gt, rowptr, col, H, d, dtype, seed, bias_sigma=1.0, taus=(CSR_ONLY,), T=128):
+    # The bias is one array in the input CSR's edge order whatever the plan: the dense tiles (sp_pos and
+    # tile_pos in the plan) and the remainder take their edges' values from it, and dB comes back in it.
     n = len(rowptr) - 1
     q, k, v, do = (normal_tensor((n, H, d), (seed, t), dtype) for t in range(4))
     b = bias_sigma * normal_tensor((len(col), H), (seed, 4), "f32")
     scale = 1.0 / np.sqrt(d)
-    say("bias case", n, len(col), H, d, dtype)
     O_ref, L_ref = OA.sparse_attn_fwd(rowptr, col, q, k, v, scale, bias=b)
     ref = OA.sparse_attn_bwd(rowptr, col, q, k, v, do, scale, bias=b)
+    floors = grad_term_rms(rowptr, col, q, k, v, do, scale)
     rp, cl = dev_csr(rowptr, col)
-    plan = gt.build_tiles(rp, cl, 128, CSR_ONLY)
-    assert plan.n_dense == 0 and plan.nnz_sparse == len(col)
     Q, K, V, dO = (dev_feat(x, dtype) for x in (q, k, v, do))
     B = dev_bias(b)
-    csc = gt.edge_map(plan)
-    O, L = gt.sparse_attn_fwd_bias(plan, Q, K, V, B, scale)
-    grads = gt.sparse_attn_bwd_bias(plan, csc, Q, K, V, B, dO, L, scale)
-    torch.cuda.synchronize()
-    assert_close(host(O), O_ref, dtype, "O")
-    assert_close(L.cpu().numpy(), L_ref, dtype, "LSE")
-    floors = grad_term_rms(rowptr, col, q, k, v, do, scale)
-    for name, x, r, rho in zip(("dQ", "dK", "dV", "dB"), grads, ref, floors):
-        assert_close(host(x), r, dtype, name, rho=rho)
+    for tau in taus:
+        say("bias case", n, len(col), H, d, dtype, T, tau)
+        plan = gt.build_tiles(rp, cl, T, tau, edge_positions=True)
+        if tau == CSR_ONLY:
+            assert plan.n_dense == 0 and plan.nnz_sparse == len(col)
+        csc = gt.edge_map(plan)
+        O, L = gt.sparse_attn_fwd_bias(plan, Q, K, V, B, scale)
+        grads = gt.sparse_attn_bwd_bias(plan, csc, Q, K, V, B, dO, L, scale)
+        torch.cuda.synchronize()
+        assert_close(host(O), O_ref, dtype, f"O tau={tau}")
+        assert_close(L.cpu().numpy(), L_ref, dtype, f"LSE tau={tau}")
+        for name, x, r, rho in zip(("dQ", "dK", "dV", "dB"), grads, ref, floors):
+            assert_close(host(x), r, dtype, f"{name} tau={tau}", rho=rho)
 
 
 def test_edge_map_is_the_stable_column_order(gt):
@@ -89,7 +95,64 @@ def test_permute_edges_carries_positions(gt):
 @pytest.mark.parametrize("H,d", [(1, 64), (4, 32), (8, 32), (8, 64), (16, 32)])
 def test_bias_small_graph(gt, dtype, H, d):
     g = make_workload("c1", 0.1).graph
-    run_bias_case(gt, g.rowptr, g.col, H, d, dtype, seed=300 + H * 10 + d)
+    run_bias_case(gt, g.rowptr, g.col, H, d, dtype, seed=300 + H * 10 + d, taus=SWEEP)
+
+
+@pytest.mark.parametrize("T", [64, 128])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_bias_on_dense_tiles_of_a_clustered_graph(gt, T, dtype):
+    # a block-model graph in planted order: diagonal tiles above 5%, so the bias reaches the matrix-core tiles
+    w = make_workload("c5", 0.03)
+    g = w.graph
+    order = np.lexsort((np.arange(g.n), g.block))
+    inv = np.empty(g.n, np.int64)
+    inv[order] = np.arange(g.n)
+    rp, cl = OP.permute_csr(g.rowptr, g.col, order, inv)
+    run_bias_case(gt, rp, cl, 4, 64, dtype, seed=T + 7, taus=SWEEP, T=T)
+
+
+def test_bias_on_hub_tiles_in_chunks(gt):
+    # hub tile rows and columns (several dense tiles per tile row and column, dealt to several workgroups and
+    # merged) with a bias of spread 4
+    n = 2117
+    rng = np.random.default_rng(15)
+    hub_r = np.repeat(np.arange(96), n // 2)
+    hub_rc = rng.integers(0, n, size=len(hub_r))
+    hub_c = np.repeat(np.arange(200, 264), n // 2)
+    hub_cr = rng.integers(0, n, size=len(hub_c))
+    bu, bv = rng.integers(0, n, size=6 * n), rng.integers(0, n, size=6 * n)
+    u = np.concatenate([hub_r, hub_cr, bu])
+    v = np.concatenate([hub_rc, hub_c, bv])
+    rowptr, col = csr_from_pairs(n, u, v, symmetric=False, self_loops=True)
+    run_bias_case(gt, rowptr, col, 8, 32, "bf16", seed=61, bias_sigma=4.0, taus=(0, 50_000), T=128)
+    run_bias_case(gt, rowptr, col, 2, 64, "f32", seed=62, taus=(0, 50_000), T=64)
+
+
+def test_plan_edge_positions(gt):
+    # sp_pos and tile_pos of a plan with dense tiles and long rows, against positions found on the host
+    g = make_workload("b1", 0.01).graph
+    assert np.diff(g.rowptr).max() > 2048  # the global token's row takes the plan's long-row fill
+    rp, cl = dev_csr(g.rowptr, g.col)
+    for T, tau in ((128, 10_000), (64, 50_000), (128, 0)):
+        plan = gt.build_tiles(rp, cl, T, tau, edge_positions=True)
+        assert plan.n_dense > 0
+        arr = plan.to_numpy()
+        rows = np.repeat(np.arange(g.n), np.diff(g.rowptr))
+        dense = set(zip(np.repeat(np.arange(len(arr["tile_rowptr"]) - 1), np.diff(arr["tile_rowptr"])).tolist(),
+                        arr["tile_col"].tolist()))
+        in_tile = np.array([(int(r) // T, int(c) // T) in dense for r, c in zip(rows, g.col)])
+        np.testing.assert_array_equal(arr["sp_pos"], np.flatnonzero(~in_tile))
+        tile_index = {t: k for k, t in enumerate(zip(np.repeat(np.arange(len(arr["tile_rowptr"]) - 1),
+                                                               np.diff(arr["tile_rowptr"])).tolist(),
+                                                     arr["tile_col"].tolist()))}
+        want = np.zeros(plan.n_dense * T, np.int64)
+        for e in np.flatnonzero(in_tile)[::-1]:  # the smallest position of each (tile, row) wins
+            r, c = int(rows[e]), int(g.col[e])
+            want[tile_index[(r // T, c // T)] * T + r % T] = e
+        np.testing.assert_array_equal(arr["tile_pos"], want)
+        csc = gt.edge_map(plan).cpu().numpy()
+        rem = np.argsort(arr["sp_col"], kind="stable")
+        np.testing.assert_array_equal(csc, arr["sp_pos"][rem])
 
 
 def test_bias_ragged_empty_rows_single_node(gt):
@@ -139,7 +202,7 @@ def test_zero_bias_matches_plain_path(gt):
     assert_close(host(withb[3]), ref[3], "bf16", "dB")
 
 
-def test_bias_refuses_a_plan_with_dense_tiles(gt):
+def test_bias_needs_edge_positions_on_a_plan_with_dense_tiles(gt):
     w = make_workload("c4", 0.01)
     g = w.graph
     rp, cl = dev_csr(g.rowptr, g.col)
@@ -147,15 +210,15 @@ def test_bias_refuses_a_plan_with_dense_tiles(gt):
     assert plan.n_dense > 0
     q, k, v, _ = w.tensors()
     Q, K, V = (dev_feat(x, "bf16") for x in (q, k, v))
-    B = torch.zeros((plan.nnz_sparse, w.heads), dtype=torch.float32, device="cuda")
+    B = torch.zeros((g.nnz, w.heads), dtype=torch.float32, device="cuda")
     with pytest.raises(gt.GtError) as e:
         gt.sparse_attn_fwd_bias(plan, Q, K, V, B)
-    assert e.value.status == gt.GT_ERR_UNSUPPORTED
+    assert e.value.status == gt.GT_ERR_INVALID_ARG
 
 
 def test_bias_pipeline_relabel_carries_the_bias(gt):
-    # reorder + relabel (with the edge map) on the GPU, the bias gathered into the new edge order, attention,
-    # everything scattered back: equals the oracle on the original graph and bias order.
+    # reorder + relabel (with the edge map) on the GPU, the bias gathered into the new edge order, attention on
+    # a plan with dense tiles, everything scattered back: equals the oracle on the original graph and bias order.
     w = make_workload("c5", 0.05)
     g = w.graph
     q, k, v, do = w.tensors()
@@ -164,7 +227,8 @@ def test_bias_pipeline_relabel_carries_the_bias(gt):
     rp, cl = dev_csr(g.rowptr, g.col)
     perm, iperm, _ = gt.reorder(rp, cl)
     rp2, cl2, src = gt.permute_csr_edges(rp, cl, perm, iperm)
-    plan = gt.build_tiles(rp2, cl2, 128, CSR_ONLY)
+    plan = gt.build_tiles(rp2, cl2, 128, 10_000, edge_positions=True)
+    assert plan.n_dense > 0
     Q, K, V, dO = (gt.gather_rows(dev_feat(x, "bf16"), perm) for x in (q, k, v, do))
     B = gt.gather_rows(dev_bias(b), src)
     O, L = gt.sparse_attn_fwd_bias(plan, Q, K, V, B, scale)
