@@ -225,6 +225,172 @@ __device__ __forceinline__ void bias_pair(const EdgeBias& eb, int64_t a, int t, 
     b1 = group_bcast0<LN::C::L>(x1);
 }
 
+// The bias of four edges of each of a wavefront's nodes moves through LDS, so
+// that a lane reads one vector (the floats 4H/G g .. of the quad's block, all
+// within one edge) instead of one float per edge: kPer floats per lane, each
+// group's block of 4H floats at `s`.  The wavefront alone uses its block, and
+// its LDS operations take effect in program order, so no barrier is needed.
+template <typename T, int D, int H>
+struct BiasStage {
+    using C = EdgeCfg<T, D, H>;
+    static constexpr int kPer = 4 * H / C::G;
+    static constexpr bool kOn = kPer >= 1 && kPer <= H;
+    static constexpr int kWaveFloats = C::NPW * 4 * H;
+};
+
+// Input-CSR positions of a row's (column's) edges t .. t + 3: base + off[u].
+struct Quad {
+    int64_t base;
+    int4 off;
+    __device__ __forceinline__ int64_t at(int u) const {
+        return base + (u == 0 ? off.x : u == 1 ? off.y : u == 2 ? off.z : off.w);
+    }
+};
+
+template <int P>
+__device__ __forceinline__ void ld_floats(float (&v)[P], const float* __restrict__ src) {
+    if constexpr (P == 4) {
+        const float4 x = *reinterpret_cast<const float4*>(src);
+        v[0] = x.x, v[1] = x.y, v[2] = x.z, v[3] = x.w;
+    } else if constexpr (P == 2) {
+        const float2 x = *reinterpret_cast<const float2*>(src);
+        v[0] = x.x, v[1] = x.y;
+    } else {
+        v[0] = *src;
+    }
+}
+template <int P>
+__device__ __forceinline__ void st_floats(float* __restrict__ dst, const float (&v)[P]) {
+    if constexpr (P == 4) *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+    else if constexpr (P == 2) *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
+    else *dst = v[0];
+}
+
+__device__ __forceinline__ void lds_order() {
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// This lane's share of the quad's bias block (kPer floats of one edge); 0 past deg.
+template <typename T, int D, int H, int P>
+__device__ __forceinline__ void bias_share(float (&v)[P], const float* __restrict__ b, const Quad& q, int t, int deg,
+                                           const Lanes<T, D, H>& ln) {
+    const int e0 = (ln.h * EdgeCfg<T, D, H>::L + ln.part) * P, u = e0 / H;
+#pragma unroll
+    for (int k = 0; k < P; ++k) v[k] = 0.f;
+    if (t + u < deg) ld_floats<P>(v, b + q.at(u) * H + e0 % H);
+}
+
+// The shares of a group through LDS: the bias (exp2 domain) of the quad's four
+// edges for this lane's head.
+template <typename T, int D, int H, int P>
+__device__ __forceinline__ float4 bias_swap(const float (&v)[P], const Lanes<T, D, H>& ln, float* s) {
+    const int e0 = (ln.h * EdgeCfg<T, D, H>::L + ln.part) * P;
+    lds_order();
+#pragma unroll
+    for (int k = 0; k < P; ++k) s[e0 + k] = v[k];
+    lds_order();
+    float4 x = make_float4(s[ln.h], s[H + ln.h], s[2 * H + ln.h], s[3 * H + ln.h]);
+    lds_order();
+    x.x *= kLog2e, x.y *= kLog2e, x.z *= kLog2e, x.w *= kLog2e;
+    return x;
+}
+
+// Write ds (this lane's head, edges t .. t + 3) to db at the quad's positions.
+template <typename T, int D, int H>
+__device__ __forceinline__ void db_quad(float* __restrict__ db, const Quad& q, int t, int deg, float4 ds,
+                                        const Lanes<T, D, H>& ln, float* s) {
+    constexpr int P = BiasStage<T, D, H>::kPer;
+    lds_order();
+    if (ln.part == 0) {
+        s[ln.h] = ds.x;
+        s[H + ln.h] = ds.y;
+        s[2 * H + ln.h] = ds.z;
+        s[3 * H + ln.h] = ds.w;
+    }
+    lds_order();
+    const int e0 = (ln.h * EdgeCfg<T, D, H>::L + ln.part) * P, u = e0 / H;
+    float v[P];
+#pragma unroll
+    for (int k = 0; k < P; ++k) v[k] = s[e0 + k];
+    lds_order();
+    if (t + u < deg) st_floats<P>(db + q.at(u) * H + e0 % H, v);
+}
+
+// Positions of a row's remainder edges t .. t + 3 (through sp_pos when the
+// plan has one) or of a column's in-edges (through csc_pos); past deg they
+// repeat a valid position.
+__device__ __forceinline__ Quad row_quad(const EdgeBias& eb, int64_t len, int64_t a, int deg, int t) {
+    Quad q;
+    if (eb.sp_pos) {
+        q.base = 0;
+        q.off = edge_quad(eb.sp_pos, len, a, deg, t, 0);
+    } else {
+        q.base = a;
+        q.off = make_int4(t, t + 1 < deg ? t + 1 : t, t + 2 < deg ? t + 2 : t, t + 3 < deg ? t + 3 : t);
+    }
+    return q;
+}
+__device__ __forceinline__ Quad col_quad(const EdgeBias& eb, int64_t len, int64_t a, int deg, int t) {
+    Quad q;
+    q.base = 0;
+    q.off = edge_quad(eb.csc_pos, len, a, deg, t, 0);
+    return q;
+}
+
+// walk_edges for a bias kernel, the bias exchanged in LDS when a quad starts;
+// step(j0, j1, t, ok0, ok1, b0, b1) takes two edges, after(t, q) runs once the
+// quad's steps are done (the column pass writes dB there).  kAhead: positions
+// two quads ahead and bias shares one quad ahead, their loads in flight across
+// a quad's steps (the forward and the column pass; the row pass, with more
+// live registers, reads each quad's when it starts).
+template <typename T, int D, int H, bool kAhead, class QuadOf, class Step, class After>
+__device__ __forceinline__ void walk_edges_bias(const int32_t* __restrict__ cl, int64_t len, int64_t a, int deg,
+                                                int dmax, int32_t self, const float* __restrict__ b,
+                                                const Lanes<T, D, H>& ln, float* s, QuadOf quad_of, Step step,
+                                                After after) {
+    constexpr int P = BiasStage<T, D, H>::kPer;
+    int4 cur = edge_quad(cl, len, a, deg, 0, self), nxt = cur;
+    if constexpr (kAhead) {
+        Quad q0 = quad_of(0);
+        Quad q1 = 4 < dmax ? quad_of(4) : q0;
+        float v[P];
+        bias_share<T, D, H, P>(v, b, q0, 0, deg, ln);
+        for (int t = 0; t < dmax; t += 4) {
+            float vn[P];
+#pragma unroll
+            for (int k = 0; k < P; ++k) vn[k] = 0.f;
+            Quad q2 = q1;
+            if (t + 4 < dmax) {
+                nxt = edge_quad(cl, len, a, deg, t + 4, self);
+                bias_share<T, D, H, P>(vn, b, q1, t + 4, deg, ln);
+            }
+            if (t + 8 < dmax) q2 = quad_of(t + 8);
+            const float4 x = bias_swap<T, D, H, P>(v, ln, s);
+            step(cur.x, cur.y, t, t < deg, t + 1 < deg, x.x, x.y);
+            if (t + 2 < dmax) step(cur.z, cur.w, t + 2, t + 2 < deg, t + 3 < deg, x.z, x.w);
+            after(t, q0);
+            cur = nxt;
+            q0 = q1;
+            q1 = q2;
+#pragma unroll
+            for (int k = 0; k < P; ++k) v[k] = vn[k];
+        }
+    } else {
+        for (int t = 0; t < dmax; t += 4) {
+            if (t + 4 < dmax) nxt = edge_quad(cl, len, a, deg, t + 4, self);
+            const Quad q = quad_of(t);
+            float v[P];
+            bias_share<T, D, H, P>(v, b, q, t, deg, ln);
+            const float4 x = bias_swap<T, D, H, P>(v, ln, s);
+            step(cur.x, cur.y, t, t < deg, t + 1 < deg, x.x, x.y);
+            if (t + 2 < dmax) step(cur.z, cur.w, t + 2, t + 2 < deg, t + 3 < deg, x.z, x.w);
+            after(t, q);
+            cur = nxt;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ forward
 
 template <typename T, int D, int H, bool kBias>
@@ -253,11 +419,24 @@ __global__ __launch_bounds__(kThreads) void k_fwd_rows(int64_t n, const int64_t*
     q.load(Q + off);
     Online<C::F> st;
     if (live && deg >= 0 && tp.has_row(i)) load_fwd_partial<T, D, H>(st, tp, i, ln.h, off);
-    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
-        float b0 = 0.f, b1 = 0.f;
-        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln, b0, b1);
-        fwd_step<T, D, H, kBias>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
-    });
+    using BS = BiasStage<T, D, H>;
+    if constexpr (kBias && BS::kOn) {
+        __shared__ float s_bias[kThreads / kWave][BS::kWaveFloats];
+        float* sb = s_bias[threadIdx.x / kWave] + ln.slot * 4 * H;
+        walk_edges_bias<T, D, H, true>(
+            cl, len, a, deg, dmax, int32_t(self), eb.b, ln, sb,
+            [&](int t) { return row_quad(eb, len, a, deg, t); },
+            [&](int64_t j0, int64_t j1, int, bool ok0, bool ok1, float b0, float b1) {
+                fwd_step<T, D, H, true>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
+            },
+            [](int, const Quad&) {});
+    } else {
+        walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
+            float b0 = 0.f, b1 = 0.f;
+            if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln, b0, b1);
+            fwd_step<T, D, H, kBias>(st, q, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
+        });
+    }
     if (live && deg >= 0) {
         const float inv = st.l > 0.f ? 1.f / st.l : 0.f;
         store_slice<T, C::F>(O + off, st.acc, inv);
@@ -362,11 +541,24 @@ __global__ __launch_bounds__(kThreads) void k_bwd_rows(int64_t n, const int64_t*
     const float lse2 = LSE[self * H + ln.h] * kLog2e;
     RowSums<C::F> rs;
     if (live && deg >= 0 && tp.has_row(i)) load_row_partial<T, D, H>(rs, tp, i, ln.h, off);
-    walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
-        float b0 = 0.f, b1 = 0.f;
-        if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln, b0, b1);
-        dq_step<T, D, H, kBias>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
-    });
+    using BS = BiasStage<T, D, H>;
+    if constexpr (kBias && BS::kOn) {
+        __shared__ float s_bias[kThreads / kWave][BS::kWaveFloats];
+        float* sb = s_bias[threadIdx.x / kWave] + ln.slot * 4 * H;
+        walk_edges_bias<T, D, H, false>(
+            cl, len, a, deg, dmax, int32_t(self), eb.b, ln, sb,
+            [&](int t) { return row_quad(eb, len, a, deg, t); },
+            [&](int64_t j0, int64_t j1, int, bool ok0, bool ok1, float b0, float b1) {
+                dq_step<T, D, H, true>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
+            },
+            [](int, const Quad&) {});
+    } else {
+        walk_edges(cl, len, a, deg, dmax, int32_t(self), [&](int64_t j0, int64_t j1, int t, bool ok0, bool ok1) {
+            float b0 = 0.f, b1 = 0.f;
+            if constexpr (kBias) bias_pair(eb, a, t, ok0, ok1, H, ln, b0, b1);
+            dq_step<T, D, H, kBias>(rs, q, g, lse2, K, V, j0, j1, ok0, ok1, ln, sl2, b0, b1);
+        });
+    }
     if (live && deg >= 0) {
 #pragma unroll
         for (int f = 0; f < C::F; ++f) rs.a.v[f] = fmaf(-rs.d, rs.b.v[f], rs.a.v[f]);
@@ -384,7 +576,8 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
                                          const Slice<T, EdgeCfg<T, D, H>::F>& v, const T* __restrict__ Q,
                                          const T* __restrict__ dO, const float2* __restrict__ stat, int64_t i0,
                                          int64_t i1, bool ok0, bool ok1, const Lanes<T, D, H>& ln, float sl2,
-                                         const EdgeBias& eb = EdgeBias{}, int64_t c0 = 0, int64_t c1 = 0) {
+                                         const EdgeBias& eb = EdgeBias{}, int64_t c0 = 0, int64_t c1 = 0,
+                                         float* staged = nullptr) {
     using C = EdgeCfg<T, D, H>;
     Slice<T, C::F> q0, q1, g0, g1;
     q0.load(Q + ln.off(i0));
@@ -402,7 +595,11 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
     float s0 = group_sum<C::L>(q0.dot(k)) * sl2;
     float s1 = group_sum<C::L>(q1.dot(k)) * sl2;
     int64_t e0 = 0, e1 = 0;
-    if constexpr (kBias) {
+    if (kBias && staged) {
+        // staged: the bias came through LDS (staged[0..1]), dS goes back in staged[2..3]
+        s0 += staged[0];
+        s1 += staged[1];
+    } else if constexpr (kBias) {
         // the node's first lane reads the CSR positions, one lane per head the bias
         int p0 = 0, p1 = 0;
         if ((lane_id() & (C::G - 1)) == 0) {
@@ -425,7 +622,10 @@ __device__ __forceinline__ void dkv_step(Acc<EdgeCfg<T, D, H>::F>& dk, Acc<EdgeC
     const float p1 = ok1 ? exp2f(s1 - l1) : 0.f;
     const float ds0 = p0 * (dp0 - D0);
     const float ds1 = p1 * (dp1 - D1);
-    if constexpr (kBias) {
+    if (kBias && staged) {
+        staged[2] = ok0 ? ds0 : 0.f;
+        staged[3] = ok1 ? ds1 : 0.f;
+    } else if constexpr (kBias) {
         if (ln.part == 0) {
             if (ok0) eb.db[e0 * H + ln.h] = ds0;
             if (ok1) eb.db[e1 * H + ln.h] = ds1;
@@ -470,9 +670,26 @@ __global__ __launch_bounds__(kThreads) void k_bwd_cols(int64_t n, const int64_t*
         load_f32_slice<C::F>(dk.v, tpk.acc + off);
         load_f32_slice<C::F>(dv.v, tpv.acc + off);
     }
-    walk_edges(rw, len, a, deg, dmax, int32_t(self), [&](int64_t i0, int64_t i1, int t, bool ok0, bool ok1) {
-        dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, stat, i0, i1, ok0, ok1, ln, sl2, eb, a + t, a + t + 1);
-    });
+    using BS = BiasStage<T, D, H>;
+    if constexpr (kBias && BS::kOn) {
+        __shared__ float s_bias[kThreads / kWave][BS::kWaveFloats];
+        float* sb = s_bias[threadIdx.x / kWave] + ln.slot * 4 * H;
+        float4 ds = make_float4(0.f, 0.f, 0.f, 0.f);
+        walk_edges_bias<T, D, H, true>(
+            rw, len, a, deg, dmax, int32_t(self), eb.b, ln, sb,
+            [&](int t) { return col_quad(eb, len, a, deg, t); },
+            [&](int64_t i0, int64_t i1, int t, bool ok0, bool ok1, float b0, float b1) {
+                float x[4] = {b0, b1, 0.f, 0.f};
+                dkv_step<T, D, H, true>(dk, dv, k, v, Q, dO, stat, i0, i1, ok0, ok1, ln, sl2, eb, 0, 0, x);
+                if (t & 2) ds.z = x[2], ds.w = x[3];
+                else ds.x = x[2], ds.y = x[3], ds.z = 0.f, ds.w = 0.f;
+            },
+            [&](int t, const Quad& q) { db_quad<T, D, H>(eb.db, q, t, deg, ds, ln, sb); });
+    } else {
+        walk_edges(rw, len, a, deg, dmax, int32_t(self), [&](int64_t i0, int64_t i1, int t, bool ok0, bool ok1) {
+            dkv_step<T, D, H, kBias>(dk, dv, k, v, Q, dO, stat, i0, i1, ok0, ok1, ln, sl2, eb, a + t, a + t + 1);
+        });
+    }
     if (live && deg >= 0) {
         store_slice<T, C::F>(dK + off, dk.v, scale);
         store_slice<T, C::F>(dV + off, dv.v, 1.f);
