@@ -51,13 +51,14 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--scale", type=float, default=1.0, help="shrink the workload's node count (testing only)")
-    ap.add_argument("--tau", type=float, default=0.05, help="tile density threshold")
+    ap.add_argument("--tau", type=float, default=None,
+                    help="tile density threshold (default: the library's measured break-even, 12%%)")
     ap.add_argument("--tile", type=int, default=128)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense-layer", action="store_true", help="skip the full-attention layer measurement")
     ap.add_argument("--tau-sweep", type=float, nargs="*", default=None,
-                    help="also time the step at other density thresholds (default 1%%, 5%%, 10%%, 20%%, 30%%, 50%% "
+                    help="also time the step at other density thresholds (default 1%%, 5%%, 10%%, 12%%, 20%%, 30%%, 50%% "
                          "and above 1, the CSR-only control); off by default so that a kernel trace of the default "
                          "command holds the headline launches only")
     ap.add_argument("--bias", action="store_true",
@@ -273,7 +274,7 @@ def measured_peaks():
     }
 
 
-SWEEP_TAUS = (0.01, 0.05, 0.10, 0.20, 0.30, 0.50, 1.01)
+SWEEP_TAUS = (0.01, 0.05, 0.10, 0.12, 0.20, 0.30, 0.50, 1.01)
 
 
 def tau_sweep(gt, rp, cl, Q, K, V, dO, scale, taus, edge_heads, T):
@@ -463,6 +464,8 @@ def main():
 
     perm, iperm, _ = timed("reorder_ms", lambda: gt.reorder(rp, cl))
     rp2, cl2 = timed("permute_ms", lambda: gt.permute_csr(rp, cl, perm, iperm))
+    if args.tau is None:
+        args.tau = gt.BREAK_EVEN_TAU_PPM / 1e6
     tau_ppm = gt.tau_to_ppm(args.tau)
     plan = timed("tile_build_ms", lambda: gt.build_tiles(rp2, cl2, args.tile, tau_ppm))
     Q, K, V, dO = timed("gather_ms", lambda: tuple(gt.gather_rows(x, perm) if x is not None else None

@@ -342,9 +342,18 @@ def tau_to_ppm(tau: float) -> int:
     return int(round(float(tau) * 1e6))
 
 
-def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: int = 10000, *,
+# Default density threshold: the break-even density measured on MI355X for bf16
+# features (a 128 x 128 tile, forward and backward, costs about what 6.6% (d=32)
+# to 12% (d=64, partial sums merged by the edge kernels included) of its pairs
+# cost as edges), so a tile the plan makes dense is not slower than its edges.
+# The paper's lower thresholds remain available through tau_ppm.
+BREAK_EVEN_TAU_PPM = 120_000
+
+
+def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: int = BREAK_EVEN_TAU_PPM, *,
                 build_ws: torch.Tensor | None = None, between=None, edge_positions: bool = False) -> Plan:
-    """Tile plan of the CSR at tile edge T and density threshold tau_ppm (parts per million).
+    """Tile plan of the CSR at tile edge T and density threshold tau_ppm (parts per million; by default
+    the measured break-even density, BREAK_EVEN_TAU_PPM).
 
     gt_tiles_count and gt_build_tiles share one workspace, so the build takes the counts from it.  build_ws
     gives the build call a workspace of its own instead, and between(ws) runs between the two calls; with
