@@ -45,6 +45,12 @@ struct RS {
 };
 
 __device__ __forceinline__ int crow(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
+
+// A compile-time flag passed as a value (generic lambdas take it as auto).
+template <bool B>
+struct Flag {
+    static constexpr bool value = B;
+};
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ f32x16_t zero16() {
@@ -147,6 +153,25 @@ struct Stager {
                 r[k][j] = *reinterpret_cast<const uint2*>(X + (src * H + h) * D + 4 * fg);
             }
         }
+    }
+    // A stage whose 64 rows are all below n: one uniform base address, per-lane
+    // 32-bit offsets that do not change from stage to stage, no clamping.
+    __device__ __forceinline__ void load_in(const uint16_t* __restrict__ X, int64_t base, int H, int h) {
+        const uint16_t* xb = X + (base * H + h) * D;
+        const int rs = H * D;
+        valid = ~0u;
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int it = item(k), rg = it / FG, fg = it % FG;
+            const uint16_t* p = xb + 4 * rg * rs + 4 * fg;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) r[k][j] = *reinterpret_cast<const uint2*>(p + j * rs);
+        }
+    }
+    // Either form, by where the stage ends.
+    __device__ __forceinline__ void load_any(const uint16_t* __restrict__ X, int64_t base, int64_t n, int H, int h) {
+        if (base + kStage <= n) load_in(X, base, H, h);
+        else load(X, base, n, H, h);
     }
     __device__ __forceinline__ uint2 row(int k, int j) const {
         return (valid >> (4 * k + j)) & 1u ? r[k][j] : make_uint2(0, 0);
@@ -255,8 +280,8 @@ __global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_
         const int buf = int(t & 1);
         const int64_t kbase = t * kStage;
         if (t + 1 < stages) {
-            gk.load(K, kbase + kStage, n, H, h);
-            gv.load(V, kbase + kStage, n, H, h);
+            gk.load_any(K, kbase + kStage, n, H, h);
+            gv.load_any(V, kbase + kStage, n, H, h);
         }
         const uint16_t* k_s = sK[buf];
         const uint16_t* v_s = sVt[buf];
@@ -272,7 +297,10 @@ __global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_
                 for (int b = 0; b < NB; ++b) s[b] = mma(a, qf[b].v[c], s[b]);
             }
             const int64_t key0 = kbase + 32 * kb;
-            if (key0 + 32 > n) {  // ragged last block: partners >= n take no weight
+            if (__builtin_expect(key0 + 32 > n, 0)) {  // ragged last block: partners >= n take no weight
+                // kept as a branch (the empty asm stops the compiler from turning
+                // it into selects on every block)
+                asm volatile("" ::: "memory");
 #pragma unroll
                 for (int i = 0; i < 16; ++i)
                     if (key0 + crow(i, lane) >= n)
@@ -403,8 +431,8 @@ __global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_
         const int buf = int(t & 1);
         const int64_t kbase = t * kStage;
         if (t + 1 < stages) {
-            gk.load(K, kbase + kStage, n, H, h);
-            gv.load(V, kbase + kStage, n, H, h);
+            gk.load_any(K, kbase + kStage, n, H, h);
+            gv.load_any(V, kbase + kStage, n, H, h);
         }
 #pragma unroll
         for (int kb = 0; kb < kStage / 32; ++kb) {
@@ -534,8 +562,8 @@ __global__ __launch_bounds__(kRowsWg / (32 * NB) * kWave) __attribute__((amdgpu_
         const int buf = int(t & 1);
         const int64_t qbase = t * kStage;
         if (t + 1 < stages) {
-            gq.load(Q, qbase + kStage, n, H, h);
-            gg.load(dO, qbase + kStage, n, H, h);
+            gq.load_any(Q, qbase + kStage, n, H, h);
+            gg.load_any(dO, qbase + kStage, n, H, h);
         }
 #pragma unroll
         for (int qb = 0; qb < kStage / 32; ++qb) {
