@@ -2,7 +2,9 @@
 // hashed partial activation, then a stable sort by (label, -degree, id).
 //
 // Rows are handled by size:
-//   deg <= 16 / 32     four / two rows per wavefront, 16 / 32 lanes each;
+//   deg <= 4 / 8 / 16 / 32
+//                      16 / 8 / 4 / 2 rows per wavefront, 4 / 8 / 16 / 32
+//                      lanes each;
 //   32 < deg <= 64     one wavefront per row; one neighbour label per lane,
 //                      multiplicities by an all-pairs compare (readlane).
 //   64 < deg <= 512    one wavefront per row, open-addressing count table in
@@ -25,14 +27,17 @@ namespace {
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kActivitySalt = 0xD6E8FEB86659FD93ull;
 constexpr int kWaveRowMax = 64;
-constexpr int kSub16 = 16, kSub32 = 32;  // rows of up to 16 / 32 edges share a wavefront
+constexpr int kSub4 = 4, kSub8 = 8, kSub16 = 16, kSub32 = 32;  // rows of up to 4 ... 32 edges share a wavefront
 constexpr int kWaveTabRowMax = 512;
 constexpr int kWaveTab = 2 * kWaveTabRowMax;  // per-wavefront table entries
 constexpr int kLdsTable = 8192;      // entries (int32 key + uint32 count): 64 KiB
 constexpr int kLdsRowMax = kLdsTable / 2;
 constexpr int kBlock = 256;
+constexpr int kMedBlock = 1024;  // threads per row of kWaveTabRowMax + 1 to kLdsRowMax edges
 constexpr int kMaxSweeps = 1000;
-constexpr int kBigGrid = 1024;  // workgroups sharing each very long row
+constexpr int kBigGrid = 2048;  // workgroups sharing the very long rows
+constexpr int kBigEdgeChunk = 1024;  // edges of a very long row counted in one workgroup's LDS table
+constexpr int kBigChunkTab = 2 * kBigEdgeChunk;
 
 __device__ __forceinline__ bool is_active(int64_t v, uint64_t key) {
     return (mix64(uint64_t(v) ^ key ^ kActivitySalt) >> 61) != 0;
@@ -63,8 +68,8 @@ __device__ __forceinline__ int wave_min_i32(int v) {
 // -------------------------------------------------------------- per-row classes
 
 __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
-                           int32_t* is_s16, int32_t* is_s32, int32_t* is_wav, int32_t* is_wmed, int32_t* is_med,
-                           int32_t* is_huge, int64_t* big_cap) {
+                           int32_t* is_s4, int32_t* is_s8, int32_t* is_s16, int32_t* is_s32, int32_t* is_wav,
+                           int32_t* is_wmed, int32_t* is_med, int32_t* is_huge, int64_t* big_cap) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         // self-loop present?  rows are sorted: binary search for v.
@@ -77,7 +82,9 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
         const bool self = lo < b && col[lo] == v;
         const int64_t deg = b - a;
         deg_off[v] = uint32_t(deg - (self ? 1 : 0));
-        is_s16[v] = deg <= kSub16 ? 1 : 0;
+        is_s4[v] = deg <= kSub4 ? 1 : 0;
+        is_s8[v] = (deg > kSub4 && deg <= kSub8) ? 1 : 0;
+        is_s16[v] = (deg > kSub8 && deg <= kSub16) ? 1 : 0;
         is_s32[v] = (deg > kSub16 && deg <= kSub32) ? 1 : 0;
         is_wav[v] = (deg > kSub32 && deg <= kWaveRowMax) ? 1 : 0;
         is_wmed[v] = (deg > kWaveRowMax && deg <= kWaveTabRowMax) ? 1 : 0;
@@ -90,13 +97,17 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
     }
 }
 
-__global__ void k_compact(int64_t n, const int32_t* is_s16, const int32_t* is_s32, const int32_t* is_wav,
-                          const int32_t* is_wmed, const int32_t* is_med, const int32_t* is_huge,
+__global__ void k_compact(int64_t n, const int32_t* is_s4, const int32_t* is_s8, const int32_t* is_s16,
+                          const int32_t* is_s32, const int32_t* is_wav, const int32_t* is_wmed, const int32_t* is_med,
+                          const int32_t* is_huge, const int64_t* pos_s4, const int64_t* pos_s8,
                           const int64_t* pos_s16, const int64_t* pos_s32, const int64_t* pos_wav,
                           const int64_t* pos_wmed, const int64_t* pos_med, const int64_t* pos_huge,
-                          const int64_t* cap_off, int32_t* s16_list, int32_t* s32_list, int32_t* wav_list,
-                          int32_t* wmed_list, int32_t* med_list, int32_t* huge_list, int64_t* huge_off) {
+                          const int64_t* cap_off, int32_t* s4_list, int32_t* s8_list, int32_t* s16_list,
+                          int32_t* s32_list, int32_t* wav_list, int32_t* wmed_list, int32_t* med_list,
+                          int32_t* huge_list, int64_t* huge_off) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
+        if (is_s4[v]) s4_list[pos_s4[v]] = int32_t(v);
+        if (is_s8[v]) s8_list[pos_s8[v]] = int32_t(v);
         if (is_s16[v]) s16_list[pos_s16[v]] = int32_t(v);
         if (is_s32[v]) s32_list[pos_s32[v]] = int32_t(v);
         if (is_wav[v]) wav_list[pos_wav[v]] = int32_t(v);
@@ -110,19 +121,19 @@ __global__ void k_compact(int64_t n, const int32_t* is_s16, const int32_t* is_s3
 }
 
 // ------------------------------------------------------------------ wave rows
+// Rows of up to kWaveRowMax edges, in five lists by size, all in one launch:
+// the grid's blocks are cut into five consecutive ranges, one per list.  Each
+// range runs its list with a grid-stride loop over its own blocks.
 
 // Rows of kSub32 + 1 to kWaveRowMax edges, one wavefront each: every lane
 // counts how many of the row's labels equal its own, reading the others with
 // readlane (the lane index is uniform over the wavefront).
-__global__ __launch_bounds__(kBlock) void k_lp_wave(const int32_t* list, const int64_t* list_len,
-                                                    const int64_t* rowptr, const int32_t* col,
-                                                    const int32_t* lab_in, int32_t* lab_out, uint64_t key,
-                                                    const uint32_t* flag_prev, uint32_t* flag_next) {
-    const bool converged = *flag_prev == 0;
+__device__ __forceinline__ void lp_wave_rows(const int32_t* list, int64_t len, unsigned blk, unsigned nblk,
+                                             const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
+                                             int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
     const int lane = lane_id();
-    const int64_t len = *list_len;
-    const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
-    for (int64_t idx = int64_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave; idx < len; idx += waves) {
+    const int64_t waves = int64_t(nblk) * (kBlock / kWave);
+    for (int64_t idx = int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave; idx < len; idx += waves) {
         const int64_t v = list[idx];
         const int own = lab_in[v];
         if (converged) {
@@ -155,8 +166,8 @@ __global__ __launch_bounds__(kBlock) void k_lp_wave(const int32_t* list, const i
     }
 }
 
-// Rows of at most S edges (S = 16 or 32), 64 / S rows per wavefront: the same
-// function as k_lp_wave with every reduction confined to the row's S lanes.
+// Rows of at most S edges (S = 4, 8, 16 or 32), 64 / S rows per wavefront: the
+// same function as lp_wave_rows with every reduction confined to the row's S lanes.
 template <int S>
 __device__ __forceinline__ int group_max_i32(int v) {
 #pragma unroll
@@ -186,18 +197,14 @@ __device__ __forceinline__ uint64_t group_min_u64(uint64_t v) {
 }
 
 template <int S>
-__global__ __launch_bounds__(kBlock) void k_lp_sub(const int32_t* list, const int64_t* list_len,
-                                                   const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
-                                                   int32_t* lab_out, uint64_t key, const uint32_t* flag_prev,
-                                                   uint32_t* flag_next) {
+__device__ __forceinline__ void lp_sub_rows(const int32_t* list, int64_t len, unsigned blk, unsigned nblk,
+                                            const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
+                                            int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
     constexpr int G = kWave / S;
-    const bool converged = *flag_prev == 0;
     const int lane = lane_id(), sub = lane / S, sl = lane % S;
     const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
-    const int64_t len = *list_len;
-    const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
-    for (int64_t base = (int64_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave) * G; base < len;
-         base += waves * G) {
+    const int64_t waves = int64_t(nblk) * (kBlock / kWave);
+    for (int64_t base = (int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave) * G; base < len; base += waves * G) {
         const int64_t idx = base + sub;
         const bool live = idx < len;
         const int64_t v = live ? list[idx] : 0;
@@ -218,12 +225,18 @@ __global__ __launch_bounds__(kBlock) void k_lp_sub(const int32_t* list, const in
         const int dmax = wave_max(deg);
         int cnt = 0;
         for (int k = 0; k < dmax; ++k) {
-            // lane sub * S + k of each group, by readlane (k is uniform over the wavefront)
-            int Lk = __builtin_amdgcn_readlane(L, k);
+            // lane sub * S + k of each group: by readlane (k is uniform over the
+            // wavefront) for few groups, by one lane permute for many
+            int Lk;
+            if constexpr (G <= 4) {
+                Lk = __builtin_amdgcn_readlane(L, k);
 #pragma unroll
-            for (int g = 1; g < G; ++g) {
-                const int x = __builtin_amdgcn_readlane(L, g * S + k);
-                Lk = sub == g ? x : Lk;
+                for (int g = 1; g < G; ++g) {
+                    const int x = __builtin_amdgcn_readlane(L, g * S + k);
+                    Lk = sub == g ? x : Lk;
+                }
+            } else {
+                Lk = __shfl(L, k, S);
             }
             cnt += (Lk == L) ? 1 : 0;
         }
@@ -243,6 +256,43 @@ __global__ __launch_bounds__(kBlock) void k_lp_sub(const int32_t* list, const in
             lab_out[v] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
         }
+    }
+}
+
+// The five short-row lists (rows of 33-64, 17-32, 9-16, 5-8 and 0-4 edges, in
+// that order) and the first block of each one's range; first[5] is the grid.
+enum { kSmWave, kSm32, kSm16, kSm8, kSm4, kSmLists };
+struct SmallRows {
+    const int32_t* list[kSmLists];
+    const int64_t* len[kSmLists];
+    unsigned first[kSmLists + 1];
+};
+
+__global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t* rowptr, const int32_t* col,
+                                                     const int32_t* lab_in, int32_t* lab_out, uint64_t key,
+                                                     const uint32_t* flag_prev, uint32_t* flag_next) {
+    const bool converged = *flag_prev == 0;
+    const unsigned b = blockIdx.x;
+    int k = 0;
+    while (k + 1 < kSmLists && b >= sr.first[k + 1]) ++k;
+    const unsigned blk = b - sr.first[k], nblk = sr.first[k + 1] - sr.first[k];
+    const int64_t len = *sr.len[k];
+    switch (k) {
+        case kSmWave:
+            lp_wave_rows(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            break;
+        case kSm32:
+            lp_sub_rows<kSub32>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            break;
+        case kSm16:
+            lp_sub_rows<kSub16>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            break;
+        case kSm8:
+            lp_sub_rows<kSub8>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            break;
+        default:
+            lp_sub_rows<kSub4>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            break;
     }
 }
 
@@ -303,6 +353,26 @@ __device__ __forceinline__ void tab_add_wave(int* tk, int* tc, int64_t cap, bool
     if (pending) tab_add(tk, tc, cap, L, 1);
 }
 
+// Inserts the labels of the edges [first + 64 k stride ... ) of one row, k <
+// R, each wavefront's 64-edge slices: every column and label load is issued
+// before the first insertion, so a row costs one round trip to memory, not one
+// per slice.  first and stride are uniform over the wavefront.
+template <int R>
+__device__ __forceinline__ void tab_add_row(int* tk, int* tc, int64_t cap, int64_t first, int64_t stride, int64_t b,
+                                            int64_t v, const int32_t* col, const int32_t* lab_in) {
+    int c[R], L[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const int64_t e = first + k * stride + lane_id();
+        c[k] = e < b ? col[e] : int(v);
+    }
+#pragma unroll
+    for (int k = 0; k < R; ++k) L[k] = c[k] != v ? lab_in[c[k]] : -1;
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+        if (first + k * stride < b) tab_add_wave(tk, tc, cap, c[k] != v, L[k]);
+}
+
 // One workgroup per listed row (rows up to kLdsRowMax).  Table: keys (label or
 // -1) and counts in LDS.
 template <int BS>
@@ -335,12 +405,8 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
         }
         __syncthreads();
         // wave-uniform rounds: each wavefront takes 64 consecutive edges per round
-        for (int64_t base = a + (threadIdx.x & ~(kWave - 1)); base < b; base += BS) {
-            const int64_t e = base + lane_id();
-            const int c = e < b ? col[e] : int(v);
-            const bool valid = c != v;
-            tab_add_wave(tk, tc, cap, valid, valid ? lab_in[c] : -1);
-        }
+        tab_add_row<(kLdsRowMax + BS - 1) / BS>(tk, tc, cap, a + (threadIdx.x & ~(kWave - 1)), BS, b, v, col,
+                                                lab_in);
         __syncthreads();
         int best = 0, own_cnt = 0;
         for (int64_t s = threadIdx.x; s < cap; s += BS) {
@@ -415,12 +481,7 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
             tc[s2] = 0;
         }
         wave_lds_sync();
-        for (int64_t base = a; base < b; base += kWave) {
-            const int64_t e = base + lane;
-            const int c = e < b ? col[e] : int(v);
-            const bool valid = c != v;
-            tab_add_wave(tk, tc, cap, valid, valid ? lab_in[c] : -1);
-        }
+        tab_add_row<kWaveTabRowMax / kWave>(tk, tc, cap, a, kWave, b, v, col, lab_in);
         wave_lds_sync();
         int best = 0, own_cnt = 0;
         for (int s2 = lane; s2 < cap; s2 += kWave) {
@@ -472,7 +533,7 @@ struct BigRows {
     const int32_t* list;
     const int64_t* len;
     const int64_t* off;   // table offset of each listed row
-    const int64_t* echunk;  // [listed rows + 1]: first edge chunk of each row (kLdsRowMax edges per chunk)
+    const int64_t* echunk;  // [listed rows + 1]: first edge chunk of each row (kBigEdgeChunk edges per chunk)
     const int64_t* schunk;  // [listed rows + 1]: first table-slot chunk of each row (kSlotChunk slots per chunk)
     int* keys;
     int* cnts;
@@ -492,7 +553,7 @@ __device__ __forceinline__ int64_t table_cap(int64_t deg) {
 // rows are numbered one after the other (the offsets are computed once per
 // call) and dealt over the grid, so every row gets as many workgroups as its
 // table needs and a workgroup finds its row by a binary search.
-constexpr int64_t kSlotChunk = 8192;
+constexpr int64_t kSlotChunk = 2048;
 
 // The listed row holding global chunk c (the last idx with off[idx] <= c).
 __device__ __forceinline__ int64_t chunk_row(const int64_t* __restrict__ off, int64_t len, int64_t c) {
@@ -513,7 +574,7 @@ __global__ void k_big_chunks(const int32_t* __restrict__ list, const int64_t* __
          idx += int64_t(gridDim.x) * blockDim.x) {
         const int64_t v = list[idx];
         const int64_t deg = rowptr[v + 1] - rowptr[v];
-        ecnt[idx] = int32_t(cdiv(deg, kLdsRowMax));
+        ecnt[idx] = int32_t(cdiv(deg, kBigEdgeChunk));
         scnt[idx] = int32_t(cdiv(table_cap(deg), kSlotChunk));
     }
 }
@@ -544,14 +605,14 @@ __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t*
     }
 }
 
-// Chunks of kLdsRowMax edges of every listed row, dealt over the grid: each
+// Chunks of kBigEdgeChunk edges of every listed row, dealt over the grid: each
 // chunk is counted in an LDS table first, then its distinct labels are added
 // to the row's table in the workspace (far fewer global atomics where
 // neighbour labels repeat, as they do once clusters form).
 __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t* rowptr, const int32_t* col,
                                                        const int32_t* lab_in, const uint32_t* flag_prev) {
-    __shared__ int s_keys[kLdsTable];
-    __shared__ int s_cnts[kLdsTable];
+    __shared__ int s_keys[kBigChunkTab];
+    __shared__ int s_cnts[kBigChunkTab];
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
     const int64_t total = br.echunk[len];
@@ -563,21 +624,21 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
         const int64_t j = c - br.echunk[idx];
         int* tk = br.keys + br.off[idx];
         int* tc = br.cnts + br.off[idx];
-        for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
+        for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) {
             s_keys[x] = -1;
             s_cnts[x] = 0;
         }
         __syncthreads();
-        const int64_t e0 = a + j * kLdsRowMax;
-        const int64_t e1 = e0 + kLdsRowMax < b ? e0 + kLdsRowMax : b;
+        const int64_t e0 = a + j * kBigEdgeChunk;
+        const int64_t e1 = e0 + kBigEdgeChunk < b ? e0 + kBigEdgeChunk : b;
         for (int64_t base = e0 + (threadIdx.x & ~(kWave - 1)); base < e1; base += kBlock) {
             const int64_t e = base + lane_id();
             const int cc = e < e1 ? col[e] : int(v);
             const bool valid = cc != v;
-            tab_add_wave(s_keys, s_cnts, kLdsTable, valid, valid ? lab_in[cc] : -1);
+            tab_add_wave(s_keys, s_cnts, kBigChunkTab, valid, valid ? lab_in[cc] : -1);
         }
         __syncthreads();
-        for (int x = threadIdx.x; x < kLdsTable; x += kBlock) {
+        for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) {
             const int L = s_keys[x];
             if (L < 0) continue;
             int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
@@ -688,6 +749,8 @@ struct ReorderWs {
     uint32_t* flags;
     int32_t* lab[2];
     uint32_t* deg_off;
+    int32_t* is_s4;
+    int32_t* is_s8;
     int32_t* is_s16;
     int32_t* is_s32;
     int32_t* is_wav;
@@ -695,6 +758,8 @@ struct ReorderWs {
     int32_t* is_med;
     int32_t* is_huge;
     int64_t* big_cap;
+    int64_t* pos_s4;
+    int64_t* pos_s8;
     int64_t* pos_s16;
     int64_t* pos_s32;
     int64_t* pos_wav;
@@ -702,6 +767,8 @@ struct ReorderWs {
     int64_t* pos_med;
     int64_t* pos_huge;
     int64_t* cap_off;
+    int32_t* s4_list;
+    int32_t* s8_list;
     int32_t* s16_list;
     int32_t* s32_list;
     int32_t* wav_list;
@@ -728,10 +795,13 @@ struct ReorderWs {
 
 // The row counts of the list classes (the totals of their scans), gathered
 // so that one copy brings them to the host.
-enum { kClsS16, kClsS32, kClsWav, kClsWmed, kClsMed, kClsHuge, kClasses };
-__global__ void k_class_counts(int64_t n, const int64_t* s16, const int64_t* s32, const int64_t* wav,
-                               const int64_t* wmed, const int64_t* med, const int64_t* huge, int64_t* out) {
+enum { kClsS4, kClsS8, kClsS16, kClsS32, kClsWav, kClsWmed, kClsMed, kClsHuge, kClasses };
+__global__ void k_class_counts(int64_t n, const int64_t* s4, const int64_t* s8, const int64_t* s16,
+                               const int64_t* s32, const int64_t* wav, const int64_t* wmed, const int64_t* med,
+                               const int64_t* huge, int64_t* out) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    out[kClsS4] = s4[n];
+    out[kClsS8] = s8[n];
     out[kClsS16] = s16[n];
     out[kClsS32] = s32[n];
     out[kClsWav] = wav[n];
@@ -753,6 +823,8 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.lab[0] = ws.take<int32_t>(n1);
     r.lab[1] = ws.take<int32_t>(n1);
     r.deg_off = ws.take<uint32_t>(n1);
+    r.is_s4 = ws.take<int32_t>(n1);
+    r.is_s8 = ws.take<int32_t>(n1);
     r.is_s16 = ws.take<int32_t>(n1);
     r.is_s32 = ws.take<int32_t>(n1);
     r.is_wav = ws.take<int32_t>(n1);
@@ -760,6 +832,8 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.is_med = ws.take<int32_t>(n1);
     r.is_huge = ws.take<int32_t>(n1);
     r.big_cap = ws.take<int64_t>(n1);
+    r.pos_s4 = ws.take<int64_t>(n1 + 1);
+    r.pos_s8 = ws.take<int64_t>(n1 + 1);
     r.pos_s16 = ws.take<int64_t>(n1 + 1);
     r.pos_s32 = ws.take<int64_t>(n1 + 1);
     r.pos_wav = ws.take<int64_t>(n1 + 1);
@@ -767,6 +841,8 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.pos_med = ws.take<int64_t>(n1 + 1);
     r.pos_huge = ws.take<int64_t>(n1 + 1);
     r.cap_off = ws.take<int64_t>(n1 + 1);
+    r.s4_list = ws.take<int32_t>(n1);
+    r.s8_list = ws.take<int32_t>(n1);
     r.s16_list = ws.take<int32_t>(n1);
     r.s32_list = ws.take<int32_t>(n1);
     r.wav_list = ws.take<int32_t>(n1);
@@ -827,9 +903,11 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if (st != GT_OK) return st;
 
     const unsigned g = grid_for(n, 256, 8192);
-    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med,
-                                      r.is_huge, r.big_cap);
+    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_s4, r.is_s8, r.is_s16, r.is_s32, r.is_wav,
+                                      r.is_wmed, r.is_med, r.is_huge, r.big_cap);
     GT_LAUNCH_CHECK("reorder_classify");
+    if ((st = exclusive_scan_i32(r.is_s4, n, r.pos_s4, r.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(r.is_s8, n, r.pos_s8, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_s16, n, r.pos_s16, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_s32, n, r.pos_s32, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_wav, n, r.pos_wav, r.scan, stream)) != GT_OK) return st;
@@ -837,9 +915,10 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(r.is_huge, n, r.pos_huge, r.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
-    k_compact<<<g, 256, 0, stream>>>(n, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med, r.is_huge, r.pos_s16,
-                                     r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_huge, r.cap_off, r.s16_list,
-                                     r.s32_list, r.wav_list, r.wmed_list, r.med_list, r.huge_list, r.huge_off);
+    k_compact<<<g, 256, 0, stream>>>(n, r.is_s4, r.is_s8, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med,
+                                     r.is_huge, r.pos_s4, r.pos_s8, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed,
+                                     r.pos_med, r.pos_huge, r.cap_off, r.s4_list, r.s8_list, r.s16_list, r.s32_list,
+                                     r.wav_list, r.wmed_list, r.med_list, r.huge_list, r.huge_off);
     GT_LAUNCH_CHECK("reorder_compact");
 
     if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
@@ -847,8 +926,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
     // the class sizes on the host: empty classes are not launched and grids fit the lists
-    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed, r.pos_med, r.pos_huge,
-                                         r.class_cnt);
+    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s4, r.pos_s8, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed,
+                                         r.pos_med, r.pos_huge, r.class_cnt);
     GT_LAUNCH_CHECK("reorder_class_counts");
     int64_t cnt[kClasses] = {};
     GT_HIP(hipMemcpyAsync(cnt, r.class_cnt, sizeof(cnt), hipMemcpyDeviceToHost, stream));
@@ -863,9 +942,23 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         if ((st = exclusive_scan_i32(r.huge_ecnt, n_huge, r.huge_echunk, r.scan, stream)) != GT_OK) return st;
         if ((st = exclusive_scan_i32(r.huge_scnt, n_huge, r.huge_schunk, r.scan, stream)) != GT_OK) return st;
     }
-    const unsigned gw = grid_cap(cnt[kClsWav], kBlock / kWave, 65536);
-    const unsigned g16 = grid_cap(cnt[kClsS16], kBlock / kSub16, 16384);
-    const unsigned g32 = grid_cap(cnt[kClsS32], kBlock / kSub32, 16384);
+    // the short-row lists in one launch, blocks in proportion to their rows
+    SmallRows sr;
+    {
+        const int64_t* lens[kSmLists] = {r.pos_wav + n, r.pos_s32 + n, r.pos_s16 + n, r.pos_s8 + n, r.pos_s4 + n};
+        const int32_t* lists[kSmLists] = {r.wav_list, r.s32_list, r.s16_list, r.s8_list, r.s4_list};
+        const int64_t rows[kSmLists] = {cnt[kClsWav], cnt[kClsS32], cnt[kClsS16], cnt[kClsS8], cnt[kClsS4]};
+        const int per_block[kSmLists] = {kBlock / kWave, kBlock / kSub32, kBlock / kSub16, kBlock / kSub8,
+                                         kBlock / kSub4};
+        unsigned at = 0;
+        for (int k = 0; k < kSmLists; ++k) {
+            sr.list[k] = lists[k];
+            sr.len[k] = lens[k];
+            sr.first[k] = at;
+            if (rows[k] > 0) at += grid_cap(rows[k], per_block[k], 16384);
+        }
+        sr.first[kSmLists] = at;
+    }
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
     const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
     for (int t = 0; t < iters; ++t) {
@@ -885,20 +978,10 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, in, out, key, fp, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_big_decide");
         }
-        if (cnt[kClsWav] > 0) {
-            k_lp_wave<<<gw, kBlock, 0, stream>>>(r.wav_list, r.pos_wav + n, rowptr, col, in, out, key, r.flags + t,
-                                                 r.flags + t + 1);
-            GT_LAUNCH_CHECK("reorder_lp_wave");
-        }
-        if (cnt[kClsS16] > 0) {
-            k_lp_sub<kSub16><<<g16, kBlock, 0, stream>>>(r.s16_list, r.pos_s16 + n, rowptr, col, in, out, key,
-                                                         r.flags + t, r.flags + t + 1);
-            GT_LAUNCH_CHECK("reorder_lp_sub16");
-        }
-        if (cnt[kClsS32] > 0) {
-            k_lp_sub<kSub32><<<g32, kBlock, 0, stream>>>(r.s32_list, r.pos_s32 + n, rowptr, col, in, out, key,
-                                                         r.flags + t, r.flags + t + 1);
-            GT_LAUNCH_CHECK("reorder_lp_sub32");
+        if (sr.first[kSmLists] > 0) {
+            k_lp_small<<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, in, out, key, r.flags + t,
+                                                                  r.flags + t + 1);
+            GT_LAUNCH_CHECK("reorder_lp_small");
         }
         if (cnt[kClsWmed] > 0) {
             k_lp_wavetab<<<gwt, kBlock, 0, stream>>>(r.wmed_list, r.pos_wmed + n, rowptr, col, in, out, key,
@@ -906,7 +989,7 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             GT_LAUNCH_CHECK("reorder_lp_wavetab");
         }
         if (cnt[kClsMed] > 0) {
-            k_lp_block<kBlock><<<gmed, kBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
+            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
                                                             r.flags + t, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_lds");
         }
