@@ -106,5 +106,7 @@ gt_status launch_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, con
                               hipStream_t s);
 // Reads the flags back (SYNC) and maps them to a status.
 gt_status read_validation(const uint32_t* flags, hipStream_t s);
+// The status of a validation flag word already on the host.
+gt_status validation_result(uint32_t flags);
 
 }  // namespace gt

@@ -394,6 +394,10 @@ gt_status read_validation(const uint32_t* flags, hipStream_t s) {
     uint32_t f = 0;
     GT_HIP(hipMemcpyAsync(&f, flags, sizeof(f), hipMemcpyDeviceToHost, s));
     GT_HIP(hipStreamSynchronize(s));
+    return validation_result(f);
+}
+
+gt_status validation_result(uint32_t f) {
     if (f & kOutOfRange) return fail(GT_ERR_OUT_OF_RANGE, "CSR: rowptr or column index out of range");
     if (f & kDuplicate) return fail(GT_ERR_DUPLICATE, "CSR: repeated column inside a row");
     if (f & kUnsorted) return fail(GT_ERR_UNSORTED, "CSR: row not strictly increasing or rowptr decreasing");

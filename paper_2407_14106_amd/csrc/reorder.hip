@@ -66,12 +66,56 @@ __device__ __forceinline__ int wave_min_i32(int v) {
 }
 
 // -------------------------------------------------------------- per-row classes
+// Every row falls in one class by its entry count; the rows of all classes go
+// to one list, class after class, each class in ascending row order.  One
+// pass counts each 256-row block's rows per class, one scan over the
+// class-major [class][block] counts gives every (class, block) its place in
+// the list, and a second pass writes the rows there.
 
-__global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col, uint32_t* deg_off,
-                           int32_t* is_s4, int32_t* is_s8, int32_t* is_s16, int32_t* is_s32, int32_t* is_wav,
-                           int32_t* is_wmed, int32_t* is_med, int32_t* is_huge, int64_t* big_cap) {
-    for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
-        const int64_t a = rowptr[v], b = rowptr[v + 1];
+enum { kClsS4, kClsS8, kClsS16, kClsS32, kClsWav, kClsWmed, kClsMed, kClsHuge, kClasses };
+constexpr int kClsBlock = 256;
+
+__device__ __forceinline__ int row_class(int64_t deg) {
+    return deg <= kSub4           ? kClsS4
+           : deg <= kSub8         ? kClsS8
+           : deg <= kSub16        ? kClsS16
+           : deg <= kSub32        ? kClsS32
+           : deg <= kWaveRowMax   ? kClsWav
+           : deg <= kWaveTabRowMax ? kClsWmed
+           : deg <= kLdsRowMax    ? kClsMed
+                                  : kClsHuge;
+}
+
+// Per-wavefront counts of each class in s[w][c]; returns the lane's rank among
+// the wavefront's lanes of its own class (cls < 0: no row).
+__device__ __forceinline__ int class_ballots(int cls, int (*s)[kClasses]) {
+    const int w = threadIdx.x / kWave;
+    int rank = 0;
+#pragma unroll
+    for (int c = 0; c < kClasses; ++c) {
+        const uint64_t m = __ballot(cls == c);
+        if (lane_id() == 0) s[w][c] = __popcll(m);
+        if (cls == c) rank = __popcll(m & lanemask_lt());
+    }
+    return rank;
+}
+
+// Off-diagonal entry count of every row (for the final order; the block's
+// largest in blk_max[block]) and the block's rows per class, in
+// blk_cnt[c * nblk + block].  It runs before the CSR check is read back, so
+// every read stays in col[0, nnz) whatever rowptr holds.
+__global__ __launch_bounds__(kClsBlock) void k_classify(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                                        const int32_t* col, uint32_t* deg_off, int32_t* blk_cnt,
+                                                        int64_t nblk, uint32_t* blk_max) {
+    __shared__ int s_cnt[kClsBlock / kWave][kClasses];
+    __shared__ uint32_t s_max[kClsBlock / kWave];
+    uint32_t dv = 0;
+    const int64_t v = int64_t(blockIdx.x) * kClsBlock + threadIdx.x;
+    int cls = -1;
+    if (v < n) {
+        int64_t a = rowptr[v], b = rowptr[v + 1];
+        a = a < 0 ? 0 : (a > nnz ? nnz : a);
+        b = b < a ? a : (b > nnz ? nnz : b);
         // self-loop present?  rows are sorted: binary search for v.
         int64_t lo = a, hi = b;
         while (lo < hi) {
@@ -80,43 +124,65 @@ __global__ void k_classify(int64_t n, const int64_t* rowptr, const int32_t* col,
             else hi = m;
         }
         const bool self = lo < b && col[lo] == v;
-        const int64_t deg = b - a;
-        deg_off[v] = uint32_t(deg - (self ? 1 : 0));
-        is_s4[v] = deg <= kSub4 ? 1 : 0;
-        is_s8[v] = (deg > kSub4 && deg <= kSub8) ? 1 : 0;
-        is_s16[v] = (deg > kSub8 && deg <= kSub16) ? 1 : 0;
-        is_s32[v] = (deg > kSub16 && deg <= kSub32) ? 1 : 0;
-        is_wav[v] = (deg > kSub32 && deg <= kWaveRowMax) ? 1 : 0;
-        is_wmed[v] = (deg > kWaveRowMax && deg <= kWaveTabRowMax) ? 1 : 0;
-        is_med[v] = (deg > kWaveTabRowMax && deg <= kLdsRowMax) ? 1 : 0;
-        const bool big = deg > kLdsRowMax;
-        is_huge[v] = big ? 1 : 0;
-        int64_t cap = 1;
-        while (cap < 2 * deg) cap <<= 1;
-        big_cap[v] = big ? cap : 0;
+        dv = uint32_t(b - a - (self ? 1 : 0));
+        deg_off[v] = dv;
+        cls = row_class(b - a);
+    }
+    class_ballots(cls, s_cnt);
+    dv = wave_max(dv);
+    if (lane_id() == 0) s_max[threadIdx.x / kWave] = dv;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t m = 0;
+#pragma unroll
+        for (int w = 0; w < kClsBlock / kWave; ++w) m = s_max[w] > m ? s_max[w] : m;
+        blk_max[blockIdx.x] = m;
+    }
+    if (threadIdx.x < kClasses) {
+        int t = 0;
+#pragma unroll
+        for (int w = 0; w < kClsBlock / kWave; ++w) t += s_cnt[w][threadIdx.x];
+        blk_cnt[threadIdx.x * nblk + blockIdx.x] = t;
     }
 }
 
-__global__ void k_compact(int64_t n, const int32_t* is_s4, const int32_t* is_s8, const int32_t* is_s16,
-                          const int32_t* is_s32, const int32_t* is_wav, const int32_t* is_wmed, const int32_t* is_med,
-                          const int32_t* is_huge, const int64_t* pos_s4, const int64_t* pos_s8,
-                          const int64_t* pos_s16, const int64_t* pos_s32, const int64_t* pos_wav,
-                          const int64_t* pos_wmed, const int64_t* pos_med, const int64_t* pos_huge,
-                          const int64_t* cap_off, int32_t* s4_list, int32_t* s8_list, int32_t* s16_list,
-                          int32_t* s32_list, int32_t* wav_list, int32_t* wmed_list, int32_t* med_list,
-                          int32_t* huge_list, int64_t* huge_off) {
-    for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x) {
-        if (is_s4[v]) s4_list[pos_s4[v]] = int32_t(v);
-        if (is_s8[v]) s8_list[pos_s8[v]] = int32_t(v);
-        if (is_s16[v]) s16_list[pos_s16[v]] = int32_t(v);
-        if (is_s32[v]) s32_list[pos_s32[v]] = int32_t(v);
-        if (is_wav[v]) wav_list[pos_wav[v]] = int32_t(v);
-        if (is_wmed[v]) wmed_list[pos_wmed[v]] = int32_t(v);
-        if (is_med[v]) med_list[pos_med[v]] = int32_t(v);
-        if (is_huge[v]) {
-            huge_list[pos_huge[v]] = int32_t(v);
-            huge_off[pos_huge[v]] = cap_off[v];
-        }
+__global__ __launch_bounds__(kClsBlock) void k_class_scatter(int64_t n, const int64_t* rowptr,
+                                                             const int64_t* blk_off, int64_t nblk, int32_t* list) {
+    __shared__ int s_cnt[kClsBlock / kWave][kClasses];
+    const int64_t v = int64_t(blockIdx.x) * kClsBlock + threadIdx.x;
+    const int cls = v < n ? row_class(rowptr[v + 1] - rowptr[v]) : -1;
+    const int rank = class_ballots(cls, s_cnt);
+    __syncthreads();
+    if (cls >= 0) {
+        int64_t pos = blk_off[cls * nblk + blockIdx.x] + rank;
+        for (int w = 0; w < int(threadIdx.x / kWave); ++w) pos += s_cnt[w][cls];
+        list[pos] = int32_t(v);
+    }
+}
+
+// info[c] = the first list position of class c, info[kClasses + c] = its rows.
+__global__ void k_class_totals(int64_t nblk, const int64_t* blk_off, int64_t* info) {
+    const int c = threadIdx.x;
+    if (blockIdx.x != 0 || c >= kClasses) return;
+    info[c] = blk_off[c * nblk];
+    info[kClasses + c] = blk_off[(c + 1) * nblk] - blk_off[c * nblk];
+}
+
+// The largest of the blocks' maxima, in *out (which starts at zero): each
+// workgroup reduces kMaxSpan of them and adds one atomic.
+constexpr int kMaxSpan = 4096;
+__global__ __launch_bounds__(256) void k_blocks_max(int64_t nblk, const uint32_t* blk_max,
+                                                    unsigned long long* out) {
+    __shared__ uint32_t s_max[256 / kWave];
+    uint32_t m = 0;
+    const int64_t b0 = int64_t(blockIdx.x) * kMaxSpan;
+    for (int64_t b = b0 + threadIdx.x; b < nblk && b < b0 + kMaxSpan; b += 256) m = blk_max[b] > m ? blk_max[b] : m;
+    m = wave_max(m);
+    if (lane_id() == 0) s_max[threadIdx.x / kWave] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < 256 / kWave; ++w) m = s_max[w] > m ? s_max[w] : m;
+        if (m) atomicMax(out, (unsigned long long)m);
     }
 }
 
@@ -566,16 +632,68 @@ __device__ __forceinline__ int64_t chunk_row(const int64_t* __restrict__ off, in
     return lo;
 }
 
-__global__ void k_big_chunks(const int32_t* __restrict__ list, const int64_t* __restrict__ len_p,
-                             const int64_t* __restrict__ rowptr, int32_t* __restrict__ ecnt,
-                             int32_t* __restrict__ scnt) {
+// Exclusive prefix of v over the workgroup in thread order; *total = the sum.
+constexpr int kPrepThreads = 1024;
+__device__ __forceinline__ int64_t prep_exscan(int64_t v, int64_t* s, int64_t* total) {
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    int64_t x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int64_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s[w] = x;
+    __syncthreads();
+    int64_t before = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kPrepThreads / kWave; ++i) {
+        const int64_t t = s[i];
+        if (i < w) before += t;
+        tot += t;
+    }
+    __syncthreads();
+    *total = tot;
+    return before + x - v;
+}
+
+// One workgroup: the first edge chunk (echunk), first slot chunk (schunk) and
+// table offset (off) of every listed row, each an exclusive scan with the
+// total at [len].
+__global__ __launch_bounds__(kPrepThreads) void k_big_prep(const int32_t* __restrict__ list,
+                                                           const int64_t* __restrict__ len_p,
+                                                           const int64_t* __restrict__ rowptr,
+                                                           int64_t* __restrict__ echunk, int64_t* __restrict__ schunk,
+                                                           int64_t* __restrict__ off) {
+    __shared__ int64_t s[kPrepThreads / kWave];
     const int64_t len = *len_p;
-    for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < len;
-         idx += int64_t(gridDim.x) * blockDim.x) {
-        const int64_t v = list[idx];
-        const int64_t deg = rowptr[v + 1] - rowptr[v];
-        ecnt[idx] = int32_t(cdiv(deg, kBigEdgeChunk));
-        scnt[idx] = int32_t(cdiv(table_cap(deg), kSlotChunk));
+    int64_t run_e = 0, run_s = 0, run_o = 0;
+    for (int64_t base = 0; base < len; base += kPrepThreads) {
+        const int64_t idx = base + threadIdx.x;
+        int64_t ne = 0, ns = 0, cap = 0;
+        if (idx < len) {
+            const int64_t v = list[idx];
+            const int64_t deg = rowptr[v + 1] - rowptr[v];
+            cap = table_cap(deg);
+            ne = cdiv(deg, kBigEdgeChunk);
+            ns = cdiv(cap, kSlotChunk);
+        }
+        int64_t te, ts, to;
+        const int64_t pe = prep_exscan(ne, s, &te);
+        const int64_t ps = prep_exscan(ns, s, &ts);
+        const int64_t po = prep_exscan(cap, s, &to);
+        if (idx < len) {
+            echunk[idx] = run_e + pe;
+            schunk[idx] = run_s + ps;
+            off[idx] = run_o + po;
+        }
+        run_e += te;
+        run_s += ts;
+        run_o += to;
+    }
+    if (threadIdx.x == 0) {
+        echunk[len] = run_e;
+        schunk[len] = run_s;
+        off[len] = run_o;
     }
 }
 
@@ -730,9 +848,12 @@ __global__ void k_big_decide(BigRows br, const int32_t* lab_in, int32_t* lab_out
 
 // --------------------------------------------------------------------- order
 
-__global__ void k_order_keys(int64_t n, const int32_t* lab, const uint32_t* deg_off, uint64_t* keys) {
+// Sort key of row v: (label, dmax - off-diagonal entries) in bits_for(n) +
+// dbits bits, dmax the largest off-diagonal entry count (< 2^dbits).
+__global__ void k_order_keys(int64_t n, const int32_t* lab, const uint32_t* deg_off, uint32_t dmax, int dbits,
+                             uint64_t* keys) {
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n; v += int64_t(gridDim.x) * blockDim.x)
-        keys[v] = (uint64_t(uint32_t(lab[v])) << 32) | uint64_t(0xFFFFFFFFu - deg_off[v]);
+        keys[v] = (uint64_t(uint32_t(lab[v])) << dbits) | uint64_t(dmax - deg_off[v]);
 }
 
 __global__ void k_finish_order(int64_t n, const uint32_t* sorted_ids, const int32_t* lab, int32_t* perm,
@@ -749,40 +870,17 @@ struct ReorderWs {
     uint32_t* flags;
     int32_t* lab[2];
     uint32_t* deg_off;
-    int32_t* is_s4;
-    int32_t* is_s8;
-    int32_t* is_s16;
-    int32_t* is_s32;
-    int32_t* is_wav;
-    int32_t* is_wmed;
-    int32_t* is_med;
-    int32_t* is_huge;
-    int64_t* big_cap;
-    int64_t* pos_s4;
-    int64_t* pos_s8;
-    int64_t* pos_s16;
-    int64_t* pos_s32;
-    int64_t* pos_wav;
-    int64_t* pos_wmed;
-    int64_t* pos_med;
-    int64_t* pos_huge;
-    int64_t* cap_off;
-    int32_t* s4_list;
-    int32_t* s8_list;
-    int32_t* s16_list;
-    int32_t* s32_list;
-    int32_t* wav_list;
-    int32_t* wmed_list;
-    int32_t* med_list;
-    int32_t* huge_list;
+    int32_t* blk_cnt;     // [kClasses * blocks]: rows of each class in each 256-row block
+    int64_t* blk_off;     // [kClasses * blocks + 1]: their exclusive scan
+    int32_t* list;        // [n]: the rows, class after class
+    int64_t* class_info;  // [2 * kClasses + 2]: first list position and rows of each class; largest
+                          // off-diagonal entry count; the CSR check's flags (low 32 bits)
+    uint32_t* blk_max;    // [blocks]: largest off-diagonal entry count of each 256-row block
     int64_t* huge_off;
-    int32_t* huge_ecnt;
-    int32_t* huge_scnt;
     int64_t* huge_echunk;
     int64_t* huge_schunk;
     int* tab_keys;
     int* tab_cnts;
-    int64_t* class_cnt;  // [kClasses]: rows of each list class, for the host
     int* big_best;
     int* big_own;
     unsigned long long* big_hbest;
@@ -792,23 +890,6 @@ struct ReorderWs {
     ScanTmp scan;
     SortTmp sort;
 };
-
-// The row counts of the list classes (the totals of their scans), gathered
-// so that one copy brings them to the host.
-enum { kClsS4, kClsS8, kClsS16, kClsS32, kClsWav, kClsWmed, kClsMed, kClsHuge, kClasses };
-__global__ void k_class_counts(int64_t n, const int64_t* s4, const int64_t* s8, const int64_t* s16,
-                               const int64_t* s32, const int64_t* wav, const int64_t* wmed, const int64_t* med,
-                               const int64_t* huge, int64_t* out) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    out[kClsS4] = s4[n];
-    out[kClsS8] = s8[n];
-    out[kClsS16] = s16[n];
-    out[kClsS32] = s32[n];
-    out[kClsWav] = wav[n];
-    out[kClsWmed] = wmed[n];
-    out[kClsMed] = med[n];
-    out[kClsHuge] = huge[n];
-}
 
 inline unsigned grid_cap(int64_t rows, int64_t per_block, unsigned cap) {
     const int64_t g = cdiv(rows, per_block);
@@ -823,48 +904,25 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.lab[0] = ws.take<int32_t>(n1);
     r.lab[1] = ws.take<int32_t>(n1);
     r.deg_off = ws.take<uint32_t>(n1);
-    r.is_s4 = ws.take<int32_t>(n1);
-    r.is_s8 = ws.take<int32_t>(n1);
-    r.is_s16 = ws.take<int32_t>(n1);
-    r.is_s32 = ws.take<int32_t>(n1);
-    r.is_wav = ws.take<int32_t>(n1);
-    r.is_wmed = ws.take<int32_t>(n1);
-    r.is_med = ws.take<int32_t>(n1);
-    r.is_huge = ws.take<int32_t>(n1);
-    r.big_cap = ws.take<int64_t>(n1);
-    r.pos_s4 = ws.take<int64_t>(n1 + 1);
-    r.pos_s8 = ws.take<int64_t>(n1 + 1);
-    r.pos_s16 = ws.take<int64_t>(n1 + 1);
-    r.pos_s32 = ws.take<int64_t>(n1 + 1);
-    r.pos_wav = ws.take<int64_t>(n1 + 1);
-    r.pos_wmed = ws.take<int64_t>(n1 + 1);
-    r.pos_med = ws.take<int64_t>(n1 + 1);
-    r.pos_huge = ws.take<int64_t>(n1 + 1);
-    r.cap_off = ws.take<int64_t>(n1 + 1);
-    r.s4_list = ws.take<int32_t>(n1);
-    r.s8_list = ws.take<int32_t>(n1);
-    r.s16_list = ws.take<int32_t>(n1);
-    r.s32_list = ws.take<int32_t>(n1);
-    r.wav_list = ws.take<int32_t>(n1);
-    r.wmed_list = ws.take<int32_t>(n1);
-    r.med_list = ws.take<int32_t>(n1);
-    r.huge_list = ws.take<int32_t>(n1);
-    r.huge_off = ws.take<int64_t>(n1);
-    r.huge_ecnt = ws.take<int32_t>(n1);
-    r.huge_scnt = ws.take<int32_t>(n1);
+    const int64_t nblk = cdiv(n1, kClsBlock);
+    r.blk_cnt = ws.take<int32_t>(size_t(kClasses * nblk));
+    r.blk_off = ws.take<int64_t>(size_t(kClasses * nblk + 1));
+    r.list = ws.take<int32_t>(n1);
+    r.class_info = ws.take<int64_t>(2 * kClasses + 2);
+    r.blk_max = ws.take<uint32_t>(size_t(nblk));
+    r.huge_off = ws.take<int64_t>(n1 + 1);
     r.huge_echunk = ws.take<int64_t>(n1 + 1);
     r.huge_schunk = ws.take<int64_t>(n1 + 1);
     const int64_t tab = 4 * (nnz > 0 ? nnz : 1);  // sum over big rows of cap <= 4 * deg
     r.tab_keys = ws.take<int>(size_t(tab));
     r.tab_cnts = ws.take<int>(size_t(tab));
-    r.class_cnt = ws.take<int64_t>(kClasses);
     r.big_best = ws.take<int>(n1);
     r.big_own = ws.take<int>(n1);
     r.big_hbest = ws.take<unsigned long long>(n1);
     r.big_lbest = ws.take<unsigned long long>(n1);
     r.sort_keys = ws.take<uint64_t>(n1);
     r.sort_vals = ws.take<uint32_t>(n1);
-    r.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1)));
+    r.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1 > kClasses * nblk + 1 ? n1 + 1 : kClasses * nblk + 1)));
     r.sort = sort_tmp(ws, n1, 8, true);
     return r;
 }
@@ -897,56 +955,60 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     }
     Ws ws(ws_ptr);
     ReorderWs r = carve(ws, n, nnz, iters);
-    gt_status st = launch_validate_csr(n, nnz, rowptr, col, r.flags, stream);
+    // the CSR check and the row classes in one go: both come back to the host with one synchronisation,
+    // and nothing past the classification runs unless the check passed
+    uint32_t* vflag = reinterpret_cast<uint32_t*>(r.class_info + 2 * kClasses + 1);
+    gt_status st = fill_u32(vflag, 2, 0u, stream);  // the high half of the slot too
     if (st != GT_OK) return st;
-    st = read_validation(r.flags, stream);
-    if (st != GT_OK) return st;
-
+    if ((st = launch_validate_csr(n, nnz, rowptr, col, vflag, stream)) != GT_OK) return st;
     const unsigned g = grid_for(n, 256, 8192);
-    k_classify<<<g, 256, 0, stream>>>(n, rowptr, col, r.deg_off, r.is_s4, r.is_s8, r.is_s16, r.is_s32, r.is_wav,
-                                      r.is_wmed, r.is_med, r.is_huge, r.big_cap);
+    const int64_t nblk = cdiv(n, kClsBlock);
+    unsigned long long* deg_max = reinterpret_cast<unsigned long long*>(r.class_info + 2 * kClasses);
+    if ((st = fill_u32(reinterpret_cast<uint32_t*>(deg_max), 2, 0u, stream)) != GT_OK) return st;
+    k_classify<<<unsigned(nblk), kClsBlock, 0, stream>>>(n, nnz, rowptr, col, r.deg_off, r.blk_cnt, nblk, r.blk_max);
     GT_LAUNCH_CHECK("reorder_classify");
-    if ((st = exclusive_scan_i32(r.is_s4, n, r.pos_s4, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_s8, n, r.pos_s8, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_s16, n, r.pos_s16, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_s32, n, r.pos_s32, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_wav, n, r.pos_wav, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_wmed, n, r.pos_wmed, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_med, n, r.pos_med, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i32(r.is_huge, n, r.pos_huge, r.scan, stream)) != GT_OK) return st;
-    if ((st = exclusive_scan_i64(r.big_cap, n, r.cap_off, r.scan, stream)) != GT_OK) return st;
-    k_compact<<<g, 256, 0, stream>>>(n, r.is_s4, r.is_s8, r.is_s16, r.is_s32, r.is_wav, r.is_wmed, r.is_med,
-                                     r.is_huge, r.pos_s4, r.pos_s8, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed,
-                                     r.pos_med, r.pos_huge, r.cap_off, r.s4_list, r.s8_list, r.s16_list, r.s32_list,
-                                     r.wav_list, r.wmed_list, r.med_list, r.huge_list, r.huge_off);
-    GT_LAUNCH_CHECK("reorder_compact");
+    k_blocks_max<<<unsigned(cdiv(nblk, kMaxSpan)), 256, 0, stream>>>(nblk, r.blk_max, deg_max);
+    GT_LAUNCH_CHECK("reorder_degree_max");
+    if ((st = exclusive_scan_i32(r.blk_cnt, kClasses * nblk, r.blk_off, r.scan, stream)) != GT_OK) return st;
+    k_class_scatter<<<unsigned(nblk), kClsBlock, 0, stream>>>(n, rowptr, r.blk_off, nblk, r.list);
+    GT_LAUNCH_CHECK("reorder_class_scatter");
+    k_class_totals<<<1, 64, 0, stream>>>(nblk, r.blk_off, r.class_info);
+    GT_LAUNCH_CHECK("reorder_class_totals");
 
     if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
     if ((st = fill_u32(r.flags, iters + 1, 0, stream)) != GT_OK) return st;
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
     // the class sizes on the host: empty classes are not launched and grids fit the lists
-    k_class_counts<<<1, 64, 0, stream>>>(n, r.pos_s4, r.pos_s8, r.pos_s16, r.pos_s32, r.pos_wav, r.pos_wmed,
-                                         r.pos_med, r.pos_huge, r.class_cnt);
-    GT_LAUNCH_CHECK("reorder_class_counts");
-    int64_t cnt[kClasses] = {};
-    GT_HIP(hipMemcpyAsync(cnt, r.class_cnt, sizeof(cnt), hipMemcpyDeviceToHost, stream));
+    int64_t info[2 * kClasses + 2] = {};
+    GT_HIP(hipMemcpyAsync(info, r.class_info, sizeof(info), hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
+    if ((st = validation_result(uint32_t(uint64_t(info[2 * kClasses + 1])))) != GT_OK) return st;
+    const int64_t* cnt = info + kClasses;
+    const int32_t* list_of[kClasses];
+    const int64_t* len_of[kClasses];
+    for (int c = 0; c < kClasses; ++c) {
+        list_of[c] = r.list + info[c];
+        len_of[c] = r.class_info + kClasses + c;
+    }
     const int64_t n_huge = cnt[kClsHuge];
-    BigRows br{r.huge_list, r.pos_huge + n, r.huge_off, r.huge_echunk, r.huge_schunk, r.tab_keys, r.tab_cnts,
-               r.big_best, r.big_own, r.big_hbest, r.big_lbest};
-    if (n_huge > 0) {  // the chunk numbering of the long rows' edges and table slots
-        k_big_chunks<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(r.huge_list, r.pos_huge + n, rowptr,
-                                                                       r.huge_ecnt, r.huge_scnt);
-        GT_LAUNCH_CHECK("reorder_big_chunks");
-        if ((st = exclusive_scan_i32(r.huge_ecnt, n_huge, r.huge_echunk, r.scan, stream)) != GT_OK) return st;
-        if ((st = exclusive_scan_i32(r.huge_scnt, n_huge, r.huge_schunk, r.scan, stream)) != GT_OK) return st;
+    BigRows br{list_of[kClsHuge], len_of[kClsHuge], r.huge_off, r.huge_echunk, r.huge_schunk, r.tab_keys,
+               r.tab_cnts, r.big_best, r.big_own, r.big_hbest, r.big_lbest};
+    if (n_huge > 0) {  // the chunk numbering of the long rows' edges and table slots, and their table offsets
+        k_big_prep<<<1, kPrepThreads, 0, stream>>>(list_of[kClsHuge], len_of[kClsHuge], rowptr, r.huge_echunk,
+                                                    r.huge_schunk, r.huge_off);
+        GT_LAUNCH_CHECK("reorder_big_prep");
     }
     // the short-row lists in one launch, blocks in proportion to their rows
     SmallRows sr;
     {
-        const int64_t* lens[kSmLists] = {r.pos_wav + n, r.pos_s32 + n, r.pos_s16 + n, r.pos_s8 + n, r.pos_s4 + n};
-        const int32_t* lists[kSmLists] = {r.wav_list, r.s32_list, r.s16_list, r.s8_list, r.s4_list};
+        const int cls[kSmLists] = {kClsWav, kClsS32, kClsS16, kClsS8, kClsS4};
+        const int64_t* lens[kSmLists];
+        const int32_t* lists[kSmLists];
+        for (int k = 0; k < kSmLists; ++k) {
+            lens[k] = len_of[cls[k]];
+            lists[k] = list_of[cls[k]];
+        }
         const int64_t rows[kSmLists] = {cnt[kClsWav], cnt[kClsS32], cnt[kClsS16], cnt[kClsS8], cnt[kClsS4]};
         const int per_block[kSmLists] = {kBlock / kWave, kBlock / kSub32, kBlock / kSub16, kBlock / kSub8,
                                          kBlock / kSub4};
@@ -984,21 +1046,23 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             GT_LAUNCH_CHECK("reorder_lp_small");
         }
         if (cnt[kClsWmed] > 0) {
-            k_lp_wavetab<<<gwt, kBlock, 0, stream>>>(r.wmed_list, r.pos_wmed + n, rowptr, col, in, out, key,
+            k_lp_wavetab<<<gwt, kBlock, 0, stream>>>(list_of[kClsWmed], len_of[kClsWmed], rowptr, col, in, out, key,
                                                      r.flags + t, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_wavetab");
         }
         if (cnt[kClsMed] > 0) {
-            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(r.med_list, r.pos_med + n, rowptr, col, in, out, key,
+            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(list_of[kClsMed], len_of[kClsMed], rowptr, col, in, out, key,
                                                             r.flags + t, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_lds");
         }
     }
     const int32_t* final_lab = r.lab[iters & 1];
-    k_order_keys<<<g, 256, 0, stream>>>(n, final_lab, r.deg_off, r.sort_keys);
+    const uint32_t dmax = uint32_t(info[2 * kClasses]);
+    const int dbits = bits_for(int64_t(dmax) + 1);
+    k_order_keys<<<g, 256, 0, stream>>>(n, final_lab, r.deg_off, dmax, dbits, r.sort_keys);
     GT_LAUNCH_CHECK("reorder_keys");
     if ((st = iota_u32(r.sort_vals, n, stream)) != GT_OK) return st;
-    if ((st = radix_sort_u64(r.sort_keys, r.sort_vals, n, 32 + bits_for(n), r.sort, stream)) != GT_OK) return st;
+    if ((st = radix_sort_u64(r.sort_keys, r.sort_vals, n, bits_for(n) + dbits, r.sort, stream)) != GT_OK) return st;
     k_finish_order<<<g, 256, 0, stream>>>(n, r.sort_vals, final_lab, perm, iperm, labels);
     GT_LAUNCH_CHECK("reorder_finish");
     if (sweeps_done) {

@@ -8,9 +8,14 @@
 // remainder CSR.  Rows of more than kLongRow edges (hubs, a global token) are
 // left out of the tile row's workgroup: the count pass publishes each tile
 // row's dense/sparse split as a bit set, and their edges are counted and
-// written chunk by chunk over the whole grid.  The remainder's transpose and
-// the column-grouped tile list come from stable radix sorts, so every output
-// is deterministic.
+// written chunk by chunk over the whole grid.
+//
+// The remainder's transpose comes from the count pass: it tags every edge with
+// its column if the edge stays in the remainder (else with n), in CSR order,
+// and a stable radix sort of (tag, row) leaves the remainder's rows grouped by
+// column, rows ascending; the column pointers are binary searches in the
+// sorted tags.  No step adds into a shared counter, so every output is
+// deterministic.
 
 #include "prim.h"
 
@@ -20,13 +25,10 @@ namespace {
 constexpr int kThreads = 256;      // the long-row kernels
 constexpr int kTileThreads = 1024;  // one workgroup per tile row: 16 wavefronts share its LDS count table
 constexpr int kMaxR = 16384;
+constexpr int kMaxT = 128;
+constexpr int kRowsPerWave = kMaxT / (kTileThreads / kWave);  // rows of a tile row per wavefront
+constexpr int kCountBatch = 8;                                 // column loads in flight per thread when counting
 constexpr uint32_t kDense = 0x80000000u;
-// LDS slots that gather the remainder column counts of a workgroup (the most
-// that keeps two tile-row workgroups per CU beside the 64 KiB count table)
-constexpr int kHash = 1024;
-constexpr uint32_t kEmpty = 0xFFFFFFFFu;
-
-__device__ __forceinline__ int hash_slot(uint32_t c) { return int((c * 2654435761u) >> 22); }
 
 // Exclusive prefix of a 0/1 flag over the workgroup, in thread order; *total = the sum.
 __device__ __forceinline__ int64_t block_flag_scan(bool flag, int64_t* s, int64_t* total) {
@@ -69,7 +71,9 @@ __device__ __forceinline__ int64_t block_exscan_i64(int64_t v, int64_t* s, int64
     return before + x - v;
 }
 
-// kFill = false: dense tiles per tile row, remainder degree per row.
+// kFill = false: dense tiles per tile row, remainder degree per row, and the
+// remainder tags: tag[e] = col[e] if edge e stays in the remainder, else n;
+// row_of_e[e] = its row.
 // kFill = true: the plan arrays (offsets from the count pass).
 // The count pass also publishes the split of tile row I for the long rows:
 // bit J of dense_bits[I * W + J / 32] marks a dense tile, dense_pre[I * W + w]
@@ -79,86 +83,109 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
                                                     int R, uint32_t tau_ppm, int32_t* dense_per_tilerow,
                                                     int32_t* sp_deg, const int64_t* tile_rowptr, int32_t* tile_col,
                                                     int32_t* tile_nnz, uint32_t* tile_mask,
-                                                    const int64_t* sp_rowptr, int32_t* sp_col,
-                                                    uint32_t* sp_colkey, uint32_t* sp_rowval, uint32_t* sp_colcnt,
-                                                    int W, uint32_t* dense_bits, uint32_t* dense_pre,
-                                                    int32_t* sp_pos, int32_t* tile_pos) {
+                                                    const int64_t* sp_rowptr, int32_t* sp_col, uint32_t* tag,
+                                                    uint32_t* row_of_e, int W, uint32_t* dense_bits,
+                                                    uint32_t* dense_pre, int32_t* sp_pos, int32_t* tile_pos) {
     __shared__ uint32_t s_cnt[kMaxR];
     __shared__ int64_t s_red[kTileThreads / kWave];
-    __shared__ uint32_t s_hkey[kHash], s_hval[kHash];
+    __shared__ int64_t s_rp[kMaxT + 1];
+    __shared__ uint64_t s_gbits[kMaxR / kWave];
+    __shared__ uint32_t s_gpre[kMaxR / kWave];
     const int I = blockIdx.x;
-    if (!kFill) {
-        for (int j = threadIdx.x; j < kHash; j += kTileThreads) {
-            s_hkey[j] = kEmpty;
-            s_hval[j] = 0;
-        }
-    }
     const int64_t r0 = int64_t(I) * T;
     const int64_t r1 = r0 + T < n ? r0 + T : n;
     const int64_t rows = r1 - r0;
     for (int J = threadIdx.x; J < R; J += kTileThreads) s_cnt[J] = 0;
+    for (int j = threadIdx.x; j <= rows; j += kTileThreads) s_rp[j] = rowptr[r0 + j];
     __syncthreads();
-    const int64_t e0 = rowptr[r0], e1 = rowptr[r1];
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += kTileThreads) atomicAdd(&s_cnt[col[e] / T], 1u);
-    __syncthreads();
-    // classify; keep the count in the low bits
-    int64_t mine = 0;
-    const int chunk = (R + kTileThreads - 1) / kTileThreads;
-    const int j0 = threadIdx.x * chunk;
-    const int j1 = j0 + chunk < R ? j0 + chunk : R;
-    for (int J = j0; J < j1; ++J) {
-        const uint32_t c = s_cnt[J];
-        const int64_t wcols = n - int64_t(J) * T < T ? n - int64_t(J) * T : T;
-        const uint64_t area = uint64_t(rows) * uint64_t(wcols);
-        if (c >= 1 && uint64_t(c) * 1000000ull >= uint64_t(tau_ppm) * area) {
-            s_cnt[J] = c | kDense;
-            ++mine;
+    const int64_t e0 = s_rp[0], e1 = s_rp[rows];
+    const int tshift = __builtin_ctz(unsigned(T));
+    // every edge of the tile row, long rows included; kCountBatch loads in
+    // flight per thread, so a tile row holding hubs is not a chain of round trips
+    for (int64_t base = e0 + threadIdx.x; base < e1; base += kCountBatch * kTileThreads) {
+        int c[kCountBatch];
+#pragma unroll
+        for (int u = 0; u < kCountBatch; ++u) {
+            const int64_t e = base + int64_t(u) * kTileThreads;
+            c[u] = e < e1 ? col[e] : -1;
         }
+#pragma unroll
+        for (int u = 0; u < kCountBatch; ++u)
+            if (c[u] >= 0) atomicAdd(&s_cnt[c[u] >> tshift], 1u);
     }
+    __syncthreads();
+    // classify 64 tile columns per wavefront step (lane j takes column 64 m + j,
+    // so LDS reads do not collide in banks); keep the count in the low bits and
+    // each group's dense bits in s_gbits[m]
+    const int ngroups = (R + kWave - 1) / kWave;
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const uint64_t lt = lanemask_lt();
+    for (int m = w; m < ngroups; m += kTileThreads / kWave) {
+        const int J = m * kWave + lane;
+        const uint32_t c = J < R ? s_cnt[J] : 0u;
+        const int64_t wcols = n - int64_t(J) * T < T ? n - int64_t(J) * T : T;
+        const uint64_t area = uint64_t(rows) * uint64_t(wcols > 0 ? wcols : 0);
+        const bool dense = c >= 1 && uint64_t(c) * 1000000ull >= uint64_t(tau_ppm) * area;
+        if (dense) s_cnt[J] = c | kDense;
+        const uint64_t bits = ballot(dense);
+        if (lane == 0) s_gbits[m] = bits;
+    }
+    __syncthreads();
+    // dense tiles before each group
     int64_t total;
-    const int64_t before = block_exscan_i64(mine, s_red, &total);
+    const int64_t gpre = block_exscan_i64(int(threadIdx.x) < ngroups ? __popcll(s_gbits[threadIdx.x]) : 0, s_red,
+                                          &total);
+    if (int(threadIdx.x) < ngroups) s_gpre[threadIdx.x] = uint32_t(gpre);
+    __syncthreads();
     if (!kFill) {
         if (threadIdx.x == 0) dense_per_tilerow[I] = int32_t(total);
-        __syncthreads();  // every classification is in s_cnt
-        // words 2t and 2t + 1 of the tile row's bit set (W <= 512)
-        uint32_t wd[2] = {0u, 0u};
-        for (int q = 0; q < 2; ++q) {
-            const int w = 2 * threadIdx.x + q;
-            if (w >= W) break;
-            for (int b = 0; b < 32; ++b) {
-                const int J = 32 * w + b;
-                if (J < R && (s_cnt[J] & kDense)) wd[q] |= 1u << b;
+        for (int m = threadIdx.x; m < ngroups; m += kTileThreads) {
+            const uint64_t bits = s_gbits[m];
+            for (int q = 0; q < 2; ++q) {
+                const int wd = 2 * m + q;
+                if (wd >= W) break;
+                dense_bits[int64_t(I) * W + wd] = uint32_t(bits >> (32 * q));
+                dense_pre[int64_t(I) * W + wd] = s_gpre[m] + (q ? uint32_t(__popc(uint32_t(bits))) : 0u);
             }
-        }
-        int64_t tot2;
-        const int64_t pre = block_exscan_i64(__popc(wd[0]) + __popc(wd[1]), s_red, &tot2);
-        for (int q = 0; q < 2; ++q) {
-            const int w = 2 * threadIdx.x + q;
-            if (w >= W) break;
-            dense_bits[int64_t(I) * W + w] = wd[q];
-            dense_pre[int64_t(I) * W + w] = uint32_t(pre + (q ? __popc(wd[0]) : 0));
         }
     } else {
         const int64_t base = tile_rowptr[I];
-        int64_t k = before;
-        for (int J = j0; J < j1; ++J) {
-            const uint32_t f = s_cnt[J];
-            if (f & kDense) {
+        for (int m = w; m < ngroups; m += kTileThreads / kWave) {
+            const int J = m * kWave + lane;
+            const uint64_t bits = s_gbits[m];
+            if ((bits >> lane) & 1u) {
+                const uint32_t k = s_gpre[m] + uint32_t(__popcll(bits & lt));
                 tile_col[base + k] = J;
-                tile_nnz[base + k] = int32_t(f & ~kDense);
-                s_cnt[J] = kDense | uint32_t(k);
-                ++k;
+                tile_nnz[base + k] = int32_t(s_cnt[J] & ~kDense);
+                s_cnt[J] = kDense | k;
             }
         }
     }
     __syncthreads();
-    // per row: remainder degree (count) or remainder edges and mask bits (fill)
-    const int lane = lane_id();
-    const uint64_t lt = lanemask_lt();
+    // per row: remainder degree and tags (count) or remainder edges and mask
+    // bits (fill).  Each wavefront takes rows w, w + 16, ... and loads the
+    // first 64 columns of all of them before handling any.
     const int wpr = T / 32;  // mask words per tile row
-    for (int64_t rl = threadIdx.x / kWave; rl < rows; rl += kTileThreads / kWave) {
+    int first[kRowsPerWave];
+    int64_t sp_first[kRowsPerWave];  // fill: the row's first remainder position
+#pragma unroll
+    for (int k = 0; k < kRowsPerWave; ++k) {
+        const int64_t rl = w + int64_t(k) * (kTileThreads / kWave);
+        first[k] = 0;
+        sp_first[k] = 0;
+        if (rl < rows) {
+            const int64_t a = s_rp[rl], b = s_rp[rl + 1];
+            if (b - a <= kLongRow && a + lane < b) first[k] = col[a + lane];
+            if (kFill && b - a <= kLongRow) sp_first[k] = sp_rowptr[r0 + rl];
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kRowsPerWave; ++k) {
+        const int64_t rl = w + int64_t(k) * (kTileThreads / kWave);
+        if (rl >= rows) break;
         const int64_t i = r0 + rl;
-        const int64_t a = rowptr[i], b = rowptr[i + 1];
+        const int64_t a = s_rp[rl], b = s_rp[rl + 1];
         if (b - a > kLongRow) {  // counted and written by the long-row kernels
             if (!kFill && lane == 0) sp_deg[i] = 0;
             continue;
@@ -167,44 +194,33 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
         for (int64_t eb = a; eb < b; eb += kWave) {
             const int64_t e = eb + lane;
             const bool valid = e < b;
-            const int c = valid ? col[e] : 0;
-            const int J = c / T;
+            const int c = !valid ? 0 : (eb == a ? first[k] : col[e]);
+            const int J = c >> tshift;
             const uint32_t f = valid ? s_cnt[J] : 0u;
             const bool dense = valid && (f & kDense);
             const bool sparse = valid && !dense;
             const uint64_t sb = ballot(sparse);
             if (kFill) {
                 if (dense) {
-                    const int64_t k = tile_rowptr[I] + int64_t(f & ~kDense);
+                    const int64_t kk = tile_rowptr[I] + int64_t(f & ~kDense);
                     const int cl = c - J * T;
-                    const int64_t word = k * int64_t(T) * wpr + rl * wpr + cl / 32;
+                    const int64_t word = kk * int64_t(T) * wpr + rl * wpr + cl / 32;
                     atomicOr(&tile_mask[word], 1u << (cl & 31));
                     // the row's first edge in this tile (its columns are sorted)
-                    if (tile_pos && (e == a || col[e - 1] / T != J)) tile_pos[k * T + rl] = int32_t(e);
+                    if (tile_pos && (e == a || (col[e - 1] >> tshift) != J)) tile_pos[kk * T + rl] = int32_t(e);
                 }
                 if (sparse) {
-                    const int64_t pos = sp_rowptr[i] + sp + __popcll(sb & lt);
+                    const int64_t pos = sp_first[k] + sp + __popcll(sb & lt);
                     sp_col[pos] = c;
-                    sp_colkey[pos] = uint32_t(c);
-                    sp_rowval[pos] = uint32_t(i);
                     if (sp_pos) sp_pos[pos] = int32_t(e);
                 }
-            }
-            if (!kFill && sparse) {
-                const int slot = hash_slot(uint32_t(c));
-                uint32_t k = s_hkey[slot];
-                if (k == kEmpty) k = atomicCAS(&s_hkey[slot], kEmpty, uint32_t(c));
-                if (k == kEmpty || k == uint32_t(c)) atomicAdd(&s_hval[slot], 1u);
-                else atomicAdd(&sp_colcnt[c], 1u);
+            } else if (valid) {
+                tag[e] = sparse ? uint32_t(c) : uint32_t(n);
+                row_of_e[e] = uint32_t(i);
             }
             sp += __popcll(sb);
         }
         if (!kFill && lane == 0) sp_deg[i] = int32_t(sp);
-    }
-    if (!kFill) {
-        __syncthreads();
-        for (int j = threadIdx.x; j < kHash; j += kTileThreads)
-            if (s_hval[j]) atomicAdd(&sp_colcnt[s_hkey[j]], s_hval[j]);
     }
 }
 
@@ -213,11 +229,11 @@ __device__ __forceinline__ bool tile_is_dense(const uint32_t* __restrict__ bits,
 }
 
 // Count pass of the long rows: remainder degree (added to the zero the tile
-// row's workgroup left) and remainder column counts.
+// row's workgroup left) and the remainder tags of their edges.
 __global__ __launch_bounds__(kThreads) void k_tiles_long_count(int64_t n, int64_t nnz, const int64_t* rowptr,
                                                                const int32_t* col, int T, int W,
                                                                const uint32_t* dense_bits, int32_t* sp_deg,
-                                                               uint32_t* sp_colcnt) {
+                                                               uint32_t* tag, uint32_t* row_of_e) {
     __shared__ int64_t s_red[kThreads / kWave];
     const int64_t chunks = long_chunks_of(nnz);
     for (int64_t ch = blockIdx.x; ch < chunks; ch += gridDim.x) {
@@ -233,7 +249,8 @@ __global__ __launch_bounds__(kThreads) void k_tiles_long_count(int64_t n, int64_
                 if (e < seg[j].b) {
                     const int c = col[e];
                     sparse = !tile_is_dense(bits, c / T);
-                    if (sparse) atomicAdd(&sp_colcnt[c], 1u);
+                    tag[e] = sparse ? uint32_t(c) : uint32_t(n);
+                    row_of_e[e] = uint32_t(r);
                 }
                 int64_t t;
                 block_flag_scan(sparse, s_red, &t);
@@ -277,7 +294,6 @@ __global__ __launch_bounds__(kThreads) void k_tiles_long_fill(int64_t n, int64_t
                                                               const uint32_t* dense_pre, const int64_t* segoff,
                                                               const int64_t* tile_rowptr, uint32_t* tile_mask,
                                                               const int64_t* sp_rowptr, int32_t* sp_col,
-                                                              uint32_t* sp_colkey, uint32_t* sp_rowval,
                                                               int32_t* sp_pos, int32_t* tile_pos) {
     __shared__ int64_t s_red[kThreads / kWave];
     const int64_t chunks = long_chunks_of(nnz);
@@ -313,8 +329,6 @@ __global__ __launch_bounds__(kThreads) void k_tiles_long_fill(int64_t n, int64_t
                 if (sparse) {
                     const int64_t pos = base + before;
                     sp_col[pos] = c;
-                    sp_colkey[pos] = uint32_t(c);
-                    sp_rowval[pos] = uint32_t(r);
                     if (sp_pos) sp_pos[pos] = int32_t(e);
                 }
                 base += t;
@@ -328,6 +342,26 @@ template <typename V>
 __global__ void k_over(int64_t m, const V* value, int64_t threshold, int32_t* flags) {
     for (int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; e < m; e += int64_t(gridDim.x) * blockDim.x)
         flags[e] = int64_t(value[e]) > threshold ? 1 : 0;
+}
+
+// colptr[c] = the first position of a tag >= c in the sorted tags (c in [0, n]):
+// the remainder transpose's column pointers, colptr[n] = the remainder size.
+__global__ void k_col_ptr(int64_t n, int64_t nnz, const uint32_t* __restrict__ tag, int64_t* __restrict__ colptr) {
+    for (int64_t c = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; c <= n; c += int64_t(gridDim.x) * blockDim.x) {
+        int64_t lo = 0, hi = nnz;
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (int64_t(tag[mid]) < c) lo = mid + 1;
+            else hi = mid;
+        }
+        colptr[c] = lo;
+    }
+}
+
+// flags[c] = the remainder column c holds more than threshold entries
+__global__ void k_long_cols(int64_t n, const int64_t* colptr, int64_t threshold, int32_t* flags) {
+    for (int64_t c = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; c < n; c += int64_t(gridDim.x) * blockDim.x)
+        flags[c] = colptr[c + 1] - colptr[c] > threshold ? 1 : 0;
 }
 
 __global__ void k_compact_list(int64_t m, const int32_t* flags, const int64_t* pos, int32_t* list) {
@@ -346,27 +380,27 @@ struct TilesWs {
     uint32_t* flags;
     unsigned long long* csum;  // checksum of the count results (kept below)
     uint64_t* record;          // [kRecordWords]: what gt_tiles_count left here (CountRecord)
+    uint32_t* tag;             // [nnz]: remainder tags (column, or n), sorted by the count pass
+    uint32_t* counts;          // per tile column
     // The count results, one contiguous range of the workspace (kept_words
-    // 8-byte words from kept_begin: dense_per_tilerow .. dense_pre), so that
+    // 8-byte words from kept_begin: dense_per_tilerow .. rows), so that
     // gt_build_tiles can take them from gt_tiles_count's workspace.
     int32_t* dense_per_tilerow;
     int32_t* sp_deg;
     int64_t* tmp_tile_rowptr;
     int64_t* tmp_sp_rowptr;
-    uint32_t* keys;     // remainder column (then tile column) keys
-    uint32_t* vals;     // remainder row (then tile index) values
-    uint32_t* counts;   // per column / per tile column
-    uint32_t* colcnt;   // remainder in-degree per column
+    int64_t* colptr;    // [n + 1]: the remainder transpose's column pointers
     int32_t* long_row_flag;
     int32_t* long_col_flag;
     int64_t* long_row_pos;
     int64_t* long_col_pos;
     uint32_t* dense_bits;  // [R, W]: the dense/sparse split of each tile row
     uint32_t* dense_pre;   // [R, W]: dense tiles before each word
-    int32_t* segcnt;       // [2 * long chunks]: remainder edges of each long-row segment
-    int64_t* segoff;       // [2 * long chunks + 1]
+    uint32_t* rows;        // [nnz]: the row of each edge, then (sorted with the tags) the remainder transpose's rows
     const uint64_t* kept_begin;
     int64_t kept_words;    // 8-byte words of the count results' range
+    int32_t* segcnt;       // [2 * long chunks]: remainder edges of each long-row segment
+    int64_t* segoff;       // [2 * long chunks + 1]
     int W;
     ScanTmp scan;
     SortTmp sort;
@@ -380,26 +414,26 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
     t.csum = ws.take<unsigned long long>(1);
     t.record = ws.take<uint64_t>(kRecordWords);
     t.W = int(cdiv(R, 32));
+    t.tag = ws.take<uint32_t>(e1);
+    t.counts = ws.take<uint32_t>(n1 + 1);
     t.dense_per_tilerow = ws.take<int32_t>(R);
     t.sp_deg = ws.take<int32_t>(n1);
     t.tmp_tile_rowptr = ws.take<int64_t>(R + 1);
     t.tmp_sp_rowptr = ws.take<int64_t>(n1 + 1);
-    t.colcnt = ws.take<uint32_t>(n1);
+    t.colptr = ws.take<int64_t>(n1 + 1);
     t.long_row_flag = ws.take<int32_t>(n1);
     t.long_col_flag = ws.take<int32_t>(n1);
     t.long_row_pos = ws.take<int64_t>(n1 + 1);
     t.long_col_pos = ws.take<int64_t>(n1 + 1);
     t.dense_bits = ws.take<uint32_t>(size_t(R * t.W));
-    t.dense_pre = ws.take<uint32_t>(size_t(R * t.W + 1));  // + 1: the range ends on an 8-byte word
+    t.dense_pre = ws.take<uint32_t>(size_t(R * t.W));
+    t.rows = ws.take<uint32_t>(size_t(e1 + (e1 & 1)));  // an even count: the range ends on an 8-byte word
     {
         const char* b = reinterpret_cast<const char*>(t.dense_per_tilerow);
-        const char* e = reinterpret_cast<const char*>(t.dense_pre + R * t.W + 1);
+        const char* e = reinterpret_cast<const char*>(t.rows + e1 + (e1 & 1));
         t.kept_begin = reinterpret_cast<const uint64_t*>(t.dense_per_tilerow);
         t.kept_words = int64_t((e - b) / 8);
     }
-    t.keys = ws.take<uint32_t>(e1);
-    t.vals = ws.take<uint32_t>(e1);
-    t.counts = ws.take<uint32_t>(n1 + 1);
     const int64_t segs = 2 * long_chunks_of(e1);
     t.segcnt = ws.take<int32_t>(size_t(segs));
     t.segoff = ws.take<int64_t>(size_t(segs + 1));
@@ -501,22 +535,25 @@ gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_
                      TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, hipStream_t stream) {
     gt_status st;
     const int R = int(cdiv(n, T));
-    if ((st = fill_u32(t.colcnt, n, 0u, stream)) != GT_OK) return st;
-    k_tiles<false><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg, nullptr,
-                                               nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                               t.colcnt, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr);
+    k_tiles<false><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg,
+                                                   nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, t.tag,
+                                                   t.rows, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr);
     GT_LAUNCH_CHECK("tiles_count");
     if (nnz > kLongRow) {
         k_tiles_long_count<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
-                                                                   t.sp_deg, t.colcnt);
+                                                                   t.sp_deg, t.tag, t.rows);
         GT_LAUNCH_CHECK("tiles_long_count");
     }
     if ((st = exclusive_scan_i32(t.dense_per_tilerow, R, tile_rowptr, t.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(t.sp_deg, n, sp_rowptr, t.scan, stream)) != GT_OK) return st;
+    // the remainder transpose: (tag, row) pairs in CSR order, stably sorted by tag
+    if (nnz > 0 && (st = radix_sort_u32(t.tag, t.rows, nnz, bits_for(n + 1), t.sort, stream)) != GT_OK) return st;
     const unsigned g = grid_for(n, 256, 8192);
+    k_col_ptr<<<grid_for(n + 1, 256, 8192), 256, 0, stream>>>(n, nnz, t.tag, t.colptr);
+    GT_LAUNCH_CHECK("tiles_colptr");
     k_over<int32_t><<<g, 256, 0, stream>>>(n, t.sp_deg, GT_LONG_ROW, t.long_row_flag);
     GT_LAUNCH_CHECK("tiles_long_rows");
-    k_over<uint32_t><<<g, 256, 0, stream>>>(n, t.colcnt, GT_LONG_ROW, t.long_col_flag);
+    k_long_cols<<<g, 256, 0, stream>>>(n, t.colptr, GT_LONG_ROW, t.long_col_flag);
     GT_LAUNCH_CHECK("tiles_long_cols");
     if ((st = exclusive_scan_i32(t.long_row_flag, n, t.long_row_pos, t.scan, stream)) != GT_OK) return st;
     if ((st = exclusive_scan_i32(t.long_col_flag, n, t.long_col_pos, t.scan, stream)) != GT_OK) return st;
@@ -635,8 +672,8 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         return st;
     k_tiles<true><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
                                               plan->tile_col, plan->tile_nnz, plan->tile_mask, plan->sp_rowptr,
-                                              plan->sp_col, t.keys, t.vals, nullptr, t.W, nullptr, nullptr,
-                                              plan->sp_pos, plan->tile_pos);
+                                              plan->sp_col, nullptr, nullptr, t.W, nullptr, nullptr, plan->sp_pos,
+                                              plan->tile_pos);
     GT_LAUNCH_CHECK("tiles_fill");
     if (nnz > kLongRow) {
         const int64_t segs = 2 * long_chunks_of(nnz);
@@ -647,27 +684,26 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         if ((st = exclusive_scan_i32(t.segcnt, segs, t.segoff, t.scan, stream)) != GT_OK) return st;
         k_tiles_long_fill<<<long_grid(nnz), kThreads, 0, stream>>>(
             n, nnz, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.segoff, plan->tile_rowptr, plan->tile_mask,
-            plan->sp_rowptr, plan->sp_col, t.keys, t.vals, plan->sp_pos, plan->tile_pos);
+            plan->sp_rowptr, plan->sp_col, plan->sp_pos, plan->tile_pos);
         GT_LAUNCH_CHECK("tiles_long_fill");
     }
-    // remainder transpose: stable sort of (column, row) pairs by column; the
-    // count pass left the column counts in colcnt
+    // remainder transpose: the count pass sorted it; its first nnz_sparse rows are the remainder's
     const int64_t m = plan->nnz_sparse;
     if (m > 0) {
-        if ((st = radix_sort_u32(t.keys, t.vals, m, bits_for(n), t.sort, stream)) != GT_OK) return st;
-        k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, t.vals, plan->sp_row);
+        k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, t.rows, plan->sp_row);
         GT_LAUNCH_CHECK("tiles_sp_row");
     }
-    if ((st = exclusive_scan_u32(t.colcnt, n, plan->sp_colptr, t.scan, stream)) != GT_OK) return st;
+    if ((st = copy_bytes(plan->sp_colptr, t.colptr, size_t(n + 1) * 8, stream)) != GT_OK) return st;
     // tiles grouped by column: stable sort of (J, tile index) by J
     const int64_t d = plan->n_dense;
     if ((st = fill_u32(t.counts, R, 0u, stream)) != GT_OK) return st;
     if (d > 0) {
         if ((st = count_keys(plan->tile_col, d, t.counts, stream)) != GT_OK) return st;
-        if ((st = copy_bytes(t.keys, plan->tile_col, d * 4, stream)) != GT_OK) return st;
-        if ((st = iota_u32(t.vals, d, stream)) != GT_OK) return st;
-        if ((st = radix_sort_u32(t.keys, t.vals, d, bits_for(R), t.sort, stream)) != GT_OK) return st;
-        k_u32_to_i32<<<grid_for(d, 256, 16384), 256, 0, stream>>>(d, t.vals, plan->tileT_idx);
+        // t.tag and t.rows are free once sp_row is out
+        if ((st = copy_bytes(t.tag, plan->tile_col, d * 4, stream)) != GT_OK) return st;
+        if ((st = iota_u32(t.rows, d, stream)) != GT_OK) return st;
+        if ((st = radix_sort_u32(t.tag, t.rows, d, bits_for(R), t.sort, stream)) != GT_OK) return st;
+        k_u32_to_i32<<<grid_for(d, 256, 16384), 256, 0, stream>>>(d, t.rows, plan->tileT_idx);
         GT_LAUNCH_CHECK("tiles_tileT");
     }
     if ((st = exclusive_scan_u32(t.counts, R, plan->tileT_ptr, t.scan, stream)) != GT_OK) return st;
