@@ -3,89 +3,155 @@
 // gathers/scatters of feature tensors.
 //
 // Rows move whole to their new place, so only each row's relabelled columns
-// need sorting.  A row of at most kShortRow entries is sorted by one wavefront
-// (a bitonic network across the lanes) and written straight to its place.
-// The longer rows' edges are packed as keys (new row << B) | new column and
-// put in order by one stable radix sort: sorted, they are grouped by new row
-// and ascending inside each row, each at its rank inside the row.
+// need sorting.  A row of at most kShortRow entries is sorted by a group of
+// 4, 8, 16, 32 or 64 lanes of a wavefront (a bitonic network across the
+// group's lanes; the row classes come from one stable partition of the new
+// rows) and written straight to its place.  The longer rows' edges are packed
+// as keys (new row << B) | new column and put in order by one stable radix
+// sort: sorted, they are grouped by new row and ascending inside each row,
+// each at its rank inside the row.
 #include "prim.h"
 
 namespace gt {
 namespace {
 
-__global__ void k_new_degrees(int64_t n, const int64_t* rowptr, const int32_t* perm, int64_t* deg_new) {
+constexpr int kShortRow = 64;  // rows sorted inside one wavefront
+
+// Row classes of the relabelling: rows of 1-4, 5-8, 9-16, 17-32 and 33-64
+// entries (sorted by lane groups), 65 to kLongRow entries (keys written by one
+// wavefront per row); empty rows and rows over kLongRow are in no list.
+enum { kRl4, kRl8, kRl16, kRl32, kRl64, kRlMed, kRlClasses };
+
+__device__ __forceinline__ int8_t relabel_class(int64_t d) {
+    return d <= 0 ? int8_t(-1)
+           : d <= 4 ? int8_t(kRl4)
+           : d <= 8 ? int8_t(kRl8)
+           : d <= 16 ? int8_t(kRl16)
+           : d <= 32 ? int8_t(kRl32)
+           : d <= kShortRow ? int8_t(kRl64)
+           : d <= kLongRow ? int8_t(kRlMed)
+                           : int8_t(-1);
+}
+
+// Entry count of every new row r (old row perm[r]), its class, and the entries
+// it sends to the radix sort (its count when longer than kShortRow, else 0).
+__global__ void k_new_degrees(int64_t n, const int64_t* rowptr, const int32_t* perm, int64_t* deg_new, int8_t* cls,
+                              int64_t* sdeg) {
     for (int64_t r = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; r < n; r += int64_t(gridDim.x) * blockDim.x) {
         const int64_t u = perm[r];
-        deg_new[r] = rowptr[u + 1] - rowptr[u];
+        const int64_t d = rowptr[u + 1] - rowptr[u];
+        deg_new[r] = d;
+        cls[r] = relabel_class(d);
+        sdeg[r] = d > kShortRow ? d : 0;
     }
 }
 
-constexpr int kShortRow = 64;  // rows sorted inside one wavefront
-
-// One wavefront per new row r (old row u = perm[r]) of 1 to kShortRow entries:
-// lane l holds iperm of the row's l-th column (padding sorts last) and, for
-// the edge map, its old CSR position; a bitonic network over the next power
-// of two of lanes sorts them ascending (the columns of a row are distinct).
-template <bool kMap>
-__global__ __launch_bounds__(256) void k_relabel_short(int64_t n, const int64_t* __restrict__ rowptr,
-                                                       const int32_t* __restrict__ col,
-                                                       const int32_t* __restrict__ perm,
-                                                       const int32_t* __restrict__ iperm,
-                                                       const int64_t* __restrict__ rowptr_out,
-                                                       int32_t* __restrict__ col_out, int32_t* __restrict__ src_pos) {
-    const int lane = lane_id();
-    const int64_t waves = int64_t(gridDim.x) * 4;
-    for (int64_t r = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; r < n; r += waves) {
-        const int64_t u = perm[r];
-        const int64_t a = rowptr[u], dl = rowptr[u + 1] - a;
-        if (dl == 0 || dl > kShortRow) continue;
-        const int d = int(dl);
-        uint32_t key = 0xFFFFFFFFu, pos = 0u;
-        if (lane < d) {
-            key = uint32_t(iperm[col[a + lane]]);
-            pos = uint32_t(a + lane);
+// The rows of one class list of at most S entries, 64 / S per wavefront: the
+// lanes of a row's group hold iperm of its columns (padding sorts last) and,
+// for the edge map, their old CSR positions; a bitonic network over the S
+// lanes sorts them ascending (the columns of a row are distinct).
+template <int S, bool kMap>
+__device__ __forceinline__ void relabel_rows(const int32_t* __restrict__ list, int64_t len, unsigned blk,
+                                             unsigned nblk, const int64_t* __restrict__ rowptr,
+                                             const int32_t* __restrict__ col, const int32_t* __restrict__ perm,
+                                             const int32_t* __restrict__ iperm,
+                                             const int64_t* __restrict__ rowptr_out, int32_t* __restrict__ col_out,
+                                             int32_t* __restrict__ src_pos) {
+    constexpr int G = kWave / S;
+    const int lane = lane_id(), sub = lane / S, sl = lane % S;
+    const int64_t waves = int64_t(nblk) * (256 / kWave);
+    for (int64_t base = (int64_t(blk) * (256 / kWave) + threadIdx.x / kWave) * G; base < len; base += waves * G) {
+        const int64_t idx = base + sub;
+        int64_t r = -1, a = 0;
+        int d = 0;
+        if (idx < len) {
+            r = list[idx];
+            const int64_t u = perm[r];
+            a = rowptr[u];
+            d = int(rowptr[u + 1] - a);
         }
-        int P = 1;
-        while (P < d) P <<= 1;
-        for (int k = 2; k <= P; k <<= 1) {
+        uint32_t key = 0xFFFFFFFFu, pos = 0u;
+        if (sl < d) {
+            key = uint32_t(iperm[col[a + sl]]);
+            pos = uint32_t(a + sl);
+        }
+#pragma unroll
+        for (int k = 2; k <= S; k <<= 1) {
+#pragma unroll
             for (int j = k >> 1; j > 0; j >>= 1) {
                 const uint32_t ok = __shfl_xor(key, j, kWave);
                 const uint32_t op = kMap ? __shfl_xor(pos, j, kWave) : 0u;
-                const bool take_min = ((lane & j) == 0) == ((lane & k) == 0);
+                const bool take_min = ((sl & j) == 0) == ((sl & k) == 0);
                 if (take_min ? ok < key : ok > key) {
                     key = ok;
                     pos = op;
                 }
             }
         }
-        if (lane < d) {
-            const int64_t o = rowptr_out[r] + lane;
+        if (sl < d) {
+            const int64_t o = rowptr_out[r] + sl;
             col_out[o] = int32_t(key);
             if (kMap) src_pos[o] = int32_t(pos);
         }
     }
 }
 
-// Entries of each new row that go to the radix sort: its degree when it is
-// longer than kShortRow, else 0.
-__global__ void k_sort_degrees(int64_t n, const int64_t* deg_new, int64_t* sdeg) {
-    for (int64_t r = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; r < n; r += int64_t(gridDim.x) * blockDim.x)
-        sdeg[r] = deg_new[r] > kShortRow ? deg_new[r] : 0;
+// The five short-row lists in one launch: the grid's blocks are cut into five
+// consecutive ranges, one per list (first[5] is the grid).
+struct ShortLists {
+    const int32_t* list[5];
+    int64_t len[5];
+    unsigned first[6];
+};
+
+template <bool kMap>
+__global__ __launch_bounds__(256) void k_relabel_short(ShortLists sl, const int64_t* __restrict__ rowptr,
+                                                       const int32_t* __restrict__ col,
+                                                       const int32_t* __restrict__ perm,
+                                                       const int32_t* __restrict__ iperm,
+                                                       const int64_t* __restrict__ rowptr_out,
+                                                       int32_t* __restrict__ col_out, int32_t* __restrict__ src_pos) {
+    const unsigned b = blockIdx.x;
+    int k = 0;
+    while (k + 1 < 5 && b >= sl.first[k + 1]) ++k;
+    const unsigned blk = b - sl.first[k], nblk = sl.first[k + 1] - sl.first[k];
+    switch (k) {
+        case 0:
+            relabel_rows<64, kMap>(sl.list[0], sl.len[0], blk, nblk, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                   src_pos);
+            break;
+        case 1:
+            relabel_rows<32, kMap>(sl.list[1], sl.len[1], blk, nblk, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                   src_pos);
+            break;
+        case 2:
+            relabel_rows<16, kMap>(sl.list[2], sl.len[2], blk, nblk, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                   src_pos);
+            break;
+        case 3:
+            relabel_rows<8, kMap>(sl.list[3], sl.len[3], blk, nblk, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                  src_pos);
+            break;
+        default:
+            relabel_rows<4, kMap>(sl.list[4], sl.len[4], blk, nblk, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                  src_pos);
+            break;
+    }
 }
 
-// Keys of the rows of kShortRow + 1 to kLongRow entries, one wavefront per new
-// row, at the row's offset soff[r] among the sorted rows' entries; for the
-// edge map, the old CSR position as the value.
+// Keys of the listed rows (kShortRow + 1 to kLongRow entries), one wavefront
+// per new row, at the row's offset soff[r] among the sorted rows' entries; for
+// the edge map, the old CSR position as the value.
 template <bool kMap>
-__global__ __launch_bounds__(256) void k_edge_keys(int64_t n, const int64_t* rowptr, const int32_t* col,
-                                                   const int32_t* perm, const int32_t* iperm, int bits,
-                                                   const int64_t* soff, uint64_t* keys, uint32_t* vals) {
+__global__ __launch_bounds__(256) void k_edge_keys(const int32_t* list, int64_t len, const int64_t* rowptr,
+                                                   const int32_t* col, const int32_t* perm, const int32_t* iperm,
+                                                   int bits, const int64_t* soff, uint64_t* keys, uint32_t* vals) {
     const int lane = lane_id();
     const int64_t waves = int64_t(gridDim.x) * 4;
-    for (int64_t r = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; r < n; r += waves) {
+    for (int64_t idx = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; idx < len; idx += waves) {
+        const int64_t r = list[idx];
         const int64_t u = perm[r];
         const int64_t a = rowptr[u], d = rowptr[u + 1] - a;
-        if (d <= kShortRow || d > kLongRow) continue;
         const uint64_t hi = uint64_t(r) << bits;
         const int64_t base = soff[r];
         for (int64_t e = lane; e < d; e += kWave) {
@@ -178,6 +244,10 @@ __global__ __launch_bounds__(256) void k_move_rows(int64_t n, int64_t words, con
 struct PermuteWs {
     uint32_t* flags;
     int64_t* deg_new;
+    int8_t* cls;      // [n]: the relabelling class of each new row
+    int32_t* list;    // [n]: the new rows by class
+    int64_t* info;    // [2 * kRlClasses + 1]: class starts and sizes; the sorted entries
+    PartitionTmp part;
     int64_t* sdeg;  // entries of each new row that go to the radix sort
     int64_t* soff;  // [n + 1]: their exclusive scan
     uint64_t* keys;
@@ -191,6 +261,10 @@ PermuteWs carve(Ws& ws, int64_t n, int64_t nnz, bool with_map) {
     const int64_t n1 = n > 0 ? n : 1, e1 = nnz > 0 ? nnz : 1;
     p.flags = ws.take<uint32_t>(1);
     p.deg_new = ws.take<int64_t>(n1);
+    p.cls = ws.take<int8_t>(n1);
+    p.list = ws.take<int32_t>(n1);
+    p.info = ws.take<int64_t>(2 * kRlClasses + 1);
+    p.part = partition_tmp(ws, n1);
     p.sdeg = ws.take<int64_t>(n1);
     p.soff = ws.take<int64_t>(n1 + 1);
     p.keys = ws.take<uint64_t>(e1);
@@ -220,30 +294,59 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     if ((st = launch_validate_csr(n, nnz, rowptr, col, p.flags, stream)) != GT_OK) return st;
     if ((st = read_validation(p.flags, stream)) != GT_OK) return st;
     const unsigned g = grid_for(n, 256, 8192);
-    k_new_degrees<<<g, 256, 0, stream>>>(n, rowptr, perm, p.deg_new);
+    k_new_degrees<<<g, 256, 0, stream>>>(n, rowptr, perm, p.deg_new, p.cls, p.sdeg);
     GT_LAUNCH_CHECK("permute_degrees");
     if ((st = exclusive_scan_i64(p.deg_new, n, rowptr_out, p.scan, stream)) != GT_OK) return st;
     if (nnz == 0) return GT_OK;
-    const unsigned gw = grid_for(n, 4, 65536);
-    if (with_map)
-        k_relabel_short<true><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, rowptr_out, col_out, src_pos);
-    else
-        k_relabel_short<false><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, rowptr_out, col_out, nullptr);
-    GT_LAUNCH_CHECK("permute_short_rows");
-    // the rows of more than kShortRow entries: packed keys, one radix sort
-    k_sort_degrees<<<g, 256, 0, stream>>>(n, p.deg_new, p.sdeg);
-    GT_LAUNCH_CHECK("permute_sort_degrees");
+    // the rows of more than kShortRow entries go to the radix sort: their offsets there
     if ((st = exclusive_scan_i64(p.sdeg, n, p.soff, p.scan, stream)) != GT_OK) return st;
-    int64_t m = 0;
-    GT_HIP(hipMemcpyAsync(&m, p.soff + n, 8, hipMemcpyDeviceToHost, stream));
+    if ((st = partition_rows(p.cls, n, kRlClasses, p.list, p.info, p.part, stream)) != GT_OK) return st;
+    int64_t info[2 * kRlClasses + 1] = {};
+    GT_HIP(hipMemcpyAsync(info, p.info, 2 * kRlClasses * 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipMemcpyAsync(info + 2 * kRlClasses, p.soff + n, 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
+    const int64_t m = info[2 * kRlClasses];
+    {
+        // the short-row lists in one launch, largest rows first, blocks in proportion to their rows
+        ShortLists sl;
+        const int order[5] = {kRl64, kRl32, kRl16, kRl8, kRl4};
+        const int per_block[5] = {256 / 64, 256 / 32, 256 / 16, 256 / 8, 256 / 4};
+        unsigned at = 0;
+        for (int k = 0; k < 5; ++k) {
+            const int c = order[k];
+            sl.list[k] = p.list + info[c];
+            sl.len[k] = info[kRlClasses + c];
+            sl.first[k] = at;
+            if (sl.len[k] > 0) {
+                const int64_t gk = cdiv(sl.len[k], per_block[k]);
+                at += unsigned(gk < 16384 ? gk : 16384);
+            }
+        }
+        sl.first[5] = at;
+        if (at > 0) {
+            if (with_map)
+                k_relabel_short<true><<<at, 256, 0, stream>>>(sl, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                                              src_pos);
+            else
+                k_relabel_short<false><<<at, 256, 0, stream>>>(sl, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                                               nullptr);
+            GT_LAUNCH_CHECK("permute_short_rows");
+        }
+    }
     if (m == 0) return GT_OK;
     const int bits = bits_for(n);
-    if (with_map)
-        k_edge_keys<true><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, bits, p.soff, p.keys, p.vals);
-    else
-        k_edge_keys<false><<<gw, 256, 0, stream>>>(n, rowptr, col, perm, iperm, bits, p.soff, p.keys, nullptr);
-    GT_LAUNCH_CHECK("permute_keys");
+    const int64_t n_med = info[kRlClasses + kRlMed];
+    if (n_med > 0) {
+        const int32_t* med = p.list + info[kRlMed];
+        const unsigned gm = grid_for(n_med, 4, 65536);
+        if (with_map)
+            k_edge_keys<true><<<gm, 256, 0, stream>>>(med, n_med, rowptr, col, perm, iperm, bits, p.soff, p.keys,
+                                                      p.vals);
+        else
+            k_edge_keys<false><<<gm, 256, 0, stream>>>(med, n_med, rowptr, col, perm, iperm, bits, p.soff, p.keys,
+                                                       nullptr);
+        GT_LAUNCH_CHECK("permute_keys");
+    }
     if (nnz > kLongRow) {
         const int64_t ch = long_chunks_of(nnz);
         const unsigned gl = unsigned(ch < 8192 ? ch : 8192);

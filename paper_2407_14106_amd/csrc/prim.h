@@ -100,6 +100,22 @@ __device__ __forceinline__ int long_segments(const int64_t* __restrict__ rowptr,
     return k;
 }
 
+// ---- Stable partition of rows [0, n) by a class per row (cls[v] in [0, ncls),
+// or -1 for no list; ncls <= kMaxClasses): list holds the rows of class 0 in
+// ascending order, then those of class 1, ...; info[c] = the first list
+// position of class c and info[ncls + c] = its rows.  One counting pass over
+// 256-row blocks, one scan of the class-major [class][block] counts, one
+// writing pass.
+constexpr int kMaxClasses = 8;
+struct PartitionTmp {
+    int32_t* blk_cnt = nullptr;  // [kMaxClasses * blocks]
+    int64_t* blk_off = nullptr;  // [kMaxClasses * blocks + 1]
+    ScanTmp scan;
+};
+PartitionTmp partition_tmp(Ws& ws, int64_t n);
+gt_status partition_rows(const int8_t* cls, int64_t n, int ncls, int32_t* list, int64_t* info, PartitionTmp t,
+                         hipStream_t s);
+
 // ---- CSR validation: accumulates error bits into *flags (one uint32, zeroed by the caller).
 enum : uint32_t { kBadRowptr = 1u, kOutOfRange = 2u, kUnsorted = 4u, kDuplicate = 8u };
 gt_status launch_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, uint32_t* flags,

@@ -301,6 +301,81 @@ gt_status radix_sort_u64(uint64_t* keys, uint32_t* values, int64_t n, int key_bi
     return radix_sort<uint64_t>(keys, values, n, key_bits, tmp, s);
 }
 
+// ========================================================== row partition
+
+constexpr int kPartBlock = 256;
+
+// Per-wavefront counts of each class in s[w][c]; returns the lane's rank
+// among its wavefront's lanes of the same class.
+__device__ __forceinline__ int part_ballots(int c, int ncls, int (*s)[kMaxClasses]) {
+    const int w = threadIdx.x / kWave;
+    int rank = 0;
+    for (int k = 0; k < ncls; ++k) {
+        const uint64_t m = __ballot(c == k);
+        if (lane_id() == 0) s[w][k] = __popcll(m);
+        if (c == k) rank = __popcll(m & lanemask_lt());
+    }
+    return rank;
+}
+
+__global__ __launch_bounds__(kPartBlock) void k_part_count(const int8_t* cls, int64_t n, int ncls, int64_t nblk,
+                                                           int32_t* blk_cnt) {
+    __shared__ int s[kPartBlock / kWave][kMaxClasses];
+    const int64_t v = int64_t(blockIdx.x) * kPartBlock + threadIdx.x;
+    part_ballots(v < n ? int(cls[v]) : -1, ncls, s);
+    __syncthreads();
+    if (int(threadIdx.x) < ncls) {
+        int t = 0;
+        for (int w = 0; w < kPartBlock / kWave; ++w) t += s[w][threadIdx.x];
+        blk_cnt[threadIdx.x * nblk + blockIdx.x] = t;
+    }
+}
+
+__global__ __launch_bounds__(kPartBlock) void k_part_scatter(const int8_t* cls, int64_t n, int ncls, int64_t nblk,
+                                                             const int64_t* blk_off, int32_t* list) {
+    __shared__ int s[kPartBlock / kWave][kMaxClasses];
+    const int64_t v = int64_t(blockIdx.x) * kPartBlock + threadIdx.x;
+    const int c = v < n ? int(cls[v]) : -1;
+    const int rank = part_ballots(c, ncls, s);
+    __syncthreads();
+    if (c >= 0 && c < ncls) {
+        int64_t pos = blk_off[c * nblk + blockIdx.x] + rank;
+        for (int w = 0; w < int(threadIdx.x / kWave); ++w) pos += s[w][c];
+        list[pos] = int32_t(v);
+    }
+}
+
+__global__ void k_part_info(int ncls, int64_t nblk, const int64_t* blk_off, int64_t* info) {
+    const int c = threadIdx.x;
+    if (blockIdx.x != 0 || c >= ncls) return;
+    info[c] = blk_off[c * nblk];
+    info[ncls + c] = blk_off[(c + 1) * nblk] - blk_off[c * nblk];
+}
+
+PartitionTmp partition_tmp(Ws& ws, int64_t n) {
+    PartitionTmp t;
+    const int64_t nblk = cdiv(n > 0 ? n : 1, kPartBlock);
+    t.blk_cnt = ws.take<int32_t>(size_t(kMaxClasses * nblk));
+    t.blk_off = ws.take<int64_t>(size_t(kMaxClasses * nblk + 1));
+    t.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(kMaxClasses * nblk + 1)));
+    return t;
+}
+
+gt_status partition_rows(const int8_t* cls, int64_t n, int ncls, int32_t* list, int64_t* info, PartitionTmp t,
+                         hipStream_t s) {
+    if (n <= 0 || ncls < 1 || ncls > kMaxClasses) return fail(GT_ERR_INVALID_ARG, "partition_rows: bad sizes");
+    const int64_t nblk = cdiv(n, kPartBlock);
+    k_part_count<<<unsigned(nblk), kPartBlock, 0, s>>>(cls, n, ncls, nblk, t.blk_cnt);
+    GT_LAUNCH_CHECK("partition_count");
+    gt_status st = exclusive_scan_i32(t.blk_cnt, ncls * nblk, t.blk_off, t.scan, s);
+    if (st != GT_OK) return st;
+    k_part_scatter<<<unsigned(nblk), kPartBlock, 0, s>>>(cls, n, ncls, nblk, t.blk_off, list);
+    GT_LAUNCH_CHECK("partition_scatter");
+    k_part_info<<<1, 64, 0, s>>>(ncls, nblk, t.blk_off, info);
+    GT_LAUNCH_CHECK("partition_info");
+    return GT_OK;
+}
+
 // =========================================================== CSR validation
 
 // Validation in two coalesced passes.  k_validate_rows checks every row's
