@@ -89,6 +89,7 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
     __shared__ uint32_t s_cnt[kMaxR];
     __shared__ int64_t s_red[kTileThreads / kWave];
     __shared__ int64_t s_rp[kMaxT + 1];
+    __shared__ int64_t s_sp[kFill ? kMaxT : 1];  // fill: each row's first remainder position
     __shared__ uint64_t s_gbits[kMaxR / kWave];
     __shared__ uint32_t s_gpre[kMaxR / kWave];
     const int I = blockIdx.x;
@@ -97,6 +98,8 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
     const int64_t rows = r1 - r0;
     for (int J = threadIdx.x; J < R; J += kTileThreads) s_cnt[J] = 0;
     for (int j = threadIdx.x; j <= rows; j += kTileThreads) s_rp[j] = rowptr[r0 + j];
+    if (kFill)
+        for (int j = threadIdx.x; j < rows; j += kTileThreads) s_sp[j] = sp_rowptr[r0 + j];
     __syncthreads();
     const int64_t e0 = s_rp[0], e1 = s_rp[rows];
     const int tshift = __builtin_ctz(unsigned(T));
@@ -168,16 +171,13 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
     // first 64 columns of all of them before handling any.
     const int wpr = T / 32;  // mask words per tile row
     int first[kRowsPerWave];
-    int64_t sp_first[kRowsPerWave];  // fill: the row's first remainder position
 #pragma unroll
     for (int k = 0; k < kRowsPerWave; ++k) {
         const int64_t rl = w + int64_t(k) * (kTileThreads / kWave);
         first[k] = 0;
-        sp_first[k] = 0;
         if (rl < rows) {
             const int64_t a = s_rp[rl], b = s_rp[rl + 1];
             if (b - a <= kLongRow && a + lane < b) first[k] = col[a + lane];
-            if (kFill && b - a <= kLongRow) sp_first[k] = sp_rowptr[r0 + rl];
         }
     }
 #pragma unroll
@@ -207,10 +207,11 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
                     const int64_t word = kk * int64_t(T) * wpr + rl * wpr + cl / 32;
                     atomicOr(&tile_mask[word], 1u << (cl & 31));
                     // the row's first edge in this tile (its columns are sorted)
-                    if (tile_pos && (e == a || (col[e - 1] >> tshift) != J)) tile_pos[kk * T + rl] = int32_t(e);
+                    if (tile_pos && (e == a || (col[e - 1] >> tshift) != J))
+                        tile_pos[kk * T + rl] = int32_t(e);
                 }
                 if (sparse) {
-                    const int64_t pos = sp_first[k] + sp + __popcll(sb & lt);
+                    const int64_t pos = s_sp[rl] + sp + __popcll(sb & lt);
                     sp_col[pos] = c;
                     if (sp_pos) sp_pos[pos] = int32_t(e);
                 }
