@@ -169,14 +169,17 @@ gt_status count_keys(const int32_t* keys, int64_t n, uint32_t* counts, hipStream
 }
 
 // =============================================================== radix sort
-// 256 threads, 16 rounds of 256 keys per tile; key idx = tile*4096 + round*256 + tid.
-// Digits are ranked in (round, wave, lane) order, which is the input order, so
-// each pass is stable and the whole LSD sort is stable.
+// 8-bit digits, least significant first.  A tile of 2048 keys per workgroup of
+// four wavefronts; wavefront w owns keys [512 w, 512 w + 512) of its tile, in
+// rounds of 64.  Each key's rank among the tile's keys of its digit follows
+// (wavefront, round, lane) order, which is the input order, so every pass is
+// stable and so is the whole sort.  The tile is put in digit order in LDS
+// first, so the keys of one digit leave in one contiguous run.
 
 constexpr int kSortThreads = 256;
-constexpr int kSortRounds = 16;
-constexpr int kSortTile = kSortThreads * kSortRounds;
 constexpr int kSortWaves = kSortThreads / kWave;
+constexpr int kSortRounds = 8;  // rounds of 64 keys per wavefront
+constexpr int kSortTile = kSortWaves * kSortRounds * kWave;
 
 int64_t sort_tiles(int64_t n) { return cdiv(n, kSortTile); }
 
@@ -198,7 +201,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_hist(const K* keys, int64
     s_h[threadIdx.x] = 0;
     __syncthreads();
     const int64_t base = int64_t(blockIdx.x) * kSortTile;
-    for (int r = 0; r < kSortRounds; ++r) {
+    for (int r = 0; r < kSortTile / kSortThreads; ++r) {
         const int64_t i = base + r * kSortThreads + threadIdx.x;
         if (i < n) atomicAdd(&s_h[uint32_t(keys[i] >> shift) & 255u], 1u);
     }
@@ -210,22 +213,33 @@ template <typename K>
 __global__ __launch_bounds__(kSortThreads) void k_sort_scatter(const K* keys, const uint32_t* vals, int64_t n,
                                                                 int shift, int64_t tiles, const int64_t* offsets,
                                                                 K* keys_out, uint32_t* vals_out) {
-    __shared__ int64_t s_base[256];
-    __shared__ int64_t s_w[kSortWaves][256];
-    const int tid = threadIdx.x;
-    const int w = tid / kWave;
-    s_base[tid] = offsets[int64_t(tid) * tiles + blockIdx.x];
+    __shared__ int s_wc[kSortWaves][256];  // per-wavefront digit counts, then their starts in the tile
+    __shared__ int s_ds[256];              // tile-local start of each digit
+    __shared__ int s_part[kSortWaves];
+    __shared__ int64_t s_go[256];          // output start of the tile's keys of each digit
+    __shared__ K s_k[kSortTile];
+    __shared__ uint32_t s_v[kSortTile];
+    const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
 #pragma unroll
-    for (int k = 0; k < kSortWaves; ++k) s_w[k][tid] = 0;
-    __syncthreads();
-    const int64_t base = int64_t(blockIdx.x) * kSortTile;
-    const uint64_t lt = lanemask_lt();
+    for (int k = 0; k < kSortWaves; ++k) s_wc[k][tid] = 0;
+    s_go[tid] = offsets[int64_t(tid) * tiles + blockIdx.x];
+    const int64_t tile0 = int64_t(blockIdx.x) * kSortTile;
+    const int64_t base = tile0 + w * (kSortRounds * kWave);
+    K key[kSortRounds];
+    uint32_t val[kSortRounds];
+    int rk[kSortRounds];
+#pragma unroll
     for (int r = 0; r < kSortRounds; ++r) {
-        const int64_t i = base + r * kSortThreads + tid;
-        const bool valid = i < n;
-        K key = valid ? keys[i] : K(0);
-        uint32_t val = (valid && vals) ? vals[i] : 0u;
-        const uint32_t d = uint32_t(key >> shift) & 255u;
+        const int64_t i = base + r * kWave + lane;
+        key[r] = i < n ? keys[i] : K(0);
+        val[r] = (i < n && vals) ? vals[i] : 0u;
+    }
+    __syncthreads();
+    const uint64_t lt = lanemask_lt();
+#pragma unroll
+    for (int r = 0; r < kSortRounds; ++r) {
+        const bool valid = base + r * kWave + lane < n;
+        const uint32_t d = uint32_t(key[r] >> shift) & 255u;
         uint64_t peers = ballot(valid);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
@@ -234,28 +248,55 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_scatter(const K* keys, co
             peers &= bit ? bm : ~bm;
         }
         const int rank = __popcll(peers & lt);
-        if (valid && rank == 0) s_w[w][d] = __popcll(peers);
-        __syncthreads();
-        {
-            int64_t run = s_base[tid];
+        // the wavefront's count of digit d so far: read by every lane of the
+        // digit, then advanced by its first lane (a wavefront's LDS accesses
+        // complete in order)
+        const int before = valid ? s_wc[w][d] : 0;
+        if (valid && rank == 0) s_wc[w][d] = before + __popcll(peers);
+        rk[r] = before + rank;
+    }
+    __syncthreads();
+    // thread tid takes digit tid: the tile's count of it and each wavefront's share
+    int tot = 0, wp[kSortWaves];
 #pragma unroll
-            for (int k = 0; k < kSortWaves; ++k) {
-                const int64_t c = s_w[k][tid];
-                s_w[k][tid] = run;
-                run += c;
-            }
-            s_base[tid] = run;
-        }
-        __syncthreads();
-        if (valid) {
-            const int64_t pos = s_w[w][d] + rank;
-            keys_out[pos] = key;
-            if (vals) vals_out[pos] = val;
-        }
-        __syncthreads();
+    for (int k = 0; k < kSortWaves; ++k) {
+        wp[k] = tot;
+        tot += s_wc[k][tid];
+    }
+    int x = tot;  // inclusive scan over the 256 digits
 #pragma unroll
-        for (int k = 0; k < kSortWaves; ++k) s_w[k][tid] = 0;
-        __syncthreads();
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s_part[w] = x;
+    __syncthreads();
+    int ds = x - tot;
+#pragma unroll
+    for (int k = 0; k < kSortWaves; ++k)
+        if (k < w) ds += s_part[k];
+    s_ds[tid] = ds;
+#pragma unroll
+    for (int k = 0; k < kSortWaves; ++k) s_wc[k][tid] = ds + wp[k];
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSortRounds; ++r) {
+        if (base + r * kWave + lane < n) {
+            const uint32_t d = uint32_t(key[r] >> shift) & 255u;
+            const int p = s_wc[w][d] + rk[r];
+            s_k[p] = key[r];
+            s_v[p] = val[r];
+        }
+    }
+    __syncthreads();
+    const int64_t left = n - tile0;
+    const int cnt = left < kSortTile ? int(left) : kSortTile;
+    for (int p = tid; p < cnt; p += kSortThreads) {
+        const K k = s_k[p];
+        const uint32_t d = uint32_t(k >> shift) & 255u;
+        const int64_t pos = s_go[d] + (p - s_ds[d]);
+        keys_out[pos] = k;
+        if (vals) vals_out[pos] = s_v[p];
     }
 }
 
