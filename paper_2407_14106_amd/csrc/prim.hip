@@ -131,11 +131,55 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_apply(const In* in, int64
     if (blockIdx.x == 0 && threadIdx.x == 0) out[n] = sums[nb];
 }
 
+// Up to kScanFewBlocks blocks: each block adds the sums of the blocks before
+// it itself, so the scan of the block sums needs no launch of its own; the
+// last block writes the total.
+constexpr int64_t kScanFewBlocks = 1024;
+template <typename In>
+__global__ __launch_bounds__(kScanThreads) void k_scan_apply_few(const In* in, int64_t n, const int64_t* sums,
+                                                                  int64_t* out) {
+    __shared__ int64_t s_pre;
+    int64_t before = 0;
+    for (int64_t b = threadIdx.x; b < int64_t(blockIdx.x); b += kScanThreads) before += sums[b];
+    int64_t ex0;
+    before = block_exscan(before, &ex0);  // the sum over the threads
+    if (threadIdx.x == 0) s_pre = before;
+    __syncthreads();
+    const int64_t base = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
+    int64_t v[kScanItems];
+    int64_t acc = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        v[k] = load_as_i64(in, base + k, n);
+        acc += v[k];
+    }
+    int64_t ex;
+    const int64_t tot = block_exscan(acc, &ex);
+    ex += s_pre;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        if (base + k < n) out[base + k] = ex;
+        ex += v[k];
+    }
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = s_pre + tot;
+}
+
 template <typename In>
 static gt_status exscan(const In* in, int64_t n, int64_t* out, ScanTmp tmp, hipStream_t s) {
     if (n <= 0) return fill_i64(out, 1, 0, s);
     const int64_t nb = cdiv(n, kScanTile);
+    if (nb == 1) {  // one block: no block sums at all
+        k_scan_apply_few<In><<<1, kScanThreads, 0, s>>>(in, n, nullptr, out);
+        GT_LAUNCH_CHECK("scan_one_block");
+        return GT_OK;
+    }
     k_scan_reduce<In><<<unsigned(nb), kScanThreads, 0, s>>>(in, n, tmp.block_sums);
+    if (nb <= kScanFewBlocks) {
+        GT_LAUNCH_CHECK("scan_reduce");
+        k_scan_apply_few<In><<<unsigned(nb), kScanThreads, 0, s>>>(in, n, tmp.block_sums, out);
+        GT_LAUNCH_CHECK("scan_apply");
+        return GT_OK;
+    }
     GT_LAUNCH_CHECK("scan_reduce");
     k_scan_sums<<<1, kScanThreads, 0, s>>>(tmp.block_sums, nb);
     GT_LAUNCH_CHECK("scan_sums");
