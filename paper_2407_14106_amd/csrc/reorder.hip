@@ -325,6 +325,48 @@ __device__ __forceinline__ void lp_sub_rows(const int32_t* list, int64_t len, un
     }
 }
 
+// ----------------------------------------------------------- the first sweep
+// The first sweep starts from every node's own id as its label, so the labels
+// of a row's neighbours all differ and each counts once: the best count is 1
+// (0 without a neighbour other than the node itself), the node's own label is
+// not among them, and the tie-break takes the neighbour whose id hashes
+// smallest.  The hash is a bijection of the 64-bit word, so that neighbour is
+// unique.  The first sweep therefore reads no labels and builds no tables: it
+// takes a minimum over each row's columns.
+
+// Rows of at most S edges, 64 / S per wavefront.
+template <int S>
+__device__ __forceinline__ void first_rows(const int32_t* list, int64_t len, unsigned blk, unsigned nblk,
+                                           const int64_t* rowptr, const int32_t* col, int32_t* lab_out, uint64_t key,
+                                           uint32_t* flag_next) {
+    constexpr int G = kWave / S;
+    const int lane = lane_id(), sub = lane / S, sl = lane % S;
+    const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
+    const int64_t waves = int64_t(nblk) * (kBlock / kWave);
+    for (int64_t base = (int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave) * G; base < len; base += waves * G) {
+        const int64_t idx = base + sub;
+        const bool live = idx < len;
+        const int64_t v = live ? list[idx] : 0;
+        int64_t a = 0;
+        int deg = 0;
+        if (live) {
+            a = rowptr[v];
+            deg = int(rowptr[v + 1] - a);
+        }
+        const int c = sl < deg ? col[a + sl] : -1;
+        const bool valid = sl < deg && c != v;
+        const uint64_t h = valid ? mix64(uint64_t(uint32_t(c)) ^ key) : ~0ull;
+        const uint64_t hmin = group_min_u64<S>(h);
+        const int lmin = group_min_i32<S>((valid && h == hmin) ? c : INT_MAX);
+        const bool any = (__ballot(valid) & gmask) != 0;
+        if (live && sl == 0) {
+            const int own = int(v), cand = any ? lmin : own;
+            lab_out[v] = is_active(v, key) ? cand : own;
+            if (cand != own) *flag_next = 1u;
+        }
+    }
+}
+
 // The five short-row lists (rows of 33-64, 17-32, 9-16, 5-8 and 0-4 edges, in
 // that order) and the first block of each one's range; first[5] is the grid.
 enum { kSmWave, kSm32, kSm16, kSm8, kSm4, kSmLists };
@@ -334,6 +376,7 @@ struct SmallRows {
     unsigned first[kSmLists + 1];
 };
 
+template <bool kFirst>
 __global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t* rowptr, const int32_t* col,
                                                      const int32_t* lab_in, int32_t* lab_out, uint64_t key,
                                                      const uint32_t* flag_prev, uint32_t* flag_next) {
@@ -343,6 +386,26 @@ __global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t
     while (k + 1 < kSmLists && b >= sr.first[k + 1]) ++k;
     const unsigned blk = b - sr.first[k], nblk = sr.first[k + 1] - sr.first[k];
     const int64_t len = *sr.len[k];
+    if constexpr (kFirst) {
+        switch (k) {
+            case kSmWave:
+                first_rows<kWave>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
+                break;
+            case kSm32:
+                first_rows<kSub32>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
+                break;
+            case kSm16:
+                first_rows<kSub16>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
+                break;
+            case kSm8:
+                first_rows<kSub8>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
+                break;
+            default:
+                first_rows<kSub4>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
+                break;
+        }
+        return;
+    }
     switch (k) {
         case kSmWave:
             lp_wave_rows(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
@@ -583,6 +646,59 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
             if (cand != own) *flag_next = 1u;
         }
         wave_lds_sync();  // every lane is done with the table before the next row clears it
+    }
+}
+
+// First sweep, rows of more than 64 edges: BS threads per row (one wavefront,
+// or the workgroup), each lane keeping the smallest hash of its edges.
+template <int BS>
+__global__ __launch_bounds__(BS > kBlock ? BS : kBlock) void k_first_wide(const int32_t* list, const int64_t* list_len,
+                                                                          const int64_t* rowptr, const int32_t* col,
+                                                                          int32_t* lab_out, uint64_t key,
+                                                                          uint32_t* flag_next) {
+    constexpr int kThreads = BS > kBlock ? BS : kBlock;
+    constexpr int kRowsPer = kThreads / BS;  // rows a workgroup takes at once
+    __shared__ uint64_t s_red64[kThreads / kWave];
+    __shared__ int s_any[kThreads / kWave];
+    const int64_t len = *list_len;
+    const int t = threadIdx.x % BS;
+    for (int64_t idx0 = int64_t(blockIdx.x) * kRowsPer; idx0 < len; idx0 += int64_t(gridDim.x) * kRowsPer) {
+        const int64_t idx = idx0 + threadIdx.x / BS;
+        const bool live = idx < len;  // uniform over a row's BS threads
+        const int64_t v = live ? list[idx] : 0;
+        uint64_t hb = ~0ull;
+        int cb = INT_MAX;
+        bool any = false;
+        if (live) {
+            const int64_t a = rowptr[v], b = rowptr[v + 1];
+            for (int64_t e = a + t; e < b; e += BS) {
+                const int c = col[e];
+                if (c == v) continue;
+                const uint64_t h = mix64(uint64_t(uint32_t(c)) ^ key);
+                if (h < hb || (h == hb && c < cb)) {
+                    hb = h;
+                    cb = c;
+                }
+                any = true;
+            }
+        }
+        uint64_t hmin;
+        int lmin;
+        bool anyr;
+        if constexpr (BS == kWave) {
+            hmin = wave_min_u64(hb);
+            lmin = wave_min_i32(hb == hmin ? cb : INT_MAX);
+            anyr = __ballot(any) != 0;
+        } else {
+            hmin = block_min_u64<BS>(hb, s_red64);
+            lmin = int(block_min_u64<BS>(hb == hmin ? uint64_t(uint32_t(cb)) : ~0ull, s_red64));
+            anyr = block_max_i32<BS>(any ? 1 : 0, s_any) != 0;
+        }
+        if (live && t == 0) {
+            const int own = int(v), cand = anyr ? lmin : own;
+            lab_out[v] = is_active(v, key) ? cand : own;
+            if (cand != own) *flag_next = 1u;
+        }
     }
 }
 
@@ -846,6 +962,60 @@ __global__ void k_big_decide(BigRows br, const int32_t* lab_in, int32_t* lab_out
     }
 }
 
+// First sweep of the very long rows: per-row results reset (the tables are
+// not used), the smallest hash over every chunk of edges (combined with a 64-bit
+// atomic minimum), then the neighbour with that hash; k_big_decide finishes.
+__global__ void k_big_first_reset(BigRows br) {
+    const int64_t len = *br.len;
+    for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < len;
+         idx += int64_t(gridDim.x) * blockDim.x) {
+        br.best[idx] = 0;
+        br.own_cnt[idx] = 0;
+        br.hbest[idx] = ~0ull;
+        br.lbest[idx] = ~0ull;
+    }
+}
+
+template <int kPass>
+__global__ __launch_bounds__(kBlock) void k_big_first(BigRows br, const int64_t* rowptr, const int32_t* col,
+                                                      uint64_t key) {
+    __shared__ uint64_t s_red64[kBlock / kWave];
+    __shared__ int s_any[kBlock / kWave];
+    const int64_t len = *br.len;
+    const int64_t total = br.echunk[len];
+    for (int64_t ch = blockIdx.x; ch < total; ch += gridDim.x) {
+        const int64_t idx = chunk_row(br.echunk, len, ch);
+        const int64_t v = br.list[idx];
+        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        const int64_t j = ch - br.echunk[idx];
+        const int64_t e0 = a + j * kBigEdgeChunk;
+        const int64_t e1 = e0 + kBigEdgeChunk < b ? e0 + kBigEdgeChunk : b;
+        if (kPass == 0) {
+            uint64_t hb = ~0ull;
+            bool any = false;
+            for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
+                const int c = col[e];
+                if (c == v) continue;
+                const uint64_t h = mix64(uint64_t(uint32_t(c)) ^ key);
+                hb = h < hb ? h : hb;
+                any = true;
+            }
+            hb = block_min_u64(hb, s_red64);
+            const bool anyr = block_max_i32(any ? 1 : 0, s_any) != 0;
+            if (threadIdx.x == 0 && anyr) {
+                atomicMin(&br.hbest[idx], (unsigned long long)hb);
+                atomicMax(&br.best[idx], 1);
+            }
+        } else {
+            const uint64_t hb = br.hbest[idx];
+            for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
+                const int c = col[e];
+                if (c != v && mix64(uint64_t(uint32_t(c)) ^ key) == hb) br.lbest[idx] = uint64_t(uint32_t(c));
+            }
+        }
+    }
+}
+
 // --------------------------------------------------------------------- order
 
 // Sort key of row v: (label, dmax - off-diagonal entries) in bits_for(n) +
@@ -1027,6 +1197,33 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
         const int32_t* in = r.lab[t & 1];
         int32_t* out = r.lab[(t + 1) & 1];
+        if (t == 0) {  // labels are the node ids: a minimum over each row's columns
+            if (n_huge > 0) {
+                k_big_first_reset<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br);
+                k_big_first<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, key);
+                k_big_first<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, key);
+                GT_LAUNCH_CHECK("reorder_big_first");
+                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, in, out, key, r.flags,
+                                                                              r.flags + 1);
+                GT_LAUNCH_CHECK("reorder_big_decide");
+            }
+            if (sr.first[kSmLists] > 0) {
+                k_lp_small<true><<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, in, out, key, r.flags,
+                                                                           r.flags + 1);
+                GT_LAUNCH_CHECK("reorder_first_small");
+            }
+            if (cnt[kClsWmed] > 0) {
+                k_first_wide<kWave><<<gwt, kBlock, 0, stream>>>(list_of[kClsWmed], len_of[kClsWmed], rowptr, col,
+                                                               out, key, r.flags + 1);
+                GT_LAUNCH_CHECK("reorder_first_wave");
+            }
+            if (cnt[kClsMed] > 0) {
+                k_first_wide<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(list_of[kClsMed], len_of[kClsMed], rowptr,
+                                                                        col, out, key, r.flags + 1);
+                GT_LAUNCH_CHECK("reorder_first_block");
+            }
+            continue;
+        }
         if (n_huge > 0) {
             const uint32_t* fp = r.flags + t;
             k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp);
@@ -1041,8 +1238,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             GT_LAUNCH_CHECK("reorder_big_decide");
         }
         if (sr.first[kSmLists] > 0) {
-            k_lp_small<<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, in, out, key, r.flags + t,
-                                                                  r.flags + t + 1);
+            k_lp_small<false><<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, in, out, key, r.flags + t,
+                                                                         r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_small");
         }
         if (cnt[kClsWmed] > 0) {
