@@ -813,7 +813,14 @@ __global__ __launch_bounds__(kPrepThreads) void k_big_prep(const int32_t* __rest
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t* rowptr, const uint32_t* flag_prev) {
+// Tables of up to kFusedCap slots are reduced, decided and cleared by one
+// workgroup each (k_big_fused); the chunked passes below handle the larger ones.
+constexpr int64_t kFusedCap = 65536;
+constexpr int kFusedThreads = 1024;
+
+// all: every table (its first use); else only those over kFusedCap slots.
+__global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t* rowptr, const uint32_t* flag_prev,
+                                                      bool all) {
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
     const int64_t total = br.schunk[len];
@@ -821,6 +828,7 @@ __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t*
         const int64_t idx = chunk_row(br.schunk, len, c);
         const int64_t v = br.list[idx];
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
+        if (!all && cap <= kFusedCap) continue;
         const int64_t j = c - br.schunk[idx];
         int* tk = br.keys + br.off[idx];
         int* tc = br.cnts + br.off[idx];
@@ -905,6 +913,7 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
         const int64_t idx = chunk_row(br.schunk, len, c);
         const int64_t v = br.list[idx];
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
+        if (cap <= kFusedCap) continue;  // k_big_fused's (uniform across the workgroup)
         const int64_t j = c - br.schunk[idx];
         const int64_t s0 = j * kSlotChunk, s1 = (j + 1) * kSlotChunk < cap ? (j + 1) * kSlotChunk : cap;
         const int own = lab_in[v];
@@ -943,13 +952,77 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
     }
 }
 
-__global__ void k_big_decide(BigRows br, const int32_t* lab_in, int32_t* lab_out, uint64_t key,
-                             const uint32_t* flag_prev, uint32_t* flag_next) {
+// One workgroup per row whose table has at most kFusedCap slots: the best
+// count and the own label's count, the tie-break when the own label is not
+// among the best, the new label, then the table cleared for the next sweep.
+__global__ __launch_bounds__(kFusedThreads) void k_big_fused(BigRows br, const int64_t* rowptr,
+                                                             const int32_t* lab_in, int32_t* lab_out, uint64_t key,
+                                                             const uint32_t* flag_prev, uint32_t* flag_next) {
+    __shared__ int s_red[kFusedThreads / kWave];
+    __shared__ uint64_t s_red64[kFusedThreads / kWave];
+    const bool converged = *flag_prev == 0;
+    const int64_t len = *br.len;
+    for (int64_t idx = blockIdx.x; idx < len; idx += gridDim.x) {
+        const int64_t v = br.list[idx];
+        const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
+        if (cap > kFusedCap) continue;  // uniform across the workgroup
+        const int own = lab_in[v];
+        if (converged) {  // the insert did not run: the table is still clear
+            if (threadIdx.x == 0) lab_out[v] = own;
+            continue;
+        }
+        int* tk = br.keys + br.off[idx];
+        int* tc = br.cnts + br.off[idx];
+        int best = 0, own_cnt = 0;
+        for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
+            const int k = tk[q];
+            if (k < 0) continue;
+            const int c = tc[q];
+            best = c > best ? c : best;
+            if (k == own) own_cnt = c;
+        }
+        best = block_max_i32<kFusedThreads>(best, s_red);
+        own_cnt = block_max_i32<kFusedThreads>(own_cnt, s_red);
+        int cand = own;
+        if (best > 0 && own_cnt != best) {
+            uint64_t hbest = ~0ull;
+            for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
+                const int k = tk[q];
+                if (k < 0 || tc[q] != best) continue;
+                const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
+                hbest = h < hbest ? h : hbest;
+            }
+            hbest = block_min_u64<kFusedThreads>(hbest, s_red64);
+            uint64_t lbest = ~0ull;
+            for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
+                const int k = tk[q];
+                if (k < 0 || tc[q] != best) continue;
+                if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
+                lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
+            }
+            cand = int(block_min_u64<kFusedThreads>(lbest, s_red64));
+        }
+        if (threadIdx.x == 0) {
+            lab_out[v] = is_active(v, key) ? cand : own;
+            if (cand != own) *flag_next = 1u;
+        }
+        __syncthreads();  // every read of the table is done
+        for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
+            tk[q] = -1;
+            tc[q] = 0;
+        }
+    }
+}
+
+// skip_fused: rows of tables up to kFusedCap slots are k_big_fused's.
+__global__ void k_big_decide(BigRows br, const int64_t* rowptr, const int32_t* lab_in, int32_t* lab_out,
+                             uint64_t key, const uint32_t* flag_prev, uint32_t* flag_next, bool skip_fused) {
     const bool converged = *flag_prev == 0;
     const int64_t len = *br.len;
     for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < len;
          idx += int64_t(gridDim.x) * blockDim.x) {
         const int64_t v = br.list[idx];
+        if (skip_fused && table_cap(rowptr[v + 1] - rowptr[v]) <= kFusedCap) continue;
         const int own = lab_in[v];
         if (converged) {
             lab_out[v] = own;
@@ -1191,6 +1264,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         }
         sr.first[kSmLists] = at;
     }
+    // rows whose count table is over kFusedCap slots (more than kFusedCap / 2 entries) take the chunked passes
+    const bool giant = info[2 * kClasses] + 1 > kFusedCap / 2;
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
     const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
     for (int t = 0; t < iters; ++t) {
@@ -1203,8 +1278,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
                 k_big_first<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, key);
                 k_big_first<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, key);
                 GT_LAUNCH_CHECK("reorder_big_first");
-                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, in, out, key, r.flags,
-                                                                              r.flags + 1);
+                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, rowptr, in, out, key, r.flags,
+                                                                              r.flags + 1, false);
                 GT_LAUNCH_CHECK("reorder_big_decide");
             }
             if (sr.first[kSmLists] > 0) {
@@ -1226,16 +1301,26 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         }
         if (n_huge > 0) {
             const uint32_t* fp = r.flags + t;
-            k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp);
-            GT_LAUNCH_CHECK("reorder_big_clear");
+            // the tables' first use clears them all; later, k_big_fused clears its own
+            if (t == 1 || giant) {
+                k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp, t == 1);
+                GT_LAUNCH_CHECK("reorder_big_clear");
+            }
             k_big_insert<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, in, fp);
             GT_LAUNCH_CHECK("reorder_big_insert");
-            k_big_reduce<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
-            k_big_reduce<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
-            k_big_reduce<2><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
-            GT_LAUNCH_CHECK("reorder_big_reduce");
-            k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, in, out, key, fp, r.flags + t + 1);
-            GT_LAUNCH_CHECK("reorder_big_decide");
+            k_big_fused<<<unsigned(n_huge < 2048 ? n_huge : 2048), kFusedThreads, 0, stream>>>(br, rowptr, in, out,
+                                                                                             key, fp,
+                                                                                             r.flags + t + 1);
+            GT_LAUNCH_CHECK("reorder_big_fused");
+            if (giant) {
+                k_big_reduce<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+                k_big_reduce<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+                k_big_reduce<2><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+                GT_LAUNCH_CHECK("reorder_big_reduce");
+                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, rowptr, in, out, key, fp,
+                                                                              r.flags + t + 1, true);
+                GT_LAUNCH_CHECK("reorder_big_decide");
+            }
         }
         if (sr.first[kSmLists] > 0) {
             k_lp_small<false><<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, in, out, key, r.flags + t,
