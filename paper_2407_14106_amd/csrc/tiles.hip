@@ -28,6 +28,15 @@ constexpr int kMaxR = 16384;
 constexpr int kMaxT = 128;
 constexpr int kRowsPerWave = kMaxT / (kTileThreads / kWave);  // rows of a tile row per wavefront
 constexpr int kCountBatch = 8;                                 // column loads in flight per thread when counting
+constexpr int kShortRow = kWave;  // rows of at most one slice of 64 edges stay in the tile row's workgroup
+constexpr int kMedBatch = 4;      // 64-edge slices of a medium row loaded at once
+// Tile rows of more than kHeavyEdges edges (hubs gathered by the reordering)
+// are counted before the tile-row pass by many workgroups, kHeavyChunk edges
+// each, into a count row of their own (at most kMaxHeavy of them; the rest
+// count in their own workgroup).
+constexpr int64_t kHeavyEdges = 32768;
+constexpr int kMaxHeavy = 64;
+constexpr int64_t kHeavyChunk = 65536;
 constexpr uint32_t kDense = 0x80000000u;
 
 // Exclusive prefix of a 0/1 flag over the workgroup, in thread order; *total = the sum.
@@ -85,7 +94,8 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
                                                     int32_t* tile_nnz, uint32_t* tile_mask,
                                                     const int64_t* sp_rowptr, int32_t* sp_col, uint32_t* tag,
                                                     uint32_t* row_of_e, int W, uint32_t* dense_bits,
-                                                    uint32_t* dense_pre, int32_t* sp_pos, int32_t* tile_pos) {
+                                                    uint32_t* dense_pre, int32_t* sp_pos, int32_t* tile_pos,
+                                                    const int32_t* heavy_slot, const uint32_t* heavy_cnt) {
     __shared__ uint32_t s_cnt[kMaxR];
     __shared__ int64_t s_red[kTileThreads / kWave];
     __shared__ int64_t s_rp[kMaxT + 1];
@@ -103,9 +113,27 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
     __syncthreads();
     const int64_t e0 = s_rp[0], e1 = s_rp[rows];
     const int tshift = __builtin_ctz(unsigned(T));
-    // every edge of the tile row, long rows included; kCountBatch loads in
-    // flight per thread, so a tile row holding hubs is not a chain of round trips
-    for (int64_t base = e0 + threadIdx.x; base < e1; base += kCountBatch * kTileThreads) {
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    // the columns of this wavefront's short rows (rows w, w + 16, ...), for the
+    // per-row pass at the end: loaded now, so they arrive while the tile row is counted
+    int first[kRowsPerWave];
+#pragma unroll
+    for (int k = 0; k < kRowsPerWave; ++k) {
+        const int64_t rl = w + int64_t(k) * (kTileThreads / kWave);
+        first[k] = 0;
+        if (rl < rows) {
+            const int64_t a = s_rp[rl], b = s_rp[rl + 1];
+            if (b - a <= kShortRow && a + lane < b) first[k] = col[a + lane];
+        }
+    }
+    // every edge of the tile row, long rows included (taken from the heavy
+    // count row if the tile row has one); kCountBatch loads in flight per
+    // thread, so a tile row holding hubs is not a chain of round trips
+    const int hslot = heavy_slot[I];
+    if (hslot >= 0)
+        for (int J = threadIdx.x; J < R; J += kTileThreads) s_cnt[J] = heavy_cnt[int64_t(hslot) * R + J];
+    for (int64_t base = e0 + threadIdx.x; hslot < 0 && base < e1; base += kCountBatch * kTileThreads) {
         int c[kCountBatch];
 #pragma unroll
         for (int u = 0; u < kCountBatch; ++u) {
@@ -121,8 +149,6 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
     // so LDS reads do not collide in banks); keep the count in the low bits and
     // each group's dense bits in s_gbits[m]
     const int ngroups = (R + kWave - 1) / kWave;
-    const int w = threadIdx.x / kWave;
-    const int lane = lane_id();
     const uint64_t lt = lanemask_lt();
     for (int m = w; m < ngroups; m += kTileThreads / kWave) {
         const int J = m * kWave + lane;
@@ -166,67 +192,211 @@ __global__ __launch_bounds__(kTileThreads) void k_tiles(int64_t n, const int64_t
         }
     }
     __syncthreads();
-    // per row: remainder degree and tags (count) or remainder edges and mask
-    // bits (fill).  Each wavefront takes rows w, w + 16, ... and loads the
-    // first 64 columns of all of them before handling any.
+    // per row of at most kShortRow edges: remainder degree and tags (count) or
+    // remainder edges and mask bits (fill), from the columns loaded at the
+    // start.  Longer rows are k_tiles_med's (up to kLongRow) or the long-row
+    // kernels'.
     const int wpr = T / 32;  // mask words per tile row
-    int first[kRowsPerWave];
-#pragma unroll
-    for (int k = 0; k < kRowsPerWave; ++k) {
-        const int64_t rl = w + int64_t(k) * (kTileThreads / kWave);
-        first[k] = 0;
-        if (rl < rows) {
-            const int64_t a = s_rp[rl], b = s_rp[rl + 1];
-            if (b - a <= kLongRow && a + lane < b) first[k] = col[a + lane];
-        }
-    }
 #pragma unroll
     for (int k = 0; k < kRowsPerWave; ++k) {
         const int64_t rl = w + int64_t(k) * (kTileThreads / kWave);
         if (rl >= rows) break;
         const int64_t i = r0 + rl;
         const int64_t a = s_rp[rl], b = s_rp[rl + 1];
-        if (b - a > kLongRow) {  // counted and written by the long-row kernels
-            if (!kFill && lane == 0) sp_deg[i] = 0;
+        if (b - a > kShortRow) {
+            if (!kFill && lane == 0 && b - a > kLongRow) sp_deg[i] = 0;  // the long-row kernels add theirs
             continue;
         }
-        int64_t sp = 0;
-        for (int64_t eb = a; eb < b; eb += kWave) {
-            const int64_t e = eb + lane;
-            const bool valid = e < b;
-            const int c = !valid ? 0 : (eb == a ? first[k] : col[e]);
-            const int J = c >> tshift;
-            const uint32_t f = valid ? s_cnt[J] : 0u;
-            const bool dense = valid && (f & kDense);
-            const bool sparse = valid && !dense;
-            const uint64_t sb = ballot(sparse);
-            if (kFill) {
-                if (dense) {
-                    const int64_t kk = tile_rowptr[I] + int64_t(f & ~kDense);
-                    const int cl = c - J * T;
-                    const int64_t word = kk * int64_t(T) * wpr + rl * wpr + cl / 32;
-                    atomicOr(&tile_mask[word], 1u << (cl & 31));
-                    // the row's first edge in this tile (its columns are sorted)
-                    if (tile_pos && (e == a || (col[e - 1] >> tshift) != J))
-                        tile_pos[kk * T + rl] = int32_t(e);
-                }
-                if (sparse) {
-                    const int64_t pos = s_sp[rl] + sp + __popcll(sb & lt);
-                    sp_col[pos] = c;
-                    if (sp_pos) sp_pos[pos] = int32_t(e);
-                }
-            } else if (valid) {
+        const int64_t e = a + lane;
+        const bool valid = e < b;
+        const int c = first[k];
+        const int J = c >> tshift;
+        const uint32_t f = valid ? s_cnt[J] : 0u;
+        const bool dense = valid && (f & kDense);
+        const bool sparse = valid && !dense;
+        const uint64_t sb = ballot(sparse);
+        if (kFill) {
+            if (dense) {
+                const int64_t kk = tile_rowptr[I] + int64_t(f & ~kDense);
+                const int cl = c - J * T;
+                const int64_t word = kk * int64_t(T) * wpr + rl * wpr + cl / 32;
+                atomicOr(&tile_mask[word], 1u << (cl & 31));
+                // the row's first edge in this tile (its columns are sorted)
+                if (tile_pos && (e == a || (col[e - 1] >> tshift) != J)) tile_pos[kk * T + rl] = int32_t(e);
+            }
+            if (sparse) {
+                const int64_t pos = s_sp[rl] + __popcll(sb & lt);
+                sp_col[pos] = c;
+                if (sp_pos) sp_pos[pos] = int32_t(e);
+            }
+        } else {
+            if (valid) {
                 tag[e] = sparse ? uint32_t(c) : uint32_t(n);
                 row_of_e[e] = uint32_t(i);
             }
-            sp += __popcll(sb);
+            if (lane == 0) sp_deg[i] = int32_t(__popcll(sb));
         }
-        if (!kFill && lane == 0) sp_deg[i] = int32_t(sp);
+    }
+}
+
+// One workgroup: the heavy tile rows (more than kHeavyEdges edges), the first
+// kMaxHeavy of them in order: heavy_slot[I] = their number (else -1),
+// heavy_list[h] = the tile row of number h, *heavy_n = how many.
+// Thread t takes tile rows [kSlotsPer t, kSlotsPer t + kSlotsPer), all loaded at once.
+constexpr int kSlotsPer = kMaxR / kTileThreads;
+__global__ __launch_bounds__(kTileThreads) void k_heavy_slots(int64_t n, const int64_t* rowptr, int T, int R,
+                                                              int32_t* heavy_slot, int32_t* heavy_list,
+                                                              int32_t* heavy_n) {
+    __shared__ int64_t s_red[kTileThreads / kWave];
+    const int I0 = threadIdx.x * kSlotsPer;
+    int64_t at[kSlotsPer + 1];
+#pragma unroll
+    for (int k = 0; k <= kSlotsPer; ++k) {
+        const int64_t r = int64_t(I0 + k) * T;
+        at[k] = I0 + k <= R ? rowptr[r < n ? r : n] : 0;
+    }
+    uint32_t heavy = 0;
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kSlotsPer; ++k)
+        if (I0 + k < R && at[k + 1] - at[k] > kHeavyEdges) {
+            heavy |= 1u << k;
+            ++cnt;
+        }
+    int64_t tot;
+    int64_t pre = block_exscan_i64(cnt, s_red, &tot);
+#pragma unroll
+    for (int k = 0; k < kSlotsPer; ++k) {
+        const int I = I0 + k;
+        if (I >= R) break;
+        const bool kept = ((heavy >> k) & 1u) && pre < kMaxHeavy;
+        heavy_slot[I] = kept ? int32_t(pre) : -1;
+        if (kept) heavy_list[pre] = I;
+        if ((heavy >> k) & 1u) ++pre;
+    }
+    if (threadIdx.x == 0) *heavy_n = int32_t(tot < kMaxHeavy ? tot : kMaxHeavy);
+}
+
+// The heavy tile rows' edges in chunks of kHeavyChunk, dealt over the grid:
+// each chunk counted per tile column in LDS, then added to its tile row's
+// count row (which starts at zero).
+__global__ __launch_bounds__(kTileThreads) void k_heavy_count(int64_t n, const int64_t* rowptr, const int32_t* col,
+                                                              int T, int R, const int32_t* heavy_list,
+                                                              const int32_t* heavy_n, uint32_t* heavy_cnt) {
+    __shared__ uint32_t s_cnt[kMaxR];
+    const int nh = *heavy_n;
+    const int tshift = __builtin_ctz(unsigned(T));
+    int64_t q0 = 0;  // chunks of the heavy rows before h
+    for (int h = 0; h < nh; ++h) {
+        const int64_t I = heavy_list[h];
+        const int64_t r0 = I * T, r1 = r0 + T < n ? r0 + T : n;
+        const int64_t E0 = rowptr[r0], E1 = rowptr[r1];
+        const int64_t nch = cdiv(E1 - E0, kHeavyChunk);
+        // this workgroup's chunks of row h: global numbers q0 + j with (q0 + j) % grid == block
+        int64_t j = (int64_t(blockIdx.x) - q0 % gridDim.x + gridDim.x) % gridDim.x;
+        for (; j < nch; j += gridDim.x) {
+            for (int J = threadIdx.x; J < R; J += kTileThreads) s_cnt[J] = 0;
+            __syncthreads();
+            const int64_t c0 = E0 + j * kHeavyChunk, c1 = c0 + kHeavyChunk < E1 ? c0 + kHeavyChunk : E1;
+            for (int64_t base = c0 + threadIdx.x; base < c1; base += kCountBatch * kTileThreads) {
+                int c[kCountBatch];
+#pragma unroll
+                for (int u = 0; u < kCountBatch; ++u) {
+                    const int64_t e = base + int64_t(u) * kTileThreads;
+                    c[u] = e < c1 ? col[e] : -1;
+                }
+#pragma unroll
+                for (int u = 0; u < kCountBatch; ++u)
+                    if (c[u] >= 0) atomicAdd(&s_cnt[c[u] >> tshift], 1u);
+            }
+            __syncthreads();
+            for (int J = threadIdx.x; J < R; J += kTileThreads)
+                if (s_cnt[J]) atomicAdd(&heavy_cnt[int64_t(h) * R + J], s_cnt[J]);
+            __syncthreads();
+        }
+        q0 += nch;
     }
 }
 
 __device__ __forceinline__ bool tile_is_dense(const uint32_t* __restrict__ bits, int J) {
     return (bits[J >> 5] >> (J & 31)) & 1u;
+}
+
+// Rows of kShortRow + 1 to kLongRow edges: class 0 of the medium-row list.
+__global__ void k_med_class(int64_t n, const int64_t* rowptr, int8_t* cls) {
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t d = rowptr[i + 1] - rowptr[i];
+        cls[i] = (d > kShortRow && d <= kLongRow) ? int8_t(0) : int8_t(-1);
+    }
+}
+
+// One wavefront per listed medium row, its slices of 64 edges kMedBatch at a
+// time: the dense test and the tile's number come from the count pass's bit
+// sets (dense_bits, dense_pre).  kFill = false: remainder degree and tags;
+// true: remainder edges, mask bits and edge positions.
+template <bool kFill>
+__global__ __launch_bounds__(256) void k_tiles_med(int64_t n, const int32_t* list, const int64_t* list_len,
+                                                   const int64_t* rowptr, const int32_t* col, int T, int W,
+                                                   const uint32_t* dense_bits, const uint32_t* dense_pre,
+                                                   int32_t* sp_deg, uint32_t* tag, uint32_t* row_of_e,
+                                                   const int64_t* tile_rowptr, uint32_t* tile_mask,
+                                                   const int64_t* sp_rowptr, int32_t* sp_col, int32_t* sp_pos,
+                                                   int32_t* tile_pos) {
+    const int lane = lane_id();
+    const uint64_t lt = lanemask_lt();
+    const int tshift = __builtin_ctz(unsigned(T));
+    const int wpr = T / 32;
+    const int64_t len = *list_len;
+    const int64_t waves = int64_t(gridDim.x) * 4;
+    for (int64_t idx = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; idx < len; idx += waves) {
+        const int64_t i = list[idx];
+        const int64_t I = i / T, rl = i - I * T;
+        const uint32_t* bits = dense_bits + I * W;
+        const uint32_t* pre = dense_pre + I * W;
+        const int64_t a = rowptr[i], b = rowptr[i + 1];
+        int64_t sp = kFill ? sp_rowptr[i] : 0;
+        const int64_t tbase = kFill ? tile_rowptr[I] : 0;
+        for (int64_t eb0 = a; eb0 < b; eb0 += kMedBatch * kWave) {
+            int cb[kMedBatch];
+#pragma unroll
+            for (int u = 0; u < kMedBatch; ++u) {
+                const int64_t e = eb0 + u * kWave + lane;
+                cb[u] = e < b ? col[e] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kMedBatch; ++u) {
+                const int64_t eb = eb0 + u * kWave;
+                if (eb >= b) break;
+                const int64_t e = eb + lane;
+                const bool valid = e < b;
+                const int c = cb[u];
+                const int J = c >> tshift;
+                const uint32_t wd = valid ? bits[J >> 5] : 0u;
+                const bool dense = valid && ((wd >> (J & 31)) & 1u);
+                const bool sparse = valid && !dense;
+                const uint64_t sb = ballot(sparse);
+                if (kFill) {
+                    if (dense) {
+                        const int64_t kk = tbase + pre[J >> 5] + __popc(wd & ((1u << (J & 31)) - 1u));
+                        const int cl = c - J * T;
+                        atomicOr(&tile_mask[kk * int64_t(T) * wpr + rl * wpr + cl / 32], 1u << (cl & 31));
+                        if (tile_pos && (e == a || (col[e - 1] >> tshift) != J))
+                            tile_pos[kk * T + rl] = int32_t(e);
+                    }
+                    if (sparse) {
+                        const int64_t pos = sp + __popcll(sb & lt);
+                        sp_col[pos] = c;
+                        if (sp_pos) sp_pos[pos] = int32_t(e);
+                    }
+                } else if (valid) {
+                    tag[e] = sparse ? uint32_t(c) : uint32_t(n);
+                    row_of_e[e] = uint32_t(i);
+                }
+                sp += __popcll(sb);
+            }
+        }
+        if (!kFill && lane == 0) sp_deg[i] = int32_t(sp);
+    }
 }
 
 // Count pass of the long rows: remainder degree (added to the zero the tile
@@ -397,9 +567,17 @@ struct TilesWs {
     int64_t* long_col_pos;
     uint32_t* dense_bits;  // [R, W]: the dense/sparse split of each tile row
     uint32_t* dense_pre;   // [R, W]: dense tiles before each word
+    int32_t* heavy_slot;   // [R]: the heavy count row of each tile row, or -1
+    int32_t* heavy_list;   // [kMaxHeavy]: the tile row of each heavy count row
+    int32_t* heavy_n;      // how many heavy count rows
+    uint32_t* heavy_cnt;   // [kMaxHeavy, R]: edges of each heavy tile row per tile column
     uint32_t* rows;        // [nnz]: the row of each edge, then (sorted with the tags) the remainder transpose's rows
     const uint64_t* kept_begin;
     int64_t kept_words;    // 8-byte words of the count results' range
+    int8_t* med_cls;       // [n]: medium-row class of each row
+    int32_t* med_list;     // [n]: the medium rows
+    int64_t* med_info;     // [2]: their list start and number
+    PartitionTmp part;
     int32_t* segcnt;       // [2 * long chunks]: remainder edges of each long-row segment
     int64_t* segoff;       // [2 * long chunks + 1]
     int W;
@@ -428,6 +606,10 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
     t.long_col_pos = ws.take<int64_t>(n1 + 1);
     t.dense_bits = ws.take<uint32_t>(size_t(R * t.W));
     t.dense_pre = ws.take<uint32_t>(size_t(R * t.W));
+    t.heavy_slot = ws.take<int32_t>(size_t(R));
+    t.heavy_list = ws.take<int32_t>(size_t(kMaxHeavy));
+    t.heavy_n = ws.take<int32_t>(2);
+    t.heavy_cnt = ws.take<uint32_t>(size_t(kMaxHeavy) * R);
     t.rows = ws.take<uint32_t>(size_t(e1 + (e1 & 1)));  // an even count: the range ends on an 8-byte word
     {
         const char* b = reinterpret_cast<const char*>(t.dense_per_tilerow);
@@ -435,6 +617,10 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
         t.kept_begin = reinterpret_cast<const uint64_t*>(t.dense_per_tilerow);
         t.kept_words = int64_t((e - b) / 8);
     }
+    t.med_cls = ws.take<int8_t>(n1);
+    t.med_list = ws.take<int32_t>(n1);
+    t.med_info = ws.take<int64_t>(2);
+    t.part = partition_tmp(ws, n1);
     const int64_t segs = 2 * long_chunks_of(e1);
     t.segcnt = ws.take<int32_t>(size_t(segs));
     t.segoff = ws.take<int64_t>(size_t(segs + 1));
@@ -532,14 +718,32 @@ inline unsigned long_grid(int64_t nnz) {
     return unsigned(c < 8192 ? c : 8192);
 }
 
+// The list of rows of kShortRow + 1 to kLongRow edges (its length on the device, in med_info[1]).
+gt_status medium_rows(int64_t n, const int64_t* rowptr, TilesWs& t, hipStream_t stream) {
+    k_med_class<<<grid_for(n, 256, 8192), 256, 0, stream>>>(n, rowptr, t.med_cls);
+    GT_LAUNCH_CHECK("tiles_medium_class");
+    return partition_rows(t.med_cls, n, 1, t.med_list, t.med_info, t.part, stream);
+}
+
 gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T, uint32_t tau_ppm,
                      TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, hipStream_t stream) {
     gt_status st;
     const int R = int(cdiv(n, T));
+    k_heavy_slots<<<1, kTileThreads, 0, stream>>>(n, rowptr, T, R, t.heavy_slot, t.heavy_list, t.heavy_n);
+    GT_LAUNCH_CHECK("tiles_heavy_slots");
+    if ((st = fill_u32(t.heavy_cnt, int64_t(kMaxHeavy) * R, 0u, stream)) != GT_OK) return st;
+    k_heavy_count<<<1024, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, t.heavy_list, t.heavy_n, t.heavy_cnt);
+    GT_LAUNCH_CHECK("tiles_heavy_count");
     k_tiles<false><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg,
                                                    nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, t.tag,
-                                                   t.rows, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr);
+                                                   t.rows, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr,
+                                                   t.heavy_slot, t.heavy_cnt);
     GT_LAUNCH_CHECK("tiles_count");
+    if ((st = medium_rows(n, rowptr, t, stream)) != GT_OK) return st;
+    k_tiles_med<false><<<grid_for(n, 4, 16384), 256, 0, stream>>>(
+        n, t.med_list, t.med_info + 1, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.sp_deg, t.tag, t.rows,
+        nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    GT_LAUNCH_CHECK("tiles_count_medium");
     if (nnz > kLongRow) {
         k_tiles_long_count<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
                                                                    t.sp_deg, t.tag, t.rows);
@@ -674,8 +878,13 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     k_tiles<true><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
                                               plan->tile_col, plan->tile_nnz, plan->tile_mask, plan->sp_rowptr,
                                               plan->sp_col, nullptr, nullptr, t.W, nullptr, nullptr, plan->sp_pos,
-                                              plan->tile_pos);
+                                              plan->tile_pos, t.heavy_slot, t.heavy_cnt);
     GT_LAUNCH_CHECK("tiles_fill");
+    if (reuse && (st = medium_rows(n, rowptr, t, stream)) != GT_OK) return st;  // else the count pass made it
+    k_tiles_med<true><<<grid_for(n, 4, 16384), 256, 0, stream>>>(
+        n, t.med_list, t.med_info + 1, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr, nullptr,
+        plan->tile_rowptr, plan->tile_mask, plan->sp_rowptr, plan->sp_col, plan->sp_pos, plan->tile_pos);
+    GT_LAUNCH_CHECK("tiles_fill_medium");
     if (nnz > kLongRow) {
         const int64_t segs = 2 * long_chunks_of(nnz);
         if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.segcnt), segs, 0u, stream)) != GT_OK) return st;
