@@ -291,20 +291,23 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     PermuteWs p = carve(ws, n, nnz, with_map);
     gt_status st;
     if (n == 0) return fill_i64(rowptr_out, 1, 0, stream);
+    // the CSR check is read back with the class sizes below: nothing before that reads col
     if ((st = launch_validate_csr(n, nnz, rowptr, col, p.flags, stream)) != GT_OK) return st;
-    if ((st = read_validation(p.flags, stream)) != GT_OK) return st;
     const unsigned g = grid_for(n, 256, 8192);
     k_new_degrees<<<g, 256, 0, stream>>>(n, rowptr, perm, p.deg_new, p.cls, p.sdeg);
     GT_LAUNCH_CHECK("permute_degrees");
     if ((st = exclusive_scan_i64(p.deg_new, n, rowptr_out, p.scan, stream)) != GT_OK) return st;
-    if (nnz == 0) return GT_OK;
+    if (nnz == 0) return read_validation(p.flags, stream);
     // the rows of more than kShortRow entries go to the radix sort: their offsets there
     if ((st = exclusive_scan_i64(p.sdeg, n, p.soff, p.scan, stream)) != GT_OK) return st;
     if ((st = partition_rows(p.cls, n, kRlClasses, p.list, p.info, p.part, stream)) != GT_OK) return st;
     int64_t info[2 * kRlClasses + 1] = {};
+    uint32_t vflags = 0;
     GT_HIP(hipMemcpyAsync(info, p.info, 2 * kRlClasses * 8, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipMemcpyAsync(info + 2 * kRlClasses, p.soff + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipMemcpyAsync(&vflags, p.flags, 4, hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
+    if ((st = validation_result(vflags)) != GT_OK) return st;
     const int64_t m = info[2 * kRlClasses];
     {
         // the short-row lists in one launch, largest rows first, blocks in proportion to their rows

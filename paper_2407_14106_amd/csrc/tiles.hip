@@ -635,13 +635,22 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
 // The wavefront sums meet in LDS, so each workgroup adds one value to the
 // total (a few hundred atomics on one address instead of one per wavefront).
 constexpr int kCsumBlocks = 512;
+constexpr int kCsumBatch = 8;
 __global__ __launch_bounds__(256) void k_ws_checksum(const uint64_t* __restrict__ p, int64_t words,
                                                      unsigned long long* __restrict__ out) {
     __shared__ uint64_t s_part[256 / kWave];
     uint64_t acc = 0;
     const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < words; i += stride)
-        acc += mix64(p[i] + uint64_t(i) * 0x9E3779B97F4A7C15ull);
+    // kCsumBatch words in flight per thread
+    int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    for (; i + (kCsumBatch - 1) * stride < words; i += kCsumBatch * stride) {
+        uint64_t x[kCsumBatch];
+#pragma unroll
+        for (int k = 0; k < kCsumBatch; ++k) x[k] = p[i + k * stride];
+#pragma unroll
+        for (int k = 0; k < kCsumBatch; ++k) acc += mix64(x[k] + uint64_t(i + k * stride) * 0x9E3779B97F4A7C15ull);
+    }
+    for (; i < words; i += stride) acc += mix64(p[i] + uint64_t(i) * 0x9E3779B97F4A7C15ull);
 #pragma unroll
     for (int o = kWave / 2; o > 0; o >>= 1) {
         const uint32_t lo = __shfl_xor(uint32_t(acc), o, kWave), hi = __shfl_xor(uint32_t(acc >> 32), o, kWave);
