@@ -7,15 +7,20 @@
 //                      lanes each;
 //   32 < deg <= 64     one wavefront per row; one neighbour label per lane,
 //                      multiplicities by an all-pairs compare (readlane).
+//                      These five classes run in one launch.
 //   64 < deg <= 512    one wavefront per row, open-addressing count table in
 //                      the wavefront's share of LDS (no workgroup barriers).
 //   512 < deg <= 4096  one workgroup per row, open-addressing count table in LDS.
 //   deg > 4096         the whole grid (hubs, a global token attending to every
 //                      node): each row's count table in the workspace, filled
-//                      chunk by chunk by every workgroup, then reduced by every
+//                      chunk by chunk by every workgroup, then, for tables of up
+//                      to 64K slots, reduced, decided and cleared by one
+//                      workgroup per row; larger tables are reduced by every
 //                      workgroup in three passes (best count, smallest hash,
 //                      smallest label).
-// All three compute the same function of the neighbour-label multiset.
+// All compute the same function of the neighbour-label multiset.  The first
+// sweep, whose labels are the node ids, reduces to a minimum over each row's
+// columns and uses none of the tables.
 #include <limits.h>
 
 #include "prim.h"
