@@ -452,8 +452,11 @@ def main():
     pre, pre_first = {}, {}
 
     def timed(name, fn):
-        # first call (includes the binding's first workspace allocations), then a warm call that is reported
+        # first call (includes the binding's first workspace and output allocations), then a warm call that is
+        # reported; the first call's outputs are released before it, so its outputs reuse their memory
+        out = None
         for rec in (pre_first, pre):
+            out = None
             a, b = ev(), ev()
             a.record()
             out = fn()

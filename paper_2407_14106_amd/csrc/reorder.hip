@@ -722,13 +722,19 @@ struct BigRows {
     const int64_t* off;   // table offset of each listed row
     const int64_t* echunk;  // [listed rows + 1]: first edge chunk of each row (kBigEdgeChunk edges per chunk)
     const int64_t* schunk;  // [listed rows + 1]: first table-slot chunk of each row (kSlotChunk slots per chunk)
-    int* keys;
-    int* cnts;
+    unsigned long long* tab;  // count tables: slot = label << 32 | count, kSlotEmpty when free
     int* best;            // [listed rows]
     int* own_cnt;
     unsigned long long* hbest;
     unsigned long long* lbest;
 };
+
+// A slot of the very long rows' count tables holds its label in the high and
+// its count in the low 32 bits, so claiming a free slot and counting the
+// first occurrences take one atomic.
+constexpr unsigned long long kSlotEmpty = 0xFFFFFFFF00000000ull;  // label -1, count 0
+__device__ __forceinline__ int slot_label(unsigned long long e) { return int(uint32_t(e >> 32)); }
+__device__ __forceinline__ int slot_count(unsigned long long e) { return int(uint32_t(e)); }
 
 __device__ __forceinline__ int64_t table_cap(int64_t deg) {
     int64_t cap = 1;
@@ -835,13 +841,9 @@ __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t*
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
         if (!all && cap <= kFusedCap) continue;
         const int64_t j = c - br.schunk[idx];
-        int* tk = br.keys + br.off[idx];
-        int* tc = br.cnts + br.off[idx];
+        unsigned long long* tab = br.tab + br.off[idx];
         const int64_t s1 = (j + 1) * kSlotChunk < cap ? (j + 1) * kSlotChunk : cap;
-        for (int64_t s = j * kSlotChunk + threadIdx.x; s < s1; s += kBlock) {
-            tk[s] = -1;
-            tc[s] = 0;
-        }
+        for (int64_t s = j * kSlotChunk + threadIdx.x; s < s1; s += kBlock) tab[s] = kSlotEmpty;
     }
     const int64_t stride = int64_t(gridDim.x) * kBlock, start = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     for (int64_t idx = start; idx < len; idx += stride) {
@@ -869,8 +871,7 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         const int64_t cap = table_cap(b - a);
         const int64_t j = c - br.echunk[idx];
-        int* tk = br.keys + br.off[idx];
-        int* tc = br.cnts + br.off[idx];
+        unsigned long long* tab = br.tab + br.off[idx];
         for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) {
             s_keys[x] = -1;
             s_cnts[x] = 0;
@@ -888,11 +889,13 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
         for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) {
             const int L = s_keys[x];
             if (L < 0) continue;
+            const unsigned long long mine = (uint64_t(uint32_t(L)) << 32) | uint32_t(s_cnts[x]);
             int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
             while (true) {
-                const int prev = atomicCAS(&tk[slot], -1, L);
-                if (prev == -1 || prev == L) {
-                    atomicAdd(&tc[slot], s_cnts[x]);
+                const unsigned long long prev = atomicCAS(&tab[slot], kSlotEmpty, mine);
+                if (prev == kSlotEmpty) break;  // claimed with the count
+                if (slot_label(prev) == L) {
+                    atomicAdd(&tab[slot], (unsigned long long)uint32_t(s_cnts[x]));
                     break;
                 }
                 slot = (slot + 1) & (cap - 1);
@@ -922,14 +925,14 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
         const int64_t j = c - br.schunk[idx];
         const int64_t s0 = j * kSlotChunk, s1 = (j + 1) * kSlotChunk < cap ? (j + 1) * kSlotChunk : cap;
         const int own = lab_in[v];
-        const int* tk = br.keys + br.off[idx];
-        const int* tc = br.cnts + br.off[idx];
+        const unsigned long long* tab = br.tab + br.off[idx];
         if (kPass == 0) {
             int best = 0, oc = 0;
             for (int64_t s = s0 + threadIdx.x; s < s1; s += kBlock) {
-                const int k = tk[s];
+                const unsigned long long en = tab[s];
+                const int k = slot_label(en);
                 if (k < 0) continue;
-                const int cnt = tc[s];
+                const int cnt = slot_count(en);
                 best = cnt > best ? cnt : best;
                 if (k == own) oc = cnt;
             }
@@ -945,8 +948,9 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
             const uint64_t hb = kPass == 2 ? br.hbest[idx] : 0;
             uint64_t r = ~0ull;
             for (int64_t s = s0 + threadIdx.x; s < s1; s += kBlock) {
-                const int k = tk[s];
-                if (k < 0 || tc[s] != best) continue;
+                const unsigned long long en = tab[s];
+                const int k = slot_label(en);
+                if (k < 0 || slot_count(en) != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 if (kPass == 1) r = h < r ? h : r;
                 else if (h == hb) r = uint64_t(uint32_t(k)) < r ? uint64_t(uint32_t(k)) : r;
@@ -976,13 +980,13 @@ __global__ __launch_bounds__(kFusedThreads) void k_big_fused(BigRows br, const i
             if (threadIdx.x == 0) lab_out[v] = own;
             continue;
         }
-        int* tk = br.keys + br.off[idx];
-        int* tc = br.cnts + br.off[idx];
+        unsigned long long* tab = br.tab + br.off[idx];
         int best = 0, own_cnt = 0;
         for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
-            const int k = tk[q];
+            const unsigned long long en = tab[q];
+            const int k = slot_label(en);
             if (k < 0) continue;
-            const int c = tc[q];
+            const int c = slot_count(en);
             best = c > best ? c : best;
             if (k == own) own_cnt = c;
         }
@@ -992,16 +996,18 @@ __global__ __launch_bounds__(kFusedThreads) void k_big_fused(BigRows br, const i
         if (best > 0 && own_cnt != best) {
             uint64_t hbest = ~0ull;
             for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
-                const int k = tk[q];
-                if (k < 0 || tc[q] != best) continue;
+                const unsigned long long en = tab[q];
+                const int k = slot_label(en);
+                if (k < 0 || slot_count(en) != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 hbest = h < hbest ? h : hbest;
             }
             hbest = block_min_u64<kFusedThreads>(hbest, s_red64);
             uint64_t lbest = ~0ull;
             for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
-                const int k = tk[q];
-                if (k < 0 || tc[q] != best) continue;
+                const unsigned long long en = tab[q];
+                const int k = slot_label(en);
+                if (k < 0 || slot_count(en) != best) continue;
                 if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
                 lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
             }
@@ -1012,10 +1018,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_big_fused(BigRows br, const i
             if (cand != own) *flag_next = 1u;
         }
         __syncthreads();  // every read of the table is done
-        for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) {
-            tk[q] = -1;
-            tc[q] = 0;
-        }
+        for (int64_t q = threadIdx.x; q < cap; q += kFusedThreads) tab[q] = kSlotEmpty;
     }
 }
 
@@ -1127,8 +1130,7 @@ struct ReorderWs {
     int64_t* huge_off;
     int64_t* huge_echunk;
     int64_t* huge_schunk;
-    int* tab_keys;
-    int* tab_cnts;
+    unsigned long long* tab;
     int* big_best;
     int* big_own;
     unsigned long long* big_hbest;
@@ -1162,8 +1164,7 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.huge_echunk = ws.take<int64_t>(n1 + 1);
     r.huge_schunk = ws.take<int64_t>(n1 + 1);
     const int64_t tab = 4 * (nnz > 0 ? nnz : 1);  // sum over big rows of cap <= 4 * deg
-    r.tab_keys = ws.take<int>(size_t(tab));
-    r.tab_cnts = ws.take<int>(size_t(tab));
+    r.tab = ws.take<unsigned long long>(size_t(tab));
     r.big_best = ws.take<int>(n1);
     r.big_own = ws.take<int>(n1);
     r.big_hbest = ws.take<unsigned long long>(n1);
@@ -1240,8 +1241,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         len_of[c] = r.class_info + kClasses + c;
     }
     const int64_t n_huge = cnt[kClsHuge];
-    BigRows br{list_of[kClsHuge], len_of[kClsHuge], r.huge_off, r.huge_echunk, r.huge_schunk, r.tab_keys,
-               r.tab_cnts, r.big_best, r.big_own, r.big_hbest, r.big_lbest};
+    BigRows br{list_of[kClsHuge], len_of[kClsHuge], r.huge_off, r.huge_echunk, r.huge_schunk, r.tab,
+               r.big_best, r.big_own, r.big_hbest, r.big_lbest};
     if (n_huge > 0) {  // the chunk numbering of the long rows' edges and table slots, and their table offsets
         k_big_prep<<<1, kPrepThreads, 0, stream>>>(list_of[kClsHuge], len_of[kClsHuge], rowptr, r.huge_echunk,
                                                     r.huge_schunk, r.huge_off);
