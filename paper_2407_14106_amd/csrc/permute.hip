@@ -139,6 +139,14 @@ __global__ __launch_bounds__(256) void k_relabel_short(ShortLists sl, const int6
     }
 }
 
+// The sorted rows' entry count and the CSR check's flags, after the class
+// starts and sizes, so that one copy brings all of them to the host.
+__global__ void k_host_words(const int64_t* sorted, const uint32_t* flags, int64_t* out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    out[0] = *sorted;
+    out[1] = int64_t(*flags);
+}
+
 // Keys of the listed rows (kShortRow + 1 to kLongRow entries), one wavefront
 // per new row, at the row's offset soff[r] among the sorted rows' entries; for
 // the edge map, the old CSR position as the value.
@@ -246,7 +254,7 @@ struct PermuteWs {
     int64_t* deg_new;
     int8_t* cls;      // [n]: the relabelling class of each new row
     int32_t* list;    // [n]: the new rows by class
-    int64_t* info;    // [2 * kRlClasses + 1]: class starts and sizes; the sorted entries
+    int64_t* info;    // [2 * kRlClasses + 2]: class starts and sizes; the sorted entries; the CSR check
     PartitionTmp part;
     int64_t* sdeg;  // entries of each new row that go to the radix sort
     int64_t* soff;  // [n + 1]: their exclusive scan
@@ -263,7 +271,7 @@ PermuteWs carve(Ws& ws, int64_t n, int64_t nnz, bool with_map) {
     p.deg_new = ws.take<int64_t>(n1);
     p.cls = ws.take<int8_t>(n1);
     p.list = ws.take<int32_t>(n1);
-    p.info = ws.take<int64_t>(2 * kRlClasses + 1);
+    p.info = ws.take<int64_t>(2 * kRlClasses + 2);
     p.part = partition_tmp(ws, n1);
     p.sdeg = ws.take<int64_t>(n1);
     p.soff = ws.take<int64_t>(n1 + 1);
@@ -301,13 +309,12 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     // the rows of more than kShortRow entries go to the radix sort: their offsets there
     if ((st = exclusive_scan_i64(p.sdeg, n, p.soff, p.scan, stream)) != GT_OK) return st;
     if ((st = partition_rows(p.cls, n, kRlClasses, p.list, p.info, p.part, stream)) != GT_OK) return st;
-    int64_t info[2 * kRlClasses + 1] = {};
-    uint32_t vflags = 0;
-    GT_HIP(hipMemcpyAsync(info, p.info, 2 * kRlClasses * 8, hipMemcpyDeviceToHost, stream));
-    GT_HIP(hipMemcpyAsync(info + 2 * kRlClasses, p.soff + n, 8, hipMemcpyDeviceToHost, stream));
-    GT_HIP(hipMemcpyAsync(&vflags, p.flags, 4, hipMemcpyDeviceToHost, stream));
+    k_host_words<<<1, 64, 0, stream>>>(p.soff + n, p.flags, p.info + 2 * kRlClasses);
+    GT_LAUNCH_CHECK("permute_host_words");
+    int64_t info[2 * kRlClasses + 2] = {};
+    GT_HIP(hipMemcpyAsync(info, p.info, sizeof(info), hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
-    if ((st = validation_result(vflags)) != GT_OK) return st;
+    if ((st = validation_result(uint32_t(info[2 * kRlClasses + 1]))) != GT_OK) return st;
     const int64_t m = info[2 * kRlClasses];
     {
         // the short-row lists in one launch, largest rows first, blocks in proportion to their rows

@@ -549,8 +549,9 @@ constexpr int kRecordWords = 8;
 
 struct TilesWs {
     uint32_t* flags;
-    unsigned long long* csum;  // checksum of the count results (kept below)
+    unsigned long long* csum;  // checksum of the count results (kept below); right after the record
     uint64_t* record;          // [kRecordWords]: what gt_tiles_count left here (CountRecord)
+    int64_t* sizes;            // [4]: dense tiles, remainder edges, long rows, long columns
     uint32_t* tag;             // [nnz]: remainder tags (column, or n), sorted by the count pass
     uint32_t* counts;          // per tile column
     // The count results, one contiguous range of the workspace (kept_words
@@ -590,8 +591,10 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
     const int64_t n1 = n > 0 ? n : 1, e1 = nnz > 0 ? nnz : 1;
     const int64_t R = cdiv(n1, T > 0 ? T : 1);
     t.flags = ws.take<uint32_t>(1);
-    t.csum = ws.take<unsigned long long>(1);
-    t.record = ws.take<uint64_t>(kRecordWords);
+    // the record, then the checksum, then the plan sizes: read back with one copy each
+    t.record = ws.take<uint64_t>(kRecordWords + 1 + 4);
+    t.csum = reinterpret_cast<unsigned long long*>(t.record + kRecordWords);
+    t.sizes = reinterpret_cast<int64_t*>(t.record + kRecordWords + 1);
     t.W = int(cdiv(R, 32));
     t.tag = ws.take<uint32_t>(e1);
     t.counts = ws.take<uint32_t>(n1 + 1);
@@ -684,6 +687,16 @@ constexpr uint64_t kRecordTag = 0x67745F74696C6573ull;
 struct CountRecord {
     uint64_t w[kRecordWords];  // tag, n, nnz, rowptr, col, T << 32 | tau_ppm, checksum, unused
 };
+
+// The plan's four sizes, next to each other for one copy to the host.
+__global__ void k_plan_sizes(const int64_t* tile_rowptr_end, const int64_t* sp_rowptr_end,
+                             const int64_t* long_row_end, const int64_t* long_col_end, int64_t* sizes) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    sizes[0] = *tile_rowptr_end;
+    sizes[1] = *sp_rowptr_end;
+    sizes[2] = *long_row_end;
+    sizes[3] = *long_col_end;
+}
 
 __global__ void k_put_record(uint64_t* __restrict__ rec, int64_t n, int64_t nnz, const int64_t* rowptr,
                              const int32_t* col, int32_t T, uint32_t tau_ppm, const unsigned long long* __restrict__ sum) {
@@ -806,11 +819,11 @@ extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowpt
     k_put_record<<<1, 64, 0, stream>>>(t.record, n, nnz, rowptr, col, T, tau_ppm, t.csum);
     GT_LAUNCH_CHECK("tiles_count_record");
     const int64_t R = plan->n_row_tiles;
+    k_plan_sizes<<<1, 64, 0, stream>>>(t.tmp_tile_rowptr + R, t.tmp_sp_rowptr + n, t.long_row_pos + n,
+                                       t.long_col_pos + n, t.sizes);
+    GT_LAUNCH_CHECK("tiles_sizes");
     int64_t h[4] = {0, 0, 0, 0};
-    GT_HIP(hipMemcpyAsync(&h[0], t.tmp_tile_rowptr + R, 8, hipMemcpyDeviceToHost, stream));
-    GT_HIP(hipMemcpyAsync(&h[1], t.tmp_sp_rowptr + n, 8, hipMemcpyDeviceToHost, stream));
-    GT_HIP(hipMemcpyAsync(&h[2], t.long_row_pos + n, 8, hipMemcpyDeviceToHost, stream));
-    GT_HIP(hipMemcpyAsync(&h[3], t.long_col_pos + n, 8, hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipMemcpyAsync(h, t.sizes, sizeof(h), hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
     plan->n_dense = h[0];
     plan->nnz_sparse = h[1];
@@ -852,11 +865,12 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     bool reuse = false;
     {
         if ((st = ws_checksum(t, stream)) != GT_OK) return st;
-        CountRecord rec;
-        uint64_t have = 0;
-        GT_HIP(hipMemcpyAsync(&rec, t.record, sizeof(rec), hipMemcpyDeviceToHost, stream));
-        GT_HIP(hipMemcpyAsync(&have, t.csum, 8, hipMemcpyDeviceToHost, stream));
+        uint64_t words[kRecordWords + 1];  // the record and the checksum just taken
+        GT_HIP(hipMemcpyAsync(words, t.record, sizeof(words), hipMemcpyDeviceToHost, stream));
         GT_HIP(hipStreamSynchronize(stream));
+        CountRecord rec;
+        for (int i = 0; i < kRecordWords; ++i) rec.w[i] = words[i];
+        const uint64_t have = words[kRecordWords];
         reuse = record_matches(rec, n, nnz, rowptr, col, T, tau_ppm) && rec.w[6] == have;
         if (rec.w[0] == kRecordTag && (st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK)
             return st;
