@@ -456,13 +456,22 @@ __device__ __forceinline__ uint64_t block_min_u64(uint64_t v, uint64_t* s) {
 }
 
 
+// A count-table slot holds its label in the high and its count in the low 32
+// bits (in LDS and in the workspace alike), so claiming a free slot and counting
+// the first occurrences take one atomic.
+constexpr unsigned long long kSlotEmpty = 0xFFFFFFFF00000000ull;  // label -1, count 0
+__device__ __forceinline__ int slot_label(unsigned long long e) { return int(uint32_t(e >> 32)); }
+__device__ __forceinline__ int slot_count(unsigned long long e) { return int(uint32_t(e)); }
+
 // Adds k to the count of label L in an open-addressing table of cap slots.
-__device__ __forceinline__ void tab_add(int* tk, int* tc, int64_t cap, int L, int k) {
+__device__ __forceinline__ void tab_add(unsigned long long* t, int64_t cap, int L, int k) {
+    const unsigned long long mine = (uint64_t(uint32_t(L)) << 32) | uint32_t(k);
     int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
     while (true) {
-        const int prev = atomicCAS(&tk[slot], -1, L);
-        if (prev == -1 || prev == L) {
-            atomicAdd(&tc[slot], k);
+        const unsigned long long prev = atomicCAS(&t[slot], kSlotEmpty, mine);
+        if (prev == kSlotEmpty) return;  // claimed with the count
+        if (slot_label(prev) == L) {
+            atomicAdd(&t[slot], (unsigned long long)uint32_t(k));
             return;
         }
         slot = (slot + 1) & (cap - 1);
@@ -473,7 +482,7 @@ __device__ __forceinline__ void tab_add(int* tk, int* tc, int64_t cap, int L, in
 // most frequent labels of the slice (once clusters form, most neighbours share
 // one) are peeled off by ballot and added once each, the rest lane by lane.
 // Must be reached by the whole wavefront.
-__device__ __forceinline__ void tab_add_wave(int* tk, int* tc, int64_t cap, bool valid, int L) {
+__device__ __forceinline__ void tab_add_wave(unsigned long long* t, int64_t cap, bool valid, int L) {
     bool pending = valid;
     for (int it = 0; it < 3; ++it) {
         const uint64_t m = __ballot(pending);
@@ -481,10 +490,10 @@ __device__ __forceinline__ void tab_add_wave(int* tk, int* tc, int64_t cap, bool
         const int leader = __builtin_ctzll(m);
         const int Ld = __shfl(L, leader, kWave);
         const uint64_t same = __ballot(pending && L == Ld);
-        if (lane_id() == leader) tab_add(tk, tc, cap, Ld, __popcll(same));
+        if (lane_id() == leader) tab_add(t, cap, Ld, __popcll(same));
         if (pending && L == Ld) pending = false;
     }
-    if (pending) tab_add(tk, tc, cap, L, 1);
+    if (pending) tab_add(t, cap, L, 1);
 }
 
 // Inserts the labels of the edges [first + 64 k stride ... ) of one row, k <
@@ -492,8 +501,8 @@ __device__ __forceinline__ void tab_add_wave(int* tk, int* tc, int64_t cap, bool
 // before the first insertion, so a row costs one round trip to memory, not one
 // per slice.  first and stride are uniform over the wavefront.
 template <int R>
-__device__ __forceinline__ void tab_add_row(int* tk, int* tc, int64_t cap, int64_t first, int64_t stride, int64_t b,
-                                            int64_t v, const int32_t* col, const int32_t* lab_in) {
+__device__ __forceinline__ void tab_add_row(unsigned long long* t, int64_t cap, int64_t first, int64_t stride,
+                                            int64_t b, int64_t v, const int32_t* col, const int32_t* lab_in) {
     int c[R], L[R];
 #pragma unroll
     for (int k = 0; k < R; ++k) {
@@ -504,7 +513,7 @@ __device__ __forceinline__ void tab_add_row(int* tk, int* tc, int64_t cap, int64
     for (int k = 0; k < R; ++k) L[k] = c[k] != v ? lab_in[c[k]] : -1;
 #pragma unroll
     for (int k = 0; k < R; ++k)
-        if (first + k * stride < b) tab_add_wave(tk, tc, cap, c[k] != v, L[k]);
+        if (first + k * stride < b) tab_add_wave(t, cap, c[k] != v, L[k]);
 }
 
 // One workgroup per listed row (rows up to kLdsRowMax).  Table: keys (label or
@@ -514,8 +523,7 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
                                                  const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
                                                  int32_t* lab_out, uint64_t key, const uint32_t* flag_prev,
                                                  uint32_t* flag_next) {
-    __shared__ int s_keys[kLdsTable];
-    __shared__ int s_cnts[kLdsTable];
+    __shared__ unsigned long long s_tab[kLdsTable];
     __shared__ int s_red[BS / kWave];
     __shared__ uint64_t s_red64[BS / kWave];
     const bool converged = *flag_prev == 0;
@@ -531,22 +539,18 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
         const int64_t deg = b - a;
         int64_t cap = 1;
         while (cap < 2 * deg) cap <<= 1;
-        int* tk = s_keys;
-        int* tc = s_cnts;
-        for (int64_t s = threadIdx.x; s < cap; s += BS) {
-            tk[s] = -1;
-            tc[s] = 0;
-        }
+        unsigned long long* t = s_tab;
+        for (int64_t s = threadIdx.x; s < cap; s += BS) t[s] = kSlotEmpty;
         __syncthreads();
         // wave-uniform rounds: each wavefront takes 64 consecutive edges per round
-        tab_add_row<(kLdsRowMax + BS - 1) / BS>(tk, tc, cap, a + (threadIdx.x & ~(kWave - 1)), BS, b, v, col,
-                                                lab_in);
+        tab_add_row<(kLdsRowMax + BS - 1) / BS>(t, cap, a + (threadIdx.x & ~(kWave - 1)), BS, b, v, col, lab_in);
         __syncthreads();
         int best = 0, own_cnt = 0;
         for (int64_t s = threadIdx.x; s < cap; s += BS) {
-            const int k = tk[s];
+            const unsigned long long en = t[s];
+            const int k = slot_label(en);
             if (k < 0) continue;
-            const int c = tc[s];
+            const int c = slot_count(en);
             best = c > best ? c : best;
             if (k == own) own_cnt = c;
         }
@@ -556,16 +560,18 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
         if (best > 0 && own_cnt != best) {
             uint64_t hbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += BS) {
-                const int k = tk[s];
-                if (k < 0 || tc[s] != best) continue;
+                const unsigned long long en = t[s];
+                const int k = slot_label(en);
+                if (k < 0 || slot_count(en) != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 hbest = h < hbest ? h : hbest;
             }
             hbest = block_min_u64<BS>(hbest, s_red64);
             uint64_t lbest = ~0ull;
             for (int64_t s = threadIdx.x; s < cap; s += BS) {
-                const int k = tk[s];
-                if (k < 0 || tc[s] != best) continue;
+                const unsigned long long en = t[s];
+                const int k = slot_label(en);
+                if (k < 0 || slot_count(en) != best) continue;
                 if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
                 lbest = uint64_t(uint32_t(k)) < lbest ? uint64_t(uint32_t(k)) : lbest;
             }
@@ -592,11 +598,9 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
                                                        const int64_t* rowptr, const int32_t* col,
                                                        const int32_t* lab_in, int32_t* lab_out, uint64_t key,
                                                        const uint32_t* flag_prev, uint32_t* flag_next) {
-    __shared__ int s_keys[kBlock / kWave][kWaveTab];
-    __shared__ int s_cnts[kBlock / kWave][kWaveTab];
+    __shared__ unsigned long long s_tab[kBlock / kWave][kWaveTab];
     const int w = threadIdx.x / kWave, lane = lane_id();
-    int* tk = s_keys[w];
-    int* tc = s_cnts[w];
+    unsigned long long* t = s_tab[w];
     const bool converged = *flag_prev == 0;
     const int64_t len = *list_len;
     const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
@@ -610,18 +614,16 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
         const int64_t a = rowptr[v], b = rowptr[v + 1];
         int cap = 1;
         while (cap < 2 * (b - a)) cap <<= 1;  // <= kWaveTab
-        for (int s2 = lane; s2 < cap; s2 += kWave) {
-            tk[s2] = -1;
-            tc[s2] = 0;
-        }
+        for (int s2 = lane; s2 < cap; s2 += kWave) t[s2] = kSlotEmpty;
         wave_lds_sync();
-        tab_add_row<kWaveTabRowMax / kWave>(tk, tc, cap, a, kWave, b, v, col, lab_in);
+        tab_add_row<kWaveTabRowMax / kWave>(t, cap, a, kWave, b, v, col, lab_in);
         wave_lds_sync();
         int best = 0, own_cnt = 0;
         for (int s2 = lane; s2 < cap; s2 += kWave) {
-            const int k = tk[s2];
+            const unsigned long long en = t[s2];
+            const int k = slot_label(en);
             if (k < 0) continue;
-            const int c = tc[s2];
+            const int c = slot_count(en);
             best = c > best ? c : best;
             if (k == own) own_cnt = c;
         }
@@ -631,16 +633,18 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
         if (best > 0 && own_cnt != best) {
             uint64_t hbest = ~0ull;
             for (int s2 = lane; s2 < cap; s2 += kWave) {
-                const int k = tk[s2];
-                if (k < 0 || tc[s2] != best) continue;
+                const unsigned long long en = t[s2];
+                const int k = slot_label(en);
+                if (k < 0 || slot_count(en) != best) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(k)) ^ key);
                 hbest = h < hbest ? h : hbest;
             }
             hbest = wave_min_u64(hbest);
             int lbest = INT_MAX;
             for (int s2 = lane; s2 < cap; s2 += kWave) {
-                const int k = tk[s2];
-                if (k < 0 || tc[s2] != best) continue;
+                const unsigned long long en = t[s2];
+                const int k = slot_label(en);
+                if (k < 0 || slot_count(en) != best) continue;
                 if (mix64(uint64_t(uint32_t(k)) ^ key) != hbest) continue;
                 lbest = k < lbest ? k : lbest;
             }
@@ -728,13 +732,6 @@ struct BigRows {
     unsigned long long* hbest;
     unsigned long long* lbest;
 };
-
-// A slot of the very long rows' count tables holds its label in the high and
-// its count in the low 32 bits, so claiming a free slot and counting the
-// first occurrences take one atomic.
-constexpr unsigned long long kSlotEmpty = 0xFFFFFFFF00000000ull;  // label -1, count 0
-__device__ __forceinline__ int slot_label(unsigned long long e) { return int(uint32_t(e >> 32)); }
-__device__ __forceinline__ int slot_count(unsigned long long e) { return int(uint32_t(e)); }
 
 __device__ __forceinline__ int64_t table_cap(int64_t deg) {
     int64_t cap = 1;
@@ -860,8 +857,7 @@ __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t*
 // neighbour labels repeat, as they do once clusters form).
 __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t* rowptr, const int32_t* col,
                                                        const int32_t* lab_in, const uint32_t* flag_prev) {
-    __shared__ int s_keys[kBigChunkTab];
-    __shared__ int s_cnts[kBigChunkTab];
+    __shared__ unsigned long long s_tab[kBigChunkTab];
     if (*flag_prev == 0) return;
     const int64_t len = *br.len;
     const int64_t total = br.echunk[len];
@@ -872,10 +868,7 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
         const int64_t cap = table_cap(b - a);
         const int64_t j = c - br.echunk[idx];
         unsigned long long* tab = br.tab + br.off[idx];
-        for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) {
-            s_keys[x] = -1;
-            s_cnts[x] = 0;
-        }
+        for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) s_tab[x] = kSlotEmpty;
         __syncthreads();
         const int64_t e0 = a + j * kBigEdgeChunk;
         const int64_t e1 = e0 + kBigEdgeChunk < b ? e0 + kBigEdgeChunk : b;
@@ -883,19 +876,20 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
             const int64_t e = base + lane_id();
             const int cc = e < e1 ? col[e] : int(v);
             const bool valid = cc != v;
-            tab_add_wave(s_keys, s_cnts, kBigChunkTab, valid, valid ? lab_in[cc] : -1);
+            tab_add_wave(s_tab, kBigChunkTab, valid, valid ? lab_in[cc] : -1);
         }
         __syncthreads();
         for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) {
-            const int L = s_keys[x];
+            const unsigned long long en = s_tab[x];
+            const int L = slot_label(en);
             if (L < 0) continue;
-            const unsigned long long mine = (uint64_t(uint32_t(L)) << 32) | uint32_t(s_cnts[x]);
+            const unsigned long long mine = en;  // the chunk's count of L
             int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
             while (true) {
                 const unsigned long long prev = atomicCAS(&tab[slot], kSlotEmpty, mine);
                 if (prev == kSlotEmpty) break;  // claimed with the count
                 if (slot_label(prev) == L) {
-                    atomicAdd(&tab[slot], (unsigned long long)uint32_t(s_cnts[x]));
+                    atomicAdd(&tab[slot], (unsigned long long)uint32_t(slot_count(en)));
                     break;
                 }
                 slot = (slot + 1) & (cap - 1);
@@ -1171,7 +1165,8 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.big_lbest = ws.take<unsigned long long>(n1);
     r.sort_keys = ws.take<uint64_t>(n1);
     r.sort_vals = ws.take<uint32_t>(n1);
-    r.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1 + 1 > kClasses * nblk + 1 ? n1 + 1 : kClasses * nblk + 1)));
+    const int64_t scan_n = n1 + 1 > kClasses * nblk + 1 ? n1 + 1 : kClasses * nblk + 1;
+    r.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(scan_n)));
     r.sort = sort_tmp(ws, n1, 8, true);
     return r;
 }
@@ -1339,8 +1334,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             GT_LAUNCH_CHECK("reorder_lp_wavetab");
         }
         if (cnt[kClsMed] > 0) {
-            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(list_of[kClsMed], len_of[kClsMed], rowptr, col, in, out, key,
-                                                            r.flags + t, r.flags + t + 1);
+            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(list_of[kClsMed], len_of[kClsMed], rowptr, col, in,
+                                                                  out, key, r.flags + t, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_lds");
         }
     }
