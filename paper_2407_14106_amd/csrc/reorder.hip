@@ -21,6 +21,14 @@
 // All compute the same function of the neighbour-label multiset.  The first
 // sweep, whose labels are the node ids, reduces to a minimum over each row's
 // columns and uses none of the tables.
+//
+// The sweeps after the first run on the graph renumbered by list position
+// (each row's place in the class-major row list): the rows' entries are laid
+// out in list order (roff, ncol; written once, during the first sweep) and a
+// node's label is kept at its list position.  A class's rows then read their
+// row offsets and entries in runs, and the classes gather the long rows, whose
+// labels most rows read, into a few cache lines.  The label values stay node
+// ids, so the result does not depend on this numbering.
 #include <limits.h>
 
 #include "prim.h"
@@ -151,17 +159,23 @@ __global__ __launch_bounds__(kClsBlock) void k_classify(int64_t n, int64_t nnz, 
     }
 }
 
+// list[pos] = v, lpos[v] = pos (the row's list position) and ldeg[pos] = its
+// entry count.
 __global__ __launch_bounds__(kClsBlock) void k_class_scatter(int64_t n, const int64_t* rowptr,
-                                                             const int64_t* blk_off, int64_t nblk, int32_t* list) {
+                                                             const int64_t* blk_off, int64_t nblk, int32_t* list,
+                                                             int32_t* lpos, uint32_t* ldeg) {
     __shared__ int s_cnt[kClsBlock / kWave][kClasses];
     const int64_t v = int64_t(blockIdx.x) * kClsBlock + threadIdx.x;
-    const int cls = v < n ? row_class(rowptr[v + 1] - rowptr[v]) : -1;
+    const int64_t deg = v < n ? rowptr[v + 1] - rowptr[v] : 0;
+    const int cls = v < n ? row_class(deg) : -1;
     const int rank = class_ballots(cls, s_cnt);
     __syncthreads();
     if (cls >= 0) {
         int64_t pos = blk_off[cls * nblk + blockIdx.x] + rank;
         for (int w = 0; w < int(threadIdx.x / kWave); ++w) pos += s_cnt[w][cls];
         list[pos] = int32_t(v);
+        lpos[v] = int32_t(pos);
+        ldeg[pos] = uint32_t(deg);
     }
 }
 
@@ -191,54 +205,12 @@ __global__ __launch_bounds__(256) void k_blocks_max(int64_t nblk, const uint32_t
     }
 }
 
-// ------------------------------------------------------------------ wave rows
+// ------------------------------------------------------------------ short rows
 // Rows of up to kWaveRowMax edges, in five lists by size, all in one launch:
-// the grid's blocks are cut into five consecutive ranges, one per list.  Each
-// range runs its list with a grid-stride loop over its own blocks.
+// the grid's blocks are cut into one range per list, each range running its
+// list with a grid-stride loop over tasks (one wavefront's rows).
 
-// Rows of kSub32 + 1 to kWaveRowMax edges, one wavefront each: every lane
-// counts how many of the row's labels equal its own, reading the others with
-// readlane (the lane index is uniform over the wavefront).
-__device__ __forceinline__ void lp_wave_rows(const int32_t* list, int64_t len, unsigned blk, unsigned nblk,
-                                             const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
-                                             int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
-    const int lane = lane_id();
-    const int64_t waves = int64_t(nblk) * (kBlock / kWave);
-    for (int64_t idx = int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave; idx < len; idx += waves) {
-        const int64_t v = list[idx];
-        const int own = lab_in[v];
-        if (converged) {
-            if (lane == 0) lab_out[v] = own;
-            continue;
-        }
-        const int64_t a = rowptr[v];
-        const int deg = int(rowptr[v + 1] - a);
-        int c = lane < deg ? col[a + lane] : -1;
-        const bool valid = lane < deg && c != v;
-        const int L = valid ? lab_in[c] : -1;
-        int cnt = 0;
-        for (int k = 0; k < deg; ++k) cnt += (__builtin_amdgcn_readlane(L, k) == L) ? 1 : 0;
-        if (!valid) cnt = 0;
-        const int best = wave_max(cnt);
-        int cand = own;
-        if (best > 0) {
-            const int own_cnt = __popcll(ballot(valid && L == own));
-            if (own_cnt != best) {
-                const bool top = valid && cnt == best;
-                const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
-                const uint64_t hmin = wave_min_u64(h);
-                cand = wave_min_i32((top && h == hmin) ? L : INT_MAX);
-            }
-        }
-        if (lane == 0) {
-            lab_out[v] = is_active(v, key) ? cand : own;
-            if (cand != own) *flag_next = 1u;
-        }
-    }
-}
-
-// Rows of at most S edges (S = 4, 8, 16 or 32), 64 / S rows per wavefront: the
-// same function as lp_wave_rows with every reduction confined to the row's S lanes.
+// Reductions over the S lanes of a row group (S = 4, 8, 16 or 32).
 template <int S>
 __device__ __forceinline__ int group_max_i32(int v) {
 #pragma unroll
@@ -267,66 +239,167 @@ __device__ __forceinline__ uint64_t group_min_u64(uint64_t v) {
     return v;
 }
 
+// Row at list position p (kSub32 + 1 to kWaveRowMax edges), one wavefront:
+// every lane counts how many of the row's labels equal its own, reading the
+// others with readlane (the lane index is uniform over the wavefront).  roff,
+// ncol: the graph by list position (row p's entries at ncol[roff[p],
+// roff[p + 1])); labels are indexed by list position.
+__device__ __forceinline__ void lp_wave_row(int64_t p, const int32_t* list, const int64_t* roff,
+                                            const int32_t* ncol, const int32_t* lab_in, int32_t* lab_out,
+                                            uint64_t key, bool converged, uint32_t* flag_next) {
+    const int lane = lane_id();
+    const int own = lab_in[p];
+    if (converged) {
+        if (lane == 0) lab_out[p] = own;
+        return;
+    }
+    const int64_t v = list[p];
+    const int64_t a = roff[p];
+    const int deg = int(roff[p + 1] - a);
+    const int c = lane < deg ? ncol[a + lane] : -1;
+    const bool valid = lane < deg && c != p;
+    const int L = valid ? lab_in[c] : -1;
+    int cnt = 0;
+    for (int k = 0; k < deg; ++k) cnt += (__builtin_amdgcn_readlane(L, k) == L) ? 1 : 0;
+    if (!valid) cnt = 0;
+    const int best = wave_max(cnt);
+    int cand = own;
+    if (best > 0) {
+        const int own_cnt = __popcll(ballot(valid && L == own));
+        if (own_cnt != best) {
+            const bool top = valid && cnt == best;
+            const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
+            const uint64_t hmin = wave_min_u64(h);
+            cand = wave_min_i32((top && h == hmin) ? L : INT_MAX);
+        }
+    }
+    if (lane == 0) {
+        lab_out[p] = is_active(v, key) ? cand : own;
+        if (cand != own) *flag_next = 1u;
+    }
+}
+
+// Rows g0 .. g0 + 64 / S - 1 of a list of rows of at most S edges (S = 4, 8,
+// 16 or 32) at list positions base + [0, len): the same function as
+// lp_wave_row with every reduction confined to the row's S lanes.
 template <int S>
-__device__ __forceinline__ void lp_sub_rows(const int32_t* list, int64_t len, unsigned blk, unsigned nblk,
-                                            const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
-                                            int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
+__device__ __forceinline__ void lp_sub_group(int64_t g0, int64_t base, int64_t len, const int32_t* list,
+                                             const int64_t* roff, const int32_t* ncol, const int32_t* lab_in,
+                                             int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
     constexpr int G = kWave / S;
     const int lane = lane_id(), sub = lane / S, sl = lane % S;
     const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
-    const int64_t waves = int64_t(nblk) * (kBlock / kWave);
-    for (int64_t base = (int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave) * G; base < len; base += waves * G) {
-        const int64_t idx = base + sub;
-        const bool live = idx < len;
-        const int64_t v = live ? list[idx] : 0;
-        const int own = live ? lab_in[v] : -1;
-        if (converged) {
-            if (live && sl == 0) lab_out[v] = own;
-            continue;
-        }
-        int64_t a = 0;
-        int deg = 0;
-        if (live) {
-            a = rowptr[v];
-            deg = int(rowptr[v + 1] - a);
-        }
-        const int c = sl < deg ? col[a + sl] : -1;
-        const bool valid = sl < deg && c != v;
-        const int L = valid ? lab_in[c] : -1;
-        const int dmax = wave_max(deg);
-        int cnt = 0;
-        for (int k = 0; k < dmax; ++k) {
-            // lane sub * S + k of each group: by readlane (k is uniform over the
-            // wavefront) for few groups, by one lane permute for many
-            int Lk;
-            if constexpr (G <= 4) {
-                Lk = __builtin_amdgcn_readlane(L, k);
+    const int64_t idx = g0 + sub;
+    const bool live = idx < len;
+    const int64_t p = base + idx;
+    const int own = live ? lab_in[p] : -1;
+    if (converged) {
+        if (live && sl == 0) lab_out[p] = own;
+        return;
+    }
+    const int64_t v = live ? list[p] : 0;
+    int64_t a = 0;
+    int deg = 0;
+    if (live) {
+        a = roff[p];
+        deg = int(roff[p + 1] - a);
+    }
+    const int c = sl < deg ? ncol[a + sl] : -1;
+    const bool valid = sl < deg && c != p;
+    const int L = valid ? lab_in[c] : -1;
+    const int dmax = wave_max(deg);
+    int cnt = 0;
+    for (int k = 0; k < dmax; ++k) {
+        // lane sub * S + k of each group: by readlane (k is uniform over the
+        // wavefront) for few groups, by one lane permute for many
+        int Lk;
+        if constexpr (G <= 4) {
+            Lk = __builtin_amdgcn_readlane(L, k);
 #pragma unroll
-                for (int g = 1; g < G; ++g) {
-                    const int x = __builtin_amdgcn_readlane(L, g * S + k);
-                    Lk = sub == g ? x : Lk;
-                }
-            } else {
-                Lk = __shfl(L, k, S);
+            for (int g = 1; g < G; ++g) {
+                const int x = __builtin_amdgcn_readlane(L, g * S + k);
+                Lk = sub == g ? x : Lk;
             }
-            cnt += (Lk == L) ? 1 : 0;
+        } else {
+            Lk = __shfl(L, k, S);
         }
-        if (!valid) cnt = 0;
-        const int best = group_max_i32<S>(cnt);
-        const int own_cnt = __popcll(__ballot(valid && L == own) & gmask);
-        const bool moves = best > 0 && own_cnt != best;
-        int cand = own;
-        if (__ballot(moves)) {  // the tie-break, unless every row of the wavefront keeps its label
-            const bool top = valid && cnt == best && moves;
-            const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
-            const uint64_t hmin = group_min_u64<S>(h);
-            const int lmin = group_min_i32<S>((top && h == hmin) ? L : INT_MAX);
-            if (moves) cand = lmin;
+        cnt += (Lk == L) ? 1 : 0;
+    }
+    if (!valid) cnt = 0;
+    const int best = group_max_i32<S>(cnt);
+    const int own_cnt = __popcll(__ballot(valid && L == own) & gmask);
+    const bool moves = best > 0 && own_cnt != best;
+    int cand = own;
+    if (__ballot(moves)) {  // the tie-break, unless every row of the wavefront keeps its label
+        const bool top = valid && cnt == best && moves;
+        const uint64_t h = top ? mix64(uint64_t(uint32_t(L)) ^ key) : ~0ull;
+        const uint64_t hmin = group_min_u64<S>(h);
+        const int lmin = group_min_i32<S>((top && h == hmin) ? L : INT_MAX);
+        if (moves) cand = lmin;
+    }
+    if (live && sl == 0) {
+        lab_out[p] = is_active(v, key) ? cand : own;
+        if (cand != own) *flag_next = 1u;
+    }
+}
+
+// The five short-row lists (rows of 33-64, 17-32, 9-16, 5-8 and 0-4 edges, in
+// that order): their first list positions and lengths, and the first block of
+// each one's range; first[5] is the grid.
+enum { kSmWave, kSm32, kSm16, kSm8, kSm4, kSmLists };
+struct SmallRows {
+    const int32_t* list;
+    int64_t base[kSmLists];
+    int64_t len[kSmLists];
+    unsigned first[kSmLists + 1];
+};
+
+// The list of this block's range, the block's index in it and the range's size.
+__device__ __forceinline__ int small_list(const SmallRows& sr, unsigned* blk, unsigned* nblk) {
+    const unsigned b = blockIdx.x;
+    int k = 0;
+    while (k + 1 < kSmLists && b >= sr.first[k + 1]) ++k;
+    *blk = b - sr.first[k];
+    *nblk = sr.first[k + 1] - sr.first[k];
+    return k;
+}
+
+template <int S>
+__device__ __forceinline__ void lp_sub_rows(const SmallRows& sr, int k, unsigned blk, unsigned nblk,
+                                            const int64_t* roff, const int32_t* ncol, const int32_t* lab_in,
+                                            int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
+    constexpr int G = kWave / S;
+    const int64_t waves = int64_t(nblk) * (kBlock / kWave);
+    for (int64_t g0 = (int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave) * G; g0 < sr.len[k]; g0 += waves * G)
+        lp_sub_group<S>(g0, sr.base[k], sr.len[k], sr.list, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+}
+
+// The sweeps after the first over the five lists.
+__global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t* roff, const int32_t* ncol,
+                                                     const int32_t* lab_in, int32_t* lab_out, uint64_t key,
+                                                     const uint32_t* flag_prev, uint32_t* flag_next) {
+    const bool converged = *flag_prev == 0;
+    unsigned blk, nblk;
+    const int k = small_list(sr, &blk, &nblk);
+    switch (k) {
+        case kSmWave: {
+            const int64_t waves = int64_t(nblk) * (kBlock / kWave);
+            for (int64_t g = int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave; g < sr.len[k]; g += waves)
+                lp_wave_row(sr.base[k] + g, sr.list, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            break;
         }
-        if (live && sl == 0) {
-            lab_out[v] = is_active(v, key) ? cand : own;
-            if (cand != own) *flag_next = 1u;
-        }
+        case kSm32:
+            lp_sub_rows<kSub32>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            break;
+        case kSm16:
+            lp_sub_rows<kSub16>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            break;
+        case kSm8:
+            lp_sub_rows<kSub8>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            break;
+        default:
+            lp_sub_rows<kSub4>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            break;
     }
 }
 
@@ -339,19 +412,22 @@ __device__ __forceinline__ void lp_sub_rows(const int32_t* list, int64_t len, un
 // unique.  The first sweep therefore reads no labels and builds no tables: it
 // takes a minimum over each row's columns.
 
-// Rows of at most S edges, 64 / S per wavefront.
+// Rows of at most S edges, 64 / S per wavefront.  Every entry is read here
+// once: its column's list position goes to ncol for the later sweeps.
 template <int S>
-__device__ __forceinline__ void first_rows(const int32_t* list, int64_t len, unsigned blk, unsigned nblk,
-                                           const int64_t* rowptr, const int32_t* col, int32_t* lab_out, uint64_t key,
-                                           uint32_t* flag_next) {
+__device__ __forceinline__ void first_rows(const int32_t* list, int64_t base, int64_t len, unsigned blk,
+                                           unsigned nblk, const int64_t* rowptr, const int32_t* col,
+                                           const int64_t* roff, const int32_t* lpos, int32_t* ncol,
+                                           int32_t* lab_out, uint64_t key, uint32_t* flag_next) {
     constexpr int G = kWave / S;
     const int lane = lane_id(), sub = lane / S, sl = lane % S;
     const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
     const int64_t waves = int64_t(nblk) * (kBlock / kWave);
-    for (int64_t base = (int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave) * G; base < len; base += waves * G) {
-        const int64_t idx = base + sub;
+    for (int64_t g0 = (int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave) * G; g0 < len; g0 += waves * G) {
+        const int64_t idx = g0 + sub;
         const bool live = idx < len;
-        const int64_t v = live ? list[idx] : 0;
+        const int64_t p = base + idx;
+        const int64_t v = live ? list[p] : 0;
         int64_t a = 0;
         int deg = 0;
         if (live) {
@@ -359,6 +435,7 @@ __device__ __forceinline__ void first_rows(const int32_t* list, int64_t len, uns
             deg = int(rowptr[v + 1] - a);
         }
         const int c = sl < deg ? col[a + sl] : -1;
+        if (sl < deg) ncol[roff[p] + sl] = lpos[c];
         const bool valid = sl < deg && c != v;
         const uint64_t h = valid ? mix64(uint64_t(uint32_t(c)) ^ key) : ~0ull;
         const uint64_t hmin = group_min_u64<S>(h);
@@ -366,66 +443,39 @@ __device__ __forceinline__ void first_rows(const int32_t* list, int64_t len, uns
         const bool any = (__ballot(valid) & gmask) != 0;
         if (live && sl == 0) {
             const int own = int(v), cand = any ? lmin : own;
-            lab_out[v] = is_active(v, key) ? cand : own;
+            lab_out[p] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
         }
     }
 }
 
-// The five short-row lists (rows of 33-64, 17-32, 9-16, 5-8 and 0-4 edges, in
-// that order) and the first block of each one's range; first[5] is the grid.
-enum { kSmWave, kSm32, kSm16, kSm8, kSm4, kSmLists };
-struct SmallRows {
-    const int32_t* list[kSmLists];
-    const int64_t* len[kSmLists];
-    unsigned first[kSmLists + 1];
-};
-
-template <bool kFirst>
-__global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t* rowptr, const int32_t* col,
-                                                     const int32_t* lab_in, int32_t* lab_out, uint64_t key,
-                                                     const uint32_t* flag_prev, uint32_t* flag_next) {
-    const bool converged = *flag_prev == 0;
-    const unsigned b = blockIdx.x;
-    int k = 0;
-    while (k + 1 < kSmLists && b >= sr.first[k + 1]) ++k;
-    const unsigned blk = b - sr.first[k], nblk = sr.first[k + 1] - sr.first[k];
-    const int64_t len = *sr.len[k];
-    if constexpr (kFirst) {
-        switch (k) {
-            case kSmWave:
-                first_rows<kWave>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
-                break;
-            case kSm32:
-                first_rows<kSub32>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
-                break;
-            case kSm16:
-                first_rows<kSub16>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
-                break;
-            case kSm8:
-                first_rows<kSub8>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
-                break;
-            default:
-                first_rows<kSub4>(sr.list[k], len, blk, nblk, rowptr, col, lab_out, key, flag_next);
-                break;
-        }
-        return;
-    }
+// The first sweep over the five short-row lists.
+__global__ __launch_bounds__(kBlock) void k_first_small(SmallRows fr, const int64_t* rowptr, const int32_t* col,
+                                                        const int64_t* roff, const int32_t* lpos, int32_t* ncol,
+                                                        int32_t* lab_out, uint64_t key, uint32_t* flag_next) {
+    unsigned blk, nblk;
+    const int k = small_list(fr, &blk, &nblk);
+    const int64_t len = fr.len[k];
     switch (k) {
         case kSmWave:
-            lp_wave_rows(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            first_rows<kWave>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
+                              flag_next);
             break;
         case kSm32:
-            lp_sub_rows<kSub32>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            first_rows<kSub32>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
+                               flag_next);
             break;
         case kSm16:
-            lp_sub_rows<kSub16>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            first_rows<kSub16>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
+                               flag_next);
             break;
         case kSm8:
-            lp_sub_rows<kSub8>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            first_rows<kSub8>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
+                              flag_next);
             break;
         default:
-            lp_sub_rows<kSub4>(sr.list[k], len, blk, nblk, rowptr, col, lab_in, lab_out, key, converged, flag_next);
+            first_rows<kSub4>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
+                              flag_next);
             break;
     }
 }
@@ -502,25 +552,26 @@ __device__ __forceinline__ void tab_add_wave(unsigned long long* t, int64_t cap,
 // per slice.  first and stride are uniform over the wavefront.
 template <int R>
 __device__ __forceinline__ void tab_add_row(unsigned long long* t, int64_t cap, int64_t first, int64_t stride,
-                                            int64_t b, int64_t v, const int32_t* col, const int32_t* lab_in) {
+                                            int64_t b, int64_t p, const int32_t* ncol, const int32_t* lab_in) {
     int c[R], L[R];
 #pragma unroll
     for (int k = 0; k < R; ++k) {
         const int64_t e = first + k * stride + lane_id();
-        c[k] = e < b ? col[e] : int(v);
+        c[k] = e < b ? ncol[e] : int(p);
     }
 #pragma unroll
-    for (int k = 0; k < R; ++k) L[k] = c[k] != v ? lab_in[c[k]] : -1;
+    for (int k = 0; k < R; ++k) L[k] = c[k] != p ? lab_in[c[k]] : -1;
 #pragma unroll
     for (int k = 0; k < R; ++k)
-        if (first + k * stride < b) tab_add_wave(t, cap, c[k] != v, L[k]);
+        if (first + k * stride < b) tab_add_wave(t, cap, c[k] != p, L[k]);
 }
 
 // One workgroup per listed row (rows up to kLdsRowMax).  Table: keys (label or
-// -1) and counts in LDS.
+// -1) and counts in LDS.  The rows are list[base + [0, len)]; roff, ncol and
+// the labels are by list position.
 template <int BS>
-__global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int64_t* list_len,
-                                                 const int64_t* rowptr, const int32_t* col, const int32_t* lab_in,
+__global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, int64_t base, const int64_t* list_len,
+                                                 const int64_t* roff, const int32_t* ncol, const int32_t* lab_in,
                                                  int32_t* lab_out, uint64_t key, const uint32_t* flag_prev,
                                                  uint32_t* flag_next) {
     __shared__ unsigned long long s_tab[kLdsTable];
@@ -529,13 +580,14 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
     const bool converged = *flag_prev == 0;
     const int64_t len = *list_len;
     for (int64_t idx = blockIdx.x; idx < len; idx += gridDim.x) {
-        const int64_t v = list[idx];
-        const int own = lab_in[v];
+        const int64_t p = base + idx;
+        const int own = lab_in[p];
         if (converged) {
-            if (threadIdx.x == 0) lab_out[v] = own;
+            if (threadIdx.x == 0) lab_out[p] = own;
             continue;
         }
-        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        const int64_t v = list[p];
+        const int64_t a = roff[p], b = roff[p + 1];
         const int64_t deg = b - a;
         int64_t cap = 1;
         while (cap < 2 * deg) cap <<= 1;
@@ -543,7 +595,7 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
         for (int64_t s = threadIdx.x; s < cap; s += BS) t[s] = kSlotEmpty;
         __syncthreads();
         // wave-uniform rounds: each wavefront takes 64 consecutive edges per round
-        tab_add_row<(kLdsRowMax + BS - 1) / BS>(t, cap, a + (threadIdx.x & ~(kWave - 1)), BS, b, v, col, lab_in);
+        tab_add_row<(kLdsRowMax + BS - 1) / BS>(t, cap, a + (threadIdx.x & ~(kWave - 1)), BS, b, p, ncol, lab_in);
         __syncthreads();
         int best = 0, own_cnt = 0;
         for (int64_t s = threadIdx.x; s < cap; s += BS) {
@@ -578,7 +630,7 @@ __global__ __launch_bounds__(BS) void k_lp_block(const int32_t* list, const int6
             cand = int(block_min_u64<BS>(lbest, s_red64));
         }
         if (threadIdx.x == 0) {
-            lab_out[v] = is_active(v, key) ? cand : own;
+            lab_out[p] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
         }
         __syncthreads();
@@ -594,8 +646,8 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, const int64_t* list_len,
-                                                       const int64_t* rowptr, const int32_t* col,
+__global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, int64_t base, const int64_t* list_len,
+                                                       const int64_t* roff, const int32_t* ncol,
                                                        const int32_t* lab_in, int32_t* lab_out, uint64_t key,
                                                        const uint32_t* flag_prev, uint32_t* flag_next) {
     __shared__ unsigned long long s_tab[kBlock / kWave][kWaveTab];
@@ -605,18 +657,19 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
     const int64_t len = *list_len;
     const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
     for (int64_t idx = int64_t(blockIdx.x) * (kBlock / kWave) + w; idx < len; idx += waves) {
-        const int64_t v = list[idx];
-        const int own = lab_in[v];
+        const int64_t p = base + idx;
+        const int own = lab_in[p];
         if (converged) {
-            if (lane == 0) lab_out[v] = own;
+            if (lane == 0) lab_out[p] = own;
             continue;
         }
-        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        const int64_t v = list[p];
+        const int64_t a = roff[p], b = roff[p + 1];
         int cap = 1;
         while (cap < 2 * (b - a)) cap <<= 1;  // <= kWaveTab
         for (int s2 = lane; s2 < cap; s2 += kWave) t[s2] = kSlotEmpty;
         wave_lds_sync();
-        tab_add_row<kWaveTabRowMax / kWave>(t, cap, a, kWave, b, v, col, lab_in);
+        tab_add_row<kWaveTabRowMax / kWave>(t, cap, a, kWave, b, p, ncol, lab_in);
         wave_lds_sync();
         int best = 0, own_cnt = 0;
         for (int s2 = lane; s2 < cap; s2 += kWave) {
@@ -651,7 +704,7 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
             cand = wave_min_i32(lbest);
         }
         if (lane == 0) {
-            lab_out[v] = is_active(v, key) ? cand : own;
+            lab_out[p] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
         }
         wave_lds_sync();  // every lane is done with the table before the next row clears it
@@ -659,12 +712,15 @@ __global__ __launch_bounds__(kBlock) void k_lp_wavetab(const int32_t* list, cons
 }
 
 // First sweep, rows of more than 64 edges: BS threads per row (one wavefront,
-// or the workgroup), each lane keeping the smallest hash of its edges.
+// or the workgroup), each lane keeping the smallest hash of its edges and
+// writing their list positions to ncol.
 template <int BS>
-__global__ __launch_bounds__(BS > kBlock ? BS : kBlock) void k_first_wide(const int32_t* list, const int64_t* list_len,
+__global__ __launch_bounds__(BS > kBlock ? BS : kBlock) void k_first_wide(const int32_t* list, int64_t base,
+                                                                          const int64_t* list_len,
                                                                           const int64_t* rowptr, const int32_t* col,
-                                                                          int32_t* lab_out, uint64_t key,
-                                                                          uint32_t* flag_next) {
+                                                                          const int64_t* roff, const int32_t* lpos,
+                                                                          int32_t* ncol, int32_t* lab_out,
+                                                                          uint64_t key, uint32_t* flag_next) {
     constexpr int kThreads = BS > kBlock ? BS : kBlock;
     constexpr int kRowsPer = kThreads / BS;  // rows a workgroup takes at once
     __shared__ uint64_t s_red64[kThreads / kWave];
@@ -674,14 +730,17 @@ __global__ __launch_bounds__(BS > kBlock ? BS : kBlock) void k_first_wide(const 
     for (int64_t idx0 = int64_t(blockIdx.x) * kRowsPer; idx0 < len; idx0 += int64_t(gridDim.x) * kRowsPer) {
         const int64_t idx = idx0 + threadIdx.x / BS;
         const bool live = idx < len;  // uniform over a row's BS threads
-        const int64_t v = live ? list[idx] : 0;
+        const int64_t p = base + idx;
+        const int64_t v = live ? list[p] : 0;
         uint64_t hb = ~0ull;
         int cb = INT_MAX;
         bool any = false;
         if (live) {
             const int64_t a = rowptr[v], b = rowptr[v + 1];
+            const int64_t shift = roff[p] - a;  // entry e of the row goes to ncol[e + shift]
             for (int64_t e = a + t; e < b; e += BS) {
                 const int c = col[e];
+                ncol[e + shift] = lpos[c];
                 if (c == v) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(c)) ^ key);
                 if (h < hb || (h == hb && c < cb)) {
@@ -705,7 +764,7 @@ __global__ __launch_bounds__(BS > kBlock ? BS : kBlock) void k_first_wide(const 
         }
         if (live && t == 0) {
             const int own = int(v), cand = anyr ? lmin : own;
-            lab_out[v] = is_active(v, key) ? cand : own;
+            lab_out[p] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
         }
     }
@@ -721,7 +780,8 @@ __global__ __launch_bounds__(BS > kBlock ? BS : kBlock) void k_first_wide(const 
 // does not depend on the order).
 
 struct BigRows {
-    const int32_t* list;
+    const int32_t* list;  // the listed rows, at list positions base + [0, len)
+    int64_t base;
     const int64_t* len;
     const int64_t* off;   // table offset of each listed row
     const int64_t* echunk;  // [listed rows + 1]: first edge chunk of each row (kBigEdgeChunk edges per chunk)
@@ -855,7 +915,7 @@ __global__ __launch_bounds__(kBlock) void k_big_clear(BigRows br, const int64_t*
 // chunk is counted in an LDS table first, then its distinct labels are added
 // to the row's table in the workspace (far fewer global atomics where
 // neighbour labels repeat, as they do once clusters form).
-__global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t* rowptr, const int32_t* col,
+__global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t* roff, const int32_t* ncol,
                                                        const int32_t* lab_in, const uint32_t* flag_prev) {
     __shared__ unsigned long long s_tab[kBigChunkTab];
     if (*flag_prev == 0) return;
@@ -863,8 +923,8 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
     const int64_t total = br.echunk[len];
     for (int64_t c = blockIdx.x; c < total; c += gridDim.x) {
         const int64_t idx = chunk_row(br.echunk, len, c);
-        const int64_t v = br.list[idx];
-        const int64_t a = rowptr[v], b = rowptr[v + 1];
+        const int64_t p = br.base + idx;
+        const int64_t a = roff[p], b = roff[p + 1];
         const int64_t cap = table_cap(b - a);
         const int64_t j = c - br.echunk[idx];
         unsigned long long* tab = br.tab + br.off[idx];
@@ -872,27 +932,46 @@ __global__ __launch_bounds__(kBlock) void k_big_insert(BigRows br, const int64_t
         __syncthreads();
         const int64_t e0 = a + j * kBigEdgeChunk;
         const int64_t e1 = e0 + kBigEdgeChunk < b ? e0 + kBigEdgeChunk : b;
-        for (int64_t base = e0 + (threadIdx.x & ~(kWave - 1)); base < e1; base += kBlock) {
-            const int64_t e = base + lane_id();
-            const int cc = e < e1 ? col[e] : int(v);
-            const bool valid = cc != v;
-            tab_add_wave(s_tab, kBigChunkTab, valid, valid ? lab_in[cc] : -1);
+        // every slice's column and label loads are issued before the first insertion
+        constexpr int R = kBigEdgeChunk / kBlock;
+        const int64_t w0 = e0 + (threadIdx.x & ~(kWave - 1));
+        int cc[R], L[R];
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const int64_t e = w0 + k * kBlock + lane_id();
+            cc[k] = e < e1 ? ncol[e] : int(p);
         }
+#pragma unroll
+        for (int k = 0; k < R; ++k) L[k] = cc[k] != p ? lab_in[cc[k]] : -1;
+#pragma unroll
+        for (int k = 0; k < R; ++k)
+            if (w0 + k * kBlock < e1) tab_add_wave(s_tab, kBigChunkTab, cc[k] != p, L[k]);
         __syncthreads();
-        for (int x = threadIdx.x; x < kBigChunkTab; x += kBlock) {
-            const unsigned long long en = s_tab[x];
-            const int L = slot_label(en);
-            if (L < 0) continue;
-            const unsigned long long mine = en;  // the chunk's count of L
-            int64_t slot = int64_t(mix64(uint64_t(uint32_t(L))) & uint64_t(cap - 1));
-            while (true) {
-                const unsigned long long prev = atomicCAS(&tab[slot], kSlotEmpty, mine);
-                if (prev == kSlotEmpty) break;  // claimed with the count
-                if (slot_label(prev) == L) {
-                    atomicAdd(&tab[slot], (unsigned long long)uint32_t(slot_count(en)));
+        // the chunk's distinct labels into the row's table: the first probe of every slot the thread holds is
+        // issued before any result is used, so a chunk of many distinct labels costs about one round trip
+        constexpr int Q = kBigChunkTab / kBlock;
+        unsigned long long en[Q], prev[Q];
+        int64_t slot[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            en[q] = s_tab[threadIdx.x + q * kBlock];  // the chunk's count of its label
+            slot[q] = int64_t(mix64(uint64_t(uint32_t(slot_label(en[q])))) & uint64_t(cap - 1));
+        }
+#pragma unroll
+        for (int q = 0; q < Q; ++q) prev[q] = slot_label(en[q]) >= 0 ? atomicCAS(&tab[slot[q]], kSlotEmpty, en[q])
+                                                                     : kSlotEmpty;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int Lq = slot_label(en[q]);
+            unsigned long long pv = prev[q];
+            int64_t sl = slot[q];
+            while (pv != kSlotEmpty) {  // kSlotEmpty: claimed with the count (or no label)
+                if (slot_label(pv) == Lq) {
+                    atomicAdd(&tab[sl], (unsigned long long)uint32_t(slot_count(en[q])));
                     break;
                 }
-                slot = (slot + 1) & (cap - 1);
+                sl = (sl + 1) & (cap - 1);
+                pv = atomicCAS(&tab[sl], kSlotEmpty, en[q]);
             }
         }
         __syncthreads();
@@ -918,7 +997,7 @@ __global__ __launch_bounds__(kBlock) void k_big_reduce(BigRows br, const int64_t
         if (cap <= kFusedCap) continue;  // k_big_fused's (uniform across the workgroup)
         const int64_t j = c - br.schunk[idx];
         const int64_t s0 = j * kSlotChunk, s1 = (j + 1) * kSlotChunk < cap ? (j + 1) * kSlotChunk : cap;
-        const int own = lab_in[v];
+        const int own = lab_in[br.base + idx];
         const unsigned long long* tab = br.tab + br.off[idx];
         if (kPass == 0) {
             int best = 0, oc = 0;
@@ -969,9 +1048,10 @@ __global__ __launch_bounds__(kFusedThreads) void k_big_fused(BigRows br, const i
         const int64_t v = br.list[idx];
         const int64_t cap = table_cap(rowptr[v + 1] - rowptr[v]);
         if (cap > kFusedCap) continue;  // uniform across the workgroup
-        const int own = lab_in[v];
+        const int64_t p = br.base + idx;
+        const int own = lab_in[p];
         if (converged) {  // the insert did not run: the table is still clear
-            if (threadIdx.x == 0) lab_out[v] = own;
+            if (threadIdx.x == 0) lab_out[p] = own;
             continue;
         }
         unsigned long long* tab = br.tab + br.off[idx];
@@ -1008,7 +1088,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_big_fused(BigRows br, const i
             cand = int(block_min_u64<kFusedThreads>(lbest, s_red64));
         }
         if (threadIdx.x == 0) {
-            lab_out[v] = is_active(v, key) ? cand : own;
+            lab_out[p] = is_active(v, key) ? cand : own;
             if (cand != own) *flag_next = 1u;
         }
         __syncthreads();  // every read of the table is done
@@ -1025,21 +1105,23 @@ __global__ void k_big_decide(BigRows br, const int64_t* rowptr, const int32_t* l
          idx += int64_t(gridDim.x) * blockDim.x) {
         const int64_t v = br.list[idx];
         if (skip_fused && table_cap(rowptr[v + 1] - rowptr[v]) <= kFusedCap) continue;
-        const int own = lab_in[v];
+        const int64_t p = br.base + idx;
+        const int own = lab_in[p];
         if (converged) {
-            lab_out[v] = own;
+            lab_out[p] = own;
             continue;
         }
         const int best = br.best[idx];
         const int cand = (best > 0 && br.own_cnt[idx] != best) ? int(br.lbest[idx]) : own;
-        lab_out[v] = is_active(v, key) ? cand : own;
+        lab_out[p] = is_active(v, key) ? cand : own;
         if (cand != own) *flag_next = 1u;
     }
 }
 
 // First sweep of the very long rows: per-row results reset (the tables are
 // not used), the smallest hash over every chunk of edges (combined with a 64-bit
-// atomic minimum), then the neighbour with that hash; k_big_decide finishes.
+// atomic minimum; the columns' list positions go to ncol), then the neighbour
+// with that hash; k_big_decide finishes.
 __global__ void k_big_first_reset(BigRows br) {
     const int64_t len = *br.len;
     for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < len;
@@ -1053,6 +1135,7 @@ __global__ void k_big_first_reset(BigRows br) {
 
 template <int kPass>
 __global__ __launch_bounds__(kBlock) void k_big_first(BigRows br, const int64_t* rowptr, const int32_t* col,
+                                                      const int64_t* roff, const int32_t* lpos, int32_t* ncol,
                                                       uint64_t key) {
     __shared__ uint64_t s_red64[kBlock / kWave];
     __shared__ int s_any[kBlock / kWave];
@@ -1068,8 +1151,10 @@ __global__ __launch_bounds__(kBlock) void k_big_first(BigRows br, const int64_t*
         if (kPass == 0) {
             uint64_t hb = ~0ull;
             bool any = false;
+            const int64_t shift = roff[br.base + idx] - a;  // entry e of the row goes to ncol[e + shift]
             for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
                 const int c = col[e];
+                ncol[e + shift] = lpos[c];
                 if (c == v) continue;
                 const uint64_t h = mix64(uint64_t(uint32_t(c)) ^ key);
                 hb = h < hb ? h : hb;
@@ -1092,6 +1177,12 @@ __global__ __launch_bounds__(kBlock) void k_big_first(BigRows br, const int64_t*
 }
 
 // --------------------------------------------------------------------- order
+
+// lab[list[p]] = lab_pos[p]: the labels from list positions to node ids.
+__global__ void k_labels_by_node(int64_t n, const int32_t* list, const int32_t* lab_pos, int32_t* lab) {
+    for (int64_t p = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; p < n; p += int64_t(gridDim.x) * blockDim.x)
+        lab[list[p]] = lab_pos[p];
+}
 
 // Sort key of row v: (label, dmax - off-diagonal entries) in bits_for(n) +
 // dbits bits, dmax the largest off-diagonal entry count (< 2^dbits).
@@ -1118,6 +1209,10 @@ struct ReorderWs {
     int32_t* blk_cnt;     // [kClasses * blocks]: rows of each class in each 256-row block
     int64_t* blk_off;     // [kClasses * blocks + 1]: their exclusive scan
     int32_t* list;        // [n]: the rows, class after class
+    int32_t* lpos;        // [n]: each row's position in list
+    uint32_t* ldeg;       // [n]: entry counts by list position
+    int64_t* roff;        // [n + 1]: their exclusive scan
+    int32_t* ncol;        // [nnz]: the rows' entries in list order, as list positions
     int64_t* class_info;  // [2 * kClasses + 2]: first list position and rows of each class; largest
                           // off-diagonal entry count; the CSR check's flags (low 32 bits)
     uint32_t* blk_max;    // [blocks]: largest off-diagonal entry count of each 256-row block
@@ -1152,6 +1247,10 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.blk_cnt = ws.take<int32_t>(size_t(kClasses * nblk));
     r.blk_off = ws.take<int64_t>(size_t(kClasses * nblk + 1));
     r.list = ws.take<int32_t>(n1);
+    r.lpos = ws.take<int32_t>(n1);
+    r.ldeg = ws.take<uint32_t>(n1);
+    r.roff = ws.take<int64_t>(n1 + 1);
+    r.ncol = ws.take<int32_t>(size_t(nnz > 0 ? nnz : 1));
     r.class_info = ws.take<int64_t>(2 * kClasses + 2);
     r.blk_max = ws.take<uint32_t>(size_t(nblk));
     r.huge_off = ws.take<int64_t>(n1 + 1);
@@ -1214,12 +1313,15 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     k_blocks_max<<<unsigned(cdiv(nblk, kMaxSpan)), 256, 0, stream>>>(nblk, r.blk_max, deg_max);
     GT_LAUNCH_CHECK("reorder_degree_max");
     if ((st = exclusive_scan_i32(r.blk_cnt, kClasses * nblk, r.blk_off, r.scan, stream)) != GT_OK) return st;
-    k_class_scatter<<<unsigned(nblk), kClsBlock, 0, stream>>>(n, rowptr, r.blk_off, nblk, r.list);
+    k_class_scatter<<<unsigned(nblk), kClsBlock, 0, stream>>>(n, rowptr, r.blk_off, nblk, r.list, r.lpos,
+                                                              r.ldeg);
     GT_LAUNCH_CHECK("reorder_class_scatter");
+    if ((st = exclusive_scan_u32(r.ldeg, n, r.roff, r.scan, stream)) != GT_OK) return st;
     k_class_totals<<<1, 64, 0, stream>>>(nblk, r.blk_off, r.class_info);
     GT_LAUNCH_CHECK("reorder_class_totals");
 
-    if ((st = iota_u32(reinterpret_cast<uint32_t*>(r.lab[0]), n, stream)) != GT_OK) return st;
+    // the labels are kept by list position and start as the node ids
+    GT_HIP(hipMemcpyAsync(r.lab[0], r.list, size_t(n) * sizeof(int32_t), hipMemcpyDeviceToDevice, stream));
     if ((st = fill_u32(r.flags, iters + 1, 0, stream)) != GT_OK) return st;
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
@@ -1236,8 +1338,8 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         len_of[c] = r.class_info + kClasses + c;
     }
     const int64_t n_huge = cnt[kClsHuge];
-    BigRows br{list_of[kClsHuge], len_of[kClsHuge], r.huge_off, r.huge_echunk, r.huge_schunk, r.tab,
-               r.big_best, r.big_own, r.big_hbest, r.big_lbest};
+    BigRows br{list_of[kClsHuge], info[kClsHuge], len_of[kClsHuge], r.huge_off, r.huge_echunk, r.huge_schunk,
+               r.tab, r.big_best, r.big_own, r.big_hbest, r.big_lbest};
     if (n_huge > 0) {  // the chunk numbering of the long rows' edges and table slots, and their table offsets
         k_big_prep<<<1, kPrepThreads, 0, stream>>>(list_of[kClsHuge], len_of[kClsHuge], rowptr, r.huge_echunk,
                                                     r.huge_schunk, r.huge_off);
@@ -1247,21 +1349,15 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     SmallRows sr;
     {
         const int cls[kSmLists] = {kClsWav, kClsS32, kClsS16, kClsS8, kClsS4};
-        const int64_t* lens[kSmLists];
-        const int32_t* lists[kSmLists];
-        for (int k = 0; k < kSmLists; ++k) {
-            lens[k] = len_of[cls[k]];
-            lists[k] = list_of[cls[k]];
-        }
-        const int64_t rows[kSmLists] = {cnt[kClsWav], cnt[kClsS32], cnt[kClsS16], cnt[kClsS8], cnt[kClsS4]};
-        const int per_block[kSmLists] = {kBlock / kWave, kBlock / kSub32, kBlock / kSub16, kBlock / kSub8,
-                                         kBlock / kSub4};
+        const int per_wave[kSmLists] = {1, kWave / kSub32, kWave / kSub16, kWave / kSub8, kWave / kSub4};
+        sr.list = r.list;
         unsigned at = 0;
         for (int k = 0; k < kSmLists; ++k) {
-            sr.list[k] = lists[k];
-            sr.len[k] = lens[k];
+            const int64_t rows = cnt[cls[k]];
+            sr.base[k] = info[cls[k]];
+            sr.len[k] = rows;
             sr.first[k] = at;
-            if (rows[k] > 0) at += grid_cap(rows[k], per_block[k], 16384);
+            if (rows > 0) at += grid_cap(rows, int64_t(per_wave[k]) * (kBlock / kWave), 16384);
         }
         sr.first[kSmLists] = at;
     }
@@ -1276,26 +1372,27 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         if (t == 0) {  // labels are the node ids: a minimum over each row's columns
             if (n_huge > 0) {
                 k_big_first_reset<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br);
-                k_big_first<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, key);
-                k_big_first<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, key);
+                k_big_first<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, r.roff, r.lpos, r.ncol, key);
+                k_big_first<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, r.roff, r.lpos, r.ncol, key);
                 GT_LAUNCH_CHECK("reorder_big_first");
                 k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, rowptr, in, out, key, r.flags,
                                                                               r.flags + 1, false);
                 GT_LAUNCH_CHECK("reorder_big_decide");
             }
             if (sr.first[kSmLists] > 0) {
-                k_lp_small<true><<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, in, out, key, r.flags,
-                                                                           r.flags + 1);
+                k_first_small<<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, r.roff, r.lpos, r.ncol,
+                                                                        out, key, r.flags + 1);
                 GT_LAUNCH_CHECK("reorder_first_small");
             }
             if (cnt[kClsWmed] > 0) {
-                k_first_wide<kWave><<<gwt, kBlock, 0, stream>>>(list_of[kClsWmed], len_of[kClsWmed], rowptr, col,
-                                                               out, key, r.flags + 1);
+                k_first_wide<kWave><<<gwt, kBlock, 0, stream>>>(r.list, info[kClsWmed], len_of[kClsWmed], rowptr,
+                                                               col, r.roff, r.lpos, r.ncol, out, key, r.flags + 1);
                 GT_LAUNCH_CHECK("reorder_first_wave");
             }
             if (cnt[kClsMed] > 0) {
-                k_first_wide<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(list_of[kClsMed], len_of[kClsMed], rowptr,
-                                                                        col, out, key, r.flags + 1);
+                k_first_wide<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(r.list, info[kClsMed], len_of[kClsMed],
+                                                                        rowptr, col, r.roff, r.lpos, r.ncol, out,
+                                                                        key, r.flags + 1);
                 GT_LAUNCH_CHECK("reorder_first_block");
             }
             continue;
@@ -1307,7 +1404,7 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
                 k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp, t == 1);
                 GT_LAUNCH_CHECK("reorder_big_clear");
             }
-            k_big_insert<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, in, fp);
+            k_big_insert<<<kBigGrid, kBlock, 0, stream>>>(br, r.roff, r.ncol, in, fp);
             GT_LAUNCH_CHECK("reorder_big_insert");
             k_big_fused<<<unsigned(n_huge < 2048 ? n_huge : 2048), kFusedThreads, 0, stream>>>(br, rowptr, in, out,
                                                                                              key, fp,
@@ -1324,22 +1421,25 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
             }
         }
         if (sr.first[kSmLists] > 0) {
-            k_lp_small<false><<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, in, out, key, r.flags + t,
-                                                                         r.flags + t + 1);
+            k_lp_small<<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, r.roff, r.ncol, in, out, key, r.flags + t,
+                                                                  r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_small");
         }
         if (cnt[kClsWmed] > 0) {
-            k_lp_wavetab<<<gwt, kBlock, 0, stream>>>(list_of[kClsWmed], len_of[kClsWmed], rowptr, col, in, out, key,
-                                                     r.flags + t, r.flags + t + 1);
+            k_lp_wavetab<<<gwt, kBlock, 0, stream>>>(r.list, info[kClsWmed], len_of[kClsWmed], r.roff, r.ncol, in,
+                                                     out, key, r.flags + t, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_wavetab");
         }
         if (cnt[kClsMed] > 0) {
-            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(list_of[kClsMed], len_of[kClsMed], rowptr, col, in,
-                                                                  out, key, r.flags + t, r.flags + t + 1);
+            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(r.list, info[kClsMed], len_of[kClsMed], r.roff,
+                                                                  r.ncol, in, out, key, r.flags + t,
+                                                                  r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_lds");
         }
     }
-    const int32_t* final_lab = r.lab[iters & 1];
+    int32_t* final_lab = r.lab[(iters + 1) & 1];
+    k_labels_by_node<<<g, 256, 0, stream>>>(n, r.list, r.lab[iters & 1], final_lab);
+    GT_LAUNCH_CHECK("reorder_labels_by_node");
     const uint32_t dmax = uint32_t(info[2 * kClasses]);
     const int dbits = bits_for(int64_t(dmax) + 1);
     k_order_keys<<<g, 256, 0, stream>>>(n, final_lab, r.deg_off, dmax, dbits, r.sort_keys);
