@@ -556,7 +556,8 @@ struct TilesWs {
     uint32_t* counts;          // per tile column
     // The count results, one contiguous range of the workspace (kept_words
     // 8-byte words from kept_begin: dense_per_tilerow .. rows), so that
-    // gt_build_tiles can take them from gt_tiles_count's workspace.
+    // gt_build_tiles can take them from gt_tiles_count's workspace.  The
+    // medium-row list is among them.
     int32_t* dense_per_tilerow;
     int32_t* sp_deg;
     int64_t* tmp_tile_rowptr;
@@ -572,12 +573,12 @@ struct TilesWs {
     int32_t* heavy_list;   // [kMaxHeavy]: the tile row of each heavy count row
     int32_t* heavy_n;      // how many heavy count rows
     uint32_t* heavy_cnt;   // [kMaxHeavy, R]: edges of each heavy tile row per tile column
+    int32_t* med_list;     // [n]: the medium rows
+    int64_t* med_info;     // [2]: their list start and number
     uint32_t* rows;        // [nnz]: the row of each edge, then (sorted with the tags) the remainder transpose's rows
     const uint64_t* kept_begin;
     int64_t kept_words;    // 8-byte words of the count results' range
     int8_t* med_cls;       // [n]: medium-row class of each row
-    int32_t* med_list;     // [n]: the medium rows
-    int64_t* med_info;     // [2]: their list start and number
     PartitionTmp part;
     int32_t* segcnt;       // [2 * long chunks]: remainder edges of each long-row segment
     int64_t* segoff;       // [2 * long chunks + 1]
@@ -613,6 +614,8 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
     t.heavy_list = ws.take<int32_t>(size_t(kMaxHeavy));
     t.heavy_n = ws.take<int32_t>(2);
     t.heavy_cnt = ws.take<uint32_t>(size_t(kMaxHeavy) * R);
+    t.med_list = ws.take<int32_t>(size_t(n1 + (n1 & 1)));
+    t.med_info = ws.take<int64_t>(2);
     t.rows = ws.take<uint32_t>(size_t(e1 + (e1 & 1)));  // an even count: the range ends on an 8-byte word
     {
         const char* b = reinterpret_cast<const char*>(t.dense_per_tilerow);
@@ -621,8 +624,6 @@ TilesWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t T) {
         t.kept_words = int64_t((e - b) / 8);
     }
     t.med_cls = ws.take<int8_t>(n1);
-    t.med_list = ws.take<int32_t>(n1);
-    t.med_info = ws.take<int64_t>(2);
     t.part = partition_tmp(ws, n1);
     const int64_t segs = 2 * long_chunks_of(e1);
     t.segcnt = ws.take<int32_t>(size_t(segs));
@@ -675,6 +676,72 @@ gt_status ws_checksum(const TilesWs& t, hipStream_t s) {
     k_ws_checksum<<<grid_for(t.kept_words, 256, kCsumBlocks), 256, 0, s>>>(t.kept_begin, t.kept_words, t.csum);
     GT_LAUNCH_CHECK("tiles_checksum");
     return GT_OK;
+}
+
+// The dense tiles grouped by tile column for plans of at most
+// kSmallTranspose tiles, in one workgroup: column counts in LDS, their scan
+// (tileT_ptr), then the tiles placed in index order, 64 at a time by one
+// wavefront.  A tile row holds at most one tile per column, and tile indices
+// run in (I, J) order, so placing them in index order keeps each column's
+// tiles in ascending I: within a 64-tile slice, a tile's rank among the
+// slice's tiles of its column comes from comparing the slice's columns by
+// readlane.
+constexpr int kSmallTranspose = 8192;
+constexpr int kTransposeThreads = 1024;
+__global__ __launch_bounds__(kTransposeThreads) void k_tile_transpose(int64_t d, int R, const int32_t* tile_col,
+                                                                      int64_t* tileT_ptr, int32_t* tileT_idx) {
+    __shared__ int s_next[kMaxR];
+    __shared__ int s_part[kTransposeThreads / kWave];
+    for (int J = threadIdx.x; J < R; J += kTransposeThreads) s_next[J] = 0;
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < d; i += kTransposeThreads) atomicAdd(&s_next[tile_col[i]], 1);
+    __syncthreads();
+    // exclusive scan: each thread a run of `per` consecutive columns
+    const int per = (R + kTransposeThreads - 1) / kTransposeThreads;
+    const int j0 = threadIdx.x * per, j1 = j0 + per < R ? j0 + per : R;
+    int sum = 0;
+    for (int J = j0; J < j1; ++J) sum += s_next[J];
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    int x = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s_part[w] = x;
+    __syncthreads();
+    int before = x - sum;
+    for (int k = 0; k < w; ++k) before += s_part[k];
+    for (int J = j0; J < j1; ++J) {
+        const int c = s_next[J];
+        tileT_ptr[J] = before;
+        s_next[J] = before;
+        before += c;
+    }
+    if (threadIdx.x == 0) tileT_ptr[R] = d;
+    __syncthreads();
+    if (threadIdx.x >= kWave) return;
+    for (int64_t base = 0; base < d; base += kWave) {
+        const int64_t i = base + lane;
+        const int J = i < d ? tile_col[i] : -1;
+        int rank = 0, same = 0;
+        for (int k = 0; k < kWave; ++k) {
+            const int Jk = __builtin_amdgcn_readlane(J, k);
+            if (Jk == J) {
+                rank += k < lane ? 1 : 0;
+                ++same;
+            }
+        }
+        const int pos = J >= 0 ? s_next[J] + rank : 0;
+        __builtin_amdgcn_wave_barrier();  // every lane has read its column's next slot
+        if (J >= 0) {
+            tileT_idx[pos] = int32_t(i);
+            if (rank == same - 1) s_next[J] = pos + 1;  // the slice's last tile of the column
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
 }
 
 // What gt_tiles_count leaves in its workspace, next to the count results: its
@@ -747,13 +814,20 @@ gt_status medium_rows(int64_t n, const int64_t* rowptr, TilesWs& t, hipStream_t 
     return partition_rows(t.med_cls, n, 1, t.med_list, t.med_info, t.part, stream);
 }
 
+// The heavy tile rows and their zeroed count rows: reads rowptr only, at
+// positions clamped to [0, n], so it may run before the CSR check is read back.
+gt_status heavy_prelude(int64_t n, const int64_t* rowptr, int32_t T, TilesWs& t, hipStream_t stream) {
+    const int R = int(cdiv(n, T));
+    k_heavy_slots<<<1, kTileThreads, 0, stream>>>(n, rowptr, T, R, t.heavy_slot, t.heavy_list, t.heavy_n);
+    GT_LAUNCH_CHECK("tiles_heavy_slots");
+    return fill_u32(t.heavy_cnt, int64_t(kMaxHeavy) * R, 0u, stream);
+}
+
+// The rest of the count pass, after heavy_prelude.
 gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T, uint32_t tau_ppm,
                      TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, hipStream_t stream) {
     gt_status st;
     const int R = int(cdiv(n, T));
-    k_heavy_slots<<<1, kTileThreads, 0, stream>>>(n, rowptr, T, R, t.heavy_slot, t.heavy_list, t.heavy_n);
-    GT_LAUNCH_CHECK("tiles_heavy_slots");
-    if ((st = fill_u32(t.heavy_cnt, int64_t(kMaxHeavy) * R, 0u, stream)) != GT_OK) return st;
     k_heavy_count<<<1024, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, t.heavy_list, t.heavy_n, t.heavy_cnt);
     GT_LAUNCH_CHECK("tiles_heavy_count");
     k_tiles<false><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg,
@@ -812,6 +886,7 @@ extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowpt
     Ws ws(ws_ptr);
     TilesWs t = carve(ws, n, nnz, T);
     if ((st = launch_validate_csr(n, nnz, rowptr, col, t.flags, stream)) != GT_OK) return st;
+    if ((st = heavy_prelude(n, rowptr, T, t, stream)) != GT_OK) return st;
     if ((st = read_validation(t.flags, stream)) != GT_OK) return st;
     if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
         return st;
@@ -872,15 +947,34 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         for (int i = 0; i < kRecordWords; ++i) rec.w[i] = words[i];
         const uint64_t have = words[kRecordWords];
         reuse = record_matches(rec, n, nnz, rowptr, col, T, tau_ppm) && rec.w[6] == have;
-        if (rec.w[0] == kRecordTag && (st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK)
+        if (!reuse && rec.w[0] == kRecordTag &&
+            (st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK)
             return st;
     }
+    if (!reuse) {
+        if ((st = heavy_prelude(n, rowptr, T, t, stream)) != GT_OK) return st;
+        if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) !=
+            GT_OK)
+            return st;
+    }
+    // the fill reads the offsets where the count pass left them; the plan's copies and the other small
+    // launches follow the fill's first kernel, so that kernel starts right after the check above
+    const int64_t* trp = reuse ? t.tmp_tile_rowptr : plan->tile_rowptr;
+    const int64_t* srp = reuse ? t.tmp_sp_rowptr : plan->sp_rowptr;
+    const int64_t words = plan->n_dense * int64_t(T) * (T / 32);
+    if ((st = fill_u32(plan->tile_mask, words, 0u, stream)) != GT_OK) return st;
+    if (plan->tile_pos && plan->n_dense > 0 &&
+        (st = fill_u32(reinterpret_cast<uint32_t*>(plan->tile_pos), plan->n_dense * T, 0u, stream)) != GT_OK)
+        return st;
+    k_tiles<true><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, trp,
+                                              plan->tile_col, plan->tile_nnz, plan->tile_mask, srp, plan->sp_col,
+                                              nullptr, nullptr, t.W, nullptr, nullptr, plan->sp_pos, plan->tile_pos,
+                                              t.heavy_slot, t.heavy_cnt);
+    GT_LAUNCH_CHECK("tiles_fill");
     if (reuse) {
+        if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK) return st;  // used once
         if ((st = copy_bytes(plan->tile_rowptr, t.tmp_tile_rowptr, size_t(R + 1) * 8, stream)) != GT_OK) return st;
         if ((st = copy_bytes(plan->sp_rowptr, t.tmp_sp_rowptr, size_t(n + 1) * 8, stream)) != GT_OK) return st;
-    } else if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) !=
-               GT_OK) {
-        return st;
     }
     {
         const unsigned g = grid_for(n, 256, 8192);
@@ -893,20 +987,10 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
             GT_LAUNCH_CHECK("tiles_long_col_list");
         }
     }
-    const int64_t words = plan->n_dense * int64_t(T) * (T / 32);
-    if ((st = fill_u32(plan->tile_mask, words, 0u, stream)) != GT_OK) return st;
-    if (plan->tile_pos && plan->n_dense > 0 &&
-        (st = fill_u32(reinterpret_cast<uint32_t*>(plan->tile_pos), plan->n_dense * T, 0u, stream)) != GT_OK)
-        return st;
-    k_tiles<true><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, plan->tile_rowptr,
-                                              plan->tile_col, plan->tile_nnz, plan->tile_mask, plan->sp_rowptr,
-                                              plan->sp_col, nullptr, nullptr, t.W, nullptr, nullptr, plan->sp_pos,
-                                              plan->tile_pos, t.heavy_slot, t.heavy_cnt);
-    GT_LAUNCH_CHECK("tiles_fill");
-    if (reuse && (st = medium_rows(n, rowptr, t, stream)) != GT_OK) return st;  // else the count pass made it
+    // the medium-row list: the count pass made it (here, or in gt_tiles_count's workspace, checked above)
     k_tiles_med<true><<<grid_for(n, 4, 16384), 256, 0, stream>>>(
         n, t.med_list, t.med_info + 1, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr, nullptr,
-        plan->tile_rowptr, plan->tile_mask, plan->sp_rowptr, plan->sp_col, plan->sp_pos, plan->tile_pos);
+        trp, plan->tile_mask, srp, plan->sp_col, plan->sp_pos, plan->tile_pos);
     GT_LAUNCH_CHECK("tiles_fill_medium");
     if (nnz > kLongRow) {
         const int64_t segs = 2 * long_chunks_of(nnz);
@@ -916,8 +1000,8 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         GT_LAUNCH_CHECK("tiles_long_segs");
         if ((st = exclusive_scan_i32(t.segcnt, segs, t.segoff, t.scan, stream)) != GT_OK) return st;
         k_tiles_long_fill<<<long_grid(nnz), kThreads, 0, stream>>>(
-            n, nnz, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.segoff, plan->tile_rowptr, plan->tile_mask,
-            plan->sp_rowptr, plan->sp_col, plan->sp_pos, plan->tile_pos);
+            n, nnz, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.segoff, trp, plan->tile_mask, srp,
+            plan->sp_col, plan->sp_pos, plan->tile_pos);
         GT_LAUNCH_CHECK("tiles_long_fill");
     }
     // remainder transpose: the count pass sorted it; its first nnz_sparse rows are the remainder's
@@ -929,6 +1013,12 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     if ((st = copy_bytes(plan->sp_colptr, t.colptr, size_t(n + 1) * 8, stream)) != GT_OK) return st;
     // tiles grouped by column: stable sort of (J, tile index) by J
     const int64_t d = plan->n_dense;
+    if (d <= kSmallTranspose) {
+        k_tile_transpose<<<1, kTransposeThreads, 0, stream>>>(d, R, plan->tile_col, plan->tileT_ptr,
+                                                              plan->tileT_idx);
+        GT_LAUNCH_CHECK("tiles_tileT_small");
+        return GT_OK;
+    }
     if ((st = fill_u32(t.counts, R, 0u, stream)) != GT_OK) return st;
     if (d > 0) {
         if ((st = count_keys(plan->tile_col, d, t.counts, stream)) != GT_OK) return st;

@@ -307,13 +307,26 @@ class AutoTuner:
         return lv.value, num.value, den.value
 
 
+_ITEMSIZE = {torch.int64: 8, torch.int32: 4}
+
+
 @dataclass
 class Plan:
-    """A tile plan: the device arrays and the C struct pointing at them."""
+    """A tile plan: the device arrays and the C struct pointing at them.  The arrays live in one device buffer;
+    `arrays` gives tensor views of them (made on first use)."""
 
     c: GtTiles
-    arrays: dict
+    buffer: torch.Tensor
+    layout: dict  # name -> (byte offset, elements, dtype)
     nnz: int = -1  # edges of the input CSR (remainder plus dense tiles)
+    _views: dict | None = None
+
+    @property
+    def arrays(self) -> dict:
+        if self._views is None:
+            self._views = {k: self.buffer[o:o + cnt * _ITEMSIZE[dt]].view(dt)
+                           for k, (o, cnt, dt) in self.layout.items()}
+        return self._views
 
     @property
     def n(self):
@@ -369,27 +382,22 @@ def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: 
     _check(lib.gt_tiles_count(n, nnz, _ptr(rowptr), _ptr(col), T, tau_ppm, ctypes.byref(c), _ptr(ws), ws.numel(), st),
            "gt_tiles_count")
     R, nd, ns = c.n_row_tiles, c.n_dense, c.nnz_sparse
-    i64 = dict(dtype=torch.int64, device=dev)
-    i32 = dict(dtype=torch.int32, device=dev)
-    arrays = {
-        "tile_rowptr": torch.empty(R + 1, **i64),
-        "tile_col": torch.empty(nd, **i32),
-        "tile_nnz": torch.empty(nd, **i32),
-        "tile_mask": torch.empty(nd * T * T // 32, **i32),
-        "sp_rowptr": torch.empty(n + 1, **i64),
-        "sp_col": torch.empty(ns, **i32),
-        "sp_colptr": torch.empty(n + 1, **i64),
-        "sp_row": torch.empty(ns, **i32),
-        "tileT_ptr": torch.empty(R + 1, **i64),
-        "tileT_idx": torch.empty(nd, **i32),
-        "long_rows": torch.empty(c.n_long_rows, **i32),
-        "long_cols": torch.empty(c.n_long_cols, **i32),
-    }
+    i64, i32 = torch.int64, torch.int32
+    sizes = [("tile_rowptr", R + 1, i64), ("tile_col", nd, i32), ("tile_nnz", nd, i32),
+             ("tile_mask", nd * T * T // 32, i32), ("sp_rowptr", n + 1, i64), ("sp_col", ns, i32),
+             ("sp_colptr", n + 1, i64), ("sp_row", ns, i32), ("tileT_ptr", R + 1, i64), ("tileT_idx", nd, i32),
+             ("long_rows", c.n_long_rows, i32), ("long_cols", c.n_long_cols, i32)]
     if edge_positions:
-        arrays["sp_pos"] = torch.empty(ns, **i32)
-        arrays["tile_pos"] = torch.empty(nd * T, **i32)
-    for k, v in arrays.items():
-        setattr(c, k, v.data_ptr())
+        sizes += [("sp_pos", ns, i32), ("tile_pos", nd * T, i32)]
+    # one allocation for all of them, each array at a 256-byte boundary
+    layout, at = {}, 0
+    for name, cnt, dt in sizes:
+        layout[name] = (at, cnt, dt)
+        at += (cnt * _ITEMSIZE[dt] + 255) & ~255
+    buf = torch.empty(max(at, 256), dtype=torch.uint8, device=dev)
+    base = buf.data_ptr()
+    for name, (off, _, _) in layout.items():
+        setattr(c, name, base + off)
     if between is not None:
         between(ws)
     if build_ws is not None:
@@ -397,8 +405,7 @@ def build_tiles(rowptr: torch.Tensor, col: torch.Tensor, T: int = 128, tau_ppm: 
         ws = build_ws
     _check(lib.gt_build_tiles(n, nnz, _ptr(rowptr), _ptr(col), T, tau_ppm, ctypes.byref(c), _ptr(ws), ws.numel(), st),
            "gt_build_tiles")
-    arrays["tile_mask"] = arrays["tile_mask"].view(torch.int32)
-    return Plan(c=c, arrays=arrays, nnz=nnz)
+    return Plan(c=c, buffer=buf, layout=layout, nnz=nnz)
 
 
 # ------------------------------------------------------------------------------ attention

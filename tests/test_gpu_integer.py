@@ -144,6 +144,36 @@ def test_tiles_bit_exact(gt, name, rowptr, col, T):
     assert n >= 1
 
 
+@pytest.mark.parametrize("tile_rows,small", [(2048, True), (4096, False)])
+def test_tile_transpose_both_paths(gt, tile_rows, small):
+    # plans of up to 8192 dense tiles group their tiles by column in one workgroup, larger ones by radix sort.
+    # Three tiles per tile row at threshold 0 (every tile with an edge is dense): the diagonal, ten tile
+    # columns to the right, and one of the first seven columns, so those seven columns hold hundreds of tiles
+    # each.  Checked against the definitions: the dense tiles are the occupied (I, J) in (I, J) order, and
+    # the transpose is their stable order by J.
+    T = 64
+    n = T * tile_rows
+    i = np.arange(n, dtype=np.int64)
+    u = np.concatenate([i, i, i])
+    v = np.concatenate([i, (i + 10 * T) % n, i % T + T * ((i // T) % 7)])
+    rowptr, col = csr_from_pairs(n, u, v, symmetric=False, self_loops=False)
+    say("tile transpose", tile_rows, len(col))
+    rp, cl = dev_csr(rowptr, col)
+    plan = gt.build_tiles(rp, cl, T, 0)
+    got = plan.to_numpy()
+    rows = np.repeat(np.arange(n, dtype=np.int64), np.diff(rowptr))
+    occupied = np.unique((rows // T) * tile_rows + col.astype(np.int64) // T)
+    assert (plan.n_dense <= 8192) == small
+    np.testing.assert_array_equal(got["tile_col"], occupied % tile_rows)
+    np.testing.assert_array_equal(got["tile_rowptr"],
+                                  np.concatenate([[0], np.cumsum(np.bincount(occupied // tile_rows,
+                                                                             minlength=tile_rows))]))
+    np.testing.assert_array_equal(got["tileT_idx"], np.argsort(occupied % tile_rows, kind="stable"))
+    np.testing.assert_array_equal(got["tileT_ptr"],
+                                  np.concatenate([[0], np.cumsum(np.bincount(occupied % tile_rows,
+                                                                             minlength=tile_rows))]))
+
+
 @pytest.mark.parametrize("name", ["hubs_6000", "three_hubs_30000", "c3@0.02", "b1@0.1"])
 def test_tiles_counts_taken_or_recounted(gt, name):
     # gt_build_tiles takes gt_tiles_count's counts from the shared workspace only while they are unchanged
