@@ -4,9 +4,38 @@
 // the caller's workspace through gt::Ws.
 #pragma once
 
+#include <mutex>
+
 #include "common.h"
 
 namespace gt {
+
+// ---- work spread over the caller's stream and the library's own side streams
+// Two streams per device, created on first use at the default priority and
+// kept until the process ends, with the events that order them.  A Spread
+// holds the device's lock from spread_open until it is destroyed, so calls on
+// one device take turns enqueueing (their kernels still overlap on the GPU).
+// fork(): the side streams wait for the work enqueued on the caller's stream
+// so far; join(): the caller's stream waits for the work enqueued on the side
+// streams.  A Spread still forked when destroyed joins first, so the caller's
+// stream never finishes before the side streams' work.  Where the caller's
+// stream is not on the current device, everything runs on the caller's stream.
+constexpr int kSideStreams = 2;
+struct Spread {
+    hipStream_t main = nullptr;
+    hipStream_t side[kSideStreams] = {};
+    hipEvent_t fork_ev = nullptr;
+    hipEvent_t join_ev[kSideStreams] = {};
+    bool on = false;      // side streams in use
+    bool forked = false;
+    std::unique_lock<std::mutex> lock;
+    // stream k: 0 the caller's, 1 .. kSideStreams the side streams
+    hipStream_t at(int k) const { return (k == 0 || !on) ? main : side[k - 1]; }
+    gt_status fork();
+    gt_status join();
+    ~Spread();
+};
+gt_status spread_open(hipStream_t main, Spread* sp);
 
 // ---- fills
 gt_status fill_u32(uint32_t* p, int64_t n, uint32_t value, hipStream_t s);

@@ -37,6 +37,68 @@ gt_status iota_u32(uint32_t* p, int64_t n, hipStream_t s) {
     GT_LAUNCH_CHECK("iota_u32");
     return GT_OK;
 }
+// ============================================================= side streams
+
+namespace {
+constexpr int kSpreadDevices = 64;
+struct DeviceSide {
+    std::mutex mu;
+    bool ready = false;
+    hipStream_t side[kSideStreams] = {};
+    hipEvent_t fork_ev = nullptr;
+    hipEvent_t join_ev[kSideStreams] = {};
+};
+DeviceSide g_side[kSpreadDevices];
+}  // namespace
+
+gt_status spread_open(hipStream_t main, Spread* sp) {
+    sp->main = main;
+    sp->on = false;
+    int dev = -1;
+    GT_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kSpreadDevices) return GT_OK;
+    if (main) {
+        hipDevice_t sdev = -1;
+        GT_HIP(hipStreamGetDevice(main, &sdev));
+        if (sdev != dev) return GT_OK;
+    }
+    DeviceSide& d = g_side[dev];
+    sp->lock = std::unique_lock<std::mutex>(d.mu);
+    if (!d.ready) {
+        for (int k = 0; k < kSideStreams; ++k) GT_HIP(hipStreamCreateWithFlags(&d.side[k], hipStreamNonBlocking));
+        GT_HIP(hipEventCreateWithFlags(&d.fork_ev, hipEventDisableTiming));
+        for (int k = 0; k < kSideStreams; ++k) GT_HIP(hipEventCreateWithFlags(&d.join_ev[k], hipEventDisableTiming));
+        d.ready = true;
+    }
+    for (int k = 0; k < kSideStreams; ++k) {
+        sp->side[k] = d.side[k];
+        sp->join_ev[k] = d.join_ev[k];
+    }
+    sp->fork_ev = d.fork_ev;
+    sp->on = true;
+    return GT_OK;
+}
+
+gt_status Spread::fork() {
+    if (!on) return GT_OK;
+    GT_HIP(hipEventRecord(fork_ev, main));
+    for (int k = 0; k < kSideStreams; ++k) GT_HIP(hipStreamWaitEvent(side[k], fork_ev, 0));
+    forked = true;
+    return GT_OK;
+}
+
+gt_status Spread::join() {
+    if (!on || !forked) return GT_OK;
+    for (int k = 0; k < kSideStreams; ++k) {
+        GT_HIP(hipEventRecord(join_ev[k], side[k]));
+        GT_HIP(hipStreamWaitEvent(main, join_ev[k], 0));
+    }
+    forked = false;
+    return GT_OK;
+}
+
+Spread::~Spread() { (void)join(); }
+
 gt_status copy_bytes(void* dst, const void* src, int64_t bytes, hipStream_t s) {
     if (bytes <= 0) return GT_OK;
     GT_HIP(hipMemcpyAsync(dst, src, size_t(bytes), hipMemcpyDeviceToDevice, s));

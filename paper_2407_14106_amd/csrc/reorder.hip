@@ -1365,77 +1365,86 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     const bool giant = info[2 * kClasses] + 1 > kFusedCap / 2;
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
     const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
+    // The classes of a sweep read the sweep's input labels and write disjoint rows of its output: they run
+    // side by side, the short rows on the caller's stream, the long rows on one side stream, the rows of
+    // 65 to 4096 entries on the other; each sweep starts when the previous one has finished on all three.
+    Spread sp;
+    if ((st = spread_open(stream, &sp)) != GT_OK) return st;
+    const hipStream_t s_short = sp.at(0), s_big = sp.at(1), s_wide = sp.at(2);
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
         const int32_t* in = r.lab[t & 1];
         int32_t* out = r.lab[(t + 1) & 1];
+        if ((st = sp.fork()) != GT_OK) return st;
         if (t == 0) {  // labels are the node ids: a minimum over each row's columns
             if (n_huge > 0) {
-                k_big_first_reset<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br);
-                k_big_first<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, r.roff, r.lpos, r.ncol, key);
-                k_big_first<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, col, r.roff, r.lpos, r.ncol, key);
+                k_big_first_reset<<<grid_for(n_huge, 256, 1024), 256, 0, s_big>>>(br);
+                k_big_first<0><<<kBigGrid, kBlock, 0, s_big>>>(br, rowptr, col, r.roff, r.lpos, r.ncol, key);
+                k_big_first<1><<<kBigGrid, kBlock, 0, s_big>>>(br, rowptr, col, r.roff, r.lpos, r.ncol, key);
                 GT_LAUNCH_CHECK("reorder_big_first");
-                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, rowptr, in, out, key, r.flags,
-                                                                              r.flags + 1, false);
+                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, s_big>>>(br, rowptr, in, out, key, r.flags,
+                                                                             r.flags + 1, false);
                 GT_LAUNCH_CHECK("reorder_big_decide");
             }
             if (sr.first[kSmLists] > 0) {
-                k_first_small<<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, rowptr, col, r.roff, r.lpos, r.ncol,
-                                                                        out, key, r.flags + 1);
+                k_first_small<<<sr.first[kSmLists], kBlock, 0, s_short>>>(sr, rowptr, col, r.roff, r.lpos, r.ncol,
+                                                                         out, key, r.flags + 1);
                 GT_LAUNCH_CHECK("reorder_first_small");
             }
             if (cnt[kClsWmed] > 0) {
-                k_first_wide<kWave><<<gwt, kBlock, 0, stream>>>(r.list, info[kClsWmed], len_of[kClsWmed], rowptr,
+                k_first_wide<kWave><<<gwt, kBlock, 0, s_wide>>>(r.list, info[kClsWmed], len_of[kClsWmed], rowptr,
                                                                col, r.roff, r.lpos, r.ncol, out, key, r.flags + 1);
                 GT_LAUNCH_CHECK("reorder_first_wave");
             }
             if (cnt[kClsMed] > 0) {
-                k_first_wide<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(r.list, info[kClsMed], len_of[kClsMed],
+                k_first_wide<kMedBlock><<<gmed, kMedBlock, 0, s_wide>>>(r.list, info[kClsMed], len_of[kClsMed],
                                                                         rowptr, col, r.roff, r.lpos, r.ncol, out,
                                                                         key, r.flags + 1);
                 GT_LAUNCH_CHECK("reorder_first_block");
             }
+            if ((st = sp.join()) != GT_OK) return st;
             continue;
         }
         if (n_huge > 0) {
             const uint32_t* fp = r.flags + t;
             // the tables' first use clears them all; later, k_big_fused clears its own
             if (t == 1 || giant) {
-                k_big_clear<<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, fp, t == 1);
+                k_big_clear<<<kBigGrid, kBlock, 0, s_big>>>(br, rowptr, fp, t == 1);
                 GT_LAUNCH_CHECK("reorder_big_clear");
             }
-            k_big_insert<<<kBigGrid, kBlock, 0, stream>>>(br, r.roff, r.ncol, in, fp);
+            k_big_insert<<<kBigGrid, kBlock, 0, s_big>>>(br, r.roff, r.ncol, in, fp);
             GT_LAUNCH_CHECK("reorder_big_insert");
-            k_big_fused<<<unsigned(n_huge < 2048 ? n_huge : 2048), kFusedThreads, 0, stream>>>(br, rowptr, in, out,
-                                                                                             key, fp,
-                                                                                             r.flags + t + 1);
+            k_big_fused<<<unsigned(n_huge < 2048 ? n_huge : 2048), kFusedThreads, 0, s_big>>>(br, rowptr, in, out,
+                                                                                            key, fp,
+                                                                                            r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_big_fused");
             if (giant) {
-                k_big_reduce<0><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
-                k_big_reduce<1><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
-                k_big_reduce<2><<<kBigGrid, kBlock, 0, stream>>>(br, rowptr, in, key, fp);
+                k_big_reduce<0><<<kBigGrid, kBlock, 0, s_big>>>(br, rowptr, in, key, fp);
+                k_big_reduce<1><<<kBigGrid, kBlock, 0, s_big>>>(br, rowptr, in, key, fp);
+                k_big_reduce<2><<<kBigGrid, kBlock, 0, s_big>>>(br, rowptr, in, key, fp);
                 GT_LAUNCH_CHECK("reorder_big_reduce");
-                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, stream>>>(br, rowptr, in, out, key, fp,
-                                                                              r.flags + t + 1, true);
+                k_big_decide<<<grid_for(n_huge, 256, 1024), 256, 0, s_big>>>(br, rowptr, in, out, key, fp,
+                                                                             r.flags + t + 1, true);
                 GT_LAUNCH_CHECK("reorder_big_decide");
             }
         }
         if (sr.first[kSmLists] > 0) {
-            k_lp_small<<<sr.first[kSmLists], kBlock, 0, stream>>>(sr, r.roff, r.ncol, in, out, key, r.flags + t,
-                                                                  r.flags + t + 1);
+            k_lp_small<<<sr.first[kSmLists], kBlock, 0, s_short>>>(sr, r.roff, r.ncol, in, out, key, r.flags + t,
+                                                                   r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_small");
         }
         if (cnt[kClsWmed] > 0) {
-            k_lp_wavetab<<<gwt, kBlock, 0, stream>>>(r.list, info[kClsWmed], len_of[kClsWmed], r.roff, r.ncol, in,
+            k_lp_wavetab<<<gwt, kBlock, 0, s_wide>>>(r.list, info[kClsWmed], len_of[kClsWmed], r.roff, r.ncol, in,
                                                      out, key, r.flags + t, r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_wavetab");
         }
         if (cnt[kClsMed] > 0) {
-            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, stream>>>(r.list, info[kClsMed], len_of[kClsMed], r.roff,
+            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, s_wide>>>(r.list, info[kClsMed], len_of[kClsMed], r.roff,
                                                                   r.ncol, in, out, key, r.flags + t,
                                                                   r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_lds");
         }
+        if ((st = sp.join()) != GT_OK) return st;
     }
     int32_t* final_lab = r.lab[(iters + 1) & 1];
     k_labels_by_node<<<g, 256, 0, stream>>>(n, r.list, r.lab[iters & 1], final_lab);
