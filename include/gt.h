@@ -114,6 +114,24 @@ size_t gt_reorder_workspace_size(int64_t n, int64_t nnz);
 gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
                      uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels, int32_t* sweeps_done,
                      void* ws, size_t ws_bytes, hipStream_t stream);
+/* gt_reorder with the rows of each sweep spread over `stream` and n_side
+ * further streams of the caller's, so that the sweep's row classes (short
+ * rows, long rows, rows of 65 to 4096 entries) run side by side.
+ *   side_streams (host) hipStream_t[n_side], n_side in [0, 2]: non-null,
+ *     distinct, not `stream`, on stream's device;
+ *   events (host) hipEvent_t[n_side + 1]: distinct events of the caller's on
+ *     stream's device, which the call records and waits on to order the
+ *     streams (timing not needed); no other work may record them until the
+ *     call has returned.
+ * Same results, workspace and errors as gt_reorder (which is this call with
+ * n_side = 0); a bad side-stream or event argument is GT_ERR_INVALID_ARG
+ * before anything is enqueued.  When the call returns, every later call on
+ * `stream` runs after all of its work; work enqueued on the side streams
+ * before the call runs before the call's work there. */
+gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
+                             uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels, int32_t* sweeps_done,
+                             void* ws, size_t ws_bytes, hipStream_t stream, const hipStream_t* side_streams,
+                             const hipEvent_t* events, int32_t n_side);
 
 /* ------------------------------------------------------------------------ */
 /* Relabelling, §3.3 (the layout is reorganised by cluster).                 */

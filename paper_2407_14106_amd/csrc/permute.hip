@@ -316,10 +316,6 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     GT_HIP(hipStreamSynchronize(stream));
     if ((st = validation_result(uint32_t(info[2 * kRlClasses + 1]))) != GT_OK) return st;
     const int64_t m = info[2 * kRlClasses];
-    // the short rows (written straight to their places) on a side stream, beside the longer rows' sort
-    Spread sp;
-    if ((st = spread_open(stream, &sp)) != GT_OK) return st;
-    if ((st = sp.fork()) != GT_OK) return st;
     {
         // the short-row lists in one launch, largest rows first, blocks in proportion to their rows
         ShortLists sl;
@@ -339,11 +335,11 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
         sl.first[5] = at;
         if (at > 0) {
             if (with_map)
-                k_relabel_short<true><<<at, 256, 0, sp.at(1)>>>(sl, rowptr, col, perm, iperm, rowptr_out, col_out,
-                                                                src_pos);
+                k_relabel_short<true><<<at, 256, 0, stream>>>(sl, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                                              src_pos);
             else
-                k_relabel_short<false><<<at, 256, 0, sp.at(1)>>>(sl, rowptr, col, perm, iperm, rowptr_out, col_out,
-                                                                 nullptr);
+                k_relabel_short<false><<<at, 256, 0, stream>>>(sl, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                                               nullptr);
             GT_LAUNCH_CHECK("permute_short_rows");
         }
     }
@@ -375,7 +371,7 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     k_place_sorted<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, p.keys, p.vals, bits, p.soff, rowptr_out, col_out,
                                                                 with_map ? src_pos : nullptr);
     GT_LAUNCH_CHECK("permute_place");
-    return sp.join();
+    return GT_OK;
 }
 
 }  // namespace

@@ -4,38 +4,41 @@
 // the caller's workspace through gt::Ws.
 #pragma once
 
-#include <mutex>
-
 #include "common.h"
 
 namespace gt {
 
-// ---- work spread over the caller's stream and the library's own side streams
-// Two streams per device, created on first use at the default priority and
-// kept until the process ends, with the events that order them.  A Spread
-// holds the device's lock from spread_open until it is destroyed, so calls on
-// one device take turns enqueueing (their kernels still overlap on the GPU).
+// ---- work spread over the caller's stream and side streams the caller gives
+// A call may spread independent work over up to kMaxSide further streams of
+// the caller's (on the same device), ordered by events the caller also gives
+// (one to fork, one per side stream to join), so the library creates nothing.
 // fork(): the side streams wait for the work enqueued on the caller's stream
 // so far; join(): the caller's stream waits for the work enqueued on the side
 // streams.  A Spread still forked when destroyed joins first, so the caller's
-// stream never finishes before the side streams' work.  Where the caller's
-// stream is not on the current device, everything runs on the caller's stream.
-constexpr int kSideStreams = 2;
+// stream never finishes before the side streams' work.  With no side streams
+// everything runs on the caller's stream.
+constexpr int kMaxSide = 2;
 struct Spread {
     hipStream_t main = nullptr;
-    hipStream_t side[kSideStreams] = {};
+    hipStream_t side[kMaxSide] = {};
     hipEvent_t fork_ev = nullptr;
-    hipEvent_t join_ev[kSideStreams] = {};
-    bool on = false;      // side streams in use
+    hipEvent_t join_ev[kMaxSide] = {};
+    int n_side = 0;
     bool forked = false;
-    std::unique_lock<std::mutex> lock;
-    // stream k: 0 the caller's, 1 .. kSideStreams the side streams
-    hipStream_t at(int k) const { return (k == 0 || !on) ? main : side[k - 1]; }
+    // stream k: 0 the caller's, 1 .. kMaxSide the side streams (dealt round the ones given)
+    hipStream_t at(int k) const { return (k == 0 || n_side == 0) ? main : side[(k - 1) % n_side]; }
     gt_status fork();
     gt_status join();
-    ~Spread();
+    Spread() = default;
+    Spread(const Spread&) = delete;
+    Spread& operator=(const Spread&) = delete;
+    ~Spread() { (void)join(); }
 };
-gt_status spread_open(hipStream_t main, Spread* sp);
+// events: n_side + 1 of them.  Checks that the side streams and events are
+// non-null and distinct and the side streams are not main, then that the side
+// streams are on main's device.
+gt_status spread_open(const char* who, hipStream_t main, const hipStream_t* side, const hipEvent_t* events,
+                      int n_side, Spread* sp);
 
 // ---- fills
 gt_status fill_u32(uint32_t* p, int64_t n, uint32_t value, hipStream_t s);

@@ -39,65 +39,63 @@ gt_status iota_u32(uint32_t* p, int64_t n, hipStream_t s) {
 }
 // ============================================================= side streams
 
-namespace {
-constexpr int kSpreadDevices = 64;
-struct DeviceSide {
-    std::mutex mu;
-    bool ready = false;
-    hipStream_t side[kSideStreams] = {};
-    hipEvent_t fork_ev = nullptr;
-    hipEvent_t join_ev[kSideStreams] = {};
-};
-DeviceSide g_side[kSpreadDevices];
-}  // namespace
-
-gt_status spread_open(hipStream_t main, Spread* sp) {
+gt_status spread_open(const char* who, hipStream_t main, const hipStream_t* side, const hipEvent_t* events,
+                      int n_side, Spread* sp) {
     sp->main = main;
-    sp->on = false;
-    int dev = -1;
-    GT_HIP(hipGetDevice(&dev));
-    if (dev < 0 || dev >= kSpreadDevices) return GT_OK;
+    sp->n_side = 0;
+    if (n_side < 0 || n_side > kMaxSide || (n_side > 0 && (!side || !events)))
+        return fail(GT_ERR_INVALID_ARG, std::string(who) + ": n_side must be in [0, 2], with stream and event arrays");
+    if (n_side == 0) return GT_OK;
+    for (int k = 0; k < n_side; ++k) {
+        if (!side[k] || side[k] == main)
+            return fail(GT_ERR_INVALID_ARG, std::string(who) + ": a side stream is null or the call's own stream");
+        for (int j = 0; j < k; ++j)
+            if (side[j] == side[k]) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": a side stream repeats");
+    }
+    for (int k = 0; k <= n_side; ++k) {
+        if (!events[k]) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": a null event");
+        for (int j = 0; j < k; ++j)
+            if (events[j] == events[k]) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": an event repeats");
+    }
+    hipDevice_t dev = -1;
     if (main) {
+        GT_HIP(hipStreamGetDevice(main, &dev));
+    } else {
+        int d = -1;
+        GT_HIP(hipGetDevice(&d));
+        dev = d;
+    }
+    for (int k = 0; k < n_side; ++k) {
         hipDevice_t sdev = -1;
-        GT_HIP(hipStreamGetDevice(main, &sdev));
-        if (sdev != dev) return GT_OK;
+        GT_HIP(hipStreamGetDevice(side[k], &sdev));
+        if (sdev != dev) return fail(GT_ERR_INVALID_ARG, std::string(who) + ": a side stream is on another device");
     }
-    DeviceSide& d = g_side[dev];
-    sp->lock = std::unique_lock<std::mutex>(d.mu);
-    if (!d.ready) {
-        for (int k = 0; k < kSideStreams; ++k) GT_HIP(hipStreamCreateWithFlags(&d.side[k], hipStreamNonBlocking));
-        GT_HIP(hipEventCreateWithFlags(&d.fork_ev, hipEventDisableTiming));
-        for (int k = 0; k < kSideStreams; ++k) GT_HIP(hipEventCreateWithFlags(&d.join_ev[k], hipEventDisableTiming));
-        d.ready = true;
+    sp->fork_ev = events[0];
+    for (int k = 0; k < n_side; ++k) {
+        sp->side[k] = side[k];
+        sp->join_ev[k] = events[k + 1];
     }
-    for (int k = 0; k < kSideStreams; ++k) {
-        sp->side[k] = d.side[k];
-        sp->join_ev[k] = d.join_ev[k];
-    }
-    sp->fork_ev = d.fork_ev;
-    sp->on = true;
+    sp->n_side = n_side;
     return GT_OK;
 }
 
 gt_status Spread::fork() {
-    if (!on) return GT_OK;
+    if (n_side == 0) return GT_OK;
     GT_HIP(hipEventRecord(fork_ev, main));
-    for (int k = 0; k < kSideStreams; ++k) GT_HIP(hipStreamWaitEvent(side[k], fork_ev, 0));
+    for (int k = 0; k < n_side; ++k) GT_HIP(hipStreamWaitEvent(side[k], fork_ev, 0));
     forked = true;
     return GT_OK;
 }
 
 gt_status Spread::join() {
-    if (!on || !forked) return GT_OK;
-    for (int k = 0; k < kSideStreams; ++k) {
+    if (n_side == 0 || !forked) return GT_OK;
+    for (int k = 0; k < n_side; ++k) {
         GT_HIP(hipEventRecord(join_ev[k], side[k]));
         GT_HIP(hipStreamWaitEvent(main, join_ev[k], 0));
     }
     forked = false;
     return GT_OK;
 }
-
-Spread::~Spread() { (void)join(); }
 
 gt_status copy_bytes(void* dst, const void* src, int64_t bytes, hipStream_t s) {
     if (bytes <= 0) return GT_OK;

@@ -1282,9 +1282,11 @@ extern "C" size_t gt_reorder_workspace_size(int64_t n, int64_t nnz) {
     return ws.size();
 }
 
-extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
-                                uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels,
-                                int32_t* sweeps_done, void* ws_ptr, size_t ws_bytes, hipStream_t stream) {
+extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
+                                        int32_t iters, uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels,
+                                        int32_t* sweeps_done, void* ws_ptr, size_t ws_bytes, hipStream_t stream,
+                                        const hipStream_t* side_streams, const hipEvent_t* events,
+                                        int32_t n_side) {
     if (n < 0 || nnz < 0 || n >= (int64_t(1) << 31) || nnz >= (int64_t(1) << 32))
         return fail(GT_ERR_INVALID_ARG, "gt_reorder: n or nnz out of range");
     if (iters < 0 || iters > kMaxSweeps) return fail(GT_ERR_INVALID_ARG, "gt_reorder: iters must be in [0, 1000]");
@@ -1292,6 +1294,13 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         return fail(GT_ERR_INVALID_ARG, "gt_reorder: null pointer");
     if (ws_bytes < gt_reorder_workspace_size(n, nnz))
         return fail(GT_ERR_WORKSPACE, "gt_reorder: workspace too small");
+    // The classes of a sweep read the sweep's input labels and write disjoint rows of its output: with side
+    // streams they run side by side, the short rows on the caller's stream, the long rows on the first side
+    // stream, the rows of 65 to 4096 entries on the second (or the first); each sweep starts when the
+    // previous one has finished on all of them.
+    Spread sp;
+    gt_status st = spread_open("gt_reorder", stream, side_streams, events, n_side, &sp);
+    if (st != GT_OK) return st;
     if (n == 0) {
         if (sweeps_done) *sweeps_done = 0;
         return GT_OK;
@@ -1301,8 +1310,7 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     // the CSR check and the row classes in one go: both come back to the host with one synchronisation,
     // and nothing past the classification runs unless the check passed
     uint32_t* vflag = reinterpret_cast<uint32_t*>(r.class_info + 2 * kClasses + 1);
-    gt_status st = fill_u32(vflag, 2, 0u, stream);  // the high half of the slot too
-    if (st != GT_OK) return st;
+    if ((st = fill_u32(vflag, 2, 0u, stream)) != GT_OK) return st;  // the high half of the slot too
     if ((st = launch_validate_csr(n, nnz, rowptr, col, vflag, stream)) != GT_OK) return st;
     const unsigned g = grid_for(n, 256, 8192);
     const int64_t nblk = cdiv(n, kClsBlock);
@@ -1365,11 +1373,6 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
     const bool giant = info[2 * kClasses] + 1 > kFusedCap / 2;
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
     const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
-    // The classes of a sweep read the sweep's input labels and write disjoint rows of its output: they run
-    // side by side, the short rows on the caller's stream, the long rows on one side stream, the rows of
-    // 65 to 4096 entries on the other; each sweep starts when the previous one has finished on all three.
-    Spread sp;
-    if ((st = spread_open(stream, &sp)) != GT_OK) return st;
     const hipStream_t s_short = sp.at(0), s_big = sp.at(1), s_wide = sp.at(2);
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
@@ -1469,4 +1472,11 @@ extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, c
         *sweeps_done = done;
     }
     return GT_OK;
+}
+
+extern "C" gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t iters,
+                                uint64_t seed, int32_t* perm, int32_t* iperm, int32_t* labels,
+                                int32_t* sweeps_done, void* ws_ptr, size_t ws_bytes, hipStream_t stream) {
+    return gt_reorder_streams(n, nnz, rowptr, col, iters, seed, perm, iperm, labels, sweeps_done, ws_ptr, ws_bytes,
+                              stream, nullptr, nullptr, 0);
 }

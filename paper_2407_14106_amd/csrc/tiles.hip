@@ -823,15 +823,11 @@ gt_status heavy_prelude(int64_t n, const int64_t* rowptr, int32_t T, TilesWs& t,
     return fill_u32(t.heavy_cnt, int64_t(kMaxHeavy) * R, 0u, stream);
 }
 
-// The rest of the count pass, after heavy_prelude.  The medium-row list (a
-// chain of small launches) is made on a side stream of sp beside the tile-row
-// counts; the rest runs in order on the caller's stream.
+// The rest of the count pass, after heavy_prelude.
 gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T, uint32_t tau_ppm,
-                     TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, Spread& sp) {
+                     TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, hipStream_t stream) {
     gt_status st;
     const int R = int(cdiv(n, T));
-    const hipStream_t stream = sp.at(0);
-    if ((st = sp.fork()) != GT_OK) return st;
     k_heavy_count<<<1024, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, t.heavy_list, t.heavy_n, t.heavy_cnt);
     GT_LAUNCH_CHECK("tiles_heavy_count");
     k_tiles<false><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, t.dense_per_tilerow, t.sp_deg,
@@ -839,8 +835,7 @@ gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_
                                                    t.rows, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr,
                                                    t.heavy_slot, t.heavy_cnt);
     GT_LAUNCH_CHECK("tiles_count");
-    if ((st = medium_rows(n, rowptr, t, sp.at(1))) != GT_OK) return st;
-    if ((st = sp.join()) != GT_OK) return st;
+    if ((st = medium_rows(n, rowptr, t, stream)) != GT_OK) return st;
     k_tiles_med<false><<<grid_for(n, 4, 16384), 256, 0, stream>>>(
         n, t.med_list, t.med_info + 1, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.sp_deg, t.tag, t.rows,
         nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
@@ -893,9 +888,7 @@ extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowpt
     if ((st = launch_validate_csr(n, nnz, rowptr, col, t.flags, stream)) != GT_OK) return st;
     if ((st = heavy_prelude(n, rowptr, T, t, stream)) != GT_OK) return st;
     if ((st = read_validation(t.flags, stream)) != GT_OK) return st;
-    Spread sp;
-    if ((st = spread_open(stream, &sp)) != GT_OK) return st;
-    if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, sp)) != GT_OK)
+    if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
         return st;
     if ((st = ws_checksum(t, stream)) != GT_OK) return st;
     k_put_record<<<1, 64, 0, stream>>>(t.record, n, nnz, rowptr, col, T, tau_ppm, t.csum);
@@ -958,11 +951,10 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
             (st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK)
             return st;
     }
-    Spread sp;
-    if ((st = spread_open(stream, &sp)) != GT_OK) return st;
     if (!reuse) {
         if ((st = heavy_prelude(n, rowptr, T, t, stream)) != GT_OK) return st;
-        if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, sp)) != GT_OK)
+        if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) !=
+            GT_OK)
             return st;
     }
     // the fill reads the offsets where the count pass left them; the plan's copies and the other small
@@ -974,54 +966,51 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     if (plan->tile_pos && plan->n_dense > 0 &&
         (st = fill_u32(reinterpret_cast<uint32_t*>(plan->tile_pos), plan->n_dense * T, 0u, stream)) != GT_OK)
         return st;
-    // the fill kernels in order on the caller's stream (the tile-row fill, with two 1,024-thread workgroups per
-    // CU, slows down when other kernels take its CUs)
-    const hipStream_t s_rows = stream, s_copy = stream;
     k_tiles<true><<<R, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, tau_ppm, nullptr, nullptr, trp,
                                               plan->tile_col, plan->tile_nnz, plan->tile_mask, srp, plan->sp_col,
                                               nullptr, nullptr, t.W, nullptr, nullptr, plan->sp_pos, plan->tile_pos,
                                               t.heavy_slot, t.heavy_cnt);
     GT_LAUNCH_CHECK("tiles_fill");
+    if (reuse) {
+        if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK) return st;  // used once
+        if ((st = copy_bytes(plan->tile_rowptr, t.tmp_tile_rowptr, size_t(R + 1) * 8, stream)) != GT_OK) return st;
+        if ((st = copy_bytes(plan->sp_rowptr, t.tmp_sp_rowptr, size_t(n + 1) * 8, stream)) != GT_OK) return st;
+    }
+    {
+        const unsigned g = grid_for(n, 256, 8192);
+        if (plan->n_long_rows > 0) {
+            k_compact_list<<<g, 256, 0, stream>>>(n, t.long_row_flag, t.long_row_pos, plan->long_rows);
+            GT_LAUNCH_CHECK("tiles_long_row_list");
+        }
+        if (plan->n_long_cols > 0) {
+            k_compact_list<<<g, 256, 0, stream>>>(n, t.long_col_flag, t.long_col_pos, plan->long_cols);
+            GT_LAUNCH_CHECK("tiles_long_col_list");
+        }
+    }
     // the medium-row list: the count pass made it (here, or in gt_tiles_count's workspace, checked above)
-    k_tiles_med<true><<<grid_for(n, 4, 16384), 256, 0, s_rows>>>(
+    k_tiles_med<true><<<grid_for(n, 4, 16384), 256, 0, stream>>>(
         n, t.med_list, t.med_info + 1, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr, nullptr,
         trp, plan->tile_mask, srp, plan->sp_col, plan->sp_pos, plan->tile_pos);
     GT_LAUNCH_CHECK("tiles_fill_medium");
     if (nnz > kLongRow) {
         const int64_t segs = 2 * long_chunks_of(nnz);
-        if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.segcnt), segs, 0u, s_rows)) != GT_OK) return st;
-        k_tiles_long_segs<<<long_grid(nnz), kThreads, 0, s_rows>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
+        if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.segcnt), segs, 0u, stream)) != GT_OK) return st;
+        k_tiles_long_segs<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
                                                                   t.segcnt);
         GT_LAUNCH_CHECK("tiles_long_segs");
-        if ((st = exclusive_scan_i32(t.segcnt, segs, t.segoff, t.scan, s_rows)) != GT_OK) return st;
-        k_tiles_long_fill<<<long_grid(nnz), kThreads, 0, s_rows>>>(
+        if ((st = exclusive_scan_i32(t.segcnt, segs, t.segoff, t.scan, stream)) != GT_OK) return st;
+        k_tiles_long_fill<<<long_grid(nnz), kThreads, 0, stream>>>(
             n, nnz, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.segoff, trp, plan->tile_mask, srp,
             plan->sp_col, plan->sp_pos, plan->tile_pos);
         GT_LAUNCH_CHECK("tiles_long_fill");
     }
-    if (reuse) {
-        if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, s_copy)) != GT_OK) return st;  // used once
-        if ((st = copy_bytes(plan->tile_rowptr, t.tmp_tile_rowptr, size_t(R + 1) * 8, s_copy)) != GT_OK) return st;
-        if ((st = copy_bytes(plan->sp_rowptr, t.tmp_sp_rowptr, size_t(n + 1) * 8, s_copy)) != GT_OK) return st;
-    }
-    {
-        const unsigned g = grid_for(n, 256, 8192);
-        if (plan->n_long_rows > 0) {
-            k_compact_list<<<g, 256, 0, s_copy>>>(n, t.long_row_flag, t.long_row_pos, plan->long_rows);
-            GT_LAUNCH_CHECK("tiles_long_row_list");
-        }
-        if (plan->n_long_cols > 0) {
-            k_compact_list<<<g, 256, 0, s_copy>>>(n, t.long_col_flag, t.long_col_pos, plan->long_cols);
-            GT_LAUNCH_CHECK("tiles_long_col_list");
-        }
-    }
     // remainder transpose: the count pass sorted it; its first nnz_sparse rows are the remainder's
     const int64_t m = plan->nnz_sparse;
     if (m > 0) {
-        k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, s_copy>>>(m, t.rows, plan->sp_row);
+        k_u32_to_i32<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, t.rows, plan->sp_row);
         GT_LAUNCH_CHECK("tiles_sp_row");
     }
-    if ((st = copy_bytes(plan->sp_colptr, t.colptr, size_t(n + 1) * 8, s_copy)) != GT_OK) return st;
+    if ((st = copy_bytes(plan->sp_colptr, t.colptr, size_t(n + 1) * 8, stream)) != GT_OK) return st;
     // tiles grouped by column: stable sort of (J, tile index) by J
     const int64_t d = plan->n_dense;
     if (d <= kSmallTranspose) {

@@ -12,6 +12,7 @@ from __future__ import annotations
 import ctypes
 import math
 import os
+import threading
 from dataclasses import dataclass
 
 import torch
@@ -73,6 +74,8 @@ SIGNATURES = {
     "gt_validate_csr": (_i32, [_i64, _i64, _vp, _vp, _vp, _sz, _vp]),
     "gt_reorder_workspace_size": (_sz, [_i64, _i64]),
     "gt_reorder": (_i32, [_i64, _i64, _vp, _vp, _i32, _u64, _vp, _vp, _vp, _P(_i32), _vp, _sz, _vp]),
+    "gt_reorder_streams": (_i32, [_i64, _i64, _vp, _vp, _i32, _u64, _vp, _vp, _vp, _P(_i32), _vp, _sz, _vp,
+                                  _vp, _vp, _i32]),
     "gt_permute_workspace_size": (_sz, [_i64, _i64]),
     "gt_permute_csr": (_i32, [_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "gt_permute_edges_workspace_size": (_sz, [_i64, _i64]),
@@ -184,8 +187,32 @@ def validate_csr(rowptr: torch.Tensor, col: torch.Tensor) -> None:
                                _stream(rowptr.device)), "gt_validate_csr")
 
 
-def reorder(rowptr: torch.Tensor, col: torch.Tensor, iters: int = 20, seed: int = 0, want_sweeps: bool = False):
-    """(perm, iperm, labels[, sweeps]) of the cluster reordering."""
+_SIDE = threading.local()
+
+
+def side_streams(dev: torch.device):
+    """(streams, events) for the calls that spread independent work beside the current stream: two streams of
+    the device (default priority) and three events, made once per host thread and kept by this module (a
+    call records the events, so two threads never share them)."""
+    idx = dev.index if dev.index is not None else torch.cuda.current_device()
+    per = getattr(_SIDE, "per_device", None)
+    if per is None:
+        per = _SIDE.per_device = {}
+    got = per.get(idx)
+    if got is None:
+        streams = [torch.cuda.Stream(device=idx) for _ in range(2)]
+        events = [torch.cuda.Event() for _ in range(3)]
+        with torch.cuda.device(idx):
+            for e in events:
+                e.record(torch.cuda.current_stream(idx))  # makes the event
+        got = per[idx] = (streams, events)
+    return got
+
+
+def reorder(rowptr: torch.Tensor, col: torch.Tensor, iters: int = 20, seed: int = 0, want_sweeps: bool = False,
+            n_side: int = 2):
+    """(perm, iperm, labels[, sweeps]) of the cluster reordering.  n_side (0 to 2) side streams run each
+    sweep's row classes beside the current stream (the same result with any n_side)."""
     lib = load_library()
     _check_csr(rowptr, col)
     n, nnz = rowptr.numel() - 1, col.numel()
@@ -195,9 +222,15 @@ def reorder(rowptr: torch.Tensor, col: torch.Tensor, iters: int = 20, seed: int 
     labels = torch.empty(n, dtype=torch.int32, device=dev)
     ws = _workspace(lib.gt_reorder_workspace_size(n, nnz), dev)
     sweeps = ctypes.c_int32(-1)
-    _check(lib.gt_reorder(n, nnz, _ptr(rowptr), _ptr(col), iters, ctypes.c_uint64(seed % (1 << 64)), _ptr(perm),
-                          _ptr(iperm), _ptr(labels), ctypes.byref(sweeps) if want_sweeps else None, _ptr(ws),
-                          ws.numel(), _stream(dev)), "gt_reorder")
+    side = events = None
+    if n_side > 0:
+        streams, evs = side_streams(dev)
+        side = (ctypes.c_void_p * 2)(*[s.cuda_stream for s in streams])
+        events = (ctypes.c_void_p * 3)(*[e.cuda_event for e in evs])
+    _check(lib.gt_reorder_streams(n, nnz, _ptr(rowptr), _ptr(col), iters, ctypes.c_uint64(seed % (1 << 64)),
+                                  _ptr(perm), _ptr(iperm), _ptr(labels),
+                                  ctypes.byref(sweeps) if want_sweeps else None, _ptr(ws), ws.numel(),
+                                  _stream(dev), side, events, n_side), "gt_reorder")
     return (perm, iperm, labels, sweeps.value) if want_sweeps else (perm, iperm, labels)
 
 

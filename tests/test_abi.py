@@ -106,6 +106,19 @@ def test_argument_errors_without_device(lib):
     assert lib.gt_reorder(100, 10, FAKE, FAKE, 5000, 0, FAKE, FAKE, None, None, FAKE, 1 << 30,
                           stream) == gt.GT_ERR_INVALID_ARG
     assert lib.gt_reorder(100, 10, FAKE, FAKE, 10, 0, FAKE, FAKE, None, None, FAKE, 8, stream) == gt.GT_ERR_WORKSPACE
+    # side streams and events: at most two streams, given, non-null, distinct and not the call's own stream;
+    # one event more, non-null and distinct (host checks, before any device query)
+    two = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    s2 = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    e3 = (ctypes.c_void_p * 3)(0x3000, 0x4000, 0x5000)
+    e3_null = (ctypes.c_void_p * 3)(0x3000, 0, 0x5000)
+    e3_rep = (ctypes.c_void_p * 3)(0x3000, 0x4000, 0x3000)
+    for side, events, n_side in ((None, e3, 1), (s2, None, 1), (s2, e3, 3), (s2, e3, -1), (two, e3, 2),
+                                 (s2, e3_null, 2), (s2, e3_rep, 2)):
+        assert lib.gt_reorder_streams(100, 10, FAKE, FAKE, 10, 0, FAKE, FAKE, None, None, FAKE, 1 << 30, stream,
+                                      side, events, n_side) == gt.GT_ERR_INVALID_ARG
+    assert lib.gt_reorder_streams(100, 10, FAKE, FAKE, 10, 0, FAKE, FAKE, None, None, FAKE, 8, stream, s2, e3,
+                                  1) == gt.GT_ERR_WORKSPACE
     assert lib.gt_permute_csr(100, 10, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
                               stream) == gt.GT_ERR_INVALID_ARG
     assert lib.gt_validate_csr(10, 10, FAKE, FAKE, FAKE, 0, stream) == gt.GT_ERR_WORKSPACE

@@ -105,6 +105,20 @@ def test_reorder_concurrent_calls(gt):
             np.testing.assert_array_equal(iperm, iperm_ref)
 
 
+@pytest.mark.parametrize("name", ["hubs_6000", "three_hubs_30000", "c3@0.02", "b1@0.1"])
+def test_reorder_side_streams_same_result(gt, name):
+    # the sweeps spread over zero, one or two side streams (the bit-exact tests above use two) give one result,
+    # call after call with the same streams and events
+    rowptr, col = next((g[1], g[2]) for g in GRAPHS if g[0] == name)
+    rp, cl = dev_csr(rowptr, col)
+    ref = [x.cpu().numpy() for x in gt.reorder(rp, cl, iters=20, seed=5, n_side=0)]
+    for n_side in (1, 2, 1):
+        say("reorder side streams", name, n_side)
+        got = gt.reorder(rp, cl, iters=20, seed=5, n_side=n_side)
+        for a, b in zip(got, ref):
+            np.testing.assert_array_equal(a.cpu().numpy(), b)
+
+
 @pytest.mark.parametrize("name,rowptr,col", GRAPHS, ids=[g[0] for g in GRAPHS])
 def test_permute_bit_exact(gt, name, rowptr, col):
     say("permute", name)
