@@ -123,6 +123,9 @@ gt_status gt_reorder(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_
  *     stream's device, which the call records and waits on to order the
  *     streams (timing not needed); no other work may record them until the
  *     call has returned.
+ * The side streams are used only when the rows of more than 64 entries hold
+ * at least a quarter of the entries (else the short rows' kernel dominates a
+ * sweep and the others gain nothing beside it).
  * Same results, workspace and errors as gt_reorder (which is this call with
  * n_side = 0); a bad side-stream or event argument is GT_ERR_INVALID_ARG
  * before anything is enqueued.  When the call returns, every later call on

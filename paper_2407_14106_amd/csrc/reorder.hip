@@ -114,15 +114,17 @@ __device__ __forceinline__ int class_ballots(int cls, int (*s)[kClasses]) {
 }
 
 // Off-diagonal entry count of every row (for the final order; the block's
-// largest in blk_max[block]) and the block's rows per class, in
-// blk_cnt[c * nblk + block].  It runs before the CSR check is read back, so
-// every read stays in col[0, nnz) whatever rowptr holds.
+// largest in blk_max[block]), the block's rows per class, in
+// blk_cnt[c * nblk + block], and the entries of its rows of more than
+// kWaveRowMax entries, in blk_long[block].  It runs before the CSR check is
+// read back, so every read stays in col[0, nnz) whatever rowptr holds.
 __global__ __launch_bounds__(kClsBlock) void k_classify(int64_t n, int64_t nnz, const int64_t* rowptr,
                                                         const int32_t* col, uint32_t* deg_off, int32_t* blk_cnt,
-                                                        int64_t nblk, uint32_t* blk_max) {
+                                                        int64_t nblk, uint32_t* blk_max, uint32_t* blk_long) {
     __shared__ int s_cnt[kClsBlock / kWave][kClasses];
     __shared__ uint32_t s_max[kClsBlock / kWave];
-    uint32_t dv = 0;
+    __shared__ uint32_t s_long[kClsBlock / kWave];
+    uint32_t dv = 0, lv = 0;
     const int64_t v = int64_t(blockIdx.x) * kClsBlock + threadIdx.x;
     int cls = -1;
     if (v < n) {
@@ -140,16 +142,26 @@ __global__ __launch_bounds__(kClsBlock) void k_classify(int64_t n, int64_t nnz, 
         dv = uint32_t(b - a - (self ? 1 : 0));
         deg_off[v] = dv;
         cls = row_class(b - a);
+        lv = b - a > kWaveRowMax ? uint32_t(b - a) : 0u;
     }
     class_ballots(cls, s_cnt);
     dv = wave_max(dv);
-    if (lane_id() == 0) s_max[threadIdx.x / kWave] = dv;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) lv += __shfl_xor(lv, o, kWave);  // < 2^32: entries of the block's rows
+    if (lane_id() == 0) {
+        s_max[threadIdx.x / kWave] = dv;
+        s_long[threadIdx.x / kWave] = lv;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
-        uint32_t m = 0;
+        uint32_t m = 0, l = 0;
 #pragma unroll
-        for (int w = 0; w < kClsBlock / kWave; ++w) m = s_max[w] > m ? s_max[w] : m;
+        for (int w = 0; w < kClsBlock / kWave; ++w) {
+            m = s_max[w] > m ? s_max[w] : m;
+            l += s_long[w];
+        }
         blk_max[blockIdx.x] = m;
+        blk_long[blockIdx.x] = l;
     }
     if (threadIdx.x < kClasses) {
         int t = 0;
@@ -187,21 +199,36 @@ __global__ void k_class_totals(int64_t nblk, const int64_t* blk_off, int64_t* in
     info[kClasses + c] = blk_off[(c + 1) * nblk] - blk_off[c * nblk];
 }
 
-// The largest of the blocks' maxima, in *out (which starts at zero): each
-// workgroup reduces kMaxSpan of them and adds one atomic.
+// The largest of the blocks' maxima, in *out_max, and the sum of their long
+// rows' entries, in *out_long (both start at zero): each workgroup reduces
+// kMaxSpan blocks and adds one atomic to each.
 constexpr int kMaxSpan = 4096;
-__global__ __launch_bounds__(256) void k_blocks_max(int64_t nblk, const uint32_t* blk_max,
-                                                    unsigned long long* out) {
+__global__ __launch_bounds__(256) void k_blocks_max(int64_t nblk, const uint32_t* blk_max, const uint32_t* blk_long,
+                                                    unsigned long long* out_max, unsigned long long* out_long) {
     __shared__ uint32_t s_max[256 / kWave];
+    __shared__ uint64_t s_sum[256 / kWave];
     uint32_t m = 0;
+    uint64_t l = 0;
     const int64_t b0 = int64_t(blockIdx.x) * kMaxSpan;
-    for (int64_t b = b0 + threadIdx.x; b < nblk && b < b0 + kMaxSpan; b += 256) m = blk_max[b] > m ? blk_max[b] : m;
+    for (int64_t b = b0 + threadIdx.x; b < nblk && b < b0 + kMaxSpan; b += 256) {
+        m = blk_max[b] > m ? blk_max[b] : m;
+        l += blk_long[b];
+    }
     m = wave_max(m);
-    if (lane_id() == 0) s_max[threadIdx.x / kWave] = m;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) l += shfl_xor_u64(l, o);
+    if (lane_id() == 0) {
+        s_max[threadIdx.x / kWave] = m;
+        s_sum[threadIdx.x / kWave] = l;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
-        for (int w = 1; w < 256 / kWave; ++w) m = s_max[w] > m ? s_max[w] : m;
-        if (m) atomicMax(out, (unsigned long long)m);
+        for (int w = 1; w < 256 / kWave; ++w) {
+            m = s_max[w] > m ? s_max[w] : m;
+            l += s_sum[w];
+        }
+        if (m) atomicMax(out_max, (unsigned long long)m);
+        if (l) atomicAdd(out_long, (unsigned long long)l);
     }
 }
 
@@ -1213,9 +1240,11 @@ struct ReorderWs {
     uint32_t* ldeg;       // [n]: entry counts by list position
     int64_t* roff;        // [n + 1]: their exclusive scan
     int32_t* ncol;        // [nnz]: the rows' entries in list order, as list positions
-    int64_t* class_info;  // [2 * kClasses + 2]: first list position and rows of each class; largest
-                          // off-diagonal entry count; the CSR check's flags (low 32 bits)
+    int64_t* class_info;  // [2 * kClasses + 3]: first list position and rows of each class; largest
+                          // off-diagonal entry count; the CSR check's flags (low 32 bits); entries of the
+                          // rows of more than kWaveRowMax entries
     uint32_t* blk_max;    // [blocks]: largest off-diagonal entry count of each 256-row block
+    uint32_t* blk_long;   // [blocks]: entries of each block's rows of more than kWaveRowMax entries
     int64_t* huge_off;
     int64_t* huge_echunk;
     int64_t* huge_schunk;
@@ -1251,8 +1280,9 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.ldeg = ws.take<uint32_t>(n1);
     r.roff = ws.take<int64_t>(n1 + 1);
     r.ncol = ws.take<int32_t>(size_t(nnz > 0 ? nnz : 1));
-    r.class_info = ws.take<int64_t>(2 * kClasses + 2);
+    r.class_info = ws.take<int64_t>(2 * kClasses + 3);
     r.blk_max = ws.take<uint32_t>(size_t(nblk));
+    r.blk_long = ws.take<uint32_t>(size_t(nblk));
     r.huge_off = ws.take<int64_t>(n1 + 1);
     r.huge_echunk = ws.take<int64_t>(n1 + 1);
     r.huge_schunk = ws.take<int64_t>(n1 + 1);
@@ -1315,10 +1345,13 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
     const unsigned g = grid_for(n, 256, 8192);
     const int64_t nblk = cdiv(n, kClsBlock);
     unsigned long long* deg_max = reinterpret_cast<unsigned long long*>(r.class_info + 2 * kClasses);
+    unsigned long long* long_sum = reinterpret_cast<unsigned long long*>(r.class_info + 2 * kClasses + 2);
     if ((st = fill_u32(reinterpret_cast<uint32_t*>(deg_max), 2, 0u, stream)) != GT_OK) return st;
-    k_classify<<<unsigned(nblk), kClsBlock, 0, stream>>>(n, nnz, rowptr, col, r.deg_off, r.blk_cnt, nblk, r.blk_max);
+    if ((st = fill_u32(reinterpret_cast<uint32_t*>(long_sum), 2, 0u, stream)) != GT_OK) return st;
+    k_classify<<<unsigned(nblk), kClsBlock, 0, stream>>>(n, nnz, rowptr, col, r.deg_off, r.blk_cnt, nblk, r.blk_max,
+                                                         r.blk_long);
     GT_LAUNCH_CHECK("reorder_classify");
-    k_blocks_max<<<unsigned(cdiv(nblk, kMaxSpan)), 256, 0, stream>>>(nblk, r.blk_max, deg_max);
+    k_blocks_max<<<unsigned(cdiv(nblk, kMaxSpan)), 256, 0, stream>>>(nblk, r.blk_max, r.blk_long, deg_max, long_sum);
     GT_LAUNCH_CHECK("reorder_degree_max");
     if ((st = exclusive_scan_i32(r.blk_cnt, kClasses * nblk, r.blk_off, r.scan, stream)) != GT_OK) return st;
     k_class_scatter<<<unsigned(nblk), kClsBlock, 0, stream>>>(n, rowptr, r.blk_off, nblk, r.list, r.lpos,
@@ -1334,7 +1367,7 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
     if ((st = fill_u32(r.flags, 1, 1, stream)) != GT_OK) return st;
 
     // the class sizes on the host: empty classes are not launched and grids fit the lists
-    int64_t info[2 * kClasses + 2] = {};
+    int64_t info[2 * kClasses + 3] = {};
     GT_HIP(hipMemcpyAsync(info, r.class_info, sizeof(info), hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
     if ((st = validation_result(uint32_t(uint64_t(info[2 * kClasses + 1])))) != GT_OK) return st;
@@ -1373,12 +1406,15 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
     const bool giant = info[2 * kClasses] + 1 > kFusedCap / 2;
     const unsigned gwt = grid_cap(cnt[kClsWmed], kBlock / kWave, 1024);
     const unsigned gmed = grid_cap(cnt[kClsMed], 1, 1024);
-    const hipStream_t s_short = sp.at(0), s_big = sp.at(1), s_wide = sp.at(2);
+    // side streams pay where the rows of more than kWaveRowMax entries hold at least a quarter of the
+    // entries; with fewer, their launches would mostly wait behind the short rows, so all stays on `stream`
+    const bool side = sp.n_side > 0 && 4 * info[2 * kClasses + 2] >= nnz;
+    const hipStream_t s_short = stream, s_big = side ? sp.at(1) : stream, s_wide = side ? sp.at(2) : stream;
     for (int t = 0; t < iters; ++t) {
         const uint64_t key = seed + uint64_t(t + 1) * kGolden;
         const int32_t* in = r.lab[t & 1];
         int32_t* out = r.lab[(t + 1) & 1];
-        if ((st = sp.fork()) != GT_OK) return st;
+        if (side && (st = sp.fork()) != GT_OK) return st;
         if (t == 0) {  // labels are the node ids: a minimum over each row's columns
             if (n_huge > 0) {
                 k_big_first_reset<<<grid_for(n_huge, 256, 1024), 256, 0, s_big>>>(br);

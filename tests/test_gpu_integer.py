@@ -105,14 +105,38 @@ def test_reorder_concurrent_calls(gt):
             np.testing.assert_array_equal(iperm, iperm_ref)
 
 
-@pytest.mark.parametrize("name", ["hubs_6000", "three_hubs_30000", "c3@0.02", "b1@0.1"])
+def mixed_classes_graph():
+    # most entries in rows of more than 64 (so a sweep's classes run on the side streams): 4,000 nodes with
+    # about 120 neighbours among themselves, 20 rows of about 1,500 and two of 6,000, the rest short rows
+    rng = np.random.default_rng(23)
+    n = 20000
+    u = [np.repeat(np.arange(4000), 60), np.repeat(np.arange(4000, 4020), 1500), np.repeat([4020, 4021], 6000)]
+    v = [rng.integers(0, 4000, 240000), rng.integers(0, n, 30000), rng.integers(0, n, 12000)]
+    short = np.arange(4022, n)
+    u.append(np.repeat(short, 2))
+    v.append(rng.integers(4022, n, 2 * len(short)))
+    return csr_from_pairs(n, np.concatenate(u), np.concatenate(v))
+
+
+@pytest.mark.parametrize("name", ["mixed_classes_20000", "hubs_6000", "c3@0.02", "b1@0.1"])
 def test_reorder_side_streams_same_result(gt, name):
-    # the sweeps spread over zero, one or two side streams (the bit-exact tests above use two) give one result,
-    # call after call with the same streams and events
-    rowptr, col = next((g[1], g[2]) for g in GRAPHS if g[0] == name)
+    # the sweeps spread over zero, one or two side streams give one result, call after call with the same
+    # streams and events; on the first graph the rows of more than 64 entries hold most entries, so the side
+    # streams are used (the others stay on one stream), and it is checked against the oracle too
+    if name == "mixed_classes_20000":
+        rowptr, col = mixed_classes_graph()
+        deg = np.diff(rowptr)
+        assert 4 * deg[deg > 64].sum() >= len(col)
+    else:
+        rowptr, col = next((g[1], g[2]) for g in GRAPHS if g[0] == name)
     rp, cl = dev_csr(rowptr, col)
     ref = [x.cpu().numpy() for x in gt.reorder(rp, cl, iters=20, seed=5, n_side=0)]
-    for n_side in (1, 2, 1):
+    if name == "mixed_classes_20000":
+        lab_ref, _ = OR.lp_labels(rowptr, col, iters=20, seed=5)
+        perm_ref, _ = OR.cluster_order(rowptr, col, lab_ref)
+        np.testing.assert_array_equal(ref[2], lab_ref)
+        np.testing.assert_array_equal(ref[0], perm_ref)
+    for n_side in (1, 2, 1, 2):
         say("reorder side streams", name, n_side)
         got = gt.reorder(rp, cl, iters=20, seed=5, n_side=n_side)
         for a, b in zip(got, ref):
