@@ -6,21 +6,24 @@
 // need sorting.  A row of at most kShortRow entries is sorted by a group of
 // 4, 8, 16, 32 or 64 lanes of a wavefront (a bitonic network across the
 // group's lanes; the row classes come from one stable partition of the new
-// rows) and written straight to its place.  The longer rows' edges are packed
-// as keys (new row << B) | new column and put in order by one stable radix
-// sort: sorted, they are grouped by new row and ascending inside each row,
-// each at its rank inside the row.
+// rows), a row of up to kWaveRow entries by one wavefront (2, 4 or 8 entries
+// per lane), and written straight to its place.  The longer rows' edges are
+// packed as keys (rank of the new row among them << B) | new column and put
+// in order by one stable radix sort: sorted, they are grouped by new row and
+// ascending inside each row, each at its rank inside the row.
 #include "prim.h"
 
 namespace gt {
 namespace {
 
-constexpr int kShortRow = 64;  // rows sorted inside one wavefront
+constexpr int kShortRow = 64;  // rows sorted by a group of lanes
+constexpr int kWaveRow = 512;  // rows sorted by one wavefront, kWaveRow / 64 entries per lane
 
 // Row classes of the relabelling: rows of 1-4, 5-8, 9-16, 17-32 and 33-64
-// entries (sorted by lane groups), 65 to kLongRow entries (keys written by one
-// wavefront per row); empty rows and rows over kLongRow are in no list.
-enum { kRl4, kRl8, kRl16, kRl32, kRl64, kRlMed, kRlClasses };
+// entries (sorted by lane groups), 65 to kWaveRow (one wavefront each),
+// kWaveRow + 1 to kLongRow entries (keys written by one wavefront per row);
+// empty rows and rows over kLongRow are in no list.
+enum { kRl4, kRl8, kRl16, kRl32, kRl64, kRlWave, kRlMed, kRlClasses };
 
 __device__ __forceinline__ int8_t relabel_class(int64_t d) {
     return d <= 0 ? int8_t(-1)
@@ -29,20 +32,119 @@ __device__ __forceinline__ int8_t relabel_class(int64_t d) {
            : d <= 16 ? int8_t(kRl16)
            : d <= 32 ? int8_t(kRl32)
            : d <= kShortRow ? int8_t(kRl64)
+           : d <= kWaveRow ? int8_t(kRlWave)
            : d <= kLongRow ? int8_t(kRlMed)
                            : int8_t(-1);
 }
 
-// Entry count of every new row r (old row perm[r]), its class, and the entries
-// it sends to the radix sort (its count when longer than kShortRow, else 0).
+// Entry count of every new row r (old row perm[r]), its class, the entries it
+// sends to the radix sort (its count when longer than kWaveRow, else 0) and
+// whether it sends any.
 __global__ void k_new_degrees(int64_t n, const int64_t* rowptr, const int32_t* perm, int64_t* deg_new, int8_t* cls,
-                              int64_t* sdeg) {
+                              int64_t* sdeg, int32_t* sflag) {
     for (int64_t r = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; r < n; r += int64_t(gridDim.x) * blockDim.x) {
         const int64_t u = perm[r];
         const int64_t d = rowptr[u + 1] - rowptr[u];
         deg_new[r] = d;
         cls[r] = relabel_class(d);
-        sdeg[r] = d > kShortRow ? d : 0;
+        sdeg[r] = d > kWaveRow ? d : 0;
+        sflag[r] = d > kWaveRow ? 1 : 0;
+    }
+}
+
+// srow[srank[r]] = r for the rows that send entries to the radix sort.
+__global__ void k_sorted_rows(int64_t n, const int32_t* sflag, const int64_t* srank, int32_t* srow) {
+    for (int64_t r = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; r < n; r += int64_t(gridDim.x) * blockDim.x)
+        if (sflag[r]) srow[srank[r]] = int32_t(r);
+}
+
+// Rows of kShortRow + 1 to kWaveRow entries, one wavefront each: element
+// i = 64 k + lane of the row sits in register k of the lane, R registers
+// (N = 64 R >= the row's entries; padding sorts last).  A bitonic network over
+// the N elements: exchanges across lanes by lane permutes, across registers
+// inside the lane.
+template <int R, bool kMap>
+__device__ __forceinline__ void relabel_wave_row(int64_t r, int64_t a, int d, const int32_t* __restrict__ col,
+                                                 const int32_t* __restrict__ iperm,
+                                                 const int64_t* __restrict__ rowptr_out,
+                                                 int32_t* __restrict__ col_out, int32_t* __restrict__ src_pos) {
+    constexpr int N = kWave * R;
+    const int lane = lane_id();
+    uint32_t key[R], pos[R];
+    int c[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) c[k] = kWave * k + lane < d ? col[a + kWave * k + lane] : 0;
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const bool in = kWave * k + lane < d;
+        key[k] = in ? uint32_t(iperm[c[k]]) : 0xFFFFFFFFu;
+        pos[k] = uint32_t(a + kWave * k + lane);
+    }
+#pragma unroll
+    for (int sz = 2; sz <= N; sz <<= 1) {
+#pragma unroll
+        for (int j = sz >> 1; j > 0; j >>= 1) {
+            if (j >= kWave) {  // partner: register k ^ (j / 64) of the same lane
+#pragma unroll
+                for (int k = 0; k < R; ++k) {
+                    const int kk = k ^ (j / kWave);
+                    if (kk < k) continue;
+                    const bool up = ((kWave * k + lane) & sz) == 0;  // ascending block
+                    const bool swap = up ? key[kk] < key[k] : key[kk] > key[k];
+                    if (swap) {
+                        const uint32_t tk = key[k], tp = pos[k];
+                        key[k] = key[kk];
+                        pos[k] = pos[kk];
+                        key[kk] = tk;
+                        pos[kk] = tp;
+                    }
+                }
+            } else {  // partner: lane ^ j, same register
+#pragma unroll
+                for (int k = 0; k < R; ++k) {
+                    const int i = kWave * k + lane;
+                    const uint32_t ok = __shfl_xor(key[k], j, kWave);
+                    const uint32_t op = kMap ? __shfl_xor(pos[k], j, kWave) : 0u;
+                    const bool take_min = ((i & j) == 0) == ((i & sz) == 0);
+                    if (take_min ? ok < key[k] : ok > key[k]) {
+                        key[k] = ok;
+                        pos[k] = op;
+                    }
+                }
+            }
+        }
+    }
+    const int64_t o = rowptr_out[r];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const int i = kWave * k + lane;
+        if (i < d) {
+            col_out[o + i] = int32_t(key[k]);
+            if (kMap) src_pos[o + i] = int32_t(pos[k]);
+        }
+    }
+}
+
+template <bool kMap>
+__global__ __launch_bounds__(256) void k_relabel_wave(const int32_t* __restrict__ list, int64_t len,
+                                                      const int64_t* __restrict__ rowptr,
+                                                      const int32_t* __restrict__ col,
+                                                      const int32_t* __restrict__ perm,
+                                                      const int32_t* __restrict__ iperm,
+                                                      const int64_t* __restrict__ rowptr_out,
+                                                      int32_t* __restrict__ col_out, int32_t* __restrict__ src_pos) {
+    const int64_t waves = int64_t(gridDim.x) * (256 / kWave);
+    for (int64_t idx = int64_t(blockIdx.x) * (256 / kWave) + threadIdx.x / kWave; idx < len; idx += waves) {
+        const int64_t r = list[idx];
+        const int64_t u = perm[r];
+        const int64_t a = rowptr[u];
+        const int d = int(rowptr[u + 1] - a);  // kShortRow < d <= kWaveRow, uniform over the wavefront
+        if (d <= 2 * kWave)
+            relabel_wave_row<2, kMap>(r, a, d, col, iperm, rowptr_out, col_out, src_pos);
+        else if (d <= 4 * kWave)
+            relabel_wave_row<4, kMap>(r, a, d, col, iperm, rowptr_out, col_out, src_pos);
+        else
+            relabel_wave_row<8, kMap>(r, a, d, col, iperm, rowptr_out, col_out, src_pos);
     }
 }
 
@@ -139,28 +241,33 @@ __global__ __launch_bounds__(256) void k_relabel_short(ShortLists sl, const int6
     }
 }
 
-// The sorted rows' entry count and the CSR check's flags, after the class
-// starts and sizes, so that one copy brings all of them to the host.
-__global__ void k_host_words(const int64_t* sorted, const uint32_t* flags, int64_t* out) {
+// The sorted rows' entry count, the CSR check's flags and the number of
+// sorted rows, after the class starts and sizes, so that one copy brings all
+// of them to the host.
+__global__ void k_host_words(const int64_t* sorted, const uint32_t* flags, const int64_t* sorted_rows,
+                             int64_t* out) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     out[0] = *sorted;
     out[1] = int64_t(*flags);
+    out[2] = *sorted_rows;
 }
 
-// Keys of the listed rows (kShortRow + 1 to kLongRow entries), one wavefront
-// per new row, at the row's offset soff[r] among the sorted rows' entries; for
-// the edge map, the old CSR position as the value.
+// Keys of the listed rows (kWaveRow + 1 to kLongRow entries), one wavefront
+// per new row, at the row's offset soff[r] among the sorted rows' entries,
+// with the row's rank srank[r] among the sorted rows; for the edge map, the
+// old CSR position as the value.
 template <bool kMap>
 __global__ __launch_bounds__(256) void k_edge_keys(const int32_t* list, int64_t len, const int64_t* rowptr,
                                                    const int32_t* col, const int32_t* perm, const int32_t* iperm,
-                                                   int bits, const int64_t* soff, uint64_t* keys, uint32_t* vals) {
+                                                   int bits, const int64_t* soff, const int64_t* srank,
+                                                   uint64_t* keys, uint32_t* vals) {
     const int lane = lane_id();
     const int64_t waves = int64_t(gridDim.x) * 4;
     for (int64_t idx = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave; idx < len; idx += waves) {
         const int64_t r = list[idx];
         const int64_t u = perm[r];
         const int64_t a = rowptr[u], d = rowptr[u + 1] - a;
-        const uint64_t hi = uint64_t(r) << bits;
+        const uint64_t hi = uint64_t(srank[r]) << bits;
         const int64_t base = soff[r];
         for (int64_t e = lane; e < d; e += kWave) {
             keys[base + e] = hi | uint64_t(uint32_t(iperm[col[a + e]]));
@@ -173,14 +280,15 @@ __global__ __launch_bounds__(256) void k_edge_keys(const int32_t* list, int64_t 
 template <bool kMap>
 __global__ __launch_bounds__(256) void k_edge_keys_long(int64_t n, int64_t nnz, const int64_t* rowptr,
                                                         const int32_t* col, const int32_t* iperm, int bits,
-                                                        const int64_t* soff, uint64_t* keys, uint32_t* vals) {
+                                                        const int64_t* soff, const int64_t* srank, uint64_t* keys,
+                                                        uint32_t* vals) {
     const int64_t chunks = long_chunks_of(nnz);
     for (int64_t c = blockIdx.x; c < chunks; c += gridDim.x) {
         LongSeg seg[2];
         const int k = long_segments(rowptr, n, nnz, c, seg);
         for (int j = 0; j < k; ++j) {
             const int64_t r = iperm[seg[j].row];
-            const uint64_t hi = uint64_t(r) << bits;
+            const uint64_t hi = uint64_t(srank[r]) << bits;
             const int64_t shift = soff[r] - rowptr[seg[j].row];  // key position = soff[r] + (e - row start)
             for (int64_t e = seg[j].a + threadIdx.x; e < seg[j].b; e += blockDim.x) {
                 keys[shift + e] = hi | uint64_t(uint32_t(iperm[col[e]]));
@@ -190,13 +298,14 @@ __global__ __launch_bounds__(256) void k_edge_keys_long(int64_t n, int64_t nnz, 
     }
 }
 
-// Sorted key i of new row r goes to rank i - soff[r] inside the row.
+// Sorted key i of new row r (rank key >> bits among the sorted rows) goes to
+// rank i - soff[r] inside the row.
 __global__ void k_place_sorted(int64_t m, const uint64_t* keys, const uint32_t* vals, int bits, const int64_t* soff,
-                               const int64_t* rowptr_out, int32_t* col_out, int32_t* src_pos) {
+                               const int32_t* srow, const int64_t* rowptr_out, int32_t* col_out, int32_t* src_pos) {
     const uint64_t mask = (uint64_t(1) << bits) - 1;
     for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < m; i += int64_t(gridDim.x) * blockDim.x) {
         const uint64_t key = keys[i];
-        const int64_t r = int64_t(key >> bits);
+        const int64_t r = srow[key >> bits];
         const int64_t o = rowptr_out[r] + (i - soff[r]);
         col_out[o] = int32_t(key & mask);
         if (src_pos) src_pos[o] = int32_t(vals[i]);
@@ -254,10 +363,14 @@ struct PermuteWs {
     int64_t* deg_new;
     int8_t* cls;      // [n]: the relabelling class of each new row
     int32_t* list;    // [n]: the new rows by class
-    int64_t* info;    // [2 * kRlClasses + 2]: class starts and sizes; the sorted entries; the CSR check
+    int64_t* info;    // [2 * kRlClasses + 3]: class starts and sizes; the sorted entries; the CSR check; the
+                      // sorted rows
     PartitionTmp part;
     int64_t* sdeg;  // entries of each new row that go to the radix sort
     int64_t* soff;  // [n + 1]: their exclusive scan
+    int32_t* sflag;  // [n]: 1 for the rows that go to the radix sort
+    int64_t* srank;  // [n + 1]: its exclusive scan (a row's rank among them)
+    int32_t* srow;   // [n]: the row of each rank
     uint64_t* keys;
     uint32_t* vals;  // source positions (edge map only)
     ScanTmp scan;
@@ -271,10 +384,13 @@ PermuteWs carve(Ws& ws, int64_t n, int64_t nnz, bool with_map) {
     p.deg_new = ws.take<int64_t>(n1);
     p.cls = ws.take<int8_t>(n1);
     p.list = ws.take<int32_t>(n1);
-    p.info = ws.take<int64_t>(2 * kRlClasses + 2);
+    p.info = ws.take<int64_t>(2 * kRlClasses + 3);
     p.part = partition_tmp(ws, n1);
     p.sdeg = ws.take<int64_t>(n1);
     p.soff = ws.take<int64_t>(n1 + 1);
+    p.sflag = ws.take<int32_t>(n1);
+    p.srank = ws.take<int64_t>(n1 + 1);
+    p.srow = ws.take<int32_t>(n1);
     p.keys = ws.take<uint64_t>(e1);
     p.vals = with_map ? ws.take<uint32_t>(e1) : nullptr;
     p.scan.block_sums = ws.take<int64_t>(size_t(scan_tmp_elems(n1)));
@@ -302,20 +418,24 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
     // the CSR check is read back with the class sizes below: nothing before that reads col
     if ((st = launch_validate_csr(n, nnz, rowptr, col, p.flags, stream)) != GT_OK) return st;
     const unsigned g = grid_for(n, 256, 8192);
-    k_new_degrees<<<g, 256, 0, stream>>>(n, rowptr, perm, p.deg_new, p.cls, p.sdeg);
+    k_new_degrees<<<g, 256, 0, stream>>>(n, rowptr, perm, p.deg_new, p.cls, p.sdeg, p.sflag);
     GT_LAUNCH_CHECK("permute_degrees");
     if ((st = exclusive_scan_i64(p.deg_new, n, rowptr_out, p.scan, stream)) != GT_OK) return st;
     if (nnz == 0) return read_validation(p.flags, stream);
-    // the rows of more than kShortRow entries go to the radix sort: their offsets there
+    // the rows of more than kWaveRow entries go to the radix sort: their offsets there and their ranks
     if ((st = exclusive_scan_i64(p.sdeg, n, p.soff, p.scan, stream)) != GT_OK) return st;
+    if ((st = exclusive_scan_i32(p.sflag, n, p.srank, p.scan, stream)) != GT_OK) return st;
+    k_sorted_rows<<<g, 256, 0, stream>>>(n, p.sflag, p.srank, p.srow);
+    GT_LAUNCH_CHECK("permute_sorted_rows");
     if ((st = partition_rows(p.cls, n, kRlClasses, p.list, p.info, p.part, stream)) != GT_OK) return st;
-    k_host_words<<<1, 64, 0, stream>>>(p.soff + n, p.flags, p.info + 2 * kRlClasses);
+    k_host_words<<<1, 64, 0, stream>>>(p.soff + n, p.flags, p.srank + n, p.info + 2 * kRlClasses);
     GT_LAUNCH_CHECK("permute_host_words");
-    int64_t info[2 * kRlClasses + 2] = {};
+    int64_t info[2 * kRlClasses + 3] = {};
     GT_HIP(hipMemcpyAsync(info, p.info, sizeof(info), hipMemcpyDeviceToHost, stream));
     GT_HIP(hipStreamSynchronize(stream));
     if ((st = validation_result(uint32_t(info[2 * kRlClasses + 1]))) != GT_OK) return st;
     const int64_t m = info[2 * kRlClasses];
+    const int64_t m_rows = info[2 * kRlClasses + 2];
     {
         // the short-row lists in one launch, largest rows first, blocks in proportion to their rows
         ShortLists sl;
@@ -343,6 +463,18 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
             GT_LAUNCH_CHECK("permute_short_rows");
         }
     }
+    const int64_t n_wave = info[kRlClasses + kRlWave];
+    if (n_wave > 0) {
+        const int32_t* rows = p.list + info[kRlWave];
+        const unsigned gw = grid_for(n_wave, 256 / kWave, 65536);
+        if (with_map)
+            k_relabel_wave<true><<<gw, 256, 0, stream>>>(rows, n_wave, rowptr, col, perm, iperm, rowptr_out, col_out,
+                                                         src_pos);
+        else
+            k_relabel_wave<false><<<gw, 256, 0, stream>>>(rows, n_wave, rowptr, col, perm, iperm, rowptr_out,
+                                                          col_out, nullptr);
+        GT_LAUNCH_CHECK("permute_wave_rows");
+    }
     if (m == 0) return GT_OK;
     const int bits = bits_for(n);
     const int64_t n_med = info[kRlClasses + kRlMed];
@@ -350,26 +482,28 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
         const int32_t* med = p.list + info[kRlMed];
         const unsigned gm = grid_for(n_med, 4, 65536);
         if (with_map)
-            k_edge_keys<true><<<gm, 256, 0, stream>>>(med, n_med, rowptr, col, perm, iperm, bits, p.soff, p.keys,
-                                                      p.vals);
+            k_edge_keys<true><<<gm, 256, 0, stream>>>(med, n_med, rowptr, col, perm, iperm, bits, p.soff, p.srank,
+                                                      p.keys, p.vals);
         else
-            k_edge_keys<false><<<gm, 256, 0, stream>>>(med, n_med, rowptr, col, perm, iperm, bits, p.soff, p.keys,
-                                                       nullptr);
+            k_edge_keys<false><<<gm, 256, 0, stream>>>(med, n_med, rowptr, col, perm, iperm, bits, p.soff, p.srank,
+                                                       p.keys, nullptr);
         GT_LAUNCH_CHECK("permute_keys");
     }
     if (nnz > kLongRow) {
         const int64_t ch = long_chunks_of(nnz);
         const unsigned gl = unsigned(ch < 8192 ? ch : 8192);
         if (with_map)
-            k_edge_keys_long<true><<<gl, 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits, p.soff, p.keys, p.vals);
+            k_edge_keys_long<true><<<gl, 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits, p.soff, p.srank,
+                                                           p.keys, p.vals);
         else
-            k_edge_keys_long<false><<<gl, 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits, p.soff, p.keys,
-                                                             nullptr);
+            k_edge_keys_long<false><<<gl, 256, 0, stream>>>(n, nnz, rowptr, col, iperm, bits, p.soff, p.srank,
+                                                            p.keys, nullptr);
         GT_LAUNCH_CHECK("permute_keys_long");
     }
-    if ((st = radix_sort_u64(p.keys, p.vals, m, 2 * bits, p.sort, stream)) != GT_OK) return st;
-    k_place_sorted<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, p.keys, p.vals, bits, p.soff, rowptr_out, col_out,
-                                                                with_map ? src_pos : nullptr);
+    // keys: (the row's rank among the m_rows sorted rows) << bits | new column
+    if ((st = radix_sort_u64(p.keys, p.vals, m, bits + bits_for(m_rows), p.sort, stream)) != GT_OK) return st;
+    k_place_sorted<<<grid_for(m, 256, 16384), 256, 0, stream>>>(m, p.keys, p.vals, bits, p.soff, p.srow, rowptr_out,
+                                                                col_out, with_map ? src_pos : nullptr);
     GT_LAUNCH_CHECK("permute_place");
     return GT_OK;
 }

@@ -157,6 +157,40 @@ def test_permute_bit_exact(gt, name, rowptr, col):
     np.testing.assert_array_equal(cl2.cpu().numpy(), ref_cl)
 
 
+def test_permute_every_row_size(gt):
+    # rows of 65 to 512 entries are sorted by one wavefront (2, 4 or 8 entries a lane), 513 to 2,048 and longer
+    # ones by the keyed radix sort: star rows at each boundary of those classes, plus short rows; with and
+    # without the edge map, against the oracle (the map: each new edge's old position holds the same edge)
+    sizes = [65, 100, 128, 129, 200, 256, 257, 400, 511, 512, 513, 1000, 2048, 2049, 5000]
+    n = 12000
+    rng = np.random.default_rng(31)
+    u = [np.full(d, 100 + 37 * k, np.int64) for k, d in enumerate(sizes)]
+    v = [rng.choice(n, d, replace=False) for d in sizes]
+    u.append(rng.integers(1000, n, 3 * n))  # short rows, away from the stars' centres
+    v.append(rng.integers(0, n, 3 * n))
+    rowptr, col = csr_from_pairs(n, np.concatenate(u), np.concatenate(v), symmetric=False, self_loops=False)
+    deg = np.diff(rowptr)
+    assert all((deg == d).any() for d in sizes)
+    perm = np.random.default_rng(12).permutation(n).astype(np.int32)
+    iperm = np.empty(n, np.int32)
+    iperm[perm] = np.arange(n)
+    rp, cl = dev_csr(rowptr, col)
+    pt, it = torch.from_numpy(perm).cuda(), torch.from_numpy(iperm).cuda()
+    ref_rp, ref_cl = OP.permute_csr(rowptr, col, perm, iperm)
+    say("permute row sizes", n, len(col))
+    rp2, cl2 = gt.permute_csr(rp, cl, pt, it)
+    np.testing.assert_array_equal(rp2.cpu().numpy(), ref_rp)
+    np.testing.assert_array_equal(cl2.cpu().numpy(), ref_cl)
+    rp3, cl3, src = gt.permute_csr_edges(rp, cl, pt, it)
+    np.testing.assert_array_equal(rp3.cpu().numpy(), ref_rp)
+    np.testing.assert_array_equal(cl3.cpu().numpy(), ref_cl)
+    src = src.cpu().numpy().astype(np.int64)
+    rows_old = np.repeat(np.arange(n), deg)
+    new_rows = np.repeat(np.arange(n), np.diff(ref_rp))
+    np.testing.assert_array_equal(iperm[rows_old[src]], new_rows)
+    np.testing.assert_array_equal(iperm[col[src]], ref_cl)
+
+
 def compare_plan(got: dict, ref: dict):
     for key in ("tile_rowptr", "tile_col", "tile_nnz", "sp_rowptr", "sp_col", "sp_colptr", "sp_row", "tileT_ptr",
                 "tileT_idx"):
