@@ -298,16 +298,37 @@ SortTmp sort_tmp(Ws& ws, int64_t n, int key_bytes, bool with_values) {
     return t;
 }
 
+// Digit counts of one tile.  The lanes of a wavefront holding the same digit
+// are found with eight ballots (one per digit bit) and counted with one LDS
+// add by the first of them, so a tile whose keys share few digits does not
+// serialise on a few LDS addresses.
 template <typename K>
 __global__ __launch_bounds__(kSortThreads) void k_sort_hist(const K* keys, int64_t n, int shift, int64_t tiles,
                                                              uint32_t* hist) {
     __shared__ uint32_t s_h[256];
     s_h[threadIdx.x] = 0;
     __syncthreads();
+    constexpr int R = kSortTile / kSortThreads;
     const int64_t base = int64_t(blockIdx.x) * kSortTile;
-    for (int r = 0; r < kSortTile / kSortThreads; ++r) {
+    K key[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
         const int64_t i = base + r * kSortThreads + threadIdx.x;
-        if (i < n) atomicAdd(&s_h[uint32_t(keys[i] >> shift) & 255u], 1u);
+        key[r] = i < n ? keys[i] : K(0);
+    }
+    const uint64_t lt = lanemask_lt();
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const bool valid = base + r * kSortThreads + threadIdx.x < n;
+        const uint32_t d = uint32_t(key[r] >> shift) & 255u;
+        uint64_t peers = ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bm = ballot(bit);
+            peers &= bit ? bm : ~bm;
+        }
+        if (valid && (peers & lt) == 0) atomicAdd(&s_h[d], uint32_t(__popcll(peers)));
     }
     __syncthreads();
     hist[int64_t(threadIdx.x) * tiles + blockIdx.x] = s_h[threadIdx.x];
