@@ -235,7 +235,12 @@ __global__ __launch_bounds__(256) void k_blocks_max(int64_t nblk, const uint32_t
 // ------------------------------------------------------------------ short rows
 // Rows of up to kWaveRowMax edges, in five lists by size, all in one launch:
 // the grid's blocks are cut into one range per list, each range running its
-// list with a grid-stride loop over tasks (one wavefront's rows).
+// list with a grid-stride loop over tasks (one wavefront's rows).  Their
+// entries (as list positions) sit in slots padded to the list's largest row
+// (S = 64, 32, 16, 8 or 4 slots a row, -1 past the row's entries), so a row's
+// slots are found from its list position alone: the entries' load does not
+// wait for a row offset.  Every class holds rows of more than S / 2 entries
+// except the 0-4 one, so the slots number at most 2 nnz + 4 n.
 
 // Reductions over the S lanes of a row group (S = 4, 8, 16 or 32).
 template <int S>
@@ -268,12 +273,12 @@ __device__ __forceinline__ uint64_t group_min_u64(uint64_t v) {
 
 // Row at list position p (kSub32 + 1 to kWaveRowMax edges), one wavefront:
 // every lane counts how many of the row's labels equal its own, reading the
-// others with readlane (the lane index is uniform over the wavefront).  roff,
-// ncol: the graph by list position (row p's entries at ncol[roff[p],
-// roff[p + 1])); labels are indexed by list position.
-__device__ __forceinline__ void lp_wave_row(int64_t p, const int32_t* list, const int64_t* roff,
-                                            const int32_t* ncol, const int32_t* lab_in, int32_t* lab_out,
-                                            uint64_t key, bool converged, uint32_t* flag_next) {
+// others with readlane (the lane index is uniform over the wavefront).  slots:
+// the row's 64 entry slots (list positions, -1 past its entries); labels are
+// indexed by list position.
+__device__ __forceinline__ void lp_wave_row(int64_t p, const int32_t* list, const int32_t* slots,
+                                            const int32_t* lab_in, int32_t* lab_out, uint64_t key, bool converged,
+                                            uint32_t* flag_next) {
     const int lane = lane_id();
     const int own = lab_in[p];
     if (converged) {
@@ -281,10 +286,9 @@ __device__ __forceinline__ void lp_wave_row(int64_t p, const int32_t* list, cons
         return;
     }
     const int64_t v = list[p];
-    const int64_t a = roff[p];
-    const int deg = int(roff[p + 1] - a);
-    const int c = lane < deg ? ncol[a + lane] : -1;
-    const bool valid = lane < deg && c != p;
+    const int c = slots[lane];
+    const int deg = __popcll(ballot(c >= 0));  // the entries fill the first deg slots
+    const bool valid = c >= 0 && c != p;
     const int L = valid ? lab_in[c] : -1;
     int cnt = 0;
     for (int k = 0; k < deg; ++k) cnt += (__builtin_amdgcn_readlane(L, k) == L) ? 1 : 0;
@@ -307,12 +311,13 @@ __device__ __forceinline__ void lp_wave_row(int64_t p, const int32_t* list, cons
 }
 
 // Rows g0 .. g0 + 64 / S - 1 of a list of rows of at most S edges (S = 4, 8,
-// 16 or 32) at list positions base + [0, len): the same function as
-// lp_wave_row with every reduction confined to the row's S lanes.
+// 16 or 32) at list positions base + [0, len), row idx's S slots at
+// slots + S idx: the same function as lp_wave_row with every reduction
+// confined to the row's S lanes.
 template <int S>
 __device__ __forceinline__ void lp_sub_group(int64_t g0, int64_t base, int64_t len, const int32_t* list,
-                                             const int64_t* roff, const int32_t* ncol, const int32_t* lab_in,
-                                             int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
+                                             const int32_t* slots, const int32_t* lab_in, int32_t* lab_out,
+                                             uint64_t key, bool converged, uint32_t* flag_next) {
     constexpr int G = kWave / S;
     const int lane = lane_id(), sub = lane / S, sl = lane % S;
     const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
@@ -325,14 +330,9 @@ __device__ __forceinline__ void lp_sub_group(int64_t g0, int64_t base, int64_t l
         return;
     }
     const int64_t v = live ? list[p] : 0;
-    int64_t a = 0;
-    int deg = 0;
-    if (live) {
-        a = roff[p];
-        deg = int(roff[p + 1] - a);
-    }
-    const int c = sl < deg ? ncol[a + sl] : -1;
-    const bool valid = sl < deg && c != p;
+    const int c = live ? slots[idx * S + sl] : -1;
+    const int deg = __popcll(__ballot(c >= 0) & gmask);  // the entries fill the row's first deg slots
+    const bool valid = c >= 0 && c != p;
     const int L = valid ? lab_in[c] : -1;
     const int dmax = wave_max(deg);
     int cnt = 0;
@@ -371,13 +371,14 @@ __device__ __forceinline__ void lp_sub_group(int64_t g0, int64_t base, int64_t l
 }
 
 // The five short-row lists (rows of 33-64, 17-32, 9-16, 5-8 and 0-4 edges, in
-// that order): their first list positions and lengths, and the first block of
-// each one's range; first[5] is the grid.
+// that order): their first list positions and lengths, the first entry slot
+// of each, and the first block of each one's range; first[5] is the grid.
 enum { kSmWave, kSm32, kSm16, kSm8, kSm4, kSmLists };
 struct SmallRows {
     const int32_t* list;
     int64_t base[kSmLists];
     int64_t len[kSmLists];
+    int64_t slot[kSmLists];
     unsigned first[kSmLists + 1];
 };
 
@@ -393,18 +394,19 @@ __device__ __forceinline__ int small_list(const SmallRows& sr, unsigned* blk, un
 
 template <int S>
 __device__ __forceinline__ void lp_sub_rows(const SmallRows& sr, int k, unsigned blk, unsigned nblk,
-                                            const int64_t* roff, const int32_t* ncol, const int32_t* lab_in,
-                                            int32_t* lab_out, uint64_t key, bool converged, uint32_t* flag_next) {
+                                            const int32_t* slots, const int32_t* lab_in, int32_t* lab_out,
+                                            uint64_t key, bool converged, uint32_t* flag_next) {
     constexpr int G = kWave / S;
     const int64_t waves = int64_t(nblk) * (kBlock / kWave);
     for (int64_t g0 = (int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave) * G; g0 < sr.len[k]; g0 += waves * G)
-        lp_sub_group<S>(g0, sr.base[k], sr.len[k], sr.list, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+        lp_sub_group<S>(g0, sr.base[k], sr.len[k], sr.list, slots + sr.slot[k], lab_in, lab_out, key, converged,
+                        flag_next);
 }
 
-// The sweeps after the first over the five lists.
-__global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t* roff, const int32_t* ncol,
-                                                     const int32_t* lab_in, int32_t* lab_out, uint64_t key,
-                                                     const uint32_t* flag_prev, uint32_t* flag_next) {
+// The sweeps after the first over the five lists; slots: the rows' padded entries.
+__global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int32_t* slots, const int32_t* lab_in,
+                                                     int32_t* lab_out, uint64_t key, const uint32_t* flag_prev,
+                                                     uint32_t* flag_next) {
     const bool converged = *flag_prev == 0;
     unsigned blk, nblk;
     const int k = small_list(sr, &blk, &nblk);
@@ -412,20 +414,21 @@ __global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t
         case kSmWave: {
             const int64_t waves = int64_t(nblk) * (kBlock / kWave);
             for (int64_t g = int64_t(blk) * (kBlock / kWave) + threadIdx.x / kWave; g < sr.len[k]; g += waves)
-                lp_wave_row(sr.base[k] + g, sr.list, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+                lp_wave_row(sr.base[k] + g, sr.list, slots + sr.slot[k] + g * kWave, lab_in, lab_out, key,
+                            converged, flag_next);
             break;
         }
         case kSm32:
-            lp_sub_rows<kSub32>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            lp_sub_rows<kSub32>(sr, k, blk, nblk, slots, lab_in, lab_out, key, converged, flag_next);
             break;
         case kSm16:
-            lp_sub_rows<kSub16>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            lp_sub_rows<kSub16>(sr, k, blk, nblk, slots, lab_in, lab_out, key, converged, flag_next);
             break;
         case kSm8:
-            lp_sub_rows<kSub8>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            lp_sub_rows<kSub8>(sr, k, blk, nblk, slots, lab_in, lab_out, key, converged, flag_next);
             break;
         default:
-            lp_sub_rows<kSub4>(sr, k, blk, nblk, roff, ncol, lab_in, lab_out, key, converged, flag_next);
+            lp_sub_rows<kSub4>(sr, k, blk, nblk, slots, lab_in, lab_out, key, converged, flag_next);
             break;
     }
 }
@@ -440,12 +443,13 @@ __global__ __launch_bounds__(kBlock) void k_lp_small(SmallRows sr, const int64_t
 // takes a minimum over each row's columns.
 
 // Rows of at most S edges, 64 / S per wavefront.  Every entry is read here
-// once: its column's list position goes to ncol for the later sweeps.
+// once: its column's list position goes to the row's slots (row idx's S slots
+// at slots + S idx, -1 past its entries) for the later sweeps.
 template <int S>
 __device__ __forceinline__ void first_rows(const int32_t* list, int64_t base, int64_t len, unsigned blk,
                                            unsigned nblk, const int64_t* rowptr, const int32_t* col,
-                                           const int64_t* roff, const int32_t* lpos, int32_t* ncol,
-                                           int32_t* lab_out, uint64_t key, uint32_t* flag_next) {
+                                           const int32_t* lpos, int32_t* slots, int32_t* lab_out, uint64_t key,
+                                           uint32_t* flag_next) {
     constexpr int G = kWave / S;
     const int lane = lane_id(), sub = lane / S, sl = lane % S;
     const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
@@ -462,7 +466,7 @@ __device__ __forceinline__ void first_rows(const int32_t* list, int64_t base, in
             deg = int(rowptr[v + 1] - a);
         }
         const int c = sl < deg ? col[a + sl] : -1;
-        if (sl < deg) ncol[roff[p] + sl] = lpos[c];
+        if (live) slots[idx * S + sl] = sl < deg ? lpos[c] : -1;
         const bool valid = sl < deg && c != v;
         const uint64_t h = valid ? mix64(uint64_t(uint32_t(c)) ^ key) : ~0ull;
         const uint64_t hmin = group_min_u64<S>(h);
@@ -476,33 +480,29 @@ __device__ __forceinline__ void first_rows(const int32_t* list, int64_t base, in
     }
 }
 
-// The first sweep over the five short-row lists.
+// The first sweep over the five short-row lists; slots: their padded entries.
 __global__ __launch_bounds__(kBlock) void k_first_small(SmallRows fr, const int64_t* rowptr, const int32_t* col,
-                                                        const int64_t* roff, const int32_t* lpos, int32_t* ncol,
-                                                        int32_t* lab_out, uint64_t key, uint32_t* flag_next) {
+                                                        const int32_t* lpos, int32_t* slots, int32_t* lab_out,
+                                                        uint64_t key, uint32_t* flag_next) {
     unsigned blk, nblk;
     const int k = small_list(fr, &blk, &nblk);
     const int64_t len = fr.len[k];
+    int32_t* sk = slots + fr.slot[k];
     switch (k) {
         case kSmWave:
-            first_rows<kWave>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
-                              flag_next);
+            first_rows<kWave>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, lpos, sk, lab_out, key, flag_next);
             break;
         case kSm32:
-            first_rows<kSub32>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
-                               flag_next);
+            first_rows<kSub32>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, lpos, sk, lab_out, key, flag_next);
             break;
         case kSm16:
-            first_rows<kSub16>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
-                               flag_next);
+            first_rows<kSub16>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, lpos, sk, lab_out, key, flag_next);
             break;
         case kSm8:
-            first_rows<kSub8>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
-                              flag_next);
+            first_rows<kSub8>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, lpos, sk, lab_out, key, flag_next);
             break;
         default:
-            first_rows<kSub4>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, roff, lpos, ncol, lab_out, key,
-                              flag_next);
+            first_rows<kSub4>(fr.list, fr.base[k], len, blk, nblk, rowptr, col, lpos, sk, lab_out, key, flag_next);
             break;
     }
 }
@@ -1239,7 +1239,8 @@ struct ReorderWs {
     int32_t* lpos;        // [n]: each row's position in list
     uint32_t* ldeg;       // [n]: entry counts by list position
     int64_t* roff;        // [n + 1]: their exclusive scan
-    int32_t* ncol;        // [nnz]: the rows' entries in list order, as list positions
+    int32_t* ncol;        // [nnz]: the rows' entries in list order, as list positions (longer rows)
+    int32_t* slots;       // [2 nnz + 4 n]: the short rows' entries, padded per list
     int64_t* class_info;  // [2 * kClasses + 3]: first list position and rows of each class; largest
                           // off-diagonal entry count; the CSR check's flags (low 32 bits); entries of the
                           // rows of more than kWaveRowMax entries
@@ -1280,6 +1281,7 @@ ReorderWs carve(Ws& ws, int64_t n, int64_t nnz, int32_t iters) {
     r.ldeg = ws.take<uint32_t>(n1);
     r.roff = ws.take<int64_t>(n1 + 1);
     r.ncol = ws.take<int32_t>(size_t(nnz > 0 ? nnz : 1));
+    r.slots = ws.take<int32_t>(size_t(2 * (nnz > 0 ? nnz : 1) + 4 * n1));
     r.class_info = ws.take<int64_t>(2 * kClasses + 3);
     r.blk_max = ws.take<uint32_t>(size_t(nblk));
     r.blk_long = ws.take<uint32_t>(size_t(nblk));
@@ -1393,14 +1395,20 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
         const int per_wave[kSmLists] = {1, kWave / kSub32, kWave / kSub16, kWave / kSub8, kWave / kSub4};
         sr.list = r.list;
         unsigned at = 0;
+        int64_t slot = 0;
         for (int k = 0; k < kSmLists; ++k) {
             const int64_t rows = cnt[cls[k]];
             sr.base[k] = info[cls[k]];
             sr.len[k] = rows;
+            sr.slot[k] = slot;
+            slot += rows * (kWave / per_wave[k]);  // the list's rows, padded to its largest
             sr.first[k] = at;
             if (rows > 0) at += grid_cap(rows, int64_t(per_wave[k]) * (kBlock / kWave), 16384);
         }
         sr.first[kSmLists] = at;
+        // within the workspace's 2 nnz + 4 n slots: every list but the 0-4 one holds rows of more than half its width
+        if (slot > 2 * nnz + 4 * n)
+            return fail(GT_ERR_WORKSPACE, "gt_reorder: short-row slots exceed the workspace");
     }
     // rows whose count table is over kFusedCap slots (more than kFusedCap / 2 entries) take the chunked passes
     const bool giant = info[2 * kClasses] + 1 > kFusedCap / 2;
@@ -1426,8 +1434,8 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
                 GT_LAUNCH_CHECK("reorder_big_decide");
             }
             if (sr.first[kSmLists] > 0) {
-                k_first_small<<<sr.first[kSmLists], kBlock, 0, s_short>>>(sr, rowptr, col, r.roff, r.lpos, r.ncol,
-                                                                         out, key, r.flags + 1);
+                k_first_small<<<sr.first[kSmLists], kBlock, 0, s_short>>>(sr, rowptr, col, r.lpos, r.slots, out,
+                                                                         key, r.flags + 1);
                 GT_LAUNCH_CHECK("reorder_first_small");
             }
             if (cnt[kClsWmed] > 0) {
@@ -1468,7 +1476,7 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
             }
         }
         if (sr.first[kSmLists] > 0) {
-            k_lp_small<<<sr.first[kSmLists], kBlock, 0, s_short>>>(sr, r.roff, r.ncol, in, out, key, r.flags + t,
+            k_lp_small<<<sr.first[kSmLists], kBlock, 0, s_short>>>(sr, r.slots, in, out, key, r.flags + t,
                                                                    r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_small");
         }
