@@ -271,6 +271,51 @@ __device__ __forceinline__ uint64_t group_min_u64(uint64_t v) {
     return v;
 }
 
+// How many valid lanes of this lane's S-lane group hold its label L (0 for
+// an invalid lane), for G = 64 / S <= 4 groups a wavefront.  Once clusters
+// form a row's neighbours carry few distinct labels, so they are peeled off
+// one per group and step (the group's first uncounted lane, read with
+// readlane, and one ballot); rows with more than kPeel distinct labels count
+// their remaining lanes by comparing every lane's label in turn (dmax: the
+// wavefront's largest row).
+constexpr int kPeel = 6;
+template <int S>
+__device__ __forceinline__ int group_counts(int L, bool valid, int dmax) {
+    constexpr int G = kWave / S;
+    static_assert(G <= 4, "peeling reads one lane per group");
+    const int lane = lane_id(), sub = lane / S;
+    const uint64_t gmask = (S == kWave ? ~0ull : ((1ull << S) - 1)) << (sub * S);
+    int cnt = 0;
+    uint64_t todo = __ballot(valid);
+    for (int it = 0; it < kPeel && todo; ++it) {
+        int Ld = -2;  // never a label
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const uint64_t t = todo & ((S == kWave ? ~0ull : ((1ull << S) - 1)) << (g * S));
+            const int x = t ? __builtin_amdgcn_readlane(L, __builtin_ctzll(t)) : -2;
+            Ld = sub == g ? x : Ld;
+        }
+        const bool eq = valid && L == Ld;
+        const uint64_t same = __ballot(eq);
+        if (eq) cnt = __popcll(same & gmask);
+        todo &= ~same;
+    }
+    if (todo) {
+        int c2 = 0;
+        for (int k = 0; k < dmax; ++k) {
+            int Lk = __builtin_amdgcn_readlane(L, k);
+#pragma unroll
+            for (int g = 1; g < G; ++g) {
+                const int x = __builtin_amdgcn_readlane(L, g * S + k);
+                Lk = sub == g ? x : Lk;
+            }
+            c2 += (Lk == L) ? 1 : 0;
+        }
+        if ((todo >> lane) & 1ull) cnt = c2;
+    }
+    return valid ? cnt : 0;
+}
+
 // Row at list position p (kSub32 + 1 to kWaveRowMax edges), one wavefront:
 // every lane counts how many of the row's labels equal its own, reading the
 // others with readlane (the lane index is uniform over the wavefront).  slots:
@@ -290,9 +335,7 @@ __device__ __forceinline__ void lp_wave_row(int64_t p, const int32_t* list, cons
     const int deg = __popcll(ballot(c >= 0));  // the entries fill the first deg slots
     const bool valid = c >= 0 && c != p;
     const int L = valid ? lab_in[c] : -1;
-    int cnt = 0;
-    for (int k = 0; k < deg; ++k) cnt += (__builtin_amdgcn_readlane(L, k) == L) ? 1 : 0;
-    if (!valid) cnt = 0;
+    const int cnt = group_counts<kWave>(L, valid, deg);
     const int best = wave_max(cnt);
     int cand = own;
     if (best > 0) {
@@ -336,23 +379,13 @@ __device__ __forceinline__ void lp_sub_group(int64_t g0, int64_t base, int64_t l
     const int L = valid ? lab_in[c] : -1;
     const int dmax = wave_max(deg);
     int cnt = 0;
-    for (int k = 0; k < dmax; ++k) {
-        // lane sub * S + k of each group: by readlane (k is uniform over the
-        // wavefront) for few groups, by one lane permute for many
-        int Lk;
-        if constexpr (G <= 4) {
-            Lk = __builtin_amdgcn_readlane(L, k);
-#pragma unroll
-            for (int g = 1; g < G; ++g) {
-                const int x = __builtin_amdgcn_readlane(L, g * S + k);
-                Lk = sub == g ? x : Lk;
-            }
-        } else {
-            Lk = __shfl(L, k, S);
-        }
-        cnt += (Lk == L) ? 1 : 0;
+    if constexpr (G <= 4) {
+        cnt = group_counts<S>(L, valid, dmax);
+    } else {
+        // eight or sixteen rows a wavefront: lane sub * S + k of each group by one lane permute
+        for (int k = 0; k < dmax; ++k) cnt += (__shfl(L, k, S) == L) ? 1 : 0;
+        if (!valid) cnt = 0;
     }
-    if (!valid) cnt = 0;
     const int best = group_max_i32<S>(cnt);
     const int own_cnt = __popcll(__ballot(valid && L == own) & gmask);
     const bool moves = best > 0 && own_cnt != best;
