@@ -242,33 +242,62 @@ __global__ __launch_bounds__(256) void k_blocks_max(int64_t nblk, const uint32_t
 // wait for a row offset.  Every class holds rows of more than S / 2 entries
 // except the 0-4 one, so the slots number at most 2 nnz + 4 n.
 
-// Reductions over the S lanes of a row group (S = 4, 8, 16 or 32).
-template <int S>
+// x of lane (lane ^ O), 0 < O < 64: a quad permute (DPP) for O < 4, a
+// bit-mode lane swizzle (lane' = lane ^ O inside each 32-lane half) up to
+// 31, a lane permute across the halves for 32.
+template <int O>
+__device__ __forceinline__ int xor_lane(int x) {
+    static_assert(O > 0 && (O < 32 || O == 32), "one lane bit");
+    if constexpr (O == 1) return __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);  // quad [1,0,3,2]
+    else if constexpr (O == 2) return __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);  // [2,3,0,1]
+    else if constexpr (O == 3) return __builtin_amdgcn_update_dpp(0, x, 0x1B, 0xF, 0xF, false);  // [3,2,1,0]
+    else if constexpr (O < 32) return __builtin_amdgcn_ds_swizzle(x, 0x1F | (O << 10));  // and 0x1F, xor O
+    else return __shfl_xor(x, 32, kWave);
+}
+template <int O>
+__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t x) {
+    const uint32_t lo = uint32_t(xor_lane<O>(int(uint32_t(x))));
+    const uint32_t hi = uint32_t(xor_lane<O>(int(uint32_t(x >> 32))));
+    return (uint64_t(hi) << 32) | lo;
+}
+
+// Reductions over the S lanes of a row group (S = 4, 8, 16 or 32), O = S / 2 down to 1.
+template <int S, int O = S / 2>
 __device__ __forceinline__ int group_max_i32(int v) {
-#pragma unroll
-    for (int o = S / 2; o > 0; o >>= 1) {
-        const int w = __shfl_xor(v, o, kWave);
-        v = w > v ? w : v;
+    if constexpr (O == 0) {
+        return v;
+    } else {
+        const int w = xor_lane<O>(v);
+        return group_max_i32<S, O / 2>(w > v ? w : v);
     }
-    return v;
 }
-template <int S>
+template <int S, int O = S / 2>
 __device__ __forceinline__ int group_min_i32(int v) {
-#pragma unroll
-    for (int o = S / 2; o > 0; o >>= 1) {
-        const int w = __shfl_xor(v, o, kWave);
-        v = w < v ? w : v;
+    if constexpr (O == 0) {
+        return v;
+    } else {
+        const int w = xor_lane<O>(v);
+        return group_min_i32<S, O / 2>(w < v ? w : v);
     }
-    return v;
 }
-template <int S>
+template <int S, int O = S / 2>
 __device__ __forceinline__ uint64_t group_min_u64(uint64_t v) {
-#pragma unroll
-    for (int o = S / 2; o > 0; o >>= 1) {
-        const uint64_t w = shfl_xor_u64(v, o);
-        v = w < v ? w : v;
+    if constexpr (O == 0) {
+        return v;
+    } else {
+        const uint64_t w = xor_lane_u64<O>(v);
+        return group_min_u64<S, O / 2>(w < v ? w : v);
     }
-    return v;
+}
+
+// Lanes of this lane's S-lane group (S <= 16) other than itself holding L.
+template <int S, int K = 1>
+__device__ __forceinline__ int xor_matches(int L) {
+    if constexpr (K >= S) {
+        return 0;
+    } else {
+        return (xor_lane<K>(L) == L ? 1 : 0) + xor_matches<S, K + 1>(L);
+    }
 }
 
 // How many valid lanes of this lane's S-lane group hold its label L (0 for
@@ -382,9 +411,10 @@ __device__ __forceinline__ void lp_sub_group(int64_t g0, int64_t base, int64_t l
     if constexpr (G <= 4) {
         cnt = group_counts<S>(L, valid, dmax);
     } else {
-        // eight or sixteen rows a wavefront: lane sub * S + k of each group by one lane permute
-        for (int k = 0; k < dmax; ++k) cnt += (__shfl(L, k, S) == L) ? 1 : 0;
-        if (!valid) cnt = 0;
+        // eight or sixteen rows a wavefront: every other lane of the group by a fixed lane pattern
+        // (an invalid lane's -1 matches no label), exchanged with every lane active
+        const int m = xor_matches<S>(L);
+        cnt = valid ? 1 + m : 0;
     }
     const int best = group_max_i32<S>(cnt);
     const int own_cnt = __popcll(__ballot(valid && L == own) & gmask);
