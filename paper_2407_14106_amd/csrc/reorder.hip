@@ -1390,9 +1390,9 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
     if (ws_bytes < gt_reorder_workspace_size(n, nnz))
         return fail(GT_ERR_WORKSPACE, "gt_reorder: workspace too small");
     // The classes of a sweep read the sweep's input labels and write disjoint rows of its output: with side
-    // streams they run side by side, the short rows on the caller's stream, the long rows on the first side
-    // stream, the rows of 65 to 4096 entries on the second (or the first); each sweep starts when the
-    // previous one has finished on all of them.
+    // streams they run side by side, the short rows and then the rows of 513 to 4096 entries on the caller's
+    // stream, the long rows on the first side stream, the rows of 65 to 512 entries on the second (or the
+    // first); each sweep starts when the previous one has finished on all of them.
     Spread sp;
     gt_status st = spread_open("gt_reorder", stream, side_streams, events, n_side, &sp);
     if (st != GT_OK) return st;
@@ -1549,7 +1549,7 @@ extern "C" gt_status gt_reorder_streams(int64_t n, int64_t nnz, const int64_t* r
             GT_LAUNCH_CHECK("reorder_lp_wavetab");
         }
         if (cnt[kClsMed] > 0) {
-            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, s_wide>>>(r.list, info[kClsMed], len_of[kClsMed], r.roff,
+            k_lp_block<kMedBlock><<<gmed, kMedBlock, 0, s_short>>>(r.list, info[kClsMed], len_of[kClsMed], r.roff,
                                                                   r.ncol, in, out, key, r.flags + t,
                                                                   r.flags + t + 1);
             GT_LAUNCH_CHECK("reorder_lp_lds");
