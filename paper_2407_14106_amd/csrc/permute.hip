@@ -11,6 +11,7 @@
 // packed as keys (rank of the new row among them << B) | new column and put
 // in order by one stable radix sort: sorted, they are grouped by new row and
 // ascending inside each row, each at its rank inside the row.
+#include "lanes.h"
 #include "prim.h"
 
 namespace gt {
@@ -103,8 +104,8 @@ __device__ __forceinline__ void relabel_wave_row(int64_t r, int64_t a, int d, co
 #pragma unroll
                 for (int k = 0; k < R; ++k) {
                     const int i = kWave * k + lane;
-                    const uint32_t ok = __shfl_xor(key[k], j, kWave);
-                    const uint32_t op = kMap ? __shfl_xor(pos[k], j, kWave) : 0u;
+                    const uint32_t ok = uint32_t(xor_lane_pow2(int(key[k]), j));
+                    const uint32_t op = kMap ? uint32_t(xor_lane_pow2(int(pos[k]), j)) : 0u;
                     const bool take_min = ((i & j) == 0) == ((i & sz) == 0);
                     if (take_min ? ok < key[k] : ok > key[k]) {
                         key[k] = ok;
@@ -151,7 +152,8 @@ __global__ __launch_bounds__(256) void k_relabel_wave(const int32_t* __restrict_
 // The rows of one class list of at most S entries, 64 / S per wavefront: the
 // lanes of a row's group hold iperm of its columns (padding sorts last) and,
 // for the edge map, their old CSR positions; a bitonic network over the S
-// lanes sorts them ascending (the columns of a row are distinct).
+// lanes sorts them ascending (the columns of a row are distinct), exchanging
+// by quad permutes and lane swizzles with every lane active.
 template <int S, bool kMap>
 __device__ __forceinline__ void relabel_rows(const int32_t* __restrict__ list, int64_t len, unsigned blk,
                                              unsigned nblk, const int64_t* __restrict__ rowptr,
@@ -181,8 +183,8 @@ __device__ __forceinline__ void relabel_rows(const int32_t* __restrict__ list, i
         for (int k = 2; k <= S; k <<= 1) {
 #pragma unroll
             for (int j = k >> 1; j > 0; j >>= 1) {
-                const uint32_t ok = __shfl_xor(key, j, kWave);
-                const uint32_t op = kMap ? __shfl_xor(pos, j, kWave) : 0u;
+                const uint32_t ok = uint32_t(xor_lane_pow2(int(key), j));
+                const uint32_t op = kMap ? uint32_t(xor_lane_pow2(int(pos), j)) : 0u;
                 const bool take_min = ((sl & j) == 0) == ((sl & k) == 0);
                 if (take_min ? ok < key : ok > key) {
                     key = ok;

@@ -31,6 +31,7 @@
 // ids, so the result does not depend on this numbering.
 #include <limits.h>
 
+#include "lanes.h"
 #include "prim.h"
 
 namespace gt {
@@ -241,25 +242,6 @@ __global__ __launch_bounds__(256) void k_blocks_max(int64_t nblk, const uint32_t
 // slots are found from its list position alone: the entries' load does not
 // wait for a row offset.  Every class holds rows of more than S / 2 entries
 // except the 0-4 one, so the slots number at most 2 nnz + 4 n.
-
-// x of lane (lane ^ O), 0 < O < 64: a quad permute (DPP) for O < 4, a
-// bit-mode lane swizzle (lane' = lane ^ O inside each 32-lane half) up to
-// 31, a lane permute across the halves for 32.
-template <int O>
-__device__ __forceinline__ int xor_lane(int x) {
-    static_assert(O > 0 && (O < 32 || O == 32), "one lane bit");
-    if constexpr (O == 1) return __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);  // quad [1,0,3,2]
-    else if constexpr (O == 2) return __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);  // [2,3,0,1]
-    else if constexpr (O == 3) return __builtin_amdgcn_update_dpp(0, x, 0x1B, 0xF, 0xF, false);  // [3,2,1,0]
-    else if constexpr (O < 32) return __builtin_amdgcn_ds_swizzle(x, 0x1F | (O << 10));  // and 0x1F, xor O
-    else return __shfl_xor(x, 32, kWave);
-}
-template <int O>
-__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t x) {
-    const uint32_t lo = uint32_t(xor_lane<O>(int(uint32_t(x))));
-    const uint32_t hi = uint32_t(xor_lane<O>(int(uint32_t(x >> 32))));
-    return (uint64_t(hi) << 32) | lo;
-}
 
 // Reductions over the S lanes of a row group (S = 4, 8, 16 or 32), O = S / 2 down to 1.
 template <int S, int O = S / 2>
