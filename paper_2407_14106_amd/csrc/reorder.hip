@@ -5,9 +5,12 @@
 //   deg <= 4 / 8 / 16 / 32
 //                      16 / 8 / 4 / 2 rows per wavefront, 4 / 8 / 16 / 32
 //                      lanes each;
-//   32 < deg <= 64     one wavefront per row; one neighbour label per lane,
-//                      multiplicities by an all-pairs compare (readlane).
-//                      These five classes run in one launch.
+//   32 < deg <= 64     one wavefront per row; one neighbour label per lane.
+//                      Multiplicities by peeling the distinct labels (ballots)
+//                      or, past a few, an all-pairs compare (readlane); rows
+//                      of up to 8 compare by fixed lane patterns.  These five
+//                      classes run in one launch, their entries in padded
+//                      slots found from the row's list position.
 //   64 < deg <= 512    one wavefront per row, open-addressing count table in
 //                      the wavefront's share of LDS (no workgroup barriers).
 //   512 < deg <= 4096  one workgroup per row, open-addressing count table in LDS.
@@ -24,11 +27,14 @@
 //
 // The sweeps after the first run on the graph renumbered by list position
 // (each row's place in the class-major row list): the rows' entries are laid
-// out in list order (roff, ncol; written once, during the first sweep) and a
-// node's label is kept at its list position.  A class's rows then read their
-// row offsets and entries in runs, and the classes gather the long rows, whose
+// out in list order (roff, ncol for the rows of more than 64 entries, padded
+// slots for the others; written once, during the first sweep) and a node's
+// label is kept at its list position.  A class's rows then read their row
+// offsets and entries in runs, and the classes gather the long rows, whose
 // labels most rows read, into a few cache lines.  The label values stay node
-// ids, so the result does not depend on this numbering.
+// ids, so the result does not depend on this numbering.  With side streams
+// from the caller, a sweep's classes run side by side where the rows of more
+// than 64 entries hold at least a quarter of the entries.
 #include <limits.h>
 
 #include "lanes.h"
