@@ -491,7 +491,7 @@ gt_status permute(const char* who, int64_t n, int64_t nnz, const int64_t* rowptr
                                                        p.keys, nullptr);
         GT_LAUNCH_CHECK("permute_keys");
     }
-    if (nnz > kLongRow) {
+    if (uint32_t(info[2 * kRlClasses + 1]) & kLongRowSeen) {  // some row has more than kLongRow entries
         const int64_t ch = long_chunks_of(nnz);
         const unsigned gl = unsigned(ch < 8192 ? ch : 8192);
         if (with_map)

@@ -150,6 +150,9 @@ gt_status partition_rows(const int8_t* cls, int64_t n, int ncls, int32_t* list, 
 
 // ---- CSR validation: accumulates error bits into *flags (one uint32, zeroed by the caller).
 enum : uint32_t { kBadRowptr = 1u, kOutOfRange = 2u, kUnsorted = 4u, kDuplicate = 8u };
+// Not an error: the rows pass saw a row of more than kLongRow entries (the
+// stages whose long-row kernels scan every entry chunk skip them without one).
+constexpr uint32_t kLongRowSeen = 16u;
 gt_status launch_validate_csr(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, uint32_t* flags,
                               hipStream_t s);
 // Reads the flags back (SYNC) and maps them to a status.

@@ -564,6 +564,7 @@ __global__ void k_validate_rows(int64_t n, int64_t nnz, const int64_t* __restric
         const int64_t a = rowptr[i], b = rowptr[i + 1];
         if (a > b) f |= kUnsorted;
         else if (a < 0 || b > nnz) f |= kOutOfRange;
+        else if (b - a > kLongRow) f |= kLongRowSeen;
     }
     if (f) atomicOr(flags, f);
 }

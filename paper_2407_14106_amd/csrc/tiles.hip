@@ -751,8 +751,9 @@ __global__ __launch_bounds__(kTransposeThreads) void k_tile_transpose(int64_t d,
 // record's tag (a record is used once).  The record lives in the caller's
 // memory, so the library keeps nothing between the two calls.
 constexpr uint64_t kRecordTag = 0x67745F74696C6573ull;
+constexpr uint64_t kLongRowTag = 0x6C6F6E675F726F77ull;
 struct CountRecord {
-    uint64_t w[kRecordWords];  // tag, n, nnz, rowptr, col, T << 32 | tau_ppm, checksum, unused
+    uint64_t w[kRecordWords];  // tag, n, nnz, rowptr, col, T << 32 | tau_ppm, checksum, rows over kLongRow
 };
 
 // The plan's four sizes, next to each other for one copy to the host.
@@ -766,7 +767,8 @@ __global__ void k_plan_sizes(const int64_t* tile_rowptr_end, const int64_t* sp_r
 }
 
 __global__ void k_put_record(uint64_t* __restrict__ rec, int64_t n, int64_t nnz, const int64_t* rowptr,
-                             const int32_t* col, int32_t T, uint32_t tau_ppm, const unsigned long long* __restrict__ sum) {
+                             const int32_t* col, int32_t T, uint32_t tau_ppm, const unsigned long long* __restrict__ sum,
+                             bool has_long) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     rec[0] = kRecordTag;
     rec[1] = uint64_t(n);
@@ -774,8 +776,9 @@ __global__ void k_put_record(uint64_t* __restrict__ rec, int64_t n, int64_t nnz,
     rec[3] = uint64_t(reinterpret_cast<uintptr_t>(rowptr));
     rec[4] = uint64_t(reinterpret_cast<uintptr_t>(col));
     rec[5] = (uint64_t(uint32_t(T)) << 32) | tau_ppm;
-    rec[6] = uint64_t(*sum);
-    rec[7] = 0;
+    // the long-row flag goes into the stored checksum too, so a changed flag fails the check
+    rec[6] = uint64_t(*sum) ^ (has_long ? kLongRowTag : 0ull);
+    rec[7] = has_long ? 1 : 0;
 }
 
 bool record_matches(const CountRecord& r, int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col,
@@ -824,8 +827,9 @@ gt_status heavy_prelude(int64_t n, const int64_t* rowptr, int32_t T, TilesWs& t,
 }
 
 // The rest of the count pass, after heavy_prelude.
+// has_long: some row has more than kLongRow entries (else the long-row kernel is skipped).
 gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_t* col, int32_t T, uint32_t tau_ppm,
-                     TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, hipStream_t stream) {
+                     TilesWs& t, int64_t* tile_rowptr, int64_t* sp_rowptr, bool has_long, hipStream_t stream) {
     gt_status st;
     const int R = int(cdiv(n, T));
     k_heavy_count<<<1024, kTileThreads, 0, stream>>>(n, rowptr, col, T, R, t.heavy_list, t.heavy_n, t.heavy_cnt);
@@ -840,7 +844,7 @@ gt_status count_pass(int64_t n, int64_t nnz, const int64_t* rowptr, const int32_
         n, t.med_list, t.med_info + 1, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, t.sp_deg, t.tag, t.rows,
         nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
     GT_LAUNCH_CHECK("tiles_count_medium");
-    if (nnz > kLongRow) {
+    if (has_long) {
         k_tiles_long_count<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
                                                                    t.sp_deg, t.tag, t.rows);
         GT_LAUNCH_CHECK("tiles_long_count");
@@ -887,11 +891,16 @@ extern "C" gt_status gt_tiles_count(int64_t n, int64_t nnz, const int64_t* rowpt
     TilesWs t = carve(ws, n, nnz, T);
     if ((st = launch_validate_csr(n, nnz, rowptr, col, t.flags, stream)) != GT_OK) return st;
     if ((st = heavy_prelude(n, rowptr, T, t, stream)) != GT_OK) return st;
-    if ((st = read_validation(t.flags, stream)) != GT_OK) return st;
-    if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, stream)) != GT_OK)
+    uint32_t vf = 0;
+    GT_HIP(hipMemcpyAsync(&vf, t.flags, sizeof(vf), hipMemcpyDeviceToHost, stream));
+    GT_HIP(hipStreamSynchronize(stream));
+    if ((st = validation_result(vf)) != GT_OK) return st;
+    const bool has_long = (vf & kLongRowSeen) != 0;
+    if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, t.tmp_tile_rowptr, t.tmp_sp_rowptr, has_long,
+                         stream)) != GT_OK)
         return st;
     if ((st = ws_checksum(t, stream)) != GT_OK) return st;
-    k_put_record<<<1, 64, 0, stream>>>(t.record, n, nnz, rowptr, col, T, tau_ppm, t.csum);
+    k_put_record<<<1, 64, 0, stream>>>(t.record, n, nnz, rowptr, col, T, tau_ppm, t.csum, has_long);
     GT_LAUNCH_CHECK("tiles_count_record");
     const int64_t R = plan->n_row_tiles;
     k_plan_sizes<<<1, 64, 0, stream>>>(t.tmp_tile_rowptr + R, t.tmp_sp_rowptr + n, t.long_row_pos + n,
@@ -938,6 +947,7 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
     // the counts of the gt_tiles_count call that used this workspace with these
     // arguments, if they are still there unchanged; else count again
     bool reuse = false;
+    bool has_long = nnz > kLongRow;  // without the count call's record: whether the CSR has a row that long
     {
         if ((st = ws_checksum(t, stream)) != GT_OK) return st;
         uint64_t words[kRecordWords + 1];  // the record and the checksum just taken
@@ -946,14 +956,17 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         CountRecord rec;
         for (int i = 0; i < kRecordWords; ++i) rec.w[i] = words[i];
         const uint64_t have = words[kRecordWords];
-        reuse = record_matches(rec, n, nnz, rowptr, col, T, tau_ppm) && rec.w[6] == have;
+        reuse = record_matches(rec, n, nnz, rowptr, col, T, tau_ppm) && rec.w[7] <= 1 &&
+                rec.w[6] == (have ^ (rec.w[7] ? kLongRowTag : 0ull));
+        if (reuse) has_long = rec.w[7] != 0;
         if (!reuse && rec.w[0] == kRecordTag &&
             (st = fill_u32(reinterpret_cast<uint32_t*>(t.record), 2, 0u, stream)) != GT_OK)
             return st;
     }
     if (!reuse) {
         if ((st = heavy_prelude(n, rowptr, T, t, stream)) != GT_OK) return st;
-        if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, stream)) !=
+        if ((st = count_pass(n, nnz, rowptr, col, T, tau_ppm, t, plan->tile_rowptr, plan->sp_rowptr, has_long,
+                             stream)) !=
             GT_OK)
             return st;
     }
@@ -992,7 +1005,7 @@ extern "C" gt_status gt_build_tiles(int64_t n, int64_t nnz, const int64_t* rowpt
         n, t.med_list, t.med_info + 1, rowptr, col, T, t.W, t.dense_bits, t.dense_pre, nullptr, nullptr, nullptr,
         trp, plan->tile_mask, srp, plan->sp_col, plan->sp_pos, plan->tile_pos);
     GT_LAUNCH_CHECK("tiles_fill_medium");
-    if (nnz > kLongRow) {
+    if (has_long) {
         const int64_t segs = 2 * long_chunks_of(nnz);
         if ((st = fill_u32(reinterpret_cast<uint32_t*>(t.segcnt), segs, 0u, stream)) != GT_OK) return st;
         k_tiles_long_segs<<<long_grid(nnz), kThreads, 0, stream>>>(n, nnz, rowptr, col, T, t.W, t.dense_bits,
