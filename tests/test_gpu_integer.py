@@ -262,6 +262,9 @@ def test_tiles_counts_taken_or_recounted(gt, name):
                                                      device=rp.device)},
             "overwritten": {"between": lambda ws: ws.fill_(0xA5)},
             "one byte changed": {"between": lambda ws: ws[ws.numel() // 3].add_(1)},
+            # the count record's last word (whether a row exceeds 2,048 entries), flipped: the record check
+            # (the flag is folded into the stored checksum) must send the build back to counting
+            "record flag flipped": {"between": lambda ws: ws[256 + 7 * 8].bitwise_xor_(1)},
         }
         for way, kw in ways.items():
             say("tiles counts", name, T, tau, way)
